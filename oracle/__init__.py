@@ -1,0 +1,173 @@
+"""CPU oracle for the message-passing aggregation path (fp64, plain loops).
+
+TEST INFRASTRUCTURE ONLY: imported by ``tests/``, ``__graft_entry__.smoke()``
+and the CPU-baseline leg of ``bench.py``, never by the device library or its
+Python binding.  It shares no code with the device path; both are fed from
+``graphgen``.
+
+The arithmetic lives in ``oracle.c`` (see its header for the paper passages it
+follows: Eq. (1), the sorted-CSR aggregation of Sec. 2.2, and the nested
+heterogeneous sum).  This module only marshals numpy arrays.
+
+Every function here is pinned by ``tests/test_oracle_*.py`` against library
+routines (numpy stable argsort, scipy.sparse, dense matmul), closed forms and
+brute force; none is "parity unpinned".
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+import subprocess
+
+import numpy as np
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+_SRC = os.path.join(_HERE, "oracle.c")
+_LIB_PATH = os.path.join(_HERE, "_liboracle.so")
+_lib = None
+
+
+def build(force: bool = True) -> str:
+    """Compile oracle.c with gcc -O2 (no fast-math) + OpenMP."""
+    if force or not os.path.exists(_LIB_PATH):
+        tmp = _LIB_PATH + ".tmp"
+        subprocess.check_call(["gcc", "-O2", "-fopenmp", "-fPIC", "-shared", "-std=c11",
+                               _SRC, "-o", tmp, "-lm"])
+        os.replace(tmp, _LIB_PATH)
+    return _LIB_PATH
+
+
+def _L():
+    global _lib
+    if _lib is None:
+        if not os.path.exists(_LIB_PATH):
+            build(force=False)
+        lib = ctypes.CDLL(_LIB_PATH)
+        i64, i32, p = ctypes.c_int64, ctypes.c_int, ctypes.c_void_p
+        lib.oracle_coo_to_csr.argtypes = [i64, i64, i64, p, p, p, p, p, p, p]
+        lib.oracle_coo_to_csr.restype = i32
+        lib.oracle_spmm.argtypes = [i64, p, i64, i64, p, p, p, p, i32, i64,
+                                    p, p, p, p, p, i32]
+        lib.oracle_spmm.restype = i32
+        lib.oracle_spmm_coo_rows.argtypes = [i64, i64, i64, p, p, p, p, i32, i64, i64, p,
+                                             p, p, p, p, p]
+        lib.oracle_spmm_coo_rows.restype = i32
+        lib.oracle_hetero_sum.argtypes = [i32, p, p, i32, i64, i32, p, p, p, p, p, p, p]
+        lib.oracle_hetero_sum.restype = i32
+        _lib = lib
+    return _lib
+
+
+def _p(a):
+    return None if a is None else ctypes.c_void_p(a.ctypes.data)
+
+
+def _c(a, dt):
+    return None if a is None else np.ascontiguousarray(a, dtype=dt)
+
+
+def coo_to_csr(src, dst, n_dst, n_src=None, val=None):
+    """Stable counting sort of the COO edges by destination.
+
+    Returns (rowptr int64[N+1], col int32[E], perm int64[E], val_out or None)."""
+    src, dst = _c(src, np.int32), _c(dst, np.int32)
+    E = src.shape[0]
+    n_src = n_dst if n_src is None else n_src
+    rowptr = np.empty(n_dst + 1, np.int64)
+    col = np.empty(E, np.int32)
+    perm = np.empty(E, np.int64)
+    val = _c(val, np.float32)
+    vout = None if val is None else np.empty(E, np.float32)
+    rc = _L().oracle_coo_to_csr(E, n_dst, n_src, _p(src), _p(dst), _p(val), _p(rowptr),
+                                _p(col), _p(perm), _p(vout))
+    if rc != 0:
+        raise ValueError(f"oracle_coo_to_csr failed ({rc})")
+    return rowptr, col, perm, vout
+
+
+def _x_args(x, x_bf16):
+    if x_bf16 is not None:
+        xb = _c(x_bf16, np.uint16)
+        return xb, 1, xb.shape[0], xb.shape[1]
+    xf = _c(x, np.float32)
+    return xf, 0, xf.shape[0], xf.shape[1]
+
+
+def spmm(rowptr, col, x=None, x_bf16=None, w=None, rows=None, nthreads=None,
+         want=("sum", "mean", "max", "scale")):
+    """Aggregate every row (or the listed rows) of a destination-major CSR.
+
+    x is fp32 [N_src, F] or x_bf16 is uint16 bit patterns.  w (fp32, CSR
+    order) optional.  Returns a dict with the requested fp64 'sum', 'mean',
+    'scale' and fp32 'max' + int64 'argmax' arrays of shape [rows, F]."""
+    rowptr, col = _c(rowptr, np.int64), _c(col, np.int32)
+    xa, isb, n_src, F = _x_args(x, x_bf16)
+    n_dst = rowptr.shape[0] - 1
+    rows = _c(rows, np.int64)
+    n = n_dst if rows is None else rows.shape[0]
+    w = _c(w, np.float32)
+    out = {}
+    s = np.empty((n, F), np.float64) if "sum" in want else None
+    m = np.empty((n, F), np.float64) if "mean" in want else None
+    mx = np.empty((n, F), np.float32) if "max" in want else None
+    am = np.empty((n, F), np.int64) if "max" in want else None
+    sc = np.empty((n, F), np.float64) if "scale" in want else None
+    if nthreads is None:
+        nthreads = os.cpu_count() or 1
+    rc = _L().oracle_spmm(n, _p(rows), n_dst, n_src, _p(rowptr), _p(col), _p(w), _p(xa), isb,
+                          F, _p(s), _p(m), _p(mx), _p(am), _p(sc), int(nthreads))
+    if rc != 0:
+        raise ValueError(f"oracle_spmm failed ({rc})")
+    for k, v in (("sum", s), ("mean", m), ("max", mx), ("argmax", am), ("scale", sc)):
+        if v is not None:
+            out[k] = v
+    return out
+
+
+def spmm_coo_rows(src, dst, n_dst, rows, x=None, x_bf16=None, w_coo=None, n_src=None):
+    """Outputs of the listed distinct rows, straight from COO (no CSR built).
+
+    argmax is reported as a position in the stable destination-major CSR."""
+    src, dst = _c(src, np.int32), _c(dst, np.int32)
+    xa, isb, nx, F = _x_args(x, x_bf16)
+    n_src = nx if n_src is None else n_src
+    rows = _c(rows, np.int64)
+    n = rows.shape[0]
+    s = np.empty((n, F), np.float64)
+    m = np.empty((n, F), np.float64)
+    mx = np.empty((n, F), np.float32)
+    am = np.empty((n, F), np.int64)
+    sc = np.empty((n, F), np.float64)
+    w_coo = _c(w_coo, np.float32)
+    rc = _L().oracle_spmm_coo_rows(src.shape[0], n_dst, n_src, _p(src), _p(dst), _p(w_coo),
+                                   _p(xa), isb, F, n, _p(rows), _p(s), _p(m), _p(mx), _p(am),
+                                   _p(sc))
+    if rc != 0:
+        raise ValueError(f"oracle_spmm_coo_rows failed ({rc})")
+    return {"sum": s, "mean": m, "max": mx, "argmax": am, "scale": sc}
+
+
+def hetero_sum(n_per_type, x_bf16_per_type, rel_src_type, rel_dst_type, rel_src, rel_dst):
+    """Nested sum: per destination type, the sum over its incoming relations of
+    the per-relation sums.  Returns (out list fp64 [N_t, F], scale list)."""
+    T = len(n_per_type)
+    xs = [_c(x, np.uint16) for x in x_bf16_per_type]
+    F = xs[0].shape[1]
+    npt = np.asarray(n_per_type, np.int64)
+    outs = [np.empty((n, F), np.float64) for n in n_per_type]
+    scs = [np.empty((n, F), np.float64) for n in n_per_type]
+    rs = [_c(a, np.int32) for a in rel_src]
+    rd = [_c(a, np.int32) for a in rel_dst]
+    R = len(rs)
+    arr = lambda lst: (ctypes.c_void_p * len(lst))(*[a.ctypes.data for a in lst])
+    # keep every temporary alive across the call
+    rst = np.asarray(rel_src_type, np.int32)
+    rdt = np.asarray(rel_dst_type, np.int32)
+    re_ = np.asarray([a.shape[0] for a in rs], np.int64)
+    rc = _L().oracle_hetero_sum(T, _p(npt), arr(xs), 1, F, R, _p(rst), _p(rdt), _p(re_),
+                                arr(rs) if R else None, arr(rd) if R else None,
+                                arr(outs), arr(scs))
+    if rc != 0:
+        raise ValueError(f"oracle_hetero_sum failed ({rc})")
+    return outs, scs
+

@@ -1,0 +1,250 @@
+/*
+ * CPU oracle for the message-passing aggregation path.
+ *
+ * TEST INFRASTRUCTURE ONLY.  Only the tests, the smoke check and the CPU
+ * baseline leg of the benchmark may load this code; the device library never
+ * links, calls or includes it, and it includes nothing from the device
+ * library.
+ *
+ * Everything here is the plain definition, written for a reader to check by
+ * eye against the paper (PyG 2.0, arXiv 2507.16991):
+ *
+ *  - Eq. (1): h_v' = f(h_v, AGG{ g(h_w, e_wv, h_v) : w in N(v) }).  This path
+ *    is the AGGREGATION step with message g = e_wv * h_w (a scalar edge
+ *    weight, or no weight) and f left to the caller.  The aggregator is one of
+ *    the permutation-invariant set functions named next to Eq. (1): sum, mean,
+ *    max (the max also reports which edge attains it).
+ *  - Sec. 2.2 "Accelerated Message Passing": the COO edge_index is converted
+ *    to a compressed sparse format sorted by node, so that aggregation becomes
+ *    a segmented reduction.  Rows here are destinations v (Eq. (1) aggregates
+ *    at v over incoming edges (w, v)); within a row, edges keep their original
+ *    COO order (a stable sort).
+ *  - Sec. 2.2 "Heterogeneous Message Passing": the nested version of Eq. (1)
+ *    adds a sum over the incoming edge types of each destination node type.
+ *
+ * Precision: all sums in fp64.  A weighted message is the fp32 product
+ * fl32(w * x) (the product of two fp32 values is exact in fp64, so rounding it
+ * once to fp32 gives the correctly rounded fp32 message).  An unweighted
+ * message is x itself (bf16 features widen exactly to fp32).
+ *
+ * Readings where the paper is silent: empty rows aggregate to 0 (and argmax
+ * -1); max keeps the first edge (lowest CSR position) among equal values,
+ * comparing with '>' so that -0.0 and +0.0 tie; mean is sum / in-degree.
+ */
+#include <math.h>
+#include <stdint.h>
+#include <stdlib.h>
+#include <string.h>
+
+/* ---- COO -> CSR (stable counting sort by destination) ------------------ */
+
+/* rowptr[N+1] (int64), col[E] = src of the p-th edge in destination order,
+ * perm[E] = its COO edge id, val_out[E] = val_in[perm] (if both given).
+ * Returns 0, or -1 when an index is out of range. */
+int oracle_coo_to_csr(int64_t E, int64_t N_dst, int64_t N_src, const int32_t* src,
+                      const int32_t* dst, const float* val_in, int64_t* rowptr,
+                      int32_t* col, int64_t* perm, float* val_out) {
+    for (int64_t e = 0; e < E; ++e)
+        if (dst[e] < 0 || dst[e] >= N_dst || src[e] < 0 || src[e] >= N_src) return -1;
+
+    /* in-degree of every destination */
+    for (int64_t v = 0; v <= N_dst; ++v) rowptr[v] = 0;
+    for (int64_t e = 0; e < E; ++e) rowptr[dst[e] + 1] += 1;
+    /* rowptr[v+1] = rowptr[v] + deg(v) */
+    for (int64_t v = 0; v < N_dst; ++v) rowptr[v + 1] += rowptr[v];
+
+    /* place edges in COO order: each destination's edges stay in order */
+    int64_t* cursor = (int64_t*)malloc(sizeof(int64_t) * (size_t)(N_dst > 0 ? N_dst : 1));
+    if (!cursor) return -2;
+    for (int64_t v = 0; v < N_dst; ++v) cursor[v] = rowptr[v];
+    for (int64_t e = 0; e < E; ++e) {
+        int64_t p = cursor[dst[e]]++;
+        if (col) col[p] = src[e];
+        if (perm) perm[p] = e;
+        if (val_in && val_out) val_out[p] = val_in[e];
+    }
+    free(cursor);
+    return 0;
+}
+
+/* ---- messages --------------------------------------------------------- */
+
+static inline float widen_bf16(uint16_t b) {
+    uint32_t u = (uint32_t)b << 16;
+    float f;
+    memcpy(&f, &u, 4);
+    return f;
+}
+
+/* feature x[row, f] widened to fp32 */
+static inline float feature(const void* x, int x_is_bf16, int64_t F, int64_t row,
+                            int64_t f) {
+    if (x_is_bf16) return widen_bf16(((const uint16_t*)x)[row * F + f]);
+    return ((const float*)x)[row * F + f];
+}
+
+/* message of edge p for feature f: x (unweighted) or fl32(w * x) */
+static inline float message(const void* x, int x_is_bf16, int64_t F, int64_t row,
+                            int64_t f, const float* w, int64_t p) {
+    float xv = feature(x, x_is_bf16, F, row, f);
+    if (!w) return xv;
+    return (float)((double)w[p] * (double)xv);
+}
+
+/* ---- aggregation over CSR ---------------------------------------------- */
+
+/* For each listed row i (rows == NULL: rows 0..n_rows-1) and each feature f,
+ * over the CSR edges p in [rowptr[i], rowptr[i+1]):
+ *   out_sum[k,f]  = sum_p m_p                      (fp64)
+ *   out_mean[k,f] = out_sum[k,f] / deg_i            (0 if deg_i = 0)
+ *   out_max[k,f]  = m_arg, argout[k,f] = arg, where arg is the first p with
+ *                   the largest m_p ('>' scan; -1 and 0.0 for an empty row)
+ *   scale[k,f]    = sum_p |m_p|                     (error scale of the sum)
+ * k indexes the output rows in list order.  Any output may be NULL.
+ * Rows are independent; nthreads > 0 splits them over OpenMP threads.
+ * Returns 0, or -1 for an out-of-range column or row. */
+int oracle_spmm(int64_t n_rows, const int64_t* rows, int64_t N_dst, int64_t N_src,
+                const int64_t* rowptr, const int32_t* col, const float* w, const void* x,
+                int x_is_bf16, int64_t F, double* out_sum, double* out_mean,
+                float* out_max, int64_t* argout, double* scale, int nthreads) {
+    int bad = 0;
+#pragma omp parallel for schedule(static) num_threads(nthreads > 0 ? nthreads : 1) reduction(| : bad)
+    for (int64_t k = 0; k < n_rows; ++k) {
+        int64_t i = rows ? rows[k] : k;
+        if (i < 0 || i >= N_dst) {
+            bad = 1;
+            continue;
+        }
+        int64_t p0 = rowptr[i], p1 = rowptr[i + 1];
+        for (int64_t p = p0; p < p1; ++p)
+            if (col[p] < 0 || col[p] >= N_src) bad = 1;
+        if (bad) continue;
+        int64_t deg = p1 - p0;
+        for (int64_t f = 0; f < F; ++f) {
+            double s = 0.0, a = 0.0;
+            float best = 0.0f;
+            int64_t arg = -1;
+            for (int64_t p = p0; p < p1; ++p) {
+                float m = message(x, x_is_bf16, F, col[p], f, w, p);
+                s += (double)m;
+                a += fabs((double)m);
+                if (arg < 0 || m > best) {
+                    best = m;
+                    arg = p;
+                }
+            }
+            if (out_sum) out_sum[k * F + f] = s;
+            if (out_mean) out_mean[k * F + f] = deg > 0 ? s / (double)deg : 0.0;
+            if (out_max) out_max[k * F + f] = arg < 0 ? 0.0f : best;
+            if (argout) argout[k * F + f] = arg;
+            if (scale) scale[k * F + f] = a;
+        }
+    }
+    return bad ? -1 : 0;
+}
+
+/* ---- aggregation of listed rows straight from COO ----------------------- */
+
+/* Same outputs as oracle_spmm for the listed (distinct) rows, computed from
+ * the COO arrays without building the CSR: one pass over the edges in COO
+ * order, so each row sees its edges in the order of the stable CSR, and the
+ * CSR position of edge e is rowptr[dst_e] + (number of earlier edges with the
+ * same destination).  `w` is in COO order here.  Meant for graphs too large to
+ * convert on the host; one thread.  Returns 0, -1 on a bad index, -2 on
+ * allocation failure. */
+int oracle_spmm_coo_rows(int64_t E, int64_t N_dst, int64_t N_src, const int32_t* src,
+                         const int32_t* dst, const float* w_coo, const void* x,
+                         int x_is_bf16, int64_t F, int64_t n_rows, const int64_t* rows,
+                         double* out_sum, double* out_mean, float* out_max,
+                         int64_t* argout, double* scale) {
+    int64_t* slot = (int64_t*)malloc(sizeof(int64_t) * (size_t)(N_dst > 0 ? N_dst : 1));
+    int64_t* below = (int64_t*)calloc((size_t)(N_dst + 1), sizeof(int64_t));
+    int64_t* seen = (int64_t*)calloc((size_t)(n_rows > 0 ? n_rows : 1), sizeof(int64_t));
+    double* acc = (double*)calloc((size_t)((n_rows > 0 ? n_rows : 1) * (F > 0 ? F : 1)),
+                                  sizeof(double));
+    if (!slot || !below || !seen || !acc) {
+        free(slot); free(below); free(seen); free(acc);
+        return -2;
+    }
+    for (int64_t v = 0; v < N_dst; ++v) slot[v] = -1;
+    for (int64_t k = 0; k < n_rows; ++k) {
+        if (rows[k] < 0 || rows[k] >= N_dst) {
+            free(slot); free(below); free(seen); free(acc);
+            return -1;
+        }
+        slot[rows[k]] = k;
+    }
+    /* rowptr[v] = number of edges whose destination is below v */
+    for (int64_t e = 0; e < E; ++e) {
+        if (dst[e] < 0 || dst[e] >= N_dst || src[e] < 0 || src[e] >= N_src) {
+            free(slot); free(below); free(seen); free(acc);
+            return -1;
+        }
+        below[dst[e] + 1] += 1;
+    }
+    for (int64_t v = 0; v < N_dst; ++v) below[v + 1] += below[v];
+
+    for (int64_t k = 0; k < n_rows; ++k)
+        for (int64_t f = 0; f < F; ++f) {
+            if (out_max) out_max[k * F + f] = 0.0f;
+            if (argout) argout[k * F + f] = -1;
+            if (scale) scale[k * F + f] = 0.0;
+        }
+    for (int64_t e = 0; e < E; ++e) {
+        int64_t k = slot[dst[e]];
+        if (k < 0) continue;
+        int64_t p = below[dst[e]] + seen[k];
+        seen[k] += 1;
+        for (int64_t f = 0; f < F; ++f) {
+            float xv = feature(x, x_is_bf16, F, src[e], f);
+            float m = w_coo ? (float)((double)w_coo[e] * (double)xv) : xv;
+            acc[k * F + f] += (double)m;
+            if (scale) scale[k * F + f] += fabs((double)m);
+            if (out_max && argout && (argout[k * F + f] < 0 || m > out_max[k * F + f])) {
+                out_max[k * F + f] = m;
+                argout[k * F + f] = p;
+            }
+        }
+    }
+    for (int64_t k = 0; k < n_rows; ++k)
+        for (int64_t f = 0; f < F; ++f) {
+            if (out_sum) out_sum[k * F + f] = acc[k * F + f];
+            if (out_mean) out_mean[k * F + f] = seen[k] > 0 ? acc[k * F + f] / (double)seen[k] : 0.0;
+        }
+    free(slot); free(below); free(seen); free(acc);
+    return 0;
+}
+
+/* ---- heterogeneous sum -------------------------------------------------- */
+
+/* Nested Eq. (1) with sum at both levels: for every destination type T,
+ *   out_T[i, f] = sum over relations r with rel_dst_type[r] == T (ascending r)
+ *                 of sum over r's edges e with rel_dst[r][e] == i (COO order)
+ *                 of x_{rel_src_type[r]}[rel_src[r][e], f].
+ * out_per_type[T] and scale_per_type[T] are [N_T, F] fp64 buffers (scale may
+ * be NULL).  Returns 0, or -1 on a bad type or index. */
+int oracle_hetero_sum(int n_types, const int64_t* n_per_type, const void* const* x_per_type,
+                      int x_is_bf16, int64_t F, int n_rel, const int32_t* rel_src_type,
+                      const int32_t* rel_dst_type, const int64_t* rel_E,
+                      const int32_t* const* rel_src, const int32_t* const* rel_dst,
+                      double* const* out_per_type, double* const* scale_per_type) {
+    for (int t = 0; t < n_types; ++t)
+        for (int64_t k = 0; k < n_per_type[t] * F; ++k) {
+            out_per_type[t][k] = 0.0;
+            if (scale_per_type) scale_per_type[t][k] = 0.0;
+        }
+    for (int r = 0; r < n_rel; ++r) {
+        int st = rel_src_type[r], dt = rel_dst_type[r];
+        if (st < 0 || st >= n_types || dt < 0 || dt >= n_types) return -1;
+        for (int64_t e = 0; e < rel_E[r]; ++e) {
+            int64_t s = rel_src[r][e], d = rel_dst[r][e];
+            if (s < 0 || s >= n_per_type[st] || d < 0 || d >= n_per_type[dt]) return -1;
+            for (int64_t f = 0; f < F; ++f) {
+                double m = (double)feature(x_per_type[st], x_is_bf16, F, s, f);
+                out_per_type[dt][d * F + f] += m;
+                if (scale_per_type) scale_per_type[dt][d * F + f] += fabs(m);
+            }
+        }
+    }
+    return 0;
+}
