@@ -295,3 +295,16 @@ def workload(name: str, seed: int = 0, scale: float = 1.0, **kw):
         return powerlaw_dst_graph(seed, s(c["n"]), s(c["e"]), c["f"], c["alpha"],
                                   feat="uniform", bf16=True, fp32=False, **kw)
     raise KeyError(name)
+
+
+def mixed_graph(seed: int, n: int = 3000, e: int = 40_000, f: int = 64, alpha: float = 2.1,
+                signed_weights: bool = False, bf16: bool = True) -> Graph:
+    """Small power-law graph with every degree regime at once: ~18% empty
+    rows, many small rows, mid rows and a few hubs of ~1-2k edges.  Weights
+    are GCN-style (positive) or U(-1,1) (signed)."""
+    g = powerlaw_dst_graph(seed, n, e, f, alpha, feat="normal", weights=not signed_weights,
+                           bf16=bf16, fp32=True)
+    if signed_weights:
+        g.w = uniform_f32(seed, 7, e)
+    g.name = f"mixed-n{n}-e{e}-f{f}"
+    return g

@@ -1,0 +1,238 @@
+/*
+ * mp.h -- C ABI of the message-passing aggregation library (libmp.so).
+ *
+ * The library implements the AGGREGATION step of message passing as written
+ * in PyG 2.0 (arXiv 2507.16991), Eq. (1):
+ *
+ *     h_v' = f( h_v, AGG{ g(h_w, e_wv, h_v) : w in N(v) } )
+ *
+ * with message g = e_wv * h_w (e_wv an optional scalar edge weight) and the
+ * permutation-invariant aggregators sum, mean and max named next to Eq. (1).
+ * The update f is left to the caller.  Following Sec. 2.2 ("Accelerated
+ * Message Passing"), the COO edge_index is first converted into a
+ * destination-sorted compressed format, after which aggregation is a
+ * segmented reduction per destination row.  The heterogeneous variant
+ * (Sec. 2.2, "Heterogeneous Message Passing", the nested Eq. (1)) sums the
+ * per-relation aggregations into each destination node type.
+ *
+ * Conventions shared by every call:
+ *  - Orientation.  "CSR" here is destination-major: row v lists the edges
+ *    (w, v) that end at v, and col holds their sources w.  This is the CSR of
+ *    A^T (equivalently the CSC of A).
+ *  - Pointers.  Array arguments are DEVICE pointers, allocated and owned by
+ *    the caller.  The library allocates no device memory and keeps no array
+ *    pointer after a call returns.  Scratch space is passed in as a
+ *    caller-allocated workspace whose size comes from the matching *_workspace
+ *    or *_size query.  Host pointers are marked "host".
+ *  - Streams.  `stream` is a hipStream_t passed as void* (NULL = the default
+ *    stream).  Every call only enqueues work and returns without waiting for
+ *    the device, except mp_spmm_plan_build (one device-to-host copy, stated
+ *    there).
+ *  - Errors.  Calls return MP_OK (0) or a negative mp_status.  Argument
+ *    errors are detected on the host before anything is enqueued, and leave
+ *    every output untouched.  MP_ERR_HIP reports a failed launch or copy.
+ *  - Index validity.  Edge indices must satisfy 0 <= src < N_src and
+ *    0 <= dst < N_dst, and a rowptr must be non-decreasing with rowptr[0] = 0
+ *    and rowptr[N_dst] = E.  Violations are not detected by the compute calls
+ *    (their behaviour is then undefined); mp_validate_coo and mp_validate_csr
+ *    count them.
+ *  - Determinism.  Every output is a deterministic function of the inputs:
+ *    the floating-point summation order is fixed by the plan geometry, and no
+ *    floating-point atomics are used.
+ */
+#ifndef MP_H_
+#define MP_H_
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+#define MP_VERSION 1
+
+/* Status codes. */
+typedef enum mp_status {
+    MP_OK = 0,
+    MP_ERR_NULL = -1,      /* a required pointer is NULL */
+    MP_ERR_SIZE = -2,      /* negative or unsupported size (see each call) */
+    MP_ERR_DTYPE = -3,     /* unknown or unsupported dtype / index type */
+    MP_ERR_REDUCE = -4,    /* unknown or unsupported reduction */
+    MP_ERR_WORKSPACE = -5, /* workspace or plan buffer too small */
+    MP_ERR_PLAN = -6,      /* plan does not match the arguments */
+    MP_ERR_HIP = -7,       /* a HIP launch, copy or query failed */
+    MP_ERR_ALIGN = -8      /* a pointer is not aligned to its element size */
+} mp_status;
+
+/* Feature / output element types. */
+typedef enum mp_dtype { MP_F32 = 0, MP_BF16 = 1 } mp_dtype;
+
+/* rowptr element types. */
+typedef enum mp_itype { MP_I32 = 0, MP_I64 = 1 } mp_itype;
+
+/* Reductions, a bit mask.  Allowed values: MP_SUM, MP_MEAN, MP_MAX,
+ * MP_SUM|MP_MAX and MP_MEAN|MP_MAX (the fused pass: one gather feeds both). */
+typedef enum mp_reduce { MP_SUM = 1, MP_MEAN = 2, MP_MAX = 4 } mp_reduce;
+
+/* Library version (MP_VERSION). */
+int mp_version(void);
+
+/* Static description of a status code; never NULL. */
+const char* mp_status_str(int status);
+
+/* ---------------------------------------------------------------------------
+ * COO -> CSR conversion (Sec. 2.2: the sorted edge_index and its CSR cache).
+ * ------------------------------------------------------------------------- */
+
+/* Workspace bytes for mp_coo_to_csr with E edges and N destination rows.
+ * with_payload: 1 if the call will request perm or val_out, else 0.
+ * Sizes: 0 <= E <= INT32_MAX, 1 <= N <= INT32_MAX (else MP_ERR_SIZE).
+ * *bytes (host) receives the size. */
+int mp_coo_to_csr_workspace(int64_t E, int64_t N, int rowptr_itype, int with_payload,
+                            size_t* bytes);
+
+/* Stable sort of the COO edges by destination, producing the
+ * destination-major CSR.
+ *   src, dst    [E] int32 COO edge endpoints (device, read only).
+ *   rowptr      [N+1] of rowptr_itype (MP_I32 or MP_I64): rowptr[0] = 0,
+ *               rowptr[v+1] - rowptr[v] = in-degree of v, rowptr[N] = E.
+ *   col         [E] int32: col[p] = source of the p-th edge in CSR order.
+ *   perm        [E] int32 or NULL: perm[p] = COO id of the p-th CSR edge.
+ *   val_in      [E] fp32 or NULL: per-edge values in COO order.
+ *   val_out     [E] fp32 or NULL (given iff val_in is): val_in[perm[p]].
+ * Within a row, edges keep ascending COO id (stable), so the result is
+ * unique and bit-exact.  Duplicates and self-loops are ordinary edges.
+ * E = 0 is valid (rowptr all zero).  ws/ws_bytes: workspace from
+ * mp_coo_to_csr_workspace.  Asynchronous on `stream`. */
+int mp_coo_to_csr(const int32_t* src, const int32_t* dst, int64_t E, int64_t N,
+                  void* rowptr, int rowptr_itype, int32_t* col, int32_t* perm,
+                  const float* val_in, float* val_out, void* ws, size_t ws_bytes,
+                  void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Aggregation plan: rows binned by in-degree (Sec. 2.2: the sorted layout
+ * "enables greater parallelism"; the plan is built once per CSR and reused,
+ * like the CSR cache).
+ * ------------------------------------------------------------------------- */
+
+typedef struct mp_plan mp_plan;
+
+/* Device bytes of the plan buffer for a CSR with N_dst rows and E edges. */
+int mp_spmm_plan_size(int64_t N_dst, int64_t E, size_t* bytes);
+
+/* Build a plan for one CSR and one feature geometry (F, x_dtype).
+ *   rowptr      [N_dst+1] of rowptr_itype (device).
+ *   plan_buf    device buffer of mp_spmm_plan_size bytes, owned by the caller,
+ *               which must keep it alive and unchanged while the plan is used.
+ *   *out        (host) receives a host-side handle; free with
+ *               mp_spmm_plan_free.
+ * This call SYNCHRONIZES `stream` once: it copies the per-bin row counts to
+ * the host to size later launches.  The plan stays valid while rowptr and
+ * plan_buf are unchanged. */
+int mp_spmm_plan_build(const void* rowptr, int rowptr_itype, int64_t N_dst, int64_t E,
+                       int64_t F, int x_dtype, void* plan_buf, size_t plan_bytes,
+                       void* stream, mp_plan** out);
+
+/* Release a host handle (NULL is ignored).  Does not touch plan_buf. */
+void mp_spmm_plan_free(mp_plan* plan);
+
+/* Workspace bytes mp_spmm needs with this plan and reduction (partial
+ * results of hub rows split into edge chunks).  plan may be NULL (then 0). */
+int mp_spmm_workspace(const mp_plan* plan, int reduce, size_t* bytes);
+
+/* Segmented aggregation over the destination-major CSR (Eq. (1), the
+ * AGGREGATION step; messages m_p = x[col[p], :] or w[p] * x[col[p], :]).
+ *   plan        from mp_spmm_plan_build for this rowptr, N_dst, E, F and
+ *               x_dtype, or NULL (then one wavefront per row, no hub split,
+ *               no workspace).
+ *   rowptr      [N_dst+1] of rowptr_itype; col [E] int32 (E = rowptr[N_dst],
+ *               taken from the plan, or read from the device when plan is
+ *               NULL -- that read is a blocking copy).
+ *   w           [E] fp32 in CSR order, or NULL (unweighted).
+ *   x           [N_src, F] row-major, x_dtype (MP_F32 or MP_BF16).
+ *   reduce      MP_SUM, MP_MEAN, MP_MAX, MP_SUM|MP_MAX or MP_MEAN|MP_MAX.
+ *   out         [N_dst, F] of out_dtype: the sum or mean (required iff
+ *               reduce has SUM or MEAN).  Accumulation is fp32; a bf16 output
+ *               is rounded to nearest even once at the end.
+ *   out_max     [N_dst, F] of max_dtype: the max message (required iff
+ *               reduce has MAX).  max_dtype MP_BF16 is allowed only for bf16
+ *               x without weights, where it is exact.
+ *   argout      [N_dst, F] int32 (required iff reduce has MAX): the CSR
+ *               position p of the first edge attaining the maximum.
+ * Output rows are written in full (nothing is accumulated into them).  An
+ * empty row gives 0 for sum, mean and max, and -1 in argout.  Messages are
+ * compared with '>' so that -0.0 and +0.0 tie and the earlier edge wins.
+ * A weighted message for MAX is the fp32 product fl32(w * x); sums may fuse
+ * the multiply into the add.  Size limits: 0 <= N_src, N_dst <= INT32_MAX,
+ * 1 <= F <= 65536, E <= INT32_MAX (argout and col are int32).
+ * Asynchronous on `stream` (no host synchronization when plan != NULL). */
+int mp_spmm(const mp_plan* plan, const void* rowptr, int rowptr_itype, const int32_t* col,
+            const float* w, const void* x, int x_dtype, int64_t N_src, int64_t N_dst,
+            int64_t F, int reduce, void* out, int out_dtype, void* out_max, int max_dtype,
+            int32_t* argout, void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Heterogeneous message passing (Sec. 2.2, nested Eq. (1)): per destination
+ * node type T, out_T = sum over relations r ending at T (ascending r) of the
+ * sum aggregation over r's edges.  Built as one combined destination-major
+ * CSR per destination type, whose edges within a row are ordered by
+ * (relation id, COO id), and whose col holds GLOBAL source ids: local id plus
+ * the offset of the source type (offsets = prefix sums of N_per_type).
+ * ------------------------------------------------------------------------- */
+
+#define MP_MAX_TYPES 16
+
+/* One relation: edges src_type -> dst_type with local int32 endpoints. */
+typedef struct mp_relation {
+    int32_t src_type;
+    int32_t dst_type;
+    const int32_t* src; /* [E] device, local ids in src_type */
+    const int32_t* dst; /* [E] device, local ids in dst_type */
+    int64_t E;
+} mp_relation;
+
+/* Workspace bytes for mp_hetero_build of destination type dst_type.
+ * N_per_type and rels are host arrays. */
+int mp_hetero_build_workspace(int n_types, const int64_t* N_per_type, int n_rel,
+                              const mp_relation* rels, int dst_type, int rowptr_itype,
+                              size_t* bytes);
+
+/* Build the combined CSR of destination type dst_type:
+ *   rowptr [N_per_type[dst_type]+1] of rowptr_itype, col [E_T] int32 global
+ *   source ids, where E_T = sum of E over relations ending at dst_type.
+ * n_types <= MP_MAX_TYPES; the total node count must fit int32. */
+int mp_hetero_build(int n_types, const int64_t* N_per_type, int n_rel,
+                    const mp_relation* rels, int dst_type, void* rowptr, int rowptr_itype,
+                    int32_t* col, void* ws, size_t ws_bytes, void* stream);
+
+/* Sum aggregation over a combined CSR from mp_hetero_build, gathering each
+ * source row from its own type's feature table.
+ *   x_per_type  host array of n_types device pointers, each [N_t, F] x_dtype.
+ *   plan        from mp_spmm_plan_build on this rowptr (or NULL).
+ *   reduce      MP_SUM only (the cross-relation aggregator is a sum).
+ *   out         [N_per_type[dst_type], F] of out_dtype. */
+int mp_hetero_spmm(int n_types, const int64_t* N_per_type, const void* const* x_per_type,
+                   int x_dtype, int64_t F, int dst_type, const mp_plan* plan,
+                   const void* rowptr, int rowptr_itype, const int32_t* col, int reduce,
+                   void* out, int out_dtype, void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Debug checks.  Each writes the number of violations into *d_count, a
+ * device int64, on `stream`.
+ * ------------------------------------------------------------------------- */
+
+/* Counts edges with src outside [0, N_src) or dst outside [0, N_dst). */
+int mp_validate_coo(const int32_t* src, const int32_t* dst, int64_t E, int64_t N_src,
+                    int64_t N_dst, int64_t* d_count, void* stream);
+
+/* Counts rowptr steps that decrease, rowptr[0] != 0, rowptr[N_dst] != E, and
+ * col entries outside [0, N_src). */
+int mp_validate_csr(const void* rowptr, int rowptr_itype, const int32_t* col, int64_t N_dst,
+                    int64_t N_src, int64_t E, int64_t* d_count, void* stream);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* MP_H_ */

@@ -1,0 +1,342 @@
+"""Python binding of libmp, the MI355X message-passing aggregation library.
+
+Argument marshalling only: every step of the path runs in the HIP kernels of
+``libmp.so`` (built from ``csrc/`` by ``build.py``).  Tensors are torch
+tensors on the GPU; torch supplies device memory and the current stream.
+There is no fallback: if the library is missing, importing the binding's
+entry points raises.
+
+Two layers:
+  * ``mp_*`` functions with the names of the C ABI (``include/mp.h``), taking
+    tensors or None for pointers and raising ``MPError`` on a non-zero status;
+  * convenience wrappers (``coo_to_csr``, ``Plan``, ``spmm``, ``hetero_build``,
+    ``hetero_spmm``) that size and allocate outputs and workspaces with torch.
+"""
+from __future__ import annotations
+
+import ctypes
+import os
+
+import torch
+
+__all__ = [
+    "MPError", "lib", "MP_F32", "MP_BF16", "MP_I32", "MP_I64", "MP_SUM", "MP_MEAN", "MP_MAX",
+    "mp_version", "mp_status_str", "mp_coo_to_csr_workspace", "mp_coo_to_csr",
+    "mp_spmm_plan_size", "mp_spmm_plan_build", "mp_spmm_plan_free", "mp_spmm_workspace",
+    "mp_spmm", "mp_hetero_build_workspace", "mp_hetero_build", "mp_hetero_spmm",
+    "mp_validate_coo", "mp_validate_csr", "coo_to_csr", "Plan", "spmm", "hetero_build",
+    "hetero_spmm", "LIB_PATH",
+]
+
+_HERE = os.path.dirname(os.path.abspath(__file__))
+LIB_PATH = os.path.join(_HERE, "libmp.so")
+
+MP_OK = 0
+MP_F32, MP_BF16 = 0, 1
+MP_I32, MP_I64 = 0, 1
+MP_SUM, MP_MEAN, MP_MAX = 1, 2, 4
+MP_MAX_TYPES = 16
+
+_lib = None
+
+
+class MPError(RuntimeError):
+    def __init__(self, fn: str, status: int):
+        super().__init__(f"{fn} failed: {status} ({mp_status_str(status)})")
+        self.status = status
+
+
+class mp_relation(ctypes.Structure):
+    _fields_ = [("src_type", ctypes.c_int32), ("dst_type", ctypes.c_int32),
+                ("src", ctypes.c_void_p), ("dst", ctypes.c_void_p), ("E", ctypes.c_int64)]
+
+
+def lib():
+    """The loaded libmp.so; raises if it has not been built."""
+    global _lib
+    if _lib is None:
+        if not os.path.exists(LIB_PATH):
+            raise ImportError(f"{LIB_PATH} is missing: build it with "
+                              "`python -m paper_2507_16991_amd.build`")
+        L = ctypes.CDLL(LIB_PATH)
+        i32, i64, p, sz = ctypes.c_int, ctypes.c_int64, ctypes.c_void_p, ctypes.c_size_t
+        psz = ctypes.POINTER(ctypes.c_size_t)
+        L.mp_version.restype = i32
+        L.mp_status_str.argtypes = [i32]
+        L.mp_status_str.restype = ctypes.c_char_p
+        L.mp_coo_to_csr_workspace.argtypes = [i64, i64, i32, i32, psz]
+        L.mp_coo_to_csr.argtypes = [p, p, i64, i64, p, i32, p, p, p, p, p, sz, p]
+        L.mp_spmm_plan_size.argtypes = [i64, i64, psz]
+        L.mp_spmm_plan_build.argtypes = [p, i32, i64, i64, i64, i32, p, sz, p,
+                                         ctypes.POINTER(ctypes.c_void_p)]
+        L.mp_spmm_plan_free.argtypes = [p]
+        L.mp_spmm_plan_free.restype = None
+        L.mp_spmm_workspace.argtypes = [p, i32, psz]
+        L.mp_spmm.argtypes = [p, p, i32, p, p, p, i32, i64, i64, i64, i32, p, i32, p, i32, p, p,
+                              sz, p]
+        L.mp_hetero_build_workspace.argtypes = [i32, p, i32, p, i32, i32, psz]
+        L.mp_hetero_build.argtypes = [i32, p, i32, p, i32, p, i32, p, p, sz, p]
+        L.mp_hetero_spmm.argtypes = [i32, p, p, i32, i64, i32, p, p, i32, p, i32, p, i32, p, sz,
+                                     p]
+        L.mp_validate_coo.argtypes = [p, p, i64, i64, i64, p, p]
+        L.mp_validate_csr.argtypes = [p, i32, p, i64, i64, i64, p, p]
+        for name in ("mp_coo_to_csr_workspace", "mp_coo_to_csr", "mp_spmm_plan_size",
+                     "mp_spmm_plan_build", "mp_spmm_workspace", "mp_spmm",
+                     "mp_hetero_build_workspace", "mp_hetero_build", "mp_hetero_spmm",
+                     "mp_validate_coo", "mp_validate_csr"):
+            getattr(L, name).restype = i32
+        _lib = L
+    return _lib
+
+
+# ---- marshalling helpers ------------------------------------------------------
+
+def _ptr(t):
+    if t is None:
+        return None
+    if isinstance(t, int):
+        return t
+    if not t.is_contiguous():
+        raise ValueError("tensors passed to libmp must be contiguous")
+    return t.data_ptr()
+
+
+def _stream(stream):
+    if stream is None:
+        return torch.cuda.current_stream().cuda_stream
+    return stream.cuda_stream if hasattr(stream, "cuda_stream") else stream
+
+
+def _dtype_code(dt):
+    if dt == torch.float32:
+        return MP_F32
+    if dt == torch.bfloat16:
+        return MP_BF16
+    raise ValueError(f"unsupported feature dtype {dt}")
+
+
+def _itype_code(dt):
+    if dt == torch.int32:
+        return MP_I32
+    if dt == torch.int64:
+        return MP_I64
+    raise ValueError(f"unsupported rowptr dtype {dt}")
+
+
+def _check(fn, st):
+    if st != MP_OK:
+        raise MPError(fn, st)
+
+
+def _bytes(fn, *args):
+    b = ctypes.c_size_t(0)
+    _check(fn, getattr(lib(), fn)(*args, ctypes.byref(b)))
+    return b.value
+
+
+def _workspace(nbytes, device):
+    return torch.empty(max(int(nbytes), 1), dtype=torch.uint8, device=device)
+
+
+# ---- C ABI names ---------------------------------------------------------------
+
+def mp_version() -> int:
+    return lib().mp_version()
+
+
+def mp_status_str(status: int) -> str:
+    return lib().mp_status_str(status).decode()
+
+
+def mp_coo_to_csr_workspace(E, N, rowptr_itype, with_payload) -> int:
+    return _bytes("mp_coo_to_csr_workspace", E, N, rowptr_itype, int(with_payload))
+
+
+def mp_coo_to_csr(src, dst, E, N, rowptr, rowptr_itype, col, perm, val_in, val_out, ws,
+                  ws_bytes, stream=None):
+    _check("mp_coo_to_csr", lib().mp_coo_to_csr(
+        _ptr(src), _ptr(dst), E, N, _ptr(rowptr), rowptr_itype, _ptr(col), _ptr(perm),
+        _ptr(val_in), _ptr(val_out), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def mp_spmm_plan_size(N_dst, E) -> int:
+    return _bytes("mp_spmm_plan_size", N_dst, E)
+
+
+def mp_spmm_plan_build(rowptr, rowptr_itype, N_dst, E, F, x_dtype, plan_buf, plan_bytes,
+                       stream=None) -> int:
+    h = ctypes.c_void_p(0)
+    _check("mp_spmm_plan_build", lib().mp_spmm_plan_build(
+        _ptr(rowptr), rowptr_itype, N_dst, E, F, x_dtype, _ptr(plan_buf), plan_bytes,
+        _stream(stream), ctypes.byref(h)))
+    return h.value
+
+
+def mp_spmm_plan_free(handle) -> None:
+    lib().mp_spmm_plan_free(handle)
+
+
+def mp_spmm_workspace(plan_handle, reduce) -> int:
+    return _bytes("mp_spmm_workspace", plan_handle, reduce)
+
+
+def mp_spmm(plan_handle, rowptr, rowptr_itype, col, w, x, x_dtype, N_src, N_dst, F, reduce, out,
+            out_dtype, out_max, max_dtype, argout, ws, ws_bytes, stream=None):
+    _check("mp_spmm", lib().mp_spmm(
+        plan_handle, _ptr(rowptr), rowptr_itype, _ptr(col), _ptr(w), _ptr(x), x_dtype, N_src,
+        N_dst, F, reduce, _ptr(out), out_dtype, _ptr(out_max), max_dtype, _ptr(argout), _ptr(ws),
+        ws_bytes, _stream(stream)))
+
+
+def _rel_array(rels):
+    arr = (mp_relation * max(len(rels), 1))()
+    for k, (st, dt, s, d) in enumerate(rels):
+        arr[k] = mp_relation(st, dt, _ptr(s), _ptr(d), int(s.numel()))
+    return arr
+
+
+def mp_hetero_build_workspace(N_per_type, rels, dst_type, rowptr_itype) -> int:
+    npt = (ctypes.c_int64 * len(N_per_type))(*N_per_type)
+    return _bytes("mp_hetero_build_workspace", len(N_per_type), npt, len(rels), _rel_array(rels),
+                  dst_type, rowptr_itype)
+
+
+def mp_hetero_build(N_per_type, rels, dst_type, rowptr, rowptr_itype, col, ws, ws_bytes,
+                    stream=None):
+    npt = (ctypes.c_int64 * len(N_per_type))(*N_per_type)
+    _check("mp_hetero_build", lib().mp_hetero_build(
+        len(N_per_type), npt, len(rels), _rel_array(rels), dst_type, _ptr(rowptr), rowptr_itype,
+        _ptr(col), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def mp_hetero_spmm(N_per_type, x_per_type, x_dtype, F, dst_type, plan_handle, rowptr,
+                   rowptr_itype, col, reduce, out, out_dtype, ws, ws_bytes, stream=None):
+    T = len(N_per_type)
+    npt = (ctypes.c_int64 * T)(*N_per_type)
+    xs = (ctypes.c_void_p * T)(*[_ptr(x) for x in x_per_type])
+    _check("mp_hetero_spmm", lib().mp_hetero_spmm(
+        T, npt, xs, x_dtype, F, dst_type, plan_handle, _ptr(rowptr), rowptr_itype, _ptr(col),
+        reduce, _ptr(out), out_dtype, _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def mp_validate_coo(src, dst, E, N_src, N_dst, d_count, stream=None):
+    _check("mp_validate_coo", lib().mp_validate_coo(_ptr(src), _ptr(dst), E, N_src, N_dst,
+                                                    _ptr(d_count), _stream(stream)))
+
+
+def mp_validate_csr(rowptr, rowptr_itype, col, N_dst, N_src, E, d_count, stream=None):
+    _check("mp_validate_csr", lib().mp_validate_csr(_ptr(rowptr), rowptr_itype, _ptr(col), N_dst,
+                                                    N_src, E, _ptr(d_count), _stream(stream)))
+
+
+# ---- convenience wrappers ---------------------------------------------------------
+
+def coo_to_csr(src: torch.Tensor, dst: torch.Tensor, N: int, *, rowptr_dtype=torch.int32,
+               want_perm=False, val=None, stream=None, ws=None):
+    """Stable destination-major CSR of the COO edges (src, dst int32 on GPU).
+
+    Returns (rowptr, col, perm or None, val_csr or None)."""
+    E = int(src.numel())
+    dev = src.device
+    it = _itype_code(rowptr_dtype)
+    rowptr = torch.empty(N + 1, dtype=rowptr_dtype, device=dev)
+    col = torch.empty(max(E, 0), dtype=torch.int32, device=dev)
+    perm = torch.empty(E, dtype=torch.int32, device=dev) if want_perm else None
+    vout = torch.empty(E, dtype=torch.float32, device=dev) if val is not None else None
+    nb = mp_coo_to_csr_workspace(E, N, it, want_perm or val is not None)
+    if ws is None or ws.numel() < nb:
+        ws = _workspace(nb, dev)
+    mp_coo_to_csr(src, dst, E, N, rowptr, it, col, perm, val, vout, ws, ws.numel(), stream)
+    return rowptr, col, perm, vout
+
+
+class Plan:
+    """Degree-binned aggregation plan for one CSR and one (F, dtype).
+
+    Building it synchronizes the stream once (bin sizes go to the host)."""
+
+    def __init__(self, rowptr: torch.Tensor, E: int, F: int, x_dtype=torch.float32, stream=None):
+        self.rowptr = rowptr
+        self.itype = _itype_code(rowptr.dtype)
+        self.N_dst = int(rowptr.numel()) - 1
+        self.E, self.F = int(E), int(F)
+        self.x_dtype = _dtype_code(x_dtype)
+        nb = mp_spmm_plan_size(self.N_dst, self.E)
+        self.buf = _workspace(nb, rowptr.device)
+        self.handle = mp_spmm_plan_build(rowptr, self.itype, self.N_dst, self.E, self.F,
+                                         self.x_dtype, self.buf, self.buf.numel(), stream)
+        self._ws = {}
+
+    def workspace(self, reduce: int) -> torch.Tensor | None:
+        nb = mp_spmm_workspace(self.handle, reduce)
+        if nb == 0:
+            return None
+        t = self._ws.get(reduce)
+        if t is None or t.numel() < nb:
+            t = self._ws[reduce] = _workspace(nb, self.rowptr.device)
+        return t
+
+    def __del__(self):
+        h = getattr(self, "handle", None)
+        if h:
+            mp_spmm_plan_free(h)
+            self.handle = None
+
+
+def spmm(rowptr, col, x, reduce, *, w=None, plan: Plan | None = None, out_dtype=torch.float32,
+         max_dtype=None, out=None, out_max=None, argout=None, stream=None):
+    """Aggregate x over the destination-major CSR.
+
+    reduce: MP_SUM, MP_MEAN, MP_MAX or MP_SUM|MP_MAX / MP_MEAN|MP_MAX.
+    Returns (out or None, out_max or None, argout or None)."""
+    N_dst = int(rowptr.numel()) - 1
+    N_src, F = int(x.shape[0]), int(x.shape[1])
+    dev = x.device
+    hs = bool(reduce & (MP_SUM | MP_MEAN))
+    hm = bool(reduce & MP_MAX)
+    if max_dtype is None:
+        max_dtype = torch.float32
+    if hs and out is None:
+        out = torch.empty(N_dst, F, dtype=out_dtype, device=dev)
+    if hm and out_max is None:
+        out_max = torch.empty(N_dst, F, dtype=max_dtype, device=dev)
+    if hm and argout is None:
+        argout = torch.empty(N_dst, F, dtype=torch.int32, device=dev)
+    ws = plan.workspace(reduce) if plan is not None else None
+    mp_spmm(plan.handle if plan is not None else None, rowptr, _itype_code(rowptr.dtype), col, w,
+            x, _dtype_code(x.dtype), N_src, N_dst, F, reduce, out if hs else None,
+            _dtype_code(out.dtype) if hs else MP_F32, out_max if hm else None,
+            _dtype_code(out_max.dtype) if hm else MP_F32, argout if hm else None, ws,
+            0 if ws is None else ws.numel(), stream)
+    return (out if hs else None, out_max if hm else None, argout if hm else None)
+
+
+def hetero_build(N_per_type, rels, dst_type, *, rowptr_dtype=torch.int32, stream=None):
+    """Combined destination-major CSR of one destination type.
+
+    rels: list of (src_type, dst_type, src int32 tensor, dst int32 tensor).
+    Returns (rowptr, col with global source ids)."""
+    it = _itype_code(rowptr_dtype)
+    dev = next(r[2].device for r in rels)
+    E_T = sum(int(r[2].numel()) for r in rels if r[1] == dst_type)
+    rowptr = torch.empty(N_per_type[dst_type] + 1, dtype=rowptr_dtype, device=dev)
+    col = torch.empty(E_T, dtype=torch.int32, device=dev)
+    nb = mp_hetero_build_workspace(N_per_type, rels, dst_type, it)
+    ws = _workspace(nb, dev)
+    mp_hetero_build(N_per_type, rels, dst_type, rowptr, it, col, ws, ws.numel(), stream)
+    return rowptr, col
+
+
+def hetero_spmm(N_per_type, x_per_type, dst_type, rowptr, col, *, plan: Plan | None = None,
+                out_dtype=torch.float32, out=None, stream=None):
+    """Sum over the combined CSR of dst_type, gathering from per-type tables."""
+    F = int(x_per_type[0].shape[1])
+    dev = x_per_type[0].device
+    if out is None:
+        out = torch.empty(N_per_type[dst_type], F, dtype=out_dtype, device=dev)
+    ws = plan.workspace(MP_SUM) if plan is not None else None
+    mp_hetero_spmm(N_per_type, x_per_type, _dtype_code(x_per_type[0].dtype), F, dst_type,
+                   plan.handle if plan is not None else None, rowptr, _itype_code(rowptr.dtype),
+                   col, MP_SUM, out, _dtype_code(out.dtype), ws, 0 if ws is None else ws.numel(),
+                   stream)
+    return out

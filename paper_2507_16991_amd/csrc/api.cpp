@@ -1,0 +1,548 @@
+// C ABI of libmp (declared in include/mp.h): argument validation, workspace
+// layout and launch sequencing.  Every compute step runs in the HIP kernels
+// of sort.hip, scan.hip and spmm.hip; this file only checks arguments, carves
+// caller-provided buffers and enqueues launches.
+#include <hip/hip_runtime.h>
+
+#include <climits>
+#include <cstdlib>
+#include <cstring>
+#include <new>
+
+#include "mp_internal.hpp"
+
+using namespace mp;
+
+namespace {
+
+inline hipStream_t as_stream(void* s) { return static_cast<hipStream_t>(s); }
+
+inline int hip_status(hipError_t e) { return e == hipSuccess ? MP_OK : MP_ERR_HIP; }
+
+// Sequential carve of a caller buffer into 256-byte aligned pieces.
+struct Carver {
+    char* base;
+    size_t off = 0;
+    explicit Carver(void* b) : base(static_cast<char*>(b)) {}
+    template <typename T>
+    T* take(size_t count) {
+        T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+        off = align_up(off + count * sizeof(T), 256);
+        return p;
+    }
+};
+
+int64_t env_int(const char* name, int64_t dflt) {
+    const char* v = std::getenv(name);
+    if (!v || !*v) return dflt;
+    char* end = nullptr;
+    long long x = std::strtoll(v, &end, 10);
+    return (end && *end == 0 && x > 0) ? (int64_t)x : dflt;
+}
+
+bool valid_itype(int t) { return t == MP_I32 || t == MP_I64; }
+bool valid_dtype(int t) { return t == MP_F32 || t == MP_BF16; }
+bool valid_reduce(int r) {
+    return r == MP_SUM || r == MP_MEAN || r == MP_MAX || r == (MP_SUM | MP_MAX) ||
+           r == (MP_MEAN | MP_MAX);
+}
+
+// ---- COO -> CSR workspace layout ---------------------------------------------
+
+struct CsrLayout {
+    int passes, digit;
+    uint32_t *kA, *kB;
+    int32_t *src_tmp, *eid_tmp, *eid_final;
+    uint32_t* counts;
+    void* scan_ws;
+    size_t bytes;
+};
+
+CsrLayout csr_layout(void* ws, int64_t E, int64_t N, int with_payload) {
+    CsrLayout L{};
+    digit_plan(key_bits(N), &L.passes, &L.digit);
+    Carver c(ws);
+    const size_t e = (size_t)(E > 0 ? E : 1);
+    L.kA = c.take<uint32_t>(e);
+    L.kB = L.passes > 1 ? c.take<uint32_t>(e) : nullptr;
+    L.src_tmp = L.passes > 1 ? c.take<int32_t>(e) : nullptr;
+    L.eid_tmp = (with_payload && L.passes > 1) ? c.take<int32_t>(e) : nullptr;
+    L.eid_final = with_payload ? c.take<int32_t>(e) : nullptr;
+    L.counts = reinterpret_cast<uint32_t*>(c.take<char>(radix_pass_counts_bytes(E, L.digit)));
+    const int64_t tiles = ceil_div(E > 0 ? E : 1, kSortTile);
+    L.scan_ws = c.take<char>(scan_workspace_bytes(tiles << L.digit));
+    L.bytes = c.off;
+    return L;
+}
+
+int check_csr_sizes(int64_t E, int64_t N) {
+    if (E < 0 || E > INT32_MAX || N < 1 || N > INT32_MAX) return MP_ERR_SIZE;
+    return MP_OK;
+}
+
+int coo_to_csr_impl(const int32_t* src, const int32_t* dst, int64_t E, int64_t N, void* rowptr,
+                    int itype, int32_t* col, int32_t* perm, const float* val_in, float* val_out,
+                    void* ws, size_t ws_bytes, hipStream_t s) {
+    const int rp64 = itype == MP_I64;
+    if (E == 0) return hip_status(launch_fill_rowptr_zero(N, rowptr, rp64, s));
+    const int payload = (perm != nullptr || val_out != nullptr) ? 1 : 0;
+    CsrLayout L = csr_layout(ws, E, N, payload);
+    if (ws_bytes < L.bytes) return MP_ERR_WORKSPACE;
+    int32_t* eid_final = perm ? perm : L.eid_final;
+
+    const uint32_t* keys_in = reinterpret_cast<const uint32_t*>(dst);
+    const int32_t* a_in = src;
+    const int32_t* b_in = nullptr;  // COO id = element index in the first pass
+    for (int p = 0; p < L.passes; ++p) {
+        const bool last_parity = ((L.passes - 1 - p) % 2) == 0;  // lands where the final pass writes
+        RadixPass rp{};
+        rp.keys_in = keys_in;
+        rp.a_in = a_in;
+        rp.b_in = b_in;
+        rp.keys_out = last_parity ? L.kA : L.kB;
+        rp.a_out = last_parity ? col : L.src_tmp;
+        rp.b_out = payload ? (last_parity ? eid_final : L.eid_tmp) : nullptr;
+        rp.n = E;
+        rp.shift = p * L.digit;
+        rp.bits = L.digit;
+        rp.counts = L.counts;
+        rp.scan_ws = L.scan_ws;
+        hipError_t e = radix_pass(rp, s);
+        if (e != hipSuccess) return MP_ERR_HIP;
+        keys_in = rp.keys_out;
+        a_in = rp.a_out;
+        b_in = rp.b_out;
+    }
+    hipError_t e = launch_rowptr_from_sorted(L.kA, E, N, rowptr, rp64, s);
+    if (e != hipSuccess) return MP_ERR_HIP;
+    if (val_in && val_out) {
+        e = launch_gather_f32(val_in, eid_final, E, val_out, s);
+        if (e != hipSuccess) return MP_ERR_HIP;
+    }
+    return MP_OK;
+}
+
+// ---- plan --------------------------------------------------------------------
+
+struct PlanLayout {
+    uint32_t* keys;
+    int32_t* rowlist;
+    uint32_t* chunk_off;
+    uint32_t* counts;
+    void* scan_ws;
+    uint32_t* header;
+    size_t bytes;
+};
+
+PlanLayout plan_layout(void* buf, int64_t N) {
+    PlanLayout L{};
+    Carver c(buf);
+    const size_t n = (size_t)(N > 0 ? N : 1);
+    L.keys = c.take<uint32_t>(n);
+    L.rowlist = c.take<int32_t>(n);
+    L.chunk_off = c.take<uint32_t>(n + 1);
+    L.counts = reinterpret_cast<uint32_t*>(c.take<char>(radix_pass_counts_bytes(N, kPlanClassBits)));
+    const int64_t tiles = ceil_div(N > 0 ? N : 1, kSortTile);
+    size_t sw = scan_workspace_bytes(tiles << kPlanClassBits);
+    size_t sw2 = scan_workspace_bytes(N + 1);
+    L.scan_ws = c.take<char>(sw > sw2 ? sw : sw2);
+    L.header = c.take<uint32_t>(64);
+    L.bytes = c.off;
+    return L;
+}
+
+}  // namespace
+
+struct mp_plan {
+    const void* rowptr;
+    int itype;
+    int64_t N_dst, E, F;
+    int x_dtype;
+    int64_t small_max, hub_min;
+    int chunk_min;
+    int64_t n_small, n_mid, n_hub, n_chunks;
+    int64_t mid_base, hub_base;
+    int32_t* rowlist;
+    uint32_t* chunk_off;
+};
+
+namespace {
+
+// Fill the work description of SpmmParams from a plan (or the plan-free
+// generic layout) and launch the main kernel plus the hub fix-up.
+int run_spmm(const mp_plan* plan, SpmmParams& P, const Geometry& g, int x_dtype, int64_t N_dst,
+             void* ws, size_t ws_bytes, hipStream_t s) {
+    P.L = g.L;
+    P.S = g.S;
+    P.FT = g.FT;
+    P.ltot = g.ltot;
+    const bool hs = (P.reduce & (MP_SUM | MP_MEAN)) != 0;
+    const bool hm = (P.reduce & MP_MAX) != 0;
+    if (plan) {
+        P.rowlist = plan->rowlist;
+        P.chunk_off = plan->chunk_off;
+        P.chunk_min = plan->chunk_min;
+        P.n_small = plan->n_small;
+        P.n_hub = plan->n_hub;
+        P.small_base = 0;
+        P.mid_base = plan->mid_base;
+        P.hub_base = plan->hub_base;
+        P.n_hub_waves = plan->n_chunks * g.FT;
+        P.n_mid_waves = plan->n_mid * g.FT;
+        P.n_small_waves = ceil_div(plan->n_small, g.S) * g.FT;
+        if (plan->n_chunks > 0) {
+            Carver c(ws);
+            const size_t cells = (size_t)plan->n_chunks * (size_t)P.F;
+            P.part_sum = hs ? c.take<float>(cells) : nullptr;
+            P.part_max = hm ? c.take<float>(cells) : nullptr;
+            P.part_arg = hm ? c.take<int32_t>(cells) : nullptr;
+            if (ws_bytes < c.off) return MP_ERR_WORKSPACE;
+        }
+    } else {
+        P.rowlist = nullptr;
+        P.n_mid_waves = N_dst * g.FT;
+    }
+    const int64_t waves = P.n_hub_waves + P.n_mid_waves + P.n_small_waves;
+    if (ceil_div(waves, 4) > (int64_t)UINT32_MAX) return MP_ERR_SIZE;
+    hipError_t e = launch_spmm(P, x_dtype, g.epl, s);
+    if (e != hipSuccess) return MP_ERR_HIP;
+    if (plan && plan->n_hub > 0) {
+        e = launch_spmm_fixup(P, s);
+        if (e != hipSuccess) return MP_ERR_HIP;
+    }
+    return MP_OK;
+}
+
+int check_plan(const mp_plan* plan, const void* rowptr, int itype, int64_t N_dst, int64_t F,
+               int x_dtype) {
+    if (!plan) return MP_OK;
+    if (plan->rowptr != rowptr || plan->itype != itype || plan->N_dst != N_dst || plan->F != F ||
+        plan->x_dtype != x_dtype)
+        return MP_ERR_PLAN;
+    return MP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mp_version(void) { return MP_VERSION; }
+
+const char* mp_status_str(int status) {
+    switch (status) {
+        case MP_OK: return "ok";
+        case MP_ERR_NULL: return "a required pointer is NULL";
+        case MP_ERR_SIZE: return "size out of range";
+        case MP_ERR_DTYPE: return "unsupported dtype or index type";
+        case MP_ERR_REDUCE: return "unsupported reduction";
+        case MP_ERR_WORKSPACE: return "workspace or plan buffer too small";
+        case MP_ERR_PLAN: return "plan does not match the arguments";
+        case MP_ERR_HIP: return "HIP launch or copy failed";
+        case MP_ERR_ALIGN: return "pointer not aligned to its element size";
+        default: return "unknown status";
+    }
+}
+
+int mp_coo_to_csr_workspace(int64_t E, int64_t N, int rowptr_itype, int with_payload,
+                            size_t* bytes) {
+    if (!bytes) return MP_ERR_NULL;
+    if (!valid_itype(rowptr_itype)) return MP_ERR_DTYPE;
+    int st = check_csr_sizes(E, N);
+    if (st != MP_OK) return st;
+    *bytes = E == 0 ? 0 : csr_layout(nullptr, E, N, with_payload ? 1 : 0).bytes;
+    return MP_OK;
+}
+
+int mp_coo_to_csr(const int32_t* src, const int32_t* dst, int64_t E, int64_t N, void* rowptr,
+                  int rowptr_itype, int32_t* col, int32_t* perm, const float* val_in,
+                  float* val_out, void* ws, size_t ws_bytes, void* stream) {
+    if (!valid_itype(rowptr_itype)) return MP_ERR_DTYPE;
+    int st = check_csr_sizes(E, N);
+    if (st != MP_OK) return st;
+    if (!rowptr) return MP_ERR_NULL;
+    if (E > 0 && (!src || !dst || !col || !ws)) return MP_ERR_NULL;
+    if ((val_in == nullptr) != (val_out == nullptr)) return MP_ERR_NULL;
+    if ((uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4)) return MP_ERR_ALIGN;
+    return coo_to_csr_impl(src, dst, E, N, rowptr, rowptr_itype, col, perm, val_in, val_out, ws,
+                           ws_bytes, as_stream(stream));
+}
+
+int mp_spmm_plan_size(int64_t N_dst, int64_t E, size_t* bytes) {
+    if (!bytes) return MP_ERR_NULL;
+    if (N_dst < 0 || N_dst > INT32_MAX || E < 0 || E > INT32_MAX) return MP_ERR_SIZE;
+    *bytes = plan_layout(nullptr, N_dst).bytes;
+    return MP_OK;
+}
+
+int mp_spmm_plan_build(const void* rowptr, int rowptr_itype, int64_t N_dst, int64_t E, int64_t F,
+                       int x_dtype, void* plan_buf, size_t plan_bytes, void* stream,
+                       mp_plan** out) {
+    if (!out || !rowptr || !plan_buf) return MP_ERR_NULL;
+    if (!valid_itype(rowptr_itype) || !valid_dtype(x_dtype)) return MP_ERR_DTYPE;
+    if (N_dst < 0 || N_dst > INT32_MAX || E < 0 || E > INT32_MAX || F < 1 || F > 65536)
+        return MP_ERR_SIZE;
+    PlanLayout L = plan_layout(plan_buf, N_dst);
+    if (plan_bytes < L.bytes) return MP_ERR_WORKSPACE;
+    hipStream_t s = as_stream(stream);
+    const int rp64 = rowptr_itype == MP_I64;
+
+    mp_plan* p = new (std::nothrow) mp_plan{};
+    if (!p) return MP_ERR_SIZE;
+    p->rowptr = rowptr;
+    p->itype = rowptr_itype;
+    p->N_dst = N_dst;
+    p->E = E;
+    p->F = F;
+    p->x_dtype = x_dtype;
+    p->small_max = env_int("MP_SMALL_MAX", 32);
+    if (p->small_max > 16383) p->small_max = 16383;
+    p->hub_min = env_int("MP_HUB_MIN", 4096);
+    if (p->hub_min < p->small_max) p->hub_min = p->small_max;
+    p->chunk_min = (int)env_int("MP_CHUNK", 1024);
+    p->rowlist = L.rowlist;
+    p->chunk_off = L.chunk_off;
+    if (N_dst == 0) {
+        *out = p;
+        return MP_OK;
+    }
+    hipError_t e = launch_plan_classes(rowptr, rp64, N_dst, p->small_max, p->hub_min, L.keys, s);
+    if (e == hipSuccess) {
+        RadixPass rp{};
+        rp.keys_in = L.keys;
+        rp.a_out = L.rowlist;  // payload = row id
+        rp.n = N_dst;
+        rp.shift = 0;
+        rp.bits = kPlanClassBits;
+        rp.counts = L.counts;
+        rp.scan_ws = L.scan_ws;
+        e = radix_pass(rp, s);
+    }
+    if (e == hipSuccess)
+        e = launch_plan_chunks(rowptr, rp64, L.rowlist, N_dst, p->hub_min, p->chunk_min,
+                               L.chunk_off, s);
+    if (e == hipSuccess) e = exclusive_scan_u32(L.chunk_off, N_dst + 1, L.scan_ws, s);
+    const int nclass = kClassHub + 1;
+    if (e == hipSuccess)
+        e = launch_plan_header(L.counts, ceil_div(N_dst, kSortTile), nclass, L.chunk_off, N_dst,
+                               L.header, s);
+    uint32_t h[64] = {0};
+    if (e == hipSuccess)
+        e = hipMemcpyAsync(h, L.header, sizeof(uint32_t) * (nclass + 2), hipMemcpyDeviceToHost, s);
+    if (e == hipSuccess) e = hipStreamSynchronize(s);
+    if (e != hipSuccess) {
+        delete p;
+        return MP_ERR_HIP;
+    }
+    p->mid_base = h[kClassMid];
+    p->hub_base = h[kClassHub];
+    p->n_small = p->mid_base;
+    p->n_mid = p->hub_base - p->mid_base;
+    p->n_hub = N_dst - p->hub_base;
+    p->n_chunks = h[nclass + 1];
+    *out = p;
+    return MP_OK;
+}
+
+void mp_spmm_plan_free(mp_plan* plan) { delete plan; }
+
+int mp_spmm_workspace(const mp_plan* plan, int reduce, size_t* bytes) {
+    if (!bytes) return MP_ERR_NULL;
+    if (!valid_reduce(reduce)) return MP_ERR_REDUCE;
+    if (!plan || plan->n_chunks == 0) {
+        *bytes = 0;
+        return MP_OK;
+    }
+    const size_t cells = (size_t)plan->n_chunks * (size_t)plan->F;
+    size_t b = 0;
+    if (reduce & (MP_SUM | MP_MEAN)) b += align_up(cells * 4, 256);
+    if (reduce & MP_MAX) b += 2 * align_up(cells * 4, 256);
+    *bytes = b;
+    return MP_OK;
+}
+
+int mp_spmm(const mp_plan* plan, const void* rowptr, int rowptr_itype, const int32_t* col,
+            const float* w, const void* x, int x_dtype, int64_t N_src, int64_t N_dst, int64_t F,
+            int reduce, void* out, int out_dtype, void* out_max, int max_dtype, int32_t* argout,
+            void* ws, size_t ws_bytes, void* stream) {
+    if (!valid_reduce(reduce)) return MP_ERR_REDUCE;
+    if (!valid_itype(rowptr_itype) || !valid_dtype(x_dtype)) return MP_ERR_DTYPE;
+    const bool hs = (reduce & (MP_SUM | MP_MEAN)) != 0;
+    const bool hm = (reduce & MP_MAX) != 0;
+    if (hs && !valid_dtype(out_dtype)) return MP_ERR_DTYPE;
+    if (hm && !valid_dtype(max_dtype)) return MP_ERR_DTYPE;
+    if (hm && max_dtype == MP_BF16 && (x_dtype != MP_BF16 || w != nullptr)) return MP_ERR_DTYPE;
+    if (N_src < 0 || N_src > INT32_MAX || N_dst < 0 || N_dst > INT32_MAX || F < 1 || F > 65536)
+        return MP_ERR_SIZE;
+    if (!rowptr) return MP_ERR_NULL;
+    if (N_dst > 0) {
+        if (!col || !x) return MP_ERR_NULL;
+        if (hs && !out) return MP_ERR_NULL;
+        if (hm && (!out_max || !argout)) return MP_ERR_NULL;
+    }
+    int st = check_plan(plan, rowptr, rowptr_itype, N_dst, F, x_dtype);
+    if (st != MP_OK) return st;
+    const int eb = x_dtype == MP_BF16 ? 2 : 4;
+    if ((uintptr_t)x % eb || (uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4) ||
+        (uintptr_t)col % 4 || (uintptr_t)w % 4 || (uintptr_t)argout % 4 ||
+        (hs && (uintptr_t)out % (out_dtype == MP_BF16 ? 2 : 4)) ||
+        (hm && (uintptr_t)out_max % (max_dtype == MP_BF16 ? 2 : 4)))
+        return MP_ERR_ALIGN;
+    if (N_dst == 0) return MP_OK;
+    const uintptr_t out_align = (hs && out_dtype == MP_F32) ? (uintptr_t)out : 16;
+    Geometry g = make_geometry(F, x_dtype, (uintptr_t)x, out_align);
+    SpmmParams P{};
+    P.rowptr = rowptr;
+    P.rp64 = rowptr_itype == MP_I64;
+    P.col = col;
+    P.w = w;
+    P.n_tables = 1;
+    P.table_ptr[0] = static_cast<const char*>(x);
+    P.table_off[0] = 0;
+    P.F = F;
+    P.reduce = reduce;
+    P.out = out;
+    P.out_bf16 = out_dtype == MP_BF16;
+    P.out_max = out_max;
+    P.max_bf16 = max_dtype == MP_BF16;
+    P.argout = argout;
+    return run_spmm(plan, P, g, x_dtype, N_dst, ws, ws_bytes, as_stream(stream));
+}
+
+// ---- heterogeneous ----------------------------------------------------------
+
+static int hetero_check(int n_types, const int64_t* N_per_type, int n_rel, const mp_relation* rels,
+                        int dst_type, int64_t* E_T, int64_t* offs) {
+    if (!N_per_type || (n_rel > 0 && !rels)) return MP_ERR_NULL;
+    if (n_types < 1 || n_types > MP_MAX_TYPES || n_rel < 0 || dst_type < 0 || dst_type >= n_types)
+        return MP_ERR_SIZE;
+    int64_t tot = 0;
+    for (int t = 0; t < n_types; ++t) {
+        if (N_per_type[t] < 0) return MP_ERR_SIZE;
+        offs[t] = tot;
+        tot += N_per_type[t];
+    }
+    offs[n_types] = tot;
+    if (tot > INT32_MAX) return MP_ERR_SIZE;
+    int64_t e = 0;
+    for (int r = 0; r < n_rel; ++r) {
+        const mp_relation& R = rels[r];
+        if (R.src_type < 0 || R.src_type >= n_types || R.dst_type < 0 || R.dst_type >= n_types ||
+            R.E < 0)
+            return MP_ERR_SIZE;
+        if (R.dst_type == dst_type) {
+            if (R.E > 0 && (!R.src || !R.dst)) return MP_ERR_NULL;
+            e += R.E;
+        }
+    }
+    if (e > INT32_MAX) return MP_ERR_SIZE;
+    if (N_per_type[dst_type] < 1) return MP_ERR_SIZE;
+    *E_T = e;
+    return MP_OK;
+}
+
+int mp_hetero_build_workspace(int n_types, const int64_t* N_per_type, int n_rel,
+                              const mp_relation* rels, int dst_type, int rowptr_itype,
+                              size_t* bytes) {
+    if (!bytes) return MP_ERR_NULL;
+    if (!valid_itype(rowptr_itype)) return MP_ERR_DTYPE;
+    int64_t E_T = 0, offs[MP_MAX_TYPES + 1];
+    int st = hetero_check(n_types, N_per_type, n_rel, rels, dst_type, &E_T, offs);
+    if (st != MP_OK) return st;
+    size_t cw = 0;
+    st = mp_coo_to_csr_workspace(E_T, N_per_type[dst_type], rowptr_itype, 0, &cw);
+    if (st != MP_OK) return st;
+    *bytes = 2 * align_up((size_t)(E_T > 0 ? E_T : 1) * 4, 256) + cw;
+    return MP_OK;
+}
+
+int mp_hetero_build(int n_types, const int64_t* N_per_type, int n_rel, const mp_relation* rels,
+                    int dst_type, void* rowptr, int rowptr_itype, int32_t* col, void* ws,
+                    size_t ws_bytes, void* stream) {
+    if (!valid_itype(rowptr_itype)) return MP_ERR_DTYPE;
+    int64_t E_T = 0, offs[MP_MAX_TYPES + 1];
+    int st = hetero_check(n_types, N_per_type, n_rel, rels, dst_type, &E_T, offs);
+    if (st != MP_OK) return st;
+    if (!rowptr || (E_T > 0 && (!col || !ws))) return MP_ERR_NULL;
+    size_t need = 0;
+    st = mp_hetero_build_workspace(n_types, N_per_type, n_rel, rels, dst_type, rowptr_itype, &need);
+    if (st != MP_OK) return st;
+    if (ws_bytes < need) return MP_ERR_WORKSPACE;
+    hipStream_t s = as_stream(stream);
+    Carver c(ws);
+    const size_t e = (size_t)(E_T > 0 ? E_T : 1);
+    int32_t* src_g = c.take<int32_t>(e);
+    int32_t* dst_c = c.take<int32_t>(e);
+    int64_t off = 0;
+    for (int r = 0; r < n_rel; ++r) {
+        const mp_relation& R = rels[r];
+        if (R.dst_type != dst_type || R.E == 0) continue;
+        hipError_t he = launch_offset_copy(R.src, R.E, (int32_t)offs[R.src_type], src_g + off, s);
+        if (he == hipSuccess) he = launch_offset_copy(R.dst, R.E, 0, dst_c + off, s);
+        if (he != hipSuccess) return MP_ERR_HIP;
+        off += R.E;
+    }
+    return coo_to_csr_impl(src_g, dst_c, E_T, N_per_type[dst_type], rowptr, rowptr_itype, col,
+                           nullptr, nullptr, nullptr, c.base + c.off, ws_bytes - c.off, s);
+}
+
+int mp_hetero_spmm(int n_types, const int64_t* N_per_type, const void* const* x_per_type,
+                   int x_dtype, int64_t F, int dst_type, const mp_plan* plan, const void* rowptr,
+                   int rowptr_itype, const int32_t* col, int reduce, void* out, int out_dtype,
+                   void* ws, size_t ws_bytes, void* stream) {
+    if (reduce != MP_SUM) return MP_ERR_REDUCE;
+    if (!valid_itype(rowptr_itype) || !valid_dtype(x_dtype) || !valid_dtype(out_dtype))
+        return MP_ERR_DTYPE;
+    int64_t E_T = 0, offs[MP_MAX_TYPES + 1];
+    int st = hetero_check(n_types, N_per_type, 0, nullptr, dst_type, &E_T, offs);
+    if (st != MP_OK) return st;
+    if (F < 1 || F > 65536) return MP_ERR_SIZE;
+    if (!x_per_type || !rowptr || !out || !col) return MP_ERR_NULL;
+    const int64_t N_dst = N_per_type[dst_type];
+    st = check_plan(plan, rowptr, rowptr_itype, N_dst, F, x_dtype);
+    if (st != MP_OK) return st;
+    const int eb = x_dtype == MP_BF16 ? 2 : 4;
+    uintptr_t xa = 0;
+    for (int t = 0; t < n_types; ++t) {
+        if (N_per_type[t] > 0 && !x_per_type[t]) return MP_ERR_NULL;
+        if ((uintptr_t)x_per_type[t] % eb) return MP_ERR_ALIGN;
+        xa |= (uintptr_t)x_per_type[t];
+    }
+    if ((uintptr_t)out % (out_dtype == MP_BF16 ? 2 : 4) || (uintptr_t)col % 4 ||
+        (uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4))
+        return MP_ERR_ALIGN;
+    Geometry g = make_geometry(F, x_dtype, xa, out_dtype == MP_F32 ? (uintptr_t)out : 16);
+    SpmmParams P{};
+    P.rowptr = rowptr;
+    P.rp64 = rowptr_itype == MP_I64;
+    P.col = col;
+    P.w = nullptr;
+    P.n_tables = n_types;
+    for (int t = 0; t < n_types; ++t) {
+        P.table_ptr[t] = static_cast<const char*>(x_per_type[t]);
+        P.table_off[t] = offs[t];
+    }
+    P.table_off[n_types] = offs[n_types];
+    P.F = F;
+    P.reduce = reduce;
+    P.out = out;
+    P.out_bf16 = out_dtype == MP_BF16;
+    return run_spmm(plan, P, g, x_dtype, N_dst, ws, ws_bytes, as_stream(stream));
+}
+
+int mp_validate_coo(const int32_t* src, const int32_t* dst, int64_t E, int64_t N_src,
+                    int64_t N_dst, int64_t* d_count, void* stream) {
+    if (!d_count || (E > 0 && (!src || !dst))) return MP_ERR_NULL;
+    if (E < 0 || N_src < 0 || N_dst < 0) return MP_ERR_SIZE;
+    return hip_status(launch_validate_coo(src, dst, E, N_src, N_dst, d_count, as_stream(stream)));
+}
+
+int mp_validate_csr(const void* rowptr, int rowptr_itype, const int32_t* col, int64_t N_dst,
+                    int64_t N_src, int64_t E, int64_t* d_count, void* stream) {
+    if (!d_count || !rowptr || (E > 0 && !col)) return MP_ERR_NULL;
+    if (!valid_itype(rowptr_itype)) return MP_ERR_DTYPE;
+    if (E < 0 || N_src < 0 || N_dst < 0) return MP_ERR_SIZE;
+    return hip_status(launch_validate_csr(rowptr, rowptr_itype == MP_I64, col, N_dst, N_src, E,
+                                          d_count, as_stream(stream)));
+}
+
+}  // extern "C"

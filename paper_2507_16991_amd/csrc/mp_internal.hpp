@@ -1,0 +1,147 @@
+// Internal declarations shared by the HIP translation units of libmp.
+// Nothing here is part of the public ABI (include/mp.h is).
+#pragma once
+
+#include <hip/hip_runtime.h>
+#include <stddef.h>
+#include <stdint.h>
+
+#include "mp.h"
+
+namespace mp {
+
+constexpr int kWave = 64;
+
+// ---- radix sort geometry (COO -> CSR) ---------------------------------------
+constexpr int kSortBlock = 256;                    // 4 wavefronts
+constexpr int kSortItems = 16;                     // keys per thread
+constexpr int kSortTile = kSortBlock * kSortItems; // 4096 keys per workgroup
+constexpr int kSortMaxBits = 8;                    // digit width cap (256 buckets)
+
+inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
+inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
+
+// Number of key bits for keys in [0, n): at least 1.
+inline int key_bits(int64_t n) {
+    int b = 1;
+    while (b < 62 && (int64_t(1) << b) < n) ++b;
+    return b;
+}
+
+// Split `bits` into passes of at most kSortMaxBits, as evenly as possible.
+inline void digit_plan(int bits, int* passes, int* digit) {
+    *passes = (bits + kSortMaxBits - 1) / kSortMaxBits;
+    *digit = (bits + *passes - 1) / *passes;
+}
+
+// ---- exclusive scan of uint32 (scan.hip) -----------------------------------
+constexpr int kScanBlock = 256;
+constexpr int kScanItems = 16;
+constexpr int kScanTile = kScanBlock * kScanItems;
+size_t scan_workspace_bytes(int64_t n);
+// In-place exclusive scan of data[0..n); returns the hipError of the launches.
+hipError_t exclusive_scan_u32(uint32_t* data, int64_t n, void* ws, hipStream_t s);
+
+// ---- one stable radix pass (sort.hip) --------------------------------------
+struct RadixPass {
+    const uint32_t* keys_in;  // [n]
+    const int32_t* a_in;      // [n] or nullptr: payload a = element index
+    const int32_t* b_in;      // [n] or nullptr: payload b = element index
+    uint32_t* keys_out;       // [n] or nullptr
+    int32_t* a_out;           // [n] or nullptr
+    int32_t* b_out;           // [n] or nullptr
+    int64_t n;
+    int shift, bits;
+    uint32_t* counts;         // [2^bits * tiles] scratch
+    void* scan_ws;
+};
+size_t radix_pass_counts_bytes(int64_t n, int bits);
+// Histogram + scan + stable scatter.  If digit_start != nullptr it receives
+// (device) nothing; callers read counts[d * tiles] after the pass for the
+// global start of digit d.
+hipError_t radix_pass(const RadixPass& p, hipStream_t s);
+
+hipError_t launch_rowptr_from_sorted(const uint32_t* keys, int64_t E, int64_t N, void* rowptr,
+                                     int rp64, hipStream_t s);
+hipError_t launch_fill_rowptr_zero(int64_t N, void* rowptr, int rp64, hipStream_t s);
+hipError_t launch_gather_f32(const float* in, const int32_t* idx, int64_t n, float* out,
+                             hipStream_t s);
+hipError_t launch_validate_coo(const int32_t* src, const int32_t* dst, int64_t E, int64_t N_src,
+                               int64_t N_dst, int64_t* d_count, hipStream_t s);
+hipError_t launch_validate_csr(const void* rowptr, int rp64, const int32_t* col, int64_t N_dst,
+                               int64_t N_src, int64_t E, int64_t* d_count, hipStream_t s);
+hipError_t launch_offset_copy(const int32_t* in, int64_t n, int32_t add, int32_t* out,
+                              hipStream_t s);
+
+// ---- aggregation (spmm.hip) --------------------------------------------------
+enum : int { kSum = MP_SUM, kMean = MP_MEAN, kMax = MP_MAX };
+
+// Feature-row geometry of one launch: a row of F elements is cut into Ltot
+// lane-chunks of EPL elements (one vector load each).  A wavefront holds S
+// slots of L lanes; when Ltot > 64 the row is split into FT feature tiles of
+// 64 lanes, each handled by its own wavefront.
+struct Geometry {
+    int elem_bytes;  // 4 (fp32) or 2 (bf16)
+    int epl;         // elements per lane-chunk: vector bytes / elem_bytes
+    int64_t ltot;    // lane-chunks per feature row
+    int L, S, FT;    // lanes per slot, slots per wave, feature tiles
+};
+// x_align / out_align: the pointer values (only their low bits matter); pass
+// 16 for out_align when no fp32 output is written.
+Geometry make_geometry(int64_t F, int x_dtype, uintptr_t x_align, uintptr_t out_align);
+
+// Degree classes of the plan (keys of the row sort).
+constexpr int kSmallClasses = 16;       // class c < 16: small row, deg < 2^c ... see plan
+constexpr int kClassMid = kSmallClasses;
+constexpr int kClassHub = kSmallClasses + 1;
+constexpr int kPlanClassBits = 5;       // 32 buckets (18 used)
+constexpr int kMaxChunksPerHub = 2048;  // hub rows are split into <= this many chunks
+
+struct PlanDevice {
+    uint32_t* keys;       // [N] class of each row
+    int32_t* rowlist;     // [N] rows sorted by class, stable by row id
+    uint32_t* chunk_off;  // [N+1] exclusive prefix of chunks per rowlist entry
+    uint32_t* counts;     // radix counts scratch
+    void* scan_ws;
+    uint32_t* header;     // [64] class starts, chunk total
+};
+
+struct SpmmParams {
+    const void* rowptr;
+    int rp64;
+    const int32_t* col;
+    const float* w;
+    int n_tables;
+    const char* table_ptr[MP_MAX_TYPES];
+    int64_t table_off[MP_MAX_TYPES + 1];
+    int64_t F;
+    int L, S, FT;
+    int64_t ltot;
+    // work list (waves, in launch order): hub chunks, mid rows, small groups
+    const int32_t* rowlist;  // nullptr: rows 0..N-1 all handled as "mid"
+    int64_t n_hub_waves, n_mid_waves, n_small_waves;
+    int64_t hub_base, mid_base, small_base, n_small, n_hub;
+    const uint32_t* chunk_off;  // indexed by rowlist position
+    int chunk_min;
+    int reduce;
+    void* out;
+    int out_bf16;
+    void* out_max;
+    int max_bf16;
+    int32_t* argout;
+    float* part_sum;
+    float* part_max;
+    int32_t* part_arg;
+};
+
+hipError_t launch_spmm(const SpmmParams& p, int x_dtype, int epl, hipStream_t s);
+hipError_t launch_spmm_fixup(const SpmmParams& p, hipStream_t s);
+hipError_t launch_plan_classes(const void* rowptr, int rp64, int64_t N, int64_t small_max,
+                               int64_t hub_min, uint32_t* keys, hipStream_t s);
+hipError_t launch_plan_chunks(const void* rowptr, int rp64, const int32_t* rowlist, int64_t N,
+                              int64_t hub_min, int chunk_min, uint32_t* nch, hipStream_t s);
+hipError_t launch_plan_header(const uint32_t* counts, int64_t tiles, int nclass,
+                              const uint32_t* chunk_off, int64_t N, uint32_t* header,
+                              hipStream_t s);
+
+}  // namespace mp

@@ -1,0 +1,585 @@
+// Segmented aggregation over the destination-major CSR (the AGGREGATION step
+// of Eq. (1) in PyG 2.0, with message w * x[src]), and its degree-binned plan.
+//
+// Work is split three ways by in-degree (Sec. 2.2: the sorted layout "enables
+// greater parallelism"), all inside ONE launch whose wavefronts take, in
+// order: hub-row edge chunks (longest first), mid rows (one wavefront per
+// row, its slots interleaving the row's edges), and groups of small rows (one
+// slot of L lanes per row).  A slot is a group of L lanes that together hold
+// one feature row: lane j loads elements [j*EPL, (j+1)*EPL) with one vector
+// load, so a feature-row gather is one coalesced access per slot.  The column
+// indices (and weights) of an iteration are loaded once, coalesced, by the
+// first lanes and broadcast with cross-lane permutes.
+//
+// Determinism: every output element is reduced in an order fixed by the
+// geometry (slot, unroll index, accumulator, then a fixed tree over
+// accumulators and slots; hub chunks are combined in chunk order by a second
+// kernel).  No floating-point atomics anywhere.
+//
+// Max: (value, CSR position) pairs; a later edge replaces the running pair
+// only when strictly greater, and pairs are combined preferring the larger
+// value, then the smaller position -- the first edge attaining the maximum.
+#include <type_traits>
+
+#include "mp_internal.hpp"
+
+namespace mp {
+namespace {
+
+constexpr int kBlock = 256;
+constexpr int kWavesPerBlock = kBlock / kWave;
+constexpr int kUnroll = 8;  // edges gathered per slot per iteration
+
+// ---- feature loads ----------------------------------------------------------
+
+template <typename TX, int EPL>
+struct RawVec;
+template <> struct RawVec<float, 4> { using T = float4; };
+template <> struct RawVec<float, 2> { using T = float2; };
+template <> struct RawVec<float, 1> { using T = float; };
+template <> struct RawVec<uint16_t, 8> { using T = uint4; };
+template <> struct RawVec<uint16_t, 4> { using T = uint2; };
+template <> struct RawVec<uint16_t, 2> { using T = uint32_t; };
+template <> struct RawVec<uint16_t, 1> { using T = uint16_t; };
+
+__device__ inline float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
+__device__ inline float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xFFFF0000u); }
+
+template <typename TX, int EPL>
+__device__ inline void widen(const typename RawVec<TX, EPL>::T& r, float (&v)[EPL]) {
+    if constexpr (std::is_same<TX, float>::value) {
+        if constexpr (EPL == 4) { v[0] = r.x; v[1] = r.y; v[2] = r.z; v[3] = r.w; }
+        else if constexpr (EPL == 2) { v[0] = r.x; v[1] = r.y; }
+        else { v[0] = r; }
+    } else {
+        if constexpr (EPL == 8) {
+            v[0] = bf16_lo(r.x); v[1] = bf16_hi(r.x); v[2] = bf16_lo(r.y); v[3] = bf16_hi(r.y);
+            v[4] = bf16_lo(r.z); v[5] = bf16_hi(r.z); v[6] = bf16_lo(r.w); v[7] = bf16_hi(r.w);
+        } else if constexpr (EPL == 4) {
+            v[0] = bf16_lo(r.x); v[1] = bf16_hi(r.x); v[2] = bf16_lo(r.y); v[3] = bf16_hi(r.y);
+        } else if constexpr (EPL == 2) {
+            v[0] = bf16_lo(r); v[1] = bf16_hi(r);
+        } else {
+            v[0] = bf16_lo((uint32_t)r);
+        }
+    }
+}
+
+// fp32 -> bf16 bits, round to nearest even (finite values).
+__device__ inline uint16_t to_bf16(float f) {
+    uint32_t u = __float_as_uint(f);
+    u += 0x7FFFu + ((u >> 16) & 1u);
+    return (uint16_t)(u >> 16);
+}
+
+__device__ inline int64_t load_rp(const void* rp, int rp64, int64_t i) {
+    return rp64 ? static_cast<const int64_t*>(rp)[i] : (int64_t) static_cast<const int32_t*>(rp)[i];
+}
+
+// Address of feature element `fe` of global source row c.  With several
+// tables (typed nodes), c is a global id and the table is the last one whose
+// offset is <= c; the select chain uses constant indices only, so the table
+// list stays in kernel-argument registers.
+template <typename TX>
+__device__ inline const char* feat_addr(const SpmmParams& P, int32_t c, int64_t fe) {
+    const char* base = P.table_ptr[0];
+    int64_t off = 0;
+    if (P.n_tables > 1) {
+#pragma unroll
+        for (int k = 1; k < MP_MAX_TYPES; ++k) {
+            if (k < P.n_tables && (int64_t)c >= P.table_off[k]) {
+                base = P.table_ptr[k];
+                off = P.table_off[k];
+            }
+        }
+    }
+    return base + (((int64_t)c - off) * P.F + fe) * (int64_t)sizeof(TX);
+}
+
+// Keep the pair with the larger value; on equal values the smaller position.
+__device__ inline void max_merge(float& va, int32_t& ia, float vb, int32_t ib) {
+    const bool take = (ib >= 0) && (ia < 0 || vb > va || (vb == va && ib < ia));
+    va = take ? vb : va;
+    ia = take ? ib : ia;
+}
+
+// ---- accumulator state -------------------------------------------------------
+
+template <int EPL, bool HS, bool HM>
+struct Acc {
+    static constexpr int A = HM ? 2 : 4;  // independent partial accumulators
+    float s[A][EPL];
+    float m[A][EPL];
+    int32_t i[A][EPL];
+
+    __device__ inline void init() {
+#pragma unroll
+        for (int a = 0; a < A; ++a)
+#pragma unroll
+            for (int k = 0; k < EPL; ++k) {
+                if constexpr (HS) s[a][k] = 0.f;
+                if constexpr (HM) { m[a][k] = 0.f; i[a][k] = -1; }
+            }
+    }
+    // message values v (already weighted) of CSR position pos
+    __device__ inline void add(int a, const float (&v)[EPL], int32_t pos) {
+#pragma unroll
+        for (int k = 0; k < EPL; ++k) {
+            if constexpr (HS) s[a][k] += v[k];
+            if constexpr (HM) {
+                const bool take = (i[a][k] < 0) || (v[k] > m[a][k]);
+                m[a][k] = take ? v[k] : m[a][k];
+                i[a][k] = take ? pos : i[a][k];
+            }
+        }
+    }
+    // fold the A partials into slot 0 (fixed tree)
+    __device__ inline void fold() {
+#pragma unroll
+        for (int step = 1; step < A; step <<= 1)
+#pragma unroll
+            for (int a = 0; a + step < A; a += 2 * step)
+#pragma unroll
+                for (int k = 0; k < EPL; ++k) {
+                    if constexpr (HS) s[a][k] += s[a + step][k];
+                    if constexpr (HM) max_merge(m[a][k], i[a][k], m[a + step][k], i[a + step][k]);
+                }
+    }
+    // fixed tree across the S slots of the wavefront (slot s at lanes s*L..);
+    // the result lands in slot 0
+    __device__ inline void reduce_slots(int S, int L, int slot, int lane) {
+        for (int off = 1; off < S; off <<= 1) {
+            const int src = lane + off * L;
+            const bool use = (slot % (2 * off) == 0) && (slot + off < S);
+#pragma unroll
+            for (int k = 0; k < EPL; ++k) {
+                if constexpr (HS) {
+                    const float o = __shfl(s[0][k], src);
+                    if (use) s[0][k] += o;
+                }
+                if constexpr (HM) {
+                    const float om = __shfl(m[0][k], src);
+                    const int32_t oi = __shfl(i[0][k], src);
+                    if (use) max_merge(m[0][k], i[0][k], om, oi);
+                }
+            }
+        }
+    }
+};
+
+template <int EPL>
+__device__ inline void store_row(const SpmmParams& P, int64_t row, int64_t fe, int64_t deg,
+                                 const float (&s)[EPL], const float (&m)[EPL],
+                                 const int32_t (&idx)[EPL], bool hs, bool hm) {
+    const int64_t o = row * P.F + fe;
+    if (hs) {
+        float v[EPL];
+        const bool mean = (P.reduce & kMean) != 0;
+        const float dv = (float)deg;
+#pragma unroll
+        for (int k = 0; k < EPL; ++k) v[k] = mean ? (deg > 0 ? s[k] / dv : 0.f) : s[k];
+        if (P.out_bf16) {
+            uint16_t* out = static_cast<uint16_t*>(P.out) + o;
+#pragma unroll
+            for (int k = 0; k < EPL; ++k) out[k] = to_bf16(v[k]);
+        } else {
+            float* out = static_cast<float*>(P.out) + o;
+            if constexpr (EPL == 4) {
+                *reinterpret_cast<float4*>(out) = make_float4(v[0], v[1], v[2], v[3]);
+            } else if constexpr (EPL == 8) {
+                reinterpret_cast<float4*>(out)[0] = make_float4(v[0], v[1], v[2], v[3]);
+                reinterpret_cast<float4*>(out)[1] = make_float4(v[4], v[5], v[6], v[7]);
+            } else {
+#pragma unroll
+                for (int k = 0; k < EPL; ++k) out[k] = v[k];
+            }
+        }
+    }
+    if (hm) {
+        if (P.max_bf16) {
+            uint16_t* out = static_cast<uint16_t*>(P.out_max) + o;
+            // exact: the max is one of the bf16 inputs (unweighted only)
+#pragma unroll
+            for (int k = 0; k < EPL; ++k) out[k] = (uint16_t)(__float_as_uint(idx[k] < 0 ? 0.f : m[k]) >> 16);
+        } else {
+            float* out = static_cast<float*>(P.out_max) + o;
+#pragma unroll
+            for (int k = 0; k < EPL; ++k) out[k] = idx[k] < 0 ? 0.f : m[k];
+        }
+        int32_t* ao = P.argout + o;
+#pragma unroll
+        for (int k = 0; k < EPL; ++k) ao[k] = idx[k];
+    }
+}
+
+// Gather-and-accumulate over edges [e0, e1) with all S slots of the wavefront
+// interleaved: in an iteration, slot s takes edges p + u*S + s for u < U.
+template <typename TX, int EPL, bool HS, bool HM>
+__device__ inline void wave_range(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int64_t e0,
+                                  int64_t e1, int lane, int slot, bool feat_ok, int64_t fe, int U) {
+    using R = typename RawVec<TX, EPL>::T;
+    const int S = P.S;
+    const int SU = S * U;
+    const bool weighted = P.w != nullptr;
+    for (int64_t p = e0; p < e1; p += SU) {
+        const int64_t pe = p + lane;
+        int32_t myc = 0;
+        float myw = 1.f;
+        if (lane < SU && pe < e1) {
+            myc = __builtin_nontemporal_load(P.col + pe);
+            if (weighted) myw = __builtin_nontemporal_load(P.w + pe);
+        }
+        R raw[kUnroll];
+        bool ok[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int t = u * S + slot;
+            const int32_t c = __shfl(myc, t);
+            ok[u] = feat_ok && (u < U) && (p + t < e1);
+            if (ok[u]) raw[u] = *reinterpret_cast<const R*>(feat_addr<TX>(P, c, fe));
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const int t = u * S + slot;
+            const float wt = weighted ? __shfl(myw, t) : 1.f;
+            if (ok[u]) {
+                float v[EPL];
+                widen<TX, EPL>(raw[u], v);
+                if (weighted) {
+#pragma unroll
+                    for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt, v[k]);
+                }
+                acc.add(u % Acc<EPL, HS, HM>::A, v, (int32_t)(p + t));
+            }
+        }
+    }
+}
+
+template <typename TX, int EPL, bool HS, bool HM>
+__global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave)) +
+                       (int64_t)blockIdx.x * kWavesPerBlock;
+    const int L = P.L, S = P.S;
+    const int slot = lane / L;
+    const int j = lane - slot * L;
+    const bool slot_ok = slot < S;
+
+    Acc<EPL, HS, HM> acc;
+    acc.init();
+
+    if (wv < P.n_hub_waves + P.n_mid_waves) {
+        // ---- one wavefront per mid row, or per hub-row edge chunk ----
+        const bool hub = wv < P.n_hub_waves;
+        const int64_t local = hub ? wv : wv - P.n_hub_waves;
+        const int64_t item = local / P.FT;
+        const int ft = (int)(local - item * P.FT);
+        const int64_t chunk_j = ft * (int64_t)kWave + j;  // lane-chunk index in the row
+        const bool feat_ok = slot_ok && chunk_j < P.ltot;
+        const int64_t fe = chunk_j * EPL;
+        int U = kUnroll;
+        if (S * U > kWave) U = kWave / S;
+
+        int64_t row, e0, e1, cidx = 0;
+        if (hub) {
+            // item = global chunk id; find its hub by binary search over the
+            // chunk offsets of the hub rows (rowlist positions hub_base..)
+            int64_t lo = 0, hi = P.n_hub - 1;
+            while (lo < hi) {
+                const int64_t mid = (lo + hi + 1) >> 1;
+                if ((int64_t)P.chunk_off[P.hub_base + mid] <= item) lo = mid; else hi = mid - 1;
+            }
+            row = P.rowlist[P.hub_base + lo];
+            const int64_t r0 = load_rp(P.rowptr, P.rp64, row);
+            const int64_t r1 = load_rp(P.rowptr, P.rp64, row + 1);
+            const int64_t deg = r1 - r0;
+            int64_t csz = (deg + kMaxChunksPerHub - 1) / kMaxChunksPerHub;
+            if (csz < P.chunk_min) csz = P.chunk_min;
+            const int64_t k = item - (int64_t)P.chunk_off[P.hub_base + lo];
+            e0 = r0 + k * csz;
+            e1 = e0 + csz < r1 ? e0 + csz : r1;
+            cidx = item;
+        } else {
+            row = P.rowlist ? (int64_t)P.rowlist[P.mid_base + item] : item;
+            e0 = load_rp(P.rowptr, P.rp64, row);
+            e1 = load_rp(P.rowptr, P.rp64, row + 1);
+        }
+        wave_range<TX, EPL, HS, HM>(P, acc, e0, e1, lane, slot, feat_ok, fe, U);
+        acc.fold();
+        acc.reduce_slots(S, L, slot, lane);
+        if (slot == 0 && feat_ok) {
+            if (hub) {
+                const int64_t o = cidx * P.F + fe;
+#pragma unroll
+                for (int k = 0; k < EPL; ++k) {
+                    if constexpr (HS) P.part_sum[o + k] = acc.s[0][k];
+                    if constexpr (HM) { P.part_max[o + k] = acc.m[0][k]; P.part_arg[o + k] = acc.i[0][k]; }
+                }
+            } else {
+                store_row<EPL>(P, row, fe, e1 - e0, acc.s[0], acc.m[0], acc.i[0], HS, HM);
+            }
+        }
+        return;
+    }
+
+    // ---- small rows: one slot per row ----
+    const int64_t local = wv - P.n_hub_waves - P.n_mid_waves;
+    if (local >= P.n_small_waves) return;
+    const int64_t group = local / P.FT;
+    const int ft = (int)(local - group * P.FT);
+    const int64_t chunk_j = ft * (int64_t)kWave + j;
+    const int64_t k_row = group * S + slot;
+    const bool row_ok = slot_ok && k_row < P.n_small;
+    const bool feat_ok = row_ok && chunk_j < P.ltot;
+    const int64_t fe = chunk_j * EPL;
+    int64_t row = 0, e0 = 0, e1 = 0;
+    if (row_ok) {
+        row = P.rowlist[P.small_base + k_row];
+        e0 = load_rp(P.rowptr, P.rp64, row);
+        e1 = load_rp(P.rowptr, P.rp64, row + 1);
+    }
+    const int32_t my_n = (int32_t)(e1 - e0);
+    int32_t max_n = my_n;
+#pragma unroll
+    for (int off = 1; off < kWave; off <<= 1) {
+        const int32_t o = __shfl_xor(max_n, off);
+        max_n = o > max_n ? o : max_n;
+    }
+    using R = typename RawVec<TX, EPL>::T;
+    const bool weighted = P.w != nullptr;
+    const bool coop = L >= kUnroll;  // enough lanes in a slot to load its columns
+    for (int32_t it = 0; it < max_n; it += kUnroll) {
+        int32_t myc = 0;
+        float myw = 1.f;
+        if (coop && j < kUnroll && it + j < my_n) {
+            myc = __builtin_nontemporal_load(P.col + e0 + it + j);
+            if (weighted) myw = __builtin_nontemporal_load(P.w + e0 + it + j);
+        }
+        R raw[kUnroll];
+        bool ok[kUnroll];
+        float wt[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            ok[u] = feat_ok && (it + u < my_n);
+            int32_t c;
+            if (coop) {
+                c = __shfl(myc, slot * L + u);
+                wt[u] = weighted ? __shfl(myw, slot * L + u) : 1.f;
+            } else {
+                c = ok[u] ? P.col[e0 + it + u] : 0;
+                wt[u] = (weighted && ok[u]) ? P.w[e0 + it + u] : 1.f;
+            }
+            if (ok[u]) raw[u] = *reinterpret_cast<const R*>(feat_addr<TX>(P, c, fe));
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            if (ok[u]) {
+                float v[EPL];
+                widen<TX, EPL>(raw[u], v);
+                if (weighted) {
+#pragma unroll
+                    for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt[u], v[k]);
+                }
+                acc.add(u % Acc<EPL, HS, HM>::A, v, (int32_t)(e0 + it + u));
+            }
+        }
+    }
+    acc.fold();
+    if (feat_ok) store_row<EPL>(P, row, fe, e1 - e0, acc.s[0], acc.m[0], acc.i[0], HS, HM);
+}
+
+// Combine the chunk partials of every hub row, in chunk order, and write the
+// row.  One wavefront per (hub row, 64-feature tile); lane = one feature.
+template <bool HS, bool HM>
+__global__ __launch_bounds__(kBlock) void spmm_fixup(SpmmParams P) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave)) +
+                       (int64_t)blockIdx.x * kWavesPerBlock;
+    const int64_t ftiles = (P.F + kWave - 1) / kWave;
+    const int64_t h = wv / ftiles;
+    if (h >= P.n_hub) return;
+    const int64_t f = (wv - h * ftiles) * kWave + lane;
+    if (f >= P.F) return;
+    const int64_t row = P.rowlist[P.hub_base + h];
+    const int64_t c0 = P.chunk_off[P.hub_base + h], c1 = P.chunk_off[P.hub_base + h + 1];
+    constexpr int A = 4;
+    float s[A] = {0.f, 0.f, 0.f, 0.f};
+    float m = 0.f;
+    int32_t mi = -1;
+    for (int64_t c = c0; c < c1; c += A) {
+        float ps[A], pm[A];
+        int32_t pi[A];
+#pragma unroll
+        for (int a = 0; a < A; ++a) {
+            const bool ok = c + a < c1;
+            const int64_t o = (c + a) * P.F + f;
+            if constexpr (HS) ps[a] = ok ? P.part_sum[o] : 0.f;
+            if constexpr (HM) { pm[a] = ok ? P.part_max[o] : 0.f; pi[a] = ok ? P.part_arg[o] : -1; }
+        }
+#pragma unroll
+        for (int a = 0; a < A; ++a) {
+            if constexpr (HS) s[a] += ps[a];
+            if constexpr (HM) max_merge(m, mi, pm[a], pi[a]);
+        }
+    }
+    const int64_t deg = load_rp(P.rowptr, P.rp64, row + 1) - load_rp(P.rowptr, P.rp64, row);
+    const int64_t o = row * P.F + f;
+    if constexpr (HS) {
+        float v = (s[0] + s[1]) + (s[2] + s[3]);
+        if (P.reduce & kMean) v = deg > 0 ? v / (float)deg : 0.f;
+        if (P.out_bf16) static_cast<uint16_t*>(P.out)[o] = to_bf16(v);
+        else static_cast<float*>(P.out)[o] = v;
+    }
+    if constexpr (HM) {
+        const float mv = mi < 0 ? 0.f : m;
+        if (P.max_bf16) static_cast<uint16_t*>(P.out_max)[o] = (uint16_t)(__float_as_uint(mv) >> 16);
+        else static_cast<float*>(P.out_max)[o] = mv;
+        P.argout[o] = mi;
+    }
+}
+
+// ---- plan kernels -------------------------------------------------------------
+
+// class of row i: small rows by bit length of the degree (0 for an empty
+// row), then mid, then hub.
+__global__ __launch_bounds__(256) void plan_classes(const void* rowptr, int rp64, int64_t N,
+                                                    int64_t small_max, int64_t hub_min,
+                                                    uint32_t* __restrict__ keys) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i >= N) return;
+    const int64_t d = load_rp(rowptr, rp64, i + 1) - load_rp(rowptr, rp64, i);
+    uint32_t c;
+    if (d > hub_min) c = kClassHub;
+    else if (d > small_max) c = kClassMid;
+    else c = d == 0 ? 0u : (uint32_t)(64 - __clzll((unsigned long long)d));
+    keys[i] = c;
+}
+
+// chunks per rowlist entry (0 unless the row is a hub)
+__global__ __launch_bounds__(256) void plan_chunks(const void* rowptr, int rp64,
+                                                   const int32_t* __restrict__ rowlist, int64_t N,
+                                                   int64_t hub_min, int chunk_min,
+                                                   uint32_t* __restrict__ nch) {
+    const int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (k > N) return;
+    if (k == N) { nch[k] = 0; return; }
+    const int64_t row = rowlist[k];
+    const int64_t d = load_rp(rowptr, rp64, row + 1) - load_rp(rowptr, rp64, row);
+    uint32_t c = 0;
+    if (d > hub_min) {
+        int64_t csz = (d + kMaxChunksPerHub - 1) / kMaxChunksPerHub;
+        if (csz < chunk_min) csz = chunk_min;
+        c = (uint32_t)((d + csz - 1) / csz);
+    }
+    nch[k] = c;
+}
+
+// header[c] = start of class c in rowlist (c < nclass), header[nclass] = N,
+// header[nclass + 1] = total hub chunks
+__global__ void plan_header(const uint32_t* __restrict__ counts, int64_t tiles, int nclass,
+                            const uint32_t* __restrict__ chunk_off, int64_t N,
+                            uint32_t* __restrict__ header) {
+    const int c = threadIdx.x;
+    if (c < nclass) header[c] = counts[(int64_t)c * tiles];
+    if (c == 0) {
+        header[nclass] = (uint32_t)N;
+        header[nclass + 1] = chunk_off[N];
+    }
+}
+
+template <typename TX, int EPL>
+hipError_t launch_typed(const SpmmParams& p, unsigned grid, hipStream_t s) {
+    const bool hs = (p.reduce & (kSum | kMean)) != 0;
+    const bool hm = (p.reduce & kMax) != 0;
+    if (hs && hm)
+        hipLaunchKernelGGL((spmm_main<TX, EPL, true, true>), dim3(grid), dim3(kBlock), 0, s, p);
+    else if (hm)
+        hipLaunchKernelGGL((spmm_main<TX, EPL, false, true>), dim3(grid), dim3(kBlock), 0, s, p);
+    else
+        hipLaunchKernelGGL((spmm_main<TX, EPL, true, false>), dim3(grid), dim3(kBlock), 0, s, p);
+    return hipGetLastError();
+}
+
+}  // namespace
+
+Geometry make_geometry(int64_t F, int x_dtype, uintptr_t x_align, uintptr_t out_align) {
+    Geometry g;
+    g.elem_bytes = x_dtype == MP_BF16 ? 2 : 4;
+    const int64_t row_bytes = F * g.elem_bytes;
+    int vec = 16;
+    // a lane-chunk of EPL >= 4 elements is stored with 16-byte fp32 stores,
+    // so it also needs a 16-byte aligned fp32 output
+    auto fits = [&](int v) {
+        const int epl = v / g.elem_bytes;
+        return row_bytes % v == 0 && x_align % v == 0 && (epl < 4 || out_align % 16 == 0);
+    };
+    while (vec > g.elem_bytes && !fits(vec)) vec >>= 1;
+    g.epl = vec / g.elem_bytes;
+    g.ltot = row_bytes / vec;
+    if (g.ltot <= kWave) {
+        g.L = (int)g.ltot;
+        g.S = kWave / g.L;
+        g.FT = 1;
+    } else {
+        g.L = kWave;
+        g.S = 1;
+        g.FT = (int)ceil_div(g.ltot, kWave);
+    }
+    return g;
+}
+
+hipError_t launch_spmm(const SpmmParams& p, int x_dtype, int epl, hipStream_t s) {
+    const int64_t waves = p.n_hub_waves + p.n_mid_waves + p.n_small_waves;
+    if (waves <= 0) return hipSuccess;
+    const unsigned grid = (unsigned)ceil_div(waves, kWavesPerBlock);
+    if (x_dtype == MP_F32) {
+        switch (epl) {
+            case 4: return launch_typed<float, 4>(p, grid, s);
+            case 2: return launch_typed<float, 2>(p, grid, s);
+            default: return launch_typed<float, 1>(p, grid, s);
+        }
+    }
+    switch (epl) {
+        case 8: return launch_typed<uint16_t, 8>(p, grid, s);
+        case 4: return launch_typed<uint16_t, 4>(p, grid, s);
+        case 2: return launch_typed<uint16_t, 2>(p, grid, s);
+        default: return launch_typed<uint16_t, 1>(p, grid, s);
+    }
+}
+
+hipError_t launch_spmm_fixup(const SpmmParams& p, hipStream_t s) {
+    if (p.n_hub <= 0) return hipSuccess;
+    const int64_t waves = p.n_hub * ceil_div(p.F, kWave);
+    const unsigned grid = (unsigned)ceil_div(waves, kWavesPerBlock);
+    const bool hs = (p.reduce & (kSum | kMean)) != 0;
+    const bool hm = (p.reduce & kMax) != 0;
+    if (hs && hm) hipLaunchKernelGGL((spmm_fixup<true, true>), dim3(grid), dim3(kBlock), 0, s, p);
+    else if (hm) hipLaunchKernelGGL((spmm_fixup<false, true>), dim3(grid), dim3(kBlock), 0, s, p);
+    else hipLaunchKernelGGL((spmm_fixup<true, false>), dim3(grid), dim3(kBlock), 0, s, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_plan_classes(const void* rowptr, int rp64, int64_t N, int64_t small_max,
+                               int64_t hub_min, uint32_t* keys, hipStream_t s) {
+    if (N <= 0) return hipSuccess;
+    hipLaunchKernelGGL(plan_classes, dim3((unsigned)ceil_div(N, 256)), dim3(256), 0, s, rowptr,
+                       rp64, N, small_max, hub_min, keys);
+    return hipGetLastError();
+}
+
+hipError_t launch_plan_chunks(const void* rowptr, int rp64, const int32_t* rowlist, int64_t N,
+                              int64_t hub_min, int chunk_min, uint32_t* nch, hipStream_t s) {
+    hipLaunchKernelGGL(plan_chunks, dim3((unsigned)ceil_div(N + 1, 256)), dim3(256), 0, s, rowptr,
+                       rp64, rowlist, N, hub_min, chunk_min, nch);
+    return hipGetLastError();
+}
+
+hipError_t launch_plan_header(const uint32_t* counts, int64_t tiles, int nclass,
+                              const uint32_t* chunk_off, int64_t N, uint32_t* header,
+                              hipStream_t s) {
+    hipLaunchKernelGGL(plan_header, dim3(1), dim3(64), 0, s, counts, tiles, nclass, chunk_off, N,
+                       header);
+    return hipGetLastError();
+}
+
+}  // namespace mp

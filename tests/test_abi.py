@@ -1,0 +1,136 @@
+"""CPU checks of the C ABI: the library loads, exports every function that
+include/mp.h declares, and rejects bad arguments on the host (before any
+device work) with the documented status codes."""
+import ctypes
+import os
+import re
+
+import pytest
+
+import paper_2507_16991_amd as mp
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+HEADER = os.path.join(ROOT, "include", "mp.h")
+
+FAKE = 0x10000  # a non-NULL, aligned pointer value; never dereferenced by these cases
+
+
+def declared_functions():
+    text = open(HEADER).read()
+    text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
+    return sorted(set(re.findall(r"\b(mp_[a-z0-9_]+)\s*\(", text)))
+
+
+def test_exports_every_declared_function():
+    L = mp.lib()
+    names = declared_functions()
+    assert "mp_spmm" in names and "mp_coo_to_csr" in names and "mp_hetero_spmm" in names
+    for n in names:
+        assert hasattr(L, n), f"{n} declared in mp.h but not exported"
+
+
+def test_version_and_status_strings():
+    assert mp.mp_version() == 1
+    for st in range(-8, 1):
+        assert mp.mp_status_str(st)
+    assert mp.mp_status_str(-99) == "unknown status"
+
+
+def test_coo_to_csr_workspace_sizes():
+    assert mp.mp_coo_to_csr_workspace(0, 5, mp.MP_I32, 0) == 0
+    a = mp.mp_coo_to_csr_workspace(1000, 5, mp.MP_I32, 0)
+    b = mp.mp_coo_to_csr_workspace(1000, 5, mp.MP_I32, 1)
+    assert 0 < a < b
+    # more key bits -> more passes -> ping-pong buffers
+    assert mp.mp_coo_to_csr_workspace(10**6, 2**20, mp.MP_I32, 0) > \
+        mp.mp_coo_to_csr_workspace(10**6, 200, mp.MP_I32, 0)
+
+
+@pytest.mark.parametrize("E,N", [(-1, 5), (5, 0), (2**31, 5), (5, 2**31)])
+def test_coo_to_csr_size_errors(E, N):
+    with pytest.raises(mp.MPError) as e:
+        mp.mp_coo_to_csr_workspace(E, N, mp.MP_I32, 0)
+    assert e.value.status == -2
+
+
+def test_coo_to_csr_argument_errors():
+    L = mp.lib()
+    # bad index type
+    assert L.mp_coo_to_csr(FAKE, FAKE, 10, 5, FAKE, 7, FAKE, None, None, None, FAKE, 1 << 20,
+                           None) == -3
+    # NULL rowptr / src
+    assert L.mp_coo_to_csr(FAKE, FAKE, 10, 5, None, 0, FAKE, None, None, None, FAKE, 1 << 20,
+                           None) == -1
+    assert L.mp_coo_to_csr(None, FAKE, 10, 5, FAKE, 0, FAKE, None, None, None, FAKE, 1 << 20,
+                           None) == -1
+    # val_in without val_out
+    assert L.mp_coo_to_csr(FAKE, FAKE, 10, 5, FAKE, 0, FAKE, None, FAKE, None, FAKE, 1 << 20,
+                           None) == -1
+    # misaligned int64 rowptr
+    assert L.mp_coo_to_csr(FAKE, FAKE, 10, 5, FAKE + 4, 1, FAKE, None, None, None, FAKE, 1 << 20,
+                           None) == -8
+    # workspace too small
+    assert L.mp_coo_to_csr(FAKE, FAKE, 10, 5, FAKE, 0, FAKE, None, None, None, FAKE, 16,
+                           None) == -5
+
+
+def test_plan_errors():
+    L = mp.lib()
+    h = ctypes.c_void_p(0)
+    assert mp.mp_spmm_plan_size(100, 1000) > 0
+    assert L.mp_spmm_plan_build(FAKE, 0, 100, 1000, 64, 0, FAKE, 16, None, ctypes.byref(h)) == -5
+    assert L.mp_spmm_plan_build(FAKE, 0, 100, 1000, 0, 0, FAKE, 1 << 30, None,
+                                ctypes.byref(h)) == -2
+    assert L.mp_spmm_plan_build(FAKE, 0, 100, 1000, 64, 9, FAKE, 1 << 30, None,
+                                ctypes.byref(h)) == -3
+    assert L.mp_spmm_plan_build(None, 0, 100, 1000, 64, 0, FAKE, 1 << 30, None,
+                                ctypes.byref(h)) == -1
+    assert mp.mp_spmm_workspace(None, mp.MP_SUM) == 0
+    with pytest.raises(mp.MPError):
+        mp.mp_spmm_workspace(None, 3)  # SUM|MEAN is not a valid combination
+
+
+def _spmm(**kw):
+    a = dict(plan=None, rowptr=FAKE, itype=0, col=FAKE, w=None, x=FAKE, x_dtype=0, N_src=10,
+             N_dst=10, F=8, reduce=1, out=FAKE, out_dtype=0, out_max=None, max_dtype=0,
+             argout=None, ws=None, ws_bytes=0, stream=None)
+    a.update(kw)
+    return mp.lib().mp_spmm(*a.values())
+
+
+def test_spmm_argument_errors():
+    assert _spmm(reduce=0) == -4
+    assert _spmm(reduce=1 | 2) == -4
+    assert _spmm(reduce=8) == -4
+    assert _spmm(x_dtype=5) == -3
+    assert _spmm(itype=3) == -3
+    assert _spmm(reduce=4, max_dtype=1, out_max=FAKE, argout=FAKE) == -3   # bf16 max of f32 x
+    assert _spmm(reduce=4, x_dtype=1, w=FAKE, max_dtype=1, out_max=FAKE, argout=FAKE) == -3
+    assert _spmm(F=0) == -2
+    assert _spmm(N_src=-1) == -2
+    assert _spmm(N_dst=2**31) == -2
+    assert _spmm(out=None) == -1
+    assert _spmm(reduce=4, out_max=FAKE, argout=None) == -1
+    assert _spmm(col=None) == -1
+    assert _spmm(x=FAKE + 2) == -8
+
+
+def test_hetero_errors():
+    L = mp.lib()
+    npt = (ctypes.c_int64 * 2)(10, 5)
+    b = ctypes.c_size_t(0)
+    rel = (mp.mp_relation * 1)(mp.mp_relation(0, 1, FAKE, FAKE, 20))
+    assert L.mp_hetero_build_workspace(2, npt, 1, rel, 1, 0, ctypes.byref(b)) == 0 and b.value > 0
+    assert L.mp_hetero_build_workspace(2, npt, 1, rel, 2, 0, ctypes.byref(b)) == -2
+    assert L.mp_hetero_build_workspace(0, npt, 1, rel, 0, 0, ctypes.byref(b)) == -2
+    bad = (mp.mp_relation * 1)(mp.mp_relation(0, 3, FAKE, FAKE, 20))
+    assert L.mp_hetero_build_workspace(2, npt, 1, bad, 1, 0, ctypes.byref(b)) == -2
+    xs = (ctypes.c_void_p * 2)(FAKE, FAKE)
+    assert L.mp_hetero_spmm(2, npt, xs, 0, 8, 1, None, FAKE, 0, FAKE, mp.MP_MEAN, FAKE, 0, None,
+                            0, None) == -4
+
+
+def test_validate_errors():
+    L = mp.lib()
+    assert L.mp_validate_coo(FAKE, FAKE, 10, 5, 5, None, None) == -1
+    assert L.mp_validate_csr(FAKE, 4, FAKE, 5, 5, 10, FAKE, None) == -3

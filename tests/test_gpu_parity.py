@@ -1,0 +1,367 @@
+"""Parity of the HIP path (through the C ABI) with the CPU oracle.
+
+Integer outputs (rowptr, col, perm, argmax) and max values must be bit-exact.
+Sums and means must satisfy max |y - y_ref| / sum_p |m_p| <= 1e-5 for fp32
+features and <= 1e-2 for bf16 features (fp32 accumulation in both cases; the
+second bound is the stated one for bf16 features, and bf16 outputs add one
+bf16 rounding).  Mean uses the same scale divided by the in-degree.
+"""
+import os
+import sys
+
+import numpy as np
+import pytest
+import torch
+
+import graphgen
+import oracle
+import paper_2507_16991_amd as mp
+from checks import check_csr_invariants, scaled_error
+
+pytestmark = pytest.mark.gpu
+DEV = torch.device("cuda:0")
+TOL = {torch.float32: 1e-5, torch.bfloat16: 1e-2}
+
+
+@pytest.fixture(autouse=True)
+def _announce(request):
+    sys.stderr.write(f"\n[gpu-case] {request.node.nodeid}\n")
+    sys.stderr.flush()
+    yield
+    torch.cuda.synchronize()
+
+
+def dev(a):
+    return torch.from_numpy(np.ascontiguousarray(a)).to(DEV)
+
+
+def x_of(g, dtype):
+    if dtype == torch.float32:
+        return dev(g.x)
+    return dev(g.x_bf16.view(np.int16)).view(torch.bfloat16)
+
+
+def x_f32_host(g, dtype):
+    return g.x if dtype == torch.float32 else graphgen.bf16_to_f32(g.x_bf16)
+
+
+# ---- COO -> CSR ------------------------------------------------------------------
+
+def check_csr(src, dst, n, rowptr_dtype=torch.int32, val=None):
+    s, d = dev(src), dev(dst)
+    v = None if val is None else dev(val)
+    rp, col, perm, vout = mp.coo_to_csr(s, d, n, rowptr_dtype=rowptr_dtype, want_perm=True, val=v)
+    rp_o, col_o, perm_o, v_o = oracle.coo_to_csr(src, dst, n, val=val)
+    assert np.array_equal(rp.cpu().numpy().astype(np.int64), rp_o), "rowptr"
+    assert np.array_equal(col.cpu().numpy(), col_o), "col"
+    assert np.array_equal(perm.cpu().numpy().astype(np.int64), perm_o), "perm"
+    if val is not None:
+        assert np.array_equal(vout.cpu().numpy().view(np.uint32), v_o.view(np.uint32)), "val"
+    return rp, col
+
+
+def test_csr_worked_example():
+    import json
+    g = json.load(open(os.path.join(os.path.dirname(__file__), "golden", "worked_example.json")))
+    rp, col = check_csr(np.array(g["src"], np.int32), np.array(g["dst"], np.int32), g["N"],
+                        val=np.array(g["w"], np.float32))
+    assert rp.cpu().tolist() == g["rowptr"] and col.cpu().tolist() == g["col"]
+
+
+@pytest.mark.parametrize("n,e", [(1, 0), (1, 7), (5, 0), (2, 4096), (255, 4095), (256, 4097),
+                                 (257, 10000), (1 << 16, 70_001), (70_000, 12_289),
+                                 ((1 << 20) + 3, 50_000), (3, 200_000)])
+@pytest.mark.parametrize("itype", [torch.int32, torch.int64])
+def test_csr_shapes(n, e, itype):
+    src = graphgen.uniform_ints(n + e, 1, e, n)
+    dst = graphgen.uniform_ints(n + e, 2, e, n)
+    val = graphgen.uniform_f32(n + e, 3, e)
+    check_csr(src, dst, n, itype, val)
+
+
+@pytest.mark.parametrize("name,scale", [("uniform-10k", 1.0), ("powerlaw-1.2M", 1.0),
+                                        ("chunglu-124M", 0.05)])
+def test_csr_workloads(name, scale):
+    g = graphgen.workload(name, seed=1, scale=scale, **({} if name != "chunglu-124M" else
+                                                         {"bf16": False}))
+    check_csr(g.src, g.dst, g.n_dst, val=g.w)
+
+
+def test_csr_sorted_and_single_row():
+    n = 1000
+    dst = np.sort(graphgen.uniform_ints(5, 2, 30_000, n))
+    src = graphgen.uniform_ints(5, 1, 30_000, n)
+    check_csr(src, dst, n)
+    check_csr(src, np.full(30_000, 999, np.int32), n)  # every edge into the last row
+
+
+# ---- aggregation ---------------------------------------------------------------------
+
+REDUCES = {"sum": mp.MP_SUM, "mean": mp.MP_MEAN, "max": mp.MP_MAX,
+           "sum+max": mp.MP_SUM | mp.MP_MAX, "mean+max": mp.MP_MEAN | mp.MP_MAX}
+
+
+def compare_spmm(rp_o, col_o, w_csr, x_host_f32, out, out_max, argout, reduce, dtype,
+                 rows=None):
+    """Compare device outputs (full arrays, or the listed rows) with the oracle."""
+    ref = oracle.spmm(rp_o, col_o, x=x_host_f32, w=w_csr, rows=rows)
+    sel = (lambda a: a) if rows is None else (lambda a: a[rows])
+    errs = {}
+    deg = np.diff(rp_o) if rows is None else (rp_o[rows + 1] - rp_o[rows])
+    if reduce & mp.MP_SUM:
+        y = sel(out.float().cpu().numpy())
+        errs["sum"] = scaled_error(y, ref["sum"], ref["scale"])
+    if reduce & mp.MP_MEAN:
+        y = sel(out.float().cpu().numpy())
+        errs["mean"] = scaled_error(y, ref["mean"], ref["scale"] / np.maximum(deg, 1)[:, None])
+    # a bf16 output adds one bf16 rounding (relative 2^-9 <= 2^-8 of the scale)
+    tol = TOL[dtype] + (2.0 ** -8 if out is not None and out.dtype == torch.bfloat16 else 0.0)
+    for k, e in errs.items():
+        assert e <= tol, f"{k} error {e}"
+    if reduce & mp.MP_MAX:
+        a = sel(argout.cpu().numpy()).astype(np.int64)
+        bad = np.argwhere(a != ref["argmax"])
+        assert bad.size == 0, f"argmax differs at {bad[:3].tolist()}: " \
+                              f"{a[tuple(bad[0])]} vs {ref['argmax'][tuple(bad[0])]}"
+        m = sel(out_max.float().cpu().numpy())
+        assert np.array_equal(m.view(np.uint32), ref["max"].view(np.uint32)), "max bits"
+    return errs
+
+
+@pytest.fixture(scope="module")
+def mixed():
+    g = graphgen.mixed_graph(0, f=64)
+    rp_o, col_o, perm_o, w_o = oracle.coo_to_csr(g.src, g.dst, g.n_dst, val=g.w)
+    return g, rp_o, col_o, w_o
+
+
+def run_case(g, rp_o, col_o, w_o, dtype, reduce, weighted, use_plan, out_dtype=torch.float32,
+             max_dtype=torch.float32, itype=torch.int32):
+    rp = dev(rp_o.astype(np.int32 if itype == torch.int32 else np.int64))
+    col = dev(col_o)
+    x = x_of(g, dtype)
+    w = dev(w_o) if weighted else None
+    plan = mp.Plan(rp, g.E, g.F, dtype) if use_plan else None
+    out, out_max, argout = mp.spmm(rp, col, x, reduce, w=w, plan=plan, out_dtype=out_dtype,
+                                   max_dtype=max_dtype)
+    torch.cuda.synchronize()
+    return compare_spmm(rp_o, col_o, w_o if weighted else None, x_f32_host(g, dtype), out,
+                        out_max, argout, reduce, dtype)
+
+
+@pytest.mark.parametrize("reduce", list(REDUCES))
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("weighted", [False, True])
+@pytest.mark.parametrize("use_plan", [False, True])
+def test_spmm_mixed(mixed, reduce, dtype, weighted, use_plan):
+    g, rp_o, col_o, w_o = mixed
+    run_case(g, rp_o, col_o, w_o, dtype, REDUCES[reduce], weighted, use_plan)
+
+
+@pytest.mark.parametrize("thresholds", [("8", "64", "16"), ("1", "2", "1"), ("64", "256", "64")])
+@pytest.mark.parametrize("reduce", ["sum", "mean+max"])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_spmm_plan_regimes(mixed, monkeypatch, thresholds, reduce, dtype):
+    """Push rows through every code path: small groups, mid rows, hub chunks
+    (with tiny chunks, so hubs have many chunks) and the chunk fix-up."""
+    g, rp_o, col_o, w_o = mixed
+    monkeypatch.setenv("MP_SMALL_MAX", thresholds[0])
+    monkeypatch.setenv("MP_HUB_MIN", thresholds[1])
+    monkeypatch.setenv("MP_CHUNK", thresholds[2])
+    run_case(g, rp_o, col_o, w_o, dtype, REDUCES[reduce], True, True)
+
+
+@pytest.mark.parametrize("F", [1, 2, 3, 5, 8, 24, 100, 128, 300, 520])
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_spmm_feature_widths(F, dtype, monkeypatch):
+    g = graphgen.mixed_graph(F, n=700, e=9000, f=F)
+    monkeypatch.setenv("MP_HUB_MIN", "128")
+    monkeypatch.setenv("MP_CHUNK", "32")
+    rp_o, col_o, _, w_o = oracle.coo_to_csr(g.src, g.dst, g.n_dst, val=g.w)
+    for reduce in (mp.MP_SUM, mp.MP_MEAN | mp.MP_MAX):
+        for use_plan in (False, True):
+            run_case(g, rp_o, col_o, w_o, dtype, reduce, True, use_plan)
+
+
+def test_spmm_signed_weights_and_ties(monkeypatch):
+    g = graphgen.mixed_graph(3, f=16, signed_weights=True)
+    g.x = (np.round(g.x * 2) / 2).astype(np.float32)  # coarse values: many ties
+    g.x_bf16 = graphgen.f32_to_bf16(g.x)
+    monkeypatch.setenv("MP_HUB_MIN", "256")
+    monkeypatch.setenv("MP_CHUNK", "64")
+    rp_o, col_o, _, w_o = oracle.coo_to_csr(g.src, g.dst, g.n_dst, val=g.w)
+    for dtype in (torch.float32, torch.bfloat16):
+        for weighted in (False, True):
+            run_case(g, rp_o, col_o, w_o, dtype, mp.MP_SUM | mp.MP_MAX, weighted, True)
+
+
+def test_spmm_output_dtypes(mixed):
+    g, rp_o, col_o, w_o = mixed
+    run_case(g, rp_o, col_o, w_o, torch.bfloat16, mp.MP_SUM | mp.MP_MAX, False, True,
+             out_dtype=torch.bfloat16, max_dtype=torch.bfloat16)
+    run_case(g, rp_o, col_o, w_o, torch.float32, mp.MP_MEAN, True, True, out_dtype=torch.bfloat16)
+    run_case(g, rp_o, col_o, w_o, torch.float32, mp.MP_MEAN | mp.MP_MAX, True, True,
+             itype=torch.int64)
+
+
+def test_spmm_empty_and_degenerate():
+    # no edges at all: every row empty
+    n = 300
+    x = torch.randn(n, 12, device=DEV)
+    rp = torch.zeros(n + 1, dtype=torch.int32, device=DEV)
+    col = torch.zeros(1, dtype=torch.int32, device=DEV)
+    for use_plan in (False, True):
+        plan = mp.Plan(rp, 0, 12) if use_plan else None
+        out, m, a = mp.spmm(rp, col, x, mp.MP_SUM | mp.MP_MAX, plan=plan)
+        assert torch.all(out == 0) and torch.all(a == -1)
+        assert torch.all(m.view(torch.int32) == 0)
+    # bipartite: N_dst != N_src, a single destination row
+    src = graphgen.uniform_ints(9, 1, 5000, 4000)
+    dst = np.zeros(5000, np.int32)
+    xs = graphgen.normal_f32(9, 3, 4000 * 4).reshape(4000, 4)
+    rp_o, col_o, _, _ = oracle.coo_to_csr(src, dst, 1, n_src=4000)
+    for use_plan in (False, True):
+        rpd = dev(rp_o.astype(np.int32))
+        plan = mp.Plan(rpd, 5000, 4) if use_plan else None
+        out, m, a = mp.spmm(rpd, dev(col_o), dev(xs), mp.MP_SUM | mp.MP_MAX, plan=plan)
+        torch.cuda.synchronize()
+        compare_spmm(rp_o, col_o, None, xs, out, m, a, mp.MP_SUM | mp.MP_MAX, torch.float32)
+
+
+def test_plan_mismatch_rejected(mixed):
+    g, rp_o, col_o, w_o = mixed
+    rp = dev(rp_o.astype(np.int32))
+    plan = mp.Plan(rp, g.E, g.F, torch.float32)
+    with pytest.raises(mp.MPError) as e:
+        mp.spmm(rp, dev(col_o), x_of(g, torch.bfloat16), mp.MP_SUM, plan=plan)
+    assert e.value.status == -6
+
+
+def test_determinism_across_runs_and_streams(mixed, monkeypatch):
+    g, rp_o, col_o, w_o = mixed
+    monkeypatch.setenv("MP_HUB_MIN", "256")
+    monkeypatch.setenv("MP_CHUNK", "64")
+    rp, col, x, w = dev(rp_o.astype(np.int32)), dev(col_o), x_of(g, torch.float32), dev(w_o)
+    plan = mp.Plan(rp, g.E, g.F)
+    outs = []
+    for k in range(3):
+        s = torch.cuda.Stream() if k == 2 else torch.cuda.current_stream()
+        with torch.cuda.stream(s):
+            outs.append(mp.spmm(rp, col, x, mp.MP_SUM | mp.MP_MAX, w=w, plan=plan))
+        torch.cuda.synchronize()
+    for o in outs[1:]:
+        assert torch.equal(o[0].view(torch.int32), outs[0][0].view(torch.int32))
+        assert torch.equal(o[2], outs[0][2])
+
+
+def test_validate_kernels():
+    src = graphgen.uniform_ints(2, 1, 1000, 50)
+    dst = graphgen.uniform_ints(2, 2, 1000, 50)
+    cnt = torch.zeros(1, dtype=torch.int64, device=DEV)
+    mp.mp_validate_coo(dev(src), dev(dst), 1000, 50, 50, cnt)
+    assert int(cnt.item()) == 0
+    bad = dst.copy()
+    bad[[3, 500]] = [50, -1]
+    mp.mp_validate_coo(dev(src), dev(bad), 1000, 50, 50, cnt)
+    assert int(cnt.item()) == 2
+    rp_o, col_o, _, _ = oracle.coo_to_csr(src, dst, 50)
+    rp = dev(rp_o.astype(np.int32))
+    mp.mp_validate_csr(rp, mp.MP_I32, dev(col_o), 50, 50, 1000, cnt)
+    assert int(cnt.item()) == 0
+    rp2 = rp.clone()
+    rp2[10] = rp2[11] + 1  # one decreasing step (10 -> 11)
+    mp.mp_validate_csr(rp2, mp.MP_I32, dev(col_o), 50, 50, 1000, cnt)
+    assert int(cnt.item()) == 1
+
+
+# ---- workloads -------------------------------------------------------------------------
+
+@pytest.mark.parametrize("name", ["uniform-10k", "powerlaw-1.2M"])
+def test_workload_small_full(name):
+    g = graphgen.workload(name, seed=0)
+    s, d = dev(g.src), dev(g.dst)
+    rp, col, perm, wc = mp.coo_to_csr(s, d, g.n_dst, want_perm=True,
+                                      val=None if g.w is None else dev(g.w))
+    rp_o, col_o, perm_o, w_o = oracle.coo_to_csr(g.src, g.dst, g.n_dst, val=g.w)
+    assert np.array_equal(col.cpu().numpy(), col_o)
+    plan = mp.Plan(rp, g.E, g.F)
+    x = dev(g.x)
+    cases = [(mp.MP_SUM, None)] if g.w is None else [(mp.MP_MEAN, None), (mp.MP_SUM, wc)]
+    for reduce, w in cases:
+        out, _, _ = mp.spmm(rp, col, x, reduce, w=w, plan=plan)
+        torch.cuda.synchronize()
+        errs = compare_spmm(rp_o, col_o, None if w is None else w_o, g.x, out, None, None, reduce,
+                            torch.float32)
+        print(name, reduce, errs)
+
+
+@pytest.fixture(scope="module")
+def chunglu_full():
+    g = graphgen.workload("chunglu-124M", seed=0)
+    rp_o, col_o, perm_o, _ = oracle.coo_to_csr(g.src, g.dst, g.n_dst)
+    return g, rp_o, col_o, perm_o
+
+
+def test_chunglu_124M_csr_bit_exact(chunglu_full):
+    g, rp_o, col_o, perm_o = chunglu_full
+    rp, col, perm, _ = mp.coo_to_csr(dev(g.src), dev(g.dst), g.n_dst, want_perm=True)
+    assert np.array_equal(rp.cpu().numpy().astype(np.int64), rp_o)
+    assert np.array_equal(col.cpu().numpy(), col_o)
+    assert np.array_equal(perm.cpu().numpy().astype(np.int64), perm_o)
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_chunglu_124M_spmm_sampled(chunglu_full, dtype):
+    """Full-size run in the benchmark's configuration; rows are independent,
+    so a sample of rows (every hub-sized row plus 20k random rows) is checked
+    exactly against the oracle."""
+    g, rp_o, col_o, _ = chunglu_full
+    rp = dev(rp_o.astype(np.int32))
+    col = dev(col_o)
+    x = x_of(g, dtype)
+    plan = mp.Plan(rp, g.E, g.F, dtype)
+    deg = np.diff(rp_o)
+    rng_rows = graphgen.uniform_ints(11, 5, 20_000, g.n_dst).astype(np.int64)
+    rows = np.unique(np.concatenate([np.nonzero(deg >= 2048)[0], rng_rows,
+                                     [0, g.n_dst - 1]])).astype(np.int64)
+    xh = x_f32_host(g, dtype)
+    for reduce in (mp.MP_SUM, mp.MP_MEAN, mp.MP_MAX):
+        out, out_max, argout = mp.spmm(rp, col, x, reduce, plan=plan)
+        torch.cuda.synchronize()
+        errs = compare_spmm(rp_o, col_o, None, xh, out, out_max, argout, reduce, dtype, rows=rows)
+        print("chunglu", dtype, reduce, errs)
+        del out, out_max, argout
+
+
+# ---- heterogeneous -------------------------------------------------------------------------
+
+def run_hetero(g, plan_on=True):
+    T = len(g.n_per_type)
+    rels = [(g.rel_src_type[r], g.rel_dst_type[r], dev(g.rel_src[r]), dev(g.rel_dst[r]))
+            for r in range(len(g.rel_src))]
+    xs = [dev(x.view(np.int16)).view(torch.bfloat16) for x in g.x_bf16]
+    outs_o, scs_o = oracle.hetero_sum(g.n_per_type, g.x_bf16, g.rel_src_type, g.rel_dst_type,
+                                      g.rel_src, g.rel_dst)
+    for t in range(T):
+        if t not in g.rel_dst_type:
+            continue
+        rp, col = mp.hetero_build(g.n_per_type, rels, t)
+        E_T = int(col.numel())
+        plan = mp.Plan(rp, E_T, g.F, torch.bfloat16) if plan_on else None
+        out = mp.hetero_spmm(g.n_per_type, xs, t, rp, col, plan=plan)
+        torch.cuda.synchronize()
+        err = scaled_error(out.cpu().numpy(), outs_o[t], scs_o[t])
+        assert err <= TOL[torch.bfloat16], f"type {t}: error {err}"
+        assert err <= 1e-5, f"type {t}: fp32 accumulation error {err}"
+
+
+def test_hetero_small():
+    g = graphgen.hetero_graph(4, [3000, 1200, 70],
+                              [(0, 0, 9000), (0, 1, 11000), (1, 0, 10000), (1, 2, 4000)], 128)
+    run_hetero(g, True)
+    run_hetero(g, False)
+
+
+def test_hetero_20M():
+    g = graphgen.workload("hetero-20M", seed=0)
+    run_hetero(g, True)
