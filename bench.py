@@ -1,0 +1,407 @@
+"""Benchmark of the message-passing aggregation path on one MI355X.
+
+Workload: a seeded Chung-Lu power-law graph with N = 2,449,029 nodes and
+E = 123,718,280 edges (mean in-degree 50.5, expected top degree 17,000),
+features N x 100 in fp32 and in bf16 (the bf16 copy is the RNE rounding of the
+fp32 draws).  It stands in for a products-scale public graph; no dataset is
+used.
+
+One step = the whole hot path over that graph, inputs already in HBM:
+  COO -> CSR (stable radix sort by destination + rowptr), the degree-binned
+  plan, then sum, mean and max+argmax aggregation for fp32 features and again
+  for bf16 features (fp32 accumulation; sums and means written fp32, bf16 max
+  written bf16, exact).
+
+value = sum over the step's operations of their algorithmic bytes (each edge
+gathers one full feature row; see algorithmic_bytes()) / step time, in GB/s.
+
+Other modes (used to produce the committed summaries under profiles/):
+  --summarize-stats DIR OUT        kernel-trace stats of a rocprofv3 run -> OUT
+  --summarize-counters F W OUT     FETCH_SIZE (F) and WRITE_SIZE (W) runs -> OUT
+"""
+from __future__ import annotations
+
+import argparse
+import csv
+import glob
+import hashlib
+import json
+import os
+import sys
+import time
+
+ROOT = os.path.dirname(os.path.abspath(__file__))
+if ROOT not in sys.path:
+    sys.path.insert(0, ROOT)
+
+METRIC = "SpMM effective HBM GB/s (% of peak) + edge·features/s, sum/mean/max"
+HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
+WORKLOAD = "chunglu-124M"
+DOMINANT = "spmm_main<float, 4, true, false>"  # fp32 sum: the step's largest launch
+DOMINANT_SRC = ["paper_2507_16991_amd/csrc/spmm.hip", "paper_2507_16991_amd/csrc/mp_internal.hpp"]
+COUNTER_SUMMARY = os.path.join(ROOT, "profiles", "spmm_main_f32_sum_chunglu124M_counters.txt")
+CALIB_BYTES = 1 << 30  # plain copy used to scale the HBM counters
+
+
+# ---- algorithmic bytes ------------------------------------------------------------
+
+def spmm_bytes(N, E, F, xb, reduce, out_b=4, max_b=4, rowptr_b=4, w=False):
+    """Each edge reads its column index and gathers one feature row; every
+    output row is written once."""
+    b = (N + 1) * rowptr_b + 4 * E + E * F * xb + (4 * E if w else 0)
+    if reduce & 3:
+        b += N * F * out_b
+    if reduce & 4:
+        b += N * F * (max_b + 4)
+    return b
+
+
+def csr_bytes(N, E, rowptr_b=4, perm=False):
+    """Read src and dst, write col (and perm) and rowptr."""
+    return 8 * E + 4 * E + (4 * E if perm else 0) + (N + 1) * rowptr_b
+
+
+def plan_bytes(N):
+    """Read rowptr, write the class-sorted row list and the chunk offsets."""
+    return 4 * (N + 1) + 4 * N + 4 * (N + 1)
+
+
+def source_digest(paths):
+    h = hashlib.sha1()
+    for p in paths:
+        with open(os.path.join(ROOT, p), "rb") as f:
+            h.update(f.read())
+    return h.hexdigest()
+
+
+def read_traffic():
+    """HBM bytes per launch of the dominant kernel from the committed counter
+    summary, or None when it is absent or was taken on different source."""
+    try:
+        kv = {}
+        for line in open(COUNTER_SUMMARY):
+            if ":" in line:
+                k, v = line.split(":", 1)
+                kv[k.strip()] = v.strip()
+        if kv.get("kernel_source_sha1") != source_digest(DOMINANT_SRC):
+            return None
+        return float(kv["hbm_bytes_per_launch"])
+    except (OSError, KeyError, ValueError):
+        return None
+
+
+# ---- benchmark ------------------------------------------------------------------------
+
+def run(args):
+    import numpy as np
+    import torch
+
+    import graphgen
+    import paper_2507_16991_amd as mp
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for {args.gpus}); the multi-GPU "
+              "path is a design, not a build", file=sys.stderr)
+        sys.exit(2)
+    mp.lib()  # fail loudly if the HIP library is missing
+    dev = torch.device("cuda:0")
+    t0 = time.time()
+    g = graphgen.workload(WORKLOAD, seed=args.seed)
+    N, E, F = g.n_dst, g.E, g.F
+    print(f"[bench] generated {WORKLOAD}: N={N} E={E} F={F} in {time.time() - t0:.1f}s",
+          file=sys.stderr, flush=True)
+    src = torch.from_numpy(g.src).to(dev)
+    dst = torch.from_numpy(g.dst).to(dev)
+    x32 = torch.from_numpy(g.x).to(dev)
+    x16 = torch.from_numpy(g.x_bf16.view(np.int16)).to(dev).view(torch.bfloat16)
+
+    # outputs and workspaces, allocated once
+    rowptr = torch.empty(N + 1, dtype=torch.int32, device=dev)
+    col = torch.empty(E, dtype=torch.int32, device=dev)
+    ws_csr = torch.empty(mp.mp_coo_to_csr_workspace(E, N, mp.MP_I32, 0), dtype=torch.uint8,
+                         device=dev)
+    plan_buf = torch.empty(mp.mp_spmm_plan_size(N, E), dtype=torch.uint8, device=dev)
+    out = torch.empty(N, F, dtype=torch.float32, device=dev)
+    mx32 = torch.empty(N, F, dtype=torch.float32, device=dev)
+    mx16 = torch.empty(N, F, dtype=torch.bfloat16, device=dev)
+    arg = torch.empty(N, F, dtype=torch.int32, device=dev)
+    stream = torch.cuda.current_stream()
+
+    ops = []  # (name, bytes, E*F)
+    for xn, xb, mb in (("f32", 4, 4), ("bf16", 2, 2)):
+        ops.append((f"sum_{xn}", spmm_bytes(N, E, F, xb, 1), E * F))
+        ops.append((f"mean_{xn}", spmm_bytes(N, E, F, xb, 2), E * F))
+        ops.append((f"max_{xn}", spmm_bytes(N, E, F, xb, 4, max_b=mb), E * F))
+    step_names = ["csr", "plan"] + [o[0] for o in ops]
+    step_bytes = csr_bytes(N, E) + plan_bytes(N) + sum(o[1] for o in ops)
+    step_ef = sum(o[2] for o in ops)
+
+    plans = {}
+    wss = {}
+
+    def step(evs=None):
+        def mark(i):
+            if evs is not None:
+                evs[i].record(stream)
+        mark(0)
+        mp.mp_coo_to_csr(src, dst, E, N, rowptr, mp.MP_I32, col, None, None, None, ws_csr,
+                         ws_csr.numel())
+        mark(1)
+        # the plan depends on F and dtype only through its check; one build
+        # per dtype keeps the ABI contract (plan matches x_dtype)
+        for k, xd in (("f32", mp.MP_F32), ("bf16", mp.MP_BF16)):
+            if k in plans:
+                mp.mp_spmm_plan_free(plans[k])
+            plans[k] = mp.mp_spmm_plan_build(rowptr, mp.MP_I32, N, E, F, xd, plan_buf if k ==
+                                             "f32" else plan_buf2, plan_buf.numel())
+        mark(2)
+        i = 2
+        for xn, x, xd, mxt, md in (("f32", x32, mp.MP_F32, mx32, mp.MP_F32),
+                                   ("bf16", x16, mp.MP_BF16, mx16, mp.MP_BF16)):
+            h = plans[xn]
+            for red in (mp.MP_SUM, mp.MP_MEAN, mp.MP_MAX):
+                nb = mp.mp_spmm_workspace(h, red)
+                key = (xn, red)
+                if key not in wss or wss[key].numel() < nb:
+                    wss[key] = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
+                hm = red == mp.MP_MAX
+                mp.mp_spmm(h, rowptr, mp.MP_I32, col, None, x, xd, N, N, F, red,
+                           None if hm else out, mp.MP_F32, mxt if hm else None, md,
+                           arg if hm else None, wss[key], wss[key].numel())
+                i += 1
+                mark(i)
+
+    plan_buf2 = torch.empty_like(plan_buf)
+    for _ in range(args.warmup):
+        step()
+    torch.cuda.synchronize()
+    if args.calibrate_copy:
+        a = torch.empty(CALIB_BYTES // 4, dtype=torch.float32, device=dev).fill_(1.0)
+        b = torch.empty_like(a)
+        torch.cuda.synchronize()
+        b.copy_(a)
+        torch.cuda.synchronize()
+        del a, b
+
+    nmark = len(step_names) + 1
+    all_evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nmark)]
+               for _ in range(args.steps)]
+    torch.cuda.synchronize()
+    t_start = time.perf_counter()
+    for k in range(args.steps):
+        step(all_evs[k])
+    torch.cuda.synchronize()
+    wall = time.perf_counter() - t_start
+    ms_step = wall * 1e3 / args.steps
+
+    per_op = {n: [] for n in step_names}
+    for evs in all_evs:
+        for i, n in enumerate(step_names):
+            per_op[n].append(evs[i].elapsed_time(evs[i + 1]))
+    op_ms = {n: float(np.mean(v)) for n, v in per_op.items()}
+    op_bytes = {"csr": csr_bytes(N, E), "plan": plan_bytes(N)}
+    op_bytes.update({o[0]: o[1] for o in ops})
+    breakdown = {n: {"ms": round(op_ms[n], 4),
+                     "GB_per_s": round(op_bytes[n] / (op_ms[n] * 1e-3) / 1e9, 1)}
+                 for n in step_names}
+
+    value = step_bytes / (ms_step * 1e-3) / 1e9
+    dom_ms = op_ms["sum_f32"]
+    dom_bytes = op_bytes["sum_f32"]
+    achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
+    traffic = read_traffic()
+    result = {
+        "metric": METRIC,
+        "value": round(value, 2),
+        "unit": "GB/s",
+        "n_gpus": 1,
+        "steps": args.steps,
+        "warmup": args.warmup,
+        "ms_per_step": round(ms_step, 3),
+        "higher_is_better": True,
+        "scaling": "weak",
+        "vs_baseline": None,
+        "dtype": "f32",
+        "data": "synthetic",
+        "config": {
+            "workload": f"{WORKLOAD}: Chung-Lu power-law graph, N={N}, E={E}, F={F}, "
+                        "features fp32 and bf16 (N(0,1)), seed " + str(args.seed),
+            "step": "COO->CSR + plan + {sum, mean, max+argmax} x {fp32, bf16 features}",
+            "accumulate": "fp32",
+            "rowptr": "int32",
+        },
+        "edge_features_per_s": round(step_ef / (ms_step * 1e-3), 1),
+        "percent_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
+        "ops": breakdown,
+        "roofline": {
+            "bound": "hbm",
+            "kernel": DOMINANT + " (+ hub fix-up), fp32 sum",
+            "achieved": round(achieved, 1),
+            "peak": HBM_PEAK_GBS,
+            "unit": "GB/s",
+            "frac": round(achieved / HBM_PEAK_GBS, 4),
+            "traffic": None if traffic is None else round(traffic / (dom_ms * 1e-3) / 1e9, 1),
+            "algorithmic_bytes_per_launch": dom_bytes,
+            "avg_launch_ms": round(dom_ms, 4),
+        },
+    }
+    if args.cpu_baseline:
+        result["cpu_baseline"] = cpu_baseline(g, N, E, F, step_bytes, args)
+    print(json.dumps(result), flush=True)
+
+
+def cpu_baseline(g, N, E, F, step_bytes, args):
+    """The CPU oracle on a bounded sample of the same step: its COO->CSR on the
+    whole graph, and its aggregation (sum, mean and max in one pass, fp32 and
+    bf16 features) on a contiguous block of rows; the aggregation time is
+    scaled by E / (edges in the block) to estimate a full step."""
+    import numpy as np
+
+    import oracle
+
+    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or (os.cpu_count() or 1)
+    t0 = time.perf_counter()
+    rp, col, _, _ = oracle.coo_to_csr(g.src, g.dst, N)
+    t_csr = time.perf_counter() - t0
+    rows_n = min(N, args.cpu_rows)
+    rows = np.arange(rows_n, dtype=np.int64)
+    e_s = int(rp[rows_n] - rp[0])
+    t0 = time.perf_counter()
+    oracle.spmm(rp, col, x=g.x, rows=rows, nthreads=threads)
+    oracle.spmm(rp, col, x_bf16=g.x_bf16, rows=rows, nthreads=threads)
+    t_agg = time.perf_counter() - t0
+    t_step = t_csr + t_agg * (E / max(e_s, 1))
+    return {
+        "value": round(step_bytes / t_step / 1e9, 3),
+        "unit": "GB/s",
+        "cores": threads,
+        "kind": "oracle",
+        "sample": f"oracle COO->CSR on all {E} edges (1 thread, {t_csr:.2f}s) + oracle "
+                  f"aggregation (sum/mean/max together, fp32 and bf16) on rows 0..{rows_n - 1} "
+                  f"({e_s} edges, {t_agg:.2f}s, {threads} threads), scaled by E/{e_s}; "
+                  f"estimated full step {t_step:.1f}s",
+    }
+
+
+# ---- rocprofv3 summaries -----------------------------------------------------------------
+
+def _find(dirname, pattern):
+    hits = glob.glob(os.path.join(dirname, "**", pattern), recursive=True)
+    if not hits:
+        raise SystemExit(f"no {pattern} under {dirname}")
+    return hits[0]
+
+
+def short_name(name):
+    """Kernel name without namespaces, return type and parameter list."""
+    name = name.replace("mp::(anonymous namespace)::", "").replace("void ", "")
+    depth = 0
+    for i, ch in enumerate(name):
+        if ch == "<":
+            depth += 1
+        elif ch == ">":
+            depth -= 1
+        elif ch == "(" and depth == 0:
+            return name[:i]
+    return name
+
+
+def summarize_stats(d, out, cmd):
+    path = _find(d, "*kernel_stats.csv")
+    rows = list(csv.DictReader(open(path)))
+    rows.sort(key=lambda r: -float(r["TotalDurationNs"]))
+    lines = [f"# rocprofv3 kernel stats ({os.path.basename(path)})", f"command: {cmd}", "",
+             f"{'kernel':<70} {'calls':>6} {'avg_us':>10} {'total_ms':>10} {'pct':>6}"]
+    for r in rows[:25]:
+        name = short_name(r["Name"])[:70]
+        lines.append(f"{name:<70} {r['Calls']:>6} {float(r['AverageNs']) / 1e3:>10.1f} "
+                     f"{float(r['TotalDurationNs']) / 1e6:>10.2f} {float(r['Percentage']):>6.2f}")
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def _counter_rows(d):
+    path = _find(d, "*counter_collection.csv")
+    return list(csv.DictReader(open(path)))
+
+
+def _per_dispatch(rows, counter):
+    """{(dispatch id, kernel name): value} summed over the counter's instances."""
+    acc = {}
+    for r in rows:
+        if r.get("Counter_Name") != counter:
+            continue
+        key = (r["Dispatch_Id"], r["Kernel_Name"])
+        acc[key] = acc.get(key, 0.0) + float(r["Counter_Value"])
+    return acc
+
+
+def summarize_counters(fetch_dir, write_dir, out, cmd):
+    fr = _per_dispatch(_counter_rows(fetch_dir), "FETCH_SIZE")
+    wr = _per_dispatch(_counter_rows(write_dir), "WRITE_SIZE")
+
+    def pick(table, needle):
+        vals = [v for (i, k), v in table.items() if needle in k]
+        return vals
+
+    # calibration: the plain copy of CALIB_BYTES (reads and writes that many)
+    copy_f = [v for (i, k), v in fr.items() if "copy" in k.lower() or "elementwise" in k.lower()]
+    copy_w = [v for (i, k), v in wr.items() if "copy" in k.lower() or "elementwise" in k.lower()]
+    cf = max(copy_f) if copy_f else None
+    cw = max(copy_w) if copy_w else None
+    scale_f = CALIB_BYTES / (cf * 1024.0) if cf else 1.0
+    scale_w = CALIB_BYTES / (cw * 1024.0) if cw else 1.0
+    dom_f = pick(fr, "spmm_main<float, 4, true, false>")
+    dom_w = pick(wr, "spmm_main<float, 4, true, false>")
+    if not dom_f or not dom_w:
+        raise SystemExit("dominant kernel not found in the counter runs")
+    f_b = sum(dom_f) / len(dom_f) * 1024.0 * scale_f
+    w_b = sum(dom_w) / len(dom_w) * 1024.0 * scale_w
+    lines = [
+        "# HBM traffic of the dominant kernel from rocprofv3 counters",
+        f"command_fetch: {cmd} (pass 1: --pmc FETCH_SIZE)",
+        f"command_write: {cmd} (pass 2: --pmc WRITE_SIZE)",
+        f"kernel: {DOMINANT}",
+        f"launches: {len(dom_f)}",
+        f"fetch_kib_per_launch_raw: {sum(dom_f) / len(dom_f):.1f}",
+        f"write_kib_per_launch_raw: {sum(dom_w) / len(dom_w):.1f}",
+        f"copy_calibration_bytes: {CALIB_BYTES}",
+        f"copy_fetch_kib_raw: {cf}",
+        f"copy_write_kib_raw: {cw}",
+        f"fetch_scale: {scale_f:.4f}",
+        f"write_scale: {scale_w:.4f}",
+        f"hbm_fetch_bytes_per_launch: {f_b:.0f}",
+        f"hbm_write_bytes_per_launch: {w_b:.0f}",
+        f"hbm_bytes_per_launch: {f_b + w_b:.0f}",
+        f"kernel_source_sha1: {source_digest(DOMINANT_SRC)}",
+    ]
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
+def main():
+    ap = argparse.ArgumentParser(description=__doc__, formatter_class=argparse.RawTextHelpFormatter)
+    ap.add_argument("--gpus", type=int, default=1)
+    ap.add_argument("--steps", type=int, default=10)
+    ap.add_argument("--warmup", type=int, default=2)
+    ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--cpu-rows", type=int, default=200_000,
+                    help="rows of the CPU-oracle aggregation sample")
+    ap.add_argument("--no-cpu-baseline", dest="cpu_baseline", action="store_false")
+    ap.add_argument("--calibrate-copy", action="store_true",
+                    help="run one plain 1 GiB copy after warm-up (counter scaling)")
+    ap.add_argument("--summarize-stats", nargs=2, metavar=("DIR", "OUT"))
+    ap.add_argument("--summarize-counters", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "OUT"))
+    ap.add_argument("--cmd", default="", help="command line recorded in a summary")
+    args = ap.parse_args()
+    if args.summarize_stats:
+        summarize_stats(*args.summarize_stats, args.cmd)
+        return
+    if args.summarize_counters:
+        summarize_counters(*args.summarize_counters, args.cmd)
+        return
+    run(args)
+
+
+if __name__ == "__main__":
+    main()
