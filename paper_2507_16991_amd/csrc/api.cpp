@@ -388,8 +388,7 @@ int mp_spmm(const mp_plan* plan, const void* rowptr, int rowptr_itype, const int
         (hm && (uintptr_t)out_max % (max_dtype == MP_BF16 ? 2 : 4)))
         return MP_ERR_ALIGN;
     if (N_dst == 0) return MP_OK;
-    const uintptr_t out_align = (hs && out_dtype == MP_F32) ? (uintptr_t)out : 16;
-    Geometry g = make_geometry(F, x_dtype, (uintptr_t)x, out_align);
+    Geometry g = make_geometry(F, x_dtype, (uintptr_t)x);
     SpmmParams P{};
     P.rowptr = rowptr;
     P.rp64 = rowptr_itype == MP_I64;
@@ -405,6 +404,7 @@ int mp_spmm(const mp_plan* plan, const void* rowptr, int rowptr_itype, const int
     P.out_max = out_max;
     P.max_bf16 = max_dtype == MP_BF16;
     P.argout = argout;
+    P.vec_store = (((uintptr_t)out | (uintptr_t)out_max | (uintptr_t)argout) % 16) == 0;
     return run_spmm(plan, P, g, x_dtype, N_dst, ws, ws_bytes, as_stream(stream));
 }
 
@@ -510,7 +510,7 @@ int mp_hetero_spmm(int n_types, const int64_t* N_per_type, const void* const* x_
     if ((uintptr_t)out % (out_dtype == MP_BF16 ? 2 : 4) || (uintptr_t)col % 4 ||
         (uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4))
         return MP_ERR_ALIGN;
-    Geometry g = make_geometry(F, x_dtype, xa, out_dtype == MP_F32 ? (uintptr_t)out : 16);
+    Geometry g = make_geometry(F, x_dtype, xa);
     SpmmParams P{};
     P.rowptr = rowptr;
     P.rp64 = rowptr_itype == MP_I64;
@@ -526,6 +526,7 @@ int mp_hetero_spmm(int n_types, const int64_t* N_per_type, const void* const* x_
     P.reduce = reduce;
     P.out = out;
     P.out_bf16 = out_dtype == MP_BF16;
+    P.vec_store = ((uintptr_t)out % 16) == 0;
     return run_spmm(plan, P, g, x_dtype, N_dst, ws, ws_bytes, as_stream(stream));
 }
 

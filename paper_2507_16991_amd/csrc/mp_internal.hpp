@@ -86,9 +86,8 @@ struct Geometry {
     int64_t ltot;    // lane-chunks per feature row
     int L, S, FT;    // lanes per slot, slots per wave, feature tiles
 };
-// x_align / out_align: the pointer values (only their low bits matter); pass
-// 16 for out_align when no fp32 output is written.
-Geometry make_geometry(int64_t F, int x_dtype, uintptr_t x_align, uintptr_t out_align);
+// x_align: the feature pointer value(s), OR-ed (only the low bits matter).
+Geometry make_geometry(int64_t F, int x_dtype, uintptr_t x_align);
 
 // Degree classes of the plan (keys of the row sort).
 constexpr int kSmallClasses = 16;       // class c < 16: small row, deg < 2^c ... see plan
@@ -129,6 +128,7 @@ struct SpmmParams {
     void* out_max;
     int max_bf16;
     int32_t* argout;
+    int vec_store;  // 1: out, out_max and argout are 16-byte aligned
     float* part_sum;
     float* part_max;
     int32_t* part_arg;

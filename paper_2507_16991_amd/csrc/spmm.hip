@@ -76,15 +76,17 @@ __device__ inline int64_t load_rp(const void* rp, int rp64, int64_t i) {
     return rp64 ? static_cast<const int64_t*>(rp)[i] : (int64_t) static_cast<const int32_t*>(rp)[i];
 }
 
-// Address of feature element `fe` of global source row c.  With several
-// tables (typed nodes), c is a global id and the table is the last one whose
+// Address of feature element `fe` of source row c.  With several tables
+// (typed nodes, MULTI), c is a global id and the table is the last one whose
 // offset is <= c; the select chain uses constant indices only, so the table
 // list stays in kernel-argument registers.
-template <typename TX>
+template <typename TX, bool MULTI>
 __device__ inline const char* feat_addr(const SpmmParams& P, int32_t c, int64_t fe) {
-    const char* base = P.table_ptr[0];
-    int64_t off = 0;
-    if (P.n_tables > 1) {
+    if constexpr (!MULTI) {
+        return P.table_ptr[0] + ((int64_t)c * P.F + fe) * (int64_t)sizeof(TX);
+    } else {
+        const char* base = P.table_ptr[0];
+        int64_t off = 0;
 #pragma unroll
         for (int k = 1; k < MP_MAX_TYPES; ++k) {
             if (k < P.n_tables && (int64_t)c >= P.table_off[k]) {
@@ -92,8 +94,8 @@ __device__ inline const char* feat_addr(const SpmmParams& P, int32_t c, int64_t 
                 off = P.table_off[k];
             }
         }
+        return base + (((int64_t)c - off) * P.F + fe) * (int64_t)sizeof(TX);
     }
-    return base + (((int64_t)c - off) * P.F + fe) * (int64_t)sizeof(TX);
 }
 
 // Keep the pair with the larger value; on equal values the smaller position.
@@ -167,11 +169,56 @@ struct Acc {
     }
 };
 
+typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
+typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
+
+// Store EPL consecutive 4-byte values; 16-byte stores when allowed.
+template <int EPL, typename T>
+__device__ inline void store4(T* out, const T (&v)[EPL], bool vec) {
+    static_assert(sizeof(T) == 4, "4-byte elements");
+    if constexpr (EPL == 4 || EPL == 8) {
+        if (vec) {
+#pragma unroll
+            for (int q = 0; q < EPL / 4; ++q) {
+                u32x4 u;
+                u.x = __builtin_bit_cast(uint32_t, v[4 * q + 0]);
+                u.y = __builtin_bit_cast(uint32_t, v[4 * q + 1]);
+                u.z = __builtin_bit_cast(uint32_t, v[4 * q + 2]);
+                u.w = __builtin_bit_cast(uint32_t, v[4 * q + 3]);
+                __builtin_nontemporal_store(u, reinterpret_cast<u32x4*>(out) + q);
+            }
+            return;
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < EPL; ++k) out[k] = v[k];
+}
+
+// Store EPL consecutive bf16 values (as bits); 8/16-byte stores when allowed.
+template <int EPL>
+__device__ inline void store2(uint16_t* out, const uint16_t (&b)[EPL], bool vec) {
+    if constexpr (EPL == 4 || EPL == 8) {
+        if (vec) {
+#pragma unroll
+            for (int q = 0; q < EPL / 4; ++q) {
+                u32x2 u;
+                u.x = (uint32_t)b[4 * q + 0] | ((uint32_t)b[4 * q + 1] << 16);
+                u.y = (uint32_t)b[4 * q + 2] | ((uint32_t)b[4 * q + 3] << 16);
+                __builtin_nontemporal_store(u, reinterpret_cast<u32x2*>(out) + q);
+            }
+            return;
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < EPL; ++k) out[k] = b[k];
+}
+
 template <int EPL>
 __device__ inline void store_row(const SpmmParams& P, int64_t row, int64_t fe, int64_t deg,
                                  const float (&s)[EPL], const float (&m)[EPL],
                                  const int32_t (&idx)[EPL], bool hs, bool hm) {
     const int64_t o = row * P.F + fe;
+    const bool vec = P.vec_store != 0;
     if (hs) {
         float v[EPL];
         const bool mean = (P.reduce & kMean) != 0;
@@ -179,83 +226,150 @@ __device__ inline void store_row(const SpmmParams& P, int64_t row, int64_t fe, i
 #pragma unroll
         for (int k = 0; k < EPL; ++k) v[k] = mean ? (deg > 0 ? s[k] / dv : 0.f) : s[k];
         if (P.out_bf16) {
-            uint16_t* out = static_cast<uint16_t*>(P.out) + o;
+            uint16_t b[EPL];
 #pragma unroll
-            for (int k = 0; k < EPL; ++k) out[k] = to_bf16(v[k]);
+            for (int k = 0; k < EPL; ++k) b[k] = to_bf16(v[k]);
+            store2<EPL>(static_cast<uint16_t*>(P.out) + o, b, vec);
         } else {
-            float* out = static_cast<float*>(P.out) + o;
-            if constexpr (EPL == 4) {
-                *reinterpret_cast<float4*>(out) = make_float4(v[0], v[1], v[2], v[3]);
-            } else if constexpr (EPL == 8) {
-                reinterpret_cast<float4*>(out)[0] = make_float4(v[0], v[1], v[2], v[3]);
-                reinterpret_cast<float4*>(out)[1] = make_float4(v[4], v[5], v[6], v[7]);
-            } else {
-#pragma unroll
-                for (int k = 0; k < EPL; ++k) out[k] = v[k];
-            }
+            store4<EPL>(static_cast<float*>(P.out) + o, v, vec);
         }
     }
     if (hm) {
+        float mv[EPL];
+#pragma unroll
+        for (int k = 0; k < EPL; ++k) mv[k] = idx[k] < 0 ? 0.f : m[k];
         if (P.max_bf16) {
-            uint16_t* out = static_cast<uint16_t*>(P.out_max) + o;
             // exact: the max is one of the bf16 inputs (unweighted only)
+            uint16_t b[EPL];
 #pragma unroll
-            for (int k = 0; k < EPL; ++k) out[k] = (uint16_t)(__float_as_uint(idx[k] < 0 ? 0.f : m[k]) >> 16);
+            for (int k = 0; k < EPL; ++k) b[k] = (uint16_t)(__float_as_uint(mv[k]) >> 16);
+            store2<EPL>(static_cast<uint16_t*>(P.out_max) + o, b, vec);
         } else {
-            float* out = static_cast<float*>(P.out_max) + o;
-#pragma unroll
-            for (int k = 0; k < EPL; ++k) out[k] = idx[k] < 0 ? 0.f : m[k];
+            store4<EPL>(static_cast<float*>(P.out_max) + o, mv, vec);
         }
-        int32_t* ao = P.argout + o;
-#pragma unroll
-        for (int k = 0; k < EPL; ++k) ao[k] = idx[k];
+        store4<EPL>(P.argout + o, idx, vec);
     }
 }
 
 // Gather-and-accumulate over edges [e0, e1) with all S slots of the wavefront
-// interleaved: in an iteration, slot s takes edges p + u*S + s for u < U.
-template <typename TX, int EPL, bool HS, bool HM>
+// interleaved.  The column indices (and weights) of up to 64 edges are loaded
+// once, coalesced, one per lane; each inner step then covers SU = S*U edges:
+// slot s takes edges base + u*S + s (u < U), gets their columns by cross-lane
+// permute, issues all U feature-row loads, and only then accumulates.
+template <typename TX, int EPL, bool HS, bool HM, bool MULTI, bool W>
 __device__ inline void wave_range(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int64_t e0,
                                   int64_t e1, int lane, int slot, bool feat_ok, int64_t fe, int U) {
     using R = typename RawVec<TX, EPL>::T;
+    constexpr int A = Acc<EPL, HS, HM>::A;
     const int S = P.S;
     const int SU = S * U;
-    const bool weighted = P.w != nullptr;
-    for (int64_t p = e0; p < e1; p += SU) {
-        const int64_t pe = p + lane;
+    const int steps = kWave / SU;
+    const int tile = steps * SU;
+    for (int64_t p0 = e0; p0 < e1; p0 += tile) {
+        const int64_t rem = e1 - p0;
         int32_t myc = 0;
         float myw = 1.f;
-        if (lane < SU && pe < e1) {
-            myc = __builtin_nontemporal_load(P.col + pe);
-            if (weighted) myw = __builtin_nontemporal_load(P.w + pe);
+        if (lane < tile && lane < rem) {
+            myc = __builtin_nontemporal_load(P.col + p0 + lane);
+            if constexpr (W) myw = __builtin_nontemporal_load(P.w + p0 + lane);
         }
-        R raw[kUnroll];
-        bool ok[kUnroll];
+        for (int st = 0; st < steps; ++st) {
+            const int base = st * SU;
+            if (base >= rem) break;
+            const char* addr[kUnroll];
+            bool ok[kUnroll];
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            const int t = u * S + slot;
-            const int32_t c = __shfl(myc, t);
-            ok[u] = feat_ok && (u < U) && (p + t < e1);
-            if (ok[u]) raw[u] = *reinterpret_cast<const R*>(feat_addr<TX>(P, c, fe));
-        }
+            for (int u = 0; u < kUnroll; ++u) {
+                const int t = base + u * S + slot;
+                const int32_t c = __shfl(myc, t);
+                ok[u] = feat_ok && (u < U) && (t < rem);
+                addr[u] = feat_addr<TX, MULTI>(P, c, fe);
+            }
+            R raw[kUnroll];
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            const int t = u * S + slot;
-            const float wt = weighted ? __shfl(myw, t) : 1.f;
-            if (ok[u]) {
-                float v[EPL];
-                widen<TX, EPL>(raw[u], v);
-                if (weighted) {
+            for (int u = 0; u < kUnroll; ++u)
+                if (ok[u]) raw[u] = *reinterpret_cast<const R*>(addr[u]);
 #pragma unroll
-                    for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt, v[k]);
+            for (int u = 0; u < kUnroll; ++u) {
+                const int t = base + u * S + slot;
+                float wt = 1.f;
+                if constexpr (W) wt = __shfl(myw, t);
+                if (ok[u]) {
+                    float v[EPL];
+                    widen<TX, EPL>(raw[u], v);
+                    if constexpr (W) {
+#pragma unroll
+                        for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt, v[k]);
+                    }
+                    acc.add(u % A, v, (int32_t)(p0 + t));
                 }
-                acc.add(u % Acc<EPL, HS, HM>::A, v, (int32_t)(p + t));
             }
         }
     }
 }
 
-template <typename TX, int EPL, bool HS, bool HM>
+// One slot per row: every slot walks its own row's edges, U at a time.
+// COOP: the slot has at least U lanes, which load its next U columns
+// together; otherwise each lane loads the columns itself.
+template <typename TX, int EPL, bool HS, bool HM, bool MULTI, bool W, bool COOP>
+__device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int64_t e0,
+                                int32_t my_n, int32_t max_n, int slot, int j, bool feat_ok,
+                                int64_t fe) {
+    using R = typename RawVec<TX, EPL>::T;
+    constexpr int A = Acc<EPL, HS, HM>::A;
+    const int L = P.L;
+    for (int32_t it = 0; it < max_n; it += kUnroll) {
+        const char* addr[kUnroll];
+        bool ok[kUnroll];
+        float wt[kUnroll];
+        if constexpr (COOP) {
+            int32_t myc = 0;
+            float myw = 1.f;
+            if (j < kUnroll && it + j < my_n) {
+                myc = __builtin_nontemporal_load(P.col + e0 + it + j);
+                if constexpr (W) myw = __builtin_nontemporal_load(P.w + e0 + it + j);
+            }
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                const int srcl = slot * L + u;
+                const int32_t c = __shfl(myc, srcl);
+                wt[u] = 1.f;
+                if constexpr (W) wt[u] = __shfl(myw, srcl);
+                ok[u] = feat_ok && (it + u < my_n);
+                addr[u] = feat_addr<TX, MULTI>(P, c, fe);
+            }
+        } else {
+            int32_t cc[kUnroll];
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                ok[u] = feat_ok && (it + u < my_n);
+                cc[u] = ok[u] ? P.col[e0 + it + u] : 0;
+                wt[u] = 1.f;
+                if constexpr (W) wt[u] = ok[u] ? P.w[e0 + it + u] : 1.f;
+            }
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) addr[u] = feat_addr<TX, MULTI>(P, cc[u], fe);
+        }
+        R raw[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u)
+            if (ok[u]) raw[u] = *reinterpret_cast<const R*>(addr[u]);
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            if (ok[u]) {
+                float v[EPL];
+                widen<TX, EPL>(raw[u], v);
+                if constexpr (W) {
+#pragma unroll
+                    for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt[u], v[k]);
+                }
+                acc.add(u % A, v, (int32_t)(e0 + it + u));
+            }
+        }
+    }
+}
+
+template <typename TX, int EPL, bool HS, bool HM, bool MULTI, bool W>
 __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave)) +
@@ -304,7 +418,7 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
             e0 = load_rp(P.rowptr, P.rp64, row);
             e1 = load_rp(P.rowptr, P.rp64, row + 1);
         }
-        wave_range<TX, EPL, HS, HM>(P, acc, e0, e1, lane, slot, feat_ok, fe, U);
+        wave_range<TX, EPL, HS, HM, MULTI, W>(P, acc, e0, e1, lane, slot, feat_ok, fe, U);
         acc.fold();
         acc.reduce_slots(S, L, slot, lane);
         if (slot == 0 && feat_ok) {
@@ -345,45 +459,10 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
         const int32_t o = __shfl_xor(max_n, off);
         max_n = o > max_n ? o : max_n;
     }
-    using R = typename RawVec<TX, EPL>::T;
-    const bool weighted = P.w != nullptr;
-    const bool coop = L >= kUnroll;  // enough lanes in a slot to load its columns
-    for (int32_t it = 0; it < max_n; it += kUnroll) {
-        int32_t myc = 0;
-        float myw = 1.f;
-        if (coop && j < kUnroll && it + j < my_n) {
-            myc = __builtin_nontemporal_load(P.col + e0 + it + j);
-            if (weighted) myw = __builtin_nontemporal_load(P.w + e0 + it + j);
-        }
-        R raw[kUnroll];
-        bool ok[kUnroll];
-        float wt[kUnroll];
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            ok[u] = feat_ok && (it + u < my_n);
-            int32_t c;
-            if (coop) {
-                c = __shfl(myc, slot * L + u);
-                wt[u] = weighted ? __shfl(myw, slot * L + u) : 1.f;
-            } else {
-                c = ok[u] ? P.col[e0 + it + u] : 0;
-                wt[u] = (weighted && ok[u]) ? P.w[e0 + it + u] : 1.f;
-            }
-            if (ok[u]) raw[u] = *reinterpret_cast<const R*>(feat_addr<TX>(P, c, fe));
-        }
-#pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
-            if (ok[u]) {
-                float v[EPL];
-                widen<TX, EPL>(raw[u], v);
-                if (weighted) {
-#pragma unroll
-                    for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt[u], v[k]);
-                }
-                acc.add(u % Acc<EPL, HS, HM>::A, v, (int32_t)(e0 + it + u));
-            }
-        }
-    }
+    if (L >= kUnroll)
+        slot_row<TX, EPL, HS, HM, MULTI, W, true>(P, acc, e0, my_n, max_n, slot, j, feat_ok, fe);
+    else
+        slot_row<TX, EPL, HS, HM, MULTI, W, false>(P, acc, e0, my_n, max_n, slot, j, feat_ok, fe);
     acc.fold();
     if (feat_ok) store_row<EPL>(P, row, fe, e1 - e0, acc.s[0], acc.m[0], acc.i[0], HS, HM);
 }
@@ -487,33 +566,37 @@ __global__ void plan_header(const uint32_t* __restrict__ counts, int64_t tiles, 
     }
 }
 
-template <typename TX, int EPL>
-hipError_t launch_typed(const SpmmParams& p, unsigned grid, hipStream_t s) {
+template <typename TX, int EPL, bool W>
+hipError_t launch_w(const SpmmParams& p, unsigned grid, hipStream_t s) {
     const bool hs = (p.reduce & (kSum | kMean)) != 0;
     const bool hm = (p.reduce & kMax) != 0;
     if (hs && hm)
-        hipLaunchKernelGGL((spmm_main<TX, EPL, true, true>), dim3(grid), dim3(kBlock), 0, s, p);
+        hipLaunchKernelGGL((spmm_main<TX, EPL, true, true, false, W>), dim3(grid), dim3(kBlock), 0, s, p);
     else if (hm)
-        hipLaunchKernelGGL((spmm_main<TX, EPL, false, true>), dim3(grid), dim3(kBlock), 0, s, p);
+        hipLaunchKernelGGL((spmm_main<TX, EPL, false, true, false, W>), dim3(grid), dim3(kBlock), 0, s, p);
     else
-        hipLaunchKernelGGL((spmm_main<TX, EPL, true, false>), dim3(grid), dim3(kBlock), 0, s, p);
+        hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, false, W>), dim3(grid), dim3(kBlock), 0, s, p);
     return hipGetLastError();
+}
+
+template <typename TX, int EPL>
+hipError_t launch_typed(const SpmmParams& p, unsigned grid, hipStream_t s) {
+    if (p.n_tables > 1) {
+        // typed-node tables: unweighted sum only
+        hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, true, false>), dim3(grid), dim3(kBlock), 0, s, p);
+        return hipGetLastError();
+    }
+    return p.w ? launch_w<TX, EPL, true>(p, grid, s) : launch_w<TX, EPL, false>(p, grid, s);
 }
 
 }  // namespace
 
-Geometry make_geometry(int64_t F, int x_dtype, uintptr_t x_align, uintptr_t out_align) {
+Geometry make_geometry(int64_t F, int x_dtype, uintptr_t x_align) {
     Geometry g;
     g.elem_bytes = x_dtype == MP_BF16 ? 2 : 4;
     const int64_t row_bytes = F * g.elem_bytes;
     int vec = 16;
-    // a lane-chunk of EPL >= 4 elements is stored with 16-byte fp32 stores,
-    // so it also needs a 16-byte aligned fp32 output
-    auto fits = [&](int v) {
-        const int epl = v / g.elem_bytes;
-        return row_bytes % v == 0 && x_align % v == 0 && (epl < 4 || out_align % 16 == 0);
-    };
-    while (vec > g.elem_bytes && !fits(vec)) vec >>= 1;
+    while (vec > g.elem_bytes && (row_bytes % vec != 0 || x_align % vec != 0)) vec >>= 1;
     g.epl = vec / g.elem_bytes;
     g.ltot = row_bytes / vec;
     if (g.ltot <= kWave) {
