@@ -37,7 +37,7 @@ if ROOT not in sys.path:
 METRIC = "SpMM effective HBM GB/s (% of peak) + edge·features/s, sum/mean/max"
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 WORKLOAD = "chunglu-124M"
-DOMINANT = "spmm_main<float, 4, true, false>"  # fp32 sum: the step's largest launch
+DOMINANT = "spmm_main<float, 4, true, false, false, false>"  # fp32 sum, the largest launch of a step
 DOMINANT_SRC = ["paper_2507_16991_amd/csrc/spmm.hip", "paper_2507_16991_amd/csrc/mp_internal.hpp"]
 COUNTER_SUMMARY = os.path.join(ROOT, "profiles", "spmm_main_f32_sum_chunglu124M_counters.txt")
 CALIB_BYTES = 1 << 30  # plain copy used to scale the HBM counters
@@ -92,49 +92,52 @@ def read_traffic():
 
 # ---- benchmark ------------------------------------------------------------------------
 
-def run(args):
-    import numpy as np
-    import torch
+def build_step(args, mp, torch, np, dev):
+    """Generate the workload, upload it, and return (graph, step(evs), op list).
 
+    Each op is (name, algorithmic bytes, edge*feature count); step(evs)
+    records events evs[0..len(ops)] around the ops on the current stream."""
     import graphgen
-    import paper_2507_16991_amd as mp
 
-    if args.gpus != 1:
-        print(f"bench.py measures one GPU only (asked for {args.gpus}); the multi-GPU "
-              "path is a design, not a build", file=sys.stderr)
-        sys.exit(2)
-    mp.lib()  # fail loudly if the HIP library is missing
-    dev = torch.device("cuda:0")
     t0 = time.time()
-    g = graphgen.workload(WORKLOAD, seed=args.seed)
+    g = graphgen.workload(args.workload, seed=args.seed)
     N, E, F = g.n_dst, g.E, g.F
-    print(f"[bench] generated {WORKLOAD}: N={N} E={E} F={F} in {time.time() - t0:.1f}s",
+    print(f"[bench] generated {args.workload}: N={N} E={E} F={F} in {time.time() - t0:.1f}s",
           file=sys.stderr, flush=True)
+    stream = torch.cuda.current_stream()
     src = torch.from_numpy(g.src).to(dev)
     dst = torch.from_numpy(g.dst).to(dev)
-    x32 = torch.from_numpy(g.x).to(dev)
-    x16 = torch.from_numpy(g.x_bf16.view(np.int16)).to(dev).view(torch.bfloat16)
-
-    # outputs and workspaces, allocated once
-    rowptr = torch.empty(N + 1, dtype=torch.int32, device=dev)
+    web = args.workload == "web-1.6B"
+    it = mp.MP_I64 if web else mp.MP_I32
+    rp_b = 8 if web else 4
+    rowptr = torch.empty(N + 1, dtype=torch.int64 if web else torch.int32, device=dev)
     col = torch.empty(E, dtype=torch.int32, device=dev)
-    ws_csr = torch.empty(mp.mp_coo_to_csr_workspace(E, N, mp.MP_I32, 0), dtype=torch.uint8,
-                         device=dev)
-    plan_buf = torch.empty(mp.mp_spmm_plan_size(N, E), dtype=torch.uint8, device=dev)
+    ws_csr = torch.empty(mp.mp_coo_to_csr_workspace(E, N, it, 0), dtype=torch.uint8, device=dev)
+    nplan = mp.mp_spmm_plan_size(N, E)
+    xs = {}
+    if g.x is not None:
+        xs["f32"] = (torch.from_numpy(g.x).to(dev), mp.MP_F32, 4)
+    if g.x_bf16 is not None:
+        xs["bf16"] = (torch.from_numpy(g.x_bf16.view(np.int16)).to(dev).view(torch.bfloat16),
+                      mp.MP_BF16, 2)
+    plan_bufs = {k: torch.empty(nplan, dtype=torch.uint8, device=dev) for k in xs}
     out = torch.empty(N, F, dtype=torch.float32, device=dev)
-    mx32 = torch.empty(N, F, dtype=torch.float32, device=dev)
-    mx16 = torch.empty(N, F, dtype=torch.bfloat16, device=dev)
+    mx = {k: torch.empty(N, F, dtype=torch.float32 if k == "f32" else torch.bfloat16,
+                         device=dev) for k in xs}
     arg = torch.empty(N, F, dtype=torch.int32, device=dev)
-    stream = torch.cuda.current_stream()
 
-    ops = []  # (name, bytes, E*F)
-    for xn, xb, mb in (("f32", 4, 4), ("bf16", 2, 2)):
-        ops.append((f"sum_{xn}", spmm_bytes(N, E, F, xb, 1), E * F))
-        ops.append((f"mean_{xn}", spmm_bytes(N, E, F, xb, 2), E * F))
-        ops.append((f"max_{xn}", spmm_bytes(N, E, F, xb, 4, max_b=mb), E * F))
-    step_names = ["csr", "plan"] + [o[0] for o in ops]
-    step_bytes = csr_bytes(N, E) + plan_bytes(N) + sum(o[1] for o in ops)
-    step_ef = sum(o[2] for o in ops)
+    ops = [("csr", csr_bytes(N, E, rowptr_b=rp_b), 0),
+           ("plan", len(xs) * plan_bytes(N), 0)]
+    if web:
+        reds = [("sum+max", mp.MP_SUM | mp.MP_MAX)]
+    else:
+        reds = [("sum", mp.MP_SUM), ("mean", mp.MP_MEAN), ("max", mp.MP_MAX)]
+    calls = []
+    for k, (x, xd, xb) in xs.items():
+        for rn, red in reds:
+            mb = 4 if k == "f32" else 2
+            ops.append((f"{rn}_{k}", spmm_bytes(N, E, F, xb, red, max_b=mb, rowptr_b=rp_b), E * F))
+            calls.append((k, x, xd, red))
 
     plans = {}
     wss = {}
@@ -144,34 +147,52 @@ def run(args):
             if evs is not None:
                 evs[i].record(stream)
         mark(0)
-        mp.mp_coo_to_csr(src, dst, E, N, rowptr, mp.MP_I32, col, None, None, None, ws_csr,
+        mp.mp_coo_to_csr(src, dst, E, N, rowptr, it, col, None, None, None, ws_csr,
                          ws_csr.numel())
         mark(1)
-        # the plan depends on F and dtype only through its check; one build
-        # per dtype keeps the ABI contract (plan matches x_dtype)
-        for k, xd in (("f32", mp.MP_F32), ("bf16", mp.MP_BF16)):
+        # one plan per feature dtype (a plan is checked against x's dtype)
+        for k, (x, xd, xb) in xs.items():
             if k in plans:
                 mp.mp_spmm_plan_free(plans[k])
-            plans[k] = mp.mp_spmm_plan_build(rowptr, mp.MP_I32, N, E, F, xd, plan_buf if k ==
-                                             "f32" else plan_buf2, plan_buf.numel())
+            plans[k] = mp.mp_spmm_plan_build(rowptr, it, N, E, F, xd, plan_bufs[k], nplan)
         mark(2)
         i = 2
-        for xn, x, xd, mxt, md in (("f32", x32, mp.MP_F32, mx32, mp.MP_F32),
-                                   ("bf16", x16, mp.MP_BF16, mx16, mp.MP_BF16)):
-            h = plans[xn]
-            for red in (mp.MP_SUM, mp.MP_MEAN, mp.MP_MAX):
-                nb = mp.mp_spmm_workspace(h, red)
-                key = (xn, red)
-                if key not in wss or wss[key].numel() < nb:
-                    wss[key] = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
-                hm = red == mp.MP_MAX
-                mp.mp_spmm(h, rowptr, mp.MP_I32, col, None, x, xd, N, N, F, red,
-                           None if hm else out, mp.MP_F32, mxt if hm else None, md,
-                           arg if hm else None, wss[key], wss[key].numel())
-                i += 1
-                mark(i)
+        for k, x, xd, red in calls:
+            h = plans[k]
+            nb = mp.mp_spmm_workspace(h, red)
+            key = (k, red)
+            if key not in wss or wss[key].numel() < nb:
+                wss[key] = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
+            hs = bool(red & (mp.MP_SUM | mp.MP_MEAN))
+            hm = bool(red & mp.MP_MAX)
+            mp.mp_spmm(h, rowptr, it, col, None, x, xd, N, N, F, red, out if hs else None,
+                       mp.MP_F32, mx[k] if hm else None, xd, arg if hm else None, wss[key],
+                       wss[key].numel())
+            i += 1
+            mark(i)
 
-    plan_buf2 = torch.empty_like(plan_buf)
+    return g, step, ops
+
+
+def run(args):
+    import numpy as np
+    import torch
+
+    import paper_2507_16991_amd as mp
+
+    if args.gpus != 1:
+        print(f"bench.py measures one GPU only (asked for {args.gpus}); the multi-GPU "
+              "path is a design, not a build", file=sys.stderr)
+        sys.exit(2)
+    mp.lib()  # fail loudly if the HIP library is missing
+    dev = torch.device("cuda:0")
+    g, step, ops = build_step(args, mp, torch, np, dev)
+    N, E, F = g.n_dst, g.E, g.F
+    names = [o[0] for o in ops]
+    op_bytes = {o[0]: o[1] for o in ops}
+    step_bytes = sum(o[1] for o in ops)
+    step_ef = sum(o[2] for o in ops)
+
     for _ in range(args.warmup):
         step()
     torch.cuda.synchronize()
@@ -183,8 +204,7 @@ def run(args):
         torch.cuda.synchronize()
         del a, b
 
-    nmark = len(step_names) + 1
-    all_evs = [[torch.cuda.Event(enable_timing=True) for _ in range(nmark)]
+    all_evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(ops) + 1)]
                for _ in range(args.steps)]
     torch.cuda.synchronize()
     t_start = time.perf_counter()
@@ -194,22 +214,27 @@ def run(args):
     wall = time.perf_counter() - t_start
     ms_step = wall * 1e3 / args.steps
 
-    per_op = {n: [] for n in step_names}
-    for evs in all_evs:
-        for i, n in enumerate(step_names):
-            per_op[n].append(evs[i].elapsed_time(evs[i + 1]))
-    op_ms = {n: float(np.mean(v)) for n, v in per_op.items()}
-    op_bytes = {"csr": csr_bytes(N, E), "plan": plan_bytes(N)}
-    op_bytes.update({o[0]: o[1] for o in ops})
+    op_ms = {n: float(np.mean([evs[i].elapsed_time(evs[i + 1]) for evs in all_evs]))
+             for i, n in enumerate(names)}
     breakdown = {n: {"ms": round(op_ms[n], 4),
                      "GB_per_s": round(op_bytes[n] / (op_ms[n] * 1e-3) / 1e9, 1)}
-                 for n in step_names}
-
+                 for n in names}
     value = step_bytes / (ms_step * 1e-3) / 1e9
-    dom_ms = op_ms["sum_f32"]
-    dom_bytes = op_bytes["sum_f32"]
+    web = args.workload == "web-1.6B"
+    dom = "sum+max_bf16" if web else "sum_f32"
+    dom_kernel = ("spmm_main<unsigned short, 8, true, true, false, false>, bf16 fused sum+max"
+                  if web else DOMINANT + ", fp32 sum")
+    dom_ms, dom_bytes = op_ms[dom], op_bytes[dom]
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
-    traffic = read_traffic()
+    traffic = None if web else read_traffic()
+    if web:
+        desc = (f"{args.workload}: power-law in-degree (alpha 2.0), uniform sources, N={N}, "
+                f"E={E}, F={F}, bf16 features U(-1,1), int64 rowptr, seed {args.seed}")
+        stepdesc = "COO->CSR + plan + fused {sum fp32, max bf16 + argmax}"
+    else:
+        desc = (f"{args.workload}: Chung-Lu power-law graph, N={N}, E={E}, F={F}, "
+                f"features fp32 and bf16 (N(0,1)), seed {args.seed}")
+        stepdesc = "COO->CSR + plan + {sum, mean, max+argmax} x {fp32, bf16 features}"
     result = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -223,19 +248,14 @@ def run(args):
         "vs_baseline": None,
         "dtype": "f32",
         "data": "synthetic",
-        "config": {
-            "workload": f"{WORKLOAD}: Chung-Lu power-law graph, N={N}, E={E}, F={F}, "
-                        "features fp32 and bf16 (N(0,1)), seed " + str(args.seed),
-            "step": "COO->CSR + plan + {sum, mean, max+argmax} x {fp32, bf16 features}",
-            "accumulate": "fp32",
-            "rowptr": "int32",
-        },
+        "config": {"workload": desc, "step": stepdesc, "accumulate": "fp32",
+                   "rowptr": "int64" if web else "int32"},
         "edge_features_per_s": round(step_ef / (ms_step * 1e-3), 1),
         "percent_of_hbm_peak": round(100 * value / HBM_PEAK_GBS, 2),
         "ops": breakdown,
         "roofline": {
             "bound": "hbm",
-            "kernel": DOMINANT + " (+ hub fix-up), fp32 sum",
+            "kernel": dom_kernel + " (+ hub fix-up)",
             "achieved": round(achieved, 1),
             "peak": HBM_PEAK_GBS,
             "unit": "GB/s",
@@ -245,7 +265,7 @@ def run(args):
             "avg_launch_ms": round(dom_ms, 4),
         },
     }
-    if args.cpu_baseline:
+    if args.cpu_baseline and not web:
         result["cpu_baseline"] = cpu_baseline(g, N, E, F, step_bytes, args)
     print(json.dumps(result), flush=True)
 
@@ -351,8 +371,8 @@ def summarize_counters(fetch_dir, write_dir, out, cmd):
     cw = max(copy_w) if copy_w else None
     scale_f = CALIB_BYTES / (cf * 1024.0) if cf else 1.0
     scale_w = CALIB_BYTES / (cw * 1024.0) if cw else 1.0
-    dom_f = pick(fr, "spmm_main<float, 4, true, false>")
-    dom_w = pick(wr, "spmm_main<float, 4, true, false>")
+    dom_f = pick(fr, DOMINANT)
+    dom_w = pick(wr, DOMINANT)
     if not dom_f or not dom_w:
         raise SystemExit("dominant kernel not found in the counter runs")
     f_b = sum(dom_f) / len(dom_f) * 1024.0 * scale_f
@@ -385,6 +405,8 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--seed", type=int, default=0)
+    ap.add_argument("--workload", default=WORKLOAD, choices=[WORKLOAD, "web-1.6B"],
+                    help="benchmark workload (the default is the metric's configuration)")
     ap.add_argument("--cpu-rows", type=int, default=200_000,
                     help="rows of the CPU-oracle aggregation sample")
     ap.add_argument("--no-cpu-baseline", dest="cpu_baseline", action="store_false")

@@ -64,6 +64,7 @@ def _L():
         lib.gg_uniform_f32.argtypes = [u64, u64, i64, p]
         lib.gg_normal_f32.argtypes = [u64, u64, i64, p]
         lib.gg_f32_to_bf16.argtypes = [i64, p, p]
+        lib.gg_uniform_bf16.argtypes = [u64, u64, i64, p]
         lib.gg_gcn_weights.argtypes = [i64, p, p, i64, i64, p]
         lib.gg_gcn_weights.restype = ctypes.c_int
         _lib = lib
@@ -130,6 +131,14 @@ def normal_f32(seed: int, stream: int, n: int) -> np.ndarray:
     out = np.empty(n, dtype=np.float32)
     if n:
         _L().gg_normal_f32(seed, stream, n, _ptr(out))
+    return out
+
+
+def uniform_bf16(seed: int, stream: int, n: int) -> np.ndarray:
+    """The bf16 rounding of uniform_f32(seed, stream, n), drawn directly."""
+    out = np.empty(n, dtype=np.uint16)
+    if n:
+        _L().gg_uniform_bf16(seed, stream, n, _ptr(out))
     return out
 
 
@@ -212,6 +221,9 @@ def powerlaw_dst_graph(seed: int, n: int, e: int, f: int, alpha: float,
     src = uniform_ints(seed, S_SRC, e, n)
     g = Graph(f"powerlaw-n{n}-e{e}-f{f}-a{alpha}", n, n, src, dst, f,
               meta={"alpha": alpha, "beta": beta})
+    if feat == "uniform" and bf16 and not fp32:
+        g.x_bf16 = uniform_bf16(seed, S_X, n * f).reshape(n, f)
+        return g
     xf = (uniform_f32 if feat == "uniform" else normal_f32)(seed, S_X, n * f).reshape(n, f)
     if bf16:
         g.x_bf16 = f32_to_bf16(xf)

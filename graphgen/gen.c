@@ -222,3 +222,17 @@ int gg_gcn_weights(int64_t e, const int32_t* src, const int32_t* dst, int64_t n_
     free(id);
     return 0;
 }
+
+/* U(-1,1) drawn exactly as gg_uniform_f32, then rounded to bfloat16 (RNE),
+ * without materializing the fp32 array. */
+void gg_uniform_bf16(uint64_t seed, uint64_t stream, int64_t n, uint16_t* out) {
+    const uint64_t key = gg_key(seed, stream);
+#pragma omp parallel for schedule(static)
+    for (int64_t i = 0; i < n; ++i) {
+        int64_t k = (int64_t)(gg_draw(key, (uint64_t)i) >> 40);
+        float f = (float)((double)(2 * k + 1 - (1LL << 24)) * (1.0 / 16777216.0));
+        uint32_t u;
+        memcpy(&u, &f, 4);
+        out[i] = (uint16_t)((u + 0x7FFFu + ((u >> 16) & 1u)) >> 16);
+    }
+}

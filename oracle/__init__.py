@@ -54,6 +54,8 @@ def _L():
         lib.oracle_spmm_coo_rows.restype = i32
         lib.oracle_hetero_sum.argtypes = [i32, p, p, i32, i64, i32, p, p, p, p, p, p, p]
         lib.oracle_hetero_sum.restype = i32
+        lib.oracle_csr_rows.argtypes = [i64, i64, p, p, i64, p, p, p]
+        lib.oracle_csr_rows.restype = i32
         _lib = lib
     return _lib
 
@@ -145,6 +147,25 @@ def spmm_coo_rows(src, dst, n_dst, rows, x=None, x_bf16=None, w_coo=None, n_src=
     if rc != 0:
         raise ValueError(f"oracle_spmm_coo_rows failed ({rc})")
     return {"sum": s, "mean": m, "max": mx, "argmax": am, "scale": sc}
+
+
+def csr_rows(src, dst, n_dst, rows):
+    """Column segments of the listed distinct rows of the stable CSR, from COO.
+
+    Returns (seg int64[len(rows)+1], cols int32[seg[-1]])."""
+    src, dst = _c(src, np.int32), _c(dst, np.int32)
+    rows = _c(rows, np.int64)
+    n = rows.shape[0]
+    seg = np.empty(n + 1, np.int64)
+    rc = _L().oracle_csr_rows(src.shape[0], n_dst, _p(src), _p(dst), n, _p(rows), _p(seg), None)
+    if rc != 0:
+        raise ValueError(f"oracle_csr_rows failed ({rc})")
+    cols = np.empty(int(seg[-1]), np.int32)
+    rc = _L().oracle_csr_rows(src.shape[0], n_dst, _p(src), _p(dst), n, _p(rows), _p(seg),
+                              _p(cols))
+    if rc != 0:
+        raise ValueError(f"oracle_csr_rows failed ({rc})")
+    return seg, cols
 
 
 def hetero_sum(n_per_type, x_bf16_per_type, rel_src_type, rel_dst_type, rel_src, rel_dst):

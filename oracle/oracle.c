@@ -248,3 +248,48 @@ int oracle_hetero_sum(int n_types, const int64_t* n_per_type, const void* const*
     }
     return 0;
 }
+
+/* ---- CSR column segments of listed rows straight from COO --------------- */
+
+/* For the listed distinct rows, the sources of their edges in COO order (which
+ * is their order in the stable destination-major CSR), concatenated in list
+ * order: row k's segment is cols[seg[k] .. seg[k+1]).  Pass 1 (cols == NULL)
+ * fills seg[0..n_rows] only.  Returns 0, -1 on a bad index, -2 on allocation
+ * failure. */
+int oracle_csr_rows(int64_t E, int64_t N_dst, const int32_t* src, const int32_t* dst,
+                    int64_t n_rows, const int64_t* rows, int64_t* seg, int32_t* cols) {
+    int64_t* slot = (int64_t*)malloc(sizeof(int64_t) * (size_t)(N_dst > 0 ? N_dst : 1));
+    int64_t* fill = (int64_t*)calloc((size_t)(n_rows > 0 ? n_rows : 1), sizeof(int64_t));
+    if (!slot || !fill) {
+        free(slot); free(fill);
+        return -2;
+    }
+    for (int64_t v = 0; v < N_dst; ++v) slot[v] = -1;
+    for (int64_t k = 0; k < n_rows; ++k) {
+        if (rows[k] < 0 || rows[k] >= N_dst) {
+            free(slot); free(fill);
+            return -1;
+        }
+        slot[rows[k]] = k;
+    }
+    if (!cols) {
+        for (int64_t k = 0; k <= n_rows; ++k) seg[k] = 0;
+        for (int64_t e = 0; e < E; ++e) {
+            if (dst[e] < 0 || dst[e] >= N_dst) {
+                free(slot); free(fill);
+                return -1;
+            }
+            int64_t k = slot[dst[e]];
+            if (k >= 0) seg[k + 1] += 1;
+        }
+        for (int64_t k = 0; k < n_rows; ++k) seg[k + 1] += seg[k];
+    } else {
+        for (int64_t e = 0; e < E; ++e) {
+            int64_t k = slot[dst[e]];
+            if (k >= 0) cols[seg[k] + fill[k]++] = src[e];
+        }
+    }
+    free(slot);
+    free(fill);
+    return 0;
+}

@@ -365,3 +365,52 @@ def test_hetero_small():
 def test_hetero_20M():
     g = graphgen.workload("hetero-20M", seed=0)
     run_hetero(g, True)
+
+
+# ---- web-scale single-GPU shard ---------------------------------------------------------
+
+def test_web_1_6B_fused_sum_max_sampled():
+    """N = 1e8, E = 1.6e9, F = 64 bf16, int64 rowptr, fused sum (fp32) + max
+    (bf16, exact) + argmax in one pass, as the benchmark option runs it.
+    rowptr is checked in full against numpy's bincount + cumsum; the column
+    segments and outputs of sampled rows (every row with >= 10^4 edges, the
+    empty rows among 20k random rows, and the random rows themselves) are
+    checked against the oracle computed straight from COO."""
+    g = graphgen.workload("web-1.6B", seed=0)
+    N, E, F = g.n_dst, g.E, g.F
+    sys.stderr.write(f"[web-1.6B] generated N={N} E={E}\n")
+    sys.stderr.flush()
+    s, d = dev(g.src), dev(g.dst)
+    rp, col, _, _ = mp.coo_to_csr(s, d, N, rowptr_dtype=torch.int64)
+    del s, d
+    torch.cuda.synchronize()
+    deg = np.bincount(g.dst, minlength=N).astype(np.int64)
+    rp_h = rp.cpu().numpy()
+    assert rp_h[0] == 0 and np.array_equal(np.diff(rp_h), deg), "rowptr"
+    sys.stderr.write(f"[web-1.6B] rowptr ok, max degree {deg.max()}\n")
+    sys.stderr.flush()
+
+    rnd = np.unique(graphgen.uniform_ints(12, 5, 20_000, N).astype(np.int64))
+    rows = np.unique(np.concatenate([np.nonzero(deg >= 10_000)[0], rnd])).astype(np.int64)
+    seg, cols_ref = oracle.csr_rows(g.src, g.dst, N, rows)
+    idx = np.concatenate([np.arange(rp_h[r], rp_h[r + 1]) for r in rows]).astype(np.int64)
+    assert np.array_equal(col[dev(idx)].cpu().numpy(), cols_ref), "col segments"
+    del idx, cols_ref
+
+    x = dev(g.x_bf16.view(np.int16)).view(torch.bfloat16)
+    plan = mp.Plan(rp, E, F, torch.bfloat16)
+    out, out_max, argout = mp.spmm(rp, col, x, mp.MP_SUM | mp.MP_MAX, plan=plan,
+                                   max_dtype=torch.bfloat16)
+    torch.cuda.synchronize()
+    rd = dev(rows)
+    y = out[rd].cpu().numpy()
+    ym = out_max[rd].view(torch.int16).cpu().numpy().view(np.uint16)
+    ya = argout[rd].cpu().numpy().astype(np.int64)
+    del out, out_max, argout, x
+    ref = oracle.spmm_coo_rows(g.src, g.dst, N, rows, x_bf16=g.x_bf16)
+    err = scaled_error(y, ref["sum"], ref["scale"])
+    sys.stderr.write(f"[web-1.6B] rows {rows.shape[0]} sum error {err:.3e}\n")
+    assert err <= TOL[torch.bfloat16], f"sum error {err}"
+    assert err <= 1e-5, f"fp32 accumulation error {err}"
+    assert np.array_equal(ya, ref["argmax"]), "argmax"
+    assert np.array_equal(ym, (ref["max"].view(np.uint32) >> 16).astype(np.uint16)), "max bits"

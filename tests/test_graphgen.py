@@ -118,3 +118,9 @@ def test_thread_count_independence():
         env = dict(os.environ, OMP_NUM_THREADS=t, PYTHONPATH=root)
         outs.append(subprocess.check_output([sys.executable, "-c", code], env=env, cwd=root))
     assert outs[0] == outs[1]
+
+
+def test_uniform_bf16_is_rounding_of_uniform_f32():
+    a = graphgen.uniform_bf16(3, 3, 50_000)
+    b = graphgen.f32_to_bf16(graphgen.uniform_f32(3, 3, 50_000))
+    assert np.array_equal(a, b)

@@ -100,3 +100,12 @@ def test_golden_worked_example():
     assert col.tolist() == g["col"]
     assert perm.tolist() == g["perm"]
     assert wc.tolist() == g["w_csr"]
+
+
+def test_csr_rows_matches_full_conversion():
+    src, dst = random_graph(11, 500, 20_000)
+    rp, col, _, _ = oracle.coo_to_csr(src, dst, 500)
+    rows = np.array([499, 3, 0, 250, 17], np.int64)
+    seg, cols = oracle.csr_rows(src, dst, 500, rows)
+    for k, r in enumerate(rows):
+        assert np.array_equal(cols[seg[k]:seg[k + 1]], col[rp[r]:rp[r + 1]])
