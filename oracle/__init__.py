@@ -50,7 +50,7 @@ def _L():
                                     p, p, p, p, p, i32]
         lib.oracle_spmm.restype = i32
         lib.oracle_spmm_coo_rows.argtypes = [i64, i64, i64, p, p, p, p, i32, i64, i64, p,
-                                             p, p, p, p, p]
+                                             p, p, p, p, p, p]
         lib.oracle_spmm_coo_rows.restype = i32
         lib.oracle_hetero_sum.argtypes = [i32, p, p, i32, i64, i32, p, p, p, p, p, p, p]
         lib.oracle_hetero_sum.restype = i32
@@ -126,10 +126,13 @@ def spmm(rowptr, col, x=None, x_bf16=None, w=None, rows=None, nthreads=None,
     return out
 
 
-def spmm_coo_rows(src, dst, n_dst, rows, x=None, x_bf16=None, w_coo=None, n_src=None):
+def spmm_coo_rows(src, dst, n_dst, rows, x=None, x_bf16=None, w_coo=None, n_src=None,
+                  row_start=None):
     """Outputs of the listed distinct rows, straight from COO (no CSR built).
 
-    argmax is reported as a position in the stable destination-major CSR."""
+    argmax is reported as a position in the stable destination-major CSR;
+    row_start (optional, int64 per listed row) gives the number of edges
+    whose destination is below each row, else it is counted here."""
     src, dst = _c(src, np.int32), _c(dst, np.int32)
     xa, isb, nx, F = _x_args(x, x_bf16)
     n_src = nx if n_src is None else n_src
@@ -141,9 +144,10 @@ def spmm_coo_rows(src, dst, n_dst, rows, x=None, x_bf16=None, w_coo=None, n_src=
     am = np.empty((n, F), np.int64)
     sc = np.empty((n, F), np.float64)
     w_coo = _c(w_coo, np.float32)
+    row_start = _c(row_start, np.int64)
     rc = _L().oracle_spmm_coo_rows(src.shape[0], n_dst, n_src, _p(src), _p(dst), _p(w_coo),
-                                   _p(xa), isb, F, n, _p(rows), _p(s), _p(m), _p(mx), _p(am),
-                                   _p(sc))
+                                   _p(xa), isb, F, n, _p(rows), _p(row_start), _p(s), _p(m),
+                                   _p(mx), _p(am), _p(sc))
     if rc != 0:
         raise ValueError(f"oracle_spmm_coo_rows failed ({rc})")
     return {"sum": s, "mean": m, "max": mx, "argmax": am, "scale": sc}

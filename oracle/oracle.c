@@ -143,46 +143,133 @@ int oracle_spmm(int64_t n_rows, const int64_t* rows, int64_t N_dst, int64_t N_sr
     return bad ? -1 : 0;
 }
 
+/* ---- listed-row lookup ------------------------------------------------- */
+
+/* Membership of row ids in a list, as a bit array over [0, N) plus the list
+ * sorted by id (with each id's position in the original list), so that a
+ * pass over E edges costs one bit test per edge and a binary search only for
+ * edges of listed rows. */
+typedef struct {
+    uint64_t* bits;
+    int64_t* sorted;  /* listed ids, ascending */
+    int64_t* where;   /* where[j] = position in the caller's list of sorted[j] */
+    int64_t n;
+} row_set;
+
+static int cmp_pair(const void* a, const void* b) {
+    const int64_t* x = (const int64_t*)a;
+    const int64_t* y = (const int64_t*)b;
+    return x[0] < y[0] ? -1 : (x[0] > y[0] ? 1 : 0);
+}
+
+static void row_set_free(row_set* s) {
+    free(s->bits);
+    free(s->sorted);
+    free(s->where);
+}
+
+/* 0, -1 (id out of range) or -2 (allocation) */
+static int row_set_make(row_set* s, int64_t N, int64_t n, const int64_t* rows) {
+    s->n = n;
+    s->bits = (uint64_t*)calloc((size_t)((N + 63) / 64 + 1), sizeof(uint64_t));
+    s->sorted = (int64_t*)malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    s->where = (int64_t*)malloc(sizeof(int64_t) * (size_t)(n > 0 ? n : 1));
+    int64_t* pairs = (int64_t*)malloc(sizeof(int64_t) * 2 * (size_t)(n > 0 ? n : 1));
+    if (!s->bits || !s->sorted || !s->where || !pairs) {
+        free(pairs);
+        row_set_free(s);
+        return -2;
+    }
+    for (int64_t k = 0; k < n; ++k) {
+        if (rows[k] < 0 || rows[k] >= N) {
+            free(pairs);
+            row_set_free(s);
+            return -1;
+        }
+        pairs[2 * k] = rows[k];
+        pairs[2 * k + 1] = k;
+        s->bits[rows[k] >> 6] |= 1ull << (rows[k] & 63);
+    }
+    qsort(pairs, (size_t)n, 2 * sizeof(int64_t), cmp_pair);
+    for (int64_t k = 0; k < n; ++k) {
+        s->sorted[k] = pairs[2 * k];
+        s->where[k] = pairs[2 * k + 1];
+    }
+    free(pairs);
+    return 0;
+}
+
+/* position in the caller's list of row v, or -1 if v is not listed */
+static inline int64_t row_set_find(const row_set* s, int64_t v) {
+    if (!((s->bits[v >> 6] >> (v & 63)) & 1ull)) return -1;
+    int64_t lo = 0, hi = s->n - 1;
+    while (lo < hi) {
+        int64_t mid = (lo + hi) >> 1;
+        if (s->sorted[mid] < v) lo = mid + 1; else hi = mid;
+    }
+    return s->where[lo];
+}
+
 /* ---- aggregation of listed rows straight from COO ----------------------- */
 
 /* Same outputs as oracle_spmm for the listed (distinct) rows, computed from
  * the COO arrays without building the CSR: one pass over the edges in COO
  * order, so each row sees its edges in the order of the stable CSR, and the
  * CSR position of edge e is rowptr[dst_e] + (number of earlier edges with the
- * same destination).  `w` is in COO order here.  Meant for graphs too large to
+ * same destination).  rowptr of the listed rows is taken from row_start when
+ * given (row_start[k] = number of edges whose destination is below rows[k]),
+ * else counted here.  `w` is in COO order.  Meant for graphs too large to
  * convert on the host; one thread.  Returns 0, -1 on a bad index, -2 on
  * allocation failure. */
 int oracle_spmm_coo_rows(int64_t E, int64_t N_dst, int64_t N_src, const int32_t* src,
                          const int32_t* dst, const float* w_coo, const void* x,
                          int x_is_bf16, int64_t F, int64_t n_rows, const int64_t* rows,
-                         double* out_sum, double* out_mean, float* out_max,
-                         int64_t* argout, double* scale) {
-    int64_t* slot = (int64_t*)malloc(sizeof(int64_t) * (size_t)(N_dst > 0 ? N_dst : 1));
-    int64_t* below = (int64_t*)calloc((size_t)(N_dst + 1), sizeof(int64_t));
+                         const int64_t* row_start, double* out_sum, double* out_mean,
+                         float* out_max, int64_t* argout, double* scale) {
+    row_set set;
+    int rc = row_set_make(&set, N_dst, n_rows, rows);
+    if (rc != 0) return rc;
+    int64_t* start = (int64_t*)calloc((size_t)(n_rows > 0 ? n_rows : 1), sizeof(int64_t));
     int64_t* seen = (int64_t*)calloc((size_t)(n_rows > 0 ? n_rows : 1), sizeof(int64_t));
     double* acc = (double*)calloc((size_t)((n_rows > 0 ? n_rows : 1) * (F > 0 ? F : 1)),
                                   sizeof(double));
-    if (!slot || !below || !seen || !acc) {
-        free(slot); free(below); free(seen); free(acc);
+    if (!start || !seen || !acc) {
+        free(start); free(seen); free(acc); row_set_free(&set);
         return -2;
     }
-    for (int64_t v = 0; v < N_dst; ++v) slot[v] = -1;
-    for (int64_t k = 0; k < n_rows; ++k) {
-        if (rows[k] < 0 || rows[k] >= N_dst) {
-            free(slot); free(below); free(seen); free(acc);
-            return -1;
-        }
-        slot[rows[k]] = k;
-    }
-    /* rowptr[v] = number of edges whose destination is below v */
-    for (int64_t e = 0; e < E; ++e) {
+    for (int64_t e = 0; e < E; ++e)
         if (dst[e] < 0 || dst[e] >= N_dst || src[e] < 0 || src[e] >= N_src) {
-            free(slot); free(below); free(seen); free(acc);
+            free(start); free(seen); free(acc); row_set_free(&set);
             return -1;
         }
-        below[dst[e] + 1] += 1;
+    if (row_start) {
+        for (int64_t k = 0; k < n_rows; ++k) start[k] = row_start[k];
+    } else {
+        /* start[k] = number of edges whose destination is below rows[k] */
+        for (int64_t e = 0; e < E; ++e) {
+            int64_t v = dst[e];
+            /* count listed rows above v: binary search in the sorted ids */
+            int64_t lo = 0, hi = set.n;
+            while (lo < hi) {
+                int64_t mid = (lo + hi) >> 1;
+                if (set.sorted[mid] <= v) lo = mid + 1; else hi = mid;
+            }
+            if (lo < set.n) start[lo] += 1; /* counted for sorted[lo] and all above */
+        }
+        /* prefix over the sorted list, then map back to list positions */
+        int64_t run = 0;
+        int64_t* tmp = (int64_t*)malloc(sizeof(int64_t) * (size_t)(n_rows > 0 ? n_rows : 1));
+        if (!tmp) {
+            free(start); free(seen); free(acc); row_set_free(&set);
+            return -2;
+        }
+        for (int64_t j = 0; j < set.n; ++j) {
+            run += start[j];
+            tmp[set.where[j]] = run;
+        }
+        for (int64_t k = 0; k < n_rows; ++k) start[k] = tmp[k];
+        free(tmp);
     }
-    for (int64_t v = 0; v < N_dst; ++v) below[v + 1] += below[v];
 
     for (int64_t k = 0; k < n_rows; ++k)
         for (int64_t f = 0; f < F; ++f) {
@@ -191,9 +278,9 @@ int oracle_spmm_coo_rows(int64_t E, int64_t N_dst, int64_t N_src, const int32_t*
             if (scale) scale[k * F + f] = 0.0;
         }
     for (int64_t e = 0; e < E; ++e) {
-        int64_t k = slot[dst[e]];
+        int64_t k = row_set_find(&set, dst[e]);
         if (k < 0) continue;
-        int64_t p = below[dst[e]] + seen[k];
+        int64_t p = start[k] + seen[k];
         seen[k] += 1;
         for (int64_t f = 0; f < F; ++f) {
             float xv = feature(x, x_is_bf16, F, src[e], f);
@@ -211,7 +298,7 @@ int oracle_spmm_coo_rows(int64_t E, int64_t N_dst, int64_t N_src, const int32_t*
             if (out_sum) out_sum[k * F + f] = acc[k * F + f];
             if (out_mean) out_mean[k * F + f] = seen[k] > 0 ? acc[k * F + f] / (double)seen[k] : 0.0;
         }
-    free(slot); free(below); free(seen); free(acc);
+    free(start); free(seen); free(acc); row_set_free(&set);
     return 0;
 }
 
@@ -258,38 +345,32 @@ int oracle_hetero_sum(int n_types, const int64_t* n_per_type, const void* const*
  * failure. */
 int oracle_csr_rows(int64_t E, int64_t N_dst, const int32_t* src, const int32_t* dst,
                     int64_t n_rows, const int64_t* rows, int64_t* seg, int32_t* cols) {
-    int64_t* slot = (int64_t*)malloc(sizeof(int64_t) * (size_t)(N_dst > 0 ? N_dst : 1));
+    row_set set;
+    int rc = row_set_make(&set, N_dst, n_rows, rows);
+    if (rc != 0) return rc;
     int64_t* fill = (int64_t*)calloc((size_t)(n_rows > 0 ? n_rows : 1), sizeof(int64_t));
-    if (!slot || !fill) {
-        free(slot); free(fill);
+    if (!fill) {
+        row_set_free(&set);
         return -2;
-    }
-    for (int64_t v = 0; v < N_dst; ++v) slot[v] = -1;
-    for (int64_t k = 0; k < n_rows; ++k) {
-        if (rows[k] < 0 || rows[k] >= N_dst) {
-            free(slot); free(fill);
-            return -1;
-        }
-        slot[rows[k]] = k;
     }
     if (!cols) {
         for (int64_t k = 0; k <= n_rows; ++k) seg[k] = 0;
         for (int64_t e = 0; e < E; ++e) {
             if (dst[e] < 0 || dst[e] >= N_dst) {
-                free(slot); free(fill);
+                free(fill); row_set_free(&set);
                 return -1;
             }
-            int64_t k = slot[dst[e]];
+            int64_t k = row_set_find(&set, dst[e]);
             if (k >= 0) seg[k + 1] += 1;
         }
         for (int64_t k = 0; k < n_rows; ++k) seg[k + 1] += seg[k];
     } else {
         for (int64_t e = 0; e < E; ++e) {
-            int64_t k = slot[dst[e]];
+            int64_t k = row_set_find(&set, dst[e]);
             if (k >= 0) cols[seg[k] + fill[k]++] = src[e];
         }
     }
-    free(slot);
     free(fill);
+    row_set_free(&set);
     return 0;
 }

@@ -29,7 +29,8 @@ __all__ = [
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-LIB_PATH = os.path.join(_HERE, "libmp.so")
+# MP_LIBRARY may point at another build of the same sources (tuning runs).
+LIB_PATH = os.environ.get("MP_LIBRARY") or os.path.join(_HERE, "libmp.so")
 
 MP_OK = 0
 MP_F32, MP_BF16 = 0, 1

@@ -26,9 +26,9 @@ FLAGS = [
 ]
 
 
-def _compile(src: str) -> str:
-    out = os.path.join(OBJ, src + ".o")
-    cmd = [HIPCC, *FLAGS, "-c", os.path.join(CSRC, src), "-o", out]
+def _compile(src: str, obj_dir: str = OBJ, extra=()) -> str:
+    out = os.path.join(obj_dir, src + ".o")
+    cmd = [HIPCC, *FLAGS, *extra, "-c", os.path.join(CSRC, src), "-o", out]
     if src.endswith(".cpp"):
         cmd[1:1] = ["-x", "hip"]
     r = subprocess.run(cmd, capture_output=True, text=True)
@@ -42,14 +42,17 @@ def _compile(src: str) -> str:
     return out
 
 
-def build() -> str:
-    os.makedirs(OBJ, exist_ok=True)
+def build(lib: str = LIB, defines=()) -> str:
+    """Compile and link; `defines` (e.g. ["-DMP_SORT_ITEMS=8"]) override the
+    compile-time tuning constants, `lib` the output path."""
+    obj_dir = OBJ if lib == LIB else lib + ".objs"
+    os.makedirs(obj_dir, exist_ok=True)
     with ThreadPoolExecutor(max_workers=4) as ex:
-        objs = list(ex.map(_compile, SOURCES))
-    tmp = LIB + ".tmp"
+        objs = list(ex.map(lambda s: _compile(s, obj_dir, defines), SOURCES))
+    tmp = lib + ".tmp"
     subprocess.check_call([HIPCC, "--offload-arch=gfx950", "-shared", "-fPIC", *objs, "-o", tmp])
-    os.replace(tmp, LIB)
-    return LIB
+    os.replace(tmp, lib)
+    return lib
 
 
 if __name__ == "__main__":

@@ -13,9 +13,15 @@ namespace mp {
 constexpr int kWave = 64;
 
 // ---- radix sort geometry (COO -> CSR) ---------------------------------------
-constexpr int kSortBlock = 256;                    // 4 wavefronts
-constexpr int kSortItems = 16;                     // keys per thread
-constexpr int kSortTile = kSortBlock * kSortItems; // 4096 keys per workgroup
+#ifndef MP_SORT_BLOCK
+#define MP_SORT_BLOCK 512
+#endif
+#ifndef MP_SORT_ITEMS
+#define MP_SORT_ITEMS 16
+#endif
+constexpr int kSortBlock = MP_SORT_BLOCK;          // threads per workgroup
+constexpr int kSortItems = MP_SORT_ITEMS;          // keys per thread
+constexpr int kSortTile = kSortBlock * kSortItems; // keys per workgroup
 constexpr int kSortMaxBits = 8;                    // digit width cap (256 buckets)
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }

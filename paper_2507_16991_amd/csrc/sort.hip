@@ -12,6 +12,10 @@
 // arithmetic: the result is bit-exact.
 #include "mp_internal.hpp"
 
+#ifndef MP_SORT_NT_STORE
+#define MP_SORT_NT_STORE 0
+#endif
+
 namespace mp {
 namespace {
 
@@ -37,10 +41,13 @@ __global__ __launch_bounds__(kSortBlock) void radix_hist(const uint32_t* __restr
     for (int d = threadIdx.x; d < R; d += kSortBlock) counts[(int64_t)d * tiles + blockIdx.x] = h[d];
 }
 
+// HAS_B: the second payload is carried (it costs 16 KB of LDS per tile, so
+// the payload-free variant fits one more workgroup per CU).
+template <bool HAS_B>
 __global__ __launch_bounds__(kSortBlock) void radix_scatter(RadixPass p, int64_t tiles) {
     __shared__ uint32_t s_key[kSortTile];
     __shared__ int32_t s_a[kSortTile];
-    __shared__ int32_t s_b[kSortTile];
+    __shared__ int32_t s_b[HAS_B ? kSortTile : 1];
     __shared__ uint32_t s_cnt[kSortWaves][kMaxBuckets];
     __shared__ uint32_t s_start[kMaxBuckets];
     __shared__ uint32_t s_gbase[kMaxBuckets];
@@ -50,6 +57,8 @@ __global__ __launch_bounds__(kSortBlock) void radix_scatter(RadixPass p, int64_t
     const int wv = threadIdx.x / kWave;
     for (int i = threadIdx.x; i < kSortWaves * kMaxBuckets; i += kSortBlock)
         (&s_cnt[0][0])[i] = 0;
+    for (int d = threadIdx.x; d < R; d += kSortBlock)
+        s_gbase[d] = p.counts[(int64_t)d * tiles + blockIdx.x];
     __syncthreads();
 
     const int64_t tbase = (int64_t)blockIdx.x * kSortTile;
@@ -63,9 +72,9 @@ __global__ __launch_bounds__(kSortBlock) void radix_scatter(RadixPass p, int64_t
     for (int k = 0; k < kSortItems; ++k) {
         const int64_t i = wbase + (int64_t)k * kWave + lane;
         const bool ok = i < p.n;
-        key[k] = ok ? p.keys_in[i] : 0u;
-        va[k] = p.a_in ? (ok ? p.a_in[i] : 0) : (int32_t)i;
-        vb[k] = p.b_in ? (ok ? p.b_in[i] : 0) : (int32_t)i;
+        key[k] = ok ? __builtin_nontemporal_load(p.keys_in + i) : 0u;
+        va[k] = p.a_in ? (ok ? __builtin_nontemporal_load(p.a_in + i) : 0) : (int32_t)i;
+        if constexpr (HAS_B) vb[k] = p.b_in ? (ok ? __builtin_nontemporal_load(p.b_in + i) : 0) : (int32_t)i;
     }
 #pragma unroll
     for (int k = 0; k < kSortItems; ++k) {
@@ -98,7 +107,6 @@ __global__ __launch_bounds__(kSortBlock) void radix_scatter(RadixPass p, int64_t
             run += c;
         }
         s_start[d] = run;
-        s_gbase[d] = p.counts[(int64_t)d * tiles + blockIdx.x];
     }
     __syncthreads();
     // exclusive scan of the digit totals (R <= 256) by wavefront 0
@@ -135,7 +143,7 @@ __global__ __launch_bounds__(kSortBlock) void radix_scatter(RadixPass p, int64_t
             const uint32_t lp = s_start[d] + s_cnt[wv][d] + rank[k];
             s_key[lp] = key[k];
             s_a[lp] = va[k];
-            s_b[lp] = vb[k];
+            if constexpr (HAS_B) s_b[lp] = vb[k];
         }
     }
     __syncthreads();
@@ -146,24 +154,43 @@ __global__ __launch_bounds__(kSortBlock) void radix_scatter(RadixPass p, int64_t
         const uint32_t d = (kk >> p.shift) & (uint32_t)(R - 1);
         const int64_t pos = (int64_t)s_gbase[d] + (i - (int64_t)s_start[d]);
         if (pos >= p.n) continue;  // cannot happen for consistent counts; never write past n
+#if MP_SORT_NT_STORE
+        if (p.keys_out) __builtin_nontemporal_store(kk, p.keys_out + pos);
+        if (p.a_out) __builtin_nontemporal_store(s_a[i], p.a_out + pos);
+        if constexpr (HAS_B) {
+            if (p.b_out) __builtin_nontemporal_store(s_b[i], p.b_out + pos);
+        }
+#else
         if (p.keys_out) p.keys_out[pos] = kk;
         if (p.a_out) p.a_out[pos] = s_a[i];
-        if (p.b_out) p.b_out[pos] = s_b[i];
+        if constexpr (HAS_B) {
+            if (p.b_out) p.b_out[pos] = s_b[i];
+        }
+#endif
     }
 }
 
 // rowptr[v] = first CSR position whose key is >= v, from the sorted keys:
 // position p writes every v in (keys[p-1], keys[p]] (keys[-1] = -1,
-// keys[E] = N), so each of the N+1 entries is written exactly once.
+// keys[E] = N), so each of the N+1 entries is written exactly once.  Each
+// thread covers kRowptrItems consecutive positions.
+constexpr int kRowptrItems = 8;
+
 template <typename RP>
 __global__ __launch_bounds__(256) void rowptr_from_sorted(const uint32_t* __restrict__ keys,
                                                           int64_t E, int64_t N, RP* __restrict__ rowptr) {
-    const int64_t p = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (p > E) return;
-    const int64_t prev = p == 0 ? -1 : (int64_t)keys[p - 1];
-    int64_t cur = p == E ? N : (int64_t)keys[p];
-    if (cur > N) cur = N;  // keys are < N for valid input; stay inside rowptr regardless
-    for (int64_t v = prev + 1; v <= cur; ++v) rowptr[v] = (RP)p;
+    const int64_t p0 = ((int64_t)blockIdx.x * 256 + threadIdx.x) * kRowptrItems;
+    if (p0 > E) return;
+    int64_t prev = p0 == 0 ? -1 : (int64_t)keys[p0 - 1];
+#pragma unroll
+    for (int k = 0; k < kRowptrItems; ++k) {
+        const int64_t p = p0 + k;
+        if (p > E) break;
+        int64_t cur = p == E ? N : (int64_t)keys[p];
+        if (cur > N) cur = N;  // keys are < N for valid input; stay inside rowptr regardless
+        for (int64_t v = prev + 1; v <= cur; ++v) rowptr[v] = (RP)p;
+        if (cur > prev) prev = cur;
+    }
 }
 
 template <typename RP>
@@ -236,13 +263,16 @@ hipError_t radix_pass(const RadixPass& p, hipStream_t s) {
     if (e != hipSuccess) return e;
     e = exclusive_scan_u32(p.counts, tiles << p.bits, p.scan_ws, s);
     if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(radix_scatter, dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p, tiles);
+    if (p.b_out)
+        hipLaunchKernelGGL(radix_scatter<true>, dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p, tiles);
+    else
+        hipLaunchKernelGGL(radix_scatter<false>, dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p, tiles);
     return hipGetLastError();
 }
 
 hipError_t launch_rowptr_from_sorted(const uint32_t* keys, int64_t E, int64_t N, void* rowptr,
                                      int rp64, hipStream_t s) {
-    const unsigned g = grid_for(E + 1, 256);
+    const unsigned g = grid_for(ceil_div(E + 1, kRowptrItems), 256);
     if (rp64)
         hipLaunchKernelGGL(rowptr_from_sorted<int64_t>, dim3(g), dim3(256), 0, s, keys, E, N,
                            static_cast<int64_t*>(rowptr));

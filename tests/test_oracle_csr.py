@@ -105,7 +105,7 @@ def test_golden_worked_example():
 def test_csr_rows_matches_full_conversion():
     src, dst = random_graph(11, 500, 20_000)
     rp, col, _, _ = oracle.coo_to_csr(src, dst, 500)
-    rows = np.array([499, 3, 0, 250, 17], np.int64)
+    rows = np.array([499, 3, 0, 250, 17, 64, 63, 65, 128], np.int64)
     seg, cols = oracle.csr_rows(src, dst, 500, rows)
     for k, r in enumerate(rows):
         assert np.array_equal(cols[seg[k]:seg[k + 1]], col[rp[r]:rp[r + 1]])

@@ -223,9 +223,14 @@ def test_row_subset_and_coo_rows_agree():
     full = oracle.spmm(rp, col, x=g.x, w=wc)
     sub = oracle.spmm(rp, col, x=g.x, w=wc, rows=rows)
     coo = oracle.spmm_coo_rows(g.src, g.dst, g.n_dst, rows, x=g.x, w_coo=g.w)
+    shuffled = rows[np.argsort(graphgen.uniform_ints(1, 9, rows.shape[0], 10**9))]
+    below = np.concatenate([[0], np.cumsum(np.bincount(g.dst, minlength=g.n_dst))])[shuffled]
+    coo2 = oracle.spmm_coo_rows(g.src, g.dst, g.n_dst, shuffled, x=g.x, w_coo=g.w,
+                                row_start=below)
     for k in ("sum", "mean", "max", "argmax", "scale"):
         assert np.array_equal(sub[k], full[k][rows]), k
         assert np.array_equal(coo[k], full[k][rows]), k
+        assert np.array_equal(coo2[k], full[k][shuffled]), k
 
 
 def test_thread_count_does_not_change_results():
