@@ -92,6 +92,20 @@ def read_traffic():
 
 # ---- benchmark ------------------------------------------------------------------------
 
+def hetero_bytes(g, F):
+    """Per destination type: combined CSR build (read src+dst, write col and
+    rowptr) and the sum (rowptr, col, one bf16 row gathered per edge, fp32 out)."""
+    b_csr = b_sum = ef = 0
+    for t, n in enumerate(g.n_per_type):
+        e = sum(g.rel_src[r].shape[0] for r in range(len(g.rel_src)) if g.rel_dst_type[r] == t)
+        if e == 0:
+            continue
+        b_csr += csr_bytes(n, e)
+        b_sum += spmm_bytes(n, e, F, 2, 1)
+        ef += e * F
+    return b_csr, b_sum, ef
+
+
 def build_step(args, mp, torch, np, dev):
     """Generate the workload, upload it, and return (graph, step(evs), op list).
 
@@ -101,23 +115,60 @@ def build_step(args, mp, torch, np, dev):
 
     t0 = time.time()
     g = graphgen.workload(args.workload, seed=args.seed)
-    N, E, F = g.n_dst, g.E, g.F
-    print(f"[bench] generated {args.workload}: N={N} E={E} F={F} in {time.time() - t0:.1f}s",
-          file=sys.stderr, flush=True)
+    print(f"[bench] generated {args.workload} in {time.time() - t0:.1f}s", file=sys.stderr,
+          flush=True)
     stream = torch.cuda.current_stream()
+
+    def mark(evs, i):
+        if evs is not None:
+            evs[i].record(stream)
+
+    if args.workload == "hetero-20M":
+        F = g.F
+        rels = [(g.rel_src_type[r], g.rel_dst_type[r], torch.from_numpy(g.rel_src[r]).to(dev),
+                 torch.from_numpy(g.rel_dst[r]).to(dev)) for r in range(len(g.rel_src))]
+        xs = [torch.from_numpy(x.view(np.int16)).to(dev).view(torch.bfloat16) for x in g.x_bf16]
+        dts = sorted(set(g.rel_dst_type))
+        b_csr, b_sum, ef = hetero_bytes(g, F)
+        ops = [("hetero_build", b_csr, 0), ("plan", sum(plan_bytes(g.n_per_type[t]) for t in dts), 0),
+               ("hetero_sum_bf16", b_sum, ef)]
+        state = {}
+        outs = {t: torch.empty(g.n_per_type[t], F, dtype=torch.float32, device=dev) for t in dts}
+
+        def step(evs=None):
+            mark(evs, 0)
+            for t in dts:
+                state[t] = mp.hetero_build(g.n_per_type, rels, t)
+            mark(evs, 1)
+            plans = {t: mp.Plan(state[t][0], int(state[t][1].numel()), F, torch.bfloat16)
+                     for t in dts}
+            mark(evs, 2)
+            for t in dts:
+                mp.hetero_spmm(g.n_per_type, xs, t, state[t][0], state[t][1], plan=plans[t],
+                               out=outs[t])
+            mark(evs, 3)
+        g.n_dst, g.E = sum(g.n_per_type), sum(a.shape[0] for a in g.rel_src)
+        return g, step, ops
+
+    N, E, F = g.n_dst, g.E, g.F
     src = torch.from_numpy(g.src).to(dev)
     dst = torch.from_numpy(g.dst).to(dev)
     web = args.workload == "web-1.6B"
     it = mp.MP_I64 if web else mp.MP_I32
     rp_b = 8 if web else 4
+    weighted = g.w is not None
     rowptr = torch.empty(N + 1, dtype=torch.int64 if web else torch.int32, device=dev)
     col = torch.empty(E, dtype=torch.int32, device=dev)
-    ws_csr = torch.empty(mp.mp_coo_to_csr_workspace(E, N, it, 0), dtype=torch.uint8, device=dev)
+    perm = torch.empty(E, dtype=torch.int32, device=dev) if weighted else None
+    w_coo = torch.from_numpy(g.w).to(dev) if weighted else None
+    w_csr = torch.empty(E, dtype=torch.float32, device=dev) if weighted else None
+    ws_csr = torch.empty(mp.mp_coo_to_csr_workspace(E, N, it, int(weighted)), dtype=torch.uint8,
+                         device=dev)
     nplan = mp.mp_spmm_plan_size(N, E)
     xs = {}
     if g.x is not None:
         xs["f32"] = (torch.from_numpy(g.x).to(dev), mp.MP_F32, 4)
-    if g.x_bf16 is not None:
+    if g.x_bf16 is not None and args.workload in (WORKLOAD, "web-1.6B"):
         xs["bf16"] = (torch.from_numpy(g.x_bf16.view(np.int16)).to(dev).view(torch.bfloat16),
                       mp.MP_BF16, 2)
     plan_bufs = {k: torch.empty(nplan, dtype=torch.uint8, device=dev) for k in xs}
@@ -126,38 +177,40 @@ def build_step(args, mp, torch, np, dev):
                          device=dev) for k in xs}
     arg = torch.empty(N, F, dtype=torch.int32, device=dev)
 
-    ops = [("csr", csr_bytes(N, E, rowptr_b=rp_b), 0),
-           ("plan", len(xs) * plan_bytes(N), 0)]
+    csr_b = csr_bytes(N, E, rowptr_b=rp_b, perm=weighted) + (8 * E if weighted else 0)
+    ops = [("csr", csr_b, 0), ("plan", len(xs) * plan_bytes(N), 0)]
     if web:
-        reds = [("sum+max", mp.MP_SUM | mp.MP_MAX)]
+        reds = [("sum+max", mp.MP_SUM | mp.MP_MAX, False)]
+    elif args.workload == "powerlaw-1.2M":
+        reds = [("mean", mp.MP_MEAN, False), ("wsum", mp.MP_SUM, True)]
+    elif args.workload == "uniform-10k":
+        reds = [("sum", mp.MP_SUM, False)]
     else:
-        reds = [("sum", mp.MP_SUM), ("mean", mp.MP_MEAN), ("max", mp.MP_MAX)]
+        reds = [("sum", mp.MP_SUM, False), ("mean", mp.MP_MEAN, False), ("max", mp.MP_MAX, False)]
     calls = []
     for k, (x, xd, xb) in xs.items():
-        for rn, red in reds:
+        for rn, red, wt in reds:
             mb = 4 if k == "f32" else 2
-            ops.append((f"{rn}_{k}", spmm_bytes(N, E, F, xb, red, max_b=mb, rowptr_b=rp_b), E * F))
-            calls.append((k, x, xd, red))
+            ops.append((f"{rn}_{k}", spmm_bytes(N, E, F, xb, red, max_b=mb, rowptr_b=rp_b, w=wt),
+                        E * F))
+            calls.append((k, x, xd, red, wt))
 
     plans = {}
     wss = {}
 
     def step(evs=None):
-        def mark(i):
-            if evs is not None:
-                evs[i].record(stream)
-        mark(0)
-        mp.mp_coo_to_csr(src, dst, E, N, rowptr, it, col, None, None, None, ws_csr,
+        mark(evs, 0)
+        mp.mp_coo_to_csr(src, dst, E, N, rowptr, it, col, perm, w_coo, w_csr, ws_csr,
                          ws_csr.numel())
-        mark(1)
+        mark(evs, 1)
         # one plan per feature dtype (a plan is checked against x's dtype)
         for k, (x, xd, xb) in xs.items():
             if k in plans:
                 mp.mp_spmm_plan_free(plans[k])
             plans[k] = mp.mp_spmm_plan_build(rowptr, it, N, E, F, xd, plan_bufs[k], nplan)
-        mark(2)
+        mark(evs, 2)
         i = 2
-        for k, x, xd, red in calls:
+        for k, x, xd, red, wt in calls:
             h = plans[k]
             nb = mp.mp_spmm_workspace(h, red)
             key = (k, red)
@@ -165,11 +218,11 @@ def build_step(args, mp, torch, np, dev):
                 wss[key] = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
             hs = bool(red & (mp.MP_SUM | mp.MP_MEAN))
             hm = bool(red & mp.MP_MAX)
-            mp.mp_spmm(h, rowptr, it, col, None, x, xd, N, N, F, red, out if hs else None,
-                       mp.MP_F32, mx[k] if hm else None, xd, arg if hm else None, wss[key],
-                       wss[key].numel())
+            mp.mp_spmm(h, rowptr, it, col, w_csr if wt else None, x, xd, N, N, F, red,
+                       out if hs else None, mp.MP_F32, mx[k] if hm else None, xd,
+                       arg if hm else None, wss[key], wss[key].numel())
             i += 1
-            mark(i)
+            mark(evs, i)
 
     return g, step, ops
 
@@ -221,20 +274,31 @@ def run(args):
                  for n in names}
     value = step_bytes / (ms_step * 1e-3) / 1e9
     web = args.workload == "web-1.6B"
-    dom = "sum+max_bf16" if web else "sum_f32"
-    dom_kernel = ("spmm_main<unsigned short, 8, true, true, false, false>, bf16 fused sum+max"
-                  if web else DOMINANT + ", fp32 sum")
+    headline = args.workload == WORKLOAD
+    dom = max((o for o in ops if o[2] > 0), key=lambda o: op_ms[o[0]])[0]
+    dom_kernel = DOMINANT + ", fp32 sum" if headline else f"spmm_main ({dom})"
+    if headline:
+        dom = "sum_f32"
     dom_ms, dom_bytes = op_ms[dom], op_bytes[dom]
     achieved = dom_bytes / (dom_ms * 1e-3) / 1e9
-    traffic = None if web else read_traffic()
-    if web:
-        desc = (f"{args.workload}: power-law in-degree (alpha 2.0), uniform sources, N={N}, "
-                f"E={E}, F={F}, bf16 features U(-1,1), int64 rowptr, seed {args.seed}")
-        stepdesc = "COO->CSR + plan + fused {sum fp32, max bf16 + argmax}"
-    else:
-        desc = (f"{args.workload}: Chung-Lu power-law graph, N={N}, E={E}, F={F}, "
-                f"features fp32 and bf16 (N(0,1)), seed {args.seed}")
-        stepdesc = "COO->CSR + plan + {sum, mean, max+argmax} x {fp32, bf16 features}"
+    traffic = read_traffic() if headline else None
+    descs = {
+        WORKLOAD: (f"{WORKLOAD}: Chung-Lu power-law graph, N={N}, E={E}, F={F}, features fp32 "
+                   f"and bf16 (N(0,1)), seed {args.seed}",
+                   "COO->CSR + plan + {sum, mean, max+argmax} x {fp32, bf16 features}"),
+        "web-1.6B": (f"web-1.6B: power-law in-degree (alpha 2.0), uniform sources, N={N}, E={E}, "
+                     f"F={F}, bf16 features U(-1,1), int64 rowptr, seed {args.seed}",
+                     "COO->CSR + plan + fused {sum fp32, max bf16 + argmax}"),
+        "powerlaw-1.2M": (f"powerlaw-1.2M: Zipf-like in-degree (alpha 2.1), uniform sources, "
+                          f"N={N}, E={E}, F={F}, fp32 N(0,1), GCN weights, seed {args.seed}",
+                          "COO->CSR (+perm, weights to CSR order) + plan + mean + weighted sum"),
+        "uniform-10k": (f"uniform-10k: uniform random graph, N={N}, E={E}, F={F}, fp32 U(-1,1), "
+                        f"seed {args.seed}", "COO->CSR + plan + sum"),
+        "hetero-20M": (f"hetero-20M: 3 node types (1.9M, 736k, 8.7k), 4 relations (5.4M, 7.1M, "
+                       f"7.1M, 1.0M edges), F={F} bf16, seed {args.seed}",
+                       "per destination type: combined CSR + plan + sum over relations"),
+    }
+    desc, stepdesc = descs[args.workload]
     result = {
         "metric": METRIC,
         "value": round(value, 2),
@@ -265,7 +329,7 @@ def run(args):
             "avg_launch_ms": round(dom_ms, 4),
         },
     }
-    if args.cpu_baseline and not web:
+    if args.cpu_baseline and headline:
         result["cpu_baseline"] = cpu_baseline(g, N, E, F, step_bytes, args)
     print(json.dumps(result), flush=True)
 
@@ -379,8 +443,8 @@ def summarize_counters(fetch_dir, write_dir, out, cmd):
     w_b = sum(dom_w) / len(dom_w) * 1024.0 * scale_w
     lines = [
         "# HBM traffic of the dominant kernel from rocprofv3 counters",
-        f"command_fetch: {cmd} (pass 1: --pmc FETCH_SIZE)",
-        f"command_write: {cmd} (pass 2: --pmc WRITE_SIZE)",
+        f"command_fetch: {cmd.format(ctr='FETCH_SIZE')}",
+        f"command_write: {cmd.format(ctr='WRITE_SIZE')}",
         f"kernel: {DOMINANT}",
         f"launches: {len(dom_f)}",
         f"fetch_kib_per_launch_raw: {sum(dom_f) / len(dom_f):.1f}",
@@ -405,7 +469,8 @@ def main():
     ap.add_argument("--steps", type=int, default=10)
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--seed", type=int, default=0)
-    ap.add_argument("--workload", default=WORKLOAD, choices=[WORKLOAD, "web-1.6B"],
+    ap.add_argument("--workload", default=WORKLOAD,
+                    choices=[WORKLOAD, "web-1.6B", "powerlaw-1.2M", "uniform-10k", "hetero-20M"],
                     help="benchmark workload (the default is the metric's configuration)")
     ap.add_argument("--cpu-rows", type=int, default=200_000,
                     help="rows of the CPU-oracle aggregation sample")
@@ -414,7 +479,8 @@ def main():
                     help="run one plain 1 GiB copy after warm-up (counter scaling)")
     ap.add_argument("--summarize-stats", nargs=2, metavar=("DIR", "OUT"))
     ap.add_argument("--summarize-counters", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "OUT"))
-    ap.add_argument("--cmd", default="", help="command line recorded in a summary")
+    ap.add_argument("--cmd", default="", help="command line recorded in a summary ({ctr} is "
+                    "replaced by the counter name in counter summaries)")
     args = ap.parse_args()
     if args.summarize_stats:
         summarize_stats(*args.summarize_stats, args.cmd)

@@ -280,7 +280,10 @@ class Plan:
     def __del__(self):
         h = getattr(self, "handle", None)
         if h:
-            mp_spmm_plan_free(h)
+            try:
+                mp_spmm_plan_free(h)
+            except Exception:  # interpreter shutdown: module globals already gone
+                pass
             self.handle = None
 
 

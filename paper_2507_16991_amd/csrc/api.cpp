@@ -53,8 +53,7 @@ struct CsrLayout {
     int passes, digit;
     uint32_t *kA, *kB;
     int32_t *src_tmp, *eid_tmp, *eid_final;
-    uint32_t* counts;
-    void* scan_ws;
+    RadixScratch sc;
     size_t bytes;
 };
 
@@ -68,9 +67,8 @@ CsrLayout csr_layout(void* ws, int64_t E, int64_t N, int with_payload) {
     L.src_tmp = L.passes > 1 ? c.take<int32_t>(e) : nullptr;
     L.eid_tmp = (with_payload && L.passes > 1) ? c.take<int32_t>(e) : nullptr;
     L.eid_final = with_payload ? c.take<int32_t>(e) : nullptr;
-    L.counts = reinterpret_cast<uint32_t*>(c.take<char>(radix_pass_counts_bytes(E, L.digit)));
-    const int64_t tiles = ceil_div(E > 0 ? E : 1, kSortTile);
-    L.scan_ws = c.take<char>(scan_workspace_bytes(tiles << L.digit));
+    char* scratch = c.take<char>(radix_scratch_bytes(E));
+    if (ws) L.sc = radix_scratch(scratch, E);
     L.bytes = c.off;
     return L;
 }
@@ -91,6 +89,7 @@ int coo_to_csr_impl(const int32_t* src, const int32_t* dst, int64_t E, int64_t N
     int32_t* eid_final = perm ? perm : L.eid_final;
 
     const uint32_t* keys_in = reinterpret_cast<const uint32_t*>(dst);
+    if (radix_sort_begin(keys_in, E, L.passes, L.digit, L.sc, s) != hipSuccess) return MP_ERR_HIP;
     const int32_t* a_in = src;
     const int32_t* b_in = nullptr;  // COO id = element index in the first pass
     for (int p = 0; p < L.passes; ++p) {
@@ -103,12 +102,11 @@ int coo_to_csr_impl(const int32_t* src, const int32_t* dst, int64_t E, int64_t N
         rp.a_out = last_parity ? col : L.src_tmp;
         rp.b_out = payload ? (last_parity ? eid_final : L.eid_tmp) : nullptr;
         rp.n = E;
+        rp.pass = p;
         rp.shift = p * L.digit;
         rp.bits = L.digit;
-        rp.counts = L.counts;
-        rp.scan_ws = L.scan_ws;
-        hipError_t e = radix_pass(rp, s);
-        if (e != hipSuccess) return MP_ERR_HIP;
+        rp.sc = L.sc;
+        if (radix_sort_pass(rp, s) != hipSuccess) return MP_ERR_HIP;
         keys_in = rp.keys_out;
         a_in = rp.a_out;
         b_in = rp.b_out;
@@ -128,7 +126,7 @@ struct PlanLayout {
     uint32_t* keys;
     int32_t* rowlist;
     uint32_t* chunk_off;
-    uint32_t* counts;
+    RadixScratch sc;
     void* scan_ws;
     uint32_t* header;
     size_t bytes;
@@ -141,11 +139,9 @@ PlanLayout plan_layout(void* buf, int64_t N) {
     L.keys = c.take<uint32_t>(n);
     L.rowlist = c.take<int32_t>(n);
     L.chunk_off = c.take<uint32_t>(n + 1);
-    L.counts = reinterpret_cast<uint32_t*>(c.take<char>(radix_pass_counts_bytes(N, kPlanClassBits)));
-    const int64_t tiles = ceil_div(N > 0 ? N : 1, kSortTile);
-    size_t sw = scan_workspace_bytes(tiles << kPlanClassBits);
-    size_t sw2 = scan_workspace_bytes(N + 1);
-    L.scan_ws = c.take<char>(sw > sw2 ? sw : sw2);
+    char* scratch = c.take<char>(radix_scratch_bytes(N));
+    if (buf) L.sc = radix_scratch(scratch, N);
+    L.scan_ws = c.take<char>(scan_workspace_bytes(N + 1));
     L.header = c.take<uint32_t>(64);
     L.bytes = c.off;
     return L;
@@ -294,7 +290,9 @@ int mp_spmm_plan_build(const void* rowptr, int rowptr_itype, int64_t N_dst, int6
     p->E = E;
     p->F = F;
     p->x_dtype = x_dtype;
-    p->small_max = env_int("MP_SMALL_MAX", 32);
+    // rows of up to 16 edges per slot get one slot; longer rows a wavefront
+    const Geometry geo = make_geometry(F, x_dtype, 16);
+    p->small_max = env_int("MP_SMALL_MAX", 16 * (int64_t)geo.S);
     if (p->small_max > 16383) p->small_max = 16383;
     p->hub_min = env_int("MP_HUB_MIN", 4096);
     if (p->hub_min < p->small_max) p->hub_min = p->small_max;
@@ -306,16 +304,17 @@ int mp_spmm_plan_build(const void* rowptr, int rowptr_itype, int64_t N_dst, int6
         return MP_OK;
     }
     hipError_t e = launch_plan_classes(rowptr, rp64, N_dst, p->small_max, p->hub_min, L.keys, s);
+    if (e == hipSuccess) e = radix_sort_begin(L.keys, N_dst, 1, kPlanClassBits, L.sc, s);
     if (e == hipSuccess) {
         RadixPass rp{};
         rp.keys_in = L.keys;
         rp.a_out = L.rowlist;  // payload = row id
         rp.n = N_dst;
+        rp.pass = 0;
         rp.shift = 0;
         rp.bits = kPlanClassBits;
-        rp.counts = L.counts;
-        rp.scan_ws = L.scan_ws;
-        e = radix_pass(rp, s);
+        rp.sc = L.sc;
+        e = radix_sort_pass(rp, s);
     }
     if (e == hipSuccess)
         e = launch_plan_chunks(rowptr, rp64, L.rowlist, N_dst, p->hub_min, p->chunk_min,
@@ -323,8 +322,7 @@ int mp_spmm_plan_build(const void* rowptr, int rowptr_itype, int64_t N_dst, int6
     if (e == hipSuccess) e = exclusive_scan_u32(L.chunk_off, N_dst + 1, L.scan_ws, s);
     const int nclass = kClassHub + 1;
     if (e == hipSuccess)
-        e = launch_plan_header(L.counts, ceil_div(N_dst, kSortTile), nclass, L.chunk_off, N_dst,
-                               L.header, s);
+        e = launch_plan_header(L.sc.gbase, nclass, L.chunk_off, N_dst, L.header, s);
     uint32_t h[64] = {0};
     if (e == hipSuccess)
         e = hipMemcpyAsync(h, L.header, sizeof(uint32_t) * (nclass + 2), hipMemcpyDeviceToHost, s);

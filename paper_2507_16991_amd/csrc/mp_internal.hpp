@@ -48,7 +48,23 @@ size_t scan_workspace_bytes(int64_t n);
 // In-place exclusive scan of data[0..n); returns the hipError of the launches.
 hipError_t exclusive_scan_u32(uint32_t* data, int64_t n, void* ws, hipStream_t s);
 
-// ---- one stable radix pass (sort.hip) --------------------------------------
+// ---- stable LSD radix sort, one sweep per digit (sort.hip) ----------------
+//
+// radix_sort_begin() computes the global digit histogram of every pass in one
+// read of the keys (and clears the look-back descriptors); then each
+// radix_sort_pass() ranks, offsets and scatters in a single kernel, getting
+// the offsets of earlier tiles by decoupled look-back.
+constexpr int kMaxPasses = 4;  // 32-bit keys, digits of at most 8 bits
+
+struct RadixScratch {
+    uint64_t* desc;     // [tiles * 256] look-back descriptors
+    uint32_t* gbase;    // [kMaxPasses * 256] global digit histogram -> exclusive starts
+    uint32_t* counter;  // [kMaxPasses] dynamic tile ids
+    uint32_t* err;      // look-back wait limit exceeded (debug)
+};
+size_t radix_scratch_bytes(int64_t n);
+RadixScratch radix_scratch(void* base, int64_t n);
+
 struct RadixPass {
     const uint32_t* keys_in;  // [n]
     const int32_t* a_in;      // [n] or nullptr: payload a = element index
@@ -57,15 +73,12 @@ struct RadixPass {
     int32_t* a_out;           // [n] or nullptr
     int32_t* b_out;           // [n] or nullptr
     int64_t n;
-    int shift, bits;
-    uint32_t* counts;         // [2^bits * tiles] scratch
-    void* scan_ws;
+    int pass, shift, bits;
+    RadixScratch sc;
 };
-size_t radix_pass_counts_bytes(int64_t n, int bits);
-// Histogram + scan + stable scatter.  If digit_start != nullptr it receives
-// (device) nothing; callers read counts[d * tiles] after the pass for the
-// global start of digit d.
-hipError_t radix_pass(const RadixPass& p, hipStream_t s);
+hipError_t radix_sort_begin(const uint32_t* keys, int64_t n, int passes, int bits,
+                            const RadixScratch& sc, hipStream_t s);
+hipError_t radix_sort_pass(const RadixPass& p, hipStream_t s);
 
 hipError_t launch_rowptr_from_sorted(const uint32_t* keys, int64_t E, int64_t N, void* rowptr,
                                      int rp64, hipStream_t s);
@@ -102,15 +115,6 @@ constexpr int kClassHub = kSmallClasses + 1;
 constexpr int kPlanClassBits = 5;       // 32 buckets (18 used)
 constexpr int kMaxChunksPerHub = 2048;  // hub rows are split into <= this many chunks
 
-struct PlanDevice {
-    uint32_t* keys;       // [N] class of each row
-    int32_t* rowlist;     // [N] rows sorted by class, stable by row id
-    uint32_t* chunk_off;  // [N+1] exclusive prefix of chunks per rowlist entry
-    uint32_t* counts;     // radix counts scratch
-    void* scan_ws;
-    uint32_t* header;     // [64] class starts, chunk total
-};
-
 struct SpmmParams {
     const void* rowptr;
     int rp64;
@@ -146,8 +150,9 @@ hipError_t launch_plan_classes(const void* rowptr, int rp64, int64_t N, int64_t 
                                int64_t hub_min, uint32_t* keys, hipStream_t s);
 hipError_t launch_plan_chunks(const void* rowptr, int rp64, const int32_t* rowlist, int64_t N,
                               int64_t hub_min, int chunk_min, uint32_t* nch, hipStream_t s);
-hipError_t launch_plan_header(const uint32_t* counts, int64_t tiles, int nclass,
-                              const uint32_t* chunk_off, int64_t N, uint32_t* header,
-                              hipStream_t s);
+// header[c] = first rowlist position of class c (c < nclass, from the class
+// sort's exclusive digit starts), header[nclass] = N, header[nclass+1] = chunks
+hipError_t launch_plan_header(const uint32_t* class_start, int nclass, const uint32_t* chunk_off,
+                              int64_t N, uint32_t* header, hipStream_t s);
 
 }  // namespace mp

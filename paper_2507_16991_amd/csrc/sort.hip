@@ -12,10 +12,6 @@
 // arithmetic: the result is bit-exact.
 #include "mp_internal.hpp"
 
-#ifndef MP_SORT_NT_STORE
-#define MP_SORT_NT_STORE 0
-#endif
-
 namespace mp {
 namespace {
 
@@ -23,45 +19,122 @@ constexpr int kSortWaves = kSortBlock / kWave;
 constexpr int kWaveKeys = kWave * kSortItems;  // keys per wavefront per tile
 constexpr int kMaxBuckets = 1 << kSortMaxBits;
 
-__global__ __launch_bounds__(kSortBlock) void radix_hist(const uint32_t* __restrict__ keys,
-                                                         int64_t n, int shift, int bits,
-                                                         uint32_t* __restrict__ counts,
-                                                         int64_t tiles) {
-    __shared__ uint32_t h[kMaxBuckets];
-    const int R = 1 << bits;
-    for (int i = threadIdx.x; i < R; i += kSortBlock) h[i] = 0;
-    __syncthreads();
-    const int64_t base = (int64_t)blockIdx.x * kSortTile;
-#pragma unroll 4
-    for (int k = 0; k < kSortItems; ++k) {
-        int64_t i = base + (int64_t)k * kSortBlock + threadIdx.x;
-        if (i < n) atomicAdd(&h[(keys[i] >> shift) & (R - 1)], 1u);
-    }
-    __syncthreads();
-    for (int d = threadIdx.x; d < R; d += kSortBlock) counts[(int64_t)d * tiles + blockIdx.x] = h[d];
+constexpr int kGhistBlock = 256;
+constexpr int kGhistItems = 8;
+constexpr uint32_t kSpinLimit = 1u << 20;
+
+// look-back descriptor: flag (bits 63..62: 1 tile count, 2 inclusive prefix),
+// pass tag (bits 61..56, pass + 1), value (bits 55..0)
+constexpr uint64_t kFlagAgg = 1ull << 62;
+constexpr uint64_t kFlagPre = 2ull << 62;
+__device__ inline uint64_t desc_make(uint64_t flag, uint32_t tag, uint64_t v) {
+    return flag | ((uint64_t)tag << 56) | v;
 }
 
-// HAS_B: the second payload is carried (it costs 16 KB of LDS per tile, so
-// the payload-free variant fits one more workgroup per CU).
+// Lanes of the wavefront that hold a valid key with the same digit as this
+// lane (one ballot per digit bit).
+__device__ inline uint64_t digit_peers(bool ok, uint32_t d, int bits) {
+    uint64_t peers = __ballot(ok);
+    for (int b = 0; b < bits; ++b) {
+        const bool bit = (d >> b) & 1u;
+        const uint64_t bal = __ballot(bit);
+        peers &= bit ? bal : ~bal;
+    }
+    return peers;
+}
+
+__global__ __launch_bounds__(256) void radix_clear(uint64_t* __restrict__ desc, int64_t ndesc,
+                                                   uint32_t* __restrict__ gbase,
+                                                   uint32_t* __restrict__ counter,
+                                                   uint32_t* __restrict__ err) {
+    const int64_t i0 = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    for (int64_t i = i0; i < ndesc; i += (int64_t)gridDim.x * 256) desc[i] = 0;
+    if (i0 < kMaxPasses * 256) gbase[i0] = 0;
+    if (i0 < kMaxPasses) counter[i0] = 0;
+    if (i0 == 0) *err = 0;
+}
+
+// Global histogram of every pass's digit: per-wave private LDS counters, one
+// update per distinct digit per 64 keys (the lowest lane of each digit group
+// adds the group size), then one integer atomic per (pass, digit) per block.
+__global__ __launch_bounds__(kGhistBlock) void radix_ghist(const uint32_t* __restrict__ keys,
+                                                           int64_t n, int passes, int bits,
+                                                           uint32_t* __restrict__ ghist) {
+    constexpr int W = kGhistBlock / kWave;
+    __shared__ uint32_t h[W][kMaxPasses][kMaxBuckets];
+    for (int i = threadIdx.x; i < W * kMaxPasses * kMaxBuckets; i += kGhistBlock)
+        (&h[0][0][0])[i] = 0;
+    __syncthreads();
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wv = threadIdx.x / kWave;
+    const uint32_t mask = (1u << bits) - 1u;
+    const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
+    const int64_t stride = (int64_t)gridDim.x * W * kWave * kGhistItems;
+    for (int64_t base = ((int64_t)blockIdx.x * W + wv) * kWave * kGhistItems; base < n;
+         base += stride) {
+        uint32_t key[kGhistItems];
+#pragma unroll
+        for (int k = 0; k < kGhistItems; ++k) {
+            const int64_t i = base + (int64_t)k * kWave + lane;
+            key[k] = i < n ? __builtin_nontemporal_load(keys + i) : 0u;
+        }
+#pragma unroll
+        for (int k = 0; k < kGhistItems; ++k) {
+            const bool ok = base + (int64_t)k * kWave + lane < n;
+            for (int p = 0; p < passes; ++p) {
+                const uint32_t d = (key[k] >> (p * bits)) & mask;
+                const uint64_t peers = digit_peers(ok, d, bits);
+                if (ok && (peers & lt_mask) == 0) h[wv][p][d] += (uint32_t)__popcll(peers);
+            }
+        }
+    }
+    __syncthreads();
+    for (int i = threadIdx.x; i < passes * kMaxBuckets; i += kGhistBlock) {
+        uint32_t t = 0;
+#pragma unroll
+        for (int w = 0; w < W; ++w) t += (&h[w][0][0])[i];
+        if (t) atomicAdd(&ghist[i], t);
+    }
+}
+
+// In place: per pass, exclusive scan over the 2^bits digit counts.
+__global__ void radix_gscan(uint32_t* __restrict__ g, int passes, int bits) {
+    const int p = threadIdx.x;
+    if (p >= passes) return;
+    uint32_t run = 0;
+    for (int d = 0; d < (1 << bits); ++d) {
+        const uint32_t c = g[p * kMaxBuckets + d];
+        g[p * kMaxBuckets + d] = run;
+        run += c;
+    }
+}
+
+// One LSD pass: rank the tile's keys stably (wave-level multisplit, per-wave
+// LDS counters), publish the tile's digit counts, look back over earlier tiles
+// for their running totals, stage the tile in LDS in digit order and write
+// every digit run contiguously.  Ranks follow (wave, round, lane) order,
+// which is element order, and tiles are numbered in the order they start, so
+// the pass is stable.  HAS_B: the second payload is carried.
 template <bool HAS_B>
-__global__ __launch_bounds__(kSortBlock) void radix_scatter(RadixPass p, int64_t tiles) {
+__global__ __launch_bounds__(kSortBlock) void radix_onesweep(RadixPass p) {
     __shared__ uint32_t s_key[kSortTile];
     __shared__ int32_t s_a[kSortTile];
     __shared__ int32_t s_b[HAS_B ? kSortTile : 1];
     __shared__ uint32_t s_cnt[kSortWaves][kMaxBuckets];
     __shared__ uint32_t s_start[kMaxBuckets];
     __shared__ uint32_t s_gbase[kMaxBuckets];
+    __shared__ uint32_t s_tile;
 
     const int R = 1 << p.bits;
     const int lane = threadIdx.x & (kWave - 1);
     const int wv = threadIdx.x / kWave;
     for (int i = threadIdx.x; i < kSortWaves * kMaxBuckets; i += kSortBlock)
         (&s_cnt[0][0])[i] = 0;
-    for (int d = threadIdx.x; d < R; d += kSortBlock)
-        s_gbase[d] = p.counts[(int64_t)d * tiles + blockIdx.x];
+    if (threadIdx.x == 0) s_tile = atomicAdd(&p.sc.counter[p.pass], 1u);
     __syncthreads();
+    const int64_t tile = s_tile;
 
-    const int64_t tbase = (int64_t)blockIdx.x * kSortTile;
+    const int64_t tbase = tile * kSortTile;
     const int64_t wbase = tbase + (int64_t)wv * kWaveKeys;
     const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
 
@@ -78,16 +151,9 @@ __global__ __launch_bounds__(kSortBlock) void radix_scatter(RadixPass p, int64_t
     }
 #pragma unroll
     for (int k = 0; k < kSortItems; ++k) {
-        const int64_t i = wbase + (int64_t)k * kWave + lane;
-        const bool ok = i < p.n;
+        const bool ok = wbase + (int64_t)k * kWave + lane < p.n;
         const uint32_t d = (key[k] >> p.shift) & (uint32_t)(R - 1);
-        // lanes holding a valid key with the same digit
-        uint64_t peers = __ballot(ok);
-        for (int b = 0; b < p.bits; ++b) {
-            const bool bit = (d >> b) & 1u;
-            const uint64_t bal = __ballot(bit);
-            peers &= bit ? bal : ~bal;
-        }
+        const uint64_t peers = digit_peers(ok, d, p.bits);
         const uint32_t below = (uint32_t)__popcll(peers & lt_mask);
         const uint32_t base = s_cnt[wv][d];
         rank[k] = base + below;
@@ -97,7 +163,7 @@ __global__ __launch_bounds__(kSortBlock) void radix_scatter(RadixPass p, int64_t
     }
     __syncthreads();
 
-    // per digit: start of each wave's run inside the digit, tile total
+    // per digit: each wave's run start inside the digit, and the tile count
     for (int d = threadIdx.x; d < R; d += kSortBlock) {
         uint32_t run = 0;
 #pragma unroll
@@ -109,7 +175,45 @@ __global__ __launch_bounds__(kSortBlock) void radix_scatter(RadixPass p, int64_t
         s_start[d] = run;
     }
     __syncthreads();
-    // exclusive scan of the digit totals (R <= 256) by wavefront 0
+
+    // decoupled look-back, one thread per digit: publish this tile's count,
+    // add up earlier tiles' counts until one that carries an inclusive prefix
+    const uint32_t tag = (uint32_t)p.pass + 1u;
+    if (threadIdx.x < R) {
+        const int d = threadIdx.x;
+        const uint64_t cnt = s_start[d];
+        uint64_t* col = p.sc.desc + d;
+        uint64_t excl = 0;
+        if (tile == 0) {
+            __hip_atomic_store(col, desc_make(kFlagPre, tag, cnt), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        } else {
+            __hip_atomic_store(col + tile * kMaxBuckets, desc_make(kFlagAgg, tag, cnt),
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            for (int64_t look = tile - 1; look >= 0; --look) {
+                uint64_t v = 0;
+                uint32_t spins = 0;
+                while (true) {
+                    v = __hip_atomic_load(col + look * kMaxBuckets, __ATOMIC_RELAXED,
+                                          __HIP_MEMORY_SCOPE_AGENT);
+                    if ((uint32_t)((v >> 56) & 63u) == tag && (v >> 62) != 0) break;
+                    if (++spins > kSpinLimit) {  // bounded: never hang; flag it instead
+                        atomicOr(p.sc.err, 1u);
+                        v = desc_make(kFlagPre, tag, 0);
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(1);
+                }
+                excl += v & ((1ull << 56) - 1);
+                if ((v >> 62) == 2) break;
+            }
+            __hip_atomic_store(col + tile * kMaxBuckets, desc_make(kFlagPre, tag, excl + cnt),
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+        s_gbase[d] = p.sc.gbase[p.pass * kMaxBuckets + d] + (uint32_t)excl;
+    }
+    __syncthreads();
+    // exclusive scan of the tile's digit counts (R <= 256) by wavefront 0
     if (wv == 0) {
         uint32_t t[kMaxBuckets / kWave];
         uint32_t s = 0;
@@ -154,19 +258,11 @@ __global__ __launch_bounds__(kSortBlock) void radix_scatter(RadixPass p, int64_t
         const uint32_t d = (kk >> p.shift) & (uint32_t)(R - 1);
         const int64_t pos = (int64_t)s_gbase[d] + (i - (int64_t)s_start[d]);
         if (pos >= p.n) continue;  // cannot happen for consistent counts; never write past n
-#if MP_SORT_NT_STORE
-        if (p.keys_out) __builtin_nontemporal_store(kk, p.keys_out + pos);
-        if (p.a_out) __builtin_nontemporal_store(s_a[i], p.a_out + pos);
-        if constexpr (HAS_B) {
-            if (p.b_out) __builtin_nontemporal_store(s_b[i], p.b_out + pos);
-        }
-#else
         if (p.keys_out) p.keys_out[pos] = kk;
         if (p.a_out) p.a_out[pos] = s_a[i];
         if constexpr (HAS_B) {
             if (p.b_out) p.b_out[pos] = s_b[i];
         }
-#endif
     }
 }
 
@@ -249,24 +345,53 @@ inline unsigned grid_for(int64_t n, int per_block) {
 
 }  // namespace
 
-size_t radix_pass_counts_bytes(int64_t n, int bits) {
+size_t radix_scratch_bytes(int64_t n) {
     const int64_t tiles = ceil_div(n > 0 ? n : 1, kSortTile);
-    return align_up((size_t)tiles * ((size_t)1 << bits) * sizeof(uint32_t), 256);
+    return align_up((size_t)tiles * kMaxBuckets * sizeof(uint64_t), 256) +
+           align_up(kMaxPasses * kMaxBuckets * sizeof(uint32_t), 256) + 256 + 256;
 }
 
-hipError_t radix_pass(const RadixPass& p, hipStream_t s) {
+RadixScratch radix_scratch(void* base, int64_t n) {
+    const int64_t tiles = ceil_div(n > 0 ? n : 1, kSortTile);
+    char* b = static_cast<char*>(base);
+    RadixScratch sc;
+    sc.desc = reinterpret_cast<uint64_t*>(b);
+    b += align_up((size_t)tiles * kMaxBuckets * sizeof(uint64_t), 256);
+    sc.gbase = reinterpret_cast<uint32_t*>(b);
+    b += align_up(kMaxPasses * kMaxBuckets * sizeof(uint32_t), 256);
+    sc.counter = reinterpret_cast<uint32_t*>(b);
+    b += 256;
+    sc.err = reinterpret_cast<uint32_t*>(b);
+    return sc;
+}
+
+hipError_t radix_sort_begin(const uint32_t* keys, int64_t n, int passes, int bits,
+                            const RadixScratch& sc, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    const int64_t tiles = ceil_div(n, kSortTile);
+    const int64_t ndesc = tiles * kMaxBuckets;
+    unsigned g = grid_for(ndesc, 256);
+    if (g > 8192) g = 8192;
+    // every histogram word needs a thread, however few descriptors there are
+    if (g < (unsigned)ceil_div(kMaxPasses * kMaxBuckets, 256)) g = (unsigned)ceil_div(kMaxPasses * kMaxBuckets, 256);
+    hipLaunchKernelGGL(radix_clear, dim3(g), dim3(256), 0, s, sc.desc, ndesc, sc.gbase,
+                       sc.counter, sc.err);
+    const int64_t per_block = (int64_t)kGhistBlock * kGhistItems;
+    unsigned gh = grid_for(n, (int)per_block);
+    if (gh > 2048) gh = 2048;
+    hipLaunchKernelGGL(radix_ghist, dim3(gh), dim3(kGhistBlock), 0, s, keys, n, passes, bits,
+                       sc.gbase);
+    hipLaunchKernelGGL(radix_gscan, dim3(1), dim3(kWave), 0, s, sc.gbase, passes, bits);
+    return hipGetLastError();
+}
+
+hipError_t radix_sort_pass(const RadixPass& p, hipStream_t s) {
     if (p.n <= 0) return hipSuccess;
     const int64_t tiles = ceil_div(p.n, kSortTile);
-    hipLaunchKernelGGL(radix_hist, dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p.keys_in, p.n,
-                       p.shift, p.bits, p.counts, tiles);
-    hipError_t e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    e = exclusive_scan_u32(p.counts, tiles << p.bits, p.scan_ws, s);
-    if (e != hipSuccess) return e;
     if (p.b_out)
-        hipLaunchKernelGGL(radix_scatter<true>, dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p, tiles);
+        hipLaunchKernelGGL(radix_onesweep<true>, dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p);
     else
-        hipLaunchKernelGGL(radix_scatter<false>, dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p, tiles);
+        hipLaunchKernelGGL(radix_onesweep<false>, dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p);
     return hipGetLastError();
 }
 

@@ -120,7 +120,8 @@ struct Acc {
 #pragma unroll
             for (int k = 0; k < EPL; ++k) {
                 if constexpr (HS) s[a][k] = 0.f;
-                if constexpr (HM) { m[a][k] = 0.f; i[a][k] = -1; }
+                // -inf: the first (finite) message always replaces it
+                if constexpr (HM) { m[a][k] = -__builtin_huge_valf(); i[a][k] = -1; }
             }
     }
     // message values v (already weighted) of CSR position pos
@@ -129,7 +130,7 @@ struct Acc {
         for (int k = 0; k < EPL; ++k) {
             if constexpr (HS) s[a][k] += v[k];
             if constexpr (HM) {
-                const bool take = (i[a][k] < 0) || (v[k] > m[a][k]);
+                const bool take = v[k] > m[a][k];
                 m[a][k] = take ? v[k] : m[a][k];
                 i[a][k] = take ? pos : i[a][k];
             }
@@ -555,11 +556,11 @@ __global__ __launch_bounds__(256) void plan_chunks(const void* rowptr, int rp64,
 
 // header[c] = start of class c in rowlist (c < nclass), header[nclass] = N,
 // header[nclass + 1] = total hub chunks
-__global__ void plan_header(const uint32_t* __restrict__ counts, int64_t tiles, int nclass,
+__global__ void plan_header(const uint32_t* __restrict__ class_start, int nclass,
                             const uint32_t* __restrict__ chunk_off, int64_t N,
                             uint32_t* __restrict__ header) {
     const int c = threadIdx.x;
-    if (c < nclass) header[c] = counts[(int64_t)c * tiles];
+    if (c < nclass) header[c] = class_start[c];
     if (c == 0) {
         header[nclass] = (uint32_t)N;
         header[nclass + 1] = chunk_off[N];
@@ -657,10 +658,9 @@ hipError_t launch_plan_chunks(const void* rowptr, int rp64, const int32_t* rowli
     return hipGetLastError();
 }
 
-hipError_t launch_plan_header(const uint32_t* counts, int64_t tiles, int nclass,
-                              const uint32_t* chunk_off, int64_t N, uint32_t* header,
-                              hipStream_t s) {
-    hipLaunchKernelGGL(plan_header, dim3(1), dim3(64), 0, s, counts, tiles, nclass, chunk_off, N,
+hipError_t launch_plan_header(const uint32_t* class_start, int nclass, const uint32_t* chunk_off,
+                              int64_t N, uint32_t* header, hipStream_t s) {
+    hipLaunchKernelGGL(plan_header, dim3(1), dim3(64), 0, s, class_start, nclass, chunk_off, N,
                        header);
     return hipGetLastError();
 }
