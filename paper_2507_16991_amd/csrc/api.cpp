@@ -125,6 +125,8 @@ int coo_to_csr_impl(const int32_t* src, const int32_t* dst, int64_t E, int64_t N
 struct PlanLayout {
     uint32_t* keys;
     int32_t* rowlist;
+    int32_t* rowbeg;
+    int32_t* rowend;
     uint32_t* chunk_off;
     RadixScratch sc;
     void* scan_ws;
@@ -138,6 +140,8 @@ PlanLayout plan_layout(void* buf, int64_t N) {
     const size_t n = (size_t)(N > 0 ? N : 1);
     L.keys = c.take<uint32_t>(n);
     L.rowlist = c.take<int32_t>(n);
+    L.rowbeg = c.take<int32_t>(n);
+    L.rowend = c.take<int32_t>(n);
     L.chunk_off = c.take<uint32_t>(n + 1);
     char* scratch = c.take<char>(radix_scratch_bytes(N));
     if (buf) L.sc = radix_scratch(scratch, N);
@@ -156,9 +160,11 @@ struct mp_plan {
     int x_dtype;
     int64_t small_max, hub_min;
     int chunk_min;
-    int64_t n_small, n_mid, n_hub, n_chunks;
+    int64_t n_tiny, n_small, n_mid, n_hub, n_chunks;
     int64_t mid_base, hub_base;
     int32_t* rowlist;
+    int32_t* rowbeg;
+    int32_t* rowend;
     uint32_t* chunk_off;
 };
 
@@ -174,18 +180,23 @@ int run_spmm(const mp_plan* plan, SpmmParams& P, const Geometry& g, int x_dtype,
     P.ltot = g.ltot;
     const bool hs = (P.reduce & (MP_SUM | MP_MEAN)) != 0;
     const bool hm = (P.reduce & MP_MAX) != 0;
+    const bool tiny = plan && plan->n_tiny > 0 && g.L > kTinyDeg;
     if (plan) {
         P.rowlist = plan->rowlist;
+        P.rowbeg = plan->rowbeg;
+        P.rowend = plan->rowend;
         P.chunk_off = plan->chunk_off;
         P.chunk_min = plan->chunk_min;
-        P.n_small = plan->n_small;
+        // tiny rows go to their own kernel when slots are wide enough
+        P.n_tiny = tiny ? plan->n_tiny : 0;
+        P.small_base = P.n_tiny;
+        P.n_small = plan->n_small - P.n_tiny;
         P.n_hub = plan->n_hub;
-        P.small_base = 0;
         P.mid_base = plan->mid_base;
         P.hub_base = plan->hub_base;
         P.n_hub_waves = plan->n_chunks * g.FT;
         P.n_mid_waves = plan->n_mid * g.FT;
-        P.n_small_waves = ceil_div(plan->n_small, g.S) * g.FT;
+        P.n_small_waves = ceil_div(P.n_small, g.S) * g.FT;
         if (plan->n_chunks > 0) {
             Carver c(ws);
             const size_t cells = (size_t)plan->n_chunks * (size_t)P.F;
@@ -200,7 +211,9 @@ int run_spmm(const mp_plan* plan, SpmmParams& P, const Geometry& g, int x_dtype,
     }
     const int64_t waves = P.n_hub_waves + P.n_mid_waves + P.n_small_waves;
     if (ceil_div(waves, 4) > (int64_t)UINT32_MAX) return MP_ERR_SIZE;
-    hipError_t e = launch_spmm(P, x_dtype, g.epl, s);
+    hipError_t e = launch_spmm_tiny(P, x_dtype, g.epl, s);
+    if (e != hipSuccess) return MP_ERR_HIP;
+    e = launch_spmm(P, x_dtype, g.epl, s);
     if (e != hipSuccess) return MP_ERR_HIP;
     if (plan && plan->n_hub > 0) {
         e = launch_spmm_fixup(P, s);
@@ -294,10 +307,16 @@ int mp_spmm_plan_build(const void* rowptr, int rowptr_itype, int64_t N_dst, int6
     const Geometry geo = make_geometry(F, x_dtype, 16);
     p->small_max = env_int("MP_SMALL_MAX", 16 * (int64_t)geo.S);
     if (p->small_max > 16383) p->small_max = 16383;
-    p->hub_min = env_int("MP_HUB_MIN", 4096);
+    // a wavefront takes S * U edges per step; rows longer than 32 steps are
+    // split into chunks of at least 32 steps, so that no wavefront runs a
+    // long chain of dependent steps on its own
+    const int64_t step_edges = (int64_t)geo.S * (geo.S * 8 > 64 ? 64 / geo.S : 8);
+    p->hub_min = env_int("MP_HUB_MIN", 32 * step_edges);
     if (p->hub_min < p->small_max) p->hub_min = p->small_max;
-    p->chunk_min = (int)env_int("MP_CHUNK", 1024);
+    p->chunk_min = (int)env_int("MP_CHUNK", 32 * step_edges);
     p->rowlist = L.rowlist;
+    p->rowbeg = L.rowbeg;
+    p->rowend = L.rowend;
     p->chunk_off = L.chunk_off;
     if (N_dst == 0) {
         *out = p;
@@ -317,6 +336,8 @@ int mp_spmm_plan_build(const void* rowptr, int rowptr_itype, int64_t N_dst, int6
         e = radix_sort_pass(rp, s);
     }
     if (e == hipSuccess)
+        e = launch_plan_rowrange(rowptr, rp64, L.rowlist, N_dst, L.rowbeg, L.rowend, s);
+    if (e == hipSuccess)
         e = launch_plan_chunks(rowptr, rp64, L.rowlist, N_dst, p->hub_min, p->chunk_min,
                                L.chunk_off, s);
     if (e == hipSuccess) e = exclusive_scan_u32(L.chunk_off, N_dst + 1, L.scan_ws, s);
@@ -334,6 +355,8 @@ int mp_spmm_plan_build(const void* rowptr, int rowptr_itype, int64_t N_dst, int6
     p->mid_base = h[kClassMid];
     p->hub_base = h[kClassHub];
     p->n_small = p->mid_base;
+    // rows of classes below kTinyClassEnd have at most kTinyDeg edges
+    p->n_tiny = h[kTinyClassEnd] < (uint32_t)p->mid_base ? h[kTinyClassEnd] : p->mid_base;
     p->n_mid = p->hub_base - p->mid_base;
     p->n_hub = N_dst - p->hub_base;
     p->n_chunks = h[nclass + 1];
@@ -514,10 +537,18 @@ int mp_hetero_spmm(int n_types, const int64_t* N_per_type, const void* const* x_
     P.rp64 = rowptr_itype == MP_I64;
     P.col = col;
     P.w = nullptr;
-    P.n_tables = n_types;
+    // tables laid out back to back in one allocation (one typed feature
+    // tensor) are a single table indexed by global id
+    bool contiguous = true;
+    for (int t = 1; t < n_types; ++t)
+        if ((uintptr_t)x_per_type[t] != (uintptr_t)x_per_type[0] + (uintptr_t)(offs[t] * F * eb))
+            contiguous = false;
+    P.n_tables = contiguous ? 1 : n_types;
     for (int t = 0; t < n_types; ++t) {
         P.table_ptr[t] = static_cast<const char*>(x_per_type[t]);
         P.table_off[t] = offs[t];
+        P.voff[t] = ((int64_t)(uintptr_t)x_per_type[t] - (int64_t)(uintptr_t)x_per_type[0]) -
+                    offs[t] * F * eb;
     }
     P.table_off[n_types] = offs[n_types];
     P.F = F;

@@ -114,6 +114,8 @@ constexpr int kClassMid = kSmallClasses;
 constexpr int kClassHub = kSmallClasses + 1;
 constexpr int kPlanClassBits = 5;       // 32 buckets (18 used)
 constexpr int kMaxChunksPerHub = 2048;  // hub rows are split into <= this many chunks
+constexpr int kTinyDeg = 7;             // rows of at most this many edges: tiny-row kernel
+constexpr int kTinyClassEnd = 4;        // classes 0..3 (bit length <= 3) are tiny
 
 struct SpmmParams {
     const void* rowptr;
@@ -123,13 +125,19 @@ struct SpmmParams {
     int n_tables;
     const char* table_ptr[MP_MAX_TYPES];
     int64_t table_off[MP_MAX_TYPES + 1];
+    // byte offset from table_ptr[0] such that global row c of table t starts
+    // at table_ptr[0] + voff[t] + c * F * elem_bytes
+    int64_t voff[MP_MAX_TYPES];
     int64_t F;
     int L, S, FT;
     int64_t ltot;
     // work list (waves, in launch order): hub chunks, mid rows, small groups
     const int32_t* rowlist;  // nullptr: rows 0..N-1 all handled as "mid"
+    const int32_t* rowbeg;   // [N] rowptr[rowlist[k]] (plan only)
+    const int32_t* rowend;   // [N] rowptr[rowlist[k] + 1] (plan only)
     int64_t n_hub_waves, n_mid_waves, n_small_waves;
     int64_t hub_base, mid_base, small_base, n_small, n_hub;
+    int64_t n_tiny;          // rowlist[0, n_tiny): rows for the tiny-row kernel
     const uint32_t* chunk_off;  // indexed by rowlist position
     int chunk_min;
     int reduce;
@@ -145,6 +153,9 @@ struct SpmmParams {
 };
 
 hipError_t launch_spmm(const SpmmParams& p, int x_dtype, int epl, hipStream_t s);
+hipError_t launch_spmm_tiny(const SpmmParams& p, int x_dtype, int epl, hipStream_t s);
+hipError_t launch_plan_rowrange(const void* rowptr, int rp64, const int32_t* rowlist, int64_t N,
+                                int32_t* rowbeg, int32_t* rowend, hipStream_t s);
 hipError_t launch_spmm_fixup(const SpmmParams& p, hipStream_t s);
 hipError_t launch_plan_classes(const void* rowptr, int rp64, int64_t N, int64_t small_max,
                                int64_t hub_min, uint32_t* keys, hipStream_t s);

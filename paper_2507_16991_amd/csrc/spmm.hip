@@ -76,25 +76,21 @@ __device__ inline int64_t load_rp(const void* rp, int rp64, int64_t i) {
     return rp64 ? static_cast<const int64_t*>(rp)[i] : (int64_t) static_cast<const int32_t*>(rp)[i];
 }
 
-// Address of feature element `fe` of source row c.  With several tables
-// (typed nodes, MULTI), c is a global id and the table is the last one whose
-// offset is <= c; the select chain uses constant indices only, so the table
-// list stays in kernel-argument registers.
-template <typename TX, bool MULTI>
+// Address of feature element `fe` of source row c.  With NT > 1 tables
+// (typed nodes; NT is a compile-time bound on n_tables), c is a global id and
+// its table is the last one whose offset is <= c: one compare and one 64-bit
+// select per table.  Addresses stay offsets from the first table's pointer,
+// so loads remain global-memory loads.
+template <typename TX, int NT>
 __device__ inline const char* feat_addr(const SpmmParams& P, int32_t c, int64_t fe) {
-    if constexpr (!MULTI) {
+    if constexpr (NT == 1) {
         return P.table_ptr[0] + ((int64_t)c * P.F + fe) * (int64_t)sizeof(TX);
     } else {
-        const char* base = P.table_ptr[0];
-        int64_t off = 0;
+        int64_t vo = 0;
 #pragma unroll
-        for (int k = 1; k < MP_MAX_TYPES; ++k) {
-            if (k < P.n_tables && (int64_t)c >= P.table_off[k]) {
-                base = P.table_ptr[k];
-                off = P.table_off[k];
-            }
-        }
-        return base + (((int64_t)c - off) * P.F + fe) * (int64_t)sizeof(TX);
+        for (int k = 1; k < NT; ++k)
+            vo = (k < P.n_tables && c >= (int32_t)P.table_off[k]) ? P.voff[k] : vo;
+        return P.table_ptr[0] + vo + ((int64_t)c * P.F + fe) * (int64_t)sizeof(TX);
     }
 }
 
@@ -107,9 +103,9 @@ __device__ inline void max_merge(float& va, int32_t& ia, float vb, int32_t ib) {
 
 // ---- accumulator state -------------------------------------------------------
 
-template <int EPL, bool HS, bool HM>
+template <int EPL, bool HS, bool HM, int NA = (HM ? 2 : 4)>
 struct Acc {
-    static constexpr int A = HM ? 2 : 4;  // independent partial accumulators
+    static constexpr int A = NA;  // independent partial accumulators
     float s[A][EPL];
     float m[A][EPL];
     int32_t i[A][EPL];
@@ -257,7 +253,7 @@ __device__ inline void store_row(const SpmmParams& P, int64_t row, int64_t fe, i
 // once, coalesced, one per lane; each inner step then covers SU = S*U edges:
 // slot s takes edges base + u*S + s (u < U), gets their columns by cross-lane
 // permute, issues all U feature-row loads, and only then accumulates.
-template <typename TX, int EPL, bool HS, bool HM, bool MULTI, bool W>
+template <typename TX, int EPL, bool HS, bool HM, int NT, bool W>
 __device__ inline void wave_range(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int64_t e0,
                                   int64_t e1, int lane, int slot, bool feat_ok, int64_t fe, int U) {
     using R = typename RawVec<TX, EPL>::T;
@@ -284,7 +280,7 @@ __device__ inline void wave_range(const SpmmParams& P, Acc<EPL, HS, HM>& acc, in
                 const int t = base + u * S + slot;
                 const int32_t c = __shfl(myc, t);
                 ok[u] = feat_ok && (u < U) && (t < rem);
-                addr[u] = feat_addr<TX, MULTI>(P, c, fe);
+                addr[u] = feat_addr<TX, NT>(P, c, fe);
             }
             R raw[kUnroll];
 #pragma unroll
@@ -312,7 +308,7 @@ __device__ inline void wave_range(const SpmmParams& P, Acc<EPL, HS, HM>& acc, in
 // One slot per row: every slot walks its own row's edges, U at a time.
 // COOP: the slot has at least U lanes, which load its next U columns
 // together; otherwise each lane loads the columns itself.
-template <typename TX, int EPL, bool HS, bool HM, bool MULTI, bool W, bool COOP>
+template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, bool COOP>
 __device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int64_t e0,
                                 int32_t my_n, int32_t max_n, int slot, int j, bool feat_ok,
                                 int64_t fe) {
@@ -337,7 +333,7 @@ __device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int6
                 wt[u] = 1.f;
                 if constexpr (W) wt[u] = __shfl(myw, srcl);
                 ok[u] = feat_ok && (it + u < my_n);
-                addr[u] = feat_addr<TX, MULTI>(P, c, fe);
+                addr[u] = feat_addr<TX, NT>(P, c, fe);
             }
         } else {
             int32_t cc[kUnroll];
@@ -349,7 +345,7 @@ __device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int6
                 if constexpr (W) wt[u] = ok[u] ? P.w[e0 + it + u] : 1.f;
             }
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) addr[u] = feat_addr<TX, MULTI>(P, cc[u], fe);
+            for (int u = 0; u < kUnroll; ++u) addr[u] = feat_addr<TX, NT>(P, cc[u], fe);
         }
         R raw[kUnroll];
 #pragma unroll
@@ -370,7 +366,7 @@ __device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int6
     }
 }
 
-template <typename TX, int EPL, bool HS, bool HM, bool MULTI, bool W>
+template <typename TX, int EPL, bool HS, bool HM, int NT, bool W>
 __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave)) +
@@ -415,11 +411,17 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
             e1 = e0 + csz < r1 ? e0 + csz : r1;
             cidx = item;
         } else {
-            row = P.rowlist ? (int64_t)P.rowlist[P.mid_base + item] : item;
-            e0 = load_rp(P.rowptr, P.rp64, row);
-            e1 = load_rp(P.rowptr, P.rp64, row + 1);
+            if (P.rowbeg) {
+                row = P.rowlist[P.mid_base + item];
+                e0 = P.rowbeg[P.mid_base + item];
+                e1 = P.rowend[P.mid_base + item];
+            } else {
+                row = P.rowlist ? (int64_t)P.rowlist[P.mid_base + item] : item;
+                e0 = load_rp(P.rowptr, P.rp64, row);
+                e1 = load_rp(P.rowptr, P.rp64, row + 1);
+            }
         }
-        wave_range<TX, EPL, HS, HM, MULTI, W>(P, acc, e0, e1, lane, slot, feat_ok, fe, U);
+        wave_range<TX, EPL, HS, HM, NT, W>(P, acc, e0, e1, lane, slot, feat_ok, fe, U);
         acc.fold();
         acc.reduce_slots(S, L, slot, lane);
         if (slot == 0 && feat_ok) {
@@ -450,8 +452,8 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
     int64_t row = 0, e0 = 0, e1 = 0;
     if (row_ok) {
         row = P.rowlist[P.small_base + k_row];
-        e0 = load_rp(P.rowptr, P.rp64, row);
-        e1 = load_rp(P.rowptr, P.rp64, row + 1);
+        e0 = P.rowbeg[P.small_base + k_row];
+        e1 = P.rowend[P.small_base + k_row];
     }
     const int32_t my_n = (int32_t)(e1 - e0);
     int32_t max_n = my_n;
@@ -461,11 +463,113 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
         max_n = o > max_n ? o : max_n;
     }
     if (L >= kUnroll)
-        slot_row<TX, EPL, HS, HM, MULTI, W, true>(P, acc, e0, my_n, max_n, slot, j, feat_ok, fe);
+        slot_row<TX, EPL, HS, HM, NT, W, true>(P, acc, e0, my_n, max_n, slot, j, feat_ok, fe);
     else
-        slot_row<TX, EPL, HS, HM, MULTI, W, false>(P, acc, e0, my_n, max_n, slot, j, feat_ok, fe);
+        slot_row<TX, EPL, HS, HM, NT, W, false>(P, acc, e0, my_n, max_n, slot, j, feat_ok, fe);
     acc.fold();
     if (feat_ok) store_row<EPL>(P, row, fe, e1 - e0, acc.s[0], acc.m[0], acc.i[0], HS, HM);
+}
+
+// Rows of at most kTinyDeg edges (most rows of low-degree graphs): one slot
+// per row as in the small-row path, but wavefronts are persistent and
+// software-pipelined: while the rows of group g are gathered, the column
+// indices of the next group and the row ranges of the one after are already
+// in flight, so a group costs about one memory round trip.  Requires slots of
+// at least kTinyDeg + 1 lanes (the columns of a row are loaded one per lane).
+// One accumulator per element: a row has at most 7 edges.
+template <typename TX, int EPL, bool HS, bool HM, bool W, int NT>
+__global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
+    using R = typename RawVec<TX, EPL>::T;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t tw = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave)) +
+                       (int64_t)blockIdx.x * kWavesPerBlock;
+    const int64_t nw = (int64_t)gridDim.x * kWavesPerBlock;
+    const int L = P.L, S = P.S;
+    const int slot = lane / L;
+    const int j = lane - slot * L;
+    const bool slot_ok = slot < S;
+    const int64_t items = ((P.n_tiny + S - 1) / S) * P.FT;
+
+    // row record (row, first edge, degree) of work item `it` for this slot
+    auto rec = [&](int64_t it, int32_t& row, int32_t& beg, int32_t& deg) {
+        row = -1;
+        beg = 0;
+        deg = 0;
+        if (it < items) {
+            const int64_t k = (it / P.FT) * S + slot;
+            if (slot_ok && k < P.n_tiny) {
+                row = P.rowlist[k];
+                beg = P.rowbeg[k];
+                deg = P.rowend[k] - beg;
+            }
+        }
+    };
+    auto cols = [&](int32_t beg, int32_t deg, int32_t& c, float& w) {
+        c = 0;
+        w = 1.f;
+        if (j < deg) {
+            c = __builtin_nontemporal_load(P.col + beg + j);
+            if constexpr (W) w = __builtin_nontemporal_load(P.w + beg + j);
+        }
+    };
+
+    int64_t it = tw;
+    int32_t row, beg, deg, nrow, nbeg, ndeg;
+    int32_t cv;
+    float wv;
+    rec(it, row, beg, deg);
+    cols(beg, deg, cv, wv);
+    rec(it + nw, nrow, nbeg, ndeg);
+    for (; it < items; it += nw) {
+        const int ft = (int)(it % P.FT);
+        const int64_t chunk_j = ft * (int64_t)kWave + j;
+        const bool feat_ok = row >= 0 && chunk_j < P.ltot;
+        const int64_t fe = chunk_j * EPL;
+        R raw[kTinyDeg];
+        bool ok[kTinyDeg];
+#pragma unroll
+        for (int u = 0; u < kTinyDeg; ++u) {
+            const int32_t c = __shfl(cv, slot * L + u);
+            ok[u] = feat_ok && (u < deg);
+            if (ok[u]) raw[u] = *reinterpret_cast<const R*>(feat_addr<TX, NT>(P, c, fe));
+        }
+        float wt[kTinyDeg];
+#pragma unroll
+        for (int u = 0; u < kTinyDeg; ++u) {
+            wt[u] = 1.f;
+            if constexpr (W) wt[u] = __shfl(wv, slot * L + u);
+        }
+        // next group's columns, and the row ranges of the group after it
+        int32_t ncv;
+        float nwv;
+        cols(nbeg, ndeg, ncv, nwv);
+        int32_t row2, beg2, deg2;
+        rec(it + 2 * nw, row2, beg2, deg2);
+
+        Acc<EPL, HS, HM, 1> acc;
+        acc.init();
+#pragma unroll
+        for (int u = 0; u < kTinyDeg; ++u) {
+            if (ok[u]) {
+                float v[EPL];
+                widen<TX, EPL>(raw[u], v);
+                if constexpr (W) {
+#pragma unroll
+                    for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt[u], v[k]);
+                }
+                acc.add(0, v, beg + u);
+            }
+        }
+        if (feat_ok) store_row<EPL>(P, row, fe, deg, acc.s[0], acc.m[0], acc.i[0], HS, HM);
+        row = nrow;
+        beg = nbeg;
+        deg = ndeg;
+        cv = ncv;
+        wv = nwv;
+        nrow = row2;
+        nbeg = beg2;
+        ndeg = deg2;
+    }
 }
 
 // Combine the chunk partials of every hub row, in chunk order, and write the
@@ -554,6 +658,18 @@ __global__ __launch_bounds__(256) void plan_chunks(const void* rowptr, int rp64,
     nch[k] = c;
 }
 
+// row range of every rowlist entry
+__global__ __launch_bounds__(256) void plan_rowrange(const void* rowptr, int rp64,
+                                                     const int32_t* __restrict__ rowlist, int64_t N,
+                                                     int32_t* __restrict__ rowbeg,
+                                                     int32_t* __restrict__ rowend) {
+    const int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (k >= N) return;
+    const int64_t row = rowlist[k];
+    rowbeg[k] = (int32_t)load_rp(rowptr, rp64, row);
+    rowend[k] = (int32_t)load_rp(rowptr, rp64, row + 1);
+}
+
 // header[c] = start of class c in rowlist (c < nclass), header[nclass] = N,
 // header[nclass + 1] = total hub chunks
 __global__ void plan_header(const uint32_t* __restrict__ class_start, int nclass,
@@ -572,11 +688,11 @@ hipError_t launch_w(const SpmmParams& p, unsigned grid, hipStream_t s) {
     const bool hs = (p.reduce & (kSum | kMean)) != 0;
     const bool hm = (p.reduce & kMax) != 0;
     if (hs && hm)
-        hipLaunchKernelGGL((spmm_main<TX, EPL, true, true, false, W>), dim3(grid), dim3(kBlock), 0, s, p);
+        hipLaunchKernelGGL((spmm_main<TX, EPL, true, true, 1, W>), dim3(grid), dim3(kBlock), 0, s, p);
     else if (hm)
-        hipLaunchKernelGGL((spmm_main<TX, EPL, false, true, false, W>), dim3(grid), dim3(kBlock), 0, s, p);
+        hipLaunchKernelGGL((spmm_main<TX, EPL, false, true, 1, W>), dim3(grid), dim3(kBlock), 0, s, p);
     else
-        hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, false, W>), dim3(grid), dim3(kBlock), 0, s, p);
+        hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 1, W>), dim3(grid), dim3(kBlock), 0, s, p);
     return hipGetLastError();
 }
 
@@ -584,7 +700,12 @@ template <typename TX, int EPL>
 hipError_t launch_typed(const SpmmParams& p, unsigned grid, hipStream_t s) {
     if (p.n_tables > 1) {
         // typed-node tables: unweighted sum only
-        hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, true, false>), dim3(grid), dim3(kBlock), 0, s, p);
+        if (p.n_tables <= 2)
+            hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 2, false>), dim3(grid), dim3(kBlock), 0, s, p);
+        else if (p.n_tables <= 4)
+            hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 4, false>), dim3(grid), dim3(kBlock), 0, s, p);
+        else
+            hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, MP_MAX_TYPES, false>), dim3(grid), dim3(kBlock), 0, s, p);
         return hipGetLastError();
     }
     return p.w ? launch_w<TX, EPL, true>(p, grid, s) : launch_w<TX, EPL, false>(p, grid, s);
@@ -629,6 +750,56 @@ hipError_t launch_spmm(const SpmmParams& p, int x_dtype, int epl, hipStream_t s)
         case 2: return launch_typed<uint16_t, 2>(p, grid, s);
         default: return launch_typed<uint16_t, 1>(p, grid, s);
     }
+}
+
+template <typename TX, int EPL>
+hipError_t launch_tiny_typed(const SpmmParams& p, unsigned grid, hipStream_t s) {
+    const bool hs = (p.reduce & (kSum | kMean)) != 0;
+    const bool hm = (p.reduce & kMax) != 0;
+    const bool w = p.w != nullptr;
+#define MP_TINY(HS, HM, WW) \
+    hipLaunchKernelGGL((spmm_tiny<TX, EPL, HS, HM, WW, 1>), dim3(grid), dim3(kBlock), 0, s, p)
+    if (p.n_tables > 1) {
+        // typed-node tables: unweighted sum only
+        if (p.n_tables <= 2)
+            hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, 2>), dim3(grid), dim3(kBlock), 0, s, p);
+        else if (p.n_tables <= 4)
+            hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, 4>), dim3(grid), dim3(kBlock), 0, s, p);
+        else
+            hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, MP_MAX_TYPES>), dim3(grid), dim3(kBlock), 0, s, p);
+    } else if (hs && hm) { if (w) MP_TINY(true, true, true); else MP_TINY(true, true, false); }
+    else if (hm) { if (w) MP_TINY(false, true, true); else MP_TINY(false, true, false); }
+    else { if (w) MP_TINY(true, false, true); else MP_TINY(true, false, false); }
+#undef MP_TINY
+    return hipGetLastError();
+}
+
+hipError_t launch_spmm_tiny(const SpmmParams& p, int x_dtype, int epl, hipStream_t s) {
+    if (p.n_tiny <= 0) return hipSuccess;
+    const int64_t items = ceil_div(p.n_tiny, p.S) * p.FT;
+    const int64_t waves = items < 4096 ? items : 4096;
+    const unsigned grid = (unsigned)ceil_div(waves, kWavesPerBlock);
+    if (x_dtype == MP_F32) {
+        switch (epl) {
+            case 4: return launch_tiny_typed<float, 4>(p, grid, s);
+            case 2: return launch_tiny_typed<float, 2>(p, grid, s);
+            default: return launch_tiny_typed<float, 1>(p, grid, s);
+        }
+    }
+    switch (epl) {
+        case 8: return launch_tiny_typed<uint16_t, 8>(p, grid, s);
+        case 4: return launch_tiny_typed<uint16_t, 4>(p, grid, s);
+        case 2: return launch_tiny_typed<uint16_t, 2>(p, grid, s);
+        default: return launch_tiny_typed<uint16_t, 1>(p, grid, s);
+    }
+}
+
+hipError_t launch_plan_rowrange(const void* rowptr, int rp64, const int32_t* rowlist, int64_t N,
+                                int32_t* rowbeg, int32_t* rowend, hipStream_t s) {
+    if (N <= 0) return hipSuccess;
+    hipLaunchKernelGGL(plan_rowrange, dim3((unsigned)ceil_div(N, 256)), dim3(256), 0, s, rowptr,
+                       rp64, rowlist, N, rowbeg, rowend);
+    return hipGetLastError();
 }
 
 hipError_t launch_spmm_fixup(const SpmmParams& p, hipStream_t s) {

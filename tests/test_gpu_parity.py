@@ -335,11 +335,17 @@ def test_chunglu_124M_spmm_sampled(chunglu_full, dtype):
 
 # ---- heterogeneous -------------------------------------------------------------------------
 
-def run_hetero(g, plan_on=True):
+def run_hetero(g, plan_on=True, one_buffer=False):
+    """one_buffer: the per-type tables are consecutive slices of one tensor
+    (the library then gathers from it as a single table)."""
     T = len(g.n_per_type)
     rels = [(g.rel_src_type[r], g.rel_dst_type[r], dev(g.rel_src[r]), dev(g.rel_dst[r]))
             for r in range(len(g.rel_src))]
-    xs = [dev(x.view(np.int16)).view(torch.bfloat16) for x in g.x_bf16]
+    if one_buffer:
+        allx = dev(np.concatenate(g.x_bf16).view(np.int16)).view(torch.bfloat16)
+        xs = list(torch.split(allx, g.n_per_type))
+    else:
+        xs = [dev(x.view(np.int16)).view(torch.bfloat16) for x in g.x_bf16]
     outs_o, scs_o = oracle.hetero_sum(g.n_per_type, g.x_bf16, g.rel_src_type, g.rel_dst_type,
                                       g.rel_src, g.rel_dst)
     for t in range(T):
@@ -360,11 +366,22 @@ def test_hetero_small():
                               [(0, 0, 9000), (0, 1, 11000), (1, 0, 10000), (1, 2, 4000)], 128)
     run_hetero(g, True)
     run_hetero(g, False)
+    run_hetero(g, True, one_buffer=True)
+
+
+def test_hetero_many_types():
+    """More node types than the 4-table kernel variant covers."""
+    n = [500, 40, 700, 1, 300, 90, 2000]
+    rels = [(a, b, 300 + 97 * (a * 7 + b)) for a in range(7) for b in range(7) if (a + b) % 3 == 0]
+    g = graphgen.hetero_graph(8, n, rels, 64)
+    run_hetero(g, True)
+    run_hetero(g, False)
 
 
 def test_hetero_20M():
     g = graphgen.workload("hetero-20M", seed=0)
     run_hetero(g, True)
+    run_hetero(g, True, one_buffer=True)
 
 
 # ---- web-scale single-GPU shard ---------------------------------------------------------
