@@ -171,14 +171,14 @@ def build_step(args, mp, torch, np, dev):
     if g.x_bf16 is not None and args.workload in (WORKLOAD, "web-1.6B"):
         xs["bf16"] = (torch.from_numpy(g.x_bf16.view(np.int16)).to(dev).view(torch.bfloat16),
                       mp.MP_BF16, 2)
-    plan_bufs = {k: torch.empty(nplan, dtype=torch.uint8, device=dev) for k in xs}
+    plan_buf = torch.empty(nplan, dtype=torch.uint8, device=dev)
     out = torch.empty(N, F, dtype=torch.float32, device=dev)
     mx = {k: torch.empty(N, F, dtype=torch.float32 if k == "f32" else torch.bfloat16,
                          device=dev) for k in xs}
     arg = torch.empty(N, F, dtype=torch.int32, device=dev)
 
     csr_b = csr_bytes(N, E, rowptr_b=rp_b, perm=weighted) + (8 * E if weighted else 0)
-    ops = [("csr", csr_b, 0), ("plan", len(xs) * plan_bytes(N), 0)]
+    ops = [("csr", csr_b, 0), ("plan", plan_bytes(N), 0)]
     if web:
         reds = [("sum+max", mp.MP_SUM | mp.MP_MAX, False)]
     elif args.workload == "powerlaw-1.2M":
@@ -203,15 +203,15 @@ def build_step(args, mp, torch, np, dev):
         mp.mp_coo_to_csr(src, dst, E, N, rowptr, it, col, perm, w_coo, w_csr, ws_csr,
                          ws_csr.numel())
         mark(evs, 1)
-        # one plan per feature dtype (a plan is checked against x's dtype)
-        for k, (x, xd, xb) in xs.items():
-            if k in plans:
-                mp.mp_spmm_plan_free(plans[k])
-            plans[k] = mp.mp_spmm_plan_build(rowptr, it, N, E, F, xd, plan_bufs[k], nplan)
+        # one plan per CSR, shared by both feature dtypes
+        k0 = next(iter(xs))
+        if "h" in plans:
+            mp.mp_spmm_plan_free(plans["h"])
+        plans["h"] = mp.mp_spmm_plan_build(rowptr, it, N, E, F, xs[k0][1], plan_buf, nplan)
         mark(evs, 2)
         i = 2
         for k, x, xd, red, wt in calls:
-            h = plans[k]
+            h = plans["h"]
             nb = mp.mp_spmm_workspace(h, red)
             key = (k, red)
             if key not in wss or wss[key].numel() < nb:

@@ -121,7 +121,9 @@ typedef struct mp_plan mp_plan;
 /* Device bytes of the plan buffer for a CSR with N_dst rows and E edges. */
 int mp_spmm_plan_size(int64_t N_dst, int64_t E, size_t* bytes);
 
-/* Build a plan for one CSR and one feature geometry (F, x_dtype).
+/* Build a plan for one CSR and one feature row width F.  Its degree classes
+ * are tuned for x_dtype, but the plan also serves the other feature dtype
+ * (the classification never changes results, only which kernel does a row).
  *   rowptr      [N_dst+1] of rowptr_itype (device).
  *   plan_buf    device buffer of mp_spmm_plan_size bytes, owned by the caller,
  *               which must keep it alive and unchanged while the plan is used.
@@ -143,12 +145,10 @@ int mp_spmm_workspace(const mp_plan* plan, int reduce, size_t* bytes);
 
 /* Segmented aggregation over the destination-major CSR (Eq. (1), the
  * AGGREGATION step; messages m_p = x[col[p], :] or w[p] * x[col[p], :]).
- *   plan        from mp_spmm_plan_build for this rowptr, N_dst, E, F and
- *               x_dtype, or NULL (then one wavefront per row, no hub split,
- *               no workspace).
- *   rowptr      [N_dst+1] of rowptr_itype; col [E] int32 (E = rowptr[N_dst],
- *               taken from the plan, or read from the device when plan is
- *               NULL -- that read is a blocking copy).
+ *   plan        from mp_spmm_plan_build for this rowptr, N_dst and F (any
+ *               x_dtype), or NULL (then one wavefront per row, no hub split,
+ *               no workspace); a mismatch returns MP_ERR_PLAN.
+ *   rowptr      [N_dst+1] of rowptr_itype; col [rowptr[N_dst]] int32.
  *   w           [E] fp32 in CSR order, or NULL (unweighted).
  *   x           [N_src, F] row-major, x_dtype (MP_F32 or MP_BF16).
  *   reduce      MP_SUM, MP_MEAN, MP_MAX, MP_SUM|MP_MAX or MP_MEAN|MP_MAX.

@@ -222,11 +222,12 @@ int run_spmm(const mp_plan* plan, SpmmParams& P, const Geometry& g, int x_dtype,
     return MP_OK;
 }
 
-int check_plan(const mp_plan* plan, const void* rowptr, int itype, int64_t N_dst, int64_t F,
-               int x_dtype) {
+// The row classes only steer work to kernels (any classification gives the
+// same result), so a plan built for one feature dtype serves the other too;
+// F must match because hub partials are sized by it.
+int check_plan(const mp_plan* plan, const void* rowptr, int itype, int64_t N_dst, int64_t F) {
     if (!plan) return MP_OK;
-    if (plan->rowptr != rowptr || plan->itype != itype || plan->N_dst != N_dst || plan->F != F ||
-        plan->x_dtype != x_dtype)
+    if (plan->rowptr != rowptr || plan->itype != itype || plan->N_dst != N_dst || plan->F != F)
         return MP_ERR_PLAN;
     return MP_OK;
 }
@@ -400,7 +401,7 @@ int mp_spmm(const mp_plan* plan, const void* rowptr, int rowptr_itype, const int
         if (hs && !out) return MP_ERR_NULL;
         if (hm && (!out_max || !argout)) return MP_ERR_NULL;
     }
-    int st = check_plan(plan, rowptr, rowptr_itype, N_dst, F, x_dtype);
+    int st = check_plan(plan, rowptr, rowptr_itype, N_dst, F);
     if (st != MP_OK) return st;
     const int eb = x_dtype == MP_BF16 ? 2 : 4;
     if ((uintptr_t)x % eb || (uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4) ||
@@ -519,7 +520,7 @@ int mp_hetero_spmm(int n_types, const int64_t* N_per_type, const void* const* x_
     if (F < 1 || F > 65536) return MP_ERR_SIZE;
     if (!x_per_type || !rowptr || !out || !col) return MP_ERR_NULL;
     const int64_t N_dst = N_per_type[dst_type];
-    st = check_plan(plan, rowptr, rowptr_itype, N_dst, F, x_dtype);
+    st = check_plan(plan, rowptr, rowptr_itype, N_dst, F);
     if (st != MP_OK) return st;
     const int eb = x_dtype == MP_BF16 ? 2 : 4;
     uintptr_t xa = 0;

@@ -54,9 +54,9 @@ __global__ __launch_bounds__(256) void radix_clear(uint64_t* __restrict__ desc, 
     if (i0 == 0) *err = 0;
 }
 
-// Global histogram of every pass's digit: per-wave private LDS counters, one
-// update per distinct digit per 64 keys (the lowest lane of each digit group
-// adds the group size), then one integer atomic per (pass, digit) per block.
+// Global histogram of every pass's digit.  Counts do not depend on order, so
+// each wavefront adds into its own LDS copy with integer atomics (no ranking
+// needed), then one integer atomic per (pass, digit) per workgroup.
 __global__ __launch_bounds__(kGhistBlock) void radix_ghist(const uint32_t* __restrict__ keys,
                                                            int64_t n, int passes, int bits,
                                                            uint32_t* __restrict__ ghist) {
@@ -68,7 +68,6 @@ __global__ __launch_bounds__(kGhistBlock) void radix_ghist(const uint32_t* __res
     const int lane = threadIdx.x & (kWave - 1);
     const int wv = threadIdx.x / kWave;
     const uint32_t mask = (1u << bits) - 1u;
-    const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
     const int64_t stride = (int64_t)gridDim.x * W * kWave * kGhistItems;
     for (int64_t base = ((int64_t)blockIdx.x * W + wv) * kWave * kGhistItems; base < n;
          base += stride) {
@@ -80,12 +79,9 @@ __global__ __launch_bounds__(kGhistBlock) void radix_ghist(const uint32_t* __res
         }
 #pragma unroll
         for (int k = 0; k < kGhistItems; ++k) {
-            const bool ok = base + (int64_t)k * kWave + lane < n;
-            for (int p = 0; p < passes; ++p) {
-                const uint32_t d = (key[k] >> (p * bits)) & mask;
-                const uint64_t peers = digit_peers(ok, d, bits);
-                if (ok && (peers & lt_mask) == 0) h[wv][p][d] += (uint32_t)__popcll(peers);
-            }
+            if (base + (int64_t)k * kWave + lane >= n) continue;
+            for (int p = 0; p < passes; ++p)
+                atomicAdd(&h[wv][p][(key[k] >> (p * bits)) & mask], 1u);
         }
     }
     __syncthreads();
@@ -275,14 +271,26 @@ constexpr int kRowptrItems = 8;
 template <typename RP>
 __global__ __launch_bounds__(256) void rowptr_from_sorted(const uint32_t* __restrict__ keys,
                                                           int64_t E, int64_t N, RP* __restrict__ rowptr) {
+    static_assert(kRowptrItems == 8, "two 16-byte loads per thread");
     const int64_t p0 = ((int64_t)blockIdx.x * 256 + threadIdx.x) * kRowptrItems;
     if (p0 > E) return;
+    uint32_t k8[kRowptrItems];
+    if (p0 + kRowptrItems <= E) {
+        // keys is 256-byte aligned and p0 a multiple of 8: aligned 16-byte loads
+        const uint4 a = reinterpret_cast<const uint4*>(keys + p0)[0];
+        const uint4 b = reinterpret_cast<const uint4*>(keys + p0)[1];
+        k8[0] = a.x; k8[1] = a.y; k8[2] = a.z; k8[3] = a.w;
+        k8[4] = b.x; k8[5] = b.y; k8[6] = b.z; k8[7] = b.w;
+    } else {
+#pragma unroll
+        for (int k = 0; k < kRowptrItems; ++k) k8[k] = p0 + k < E ? keys[p0 + k] : 0u;
+    }
     int64_t prev = p0 == 0 ? -1 : (int64_t)keys[p0 - 1];
 #pragma unroll
     for (int k = 0; k < kRowptrItems; ++k) {
         const int64_t p = p0 + k;
         if (p > E) break;
-        int64_t cur = p == E ? N : (int64_t)keys[p];
+        int64_t cur = p == E ? N : (int64_t)k8[k];
         if (cur > N) cur = N;  // keys are < N for valid input; stay inside rowptr regardless
         for (int64_t v = prev + 1; v <= cur; ++v) rowptr[v] = (RP)p;
         if (cur > prev) prev = cur;

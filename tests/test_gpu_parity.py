@@ -228,12 +228,22 @@ def test_spmm_empty_and_degenerate():
         compare_spmm(rp_o, col_o, None, xs, out, m, a, mp.MP_SUM | mp.MP_MAX, torch.float32)
 
 
-def test_plan_mismatch_rejected(mixed):
+def test_plan_mismatch_rejected_and_dtype_shared(mixed):
     g, rp_o, col_o, w_o = mixed
     rp = dev(rp_o.astype(np.int32))
     plan = mp.Plan(rp, g.E, g.F, torch.float32)
+    # a plan serves both feature dtypes
+    out, _, _ = mp.spmm(rp, dev(col_o), x_of(g, torch.bfloat16), mp.MP_SUM, plan=plan)
+    torch.cuda.synchronize()
+    compare_spmm(rp_o, col_o, None, x_f32_host(g, torch.bfloat16), out, None, None, mp.MP_SUM,
+                 torch.bfloat16)
+    # a different feature width or rowptr does not
+    x8 = torch.zeros(g.n_src, 8, device=DEV)
     with pytest.raises(mp.MPError) as e:
-        mp.spmm(rp, dev(col_o), x_of(g, torch.bfloat16), mp.MP_SUM, plan=plan)
+        mp.spmm(rp, dev(col_o), x8, mp.MP_SUM, plan=plan)
+    assert e.value.status == -6
+    with pytest.raises(mp.MPError) as e:
+        mp.spmm(rp.clone(), dev(col_o), x_of(g, torch.float32), mp.MP_SUM, plan=plan)
     assert e.value.status == -6
 
 
