@@ -110,6 +110,16 @@ int mp_coo_to_csr(const int32_t* src, const int32_t* dst, int64_t E, int64_t N,
                   const float* val_in, float* val_out, void* ws, size_t ws_bytes,
                   void* stream);
 
+/* COO edges already sorted by destination (the sort-order metadata the
+ * paper's EdgeIndex carries, Sec. 2.2): the CSR is the COO itself, so rowptr
+ * is derived from dst directly, col = src, perm = 0..E-1 and val_out =
+ * val_in (each optional output as in mp_coo_to_csr).  The caller asserts the
+ * order; mp_validate_sorted counts violations.  No workspace.  If dst is not
+ * non-decreasing the outputs are unspecified (but stay in bounds). */
+int mp_sorted_coo_to_csr(const int32_t* src, const int32_t* dst, int64_t E, int64_t N,
+                         void* rowptr, int rowptr_itype, int32_t* col, int32_t* perm,
+                         const float* val_in, float* val_out, void* stream);
+
 /* ---------------------------------------------------------------------------
  * Aggregation plan: rows binned by in-degree (Sec. 2.2: the sorted layout
  * "enables greater parallelism"; the plan is built once per CSR and reused,
@@ -225,6 +235,9 @@ int mp_hetero_spmm(int n_types, const int64_t* N_per_type, const void* const* x_
 /* Counts edges with src outside [0, N_src) or dst outside [0, N_dst). */
 int mp_validate_coo(const int32_t* src, const int32_t* dst, int64_t E, int64_t N_src,
                     int64_t N_dst, int64_t* d_count, void* stream);
+
+/* Counts positions p with dst[p] < dst[p-1] (0 when dst is sorted). */
+int mp_validate_sorted(const int32_t* dst, int64_t E, int64_t* d_count, void* stream);
 
 /* Counts rowptr steps that decrease, rowptr[0] != 0, rowptr[N_dst] != E, and
  * col entries outside [0, N_src). */

@@ -22,6 +22,7 @@ import torch
 __all__ = [
     "MPError", "lib", "MP_F32", "MP_BF16", "MP_I32", "MP_I64", "MP_SUM", "MP_MEAN", "MP_MAX",
     "mp_version", "mp_status_str", "mp_coo_to_csr_workspace", "mp_coo_to_csr",
+    "mp_sorted_coo_to_csr", "mp_validate_sorted", "sorted_coo_to_csr",
     "mp_spmm_plan_size", "mp_spmm_plan_build", "mp_spmm_plan_free", "mp_spmm_workspace",
     "mp_spmm", "mp_hetero_build_workspace", "mp_hetero_build", "mp_hetero_spmm",
     "mp_validate_coo", "mp_validate_csr", "coo_to_csr", "Plan", "spmm", "hetero_build",
@@ -67,6 +68,7 @@ def lib():
         L.mp_status_str.restype = ctypes.c_char_p
         L.mp_coo_to_csr_workspace.argtypes = [i64, i64, i32, i32, psz]
         L.mp_coo_to_csr.argtypes = [p, p, i64, i64, p, i32, p, p, p, p, p, sz, p]
+        L.mp_sorted_coo_to_csr.argtypes = [p, p, i64, i64, p, i32, p, p, p, p, p]
         L.mp_spmm_plan_size.argtypes = [i64, i64, psz]
         L.mp_spmm_plan_build.argtypes = [p, i32, i64, i64, i64, i32, p, sz, p,
                                          ctypes.POINTER(ctypes.c_void_p)]
@@ -81,7 +83,9 @@ def lib():
                                      p]
         L.mp_validate_coo.argtypes = [p, p, i64, i64, i64, p, p]
         L.mp_validate_csr.argtypes = [p, i32, p, i64, i64, i64, p, p]
-        for name in ("mp_coo_to_csr_workspace", "mp_coo_to_csr", "mp_spmm_plan_size",
+        L.mp_validate_sorted.argtypes = [p, i64, p, p]
+        for name in ("mp_coo_to_csr_workspace", "mp_coo_to_csr", "mp_sorted_coo_to_csr",
+                     "mp_validate_sorted", "mp_spmm_plan_size",
                      "mp_spmm_plan_build", "mp_spmm_workspace", "mp_spmm",
                      "mp_hetero_build_workspace", "mp_hetero_build", "mp_hetero_spmm",
                      "mp_validate_coo", "mp_validate_csr"):
@@ -160,6 +164,13 @@ def mp_coo_to_csr(src, dst, E, N, rowptr, rowptr_itype, col, perm, val_in, val_o
         _ptr(val_in), _ptr(val_out), _ptr(ws), ws_bytes, _stream(stream)))
 
 
+def mp_sorted_coo_to_csr(src, dst, E, N, rowptr, rowptr_itype, col, perm, val_in, val_out,
+                         stream=None):
+    _check("mp_sorted_coo_to_csr", lib().mp_sorted_coo_to_csr(
+        _ptr(src), _ptr(dst), E, N, _ptr(rowptr), rowptr_itype, _ptr(col), _ptr(perm),
+        _ptr(val_in), _ptr(val_out), _stream(stream)))
+
+
 def mp_spmm_plan_size(N_dst, E) -> int:
     return _bytes("mp_spmm_plan_size", N_dst, E)
 
@@ -225,6 +236,11 @@ def mp_validate_coo(src, dst, E, N_src, N_dst, d_count, stream=None):
                                                     _ptr(d_count), _stream(stream)))
 
 
+def mp_validate_sorted(dst, E, d_count, stream=None):
+    _check("mp_validate_sorted", lib().mp_validate_sorted(_ptr(dst), E, _ptr(d_count),
+                                                          _stream(stream)))
+
+
 def mp_validate_csr(rowptr, rowptr_itype, col, N_dst, N_src, E, d_count, stream=None):
     _check("mp_validate_csr", lib().mp_validate_csr(_ptr(rowptr), rowptr_itype, _ptr(col), N_dst,
                                                     N_src, E, _ptr(d_count), _stream(stream)))
@@ -248,6 +264,22 @@ def coo_to_csr(src: torch.Tensor, dst: torch.Tensor, N: int, *, rowptr_dtype=tor
     if ws is None or ws.numel() < nb:
         ws = _workspace(nb, dev)
     mp_coo_to_csr(src, dst, E, N, rowptr, it, col, perm, val, vout, ws, ws.numel(), stream)
+    return rowptr, col, perm, vout
+
+
+def sorted_coo_to_csr(src: torch.Tensor, dst: torch.Tensor, N: int, *, rowptr_dtype=torch.int32,
+                      want_perm=False, val=None, stream=None):
+    """CSR of COO edges already sorted by destination (no sort is run).
+
+    Returns (rowptr, col, perm or None, val_csr or None) like coo_to_csr."""
+    E = int(src.numel())
+    dev = src.device
+    it = _itype_code(rowptr_dtype)
+    rowptr = torch.empty(N + 1, dtype=rowptr_dtype, device=dev)
+    col = torch.empty(max(E, 0), dtype=torch.int32, device=dev)
+    perm = torch.empty(E, dtype=torch.int32, device=dev) if want_perm else None
+    vout = torch.empty(E, dtype=torch.float32, device=dev) if val is not None else None
+    mp_sorted_coo_to_csr(src, dst, E, N, rowptr, it, col, perm, val, vout, stream)
     return rowptr, col, perm, vout
 
 

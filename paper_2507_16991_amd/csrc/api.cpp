@@ -277,6 +277,28 @@ int mp_coo_to_csr(const int32_t* src, const int32_t* dst, int64_t E, int64_t N, 
                            ws_bytes, as_stream(stream));
 }
 
+int mp_sorted_coo_to_csr(const int32_t* src, const int32_t* dst, int64_t E, int64_t N,
+                         void* rowptr, int rowptr_itype, int32_t* col, int32_t* perm,
+                         const float* val_in, float* val_out, void* stream) {
+    if (!valid_itype(rowptr_itype)) return MP_ERR_DTYPE;
+    int st = check_csr_sizes(E, N);
+    if (st != MP_OK) return st;
+    if (!rowptr) return MP_ERR_NULL;
+    if (E > 0 && (!src || !dst || !col)) return MP_ERR_NULL;
+    if ((val_in == nullptr) != (val_out == nullptr)) return MP_ERR_NULL;
+    if ((uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4)) return MP_ERR_ALIGN;
+    hipStream_t s = as_stream(stream);
+    const int rp64 = rowptr_itype == MP_I64;
+    if (E == 0) return hip_status(launch_fill_rowptr_zero(N, rowptr, rp64, s));
+    // the sorted keys are dst itself (non-negative int32 read as uint32)
+    hipError_t e = launch_rowptr_from_sorted(reinterpret_cast<const uint32_t*>(dst), E, N,
+                                             rowptr, rp64, s);
+    if (e == hipSuccess) e = launch_offset_copy(src, E, 0, col, s);
+    if (e == hipSuccess && perm) e = launch_iota(E, perm, s);
+    if (e == hipSuccess && val_in) e = launch_copy_f32(val_in, E, val_out, s);
+    return hip_status(e);
+}
+
 int mp_spmm_plan_size(int64_t N_dst, int64_t E, size_t* bytes) {
     if (!bytes) return MP_ERR_NULL;
     if (N_dst < 0 || N_dst > INT32_MAX || E < 0 || E > INT32_MAX) return MP_ERR_SIZE;
@@ -565,6 +587,12 @@ int mp_validate_coo(const int32_t* src, const int32_t* dst, int64_t E, int64_t N
     if (!d_count || (E > 0 && (!src || !dst))) return MP_ERR_NULL;
     if (E < 0 || N_src < 0 || N_dst < 0) return MP_ERR_SIZE;
     return hip_status(launch_validate_coo(src, dst, E, N_src, N_dst, d_count, as_stream(stream)));
+}
+
+int mp_validate_sorted(const int32_t* dst, int64_t E, int64_t* d_count, void* stream) {
+    if (!d_count || (E > 0 && !dst)) return MP_ERR_NULL;
+    if (E < 0) return MP_ERR_SIZE;
+    return hip_status(launch_validate_sorted(dst, E, d_count, as_stream(stream)));
 }
 
 int mp_validate_csr(const void* rowptr, int rowptr_itype, const int32_t* col, int64_t N_dst,

@@ -91,6 +91,9 @@ hipError_t launch_validate_csr(const void* rowptr, int rp64, const int32_t* col,
                                int64_t N_src, int64_t E, int64_t* d_count, hipStream_t s);
 hipError_t launch_offset_copy(const int32_t* in, int64_t n, int32_t add, int32_t* out,
                               hipStream_t s);
+hipError_t launch_iota(int64_t n, int32_t* out, hipStream_t s);
+hipError_t launch_copy_f32(const float* in, int64_t n, float* out, hipStream_t s);
+hipError_t launch_validate_sorted(const int32_t* dst, int64_t E, int64_t* d_count, hipStream_t s);
 
 // ---- aggregation (spmm.hip) --------------------------------------------------
 enum : int { kSum = MP_SUM, kMean = MP_MEAN, kMax = MP_MAX };

@@ -268,15 +268,15 @@ __global__ __launch_bounds__(kSortBlock) void radix_onesweep(RadixPass p) {
 // thread covers kRowptrItems consecutive positions.
 constexpr int kRowptrItems = 8;
 
-template <typename RP>
+template <typename RP, bool VEC>
 __global__ __launch_bounds__(256) void rowptr_from_sorted(const uint32_t* __restrict__ keys,
                                                           int64_t E, int64_t N, RP* __restrict__ rowptr) {
     static_assert(kRowptrItems == 8, "two 16-byte loads per thread");
     const int64_t p0 = ((int64_t)blockIdx.x * 256 + threadIdx.x) * kRowptrItems;
     if (p0 > E) return;
     uint32_t k8[kRowptrItems];
-    if (p0 + kRowptrItems <= E) {
-        // keys is 256-byte aligned and p0 a multiple of 8: aligned 16-byte loads
+    if (VEC && p0 + kRowptrItems <= E) {
+        // VEC: keys is 16-byte aligned and p0 a multiple of 8, so the loads are aligned
         const uint4 a = reinterpret_cast<const uint4*>(keys + p0)[0];
         const uint4 b = reinterpret_cast<const uint4*>(keys + p0)[1];
         k8[0] = a.x; k8[1] = a.y; k8[2] = a.z; k8[3] = a.w;
@@ -316,7 +316,24 @@ __global__ __launch_bounds__(256) void offset_copy(const int32_t* __restrict__ i
     if (i < n) out[i] = in[i] + add;
 }
 
+__global__ __launch_bounds__(256) void iota_i32(int64_t n, int32_t* __restrict__ out) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < n) out[i] = (int32_t)i;
+}
+
+__global__ __launch_bounds__(256) void copy_f32(const float* __restrict__ in, int64_t n,
+                                                float* __restrict__ out) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i < n) out[i] = in[i];
+}
+
 __global__ void zero_i64(int64_t* p) { *p = 0; }
+
+__global__ __launch_bounds__(256) void validate_sorted(const int32_t* __restrict__ dst, int64_t E,
+                                                       unsigned long long* count) {
+    const int64_t i = (int64_t)blockIdx.x * 256 + threadIdx.x;
+    if (i > 0 && i < E && dst[i] < dst[i - 1]) atomicAdd(count, 1ull);
+}
 
 __global__ __launch_bounds__(256) void validate_coo(const int32_t* __restrict__ src,
                                                     const int32_t* __restrict__ dst, int64_t E,
@@ -406,12 +423,20 @@ hipError_t radix_sort_pass(const RadixPass& p, hipStream_t s) {
 hipError_t launch_rowptr_from_sorted(const uint32_t* keys, int64_t E, int64_t N, void* rowptr,
                                      int rp64, hipStream_t s) {
     const unsigned g = grid_for(ceil_div(E + 1, kRowptrItems), 256);
-    if (rp64)
-        hipLaunchKernelGGL(rowptr_from_sorted<int64_t>, dim3(g), dim3(256), 0, s, keys, E, N,
-                           static_cast<int64_t*>(rowptr));
-    else
-        hipLaunchKernelGGL(rowptr_from_sorted<int32_t>, dim3(g), dim3(256), 0, s, keys, E, N,
-                           static_cast<int32_t*>(rowptr));
+    const bool vec = reinterpret_cast<uintptr_t>(keys) % 16 == 0;
+    if (rp64) {
+        auto* rp = static_cast<int64_t*>(rowptr);
+        if (vec)
+            hipLaunchKernelGGL((rowptr_from_sorted<int64_t, true>), dim3(g), dim3(256), 0, s, keys, E, N, rp);
+        else
+            hipLaunchKernelGGL((rowptr_from_sorted<int64_t, false>), dim3(g), dim3(256), 0, s, keys, E, N, rp);
+    } else {
+        auto* rp = static_cast<int32_t*>(rowptr);
+        if (vec)
+            hipLaunchKernelGGL((rowptr_from_sorted<int32_t, true>), dim3(g), dim3(256), 0, s, keys, E, N, rp);
+        else
+            hipLaunchKernelGGL((rowptr_from_sorted<int32_t, false>), dim3(g), dim3(256), 0, s, keys, E, N, rp);
+    }
     return hipGetLastError();
 }
 
@@ -439,6 +464,27 @@ hipError_t launch_offset_copy(const int32_t* in, int64_t n, int32_t add, int32_t
                               hipStream_t s) {
     if (n <= 0) return hipSuccess;
     hipLaunchKernelGGL(offset_copy, dim3(grid_for(n, 256)), dim3(256), 0, s, in, n, add, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_iota(int64_t n, int32_t* out, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(iota_i32, dim3(grid_for(n, 256)), dim3(256), 0, s, n, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_copy_f32(const float* in, int64_t n, float* out, hipStream_t s) {
+    if (n <= 0) return hipSuccess;
+    hipLaunchKernelGGL(copy_f32, dim3(grid_for(n, 256)), dim3(256), 0, s, in, n, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_validate_sorted(const int32_t* dst, int64_t E, int64_t* d_count,
+                                  hipStream_t s) {
+    hipLaunchKernelGGL(zero_i64, dim3(1), dim3(1), 0, s, d_count);
+    if (E > 1)
+        hipLaunchKernelGGL(validate_sorted, dim3(grid_for(E, 256)), dim3(256), 0, s, dst, E,
+                           reinterpret_cast<unsigned long long*>(d_count));
     return hipGetLastError();
 }
 

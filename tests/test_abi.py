@@ -130,7 +130,20 @@ def test_hetero_errors():
                             0, None) == -4
 
 
+def test_sorted_coo_to_csr_errors():
+    L = mp.lib()
+    assert L.mp_sorted_coo_to_csr(FAKE, FAKE, 10, 5, FAKE, 7, FAKE, None, None, None, None) == -3
+    assert L.mp_sorted_coo_to_csr(FAKE, FAKE, 10, 5, None, 0, FAKE, None, None, None, None) == -1
+    assert L.mp_sorted_coo_to_csr(None, FAKE, 10, 5, FAKE, 0, FAKE, None, None, None, None) == -1
+    assert L.mp_sorted_coo_to_csr(FAKE, FAKE, 10, 5, FAKE, 0, FAKE, None, FAKE, None, None) == -1
+    assert L.mp_sorted_coo_to_csr(FAKE, FAKE, 10, 5, FAKE + 4, 1, FAKE, None, None, None,
+                                  None) == -8
+    assert L.mp_sorted_coo_to_csr(FAKE, FAKE, -1, 5, FAKE, 0, FAKE, None, None, None, None) < 0
+
+
 def test_validate_errors():
     L = mp.lib()
+    assert L.mp_validate_sorted(FAKE, 10, None, None) == -1
+    assert L.mp_validate_sorted(FAKE, -1, FAKE, None) == -2
     assert L.mp_validate_coo(FAKE, FAKE, 10, 5, 5, None, None) == -1
     assert L.mp_validate_csr(FAKE, 4, FAKE, 5, 5, 10, FAKE, None) == -3

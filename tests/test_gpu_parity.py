@@ -95,6 +95,40 @@ def test_csr_sorted_and_single_row():
     check_csr(src, np.full(30_000, 999, np.int32), n)  # every edge into the last row
 
 
+@pytest.mark.parametrize("n,e", [(1, 0), (7, 0), (1, 9), (300, 4095), (70_000, 12_289),
+                                 ((1 << 20) + 3, 50_001), (3, 200_000)])
+@pytest.mark.parametrize("itype", [torch.int32, torch.int64])
+@pytest.mark.parametrize("offset", [0, 1])
+def test_sorted_coo_to_csr(n, e, itype, offset):
+    # destination-sorted input: no sort runs and the result equals the stable sort's;
+    # offset 1 starts dst one element into its buffer (4-byte, not 16-byte, aligned)
+    dst = np.sort(graphgen.uniform_ints(n + e, 2, e, n))
+    src = graphgen.uniform_ints(n + e, 1, e, n)
+    val = graphgen.uniform_f32(n + e, 3, e)
+    pad = lambda a: dev(np.concatenate([np.zeros(offset, a.dtype), a]))[offset:]
+    s, d, v = pad(src), pad(dst), pad(val)
+    rp, col, perm, vout = mp.sorted_coo_to_csr(s, d, n, rowptr_dtype=itype, want_perm=True, val=v)
+    rp_o, col_o, perm_o, v_o = oracle.coo_to_csr(src, dst, n, val=val)
+    assert np.array_equal(rp.cpu().numpy().astype(np.int64), rp_o), "rowptr"
+    assert np.array_equal(col.cpu().numpy(), col_o), "col"
+    assert np.array_equal(perm.cpu().numpy().astype(np.int64), perm_o), "perm"
+    assert np.array_equal(vout.cpu().numpy().view(np.uint32), v_o.view(np.uint32)), "val"
+    cnt = torch.zeros(1, dtype=torch.int64, device=DEV)
+    mp.mp_validate_sorted(d, e, cnt)
+    assert int(cnt.item()) == 0
+
+
+def test_validate_sorted_counts_descents():
+    dst = np.sort(graphgen.uniform_ints(4, 2, 5000, 100))
+    bad = dst.copy()
+    bad[[0, 1]] = bad[[1, 0]]   # a descent at 1 unless the two are equal
+    bad[2500], bad[2501] = 99, 0  # a descent at 2501
+    expect = int(np.count_nonzero(bad[1:] < bad[:-1]))
+    cnt = torch.zeros(1, dtype=torch.int64, device=DEV)
+    mp.mp_validate_sorted(dev(bad), 5000, cnt)
+    assert int(cnt.item()) == expect and expect >= 1
+
+
 # ---- aggregation ---------------------------------------------------------------------
 
 REDUCES = {"sum": mp.MP_SUM, "mean": mp.MP_MEAN, "max": mp.MP_MAX,
