@@ -56,6 +56,14 @@ def _L():
         lib.oracle_hetero_sum.restype = i32
         lib.oracle_csr_rows.argtypes = [i64, i64, p, p, i64, p, p, p]
         lib.oracle_csr_rows.restype = i32
+        lib.oracle_csr_transpose.argtypes = [i64, i64, p, p, p, p, p]
+        lib.oracle_csr_transpose.restype = i32
+        lib.oracle_spmm_backward_x.argtypes = [i64, p, i64, i64, p, p, p, p, i32, i64, i32, p,
+                                               p, p]
+        lib.oracle_spmm_backward_x.restype = i32
+        lib.oracle_spmm_backward_w.argtypes = [i64, p, i64, i64, p, p, p, i32, p, i32, i64, i32,
+                                               p, p, p, i32]
+        lib.oracle_spmm_backward_w.restype = i32
         _lib = lib
     return _lib
 
@@ -196,3 +204,85 @@ def hetero_sum(n_per_type, x_bf16_per_type, rel_src_type, rel_dst_type, rel_src,
         raise ValueError(f"oracle_hetero_sum failed ({rc})")
     return outs, scs
 
+
+
+REDUCE_CODES = {"sum": 1, "mean": 2, "max": 4}
+
+
+def csr_transpose(rowptr, col, n_src):
+    """Source-major CSR of the same edges, stable in forward CSR order.
+
+    Returns (rowptrT int64[N_src+1], colT int32[E] = destination,
+    posT int64[E] = forward CSR position)."""
+    rowptr, col = _c(rowptr, np.int64), _c(col, np.int32)
+    n_dst = rowptr.shape[0] - 1
+    E = col.shape[0]
+    rpt = np.empty(n_src + 1, np.int64)
+    colt = np.empty(E, np.int32)
+    post = np.empty(E, np.int64)
+    rc = _L().oracle_csr_transpose(n_dst, n_src, _p(rowptr), _p(col), _p(rpt), _p(colt),
+                                   _p(post))
+    if rc != 0:
+        raise ValueError(f"oracle_csr_transpose failed ({rc})")
+    return rpt, colt, post
+
+
+def _g_args(g, g_bf16):
+    if g_bf16 is not None:
+        gb = _c(g_bf16, np.uint16)
+        return gb, 1, gb.shape[1]
+    gf = _c(g, np.float32)
+    return gf, 0, gf.shape[1]
+
+
+def spmm_backward_x(rowptr, col, n_src, reduce, g=None, g_bf16=None, w=None, argout=None,
+                    rows=None):
+    """Gradient of the aggregation with respect to x (sum, mean or max).
+
+    g (fp32 [N_dst, F], or g_bf16 bits) is the gradient of the output; w the
+    CSR-order edge weights (optional); argout [N_dst, F] the forward argmax
+    (max only).  Returns (gx fp64 [rows, F], scale fp64 [rows, F]) for the
+    listed source rows (all when rows is None)."""
+    rowptr, col = _c(rowptr, np.int64), _c(col, np.int32)
+    ga, gisb, F = _g_args(g, g_bf16)
+    n_dst = rowptr.shape[0] - 1
+    rows = _c(rows, np.int64)
+    n = n_src if rows is None else rows.shape[0]
+    w = _c(w, np.float32)
+    am = _c(argout, np.int64)
+    gx = np.empty((n, F), np.float64)
+    sc = np.empty((n, F), np.float64)
+    rc = _L().oracle_spmm_backward_x(n, _p(rows), n_dst, n_src, _p(rowptr), _p(col), _p(w),
+                                     _p(ga), gisb, F, REDUCE_CODES[reduce], _p(am), _p(gx),
+                                     _p(sc))
+    if rc != 0:
+        raise ValueError(f"oracle_spmm_backward_x failed ({rc})")
+    return gx, sc
+
+
+def spmm_backward_w(rowptr, col, reduce, x=None, x_bf16=None, g=None, g_bf16=None,
+                    argout=None, rows=None, nthreads=None):
+    """Gradient of the aggregation with respect to the CSR-order edge weights.
+
+    Returns (gw fp64 [E], scale fp64 [E]); with rows given, only the edges of
+    those destination rows are filled (the rest are NaN)."""
+    rowptr, col = _c(rowptr, np.int64), _c(col, np.int32)
+    xa, xisb, n_src, F = _x_args(x, x_bf16)
+    ga, gisb, Fg = _g_args(g, g_bf16)
+    if Fg != F:
+        raise ValueError("x and g widths differ")
+    n_dst = rowptr.shape[0] - 1
+    rows = _c(rows, np.int64)
+    n = n_dst if rows is None else rows.shape[0]
+    am = _c(argout, np.int64)
+    E = col.shape[0]
+    gw = np.full(E, np.nan, np.float64)
+    sc = np.full(E, np.nan, np.float64)
+    if nthreads is None:
+        nthreads = os.cpu_count() or 1
+    rc = _L().oracle_spmm_backward_w(n, _p(rows), n_dst, n_src, _p(rowptr), _p(col), _p(xa), xisb,
+                                     _p(ga), gisb, F, REDUCE_CODES[reduce], _p(am), _p(gw),
+                                     _p(sc), int(nthreads))
+    if rc != 0:
+        raise ValueError(f"oracle_spmm_backward_w failed ({rc})")
+    return gw, sc

@@ -30,6 +30,14 @@
  * Readings where the paper is silent: empty rows aggregate to 0 (and argmax
  * -1); max keeps the first edge (lowest CSR position) among equal values,
  * comparing with '>' so that -0.0 and +0.0 tie; mean is sum / in-degree.
+ *
+ * Backward (Sec. 2.2: the backward pass of an aggregation runs over the
+ * transposed adjacency, which is why CSR and CSC are both cached): the
+ * derivatives of the aggregation above with respect to the features x and the
+ * edge weights w, given the gradient g of its output.  The fp32 rounding of a
+ * weighted message is not differentiated (the message is taken as w * x).
+ * The max routes each output element's gradient to the one edge the forward
+ * pass reported for it (argmax), and nowhere for an empty row.
  */
 #include <math.h>
 #include <stdint.h>
@@ -373,4 +381,129 @@ int oracle_csr_rows(int64_t E, int64_t N_dst, const int32_t* src, const int32_t*
     free(fill);
     row_set_free(&set);
     return 0;
+}
+
+/* ---- transposed CSR (source-major) ------------------------------------- */
+
+/* The same edges grouped by source: rowptrT[N_src+1]; for the t-th edge in
+ * source order, colT[t] = its destination (the forward CSR row of the edge)
+ * and posT[t] = its forward CSR position.  Within a source, edges keep their
+ * forward CSR order (stable counting sort by col over the positions).
+ * Returns 0, -1 on an out-of-range column, -2 on allocation failure. */
+int oracle_csr_transpose(int64_t N_dst, int64_t N_src, const int64_t* rowptr,
+                         const int32_t* col, int64_t* rowptrT, int32_t* colT, int64_t* posT) {
+    int64_t E = rowptr[N_dst];
+    for (int64_t p = 0; p < E; ++p)
+        if (col[p] < 0 || col[p] >= N_src) return -1;
+    for (int64_t u = 0; u <= N_src; ++u) rowptrT[u] = 0;
+    for (int64_t p = 0; p < E; ++p) rowptrT[col[p] + 1] += 1;
+    for (int64_t u = 0; u < N_src; ++u) rowptrT[u + 1] += rowptrT[u];
+    int64_t* cursor = (int64_t*)malloc(sizeof(int64_t) * (size_t)(N_src > 0 ? N_src : 1));
+    if (!cursor) return -2;
+    for (int64_t u = 0; u < N_src; ++u) cursor[u] = rowptrT[u];
+    for (int64_t v = 0; v < N_dst; ++v)
+        for (int64_t p = rowptr[v]; p < rowptr[v + 1]; ++p) {
+            int64_t t = cursor[col[p]]++;
+            colT[t] = (int32_t)v;
+            posT[t] = p;
+        }
+    free(cursor);
+    return 0;
+}
+
+/* ---- gradients of the aggregation ---------------------------------------- */
+
+/* reduce codes of the backward functions */
+enum { ORACLE_SUM = 1, ORACLE_MEAN = 2, ORACLE_MAX = 4 };
+
+/* Coefficient with which g[v, f] reaches edge p (in row v) for feature f:
+ * sum 1, mean 1/deg(v), max 1 if argout[v, f] == p else 0. */
+static inline double route(int reduce, int64_t deg, const int64_t* argout, int64_t F,
+                           int64_t v, int64_t f, int64_t p) {
+    if (reduce == ORACLE_SUM) return 1.0;
+    if (reduce == ORACLE_MEAN) return 1.0 / (double)deg;
+    return argout[v * F + f] == p ? 1.0 : 0.0;
+}
+
+/* Gradient with respect to x, for the listed source rows (rows == NULL: all
+ * N_src rows, in order):
+ *   gx[k, f] = sum over forward CSR edges p with col[p] == u_k, in CSR order,
+ *              of route(v, f, p) * w_p * g[v, f]      (v = row of p; w_p = 1
+ *              when w is NULL)
+ *   scale[k, f] = the same sum of absolute values (error scale).
+ * g is [N_dst, F] fp32 or bf16 bits.  argout [N_dst, F] is needed for max.
+ * Returns 0, -1 on a bad index or reduce, -2 on allocation failure. */
+int oracle_spmm_backward_x(int64_t n_rows, const int64_t* rows, int64_t N_dst, int64_t N_src,
+                           const int64_t* rowptr, const int32_t* col, const float* w,
+                           const void* g, int g_is_bf16, int64_t F, int reduce,
+                           const int64_t* argout, double* gx, double* scale) {
+    if (reduce != ORACLE_SUM && reduce != ORACLE_MEAN && reduce != ORACLE_MAX) return -1;
+    if (reduce == ORACLE_MAX && !argout) return -1;
+    int64_t n = rows ? n_rows : N_src;
+    row_set set;
+    if (rows) {
+        int rc = row_set_make(&set, N_src, n_rows, rows);
+        if (rc != 0) return rc;
+    }
+    for (int64_t k = 0; k < n * F; ++k) {
+        gx[k] = 0.0;
+        if (scale) scale[k] = 0.0;
+    }
+    int bad = 0;
+    for (int64_t v = 0; v < N_dst && !bad; ++v) {
+        int64_t deg = rowptr[v + 1] - rowptr[v];
+        for (int64_t p = rowptr[v]; p < rowptr[v + 1]; ++p) {
+            int64_t u = col[p];
+            if (u < 0 || u >= N_src) { bad = 1; break; }
+            int64_t k = rows ? row_set_find(&set, u) : u;
+            if (k < 0) continue;
+            double wp = w ? (double)w[p] : 1.0;
+            for (int64_t f = 0; f < F; ++f) {
+                double t = route(reduce, deg, argout, F, v, f, p) * wp *
+                           (double)feature(g, g_is_bf16, F, v, f);
+                gx[k * F + f] += t;
+                if (scale) scale[k * F + f] += fabs(t);
+            }
+        }
+    }
+    if (rows) row_set_free(&set);
+    return bad ? -1 : 0;
+}
+
+/* Gradient with respect to the edge weights, for every CSR edge p of the
+ * listed destination rows (rows == NULL: all rows):
+ *   gw[p] = sum over f of route(v, f, p) * g[v, f] * x[col[p], f]
+ *   scale[p] = the same sum of absolute values.
+ * Entries of unlisted rows are left untouched.  x is [N_src, F], g is
+ * [N_dst, F], each fp32 or bf16 bits.  Rows are independent; nthreads > 0
+ * splits them over OpenMP threads.  Returns 0, or -1 on a bad index/reduce. */
+int oracle_spmm_backward_w(int64_t n_rows, const int64_t* rows, int64_t N_dst, int64_t N_src,
+                           const int64_t* rowptr, const int32_t* col, const void* x,
+                           int x_is_bf16, const void* g, int g_is_bf16, int64_t F, int reduce,
+                           const int64_t* argout, double* gw, double* scale, int nthreads) {
+    if (reduce != ORACLE_SUM && reduce != ORACLE_MEAN && reduce != ORACLE_MAX) return -1;
+    if (reduce == ORACLE_MAX && !argout) return -1;
+    int64_t n = rows ? n_rows : N_dst;
+    int bad = 0;
+#pragma omp parallel for schedule(dynamic, 64) num_threads(nthreads > 0 ? nthreads : 1) reduction(| : bad)
+    for (int64_t k = 0; k < n; ++k) {
+        int64_t v = rows ? rows[k] : k;
+        if (v < 0 || v >= N_dst) { bad = 1; continue; }
+        int64_t deg = rowptr[v + 1] - rowptr[v];
+        for (int64_t p = rowptr[v]; p < rowptr[v + 1]; ++p) {
+            int64_t u = col[p];
+            if (u < 0 || u >= N_src) { bad = 1; break; }
+            double s = 0.0, a = 0.0;
+            for (int64_t f = 0; f < F; ++f) {
+                double t = route(reduce, deg, argout, F, v, f, p) *
+                           (double)feature(g, g_is_bf16, F, v, f) *
+                           (double)feature(x, x_is_bf16, F, u, f);
+                s += t;
+                a += fabs(t);
+            }
+            gw[p] = s;
+            if (scale) scale[p] = a;
+        }
+    }
+    return bad ? -1 : 0;
 }
