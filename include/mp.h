@@ -183,6 +183,79 @@ int mp_spmm(const mp_plan* plan, const void* rowptr, int rowptr_itype, const int
             int32_t* argout, void* ws, size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * Backward pass (Sec. 2.2: the backward pass of an aggregation over A runs
+ * over the transposed adjacency, so the source-major CSR is built once and
+ * kept next to the destination-major one, like the cached CSC).  Given the
+ * gradient G = dL/d out of mp_spmm's output, with v = the destination row of
+ * CSR edge p and route(v, f, p) = 1 (MP_SUM), 1/deg(v) (MP_MEAN) or
+ * [argout[v, f] == p] (MP_MAX):
+ *     dL/dx[u, f] = sum over edges p with col[p] == u of route * w[p] * G[v, f]
+ *     dL/dw[p]    = sum over f of route * G[v, f] * x[col[p], f]
+ * The fp32 rounding of a weighted message is not differentiated.  For an
+ * undirected graph with symmetric weights the forward CSR is its own
+ * transpose for MP_SUM and MP_MEAN (pass it as rowptrT/colT/wT, posT NULL).
+ * ------------------------------------------------------------------------- */
+
+/* Workspace bytes for mp_csr_transpose (with_payload: posT or val_out is
+ * requested). */
+int mp_csr_transpose_workspace(int64_t E, int64_t N_src, int rowptrT_itype, int with_payload,
+                               size_t* bytes);
+
+/* Source-major CSR of the edges of a destination-major CSR.
+ *   rowptr      [N_dst+1] of rowptr_itype, col [E] int32: the forward CSR.
+ *   rowptrT     [N_src+1] of rowptrT_itype: out, edges per source.
+ *   colT        [E] int32: out, the destination (forward row) of each edge.
+ *   posT        [E] int32 or NULL: out, the forward CSR position of each edge.
+ *   val_in      [E] fp32 in forward CSR order, or NULL; val_out [E] receives
+ *               val_in[posT[t]] (both or neither).
+ * Within a source, edges keep their forward CSR order (a stable sort by col),
+ * so the result is unique and bit-exact.  Sizes: 1 <= N_dst, N_src <=
+ * INT32_MAX, 0 <= E <= INT32_MAX.  Asynchronous on `stream`. */
+int mp_csr_transpose(const void* rowptr, int rowptr_itype, const int32_t* col, int64_t N_dst,
+                     int64_t N_src, int64_t E, void* rowptrT, int rowptrT_itype, int32_t* colT,
+                     int32_t* posT, const float* val_in, float* val_out, void* ws,
+                     size_t ws_bytes, void* stream);
+
+/* Workspace bytes for mp_spmm_backward_x (hub partials of planT; for MP_MEAN
+ * also an fp32 copy of G divided by the in-degrees, N_dst * F * 4 bytes). */
+int mp_spmm_backward_x_workspace(const mp_plan* planT, int64_t N_dst, int64_t F, int reduce,
+                                 size_t* bytes);
+
+/* dL/dx of mp_spmm for one reduction (MP_SUM, MP_MEAN or MP_MAX; for a fused
+ * forward call add the gradients of its parts).
+ *   planT       plan built on rowptrT (N_src rows, same F), or NULL.
+ *   rowptrT, colT, posT, wT   from mp_csr_transpose (wT = the forward weights
+ *               in transposed order, NULL if unweighted; posT needed for MAX).
+ *   rowptr      the forward rowptr (needed for MP_MEAN: in-degrees).
+ *   argout      [N_dst, F] int32 from the forward call (needed for MP_MAX).
+ *   grad_out    [N_dst, F] of g_dtype: G.
+ *   grad_x      [N_src, F] of out_dtype, written in full (fp32 accumulation;
+ *               a bf16 output is rounded to nearest even once).
+ * Deterministic: one gather-reduce per source row, no atomics.  Asynchronous
+ * on `stream`. */
+int mp_spmm_backward_x(const mp_plan* planT, const void* rowptrT, int rowptrT_itype,
+                       const int32_t* colT, const int32_t* posT, const float* wT,
+                       const void* rowptr, int rowptr_itype, const int32_t* argout,
+                       const void* grad_out, int g_dtype, int64_t N_dst, int64_t N_src, int64_t F,
+                       int reduce, void* grad_x, int out_dtype, void* ws, size_t ws_bytes,
+                       void* stream);
+
+/* Workspace bytes for mp_spmm_backward_w (the row of every CSR edge, 4E). */
+int mp_spmm_backward_w_workspace(int64_t E, size_t* bytes);
+
+/* dL/dw of a weighted mp_spmm for one reduction: one dot product of G[v, :]
+ * and x[col[p], :] per forward CSR edge p (fp32, a fixed reduction order).
+ *   x           [N_src, F] of x_dtype; grad_out [N_dst, F] of g_dtype.
+ *   argout      [N_dst, F] int32 from the forward call (needed for MP_MAX).
+ *   grad_w      [E] fp32 out, forward CSR order (map to COO order with perm).
+ * Sizes: 1 <= N_dst, 0 <= N_src, E <= INT32_MAX, 1 <= F <= 65536.
+ * Asynchronous on `stream`. */
+int mp_spmm_backward_w(const void* rowptr, int rowptr_itype, const int32_t* col, const void* x,
+                       int x_dtype, const void* grad_out, int g_dtype, const int32_t* argout,
+                       int64_t N_src, int64_t N_dst, int64_t E, int64_t F, int reduce,
+                       float* grad_w, void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Heterogeneous message passing (Sec. 2.2, nested Eq. (1)): per destination
  * node type T, out_T = sum over relations r ending at T (ascending r) of the
  * sum aggregation over r's edges.  Built as one combined destination-major

@@ -23,6 +23,9 @@ __all__ = [
     "MPError", "lib", "MP_F32", "MP_BF16", "MP_I32", "MP_I64", "MP_SUM", "MP_MEAN", "MP_MAX",
     "mp_version", "mp_status_str", "mp_coo_to_csr_workspace", "mp_coo_to_csr",
     "mp_sorted_coo_to_csr", "mp_validate_sorted", "sorted_coo_to_csr",
+    "mp_csr_transpose_workspace", "mp_csr_transpose", "mp_spmm_backward_x_workspace",
+    "mp_spmm_backward_x", "mp_spmm_backward_w_workspace", "mp_spmm_backward_w",
+    "csr_transpose", "spmm_backward_x", "spmm_backward_w",
     "mp_spmm_plan_size", "mp_spmm_plan_build", "mp_spmm_plan_free", "mp_spmm_workspace",
     "mp_spmm", "mp_hetero_build_workspace", "mp_hetero_build", "mp_hetero_spmm",
     "mp_validate_coo", "mp_validate_csr", "coo_to_csr", "Plan", "spmm", "hetero_build",
@@ -84,8 +87,18 @@ def lib():
         L.mp_validate_coo.argtypes = [p, p, i64, i64, i64, p, p]
         L.mp_validate_csr.argtypes = [p, i32, p, i64, i64, i64, p, p]
         L.mp_validate_sorted.argtypes = [p, i64, p, p]
+        L.mp_csr_transpose_workspace.argtypes = [i64, i64, i32, i32, psz]
+        L.mp_csr_transpose.argtypes = [p, i32, p, i64, i64, i64, p, i32, p, p, p, p, p, sz, p]
+        L.mp_spmm_backward_x_workspace.argtypes = [p, i64, i64, i32, psz]
+        L.mp_spmm_backward_x.argtypes = [p, p, i32, p, p, p, p, i32, p, p, i32, i64, i64, i64,
+                                         i32, p, i32, p, sz, p]
+        L.mp_spmm_backward_w_workspace.argtypes = [i64, psz]
+        L.mp_spmm_backward_w.argtypes = [p, i32, p, p, i32, p, i32, p, i64, i64, i64, i64, i32, p,
+                                         p, sz, p]
         for name in ("mp_coo_to_csr_workspace", "mp_coo_to_csr", "mp_sorted_coo_to_csr",
-                     "mp_validate_sorted", "mp_spmm_plan_size",
+                     "mp_validate_sorted", "mp_csr_transpose_workspace", "mp_csr_transpose",
+                     "mp_spmm_backward_x_workspace", "mp_spmm_backward_x",
+                     "mp_spmm_backward_w_workspace", "mp_spmm_backward_w", "mp_spmm_plan_size",
                      "mp_spmm_plan_build", "mp_spmm_workspace", "mp_spmm",
                      "mp_hetero_build_workspace", "mp_hetero_build", "mp_hetero_spmm",
                      "mp_validate_coo", "mp_validate_csr"):
@@ -236,6 +249,42 @@ def mp_validate_coo(src, dst, E, N_src, N_dst, d_count, stream=None):
                                                     _ptr(d_count), _stream(stream)))
 
 
+def mp_csr_transpose_workspace(E, N_src, rowptrT_itype, with_payload) -> int:
+    return _bytes("mp_csr_transpose_workspace", E, N_src, rowptrT_itype, int(with_payload))
+
+
+def mp_csr_transpose(rowptr, rowptr_itype, col, N_dst, N_src, E, rowptrT, rowptrT_itype, colT,
+                     posT, val_in, val_out, ws, ws_bytes, stream=None):
+    _check("mp_csr_transpose", lib().mp_csr_transpose(
+        _ptr(rowptr), rowptr_itype, _ptr(col), N_dst, N_src, E, _ptr(rowptrT), rowptrT_itype,
+        _ptr(colT), _ptr(posT), _ptr(val_in), _ptr(val_out), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def mp_spmm_backward_x_workspace(planT_handle, N_dst, F, reduce) -> int:
+    return _bytes("mp_spmm_backward_x_workspace", planT_handle, N_dst, F, reduce)
+
+
+def mp_spmm_backward_x(planT_handle, rowptrT, rowptrT_itype, colT, posT, wT, rowptr,
+                       rowptr_itype, argout, grad_out, g_dtype, N_dst, N_src, F, reduce, grad_x,
+                       out_dtype, ws, ws_bytes, stream=None):
+    _check("mp_spmm_backward_x", lib().mp_spmm_backward_x(
+        planT_handle, _ptr(rowptrT), rowptrT_itype, _ptr(colT), _ptr(posT), _ptr(wT),
+        _ptr(rowptr), rowptr_itype, _ptr(argout), _ptr(grad_out), g_dtype, N_dst, N_src, F,
+        reduce, _ptr(grad_x), out_dtype, _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def mp_spmm_backward_w_workspace(E) -> int:
+    return _bytes("mp_spmm_backward_w_workspace", E)
+
+
+def mp_spmm_backward_w(rowptr, rowptr_itype, col, x, x_dtype, grad_out, g_dtype, argout, N_src,
+                       N_dst, E, F, reduce, grad_w, ws, ws_bytes, stream=None):
+    _check("mp_spmm_backward_w", lib().mp_spmm_backward_w(
+        _ptr(rowptr), rowptr_itype, _ptr(col), _ptr(x), x_dtype, _ptr(grad_out), g_dtype,
+        _ptr(argout), N_src, N_dst, E, F, reduce, _ptr(grad_w), _ptr(ws), ws_bytes,
+        _stream(stream)))
+
+
 def mp_validate_sorted(dst, E, d_count, stream=None):
     _check("mp_validate_sorted", lib().mp_validate_sorted(_ptr(dst), E, _ptr(d_count),
                                                           _stream(stream)))
@@ -345,6 +394,62 @@ def spmm(rowptr, col, x, reduce, *, w=None, plan: Plan | None = None, out_dtype=
             _dtype_code(out_max.dtype) if hm else MP_F32, argout if hm else None, ws,
             0 if ws is None else ws.numel(), stream)
     return (out if hs else None, out_max if hm else None, argout if hm else None)
+
+
+def csr_transpose(rowptr, col, N_src, *, rowptrT_dtype=torch.int32, want_pos=True, val=None,
+                  stream=None):
+    """Source-major CSR of a destination-major CSR's edges.
+
+    Returns (rowptrT, colT = destinations, posT = forward CSR positions or
+    None, val in transposed order or None)."""
+    N_dst = int(rowptr.numel()) - 1
+    E = int(col.numel())
+    dev = col.device
+    itT = _itype_code(rowptrT_dtype)
+    rowptrT = torch.empty(N_src + 1, dtype=rowptrT_dtype, device=dev)
+    colT = torch.empty(E, dtype=torch.int32, device=dev)
+    posT = torch.empty(E, dtype=torch.int32, device=dev) if want_pos else None
+    vout = torch.empty(E, dtype=torch.float32, device=dev) if val is not None else None
+    nb = mp_csr_transpose_workspace(E, N_src, itT, want_pos or val is not None)
+    ws = _workspace(nb, dev) if nb else None
+    mp_csr_transpose(rowptr, _itype_code(rowptr.dtype), col, N_dst, N_src, E, rowptrT, itT, colT,
+                     posT, val, vout, ws, 0 if ws is None else ws.numel(), stream)
+    return rowptrT, colT, posT, vout
+
+
+def spmm_backward_x(rowptrT, colT, grad_out, reduce, *, posT=None, wT=None, rowptr=None,
+                    argout=None, planT: Plan | None = None, out_dtype=torch.float32, out=None,
+                    stream=None):
+    """dL/dx of spmm for one reduction, over the transposed CSR."""
+    N_src = int(rowptrT.numel()) - 1
+    N_dst, F = int(grad_out.shape[0]), int(grad_out.shape[1])
+    dev = grad_out.device
+    if out is None:
+        out = torch.empty(N_src, F, dtype=out_dtype, device=dev)
+    h = planT.handle if planT is not None else None
+    nb = mp_spmm_backward_x_workspace(h, N_dst, F, reduce)
+    ws = _workspace(nb, dev) if nb else None
+    mp_spmm_backward_x(h, rowptrT, _itype_code(rowptrT.dtype), colT, posT, wT, rowptr,
+                       _itype_code(rowptr.dtype) if rowptr is not None else MP_I32, argout,
+                       grad_out, _dtype_code(grad_out.dtype), N_dst, N_src, F, reduce, out,
+                       _dtype_code(out.dtype), ws, 0 if ws is None else ws.numel(), stream)
+    return out
+
+
+def spmm_backward_w(rowptr, col, x, grad_out, reduce, *, argout=None, out=None, stream=None):
+    """dL/dw (forward CSR order, fp32) of a weighted spmm for one reduction."""
+    N_dst = int(rowptr.numel()) - 1
+    N_src, F = int(x.shape[0]), int(x.shape[1])
+    E = int(col.numel())
+    dev = x.device
+    if out is None:
+        out = torch.empty(E, dtype=torch.float32, device=dev)
+    nb = mp_spmm_backward_w_workspace(E)
+    ws = _workspace(nb, dev) if nb else None
+    mp_spmm_backward_w(rowptr, _itype_code(rowptr.dtype), col, x, _dtype_code(x.dtype), grad_out,
+                       _dtype_code(grad_out.dtype), argout, N_src, N_dst, E, F, reduce, out, ws,
+                       0 if ws is None else ws.numel(), stream)
+    return out
 
 
 def hetero_build(N_per_type, rels, dst_type, *, rowptr_dtype=torch.int32, stream=None):

@@ -452,6 +452,191 @@ int mp_spmm(const mp_plan* plan, const void* rowptr, int rowptr_itype, const int
     return run_spmm(plan, P, g, x_dtype, N_dst, ws, ws_bytes, as_stream(stream));
 }
 
+// ---- backward ------------------------------------------------------------------
+
+int mp_csr_transpose_workspace(int64_t E, int64_t N_src, int rowptrT_itype, int with_payload,
+                               size_t* bytes) {
+    if (!bytes) return MP_ERR_NULL;
+    if (!valid_itype(rowptrT_itype)) return MP_ERR_DTYPE;
+    int st = check_csr_sizes(E, N_src);
+    if (st != MP_OK) return st;
+    if (E == 0) {
+        *bytes = 0;
+        return MP_OK;
+    }
+    *bytes = align_up((size_t)E * 4, 256) + csr_layout(nullptr, E, N_src, with_payload ? 1 : 0).bytes;
+    return MP_OK;
+}
+
+int mp_csr_transpose(const void* rowptr, int rowptr_itype, const int32_t* col, int64_t N_dst,
+                     int64_t N_src, int64_t E, void* rowptrT, int rowptrT_itype, int32_t* colT,
+                     int32_t* posT, const float* val_in, float* val_out, void* ws,
+                     size_t ws_bytes, void* stream) {
+    if (!valid_itype(rowptr_itype) || !valid_itype(rowptrT_itype)) return MP_ERR_DTYPE;
+    int st = check_csr_sizes(E, N_src);
+    if (st != MP_OK) return st;
+    if (N_dst < 1 || N_dst > INT32_MAX) return MP_ERR_SIZE;
+    if (!rowptr || !rowptrT) return MP_ERR_NULL;
+    if (E > 0 && (!col || !colT || !ws)) return MP_ERR_NULL;
+    if ((val_in == nullptr) != (val_out == nullptr)) return MP_ERR_NULL;
+    if ((uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4) ||
+        (uintptr_t)rowptrT % (rowptrT_itype == MP_I64 ? 8 : 4))
+        return MP_ERR_ALIGN;
+    hipStream_t s = as_stream(stream);
+    if (E == 0) return hip_status(launch_fill_rowptr_zero(N_src, rowptrT, rowptrT_itype == MP_I64, s));
+    size_t need = 0;
+    mp_csr_transpose_workspace(E, N_src, rowptrT_itype, posT || val_out, &need);
+    if (ws_bytes < need) return MP_ERR_WORKSPACE;
+    // the forward CSR listed as COO (row of every position, col) is already in
+    // position order, so a stable sort by col keeps forward order per source
+    Carver c(ws);
+    int32_t* row = c.take<int32_t>((size_t)E);
+    if (launch_rows_of_edges(rowptr, rowptr_itype == MP_I64, N_dst, E, row, s) != hipSuccess)
+        return MP_ERR_HIP;
+    return coo_to_csr_impl(row, col, E, N_src, rowptrT, rowptrT_itype, colT, posT, val_in,
+                           val_out, static_cast<char*>(ws) + c.off, ws_bytes - c.off, s);
+}
+
+int mp_spmm_backward_x_workspace(const mp_plan* planT, int64_t N_dst, int64_t F, int reduce,
+                                 size_t* bytes) {
+    if (!bytes) return MP_ERR_NULL;
+    if (reduce != MP_SUM && reduce != MP_MEAN && reduce != MP_MAX) return MP_ERR_REDUCE;
+    if (N_dst < 0 || F < 1) return MP_ERR_SIZE;
+    size_t b = 0;
+    int st = mp_spmm_workspace(planT, MP_SUM, &b);
+    if (st != MP_OK) return st;
+    if (reduce == MP_MEAN) b = align_up(b, 256) + align_up((size_t)N_dst * (size_t)F * 4, 256);
+    *bytes = b;
+    return MP_OK;
+}
+
+int mp_spmm_backward_x(const mp_plan* planT, const void* rowptrT, int rowptrT_itype,
+                       const int32_t* colT, const int32_t* posT, const float* wT,
+                       const void* rowptr, int rowptr_itype, const int32_t* argout,
+                       const void* grad_out, int g_dtype, int64_t N_dst, int64_t N_src, int64_t F,
+                       int reduce, void* grad_x, int out_dtype, void* ws, size_t ws_bytes,
+                       void* stream) {
+    if (reduce != MP_SUM && reduce != MP_MEAN && reduce != MP_MAX) return MP_ERR_REDUCE;
+    if (!valid_itype(rowptrT_itype) || !valid_dtype(g_dtype) || !valid_dtype(out_dtype))
+        return MP_ERR_DTYPE;
+    if (reduce == MP_MEAN && !valid_itype(rowptr_itype)) return MP_ERR_DTYPE;
+    if (N_src < 0 || N_src > INT32_MAX || N_dst < 0 || N_dst > INT32_MAX || F < 1 || F > 65536)
+        return MP_ERR_SIZE;
+    if (!rowptrT) return MP_ERR_NULL;
+    if (N_src > 0) {
+        if (!colT || !grad_out || !grad_x) return MP_ERR_NULL;
+        if (reduce == MP_MEAN && !rowptr) return MP_ERR_NULL;
+        if (reduce == MP_MAX && (!argout || !posT)) return MP_ERR_NULL;
+    }
+    int st = check_plan(planT, rowptrT, rowptrT_itype, N_src, F);
+    if (st != MP_OK) return st;
+    const int eb = g_dtype == MP_BF16 ? 2 : 4;
+    if ((uintptr_t)grad_out % eb || (uintptr_t)rowptrT % (rowptrT_itype == MP_I64 ? 8 : 4) ||
+        (uintptr_t)colT % 4 || (uintptr_t)posT % 4 || (uintptr_t)wT % 4 ||
+        (uintptr_t)argout % 4 || (uintptr_t)grad_x % (out_dtype == MP_BF16 ? 2 : 4) ||
+        (reduce == MP_MEAN && (uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4)))
+        return MP_ERR_ALIGN;
+    if (N_src == 0) return MP_OK;
+    hipStream_t s = as_stream(stream);
+    const void* table = grad_out;
+    int t_dtype = g_dtype;
+    void* spmm_ws = ws;
+    size_t spmm_ws_bytes = ws_bytes;
+    if (reduce == MP_MEAN) {
+        // mean: a sum over the transposed CSR of grad_out / in-degree
+        size_t part = 0;
+        mp_spmm_workspace(planT, MP_SUM, &part);
+        part = align_up(part, 256);
+        const size_t need = part + align_up((size_t)N_dst * (size_t)F * 4, 256);
+        if (ws_bytes < need || (!ws && need > 0)) return MP_ERR_WORKSPACE;
+        float* scaled = reinterpret_cast<float*>(static_cast<char*>(ws) + part);
+        if (launch_scale_inv_deg(grad_out, g_dtype == MP_BF16, rowptr, rowptr_itype == MP_I64,
+                                 N_dst, F, scaled, s) != hipSuccess)
+            return MP_ERR_HIP;
+        table = scaled;
+        t_dtype = MP_F32;
+        spmm_ws_bytes = part;
+    }
+    // the mask table is read in lane-chunks of EPL int32: keep its alignment
+    // within what the feature geometry assumes
+    const uintptr_t mask_align =
+        reduce == MP_MAX ? (t_dtype == MP_BF16 ? (uintptr_t)argout >> 1 : (uintptr_t)argout) : 0;
+    Geometry g = make_geometry(F, t_dtype, (uintptr_t)table | mask_align);
+    SpmmParams P{};
+    P.rowptr = rowptrT;
+    P.rp64 = rowptrT_itype == MP_I64;
+    P.col = colT;
+    P.w = wT;
+    P.n_tables = 1;
+    P.table_ptr[0] = static_cast<const char*>(table);
+    P.F = F;
+    P.reduce = MP_SUM;
+    P.out = grad_x;
+    P.out_bf16 = out_dtype == MP_BF16;
+    P.vec_store = ((uintptr_t)grad_x % 16) == 0;
+    if (reduce == MP_MAX) {
+        P.ekey = posT;
+        P.mtab = argout;
+    }
+    return run_spmm(planT, P, g, t_dtype, N_src, spmm_ws, spmm_ws_bytes, s);
+}
+
+int mp_spmm_backward_w_workspace(int64_t E, size_t* bytes) {
+    if (!bytes) return MP_ERR_NULL;
+    if (E < 0 || E > INT32_MAX) return MP_ERR_SIZE;
+    *bytes = E == 0 ? 0 : align_up((size_t)E * 4, 256);
+    return MP_OK;
+}
+
+int mp_spmm_backward_w(const void* rowptr, int rowptr_itype, const int32_t* col, const void* x,
+                       int x_dtype, const void* grad_out, int g_dtype, const int32_t* argout,
+                       int64_t N_src, int64_t N_dst, int64_t E, int64_t F, int reduce,
+                       float* grad_w, void* ws, size_t ws_bytes, void* stream) {
+    if (reduce != MP_SUM && reduce != MP_MEAN && reduce != MP_MAX) return MP_ERR_REDUCE;
+    if (!valid_itype(rowptr_itype) || !valid_dtype(x_dtype) || !valid_dtype(g_dtype))
+        return MP_ERR_DTYPE;
+    if (N_src < 0 || N_src > INT32_MAX || N_dst < 1 || N_dst > INT32_MAX || E < 0 ||
+        E > INT32_MAX || F < 1 || F > 65536)
+        return MP_ERR_SIZE;
+    if (!rowptr) return MP_ERR_NULL;
+    if (E == 0) return MP_OK;
+    if (!col || !x || !grad_out || !grad_w || !ws) return MP_ERR_NULL;
+    if (reduce == MP_MAX && !argout) return MP_ERR_NULL;
+    if (ws_bytes < align_up((size_t)E * 4, 256)) return MP_ERR_WORKSPACE;
+    const int ex = x_dtype == MP_BF16 ? 2 : 4, eg = g_dtype == MP_BF16 ? 2 : 4;
+    if ((uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4) || (uintptr_t)col % 4 ||
+        (uintptr_t)x % ex || (uintptr_t)grad_out % eg || (uintptr_t)argout % 4 ||
+        (uintptr_t)grad_w % 4)
+        return MP_ERR_ALIGN;
+    hipStream_t s = as_stream(stream);
+    int32_t* row = static_cast<int32_t*>(ws);
+    if (launch_rows_of_edges(rowptr, rowptr_itype == MP_I64, N_dst, E, row, s) != hipSuccess)
+        return MP_ERR_HIP;
+    // one lane-chunk of EPL elements per table: x's vector width must keep
+    // every table's chunk aligned (g and argout scaled to x's element size)
+    uintptr_t al = (uintptr_t)x;
+    al |= eg == ex ? (uintptr_t)grad_out : (eg > ex ? (uintptr_t)grad_out >> 1 : (uintptr_t)grad_out << 1);
+    if (reduce == MP_MAX) al |= ex == 4 ? (uintptr_t)argout : (uintptr_t)argout >> 1;
+    Geometry g = make_geometry(F, x_dtype, al);
+    GradWParams P{};
+    P.rowptr = rowptr;
+    P.rp64 = rowptr_itype == MP_I64;
+    P.col = col;
+    P.row = row;
+    P.x = x;
+    P.g = grad_out;
+    P.argout = argout;
+    P.F = F;
+    P.E = E;
+    P.L = g.L;
+    P.S = g.S;
+    P.FT = g.FT;
+    P.ltot = g.ltot;
+    P.reduce = reduce;
+    P.grad_w = grad_w;
+    return hip_status(launch_spmm_grad_w(P, x_dtype, g_dtype, g.epl, s));
+}
+
 // ---- heterogeneous ----------------------------------------------------------
 
 static int hetero_check(int n_types, const int64_t* N_per_type, int n_rel, const mp_relation* rels,

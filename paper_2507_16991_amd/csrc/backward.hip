@@ -1,0 +1,275 @@
+// Backward pass of the aggregation (Sec. 2.2 of PyG 2.0: the gradient of an
+// aggregation over A runs over the transposed adjacency, which the library
+// builds once as a source-major CSR, the analogue of the cached CSC).
+//
+//   * rows_of_edges: the destination row of every forward CSR position (the
+//     keys the transposed CSR is sorted by carry it as payload).
+//   * scale_inv_deg: grad_out / in-degree per destination row, the input of
+//     the gradient of mean.
+//   * spmm_grad_w: the gradient with respect to the edge weights, one dot
+//     product of grad_out[v] and x[col[p]] per CSR edge p of row v (a
+//     sampled dense-dense product).  Edge-parallel: every wavefront takes 64
+//     consecutive CSR positions, so hub rows need no special handling; the
+//     per-edge dot is reduced over the lanes of a slot in a fixed tree.
+//
+// The gradient with respect to x reuses the aggregation kernels of spmm.hip
+// over the transposed CSR (sum, mean after scale_inv_deg, and a masked sum
+// for max).
+#include <type_traits>
+
+#include "mp_internal.hpp"
+
+namespace mp {
+namespace {
+
+constexpr int kBlock = 256;
+constexpr int kWavesPerBlock = kBlock / kWave;
+constexpr int kRowItems = 8;  // CSR positions per thread in rows_of_edges
+
+__device__ inline int64_t rp_at(const void* rp, int rp64, int64_t i) {
+    return rp64 ? static_cast<const int64_t*>(rp)[i] : (int64_t) static_cast<const int32_t*>(rp)[i];
+}
+
+// row[p] = the v with rowptr[v] <= p < rowptr[v+1].  One binary search per
+// thread for its first position, then a forward walk over its 8 positions.
+__global__ __launch_bounds__(kBlock) void rows_of_edges(const void* __restrict__ rowptr, int rp64,
+                                                        int64_t N, int64_t E,
+                                                        int32_t* __restrict__ row) {
+    const int64_t p0 = ((int64_t)blockIdx.x * kBlock + threadIdx.x) * kRowItems;
+    if (p0 >= E) return;
+    // largest v in [0, N) with rowptr[v] <= p0
+    int64_t lo = 0, hi = N - 1;
+    while (lo < hi) {
+        const int64_t mid = (lo + hi + 1) >> 1;
+        if (rp_at(rowptr, rp64, mid) <= p0) lo = mid; else hi = mid - 1;
+    }
+    int64_t v = lo;
+    int64_t next = rp_at(rowptr, rp64, v + 1);
+#pragma unroll
+    for (int k = 0; k < kRowItems; ++k) {
+        const int64_t p = p0 + k;
+        if (p >= E) break;
+        while (next <= p && v + 1 < N) {  // skip rows ending at or before p (and empty rows)
+            ++v;
+            next = rp_at(rowptr, rp64, v + 1);
+        }
+        row[p] = (int32_t)v;
+    }
+}
+
+__device__ inline float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+
+// out[v, f] = g[v, f] / deg(v) in fp32 (0 for an empty row).
+template <bool GB>
+__global__ __launch_bounds__(kBlock) void scale_inv_deg(const void* __restrict__ g,
+                                                        const void* __restrict__ rowptr, int rp64,
+                                                        int64_t N, int64_t F,
+                                                        float* __restrict__ out) {
+    const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (i >= N * F) return;
+    const int64_t v = i / F;
+    const int64_t deg = rp_at(rowptr, rp64, v + 1) - rp_at(rowptr, rp64, v);
+    const float gv = GB ? bf16_bits_to_f32(static_cast<const uint16_t*>(g)[i])
+                        : static_cast<const float*>(g)[i];
+    out[i] = deg > 0 ? gv / (float)deg : 0.f;
+}
+
+// EPL consecutive values of a fp32 or bf16 row, widened to fp32; p is aligned
+// to min(16, EPL * sizeof(T)) bytes.
+template <typename T, int EPL>
+__device__ inline void load_vals(const T* p, float (&v)[EPL]) {
+    if constexpr (std::is_same<T, float>::value) {
+        if constexpr (EPL >= 4) {
+#pragma unroll
+            for (int q = 0; q < EPL / 4; ++q) {
+                const float4 a = reinterpret_cast<const float4*>(p)[q];
+                v[4 * q + 0] = a.x; v[4 * q + 1] = a.y; v[4 * q + 2] = a.z; v[4 * q + 3] = a.w;
+            }
+        } else if constexpr (EPL == 2) {
+            const float2 a = *reinterpret_cast<const float2*>(p);
+            v[0] = a.x; v[1] = a.y;
+        } else {
+            v[0] = *p;
+        }
+    } else {
+        uint32_t u[(EPL + 1) / 2];
+        if constexpr (EPL == 8) {
+            const uint4 a = *reinterpret_cast<const uint4*>(p);
+            u[0] = a.x; u[1] = a.y; u[2] = a.z; u[3] = a.w;
+        } else if constexpr (EPL == 4) {
+            const uint2 a = *reinterpret_cast<const uint2*>(p);
+            u[0] = a.x; u[1] = a.y;
+        } else if constexpr (EPL == 2) {
+            u[0] = *reinterpret_cast<const uint32_t*>(p);
+        } else {
+            u[0] = *reinterpret_cast<const uint16_t*>(p);
+        }
+#pragma unroll
+        for (int k = 0; k < EPL; ++k)
+            v[k] = (k & 1) ? __uint_as_float(u[k / 2] & 0xFFFF0000u) : bf16_bits_to_f32(u[k / 2] & 0xFFFFu);
+    }
+}
+
+template <int EPL>
+__device__ inline void load_ints(const int32_t* p, int32_t (&v)[EPL]) {
+    if constexpr (EPL >= 4) {
+#pragma unroll
+        for (int q = 0; q < EPL / 4; ++q) {
+            const int4 a = reinterpret_cast<const int4*>(p)[q];
+            v[4 * q + 0] = a.x; v[4 * q + 1] = a.y; v[4 * q + 2] = a.z; v[4 * q + 3] = a.w;
+        }
+    } else if constexpr (EPL == 2) {
+        const int2 a = *reinterpret_cast<const int2*>(p);
+        v[0] = a.x; v[1] = a.y;
+    } else {
+        v[0] = *p;
+    }
+}
+
+// grad_w[p] = sum_f route(v, f, p) * g[v, f] * x[col[p], f] for the CSR edge
+// p of row v = row[p]; route is 1 (sum), 1/deg(v) (mean, applied to the
+// finished dot) or [argout[v, f] == p] (max).  A wavefront takes 64
+// consecutive positions; slot s of its S slots takes positions base + u*S + s
+// (u < U) of each step, its L lanes covering the feature row in FT tiles.
+template <typename TX, typename TG, int EPL, int MODE>
+__global__ __launch_bounds__(kBlock) void spmm_grad_w(GradWParams P) {
+    constexpr int U = MODE == kMax ? 4 : 8;
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave)) +
+                       (int64_t)blockIdx.x * kWavesPerBlock;
+    const int64_t p0 = wv * kWave;
+    if (p0 >= P.E) return;
+    const int L = P.L, S = P.S;
+    const int slot = lane / L;
+    const int j = lane - slot * L;
+    const bool slot_ok = slot < S;
+    const int64_t rem = P.E - p0;
+
+    int32_t myc = 0, myv = 0;
+    if (lane < rem) {
+        myc = __builtin_nontemporal_load(P.col + p0 + lane);
+        myv = __builtin_nontemporal_load(P.row + p0 + lane);
+    }
+    // the largest power of two below L: first stride of the slot reduction
+    int top = 1;
+    while (2 * top < L) top *= 2;
+
+    float result = 0.f;  // lane t ends with the dot of position p0 + t
+    const int SU = S * U;
+    for (int base = 0; base < kWave && base < rem; base += SU) {
+        float dot[U];
+#pragma unroll
+        for (int u = 0; u < U; ++u) dot[u] = 0.f;
+        for (int ft = 0; ft < P.FT; ++ft) {
+            const int64_t chunk = (int64_t)ft * kWave + j;
+            const bool feat_ok = slot_ok && chunk < P.ltot;
+            const int64_t fe = chunk * EPL;
+            float xv[U][EPL], gv[U][EPL];
+            int32_t mv[MODE == kMax ? U : 1][EPL];
+            bool ok[U];
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                const int t = base + u * S + slot;
+                const int32_t c = __shfl(myc, t & (kWave - 1));
+                const int32_t v = __shfl(myv, t & (kWave - 1));
+                ok[u] = feat_ok && t < kWave && t < rem;
+                if (ok[u]) {
+                    load_vals<TX, EPL>(reinterpret_cast<const TX*>(P.x) + (int64_t)c * P.F + fe, xv[u]);
+                    load_vals<TG, EPL>(reinterpret_cast<const TG*>(P.g) + (int64_t)v * P.F + fe, gv[u]);
+                    if constexpr (MODE == kMax) load_ints<EPL>(P.argout + (int64_t)v * P.F + fe, mv[u]);
+                }
+            }
+#pragma unroll
+            for (int u = 0; u < U; ++u) {
+                if (!ok[u]) continue;
+                const int32_t pos = (int32_t)(p0 + base + u * S + slot);
+#pragma unroll
+                for (int k = 0; k < EPL; ++k) {
+                    float t = gv[u][k] * xv[u][k];
+                    if constexpr (MODE == kMax) t = mv[u][k] == pos ? t : 0.f;
+                    dot[u] += t;
+                }
+            }
+        }
+        // reduce each dot over the slot's L lanes (fixed tree; lane j = 0 holds it)
+#pragma unroll
+        for (int u = 0; u < U; ++u)
+            for (int off = top; off >= 1; off >>= 1) {
+                const float o = __shfl(dot[u], (lane + off) & (kWave - 1));
+                if (j + off < L) dot[u] += o;
+            }
+        // lane t picks the dot of position base + u*S + s from lane s*L
+        const int rel = lane - base;
+#pragma unroll
+        for (int u = 0; u < U; ++u) {
+            const int s = rel - u * S;
+            const float o = __shfl(dot[u], (s >= 0 && s < S ? s * L : 0) & (kWave - 1));
+            if (s >= 0 && s < S) result = o;
+        }
+    }
+    if (lane < rem) {
+        if constexpr (MODE == kMean) {
+            const int64_t deg = rp_at(P.rowptr, P.rp64, (int64_t)myv + 1) - rp_at(P.rowptr, P.rp64, myv);
+            result = result / (float)deg;
+        }
+        P.grad_w[p0 + lane] = result;
+    }
+}
+
+template <typename TX, typename TG, int EPL>
+hipError_t launch_gw_mode(const GradWParams& p, unsigned grid, hipStream_t s) {
+    if (p.reduce == kMax)
+        hipLaunchKernelGGL((spmm_grad_w<TX, TG, EPL, kMax>), dim3(grid), dim3(kBlock), 0, s, p);
+    else if (p.reduce == kMean)
+        hipLaunchKernelGGL((spmm_grad_w<TX, TG, EPL, kMean>), dim3(grid), dim3(kBlock), 0, s, p);
+    else
+        hipLaunchKernelGGL((spmm_grad_w<TX, TG, EPL, kSum>), dim3(grid), dim3(kBlock), 0, s, p);
+    return hipGetLastError();
+}
+
+template <typename TX, typename TG>
+hipError_t launch_gw_epl(const GradWParams& p, int epl, unsigned grid, hipStream_t s) {
+    switch (epl) {
+        case 8: return launch_gw_mode<TX, TG, 8>(p, grid, s);
+        case 4: return launch_gw_mode<TX, TG, 4>(p, grid, s);
+        case 2: return launch_gw_mode<TX, TG, 2>(p, grid, s);
+        default: return launch_gw_mode<TX, TG, 1>(p, grid, s);
+    }
+}
+
+}  // namespace
+
+hipError_t launch_rows_of_edges(const void* rowptr, int rp64, int64_t N, int64_t E, int32_t* row,
+                                hipStream_t s) {
+    if (E <= 0) return hipSuccess;
+    const int64_t threads = ceil_div(E, kRowItems);
+    hipLaunchKernelGGL(rows_of_edges, dim3((unsigned)ceil_div(threads, kBlock)), dim3(kBlock), 0,
+                       s, rowptr, rp64, N, E, row);
+    return hipGetLastError();
+}
+
+hipError_t launch_scale_inv_deg(const void* g, int g_bf16, const void* rowptr, int rp64, int64_t N,
+                                int64_t F, float* out, hipStream_t s) {
+    const int64_t n = N * F;
+    if (n <= 0) return hipSuccess;
+    const unsigned grid = (unsigned)ceil_div(n, kBlock);
+    if (g_bf16)
+        hipLaunchKernelGGL(scale_inv_deg<true>, dim3(grid), dim3(kBlock), 0, s, g, rowptr, rp64, N, F, out);
+    else
+        hipLaunchKernelGGL(scale_inv_deg<false>, dim3(grid), dim3(kBlock), 0, s, g, rowptr, rp64, N, F, out);
+    return hipGetLastError();
+}
+
+hipError_t launch_spmm_grad_w(const GradWParams& p, int x_dtype, int g_dtype, int epl,
+                              hipStream_t s) {
+    if (p.E <= 0) return hipSuccess;
+    const int64_t waves = ceil_div(p.E, kWave);
+    const unsigned grid = (unsigned)ceil_div(waves, kWavesPerBlock);
+    if (x_dtype == MP_F32)
+        return g_dtype == MP_F32 ? launch_gw_epl<float, float>(p, epl, grid, s)
+                                 : launch_gw_epl<float, uint16_t>(p, epl, grid, s);
+    return g_dtype == MP_F32 ? launch_gw_epl<uint16_t, float>(p, epl, grid, s)
+                             : launch_gw_epl<uint16_t, uint16_t>(p, epl, grid, s);
+}
+
+}  // namespace mp

@@ -150,10 +150,36 @@ struct SpmmParams {
     int max_bf16;
     int32_t* argout;
     int vec_store;  // 1: out, out_max and argout are 16-byte aligned
+    // masked sum (gradient of max): edge t contributes feature f only where
+    // mtab[c_t * F + f] == ekey[t]; both nullptr otherwise
+    const int32_t* ekey;
+    const int32_t* mtab;
     float* part_sum;
     float* part_max;
     int32_t* part_arg;
 };
+
+// ---- backward (backward.hip) -----------------------------------------------
+struct GradWParams {
+    const void* rowptr;
+    int rp64;
+    const int32_t* col;
+    const int32_t* row;     // destination row of every CSR position
+    const void* x;          // [N_src, F]
+    const void* g;          // [N_dst, F] gradient of the aggregation output
+    const int32_t* argout;  // [N_dst, F] (max only)
+    int64_t F, E;
+    int L, S, FT;
+    int64_t ltot;
+    int reduce;             // exactly one of kSum, kMean, kMax
+    float* grad_w;          // [E]
+};
+hipError_t launch_rows_of_edges(const void* rowptr, int rp64, int64_t N, int64_t E, int32_t* row,
+                                hipStream_t s);
+hipError_t launch_scale_inv_deg(const void* g, int g_bf16, const void* rowptr, int rp64, int64_t N,
+                                int64_t F, float* out, hipStream_t s);
+hipError_t launch_spmm_grad_w(const GradWParams& p, int x_dtype, int g_dtype, int epl,
+                              hipStream_t s);
 
 hipError_t launch_spmm(const SpmmParams& p, int x_dtype, int epl, hipStream_t s);
 hipError_t launch_spmm_tiny(const SpmmParams& p, int x_dtype, int epl, hipStream_t s);

@@ -65,6 +65,31 @@ __device__ inline void widen(const typename RawVec<TX, EPL>::T& r, float (&v)[EP
     }
 }
 
+// EPL consecutive int32 (a lane-chunk of the mask table), 16-byte loads
+// when EPL >= 4; p is aligned to min(16, 4 * EPL) bytes.
+template <int EPL>
+__device__ inline void load_mask(const int32_t* p, int32_t (&v)[EPL]) {
+    if constexpr (EPL >= 4) {
+#pragma unroll
+        for (int q = 0; q < EPL / 4; ++q) {
+            const int4 a = reinterpret_cast<const int4*>(p)[q];
+            v[4 * q + 0] = a.x; v[4 * q + 1] = a.y; v[4 * q + 2] = a.z; v[4 * q + 3] = a.w;
+        }
+    } else if constexpr (EPL == 2) {
+        const int2 a = *reinterpret_cast<const int2*>(p);
+        v[0] = a.x; v[1] = a.y;
+    } else {
+        v[0] = *p;
+    }
+}
+
+// Keep only the features whose mask entry names this edge.
+template <int EPL>
+__device__ inline void apply_mask(float (&v)[EPL], const int32_t (&m)[EPL], int32_t key) {
+#pragma unroll
+    for (int k = 0; k < EPL; ++k) v[k] = m[k] == key ? v[k] : 0.f;
+}
+
 // fp32 -> bf16 bits, round to nearest even (finite values).
 __device__ inline uint16_t to_bf16(float f) {
     uint32_t u = __float_as_uint(f);
@@ -253,7 +278,7 @@ __device__ inline void store_row(const SpmmParams& P, int64_t row, int64_t fe, i
 // once, coalesced, one per lane; each inner step then covers SU = S*U edges:
 // slot s takes edges base + u*S + s (u < U), gets their columns by cross-lane
 // permute, issues all U feature-row loads, and only then accumulates.
-template <typename TX, int EPL, bool HS, bool HM, int NT, bool W>
+template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, bool MK>
 __device__ inline void wave_range(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int64_t e0,
                                   int64_t e1, int lane, int slot, bool feat_ok, int64_t fe, int U) {
     using R = typename RawVec<TX, EPL>::T;
@@ -264,16 +289,18 @@ __device__ inline void wave_range(const SpmmParams& P, Acc<EPL, HS, HM>& acc, in
     const int tile = steps * SU;
     for (int64_t p0 = e0; p0 < e1; p0 += tile) {
         const int64_t rem = e1 - p0;
-        int32_t myc = 0;
+        int32_t myc = 0, myk = -1;
         float myw = 1.f;
         if (lane < tile && lane < rem) {
             myc = __builtin_nontemporal_load(P.col + p0 + lane);
             if constexpr (W) myw = __builtin_nontemporal_load(P.w + p0 + lane);
+            if constexpr (MK) myk = __builtin_nontemporal_load(P.ekey + p0 + lane);
         }
         for (int st = 0; st < steps; ++st) {
             const int base = st * SU;
             if (base >= rem) break;
             const char* addr[kUnroll];
+            const int32_t* maddr[kUnroll];
             bool ok[kUnroll];
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
@@ -281,16 +308,23 @@ __device__ inline void wave_range(const SpmmParams& P, Acc<EPL, HS, HM>& acc, in
                 const int32_t c = __shfl(myc, t);
                 ok[u] = feat_ok && (u < U) && (t < rem);
                 addr[u] = feat_addr<TX, NT>(P, c, fe);
+                if constexpr (MK) maddr[u] = P.mtab + (int64_t)c * P.F + fe;
             }
             R raw[kUnroll];
+            int32_t mraw[MK ? kUnroll : 1][EPL];
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u)
-                if (ok[u]) raw[u] = *reinterpret_cast<const R*>(addr[u]);
+                if (ok[u]) {
+                    raw[u] = *reinterpret_cast<const R*>(addr[u]);
+                    if constexpr (MK) load_mask<EPL>(maddr[u], mraw[u]);
+                }
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
                 const int t = base + u * S + slot;
                 float wt = 1.f;
                 if constexpr (W) wt = __shfl(myw, t);
+                int32_t key = -1;
+                if constexpr (MK) key = __shfl(myk, t);
                 if (ok[u]) {
                     float v[EPL];
                     widen<TX, EPL>(raw[u], v);
@@ -298,6 +332,7 @@ __device__ inline void wave_range(const SpmmParams& P, Acc<EPL, HS, HM>& acc, in
 #pragma unroll
                         for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt, v[k]);
                     }
+                    if constexpr (MK) apply_mask<EPL>(v, mraw[u], key);
                     acc.add(u % A, v, (int32_t)(p0 + t));
                 }
             }
@@ -308,7 +343,7 @@ __device__ inline void wave_range(const SpmmParams& P, Acc<EPL, HS, HM>& acc, in
 // One slot per row: every slot walks its own row's edges, U at a time.
 // COOP: the slot has at least U lanes, which load its next U columns
 // together; otherwise each lane loads the columns itself.
-template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, bool COOP>
+template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, bool MK, bool COOP>
 __device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int64_t e0,
                                 int32_t my_n, int32_t max_n, int slot, int j, bool feat_ok,
                                 int64_t fe) {
@@ -317,14 +352,17 @@ __device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int6
     const int L = P.L;
     for (int32_t it = 0; it < max_n; it += kUnroll) {
         const char* addr[kUnroll];
+        const int32_t* maddr[kUnroll];
         bool ok[kUnroll];
         float wt[kUnroll];
+        int32_t key[kUnroll];
         if constexpr (COOP) {
-            int32_t myc = 0;
+            int32_t myc = 0, myk = -1;
             float myw = 1.f;
             if (j < kUnroll && it + j < my_n) {
                 myc = __builtin_nontemporal_load(P.col + e0 + it + j);
                 if constexpr (W) myw = __builtin_nontemporal_load(P.w + e0 + it + j);
+                if constexpr (MK) myk = __builtin_nontemporal_load(P.ekey + e0 + it + j);
             }
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
@@ -332,8 +370,11 @@ __device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int6
                 const int32_t c = __shfl(myc, srcl);
                 wt[u] = 1.f;
                 if constexpr (W) wt[u] = __shfl(myw, srcl);
+                key[u] = -1;
+                if constexpr (MK) key[u] = __shfl(myk, srcl);
                 ok[u] = feat_ok && (it + u < my_n);
                 addr[u] = feat_addr<TX, NT>(P, c, fe);
+                if constexpr (MK) maddr[u] = P.mtab + (int64_t)c * P.F + fe;
             }
         } else {
             int32_t cc[kUnroll];
@@ -343,14 +384,23 @@ __device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int6
                 cc[u] = ok[u] ? P.col[e0 + it + u] : 0;
                 wt[u] = 1.f;
                 if constexpr (W) wt[u] = ok[u] ? P.w[e0 + it + u] : 1.f;
+                key[u] = -1;
+                if constexpr (MK) key[u] = ok[u] ? P.ekey[e0 + it + u] : -1;
             }
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) addr[u] = feat_addr<TX, NT>(P, cc[u], fe);
+            for (int u = 0; u < kUnroll; ++u) {
+                addr[u] = feat_addr<TX, NT>(P, cc[u], fe);
+                if constexpr (MK) maddr[u] = P.mtab + (int64_t)cc[u] * P.F + fe;
+            }
         }
         R raw[kUnroll];
+        int32_t mraw[MK ? kUnroll : 1][EPL];
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u)
-            if (ok[u]) raw[u] = *reinterpret_cast<const R*>(addr[u]);
+            if (ok[u]) {
+                raw[u] = *reinterpret_cast<const R*>(addr[u]);
+                if constexpr (MK) load_mask<EPL>(maddr[u], mraw[u]);
+            }
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
             if (ok[u]) {
@@ -360,13 +410,14 @@ __device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int6
 #pragma unroll
                     for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt[u], v[k]);
                 }
+                if constexpr (MK) apply_mask<EPL>(v, mraw[u], key[u]);
                 acc.add(u % A, v, (int32_t)(e0 + it + u));
             }
         }
     }
 }
 
-template <typename TX, int EPL, bool HS, bool HM, int NT, bool W>
+template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, bool MK>
 __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave)) +
@@ -421,7 +472,7 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
                 e1 = load_rp(P.rowptr, P.rp64, row + 1);
             }
         }
-        wave_range<TX, EPL, HS, HM, NT, W>(P, acc, e0, e1, lane, slot, feat_ok, fe, U);
+        wave_range<TX, EPL, HS, HM, NT, W, MK>(P, acc, e0, e1, lane, slot, feat_ok, fe, U);
         acc.fold();
         acc.reduce_slots(S, L, slot, lane);
         if (slot == 0 && feat_ok) {
@@ -463,9 +514,9 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
         max_n = o > max_n ? o : max_n;
     }
     if (L >= kUnroll)
-        slot_row<TX, EPL, HS, HM, NT, W, true>(P, acc, e0, my_n, max_n, slot, j, feat_ok, fe);
+        slot_row<TX, EPL, HS, HM, NT, W, MK, true>(P, acc, e0, my_n, max_n, slot, j, feat_ok, fe);
     else
-        slot_row<TX, EPL, HS, HM, NT, W, false>(P, acc, e0, my_n, max_n, slot, j, feat_ok, fe);
+        slot_row<TX, EPL, HS, HM, NT, W, MK, false>(P, acc, e0, my_n, max_n, slot, j, feat_ok, fe);
     acc.fold();
     if (feat_ok) store_row<EPL>(P, row, fe, e1 - e0, acc.s[0], acc.m[0], acc.i[0], HS, HM);
 }
@@ -477,7 +528,7 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
 // in flight, so a group costs about one memory round trip.  Requires slots of
 // at least kTinyDeg + 1 lanes (the columns of a row are loaded one per lane).
 // One accumulator per element: a row has at most 7 edges.
-template <typename TX, int EPL, bool HS, bool HM, bool W, int NT>
+template <typename TX, int EPL, bool HS, bool HM, bool W, int NT, bool MK>
 __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
     using R = typename RawVec<TX, EPL>::T;
     const int lane = threadIdx.x & (kWave - 1);
@@ -504,21 +555,23 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
             }
         }
     };
-    auto cols = [&](int32_t beg, int32_t deg, int32_t& c, float& w) {
+    auto cols = [&](int32_t beg, int32_t deg, int32_t& c, float& w, int32_t& key) {
         c = 0;
         w = 1.f;
+        key = -1;
         if (j < deg) {
             c = __builtin_nontemporal_load(P.col + beg + j);
             if constexpr (W) w = __builtin_nontemporal_load(P.w + beg + j);
+            if constexpr (MK) key = __builtin_nontemporal_load(P.ekey + beg + j);
         }
     };
 
     int64_t it = tw;
     int32_t row, beg, deg, nrow, nbeg, ndeg;
-    int32_t cv;
+    int32_t cv, kv;
     float wv;
     rec(it, row, beg, deg);
-    cols(beg, deg, cv, wv);
+    cols(beg, deg, cv, wv, kv);
     rec(it + nw, nrow, nbeg, ndeg);
     for (; it < items; it += nw) {
         const int ft = (int)(it % P.FT);
@@ -526,23 +579,30 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
         const bool feat_ok = row >= 0 && chunk_j < P.ltot;
         const int64_t fe = chunk_j * EPL;
         R raw[kTinyDeg];
+        int32_t mraw[MK ? kTinyDeg : 1][EPL];
         bool ok[kTinyDeg];
 #pragma unroll
         for (int u = 0; u < kTinyDeg; ++u) {
             const int32_t c = __shfl(cv, slot * L + u);
             ok[u] = feat_ok && (u < deg);
-            if (ok[u]) raw[u] = *reinterpret_cast<const R*>(feat_addr<TX, NT>(P, c, fe));
+            if (ok[u]) {
+                raw[u] = *reinterpret_cast<const R*>(feat_addr<TX, NT>(P, c, fe));
+                if constexpr (MK) load_mask<EPL>(P.mtab + (int64_t)c * P.F + fe, mraw[u]);
+            }
         }
         float wt[kTinyDeg];
+        int32_t key[kTinyDeg];
 #pragma unroll
         for (int u = 0; u < kTinyDeg; ++u) {
             wt[u] = 1.f;
             if constexpr (W) wt[u] = __shfl(wv, slot * L + u);
+            key[u] = -1;
+            if constexpr (MK) key[u] = __shfl(kv, slot * L + u);
         }
         // next group's columns, and the row ranges of the group after it
-        int32_t ncv;
+        int32_t ncv, nkv;
         float nwv;
-        cols(nbeg, ndeg, ncv, nwv);
+        cols(nbeg, ndeg, ncv, nwv, nkv);
         int32_t row2, beg2, deg2;
         rec(it + 2 * nw, row2, beg2, deg2);
 
@@ -557,6 +617,7 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
 #pragma unroll
                     for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt[u], v[k]);
                 }
+                if constexpr (MK) apply_mask<EPL>(v, mraw[u], key[u]);
                 acc.add(0, v, beg + u);
             }
         }
@@ -566,6 +627,7 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
         deg = ndeg;
         cv = ncv;
         wv = nwv;
+        kv = nkv;
         nrow = row2;
         nbeg = beg2;
         ndeg = deg2;
@@ -687,12 +749,14 @@ template <typename TX, int EPL, bool W>
 hipError_t launch_w(const SpmmParams& p, unsigned grid, hipStream_t s) {
     const bool hs = (p.reduce & (kSum | kMean)) != 0;
     const bool hm = (p.reduce & kMax) != 0;
-    if (hs && hm)
-        hipLaunchKernelGGL((spmm_main<TX, EPL, true, true, 1, W>), dim3(grid), dim3(kBlock), 0, s, p);
+    if (p.mtab)  // masked sum: the gradient of max
+        hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 1, W, true>), dim3(grid), dim3(kBlock), 0, s, p);
+    else if (hs && hm)
+        hipLaunchKernelGGL((spmm_main<TX, EPL, true, true, 1, W, false>), dim3(grid), dim3(kBlock), 0, s, p);
     else if (hm)
-        hipLaunchKernelGGL((spmm_main<TX, EPL, false, true, 1, W>), dim3(grid), dim3(kBlock), 0, s, p);
+        hipLaunchKernelGGL((spmm_main<TX, EPL, false, true, 1, W, false>), dim3(grid), dim3(kBlock), 0, s, p);
     else
-        hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 1, W>), dim3(grid), dim3(kBlock), 0, s, p);
+        hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 1, W, false>), dim3(grid), dim3(kBlock), 0, s, p);
     return hipGetLastError();
 }
 
@@ -701,11 +765,11 @@ hipError_t launch_typed(const SpmmParams& p, unsigned grid, hipStream_t s) {
     if (p.n_tables > 1) {
         // typed-node tables: unweighted sum only
         if (p.n_tables <= 2)
-            hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 2, false>), dim3(grid), dim3(kBlock), 0, s, p);
+            hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 2, false, false>), dim3(grid), dim3(kBlock), 0, s, p);
         else if (p.n_tables <= 4)
-            hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 4, false>), dim3(grid), dim3(kBlock), 0, s, p);
+            hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 4, false, false>), dim3(grid), dim3(kBlock), 0, s, p);
         else
-            hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, MP_MAX_TYPES, false>), dim3(grid), dim3(kBlock), 0, s, p);
+            hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, MP_MAX_TYPES, false, false>), dim3(grid), dim3(kBlock), 0, s, p);
         return hipGetLastError();
     }
     return p.w ? launch_w<TX, EPL, true>(p, grid, s) : launch_w<TX, EPL, false>(p, grid, s);
@@ -758,15 +822,19 @@ hipError_t launch_tiny_typed(const SpmmParams& p, unsigned grid, hipStream_t s) 
     const bool hm = (p.reduce & kMax) != 0;
     const bool w = p.w != nullptr;
 #define MP_TINY(HS, HM, WW) \
-    hipLaunchKernelGGL((spmm_tiny<TX, EPL, HS, HM, WW, 1>), dim3(grid), dim3(kBlock), 0, s, p)
+    hipLaunchKernelGGL((spmm_tiny<TX, EPL, HS, HM, WW, 1, false>), dim3(grid), dim3(kBlock), 0, s, p)
     if (p.n_tables > 1) {
         // typed-node tables: unweighted sum only
         if (p.n_tables <= 2)
-            hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, 2>), dim3(grid), dim3(kBlock), 0, s, p);
+            hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, 2, false>), dim3(grid), dim3(kBlock), 0, s, p);
         else if (p.n_tables <= 4)
-            hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, 4>), dim3(grid), dim3(kBlock), 0, s, p);
+            hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, 4, false>), dim3(grid), dim3(kBlock), 0, s, p);
         else
-            hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, MP_MAX_TYPES>), dim3(grid), dim3(kBlock), 0, s, p);
+            hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, MP_MAX_TYPES, false>), dim3(grid), dim3(kBlock), 0, s, p);
+    } else if (p.mtab) {
+        // masked sum: the gradient of max
+        if (w) hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, true, 1, true>), dim3(grid), dim3(kBlock), 0, s, p);
+        else hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, 1, true>), dim3(grid), dim3(kBlock), 0, s, p);
     } else if (hs && hm) { if (w) MP_TINY(true, true, true); else MP_TINY(true, true, false); }
     else if (hm) { if (w) MP_TINY(false, true, true); else MP_TINY(false, true, false); }
     else { if (w) MP_TINY(true, false, true); else MP_TINY(true, false, false); }

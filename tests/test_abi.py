@@ -141,6 +141,65 @@ def test_sorted_coo_to_csr_errors():
     assert L.mp_sorted_coo_to_csr(FAKE, FAKE, -1, 5, FAKE, 0, FAKE, None, None, None, None) < 0
 
 
+def test_transpose_errors_and_sizes():
+    L = mp.lib()
+    nb = ctypes.c_size_t(0)
+    assert L.mp_csr_transpose_workspace(1000, 50, 0, 1, ctypes.byref(nb)) == 0
+    assert nb.value >= 4 * 1000
+    assert L.mp_csr_transpose_workspace(1000, 0, 0, 1, ctypes.byref(nb)) == -2
+    args = [FAKE, 0, FAKE, 10, 20, 100, FAKE, 0, FAKE, FAKE, None, None, FAKE, 1 << 20, None]
+    def call(**kw):
+        a = list(args)
+        names = ["rowptr", "it", "col", "N_dst", "N_src", "E", "rowptrT", "itT", "colT", "posT",
+                 "val_in", "val_out", "ws", "ws_bytes", "stream"]
+        for k, v in kw.items():
+            a[names.index(k)] = v
+        return L.mp_csr_transpose(*a)
+    assert call(it=5) == -3
+    assert call(itT=5) == -3
+    assert call(N_dst=0) == -2
+    assert call(rowptrT=None) == -1
+    assert call(val_in=FAKE) == -1
+    assert call(rowptrT=FAKE + 4, itT=1) == -8
+    assert call(ws_bytes=16) == -5
+
+
+def test_backward_errors_and_sizes():
+    L = mp.lib()
+    nb = ctypes.c_size_t(0)
+    assert L.mp_spmm_backward_w_workspace(1000, ctypes.byref(nb)) == 0 and nb.value == 4096
+    assert L.mp_spmm_backward_x_workspace(None, 10, 8, mp.MP_MEAN, ctypes.byref(nb)) == 0
+    assert nb.value == 512
+    assert L.mp_spmm_backward_x_workspace(None, 10, 8, mp.MP_SUM | mp.MP_MAX,
+                                          ctypes.byref(nb)) == -4
+    bx = dict(planT=None, rowptrT=FAKE, itT=0, colT=FAKE, posT=FAKE, wT=None, rowptr=FAKE, it=0,
+              argout=FAKE, g=FAKE, g_dtype=0, N_dst=10, N_src=10, F=8, reduce=mp.MP_SUM,
+              out=FAKE, out_dtype=0, ws=None, ws_bytes=0, stream=None)
+    def bwx(**kw):
+        a = dict(bx, **kw)
+        return L.mp_spmm_backward_x(*a.values())
+    assert bwx(reduce=mp.MP_SUM | mp.MP_MAX) == -4
+    assert bwx(reduce=mp.MP_MAX, argout=None) == -1
+    assert bwx(reduce=mp.MP_MAX, posT=None) == -1
+    assert bwx(reduce=mp.MP_MEAN, rowptr=None) == -1
+    assert bwx(reduce=mp.MP_MEAN) == -5  # needs a workspace for the scaled gradient
+    assert bwx(g_dtype=3) == -3
+    assert bwx(g=FAKE + 2) == -8
+    assert bwx(F=0) == -2
+    bw = dict(rowptr=FAKE, it=0, col=FAKE, x=FAKE, x_dtype=0, g=FAKE, g_dtype=0, argout=None,
+              N_src=10, N_dst=10, E=100, F=8, reduce=mp.MP_SUM, out=FAKE, ws=FAKE,
+              ws_bytes=1 << 20, stream=None)
+    def bww(**kw):
+        a = dict(bw, **kw)
+        return L.mp_spmm_backward_w(*a.values())
+    assert bww(reduce=mp.MP_MEAN | mp.MP_MAX) == -4
+    assert bww(reduce=mp.MP_MAX) == -1
+    assert bww(ws_bytes=16) == -5
+    assert bww(N_dst=0) == -2
+    assert bww(x=FAKE + 2) == -8
+    assert bww(x_dtype=7) == -3
+
+
 def test_validate_errors():
     L = mp.lib()
     assert L.mp_validate_sorted(FAKE, 10, None, None) == -1
