@@ -116,6 +116,10 @@ def _ptr(t):
         return t
     if not t.is_contiguous():
         raise ValueError("tensors passed to libmp must be contiguous")
+    if t.numel() == 0:
+        # torch reports 0 for an empty tensor; pass its storage address (NULL
+        # only when nothing was ever allocated, see _edge_array)
+        return t.untyped_storage().data_ptr() + t.storage_offset() * t.element_size() or None
     return t.data_ptr()
 
 
@@ -150,6 +154,12 @@ def _bytes(fn, *args):
     b = ctypes.c_size_t(0)
     _check(fn, getattr(lib(), fn)(*args, ctypes.byref(b)))
     return b.value
+
+
+def _edge_array(E, dtype, device):
+    """[E] tensor whose storage holds at least one element, so that its data
+    pointer is never NULL (an empty graph still passes valid pointers)."""
+    return torch.empty(max(E, 1), dtype=dtype, device=device)[:E]
 
 
 def _workspace(nbytes, device):
@@ -306,9 +316,9 @@ def coo_to_csr(src: torch.Tensor, dst: torch.Tensor, N: int, *, rowptr_dtype=tor
     dev = src.device
     it = _itype_code(rowptr_dtype)
     rowptr = torch.empty(N + 1, dtype=rowptr_dtype, device=dev)
-    col = torch.empty(max(E, 0), dtype=torch.int32, device=dev)
-    perm = torch.empty(E, dtype=torch.int32, device=dev) if want_perm else None
-    vout = torch.empty(E, dtype=torch.float32, device=dev) if val is not None else None
+    col = _edge_array(E, torch.int32, dev)
+    perm = _edge_array(E, torch.int32, dev) if want_perm else None
+    vout = _edge_array(E, torch.float32, dev) if val is not None else None
     nb = mp_coo_to_csr_workspace(E, N, it, want_perm or val is not None)
     if ws is None or ws.numel() < nb:
         ws = _workspace(nb, dev)
@@ -325,9 +335,9 @@ def sorted_coo_to_csr(src: torch.Tensor, dst: torch.Tensor, N: int, *, rowptr_dt
     dev = src.device
     it = _itype_code(rowptr_dtype)
     rowptr = torch.empty(N + 1, dtype=rowptr_dtype, device=dev)
-    col = torch.empty(max(E, 0), dtype=torch.int32, device=dev)
-    perm = torch.empty(E, dtype=torch.int32, device=dev) if want_perm else None
-    vout = torch.empty(E, dtype=torch.float32, device=dev) if val is not None else None
+    col = _edge_array(E, torch.int32, dev)
+    perm = _edge_array(E, torch.int32, dev) if want_perm else None
+    vout = _edge_array(E, torch.float32, dev) if val is not None else None
     mp_sorted_coo_to_csr(src, dst, E, N, rowptr, it, col, perm, val, vout, stream)
     return rowptr, col, perm, vout
 
@@ -407,9 +417,9 @@ def csr_transpose(rowptr, col, N_src, *, rowptrT_dtype=torch.int32, want_pos=Tru
     dev = col.device
     itT = _itype_code(rowptrT_dtype)
     rowptrT = torch.empty(N_src + 1, dtype=rowptrT_dtype, device=dev)
-    colT = torch.empty(E, dtype=torch.int32, device=dev)
-    posT = torch.empty(E, dtype=torch.int32, device=dev) if want_pos else None
-    vout = torch.empty(E, dtype=torch.float32, device=dev) if val is not None else None
+    colT = _edge_array(E, torch.int32, dev)
+    posT = _edge_array(E, torch.int32, dev) if want_pos else None
+    vout = _edge_array(E, torch.float32, dev) if val is not None else None
     nb = mp_csr_transpose_workspace(E, N_src, itT, want_pos or val is not None)
     ws = _workspace(nb, dev) if nb else None
     mp_csr_transpose(rowptr, _itype_code(rowptr.dtype), col, N_dst, N_src, E, rowptrT, itT, colT,
@@ -443,7 +453,7 @@ def spmm_backward_w(rowptr, col, x, grad_out, reduce, *, argout=None, out=None, 
     E = int(col.numel())
     dev = x.device
     if out is None:
-        out = torch.empty(E, dtype=torch.float32, device=dev)
+        out = _edge_array(E, torch.float32, dev)
     nb = mp_spmm_backward_w_workspace(E)
     ws = _workspace(nb, dev) if nb else None
     mp_spmm_backward_w(rowptr, _itype_code(rowptr.dtype), col, x, _dtype_code(x.dtype), grad_out,
@@ -461,7 +471,7 @@ def hetero_build(N_per_type, rels, dst_type, *, rowptr_dtype=torch.int32, stream
     dev = next(r[2].device for r in rels)
     E_T = sum(int(r[2].numel()) for r in rels if r[1] == dst_type)
     rowptr = torch.empty(N_per_type[dst_type] + 1, dtype=rowptr_dtype, device=dev)
-    col = torch.empty(E_T, dtype=torch.int32, device=dev)
+    col = _edge_array(E_T, torch.int32, dev)
     nb = mp_hetero_build_workspace(N_per_type, rels, dst_type, it)
     ws = _workspace(nb, dev)
     mp_hetero_build(N_per_type, rels, dst_type, rowptr, it, col, ws, ws.numel(), stream)
