@@ -271,7 +271,7 @@ int mp_coo_to_csr(const int32_t* src, const int32_t* dst, int64_t E, int64_t N, 
     if (st != MP_OK) return st;
     if (!rowptr) return MP_ERR_NULL;
     if (E > 0 && (!src || !dst || !col || !ws)) return MP_ERR_NULL;
-    if ((val_in == nullptr) != (val_out == nullptr)) return MP_ERR_NULL;
+    if (E > 0 && (val_in == nullptr) != (val_out == nullptr)) return MP_ERR_NULL;
     if ((uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4)) return MP_ERR_ALIGN;
     return coo_to_csr_impl(src, dst, E, N, rowptr, rowptr_itype, col, perm, val_in, val_out, ws,
                            ws_bytes, as_stream(stream));
@@ -285,7 +285,7 @@ int mp_sorted_coo_to_csr(const int32_t* src, const int32_t* dst, int64_t E, int6
     if (st != MP_OK) return st;
     if (!rowptr) return MP_ERR_NULL;
     if (E > 0 && (!src || !dst || !col)) return MP_ERR_NULL;
-    if ((val_in == nullptr) != (val_out == nullptr)) return MP_ERR_NULL;
+    if (E > 0 && (val_in == nullptr) != (val_out == nullptr)) return MP_ERR_NULL;
     if ((uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4)) return MP_ERR_ALIGN;
     hipStream_t s = as_stream(stream);
     const int rp64 = rowptr_itype == MP_I64;
@@ -478,7 +478,7 @@ int mp_csr_transpose(const void* rowptr, int rowptr_itype, const int32_t* col, i
     if (N_dst < 1 || N_dst > INT32_MAX) return MP_ERR_SIZE;
     if (!rowptr || !rowptrT) return MP_ERR_NULL;
     if (E > 0 && (!col || !colT || !ws)) return MP_ERR_NULL;
-    if ((val_in == nullptr) != (val_out == nullptr)) return MP_ERR_NULL;
+    if (E > 0 && (val_in == nullptr) != (val_out == nullptr)) return MP_ERR_NULL;
     if ((uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4) ||
         (uintptr_t)rowptrT % (rowptrT_itype == MP_I64 ? 8 : 4))
         return MP_ERR_ALIGN;
