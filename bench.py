@@ -37,7 +37,8 @@ if ROOT not in sys.path:
 METRIC = "SpMM effective HBM GB/s (% of peak) + edge·features/s, sum/mean/max"
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 WORKLOAD = "chunglu-124M"
-DOMINANT = "spmm_main<float, 4, true, false, 1, false>"  # fp32 sum, the largest launch of a step
+BACKWARD = "chunglu-124M-backward"
+DOMINANT = "spmm_main<float, 4, true, false, 1, false, false>"  # fp32 sum, the largest launch of a step
 DOMINANT_SRC = ["paper_2507_16991_amd/csrc/spmm.hip", "paper_2507_16991_amd/csrc/mp_internal.hpp"]
 COUNTER_SUMMARY = os.path.join(ROOT, "profiles", "spmm_main_f32_sum_chunglu124M_counters.txt")
 CALIB_BYTES = 1 << 30  # plain copy used to scale the HBM counters
@@ -59,6 +60,28 @@ def spmm_bytes(N, E, F, xb, reduce, out_b=4, max_b=4, rowptr_b=4, w=False):
 def csr_bytes(N, E, rowptr_b=4, perm=False):
     """Read src and dst, write col (and perm) and rowptr."""
     return 8 * E + 4 * E + (4 * E if perm else 0) + (N + 1) * rowptr_b
+
+
+def transpose_bytes(N_dst, N_src, E):
+    """Read rowptr and col, write rowptrT, colT and posT."""
+    return 4 * (N_dst + 1) + 4 * E + 4 * (N_src + 1) + 8 * E
+
+
+def grad_x_bytes(N_dst, N_src, E, F, mode):
+    """Transposed gather of the output gradient (plus the argmax table for
+    max, plus the scaled copy for mean), one output row per source."""
+    b = 4 * (N_src + 1) + 4 * E + E * F * 4 + N_src * F * 4
+    if mode == "mean":
+        b += 4 * (N_dst + 1) + 2 * N_dst * F * 4
+    if mode == "max":
+        b += 4 * E + E * F * 4
+    return b
+
+
+def grad_w_bytes(N_dst, E, F):
+    """One x row gathered per edge, the output gradient read once per row,
+    one fp32 per edge written."""
+    return 4 * (N_dst + 1) + 4 * E + E * F * 4 + N_dst * F * 4 + 4 * E
 
 
 def plan_bytes(N):
@@ -114,7 +137,10 @@ def build_step(args, mp, torch, np, dev):
     import graphgen
 
     t0 = time.time()
-    g = graphgen.workload(args.workload, seed=args.seed)
+    if args.workload == BACKWARD:
+        g = graphgen.workload(WORKLOAD, seed=args.seed, bf16=False)
+    else:
+        g = graphgen.workload(args.workload, seed=args.seed)
     print(f"[bench] generated {args.workload} in {time.time() - t0:.1f}s", file=sys.stderr,
           flush=True)
     stream = torch.cuda.current_stream()
@@ -149,6 +175,9 @@ def build_step(args, mp, torch, np, dev):
             mark(evs, 3)
         g.n_dst, g.E = sum(g.n_per_type), sum(a.shape[0] for a in g.rel_src)
         return g, step, ops
+
+    if args.workload == BACKWARD:
+        return backward_step(g, mp, torch, np, dev, mark)
 
     N, E, F = g.n_dst, g.E, g.F
     src = torch.from_numpy(g.src).to(dev)
@@ -227,6 +256,71 @@ def build_step(args, mp, torch, np, dev):
     return g, step, ops
 
 
+def backward_step(g, mp, torch, np, dev, mark):
+    """Backward of the headline graph's aggregation: the transposed CSR with
+    its plan, then dL/dx for sum, mean and max and dL/dw for sum, from a
+    seeded fp32 output gradient.  The forward CSR and the forward argmax are
+    built once before timing (they come from the forward pass)."""
+    import graphgen
+
+    N, E, F = g.n_dst, g.E, g.F
+    it = mp.MP_I32
+    src = torch.from_numpy(g.src).to(dev)
+    dst = torch.from_numpy(g.dst).to(dev)
+    rowptr, col, _, _ = mp.coo_to_csr(src, dst, N)
+    del src, dst
+    x = torch.from_numpy(g.x).to(dev)
+    G = torch.from_numpy(graphgen.normal_f32(1, 11, N * F).reshape(N, F)).to(dev)
+    _, _, argout = mp.spmm(rowptr, col, x, mp.MP_MAX, plan=mp.Plan(rowptr, E, F))
+    rowptrT = torch.empty(N + 1, dtype=torch.int32, device=dev)
+    colT = torch.empty(E, dtype=torch.int32, device=dev)
+    posT = torch.empty(E, dtype=torch.int32, device=dev)
+    ws_t = torch.empty(mp.mp_csr_transpose_workspace(E, N, it, 1), dtype=torch.uint8, device=dev)
+    nplan = mp.mp_spmm_plan_size(N, E)
+    plan_buf = torch.empty(nplan, dtype=torch.uint8, device=dev)
+    gx = torch.empty(N, F, dtype=torch.float32, device=dev)
+    gw = torch.empty(E, dtype=torch.float32, device=dev)
+    ws_w = torch.empty(mp.mp_spmm_backward_w_workspace(E), dtype=torch.uint8, device=dev)
+    ops = [("transpose", transpose_bytes(N, N, E), 0), ("plan", plan_bytes(N), 0)]
+    for m in ("sum", "mean", "max"):
+        ops.append((f"grad_x_{m}_f32", grad_x_bytes(N, N, E, F, m), E * F))
+    ops.append(("grad_w_sum_f32", grad_w_bytes(N, E, F), E * F))
+    plans, wss = {}, {}
+
+    def step(evs=None):
+        mark(evs, 0)
+        mp.mp_csr_transpose(rowptr, it, col, N, N, E, rowptrT, it, colT, posT, None, None, ws_t,
+                            ws_t.numel())
+        mark(evs, 1)
+        if "h" in plans:
+            mp.mp_spmm_plan_free(plans["h"])
+        plans["h"] = h = mp.mp_spmm_plan_build(rowptrT, it, N, E, F, mp.MP_F32, plan_buf, nplan)
+        mark(evs, 2)
+        i = 2
+        for red in (mp.MP_SUM, mp.MP_MEAN, mp.MP_MAX):
+            nb = mp.mp_spmm_backward_x_workspace(h, N, F, red)
+            if red not in wss or wss[red].numel() < nb:
+                wss[red] = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
+            mp.mp_spmm_backward_x(h, rowptrT, it, colT, posT, None, rowptr, it, argout, G,
+                                  mp.MP_F32, N, N, F, red, gx, mp.MP_F32, wss[red],
+                                  wss[red].numel())
+            i += 1
+            mark(evs, i)
+        mp.mp_spmm_backward_w(rowptr, it, col, x, mp.MP_F32, G, mp.MP_F32, None, N, N, E, F,
+                              mp.MP_SUM, gw, ws_w, ws_w.numel())
+        mark(evs, i + 1)
+
+    return g, step, ops
+
+
+OP_KERNELS = {
+    "grad_x_sum_f32": "spmm_main (sum over the transposed CSR)",
+    "grad_x_mean_f32": "spmm_main (sum over the transposed CSR of G/deg)",
+    "grad_x_max_f32": "spmm_main, masked (argmax routing over the transposed CSR)",
+    "grad_w_sum_f32": "spmm_grad_w (per-edge dot products)",
+}
+
+
 def run(args):
     import numpy as np
     import torch
@@ -276,7 +370,7 @@ def run(args):
     web = args.workload == "web-1.6B"
     headline = args.workload == WORKLOAD
     dom = max((o for o in ops if o[2] > 0), key=lambda o: op_ms[o[0]])[0]
-    dom_kernel = DOMINANT + ", fp32 sum" if headline else f"spmm_main ({dom})"
+    dom_kernel = DOMINANT + ", fp32 sum" if headline else OP_KERNELS.get(dom, f"spmm_main ({dom})")
     if headline:
         dom = "sum_f32"
     dom_ms, dom_bytes = op_ms[dom], op_bytes[dom]
@@ -294,6 +388,9 @@ def run(args):
                           "COO->CSR (+perm, weights to CSR order) + plan + mean + weighted sum"),
         "uniform-10k": (f"uniform-10k: uniform random graph, N={N}, E={E}, F={F}, fp32 U(-1,1), "
                         f"seed {args.seed}", "COO->CSR + plan + sum"),
+        BACKWARD: (f"{BACKWARD}: the Chung-Lu graph of {WORKLOAD} (N={N}, E={E}, F={F}, fp32 "
+                   f"x and output gradient N(0,1)), seed {args.seed}",
+                   "CSR transpose + plan + dL/dx {sum, mean, max} + dL/dw sum"),
         "hetero-20M": (f"hetero-20M: 3 node types (1.9M, 736k, 8.7k), 4 relations (5.4M, 7.1M, "
                        f"7.1M, 1.0M edges), F={F} bf16, seed {args.seed}",
                        "per destination type: combined CSR + plan + sum over relations"),
@@ -471,7 +568,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--workload", default=WORKLOAD,
-                    choices=[WORKLOAD, "web-1.6B", "powerlaw-1.2M", "uniform-10k", "hetero-20M"],
+                    choices=[WORKLOAD, BACKWARD, "web-1.6B", "powerlaw-1.2M", "uniform-10k",
+                             "hetero-20M"],
                     help="benchmark workload (the default is the metric's configuration)")
     ap.add_argument("--cpu-rows", type=int, default=0,
                     help="rows of the CPU-oracle aggregation sample (0: all rows)")
