@@ -13,8 +13,8 @@
 //     per-edge dot is reduced over the lanes of a slot in a fixed tree.
 //
 // The gradient with respect to x reuses the aggregation kernels of spmm.hip
-// over the transposed CSR (sum, mean after scale_inv_deg, and a masked sum
-// for max).
+// over the transposed CSR (sum, mean after scale_inv_deg, and for max a
+// masked sum driven by the win mask built here by win_mask).
 #include <type_traits>
 
 #include "mp_internal.hpp"
@@ -58,6 +58,28 @@ __global__ __launch_bounds__(kBlock) void rows_of_edges(const void* __restrict__
 }
 
 __device__ inline float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
+
+__global__ __launch_bounds__(kBlock) void clear_u32(int64_t n, uint32_t* __restrict__ p) {
+    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n;
+         i += (int64_t)gridDim.x * kBlock)
+        p[i] = 0u;
+}
+
+// Win mask of the forward max: for every (v, f) whose argmax is the CSR
+// position p, set bit f of position p's mask words.  Consecutive threads take
+// consecutive features of one row, whose positions all lie in that row's CSR
+// range, so the integer ORs stay within a few cache lines.  OR is
+// order-independent: the mask is deterministic.
+__global__ __launch_bounds__(kBlock) void win_mask(const int32_t* __restrict__ argout, int64_t N,
+                                                   int64_t F, int64_t words,
+                                                   uint32_t* __restrict__ mask) {
+    const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (i >= N * F) return;
+    const int32_t p = argout[i];
+    if (p < 0) return;
+    const int64_t f = i - (i / F) * F;
+    atomicOr(mask + (int64_t)p * words + (f >> 5), 1u << (f & 31));
+}
 
 // out[v, f] = g[v, f] / deg(v) in fp32 (0 for an empty row).
 template <bool GB>
@@ -245,6 +267,19 @@ hipError_t launch_rows_of_edges(const void* rowptr, int rp64, int64_t N, int64_t
     const int64_t threads = ceil_div(E, kRowItems);
     hipLaunchKernelGGL(rows_of_edges, dim3((unsigned)ceil_div(threads, kBlock)), dim3(kBlock), 0,
                        s, rowptr, rp64, N, E, row);
+    return hipGetLastError();
+}
+
+hipError_t launch_win_mask(const int32_t* argout, int64_t N_dst, int64_t F, int64_t E,
+                           int64_t words, uint32_t* mask, hipStream_t s) {
+    const int64_t n = E * words;
+    if (n <= 0) return hipSuccess;
+    const int64_t blocks = ceil_div(n, kBlock);
+    hipLaunchKernelGGL(clear_u32, dim3((unsigned)(blocks < 65536 ? blocks : 65536)), dim3(kBlock), 0,
+                       s, n, mask);
+    if (N_dst * F > 0)
+        hipLaunchKernelGGL(win_mask, dim3((unsigned)ceil_div(N_dst * F, kBlock)), dim3(kBlock), 0,
+                           s, argout, N_dst, F, words, mask);
     return hipGetLastError();
 }
 

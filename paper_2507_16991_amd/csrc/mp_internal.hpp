@@ -150,10 +150,12 @@ struct SpmmParams {
     int max_bf16;
     int32_t* argout;
     int vec_store;  // 1: out, out_max and argout are 16-byte aligned
-    // masked sum (gradient of max): edge t contributes feature f only where
-    // mtab[c_t * F + f] == ekey[t]; both nullptr otherwise
+    // masked sum (the gradient of max): edge t contributes feature f only if
+    // bit f of the win mask of forward position ekey[t] is set (mwords
+    // 32-bit words per position); nullptr otherwise
     const int32_t* ekey;
-    const int32_t* mtab;
+    const uint32_t* mbits;
+    int64_t mwords;
     float* part_sum;
     float* part_max;
     int32_t* part_arg;
@@ -180,6 +182,10 @@ hipError_t launch_scale_inv_deg(const void* g, int g_bf16, const void* rowptr, i
                                 int64_t F, float* out, hipStream_t s);
 hipError_t launch_spmm_grad_w(const GradWParams& p, int x_dtype, int g_dtype, int epl,
                               hipStream_t s);
+// win mask of the forward max: bit f of position argout[v, f] for every (v, f)
+// with a non-empty row; the mask is cleared first (E * words 32-bit words)
+hipError_t launch_win_mask(const int32_t* argout, int64_t N_dst, int64_t F, int64_t E,
+                           int64_t words, uint32_t* mask, hipStream_t s);
 
 hipError_t launch_spmm(const SpmmParams& p, int x_dtype, int epl, hipStream_t s);
 hipError_t launch_spmm_tiny(const SpmmParams& p, int x_dtype, int epl, hipStream_t s);
