@@ -71,15 +71,15 @@ def grad_x_bytes(N_dst, N_src, E, F, mode):
     """Transposed gather of the output gradient, one output row per source.
     Mean adds the scaled copy of the gradient.  Max routes one gradient
     element per destination row and feature: it reads the argmax table once,
-    writes and reads a win mask of one bit per edge and feature (in 32-bit
-    words), reads the forward positions, and gathers only the routed
-    elements."""
+    builds a win mask of one bit per edge and feature (in 32-bit words: written
+    in forward order, permuted to transposed order through the positions, read
+    once by the gather), and gathers only the routed elements."""
     b = 4 * (N_src + 1) + 4 * E + N_src * F * 4
     if mode == "mean":
         b += 4 * (N_dst + 1) + 2 * N_dst * F * 4
     if mode == "max":
         mask = E * ((F + 31) // 32) * 4
-        return b + 4 * E + N_dst * F * 4 + 2 * mask + N_dst * F * 4
+        return b + 4 * E + N_dst * F * 4 + 4 * mask + N_dst * F * 4
     return b + E * F * 4
 
 

@@ -501,7 +501,8 @@ int mp_csr_transpose(const void* rowptr, int rowptr_itype, const int32_t* col, i
 // gradient (mean) or the win mask (max).
 size_t backward_x_extra(int64_t N_dst, int64_t E, int64_t F, int reduce) {
     if (reduce == MP_MEAN) return align_up((size_t)N_dst * (size_t)F * 4, 256);
-    if (reduce == MP_MAX) return align_up((size_t)E * (size_t)ceil_div(F, 32) * 4, 256);
+    // max: the win mask in forward order and in transposed order
+    if (reduce == MP_MAX) return 2 * align_up((size_t)E * (size_t)ceil_div(F, 32) * 4, 256);
     return 0;
 }
 
@@ -526,14 +527,14 @@ int mp_spmm_backward_x(const mp_plan* planT, const void* rowptrT, int rowptrT_it
     if (reduce != MP_SUM && reduce != MP_MEAN && reduce != MP_MAX) return MP_ERR_REDUCE;
     if (!valid_itype(rowptrT_itype) || !valid_dtype(g_dtype) || !valid_dtype(out_dtype))
         return MP_ERR_DTYPE;
-    if (reduce == MP_MEAN && !valid_itype(rowptr_itype)) return MP_ERR_DTYPE;
+    if (reduce != MP_SUM && !valid_itype(rowptr_itype)) return MP_ERR_DTYPE;
     if (N_src < 0 || N_src > INT32_MAX || N_dst < 0 || N_dst > INT32_MAX || E < 0 ||
         E > INT32_MAX || F < 1 || F > 65536)
         return MP_ERR_SIZE;
     if (!rowptrT) return MP_ERR_NULL;
     if (N_src > 0) {
         if (!colT || !grad_out || !grad_x) return MP_ERR_NULL;
-        if (reduce == MP_MEAN && !rowptr) return MP_ERR_NULL;
+        if (reduce != MP_SUM && !rowptr) return MP_ERR_NULL;
         if (reduce == MP_MAX && (!argout || !posT)) return MP_ERR_NULL;
     }
     int st = check_plan(planT, rowptrT, rowptrT_itype, N_src, F);
@@ -543,7 +544,7 @@ int mp_spmm_backward_x(const mp_plan* planT, const void* rowptrT, int rowptrT_it
     if ((uintptr_t)grad_out % eb || (uintptr_t)rowptrT % (rowptrT_itype == MP_I64 ? 8 : 4) ||
         (uintptr_t)colT % 4 || (uintptr_t)posT % 4 || (uintptr_t)wT % 4 ||
         (uintptr_t)argout % 4 || (uintptr_t)grad_x % (out_dtype == MP_BF16 ? 2 : 4) ||
-        (reduce == MP_MEAN && (uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4)))
+        (reduce != MP_SUM && (uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4)))
         return MP_ERR_ALIGN;
     if (N_src == 0) return MP_OK;
     hipStream_t s = as_stream(stream);
@@ -566,12 +567,15 @@ int mp_spmm_backward_x(const mp_plan* planT, const void* rowptrT, int rowptrT_it
         t_dtype = MP_F32;
     } else if (reduce == MP_MAX) {
         // max: a sum over the transposed CSR restricted, per edge, to the
-        // features its forward position won
-        uint32_t* mask = reinterpret_cast<uint32_t*>(extra_buf);
+        // features it won in the forward pass
         const int64_t words = ceil_div(F, 32);
-        if (launch_win_mask(argout, N_dst, F, E, words, mask, s) != hipSuccess) return MP_ERR_HIP;
-        P.ekey = posT;
-        P.mbits = mask;
+        uint32_t* mask = reinterpret_cast<uint32_t*>(extra_buf);
+        uint32_t* maskT = reinterpret_cast<uint32_t*>(
+            extra_buf + align_up((size_t)E * (size_t)words * 4, 256));
+        if (launch_win_mask(argout, rowptr, rowptr_itype == MP_I64, N_dst, F, E, posT, words, mask,
+                            maskT, s) != hipSuccess)
+            return MP_ERR_HIP;
+        P.mbits = maskT;
         P.mwords = words;
     }
     Geometry g = make_geometry(F, t_dtype, (uintptr_t)table);

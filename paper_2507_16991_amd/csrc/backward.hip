@@ -14,7 +14,7 @@
 //
 // The gradient with respect to x reuses the aggregation kernels of spmm.hip
 // over the transposed CSR (sum, mean after scale_inv_deg, and for max a
-// masked sum driven by the win mask built here by win_mask).
+// masked sum driven by the win mask built here, in transposed order).
 #include <type_traits>
 
 #include "mp_internal.hpp"
@@ -59,26 +59,48 @@ __global__ __launch_bounds__(kBlock) void rows_of_edges(const void* __restrict__
 
 __device__ inline float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
 
-__global__ __launch_bounds__(kBlock) void clear_u32(int64_t n, uint32_t* __restrict__ p) {
-    for (int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x; i < n;
-         i += (int64_t)gridDim.x * kBlock)
-        p[i] = 0u;
+// Win mask of the forward max, in forward CSR order: bit b of word k of
+// position p is set iff argout[row(p), 32k + b] == p.  One thread per
+// position assembles its words from its row of argout (neighbouring positions
+// share rows, so those reads are served by the cache); no atomics, and every
+// word is written, so nothing needs clearing first.  V4: F % 4 == 0 and argout
+// is 16-byte aligned (int4 reads).
+template <bool V4>
+__global__ __launch_bounds__(kBlock) void win_mask_fwd(const int32_t* __restrict__ argout,
+                                                       const int32_t* __restrict__ row, int64_t E,
+                                                       int64_t F, int64_t words,
+                                                       uint32_t* __restrict__ mask) {
+    const int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    if (p >= E) return;
+    const int32_t* a = argout + (int64_t)row[p] * F;
+    const int32_t me = (int32_t)p;
+    for (int64_t k = 0; k < words; ++k) {
+        const int64_t f0 = k * 32;
+        const int n = F - f0 < 32 ? (int)(F - f0) : 32;
+        uint32_t word = 0;
+        if (V4) {
+            for (int b = 0; b < n; b += 4) {
+                const int4 q = *reinterpret_cast<const int4*>(a + f0 + b);
+                word |= ((uint32_t)(q.x == me) << b) | ((uint32_t)(q.y == me) << (b + 1)) |
+                        ((uint32_t)(q.z == me) << (b + 2)) | ((uint32_t)(q.w == me) << (b + 3));
+            }
+        } else {
+            for (int b = 0; b < n; ++b) word |= (uint32_t)(a[f0 + b] == me) << b;
+        }
+        mask[p * words + k] = word;
+    }
 }
 
-// Win mask of the forward max: for every (v, f) whose argmax is the CSR
-// position p, set bit f of position p's mask words.  Consecutive threads take
-// consecutive features of one row, whose positions all lie in that row's CSR
-// range, so the integer ORs stay within a few cache lines.  OR is
-// order-independent: the mask is deterministic.
-__global__ __launch_bounds__(kBlock) void win_mask(const int32_t* __restrict__ argout, int64_t N,
-                                                   int64_t F, int64_t words,
-                                                   uint32_t* __restrict__ mask) {
+// The same mask in transposed CSR order: maskT[t] = mask[posT[t]] (one
+// thread per 32-bit word).
+__global__ __launch_bounds__(kBlock) void mask_to_transposed(const uint32_t* __restrict__ mask,
+                                                             const int32_t* __restrict__ posT,
+                                                             int64_t E, int64_t words,
+                                                             uint32_t* __restrict__ maskT) {
     const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (i >= N * F) return;
-    const int32_t p = argout[i];
-    if (p < 0) return;
-    const int64_t f = i - (i / F) * F;
-    atomicOr(mask + (int64_t)p * words + (f >> 5), 1u << (f & 31));
+    if (i >= E * words) return;
+    const int64_t t = i / words;
+    maskT[i] = mask[(int64_t)posT[t] * words + (i - t * words)];
 }
 
 // out[v, f] = g[v, f] / deg(v) in fp32 (0 for an empty row).
@@ -270,16 +292,26 @@ hipError_t launch_rows_of_edges(const void* rowptr, int rp64, int64_t N, int64_t
     return hipGetLastError();
 }
 
-hipError_t launch_win_mask(const int32_t* argout, int64_t N_dst, int64_t F, int64_t E,
-                           int64_t words, uint32_t* mask, hipStream_t s) {
-    const int64_t n = E * words;
-    if (n <= 0) return hipSuccess;
-    const int64_t blocks = ceil_div(n, kBlock);
-    hipLaunchKernelGGL(clear_u32, dim3((unsigned)(blocks < 65536 ? blocks : 65536)), dim3(kBlock), 0,
-                       s, n, mask);
-    if (N_dst * F > 0)
-        hipLaunchKernelGGL(win_mask, dim3((unsigned)ceil_div(N_dst * F, kBlock)), dim3(kBlock), 0,
-                           s, argout, N_dst, F, words, mask);
+hipError_t launch_win_mask(const int32_t* argout, const void* rowptr, int rp64, int64_t N_dst,
+                           int64_t F, int64_t E, const int32_t* posT, int64_t words,
+                           uint32_t* mask, uint32_t* maskT, hipStream_t s) {
+    if (E <= 0) return hipSuccess;
+    // the row of every forward position, kept in maskT's space until the
+    // permutation overwrites it (maskT holds E * words >= E words)
+    int32_t* row = reinterpret_cast<int32_t*>(maskT);
+    hipError_t e = launch_rows_of_edges(rowptr, rp64, N_dst, E, row, s);
+    if (e != hipSuccess) return e;
+    const unsigned g1 = (unsigned)ceil_div(E, kBlock);
+    if (F % 4 == 0 && reinterpret_cast<uintptr_t>(argout) % 16 == 0)
+        hipLaunchKernelGGL(win_mask_fwd<true>, dim3(g1), dim3(kBlock), 0, s, argout, row, E, F,
+                           words, mask);
+    else
+        hipLaunchKernelGGL(win_mask_fwd<false>, dim3(g1), dim3(kBlock), 0, s, argout, row, E, F,
+                           words, mask);
+    e = hipGetLastError();
+    if (e != hipSuccess) return e;
+    hipLaunchKernelGGL(mask_to_transposed, dim3((unsigned)ceil_div(E * words, kBlock)), dim3(kBlock),
+                       0, s, mask, posT, E, words, maskT);
     return hipGetLastError();
 }
 

@@ -114,7 +114,8 @@ __global__ void radix_gscan(uint32_t* __restrict__ g, int passes, int bits) {
 template <bool HAS_B>
 __global__ __launch_bounds__(kSortBlock) void radix_onesweep(RadixPass p) {
     __shared__ uint32_t s_key[kSortTile];
-    __shared__ int32_t s_a[kSortTile];  // staging of payload a, then of payload b
+    __shared__ int32_t s_a[kSortTile];
+    __shared__ int32_t s_b[HAS_B ? kSortTile : 1];
     __shared__ uint32_t s_cnt[kSortWaves][kMaxBuckets];
     __shared__ uint32_t s_start[kMaxBuckets];
     __shared__ uint32_t s_gbase[kMaxBuckets];
@@ -242,6 +243,7 @@ __global__ __launch_bounds__(kSortBlock) void radix_onesweep(RadixPass p) {
             const uint32_t lp = s_start[d] + s_cnt[wv][d] + rank[k];
             s_key[lp] = key[k];
             s_a[lp] = va[k];
+            if constexpr (HAS_B) s_b[lp] = vb[k];
         }
     }
     __syncthreads();
@@ -254,26 +256,8 @@ __global__ __launch_bounds__(kSortBlock) void radix_onesweep(RadixPass p) {
         if (pos >= p.n) continue;  // cannot happen for consistent counts; never write past n
         if (p.keys_out) p.keys_out[pos] = kk;
         if (p.a_out) p.a_out[pos] = s_a[i];
-    }
-    if constexpr (HAS_B) {
-        // second payload through the same staging buffer: the tile's LDS stays
-        // at two arrays, so two workgroups fit on a CU
-        __syncthreads();
-#pragma unroll
-        for (int k = 0; k < kSortItems; ++k) {
-            const int64_t i = wbase + (int64_t)k * kWave + lane;
-            if (i < p.n) {
-                const uint32_t d = (key[k] >> p.shift) & (uint32_t)(R - 1);
-                s_a[s_start[d] + s_cnt[wv][d] + rank[k]] = vb[k];
-            }
-        }
-        __syncthreads();
-        if (p.b_out) {
-            for (int i = threadIdx.x; i < nvalid; i += kSortBlock) {
-                const uint32_t d = (s_key[i] >> p.shift) & (uint32_t)(R - 1);
-                const int64_t pos = (int64_t)s_gbase[d] + (i - (int64_t)s_start[d]);
-                if (pos < p.n) p.b_out[pos] = s_a[i];
-            }
+        if constexpr (HAS_B) {
+            if (p.b_out) p.b_out[pos] = s_b[i];
         }
     }
 }

@@ -65,13 +65,13 @@ __device__ inline void widen(const typename RawVec<TX, EPL>::T& r, float (&v)[EP
     }
 }
 
-// Masked sum (the gradient of max): the win mask holds, for every forward
-// CSR position, one bit per feature that the position won (mwords 32-bit
-// words per position).  win_bits returns the bits of this lane's EPL features
-// (EPL divides 32, so they never straddle two words).
+// Masked sum (the gradient of max): the win mask holds, for every CSR
+// position, one bit per feature that the edge won (mwords 32-bit words per
+// position).  win_bits returns the bits of this lane's EPL features (EPL
+// divides 32, so they never straddle two words).
 template <int EPL>
-__device__ inline uint32_t win_bits(const SpmmParams& P, int32_t key, int64_t fe) {
-    const uint32_t w = P.mbits[(int64_t)key * P.mwords + (fe >> 5)];
+__device__ inline uint32_t win_bits(const SpmmParams& P, int64_t pos, int64_t fe) {
+    const uint32_t w = P.mbits[pos * P.mwords + (fe >> 5)];
     return (w >> (fe & 31)) & ((1u << EPL) - 1u);
 }
 
@@ -280,12 +280,11 @@ __device__ inline void wave_range(const SpmmParams& P, Acc<EPL, HS, HM>& acc, in
     const int tile = steps * SU;
     for (int64_t p0 = e0; p0 < e1; p0 += tile) {
         const int64_t rem = e1 - p0;
-        int32_t myc = 0, myk = 0;
+        int32_t myc = 0;
         float myw = 1.f;
         if (lane < tile && lane < rem) {
             myc = __builtin_nontemporal_load(P.col + p0 + lane);
             if constexpr (W) myw = __builtin_nontemporal_load(P.w + p0 + lane);
-            if constexpr (MK) myk = __builtin_nontemporal_load(P.ekey + p0 + lane);
         }
         for (int st = 0; st < steps; ++st) {
             const int base = st * SU;
@@ -301,8 +300,7 @@ __device__ inline void wave_range(const SpmmParams& P, Acc<EPL, HS, HM>& acc, in
                 addr[u] = feat_addr<TX, NT>(P, c, fe);
                 if constexpr (MK) {
                     // only chunks holding a won feature are gathered
-                    const int32_t key = __shfl(myk, t);
-                    bits[u] = ok[u] ? win_bits<EPL>(P, key, fe) : 0u;
+                    bits[u] = ok[u] ? win_bits<EPL>(P, p0 + t, fe) : 0u;
                     ok[u] = bits[u] != 0u;
                 }
             }
@@ -344,14 +342,12 @@ __device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int6
         const char* addr[kUnroll];
         bool ok[kUnroll];
         float wt[kUnroll];
-        int32_t key[kUnroll];
         if constexpr (COOP) {
-            int32_t myc = 0, myk = 0;
+            int32_t myc = 0;
             float myw = 1.f;
             if (j < kUnroll && it + j < my_n) {
                 myc = __builtin_nontemporal_load(P.col + e0 + it + j);
                 if constexpr (W) myw = __builtin_nontemporal_load(P.w + e0 + it + j);
-                if constexpr (MK) myk = __builtin_nontemporal_load(P.ekey + e0 + it + j);
             }
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
@@ -359,8 +355,6 @@ __device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int6
                 const int32_t c = __shfl(myc, srcl);
                 wt[u] = 1.f;
                 if constexpr (W) wt[u] = __shfl(myw, srcl);
-                key[u] = 0;
-                if constexpr (MK) key[u] = __shfl(myk, srcl);
                 ok[u] = feat_ok && (it + u < my_n);
                 addr[u] = feat_addr<TX, NT>(P, c, fe);
             }
@@ -372,8 +366,6 @@ __device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int6
                 cc[u] = ok[u] ? P.col[e0 + it + u] : 0;
                 wt[u] = 1.f;
                 if constexpr (W) wt[u] = ok[u] ? P.w[e0 + it + u] : 1.f;
-                key[u] = 0;
-                if constexpr (MK) key[u] = ok[u] ? P.ekey[e0 + it + u] : 0;
             }
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) addr[u] = feat_addr<TX, NT>(P, cc[u], fe);
@@ -382,7 +374,7 @@ __device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int6
         if constexpr (MK) {
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
-                bits[u] = ok[u] ? win_bits<EPL>(P, key[u], fe) : 0u;
+                bits[u] = ok[u] ? win_bits<EPL>(P, e0 + it + u, fe) : 0u;
                 ok[u] = bits[u] != 0u;
             }
         }
@@ -544,23 +536,21 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
             }
         }
     };
-    auto cols = [&](int32_t beg, int32_t deg, int32_t& c, float& w, int32_t& key) {
+    auto cols = [&](int32_t beg, int32_t deg, int32_t& c, float& w) {
         c = 0;
         w = 1.f;
-        key = 0;
         if (j < deg) {
             c = __builtin_nontemporal_load(P.col + beg + j);
             if constexpr (W) w = __builtin_nontemporal_load(P.w + beg + j);
-            if constexpr (MK) key = __builtin_nontemporal_load(P.ekey + beg + j);
         }
     };
 
     int64_t it = tw;
     int32_t row, beg, deg, nrow, nbeg, ndeg;
-    int32_t cv, kv;
+    int32_t cv;
     float wv;
     rec(it, row, beg, deg);
-    cols(beg, deg, cv, wv, kv);
+    cols(beg, deg, cv, wv);
     rec(it + nw, nrow, nbeg, ndeg);
     for (; it < items; it += nw) {
         const int ft = (int)(it % P.FT);
@@ -575,8 +565,7 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
             ok[u] = feat_ok && (u < deg);
             if constexpr (MK) {
                 // only chunks holding a won feature are gathered
-                const int32_t key = __shfl(kv, slot * L + u);
-                bits[u] = ok[u] ? win_bits<EPL>(P, key, fe) : 0u;
+                bits[u] = ok[u] ? win_bits<EPL>(P, (int64_t)beg + u, fe) : 0u;
                 ok[u] = bits[u] != 0u;
             }
         }
@@ -592,9 +581,9 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
             if constexpr (W) wt[u] = __shfl(wv, slot * L + u);
         }
         // next group's columns, and the row ranges of the group after it
-        int32_t ncv, nkv;
+        int32_t ncv;
         float nwv;
-        cols(nbeg, ndeg, ncv, nwv, nkv);
+        cols(nbeg, ndeg, ncv, nwv);
         int32_t row2, beg2, deg2;
         rec(it + 2 * nw, row2, beg2, deg2);
 
@@ -619,7 +608,6 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
         deg = ndeg;
         cv = ncv;
         wv = nwv;
-        kv = nkv;
         nrow = row2;
         nbeg = beg2;
         ndeg = deg2;

@@ -172,7 +172,7 @@ def test_backward_errors_and_sizes():
     assert nb.value == 512
     # max: one bit per edge and feature, 32-bit words
     assert L.mp_spmm_backward_x_workspace(None, 10, 1000, 40, mp.MP_MAX, ctypes.byref(nb)) == 0
-    assert nb.value == 8192
+    assert nb.value == 2 * 8192
     assert L.mp_spmm_backward_x_workspace(None, 10, 100, 8, mp.MP_SUM | mp.MP_MAX,
                                           ctypes.byref(nb)) == -4
     bx = dict(planT=None, rowptrT=FAKE, itT=0, colT=FAKE, posT=FAKE, wT=None, rowptr=FAKE, it=0,
@@ -185,6 +185,7 @@ def test_backward_errors_and_sizes():
     assert bwx(reduce=mp.MP_MAX, argout=None) == -1
     assert bwx(reduce=mp.MP_MAX, posT=None) == -1
     assert bwx(reduce=mp.MP_MEAN, rowptr=None) == -1
+    assert bwx(reduce=mp.MP_MAX, rowptr=None) == -1
     assert bwx(reduce=mp.MP_MEAN) == -5  # needs a workspace for the scaled gradient
     assert bwx(reduce=mp.MP_MAX) == -5  # and one for the win mask
     assert bwx(E=-1) == -2
