@@ -68,19 +68,14 @@ def transpose_bytes(N_dst, N_src, E):
 
 
 def grad_x_bytes(N_dst, N_src, E, F, mode):
-    """Transposed gather of the output gradient, one output row per source.
-    Mean adds the scaled copy of the gradient.  Max routes one gradient
-    element per destination row and feature: it reads the argmax table once,
-    builds a win mask of one bit per edge and feature (in 32-bit words: written
-    in forward order, permuted to transposed order through the positions, read
-    once by the gather), and gathers only the routed elements."""
-    b = 4 * (N_src + 1) + 4 * E + N_src * F * 4
+    """Transposed gather of the output gradient (plus the argmax table for
+    max, plus the scaled copy for mean), one output row per source."""
+    b = 4 * (N_src + 1) + 4 * E + E * F * 4 + N_src * F * 4
     if mode == "mean":
         b += 4 * (N_dst + 1) + 2 * N_dst * F * 4
     if mode == "max":
-        mask = E * ((F + 31) // 32) * 4
-        return b + 4 * E + N_dst * F * 4 + 4 * mask + N_dst * F * 4
-    return b + E * F * 4
+        b += 4 * E + E * F * 4
+    return b
 
 
 def grad_w_bytes(N_dst, E, F):
@@ -303,11 +298,11 @@ def backward_step(g, mp, torch, np, dev, mark):
         mark(evs, 2)
         i = 2
         for red in (mp.MP_SUM, mp.MP_MEAN, mp.MP_MAX):
-            nb = mp.mp_spmm_backward_x_workspace(h, N, E, F, red)
+            nb = mp.mp_spmm_backward_x_workspace(h, N, F, red)
             if red not in wss or wss[red].numel() < nb:
                 wss[red] = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
             mp.mp_spmm_backward_x(h, rowptrT, it, colT, posT, None, rowptr, it, argout, G,
-                                  mp.MP_F32, N, N, E, F, red, gx, mp.MP_F32, wss[red],
+                                  mp.MP_F32, N, N, F, red, gx, mp.MP_F32, wss[red],
                                   wss[red].numel())
             i += 1
             mark(evs, i)
@@ -321,7 +316,7 @@ def backward_step(g, mp, torch, np, dev, mark):
 OP_KERNELS = {
     "grad_x_sum_f32": "spmm_main (sum over the transposed CSR)",
     "grad_x_mean_f32": "spmm_main (sum over the transposed CSR of G/deg)",
-    "grad_x_max_f32": "spmm_main, masked by the win mask (argmax routing over the transposed CSR)",
+    "grad_x_max_f32": "spmm_main, masked (argmax routing over the transposed CSR)",
     "grad_w_sum_f32": "spmm_grad_w (per-edge dot products)",
 }
 

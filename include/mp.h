@@ -216,24 +216,17 @@ int mp_csr_transpose(const void* rowptr, int rowptr_itype, const int32_t* col, i
                      int32_t* posT, const float* val_in, float* val_out, void* ws,
                      size_t ws_bytes, void* stream);
 
-/* Workspace bytes for mp_spmm_backward_x: hub partials of planT, plus for
- * MP_MEAN an fp32 copy of G divided by the in-degrees (N_dst * F * 4 bytes),
- * for MP_MAX the win mask in forward and in transposed order (one bit per
- * edge and feature: 2 * E * ceil(F/32) * 4 bytes). */
-int mp_spmm_backward_x_workspace(const mp_plan* planT, int64_t N_dst, int64_t E, int64_t F,
-                                 int reduce, size_t* bytes);
+/* Workspace bytes for mp_spmm_backward_x (hub partials of planT; for MP_MEAN
+ * also an fp32 copy of G divided by the in-degrees, N_dst * F * 4 bytes). */
+int mp_spmm_backward_x_workspace(const mp_plan* planT, int64_t N_dst, int64_t F, int reduce,
+                                 size_t* bytes);
 
 /* dL/dx of mp_spmm for one reduction (MP_SUM, MP_MEAN or MP_MAX; for a fused
- * forward call add the gradients of its parts).  For MP_MAX the argmax table
- * is first turned into a win mask (one bit per edge and feature, built per
- * forward position, then permuted to transposed order through posT), and the
- * transposed gather loads a G chunk only where the edge won one of its
- * features.
- *   planT       plan built on rowptrT (N_src rows, E edges, same F), or NULL.
+ * forward call add the gradients of its parts).
+ *   planT       plan built on rowptrT (N_src rows, same F), or NULL.
  *   rowptrT, colT, posT, wT   from mp_csr_transpose (wT = the forward weights
  *               in transposed order, NULL if unweighted; posT needed for MAX).
- *   rowptr      the forward rowptr (needed for MP_MEAN: in-degrees, and for
- *               MP_MAX: the row of each forward position).
+ *   rowptr      the forward rowptr (needed for MP_MEAN: in-degrees).
  *   argout      [N_dst, F] int32 from the forward call (needed for MP_MAX).
  *   grad_out    [N_dst, F] of g_dtype: G.
  *   grad_x      [N_src, F] of out_dtype, written in full (fp32 accumulation;
@@ -243,9 +236,9 @@ int mp_spmm_backward_x_workspace(const mp_plan* planT, int64_t N_dst, int64_t E,
 int mp_spmm_backward_x(const mp_plan* planT, const void* rowptrT, int rowptrT_itype,
                        const int32_t* colT, const int32_t* posT, const float* wT,
                        const void* rowptr, int rowptr_itype, const int32_t* argout,
-                       const void* grad_out, int g_dtype, int64_t N_dst, int64_t N_src, int64_t E,
-                       int64_t F, int reduce, void* grad_x, int out_dtype, void* ws,
-                       size_t ws_bytes, void* stream);
+                       const void* grad_out, int g_dtype, int64_t N_dst, int64_t N_src, int64_t F,
+                       int reduce, void* grad_x, int out_dtype, void* ws, size_t ws_bytes,
+                       void* stream);
 
 /* Workspace bytes for mp_spmm_backward_w (the row of every CSR edge, 4E). */
 int mp_spmm_backward_w_workspace(int64_t E, size_t* bytes);

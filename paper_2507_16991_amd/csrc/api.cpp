@@ -497,88 +497,72 @@ int mp_csr_transpose(const void* rowptr, int rowptr_itype, const int32_t* col, i
                            val_out, static_cast<char*>(ws) + c.off, ws_bytes - c.off, s);
 }
 
-// Workspace of mp_spmm_backward_x: hub partials of planT, then the scaled
-// gradient (mean) or the win mask (max).
-size_t backward_x_extra(int64_t N_dst, int64_t E, int64_t F, int reduce) {
-    if (reduce == MP_MEAN) return align_up((size_t)N_dst * (size_t)F * 4, 256);
-    // max: the win mask in forward order and in transposed order
-    if (reduce == MP_MAX) return 2 * align_up((size_t)E * (size_t)ceil_div(F, 32) * 4, 256);
-    return 0;
-}
-
-int mp_spmm_backward_x_workspace(const mp_plan* planT, int64_t N_dst, int64_t E, int64_t F,
-                                 int reduce, size_t* bytes) {
+int mp_spmm_backward_x_workspace(const mp_plan* planT, int64_t N_dst, int64_t F, int reduce,
+                                 size_t* bytes) {
     if (!bytes) return MP_ERR_NULL;
     if (reduce != MP_SUM && reduce != MP_MEAN && reduce != MP_MAX) return MP_ERR_REDUCE;
-    if (N_dst < 0 || E < 0 || E > INT32_MAX || F < 1 || F > 65536) return MP_ERR_SIZE;
+    if (N_dst < 0 || F < 1) return MP_ERR_SIZE;
     size_t b = 0;
     int st = mp_spmm_workspace(planT, MP_SUM, &b);
     if (st != MP_OK) return st;
-    *bytes = align_up(b, 256) + backward_x_extra(N_dst, E, F, reduce);
+    if (reduce == MP_MEAN) b = align_up(b, 256) + align_up((size_t)N_dst * (size_t)F * 4, 256);
+    *bytes = b;
     return MP_OK;
 }
 
 int mp_spmm_backward_x(const mp_plan* planT, const void* rowptrT, int rowptrT_itype,
                        const int32_t* colT, const int32_t* posT, const float* wT,
                        const void* rowptr, int rowptr_itype, const int32_t* argout,
-                       const void* grad_out, int g_dtype, int64_t N_dst, int64_t N_src, int64_t E,
-                       int64_t F, int reduce, void* grad_x, int out_dtype, void* ws,
-                       size_t ws_bytes, void* stream) {
+                       const void* grad_out, int g_dtype, int64_t N_dst, int64_t N_src, int64_t F,
+                       int reduce, void* grad_x, int out_dtype, void* ws, size_t ws_bytes,
+                       void* stream) {
     if (reduce != MP_SUM && reduce != MP_MEAN && reduce != MP_MAX) return MP_ERR_REDUCE;
     if (!valid_itype(rowptrT_itype) || !valid_dtype(g_dtype) || !valid_dtype(out_dtype))
         return MP_ERR_DTYPE;
-    if (reduce != MP_SUM && !valid_itype(rowptr_itype)) return MP_ERR_DTYPE;
-    if (N_src < 0 || N_src > INT32_MAX || N_dst < 0 || N_dst > INT32_MAX || E < 0 ||
-        E > INT32_MAX || F < 1 || F > 65536)
+    if (reduce == MP_MEAN && !valid_itype(rowptr_itype)) return MP_ERR_DTYPE;
+    if (N_src < 0 || N_src > INT32_MAX || N_dst < 0 || N_dst > INT32_MAX || F < 1 || F > 65536)
         return MP_ERR_SIZE;
     if (!rowptrT) return MP_ERR_NULL;
     if (N_src > 0) {
         if (!colT || !grad_out || !grad_x) return MP_ERR_NULL;
-        if (reduce != MP_SUM && !rowptr) return MP_ERR_NULL;
+        if (reduce == MP_MEAN && !rowptr) return MP_ERR_NULL;
         if (reduce == MP_MAX && (!argout || !posT)) return MP_ERR_NULL;
     }
     int st = check_plan(planT, rowptrT, rowptrT_itype, N_src, F);
     if (st != MP_OK) return st;
-    if (planT && planT->E != E) return MP_ERR_PLAN;
     const int eb = g_dtype == MP_BF16 ? 2 : 4;
     if ((uintptr_t)grad_out % eb || (uintptr_t)rowptrT % (rowptrT_itype == MP_I64 ? 8 : 4) ||
         (uintptr_t)colT % 4 || (uintptr_t)posT % 4 || (uintptr_t)wT % 4 ||
         (uintptr_t)argout % 4 || (uintptr_t)grad_x % (out_dtype == MP_BF16 ? 2 : 4) ||
-        (reduce != MP_SUM && (uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4)))
+        (reduce == MP_MEAN && (uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4)))
         return MP_ERR_ALIGN;
     if (N_src == 0) return MP_OK;
     hipStream_t s = as_stream(stream);
-    size_t part = 0;
-    mp_spmm_workspace(planT, MP_SUM, &part);
-    part = align_up(part, 256);
-    const size_t extra = backward_x_extra(N_dst, E, F, reduce);
-    if (ws_bytes < part + extra || (!ws && part + extra > 0)) return MP_ERR_WORKSPACE;
-    char* extra_buf = static_cast<char*>(ws) + part;
     const void* table = grad_out;
     int t_dtype = g_dtype;
-    SpmmParams P{};
+    void* spmm_ws = ws;
+    size_t spmm_ws_bytes = ws_bytes;
     if (reduce == MP_MEAN) {
         // mean: a sum over the transposed CSR of grad_out / in-degree
-        float* scaled = reinterpret_cast<float*>(extra_buf);
+        size_t part = 0;
+        mp_spmm_workspace(planT, MP_SUM, &part);
+        part = align_up(part, 256);
+        const size_t need = part + align_up((size_t)N_dst * (size_t)F * 4, 256);
+        if (ws_bytes < need || (!ws && need > 0)) return MP_ERR_WORKSPACE;
+        float* scaled = reinterpret_cast<float*>(static_cast<char*>(ws) + part);
         if (launch_scale_inv_deg(grad_out, g_dtype == MP_BF16, rowptr, rowptr_itype == MP_I64,
                                  N_dst, F, scaled, s) != hipSuccess)
             return MP_ERR_HIP;
         table = scaled;
         t_dtype = MP_F32;
-    } else if (reduce == MP_MAX) {
-        // max: a sum over the transposed CSR restricted, per edge, to the
-        // features it won in the forward pass
-        const int64_t words = ceil_div(F, 32);
-        uint32_t* mask = reinterpret_cast<uint32_t*>(extra_buf);
-        uint32_t* maskT = reinterpret_cast<uint32_t*>(
-            extra_buf + align_up((size_t)E * (size_t)words * 4, 256));
-        if (launch_win_mask(argout, rowptr, rowptr_itype == MP_I64, N_dst, F, E, posT, words, mask,
-                            maskT, s) != hipSuccess)
-            return MP_ERR_HIP;
-        P.mbits = maskT;
-        P.mwords = words;
+        spmm_ws_bytes = part;
     }
-    Geometry g = make_geometry(F, t_dtype, (uintptr_t)table);
+    // the mask table is read in lane-chunks of EPL int32: keep its alignment
+    // within what the feature geometry assumes
+    const uintptr_t mask_align =
+        reduce == MP_MAX ? (t_dtype == MP_BF16 ? (uintptr_t)argout >> 1 : (uintptr_t)argout) : 0;
+    Geometry g = make_geometry(F, t_dtype, (uintptr_t)table | mask_align);
+    SpmmParams P{};
     P.rowptr = rowptrT;
     P.rp64 = rowptrT_itype == MP_I64;
     P.col = colT;
@@ -590,7 +574,11 @@ int mp_spmm_backward_x(const mp_plan* planT, const void* rowptrT, int rowptrT_it
     P.out = grad_x;
     P.out_bf16 = out_dtype == MP_BF16;
     P.vec_store = ((uintptr_t)grad_x % 16) == 0;
-    return run_spmm(planT, P, g, t_dtype, N_src, ws, part, s);
+    if (reduce == MP_MAX) {
+        P.ekey = posT;
+        P.mtab = argout;
+    }
+    return run_spmm(planT, P, g, t_dtype, N_src, spmm_ws, spmm_ws_bytes, s);
 }
 
 int mp_spmm_backward_w_workspace(int64_t E, size_t* bytes) {

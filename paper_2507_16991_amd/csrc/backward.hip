@@ -13,8 +13,8 @@
 //     per-edge dot is reduced over the lanes of a slot in a fixed tree.
 //
 // The gradient with respect to x reuses the aggregation kernels of spmm.hip
-// over the transposed CSR (sum, mean after scale_inv_deg, and for max a
-// masked sum driven by the win mask built here, in transposed order).
+// over the transposed CSR (sum, mean after scale_inv_deg, and a masked sum
+// for max).
 #include <type_traits>
 
 #include "mp_internal.hpp"
@@ -58,50 +58,6 @@ __global__ __launch_bounds__(kBlock) void rows_of_edges(const void* __restrict__
 }
 
 __device__ inline float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
-
-// Win mask of the forward max, in forward CSR order: bit b of word k of
-// position p is set iff argout[row(p), 32k + b] == p.  One thread per
-// position assembles its words from its row of argout (neighbouring positions
-// share rows, so those reads are served by the cache); no atomics, and every
-// word is written, so nothing needs clearing first.  V4: F % 4 == 0 and argout
-// is 16-byte aligned (int4 reads).
-template <bool V4>
-__global__ __launch_bounds__(kBlock) void win_mask_fwd(const int32_t* __restrict__ argout,
-                                                       const int32_t* __restrict__ row, int64_t E,
-                                                       int64_t F, int64_t words,
-                                                       uint32_t* __restrict__ mask) {
-    const int64_t p = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (p >= E) return;
-    const int32_t* a = argout + (int64_t)row[p] * F;
-    const int32_t me = (int32_t)p;
-    for (int64_t k = 0; k < words; ++k) {
-        const int64_t f0 = k * 32;
-        const int n = F - f0 < 32 ? (int)(F - f0) : 32;
-        uint32_t word = 0;
-        if (V4) {
-            for (int b = 0; b < n; b += 4) {
-                const int4 q = *reinterpret_cast<const int4*>(a + f0 + b);
-                word |= ((uint32_t)(q.x == me) << b) | ((uint32_t)(q.y == me) << (b + 1)) |
-                        ((uint32_t)(q.z == me) << (b + 2)) | ((uint32_t)(q.w == me) << (b + 3));
-            }
-        } else {
-            for (int b = 0; b < n; ++b) word |= (uint32_t)(a[f0 + b] == me) << b;
-        }
-        mask[p * words + k] = word;
-    }
-}
-
-// The same mask in transposed CSR order: maskT[t] = mask[posT[t]] (one
-// thread per 32-bit word).
-__global__ __launch_bounds__(kBlock) void mask_to_transposed(const uint32_t* __restrict__ mask,
-                                                             const int32_t* __restrict__ posT,
-                                                             int64_t E, int64_t words,
-                                                             uint32_t* __restrict__ maskT) {
-    const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (i >= E * words) return;
-    const int64_t t = i / words;
-    maskT[i] = mask[(int64_t)posT[t] * words + (i - t * words)];
-}
 
 // out[v, f] = g[v, f] / deg(v) in fp32 (0 for an empty row).
 template <bool GB>
@@ -289,29 +245,6 @@ hipError_t launch_rows_of_edges(const void* rowptr, int rp64, int64_t N, int64_t
     const int64_t threads = ceil_div(E, kRowItems);
     hipLaunchKernelGGL(rows_of_edges, dim3((unsigned)ceil_div(threads, kBlock)), dim3(kBlock), 0,
                        s, rowptr, rp64, N, E, row);
-    return hipGetLastError();
-}
-
-hipError_t launch_win_mask(const int32_t* argout, const void* rowptr, int rp64, int64_t N_dst,
-                           int64_t F, int64_t E, const int32_t* posT, int64_t words,
-                           uint32_t* mask, uint32_t* maskT, hipStream_t s) {
-    if (E <= 0) return hipSuccess;
-    // the row of every forward position, kept in maskT's space until the
-    // permutation overwrites it (maskT holds E * words >= E words)
-    int32_t* row = reinterpret_cast<int32_t*>(maskT);
-    hipError_t e = launch_rows_of_edges(rowptr, rp64, N_dst, E, row, s);
-    if (e != hipSuccess) return e;
-    const unsigned g1 = (unsigned)ceil_div(E, kBlock);
-    if (F % 4 == 0 && reinterpret_cast<uintptr_t>(argout) % 16 == 0)
-        hipLaunchKernelGGL(win_mask_fwd<true>, dim3(g1), dim3(kBlock), 0, s, argout, row, E, F,
-                           words, mask);
-    else
-        hipLaunchKernelGGL(win_mask_fwd<false>, dim3(g1), dim3(kBlock), 0, s, argout, row, E, F,
-                           words, mask);
-    e = hipGetLastError();
-    if (e != hipSuccess) return e;
-    hipLaunchKernelGGL(mask_to_transposed, dim3((unsigned)ceil_div(E * words, kBlock)), dim3(kBlock),
-                       0, s, mask, posT, E, words, maskT);
     return hipGetLastError();
 }
 

@@ -150,11 +150,10 @@ struct SpmmParams {
     int max_bf16;
     int32_t* argout;
     int vec_store;  // 1: out, out_max and argout are 16-byte aligned
-    // masked sum (the gradient of max): the edge at CSR position t
-    // contributes feature f only if bit f of its win mask is set (mwords
-    // 32-bit words per position); nullptr otherwise
-    const uint32_t* mbits;
-    int64_t mwords;
+    // masked sum (gradient of max): edge t contributes feature f only where
+    // mtab[c_t * F + f] == ekey[t]; both nullptr otherwise
+    const int32_t* ekey;
+    const int32_t* mtab;
     float* part_sum;
     float* part_max;
     int32_t* part_arg;
@@ -181,12 +180,6 @@ hipError_t launch_scale_inv_deg(const void* g, int g_bf16, const void* rowptr, i
                                 int64_t F, float* out, hipStream_t s);
 hipError_t launch_spmm_grad_w(const GradWParams& p, int x_dtype, int g_dtype, int epl,
                               hipStream_t s);
-// win mask of the forward max in transposed CSR order: maskT[t * words + k]
-// bit b set iff the forward position posT[t] is the argmax of feature 32k + b
-// of its row.  mask (forward order) and maskT each hold E * words words.
-hipError_t launch_win_mask(const int32_t* argout, const void* rowptr, int rp64, int64_t N_dst,
-                           int64_t F, int64_t E, const int32_t* posT, int64_t words,
-                           uint32_t* mask, uint32_t* maskT, hipStream_t s);
 
 hipError_t launch_spmm(const SpmmParams& p, int x_dtype, int epl, hipStream_t s);
 hipError_t launch_spmm_tiny(const SpmmParams& p, int x_dtype, int epl, hipStream_t s);

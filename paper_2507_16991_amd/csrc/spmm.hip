@@ -65,20 +65,29 @@ __device__ inline void widen(const typename RawVec<TX, EPL>::T& r, float (&v)[EP
     }
 }
 
-// Masked sum (the gradient of max): the win mask holds, for every CSR
-// position, one bit per feature that the edge won (mwords 32-bit words per
-// position).  win_bits returns the bits of this lane's EPL features (EPL
-// divides 32, so they never straddle two words).
+// EPL consecutive int32 (a lane-chunk of the mask table), 16-byte loads
+// when EPL >= 4; p is aligned to min(16, 4 * EPL) bytes.
 template <int EPL>
-__device__ inline uint32_t win_bits(const SpmmParams& P, int64_t pos, int64_t fe) {
-    const uint32_t w = P.mbits[pos * P.mwords + (fe >> 5)];
-    return (w >> (fe & 31)) & ((1u << EPL) - 1u);
+__device__ inline void load_mask(const int32_t* p, int32_t (&v)[EPL]) {
+    if constexpr (EPL >= 4) {
+#pragma unroll
+        for (int q = 0; q < EPL / 4; ++q) {
+            const int4 a = reinterpret_cast<const int4*>(p)[q];
+            v[4 * q + 0] = a.x; v[4 * q + 1] = a.y; v[4 * q + 2] = a.z; v[4 * q + 3] = a.w;
+        }
+    } else if constexpr (EPL == 2) {
+        const int2 a = *reinterpret_cast<const int2*>(p);
+        v[0] = a.x; v[1] = a.y;
+    } else {
+        v[0] = *p;
+    }
 }
 
+// Keep only the features whose mask entry names this edge.
 template <int EPL>
-__device__ inline void keep_won(float (&v)[EPL], uint32_t bits) {
+__device__ inline void apply_mask(float (&v)[EPL], const int32_t (&m)[EPL], int32_t key) {
 #pragma unroll
-    for (int k = 0; k < EPL; ++k) v[k] = ((bits >> k) & 1u) ? v[k] : 0.f;
+    for (int k = 0; k < EPL; ++k) v[k] = m[k] == key ? v[k] : 0.f;
 }
 
 // fp32 -> bf16 bits, round to nearest even (finite values).
@@ -280,39 +289,42 @@ __device__ inline void wave_range(const SpmmParams& P, Acc<EPL, HS, HM>& acc, in
     const int tile = steps * SU;
     for (int64_t p0 = e0; p0 < e1; p0 += tile) {
         const int64_t rem = e1 - p0;
-        int32_t myc = 0;
+        int32_t myc = 0, myk = -1;
         float myw = 1.f;
         if (lane < tile && lane < rem) {
             myc = __builtin_nontemporal_load(P.col + p0 + lane);
             if constexpr (W) myw = __builtin_nontemporal_load(P.w + p0 + lane);
+            if constexpr (MK) myk = __builtin_nontemporal_load(P.ekey + p0 + lane);
         }
         for (int st = 0; st < steps; ++st) {
             const int base = st * SU;
             if (base >= rem) break;
             const char* addr[kUnroll];
+            const int32_t* maddr[kUnroll];
             bool ok[kUnroll];
-            uint32_t bits[MK ? kUnroll : 1];
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
                 const int t = base + u * S + slot;
                 const int32_t c = __shfl(myc, t);
                 ok[u] = feat_ok && (u < U) && (t < rem);
                 addr[u] = feat_addr<TX, NT>(P, c, fe);
-                if constexpr (MK) {
-                    // only chunks holding a won feature are gathered
-                    bits[u] = ok[u] ? win_bits<EPL>(P, p0 + t, fe) : 0u;
-                    ok[u] = bits[u] != 0u;
-                }
+                if constexpr (MK) maddr[u] = P.mtab + (int64_t)c * P.F + fe;
             }
             R raw[kUnroll];
+            int32_t mraw[MK ? kUnroll : 1][EPL];
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u)
-                if (ok[u]) raw[u] = *reinterpret_cast<const R*>(addr[u]);
+                if (ok[u]) {
+                    raw[u] = *reinterpret_cast<const R*>(addr[u]);
+                    if constexpr (MK) load_mask<EPL>(maddr[u], mraw[u]);
+                }
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
                 const int t = base + u * S + slot;
                 float wt = 1.f;
                 if constexpr (W) wt = __shfl(myw, t);
+                int32_t key = -1;
+                if constexpr (MK) key = __shfl(myk, t);
                 if (ok[u]) {
                     float v[EPL];
                     widen<TX, EPL>(raw[u], v);
@@ -320,7 +332,7 @@ __device__ inline void wave_range(const SpmmParams& P, Acc<EPL, HS, HM>& acc, in
 #pragma unroll
                         for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt, v[k]);
                     }
-                    if constexpr (MK) keep_won<EPL>(v, bits[u]);
+                    if constexpr (MK) apply_mask<EPL>(v, mraw[u], key);
                     acc.add(u % A, v, (int32_t)(p0 + t));
                 }
             }
@@ -340,14 +352,17 @@ __device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int6
     const int L = P.L;
     for (int32_t it = 0; it < max_n; it += kUnroll) {
         const char* addr[kUnroll];
+        const int32_t* maddr[kUnroll];
         bool ok[kUnroll];
         float wt[kUnroll];
+        int32_t key[kUnroll];
         if constexpr (COOP) {
-            int32_t myc = 0;
+            int32_t myc = 0, myk = -1;
             float myw = 1.f;
             if (j < kUnroll && it + j < my_n) {
                 myc = __builtin_nontemporal_load(P.col + e0 + it + j);
                 if constexpr (W) myw = __builtin_nontemporal_load(P.w + e0 + it + j);
+                if constexpr (MK) myk = __builtin_nontemporal_load(P.ekey + e0 + it + j);
             }
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
@@ -355,8 +370,11 @@ __device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int6
                 const int32_t c = __shfl(myc, srcl);
                 wt[u] = 1.f;
                 if constexpr (W) wt[u] = __shfl(myw, srcl);
+                key[u] = -1;
+                if constexpr (MK) key[u] = __shfl(myk, srcl);
                 ok[u] = feat_ok && (it + u < my_n);
                 addr[u] = feat_addr<TX, NT>(P, c, fe);
+                if constexpr (MK) maddr[u] = P.mtab + (int64_t)c * P.F + fe;
             }
         } else {
             int32_t cc[kUnroll];
@@ -366,22 +384,23 @@ __device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int6
                 cc[u] = ok[u] ? P.col[e0 + it + u] : 0;
                 wt[u] = 1.f;
                 if constexpr (W) wt[u] = ok[u] ? P.w[e0 + it + u] : 1.f;
+                key[u] = -1;
+                if constexpr (MK) key[u] = ok[u] ? P.ekey[e0 + it + u] : -1;
             }
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) addr[u] = feat_addr<TX, NT>(P, cc[u], fe);
-        }
-        uint32_t bits[MK ? kUnroll : 1];
-        if constexpr (MK) {
-#pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
-                bits[u] = ok[u] ? win_bits<EPL>(P, e0 + it + u, fe) : 0u;
-                ok[u] = bits[u] != 0u;
+                addr[u] = feat_addr<TX, NT>(P, cc[u], fe);
+                if constexpr (MK) maddr[u] = P.mtab + (int64_t)cc[u] * P.F + fe;
             }
         }
         R raw[kUnroll];
+        int32_t mraw[MK ? kUnroll : 1][EPL];
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u)
-            if (ok[u]) raw[u] = *reinterpret_cast<const R*>(addr[u]);
+            if (ok[u]) {
+                raw[u] = *reinterpret_cast<const R*>(addr[u]);
+                if constexpr (MK) load_mask<EPL>(maddr[u], mraw[u]);
+            }
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
             if (ok[u]) {
@@ -391,7 +410,7 @@ __device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int6
 #pragma unroll
                     for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt[u], v[k]);
                 }
-                if constexpr (MK) keep_won<EPL>(v, bits[u]);
+                if constexpr (MK) apply_mask<EPL>(v, mraw[u], key[u]);
                 acc.add(u % A, v, (int32_t)(e0 + it + u));
             }
         }
@@ -536,21 +555,23 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
             }
         }
     };
-    auto cols = [&](int32_t beg, int32_t deg, int32_t& c, float& w) {
+    auto cols = [&](int32_t beg, int32_t deg, int32_t& c, float& w, int32_t& key) {
         c = 0;
         w = 1.f;
+        key = -1;
         if (j < deg) {
             c = __builtin_nontemporal_load(P.col + beg + j);
             if constexpr (W) w = __builtin_nontemporal_load(P.w + beg + j);
+            if constexpr (MK) key = __builtin_nontemporal_load(P.ekey + beg + j);
         }
     };
 
     int64_t it = tw;
     int32_t row, beg, deg, nrow, nbeg, ndeg;
-    int32_t cv;
+    int32_t cv, kv;
     float wv;
     rec(it, row, beg, deg);
-    cols(beg, deg, cv, wv);
+    cols(beg, deg, cv, wv, kv);
     rec(it + nw, nrow, nbeg, ndeg);
     for (; it < items; it += nw) {
         const int ft = (int)(it % P.FT);
@@ -558,32 +579,30 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
         const bool feat_ok = row >= 0 && chunk_j < P.ltot;
         const int64_t fe = chunk_j * EPL;
         R raw[kTinyDeg];
+        int32_t mraw[MK ? kTinyDeg : 1][EPL];
         bool ok[kTinyDeg];
-        uint32_t bits[MK ? kTinyDeg : 1];
-#pragma unroll
-        for (int u = 0; u < kTinyDeg; ++u) {
-            ok[u] = feat_ok && (u < deg);
-            if constexpr (MK) {
-                // only chunks holding a won feature are gathered
-                bits[u] = ok[u] ? win_bits<EPL>(P, (int64_t)beg + u, fe) : 0u;
-                ok[u] = bits[u] != 0u;
-            }
-        }
 #pragma unroll
         for (int u = 0; u < kTinyDeg; ++u) {
             const int32_t c = __shfl(cv, slot * L + u);
-            if (ok[u]) raw[u] = *reinterpret_cast<const R*>(feat_addr<TX, NT>(P, c, fe));
+            ok[u] = feat_ok && (u < deg);
+            if (ok[u]) {
+                raw[u] = *reinterpret_cast<const R*>(feat_addr<TX, NT>(P, c, fe));
+                if constexpr (MK) load_mask<EPL>(P.mtab + (int64_t)c * P.F + fe, mraw[u]);
+            }
         }
         float wt[kTinyDeg];
+        int32_t key[kTinyDeg];
 #pragma unroll
         for (int u = 0; u < kTinyDeg; ++u) {
             wt[u] = 1.f;
             if constexpr (W) wt[u] = __shfl(wv, slot * L + u);
+            key[u] = -1;
+            if constexpr (MK) key[u] = __shfl(kv, slot * L + u);
         }
         // next group's columns, and the row ranges of the group after it
-        int32_t ncv;
+        int32_t ncv, nkv;
         float nwv;
-        cols(nbeg, ndeg, ncv, nwv);
+        cols(nbeg, ndeg, ncv, nwv, nkv);
         int32_t row2, beg2, deg2;
         rec(it + 2 * nw, row2, beg2, deg2);
 
@@ -598,7 +617,7 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
 #pragma unroll
                     for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt[u], v[k]);
                 }
-                if constexpr (MK) keep_won<EPL>(v, bits[u]);
+                if constexpr (MK) apply_mask<EPL>(v, mraw[u], key[u]);
                 acc.add(0, v, beg + u);
             }
         }
@@ -608,6 +627,7 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
         deg = ndeg;
         cv = ncv;
         wv = nwv;
+        kv = nkv;
         nrow = row2;
         nbeg = beg2;
         ndeg = deg2;
@@ -729,7 +749,7 @@ template <typename TX, int EPL, bool W>
 hipError_t launch_w(const SpmmParams& p, unsigned grid, hipStream_t s) {
     const bool hs = (p.reduce & (kSum | kMean)) != 0;
     const bool hm = (p.reduce & kMax) != 0;
-    if (p.mbits)  // masked sum: the gradient of max
+    if (p.mtab)  // masked sum: the gradient of max
         hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 1, W, true>), dim3(grid), dim3(kBlock), 0, s, p);
     else if (hs && hm)
         hipLaunchKernelGGL((spmm_main<TX, EPL, true, true, 1, W, false>), dim3(grid), dim3(kBlock), 0, s, p);
@@ -811,7 +831,7 @@ hipError_t launch_tiny_typed(const SpmmParams& p, unsigned grid, hipStream_t s) 
             hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, 4, false>), dim3(grid), dim3(kBlock), 0, s, p);
         else
             hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, MP_MAX_TYPES, false>), dim3(grid), dim3(kBlock), 0, s, p);
-    } else if (p.mbits) {
+    } else if (p.mtab) {
         // masked sum: the gradient of max
         if (w) hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, true, 1, true>), dim3(grid), dim3(kBlock), 0, s, p);
         else hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, 1, true>), dim3(grid), dim3(kBlock), 0, s, p);
