@@ -312,19 +312,33 @@ __device__ inline void wave_range(const SpmmParams& P, Acc<EPL, HS, HM>& acc, in
             }
             R raw[kUnroll];
             int32_t mraw[MK ? kUnroll : 1][EPL];
+            int32_t keys[MK ? kUnroll : 1];
+            if constexpr (MK) {
+                // masked sum: load the argmax chunks first and gather a
+                // feature chunk only if one of its features names this edge
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u) {
+                    keys[u] = __shfl(myk, base + u * S + slot);
+                    if (ok[u]) load_mask<EPL>(maddr[u], mraw[u]);
+                }
+#pragma unroll
+                for (int u = 0; u < kUnroll; ++u) {
+                    bool hit = false;
+#pragma unroll
+                    for (int k = 0; k < EPL; ++k) hit |= mraw[u][k] == keys[u];
+                    ok[u] = ok[u] && hit;
+                }
+            }
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u)
-                if (ok[u]) {
-                    raw[u] = *reinterpret_cast<const R*>(addr[u]);
-                    if constexpr (MK) load_mask<EPL>(maddr[u], mraw[u]);
-                }
+                if (ok[u]) raw[u] = *reinterpret_cast<const R*>(addr[u]);
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
                 const int t = base + u * S + slot;
                 float wt = 1.f;
                 if constexpr (W) wt = __shfl(myw, t);
                 int32_t key = -1;
-                if constexpr (MK) key = __shfl(myk, t);
+                if constexpr (MK) key = keys[u];
                 if (ok[u]) {
                     float v[EPL];
                     widen<TX, EPL>(raw[u], v);
@@ -395,12 +409,22 @@ __device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int6
         }
         R raw[kUnroll];
         int32_t mraw[MK ? kUnroll : 1][EPL];
+        if constexpr (MK) {
+            // masked sum: argmax chunks first, then only the chunks that hit
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u)
+                if (ok[u]) load_mask<EPL>(maddr[u], mraw[u]);
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                bool hit = false;
+#pragma unroll
+                for (int k = 0; k < EPL; ++k) hit |= mraw[u][k] == key[u];
+                ok[u] = ok[u] && hit;
+            }
+        }
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u)
-            if (ok[u]) {
-                raw[u] = *reinterpret_cast<const R*>(addr[u]);
-                if constexpr (MK) load_mask<EPL>(maddr[u], mraw[u]);
-            }
+            if (ok[u]) raw[u] = *reinterpret_cast<const R*>(addr[u]);
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
             if (ok[u]) {
@@ -581,23 +605,36 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
         R raw[kTinyDeg];
         int32_t mraw[MK ? kTinyDeg : 1][EPL];
         bool ok[kTinyDeg];
+        int32_t cc[kTinyDeg];
+        int32_t key[kTinyDeg];
 #pragma unroll
         for (int u = 0; u < kTinyDeg; ++u) {
-            const int32_t c = __shfl(cv, slot * L + u);
+            cc[u] = __shfl(cv, slot * L + u);
             ok[u] = feat_ok && (u < deg);
-            if (ok[u]) {
-                raw[u] = *reinterpret_cast<const R*>(feat_addr<TX, NT>(P, c, fe));
-                if constexpr (MK) load_mask<EPL>(P.mtab + (int64_t)c * P.F + fe, mraw[u]);
+            key[u] = -1;
+            if constexpr (MK) {
+                key[u] = __shfl(kv, slot * L + u);
+                if (ok[u]) load_mask<EPL>(P.mtab + (int64_t)cc[u] * P.F + fe, mraw[u]);
             }
         }
+        if constexpr (MK) {
+            // gather a chunk only if one of its features names this edge
+#pragma unroll
+            for (int u = 0; u < kTinyDeg; ++u) {
+                bool hit = false;
+#pragma unroll
+                for (int k = 0; k < EPL; ++k) hit |= mraw[u][k] == key[u];
+                ok[u] = ok[u] && hit;
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kTinyDeg; ++u)
+            if (ok[u]) raw[u] = *reinterpret_cast<const R*>(feat_addr<TX, NT>(P, cc[u], fe));
         float wt[kTinyDeg];
-        int32_t key[kTinyDeg];
 #pragma unroll
         for (int u = 0; u < kTinyDeg; ++u) {
             wt[u] = 1.f;
             if constexpr (W) wt[u] = __shfl(wv, slot * L + u);
-            key[u] = -1;
-            if constexpr (MK) key[u] = __shfl(kv, slot * L + u);
         }
         // next group's columns, and the row ranges of the group after it
         int32_t ncv, nkv;
