@@ -68,14 +68,16 @@ def transpose_bytes(N_dst, N_src, E):
 
 
 def grad_x_bytes(N_dst, N_src, E, F, mode):
-    """Transposed gather of the output gradient (plus the argmax table for
-    max, plus the scaled copy for mean), one output row per source."""
-    b = 4 * (N_src + 1) + 4 * E + E * F * 4 + N_src * F * 4
+    """Transposed gather of the output gradient, one output row per source.
+    Mean adds the scaled copy of the gradient.  Max gathers the argmax chunk
+    of every edge and feature (and the edge's forward position), but only the
+    routed gradient elements, one per destination row and feature."""
+    b = 4 * (N_src + 1) + 4 * E + N_src * F * 4
     if mode == "mean":
         b += 4 * (N_dst + 1) + 2 * N_dst * F * 4
     if mode == "max":
-        b += 4 * E + E * F * 4
-    return b
+        return b + 4 * E + E * F * 4 + N_dst * F * 4
+    return b + E * F * 4
 
 
 def grad_w_bytes(N_dst, E, F):
