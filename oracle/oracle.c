@@ -31,6 +31,13 @@
  * -1); max keeps the first edge (lowest CSR position) among equal values,
  * comparing with '>' so that -0.0 and +0.0 tie; mean is sum / in-degree.
  *
+ * More aggregators (Sec. 2.2 "Aggregations as a First-Class Principle":
+ * besides sum, mean and max, advanced ones such as variance and standard
+ * deviation, stacked together, in message passing and in global readouts):
+ * min (with the first edge attaining it), the population variance of a row's
+ * messages, sum of (m - mean)^2 / deg, and its square root.  A global readout
+ * is the same aggregation over contiguous segments of nodes (col = identity).
+ *
  * Backward (Sec. 2.2: the backward pass of an aggregation runs over the
  * transposed adjacency, which is why CSR and CSC are both cached): the
  * derivatives of the aggregation above with respect to the features x and the
@@ -503,6 +510,71 @@ int oracle_spmm_backward_w(int64_t n_rows, const int64_t* rows, int64_t N_dst, i
             }
             gw[p] = s;
             if (scale) scale[p] = a;
+        }
+    }
+    return bad ? -1 : 0;
+}
+
+/* ---- more aggregators ---------------------------------------------------- */
+
+/* For each listed row (rows == NULL: rows 0..n_rows-1), each feature f, over
+ * the row's messages m_p (as in oracle_spmm):
+ *   out_min[k,f], argmin[k,f]: the first p with the smallest m_p ('<' scan;
+ *                 0.0 and -1 for an empty row)
+ *   out_var[k,f]: sum_p (m_p - mean)^2 / deg, mean = sum_p m_p / deg, both
+ *                 in fp64 (two passes; 0 for an empty row)
+ *   out_std[k,f]: sqrt(out_var[k,f])
+ *   var_scale[k,f]: sum_p m_p^2 / deg + (sum_p |m_p| / deg)^2, the size of
+ *                 the terms a one-pass fp32 evaluation of the variance
+ *                 subtracts (error scale)
+ * Any output may be NULL.  Returns 0, or -1 for a bad row or column. */
+int oracle_spmm_multi(int64_t n_rows, const int64_t* rows, int64_t N_dst, int64_t N_src,
+                      const int64_t* rowptr, const int32_t* col, const float* w, const void* x,
+                      int x_is_bf16, int64_t F, float* out_min, int64_t* argmin,
+                      double* out_var, double* out_std, double* var_scale, int nthreads) {
+    int bad = 0;
+#pragma omp parallel for schedule(static) num_threads(nthreads > 0 ? nthreads : 1) reduction(| : bad)
+    for (int64_t k = 0; k < n_rows; ++k) {
+        int64_t i = rows ? rows[k] : k;
+        if (i < 0 || i >= N_dst) {
+            bad = 1;
+            continue;
+        }
+        int64_t p0 = rowptr[i], p1 = rowptr[i + 1];
+        for (int64_t p = p0; p < p1; ++p)
+            if (col[p] < 0 || col[p] >= N_src) bad = 1;
+        if (bad) continue;
+        int64_t deg = p1 - p0;
+        for (int64_t f = 0; f < F; ++f) {
+            float least = 0.0f;
+            int64_t arg = -1;
+            double s = 0.0, a = 0.0, q = 0.0;
+            for (int64_t p = p0; p < p1; ++p) {
+                float m = message(x, x_is_bf16, F, col[p], f, w, p);
+                if (arg < 0 || m < least) {
+                    least = m;
+                    arg = p;
+                }
+                s += (double)m;
+                a += fabs((double)m);
+                q += (double)m * (double)m;
+            }
+            double var = 0.0;
+            if (deg > 0) {
+                double mean = s / (double)deg;
+                for (int64_t p = p0; p < p1; ++p) {
+                    double d = (double)message(x, x_is_bf16, F, col[p], f, w, p) - mean;
+                    var += d * d;
+                }
+                var /= (double)deg;
+            }
+            if (out_min) out_min[k * F + f] = arg < 0 ? 0.0f : least;
+            if (argmin) argmin[k * F + f] = arg;
+            if (out_var) out_var[k * F + f] = var;
+            if (out_std) out_std[k * F + f] = sqrt(var);
+            if (var_scale)
+                var_scale[k * F + f] =
+                    deg > 0 ? q / (double)deg + (a / (double)deg) * (a / (double)deg) : 0.0;
         }
     }
     return bad ? -1 : 0;
