@@ -71,9 +71,17 @@ typedef enum mp_dtype { MP_F32 = 0, MP_BF16 = 1 } mp_dtype;
 /* rowptr element types. */
 typedef enum mp_itype { MP_I32 = 0, MP_I64 = 1 } mp_itype;
 
-/* Reductions, a bit mask.  Allowed values: MP_SUM, MP_MEAN, MP_MAX,
- * MP_SUM|MP_MAX and MP_MEAN|MP_MAX (the fused pass: one gather feeds both). */
-typedef enum mp_reduce { MP_SUM = 1, MP_MEAN = 2, MP_MAX = 4 } mp_reduce;
+/* Reductions, a bit mask.  mp_spmm allows MP_SUM, MP_MEAN, MP_MAX,
+ * MP_SUM|MP_MAX and MP_MEAN|MP_MAX (the fused pass: one gather feeds both);
+ * MP_MIN, MP_VAR and MP_STD are for mp_spmm_multi / mp_readout_multi. */
+typedef enum mp_reduce {
+    MP_SUM = 1,
+    MP_MEAN = 2,
+    MP_MAX = 4,
+    MP_MIN = 8,
+    MP_VAR = 16,
+    MP_STD = 32
+} mp_reduce;
 
 /* Library version (MP_VERSION). */
 int mp_version(void);
@@ -181,6 +189,52 @@ int mp_spmm(const mp_plan* plan, const void* rowptr, int rowptr_itype, const int
             const float* w, const void* x, int x_dtype, int64_t N_src, int64_t N_dst,
             int64_t F, int reduce, void* out, int out_dtype, void* out_max, int max_dtype,
             int32_t* argout, void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Stacked aggregations (Sec. 2.2, "Aggregations as a First-Class Principle":
+ * simple aggregators (sum, mean, max), advanced ones (variance, standard
+ * deviation) and stacks of several, for message passing and for global
+ * readouts).  One gather of each edge's message feeds every requested output.
+ * Definitions over the messages m_p of a row (deg = row length):
+ *   MP_SUM  sum m_p;  MP_MEAN  sum / deg;
+ *   MP_MAX / MP_MIN  the largest / smallest m_p and, in arg, the CSR position
+ *           of the first edge attaining it ('>' / '<' comparisons, so -0.0
+ *           and +0.0 tie and the earlier edge wins);
+ *   MP_VAR  population variance, sum m_p^2 / deg - mean^2 (fp32, clamped at
+ *           0);  MP_STD  its square root.
+ * An empty row gives 0 everywhere and -1 in arg.  All sums accumulate in
+ * fp32 in an order fixed by the plan; outputs are fp32.
+ * ------------------------------------------------------------------------- */
+
+/* One output of a stacked aggregation. */
+typedef struct mp_aggr_out {
+    int aggr;     /* exactly one of MP_SUM .. MP_STD; each at most once per call */
+    float* out;   /* [N_dst, F] fp32, device */
+    int32_t* arg; /* [N_dst, F] int32, device: required for MP_MAX and MP_MIN,
+                     ignored otherwise */
+} mp_aggr_out;
+
+/* Workspace bytes for mp_spmm_multi / mp_readout_multi with this plan (hub
+ * partials of every statistic); 0 for a NULL plan. */
+int mp_spmm_multi_workspace(const mp_plan* plan, size_t* bytes);
+
+/* Stacked aggregation over the destination-major CSR: arguments as in
+ * mp_spmm (x fp32 or bf16, optional CSR-order weights w, plan optional), plus
+ * n_out (1..6) outputs described by the host array outs.  Duplicate or
+ * unknown aggregators give MP_ERR_REDUCE.  Asynchronous on `stream`. */
+int mp_spmm_multi(const mp_plan* plan, const void* rowptr, int rowptr_itype, const int32_t* col,
+                  const float* w, const void* x, int x_dtype, int64_t N_src, int64_t N_dst,
+                  int64_t F, int n_out, const mp_aggr_out* outs, void* ws, size_t ws_bytes,
+                  void* stream);
+
+/* Global readout: the same stacked aggregation over segments of consecutive
+ * node rows, given by ptr [N_seg+1] (the CSR of a sorted batch vector, e.g.
+ * from mp_sorted_coo_to_csr of (node id, batch)); ptr[N_seg] must equal
+ * N_nodes.  x is [N_nodes, F]; arg holds node indices.  plan (optional) is
+ * built on ptr with N_seg rows and E = N_nodes. */
+int mp_readout_multi(const mp_plan* plan, const void* ptr, int ptr_itype, const void* x,
+                     int x_dtype, int64_t N_nodes, int64_t N_seg, int64_t F, int n_out,
+                     const mp_aggr_out* outs, void* ws, size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
  * Backward pass (Sec. 2.2: the backward pass of an aggregation over A runs

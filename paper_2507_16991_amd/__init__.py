@@ -25,7 +25,9 @@ __all__ = [
     "mp_sorted_coo_to_csr", "mp_validate_sorted", "sorted_coo_to_csr",
     "mp_csr_transpose_workspace", "mp_csr_transpose", "mp_spmm_backward_x_workspace",
     "mp_spmm_backward_x", "mp_spmm_backward_w_workspace", "mp_spmm_backward_w",
-    "csr_transpose", "spmm_backward_x", "spmm_backward_w",
+    "csr_transpose", "spmm_backward_x", "spmm_backward_w", "MP_MIN", "MP_VAR", "MP_STD", "AGGR",
+    "mp_aggr_out", "mp_spmm_multi_workspace", "mp_spmm_multi", "mp_readout_multi", "spmm_multi",
+    "readout",
     "mp_spmm_plan_size", "mp_spmm_plan_build", "mp_spmm_plan_free", "mp_spmm_workspace",
     "mp_spmm", "mp_hetero_build_workspace", "mp_hetero_build", "mp_hetero_spmm",
     "mp_validate_coo", "mp_validate_csr", "coo_to_csr", "Plan", "spmm", "hetero_build",
@@ -40,6 +42,9 @@ MP_OK = 0
 MP_F32, MP_BF16 = 0, 1
 MP_I32, MP_I64 = 0, 1
 MP_SUM, MP_MEAN, MP_MAX = 1, 2, 4
+MP_MIN, MP_VAR, MP_STD = 8, 16, 32
+AGGR = {"sum": MP_SUM, "mean": MP_MEAN, "max": MP_MAX, "min": MP_MIN, "var": MP_VAR,
+        "std": MP_STD}
 MP_MAX_TYPES = 16
 
 _lib = None
@@ -54,6 +59,10 @@ class MPError(RuntimeError):
 class mp_relation(ctypes.Structure):
     _fields_ = [("src_type", ctypes.c_int32), ("dst_type", ctypes.c_int32),
                 ("src", ctypes.c_void_p), ("dst", ctypes.c_void_p), ("E", ctypes.c_int64)]
+
+
+class mp_aggr_out(ctypes.Structure):
+    _fields_ = [("aggr", ctypes.c_int), ("out", ctypes.c_void_p), ("arg", ctypes.c_void_p)]
 
 
 def lib():
@@ -87,6 +96,9 @@ def lib():
         L.mp_validate_coo.argtypes = [p, p, i64, i64, i64, p, p]
         L.mp_validate_csr.argtypes = [p, i32, p, i64, i64, i64, p, p]
         L.mp_validate_sorted.argtypes = [p, i64, p, p]
+        L.mp_spmm_multi_workspace.argtypes = [p, psz]
+        L.mp_spmm_multi.argtypes = [p, p, i32, p, p, p, i32, i64, i64, i64, i32, p, p, sz, p]
+        L.mp_readout_multi.argtypes = [p, p, i32, p, i32, i64, i64, i64, i32, p, p, sz, p]
         L.mp_csr_transpose_workspace.argtypes = [i64, i64, i32, i32, psz]
         L.mp_csr_transpose.argtypes = [p, i32, p, i64, i64, i64, p, i32, p, p, p, p, p, sz, p]
         L.mp_spmm_backward_x_workspace.argtypes = [p, i64, i64, i32, psz]
@@ -97,6 +109,7 @@ def lib():
                                          p, sz, p]
         for name in ("mp_coo_to_csr_workspace", "mp_coo_to_csr", "mp_sorted_coo_to_csr",
                      "mp_validate_sorted", "mp_csr_transpose_workspace", "mp_csr_transpose",
+                     "mp_spmm_multi_workspace", "mp_spmm_multi", "mp_readout_multi",
                      "mp_spmm_backward_x_workspace", "mp_spmm_backward_x",
                      "mp_spmm_backward_w_workspace", "mp_spmm_backward_w", "mp_spmm_plan_size",
                      "mp_spmm_plan_build", "mp_spmm_workspace", "mp_spmm",
@@ -295,6 +308,34 @@ def mp_spmm_backward_w(rowptr, rowptr_itype, col, x, x_dtype, grad_out, g_dtype,
         _stream(stream)))
 
 
+def mp_spmm_multi_workspace(plan_handle) -> int:
+    return _bytes("mp_spmm_multi_workspace", plan_handle)
+
+
+def _aggr_array(outs):
+    """outs: list of (aggr code, out tensor, arg tensor or None)."""
+    arr = (mp_aggr_out * len(outs))()
+    for k, (a, o, g) in enumerate(outs):
+        arr[k].aggr, arr[k].out, arr[k].arg = a, _ptr(o), _ptr(g)
+    return arr
+
+
+def mp_spmm_multi(plan_handle, rowptr, rowptr_itype, col, w, x, x_dtype, N_src, N_dst, F, outs,
+                  ws, ws_bytes, stream=None):
+    arr = _aggr_array(outs)
+    _check("mp_spmm_multi", lib().mp_spmm_multi(
+        plan_handle, _ptr(rowptr), rowptr_itype, _ptr(col), _ptr(w), _ptr(x), x_dtype, N_src,
+        N_dst, F, len(outs), arr, _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def mp_readout_multi(plan_handle, ptr, ptr_itype, x, x_dtype, N_nodes, N_seg, F, outs, ws,
+                     ws_bytes, stream=None):
+    arr = _aggr_array(outs)
+    _check("mp_readout_multi", lib().mp_readout_multi(
+        plan_handle, _ptr(ptr), ptr_itype, _ptr(x), x_dtype, N_nodes, N_seg, F, len(outs), arr,
+        _ptr(ws), ws_bytes, _stream(stream)))
+
+
 def mp_validate_sorted(dst, E, d_count, stream=None):
     _check("mp_validate_sorted", lib().mp_validate_sorted(_ptr(dst), E, _ptr(d_count),
                                                           _stream(stream)))
@@ -460,6 +501,47 @@ def spmm_backward_w(rowptr, col, x, grad_out, reduce, *, argout=None, out=None, 
                        _dtype_code(grad_out.dtype), argout, N_src, N_dst, E, F, reduce, out, ws,
                        0 if ws is None else ws.numel(), stream)
     return out
+
+
+def _multi_outputs(names, N, F, dev):
+    res, outs = {}, []
+    for n in names:
+        o = torch.empty(N, F, dtype=torch.float32, device=dev)
+        g = torch.empty(N, F, dtype=torch.int32, device=dev) if n in ("max", "min") else None
+        res[n] = o
+        if g is not None:
+            res["arg" + n] = g
+        outs.append((AGGR[n], o, g))
+    return res, outs
+
+
+def spmm_multi(rowptr, col, x, aggrs, *, w=None, plan: Plan | None = None, stream=None):
+    """Several aggregations from one gather.  aggrs: names among sum, mean,
+    max, min, var, std.  Returns {name: [N_dst, F] fp32, 'argmax'/'argmin':
+    int32 positions}."""
+    N_dst = int(rowptr.numel()) - 1
+    N_src, F = int(x.shape[0]), int(x.shape[1])
+    res, outs = _multi_outputs(aggrs, N_dst, F, x.device)
+    h = plan.handle if plan is not None else None
+    nb = mp_spmm_multi_workspace(h)
+    ws = _workspace(nb, x.device) if nb else None
+    mp_spmm_multi(h, rowptr, _itype_code(rowptr.dtype), col, w, x, _dtype_code(x.dtype), N_src,
+                  N_dst, F, outs, ws, 0 if ws is None else ws.numel(), stream)
+    return res
+
+
+def readout(ptr, x, aggrs, *, plan: Plan | None = None, stream=None):
+    """Global readout over segments of consecutive rows of x (ptr: [S+1], the
+    CSR of a sorted batch vector).  Same outputs as spmm_multi, arg = row."""
+    N_seg = int(ptr.numel()) - 1
+    N_nodes, F = int(x.shape[0]), int(x.shape[1])
+    res, outs = _multi_outputs(aggrs, N_seg, F, x.device)
+    h = plan.handle if plan is not None else None
+    nb = mp_spmm_multi_workspace(h)
+    ws = _workspace(nb, x.device) if nb else None
+    mp_readout_multi(h, ptr, _itype_code(ptr.dtype), x, _dtype_code(x.dtype), N_nodes, N_seg, F,
+                     outs, ws, 0 if ws is None else ws.numel(), stream)
+    return res
 
 
 def hetero_build(N_per_type, rels, dst_type, *, rowptr_dtype=torch.int32, stream=None):

@@ -178,8 +178,9 @@ int run_spmm(const mp_plan* plan, SpmmParams& P, const Geometry& g, int x_dtype,
     P.S = g.S;
     P.FT = g.FT;
     P.ltot = g.ltot;
-    const bool hs = (P.reduce & (MP_SUM | MP_MEAN)) != 0;
-    const bool hm = (P.reduce & MP_MAX) != 0;
+    const bool hx = P.stats != 0;
+    const bool hs = hx || (P.reduce & (MP_SUM | MP_MEAN)) != 0;
+    const bool hm = hx || (P.reduce & MP_MAX) != 0;
     const bool tiny = plan && plan->n_tiny > 0 && g.L > kTinyDeg;
     if (plan) {
         P.rowlist = plan->rowlist;
@@ -203,7 +204,10 @@ int run_spmm(const mp_plan* plan, SpmmParams& P, const Geometry& g, int x_dtype,
             P.part_sum = hs ? c.take<float>(cells) : nullptr;
             P.part_max = hm ? c.take<float>(cells) : nullptr;
             P.part_arg = hm ? c.take<int32_t>(cells) : nullptr;
-            if (ws_bytes < c.off) return MP_ERR_WORKSPACE;
+            P.part_sq = hx ? c.take<float>(cells) : nullptr;
+            P.part_min = hx ? c.take<float>(cells) : nullptr;
+            P.part_amin = hx ? c.take<int32_t>(cells) : nullptr;
+            if (ws_bytes < c.off || !ws) return MP_ERR_WORKSPACE;
         }
     } else {
         P.rowlist = nullptr;
@@ -230,6 +234,69 @@ int check_plan(const mp_plan* plan, const void* rowptr, int itype, int64_t N_dst
     if (plan->rowptr != rowptr || plan->itype != itype || plan->N_dst != N_dst || plan->F != F)
         return MP_ERR_PLAN;
     return MP_OK;
+}
+
+// ---- stacked aggregations ---------------------------------------------------------
+
+constexpr int kAllAggr = MP_SUM | MP_MEAN | MP_MAX | MP_MIN | MP_VAR | MP_STD;
+
+// Check the output list and fill the stats-mode outputs of P.
+int fill_multi_outputs(int n_out, const mp_aggr_out* outs, int64_t rows, SpmmParams& P) {
+    if (n_out < 1 || n_out > 6) return MP_ERR_SIZE;
+    if (!outs) return MP_ERR_NULL;
+    int seen = 0;
+    uintptr_t all = 0;
+    for (int k = 0; k < n_out; ++k) {
+        const mp_aggr_out& o = outs[k];
+        const int a = o.aggr;
+        if ((a & kAllAggr) != a || a == 0 || (a & (a - 1)) != 0 || (seen & a)) return MP_ERR_REDUCE;
+        seen |= a;
+        const bool has_arg = a == MP_MAX || a == MP_MIN;
+        if (rows > 0 && (!o.out || (has_arg && !o.arg))) return MP_ERR_NULL;
+        if ((uintptr_t)o.out % 4 || (uintptr_t)o.arg % 4) return MP_ERR_ALIGN;
+        all |= (uintptr_t)o.out | (has_arg ? (uintptr_t)o.arg : 0);
+        switch (a) {
+            case MP_SUM: P.o_sum = o.out; break;
+            case MP_MEAN: P.o_mean = o.out; break;
+            case MP_MAX: P.o_max = o.out; P.o_amax = o.arg; break;
+            case MP_MIN: P.o_min = o.out; P.o_amin = o.arg; break;
+            case MP_VAR: P.o_var = o.out; break;
+            default: P.o_std = o.out; break;
+        }
+    }
+    P.stats = 1;
+    P.reduce = MP_SUM | MP_MAX;
+    P.vec_store = (all % 16) == 0;
+    return MP_OK;
+}
+
+int multi_impl(const mp_plan* plan, const void* rowptr, int rowptr_itype, const int32_t* col,
+               const float* w, const void* x, int x_dtype, int64_t N_src, int64_t N_dst, int64_t F,
+               int n_out, const mp_aggr_out* outs, void* ws, size_t ws_bytes, hipStream_t s) {
+    if (!valid_itype(rowptr_itype) || !valid_dtype(x_dtype)) return MP_ERR_DTYPE;
+    if (N_src < 0 || N_src > INT32_MAX || N_dst < 0 || N_dst > INT32_MAX || F < 1 || F > 65536)
+        return MP_ERR_SIZE;
+    if (!rowptr) return MP_ERR_NULL;
+    if (N_dst > 0 && !x) return MP_ERR_NULL;
+    SpmmParams P{};
+    int st = fill_multi_outputs(n_out, outs, N_dst, P);
+    if (st != MP_OK) return st;
+    st = check_plan(plan, rowptr, rowptr_itype, N_dst, F);
+    if (st != MP_OK) return st;
+    const int eb = x_dtype == MP_BF16 ? 2 : 4;
+    if ((uintptr_t)x % eb || (uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4) ||
+        (uintptr_t)col % 4 || (uintptr_t)w % 4)
+        return MP_ERR_ALIGN;
+    if (N_dst == 0) return MP_OK;
+    Geometry g = make_geometry(F, x_dtype, (uintptr_t)x);
+    P.rowptr = rowptr;
+    P.rp64 = rowptr_itype == MP_I64;
+    P.col = col;
+    P.w = w;
+    P.n_tables = 1;
+    P.table_ptr[0] = static_cast<const char*>(x);
+    P.F = F;
+    return run_spmm(plan, P, g, x_dtype, N_dst, ws, ws_bytes, s);
 }
 
 }  // namespace
@@ -402,6 +469,35 @@ int mp_spmm_workspace(const mp_plan* plan, int reduce, size_t* bytes) {
     if (reduce & MP_MAX) b += 2 * align_up(cells * 4, 256);
     *bytes = b;
     return MP_OK;
+}
+
+int mp_spmm_multi_workspace(const mp_plan* plan, size_t* bytes) {
+    if (!bytes) return MP_ERR_NULL;
+    if (!plan || plan->n_chunks == 0) {
+        *bytes = 0;
+        return MP_OK;
+    }
+    // hub partials: sum, sum of squares, max and min values, their positions
+    *bytes = 6 * align_up((size_t)plan->n_chunks * (size_t)plan->F * 4, 256);
+    return MP_OK;
+}
+
+int mp_spmm_multi(const mp_plan* plan, const void* rowptr, int rowptr_itype, const int32_t* col,
+                  const float* w, const void* x, int x_dtype, int64_t N_src, int64_t N_dst,
+                  int64_t F, int n_out, const mp_aggr_out* outs, void* ws, size_t ws_bytes,
+                  void* stream) {
+    if (N_dst > 0 && !col) return MP_ERR_NULL;
+    return multi_impl(plan, rowptr, rowptr_itype, col, w, x, x_dtype, N_src, N_dst, F, n_out, outs,
+                      ws, ws_bytes, as_stream(stream));
+}
+
+int mp_readout_multi(const mp_plan* plan, const void* ptr, int ptr_itype, const void* x,
+                     int x_dtype, int64_t N_nodes, int64_t N_seg, int64_t F, int n_out,
+                     const mp_aggr_out* outs, void* ws, size_t ws_bytes, void* stream) {
+    // segments of consecutive node rows: the CSR of the sorted batch vector,
+    // whose column of position p is p itself
+    return multi_impl(plan, ptr, ptr_itype, nullptr, nullptr, x, x_dtype, N_nodes, N_seg, F, n_out,
+                      outs, ws, ws_bytes, as_stream(stream));
 }
 
 int mp_spmm(const mp_plan* plan, const void* rowptr, int rowptr_itype, const int32_t* col,

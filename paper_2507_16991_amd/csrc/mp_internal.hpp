@@ -123,7 +123,7 @@ constexpr int kTinyClassEnd = 4;        // classes 0..3 (bit length <= 3) are ti
 struct SpmmParams {
     const void* rowptr;
     int rp64;
-    const int32_t* col;
+    const int32_t* col;  // nullptr: col[p] = p (a readout over contiguous segments)
     const float* w;
     int n_tables;
     const char* table_ptr[MP_MAX_TYPES];
@@ -154,9 +154,23 @@ struct SpmmParams {
     // mtab[c_t * F + f] == ekey[t]; both nullptr otherwise
     const int32_t* ekey;
     const int32_t* mtab;
+    // stats mode (stacked statistics from one gather): each non-null output
+    // [N_dst, F] fp32 (arguments int32) is written
+    int stats;
+    float* o_sum;
+    float* o_mean;
+    float* o_max;
+    int32_t* o_amax;
+    float* o_min;
+    int32_t* o_amin;
+    float* o_var;
+    float* o_std;
     float* part_sum;
     float* part_max;
     int32_t* part_arg;
+    float* part_sq;
+    float* part_min;
+    int32_t* part_amin;
 };
 
 // ---- backward (backward.hip) -----------------------------------------------

@@ -30,6 +30,14 @@ constexpr int kBlock = 256;
 constexpr int kWavesPerBlock = kBlock / kWave;
 constexpr int kUnroll = 8;  // edges gathered per slot per iteration
 
+// Kernel modes: the plain aggregation (sum/mean and/or max); the masked sum
+// (the gradient of max); and the stacked statistics (sum, sum of squares, max
+// and min with their positions, from one gather: sum, mean, max, min,
+// variance and standard deviation).
+constexpr int kModePlain = 0;
+constexpr int kModeMasked = 1;
+constexpr int kModeStats = 2;
+
 // ---- feature loads ----------------------------------------------------------
 
 template <typename TX, int EPL>
@@ -126,14 +134,27 @@ __device__ inline void max_merge(float& va, int32_t& ia, float vb, int32_t ib) {
     ia = take ? ib : ia;
 }
 
+// Keep the pair with the smaller value; on equal values the smaller position.
+__device__ inline void min_merge(float& va, int32_t& ia, float vb, int32_t ib) {
+    const bool take = (ib >= 0) && (ia < 0 || vb < va || (vb == va && ib < ia));
+    va = take ? vb : va;
+    ia = take ? ib : ia;
+}
+
 // ---- accumulator state -------------------------------------------------------
 
-template <int EPL, bool HS, bool HM, int NA = (HM ? 2 : 4)>
+// HX (stats mode, which also sets HS and HM): the sum of squares and the
+// (min, position) pair are kept as well.
+template <int EPL, bool HS, bool HM, bool HX = false, int NA = ((HM || HX) ? 2 : 4)>
 struct Acc {
     static constexpr int A = NA;  // independent partial accumulators
+    static constexpr int AX = HX ? NA : 1;
     float s[A][EPL];
     float m[A][EPL];
     int32_t i[A][EPL];
+    float q[AX][EPL];
+    float n[AX][EPL];
+    int32_t j[AX][EPL];
 
     __device__ inline void init() {
 #pragma unroll
@@ -143,6 +164,11 @@ struct Acc {
                 if constexpr (HS) s[a][k] = 0.f;
                 // -inf: the first (finite) message always replaces it
                 if constexpr (HM) { m[a][k] = -__builtin_huge_valf(); i[a][k] = -1; }
+                if constexpr (HX) {
+                    q[a][k] = 0.f;
+                    n[a][k] = __builtin_huge_valf();
+                    j[a][k] = -1;
+                }
             }
     }
     // message values v (already weighted) of CSR position pos
@@ -154,6 +180,12 @@ struct Acc {
                 const bool take = v[k] > m[a][k];
                 m[a][k] = take ? v[k] : m[a][k];
                 i[a][k] = take ? pos : i[a][k];
+            }
+            if constexpr (HX) {
+                q[a][k] = __builtin_fmaf(v[k], v[k], q[a][k]);
+                const bool take = v[k] < n[a][k];
+                n[a][k] = take ? v[k] : n[a][k];
+                j[a][k] = take ? pos : j[a][k];
             }
         }
     }
@@ -167,6 +199,10 @@ struct Acc {
                 for (int k = 0; k < EPL; ++k) {
                     if constexpr (HS) s[a][k] += s[a + step][k];
                     if constexpr (HM) max_merge(m[a][k], i[a][k], m[a + step][k], i[a + step][k]);
+                    if constexpr (HX) {
+                        q[a][k] += q[a + step][k];
+                        min_merge(n[a][k], j[a][k], n[a + step][k], j[a + step][k]);
+                    }
                 }
     }
     // fixed tree across the S slots of the wavefront (slot s at lanes s*L..);
@@ -185,6 +221,15 @@ struct Acc {
                     const float om = __shfl(m[0][k], src);
                     const int32_t oi = __shfl(i[0][k], src);
                     if (use) max_merge(m[0][k], i[0][k], om, oi);
+                }
+                if constexpr (HX) {
+                    const float oq = __shfl(q[0][k], src);
+                    const float on = __shfl(n[0][k], src);
+                    const int32_t oj = __shfl(j[0][k], src);
+                    if (use) {
+                        q[0][k] += oq;
+                        min_merge(n[0][k], j[0][k], on, oj);
+                    }
                 }
             }
         }
@@ -273,16 +318,51 @@ __device__ inline void store_row(const SpmmParams& P, int64_t row, int64_t fe, i
     }
 }
 
+// Stats mode: write every requested statistic of a finished row (fp32).
+// Variance is the population variance E[m^2] - E[m]^2, clamped at 0.
+template <int EPL>
+__device__ inline void store_stats(const SpmmParams& P, int64_t row, int64_t fe, int64_t deg,
+                                   const float (&s)[EPL], const float (&q)[EPL],
+                                   const float (&m)[EPL], const int32_t (&im)[EPL],
+                                   const float (&n)[EPL], const int32_t (&in)[EPL], bool vec) {
+    const int64_t o = row * P.F + fe;
+    const float dv = (float)deg;
+    float mean[EPL], var[EPL], sd[EPL], mx[EPL], mn[EPL];
+#pragma unroll
+    for (int k = 0; k < EPL; ++k) {
+        mean[k] = deg > 0 ? s[k] / dv : 0.f;
+        const float v = deg > 0 ? q[k] / dv - mean[k] * mean[k] : 0.f;
+        var[k] = v > 0.f ? v : 0.f;
+        sd[k] = __builtin_sqrtf(var[k]);
+        mx[k] = im[k] < 0 ? 0.f : m[k];
+        mn[k] = in[k] < 0 ? 0.f : n[k];
+    }
+    if (P.o_sum) store4<EPL>(P.o_sum + o, s, vec);
+    if (P.o_mean) store4<EPL>(P.o_mean + o, mean, vec);
+    if (P.o_max) { store4<EPL>(P.o_max + o, mx, vec); store4<EPL>(P.o_amax + o, im, vec); }
+    if (P.o_min) { store4<EPL>(P.o_min + o, mn, vec); store4<EPL>(P.o_amin + o, in, vec); }
+    if (P.o_var) store4<EPL>(P.o_var + o, var, vec);
+    if (P.o_std) store4<EPL>(P.o_std + o, sd, vec);
+}
+
+// Column of CSR position p: col[p], or p itself when col is absent (a
+// readout over contiguous segments of nodes).
+__device__ inline int32_t col_at(const SpmmParams& P, int64_t p) {
+    return P.col ? __builtin_nontemporal_load(P.col + p) : (int32_t)p;
+}
+
 // Gather-and-accumulate over edges [e0, e1) with all S slots of the wavefront
 // interleaved.  The column indices (and weights) of up to 64 edges are loaded
 // once, coalesced, one per lane; each inner step then covers SU = S*U edges:
 // slot s takes edges base + u*S + s (u < U), gets their columns by cross-lane
 // permute, issues all U feature-row loads, and only then accumulates.
-template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, bool MK>
-__device__ inline void wave_range(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int64_t e0,
+template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, int MODE>
+__device__ inline void wave_range(const SpmmParams& P,
+                                  Acc<EPL, HS, HM, MODE == kModeStats>& acc, int64_t e0,
                                   int64_t e1, int lane, int slot, bool feat_ok, int64_t fe, int U) {
+    constexpr bool MK = MODE == kModeMasked;
     using R = typename RawVec<TX, EPL>::T;
-    constexpr int A = Acc<EPL, HS, HM>::A;
+    constexpr int A = Acc<EPL, HS, HM, MODE == kModeStats>::A;
     const int S = P.S;
     const int SU = S * U;
     const int steps = kWave / SU;
@@ -292,7 +372,7 @@ __device__ inline void wave_range(const SpmmParams& P, Acc<EPL, HS, HM>& acc, in
         int32_t myc = 0, myk = -1;
         float myw = 1.f;
         if (lane < tile && lane < rem) {
-            myc = __builtin_nontemporal_load(P.col + p0 + lane);
+            myc = col_at(P, p0 + lane);
             if constexpr (W) myw = __builtin_nontemporal_load(P.w + p0 + lane);
             if constexpr (MK) myk = __builtin_nontemporal_load(P.ekey + p0 + lane);
         }
@@ -357,12 +437,13 @@ __device__ inline void wave_range(const SpmmParams& P, Acc<EPL, HS, HM>& acc, in
 // One slot per row: every slot walks its own row's edges, U at a time.
 // COOP: the slot has at least U lanes, which load its next U columns
 // together; otherwise each lane loads the columns itself.
-template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, bool MK, bool COOP>
-__device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int64_t e0,
-                                int32_t my_n, int32_t max_n, int slot, int j, bool feat_ok,
-                                int64_t fe) {
+template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, int MODE, bool COOP>
+__device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM, MODE == kModeStats>& acc,
+                                int64_t e0, int32_t my_n, int32_t max_n, int slot, int j,
+                                bool feat_ok, int64_t fe) {
+    constexpr bool MK = MODE == kModeMasked;
     using R = typename RawVec<TX, EPL>::T;
-    constexpr int A = Acc<EPL, HS, HM>::A;
+    constexpr int A = Acc<EPL, HS, HM, MODE == kModeStats>::A;
     const int L = P.L;
     for (int32_t it = 0; it < max_n; it += kUnroll) {
         const char* addr[kUnroll];
@@ -374,7 +455,7 @@ __device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int6
             int32_t myc = 0, myk = -1;
             float myw = 1.f;
             if (j < kUnroll && it + j < my_n) {
-                myc = __builtin_nontemporal_load(P.col + e0 + it + j);
+                myc = col_at(P, e0 + it + j);
                 if constexpr (W) myw = __builtin_nontemporal_load(P.w + e0 + it + j);
                 if constexpr (MK) myk = __builtin_nontemporal_load(P.ekey + e0 + it + j);
             }
@@ -395,7 +476,7 @@ __device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int6
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
                 ok[u] = feat_ok && (it + u < my_n);
-                cc[u] = ok[u] ? P.col[e0 + it + u] : 0;
+                cc[u] = ok[u] ? (P.col ? P.col[e0 + it + u] : (int32_t)(e0 + it + u)) : 0;
                 wt[u] = 1.f;
                 if constexpr (W) wt[u] = ok[u] ? P.w[e0 + it + u] : 1.f;
                 key[u] = -1;
@@ -441,8 +522,9 @@ __device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM>& acc, int6
     }
 }
 
-template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, bool MK>
+template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, int MODE>
 __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
+    constexpr bool HX = MODE == kModeStats;
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave)) +
                        (int64_t)blockIdx.x * kWavesPerBlock;
@@ -451,7 +533,7 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
     const int j = lane - slot * L;
     const bool slot_ok = slot < S;
 
-    Acc<EPL, HS, HM> acc;
+    Acc<EPL, HS, HM, HX> acc;
     acc.init();
 
     if (wv < P.n_hub_waves + P.n_mid_waves) {
@@ -496,7 +578,7 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
                 e1 = load_rp(P.rowptr, P.rp64, row + 1);
             }
         }
-        wave_range<TX, EPL, HS, HM, NT, W, MK>(P, acc, e0, e1, lane, slot, feat_ok, fe, U);
+        wave_range<TX, EPL, HS, HM, NT, W, MODE>(P, acc, e0, e1, lane, slot, feat_ok, fe, U);
         acc.fold();
         acc.reduce_slots(S, L, slot, lane);
         if (slot == 0 && feat_ok) {
@@ -506,7 +588,15 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
                 for (int k = 0; k < EPL; ++k) {
                     if constexpr (HS) P.part_sum[o + k] = acc.s[0][k];
                     if constexpr (HM) { P.part_max[o + k] = acc.m[0][k]; P.part_arg[o + k] = acc.i[0][k]; }
+                    if constexpr (HX) {
+                        P.part_sq[o + k] = acc.q[0][k];
+                        P.part_min[o + k] = acc.n[0][k];
+                        P.part_amin[o + k] = acc.j[0][k];
+                    }
                 }
+            } else if constexpr (HX) {
+                store_stats<EPL>(P, row, fe, e1 - e0, acc.s[0], acc.q[0], acc.m[0], acc.i[0],
+                                 acc.n[0], acc.j[0], P.vec_store != 0);
             } else {
                 store_row<EPL>(P, row, fe, e1 - e0, acc.s[0], acc.m[0], acc.i[0], HS, HM);
             }
@@ -538,11 +628,17 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
         max_n = o > max_n ? o : max_n;
     }
     if (L >= kUnroll)
-        slot_row<TX, EPL, HS, HM, NT, W, MK, true>(P, acc, e0, my_n, max_n, slot, j, feat_ok, fe);
+        slot_row<TX, EPL, HS, HM, NT, W, MODE, true>(P, acc, e0, my_n, max_n, slot, j, feat_ok, fe);
     else
-        slot_row<TX, EPL, HS, HM, NT, W, MK, false>(P, acc, e0, my_n, max_n, slot, j, feat_ok, fe);
+        slot_row<TX, EPL, HS, HM, NT, W, MODE, false>(P, acc, e0, my_n, max_n, slot, j, feat_ok, fe);
     acc.fold();
-    if (feat_ok) store_row<EPL>(P, row, fe, e1 - e0, acc.s[0], acc.m[0], acc.i[0], HS, HM);
+    if (feat_ok) {
+        if constexpr (HX)
+            store_stats<EPL>(P, row, fe, e1 - e0, acc.s[0], acc.q[0], acc.m[0], acc.i[0],
+                             acc.n[0], acc.j[0], P.vec_store != 0);
+        else
+            store_row<EPL>(P, row, fe, e1 - e0, acc.s[0], acc.m[0], acc.i[0], HS, HM);
+    }
 }
 
 // Rows of at most kTinyDeg edges (most rows of low-degree graphs): one slot
@@ -552,8 +648,10 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
 // in flight, so a group costs about one memory round trip.  Requires slots of
 // at least kTinyDeg + 1 lanes (the columns of a row are loaded one per lane).
 // One accumulator per element: a row has at most 7 edges.
-template <typename TX, int EPL, bool HS, bool HM, bool W, int NT, bool MK>
+template <typename TX, int EPL, bool HS, bool HM, bool W, int NT, int MODE>
 __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
+    constexpr bool MK = MODE == kModeMasked;
+    constexpr bool HX = MODE == kModeStats;
     using R = typename RawVec<TX, EPL>::T;
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t tw = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave)) +
@@ -584,7 +682,7 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
         w = 1.f;
         key = -1;
         if (j < deg) {
-            c = __builtin_nontemporal_load(P.col + beg + j);
+            c = col_at(P, (int64_t)beg + j);
             if constexpr (W) w = __builtin_nontemporal_load(P.w + beg + j);
             if constexpr (MK) key = __builtin_nontemporal_load(P.ekey + beg + j);
         }
@@ -643,7 +741,7 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
         int32_t row2, beg2, deg2;
         rec(it + 2 * nw, row2, beg2, deg2);
 
-        Acc<EPL, HS, HM, 1> acc;
+        Acc<EPL, HS, HM, HX, 1> acc;
         acc.init();
 #pragma unroll
         for (int u = 0; u < kTinyDeg; ++u) {
@@ -658,7 +756,13 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
                 acc.add(0, v, beg + u);
             }
         }
-        if (feat_ok) store_row<EPL>(P, row, fe, deg, acc.s[0], acc.m[0], acc.i[0], HS, HM);
+        if (feat_ok) {
+            if constexpr (HX)
+                store_stats<EPL>(P, row, fe, deg, acc.s[0], acc.q[0], acc.m[0], acc.i[0], acc.n[0],
+                                 acc.j[0], P.vec_store != 0);
+            else
+                store_row<EPL>(P, row, fe, deg, acc.s[0], acc.m[0], acc.i[0], HS, HM);
+        }
         row = nrow;
         beg = nbeg;
         deg = ndeg;
@@ -673,7 +777,8 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
 
 // Combine the chunk partials of every hub row, in chunk order, and write the
 // row.  One wavefront per (hub row, 64-feature tile); lane = one feature.
-template <bool HS, bool HM>
+// HX: the stats partials too (sum of squares, min and its position).
+template <bool HS, bool HM, bool HX>
 __global__ __launch_bounds__(kBlock) void spmm_fixup(SpmmParams P) {
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave)) +
@@ -687,26 +792,44 @@ __global__ __launch_bounds__(kBlock) void spmm_fixup(SpmmParams P) {
     const int64_t c0 = P.chunk_off[P.hub_base + h], c1 = P.chunk_off[P.hub_base + h + 1];
     constexpr int A = 4;
     float s[A] = {0.f, 0.f, 0.f, 0.f};
-    float m = 0.f;
-    int32_t mi = -1;
+    float qs[A] = {0.f, 0.f, 0.f, 0.f};
+    float m = 0.f, mn = 0.f;
+    int32_t mi = -1, ni = -1;
     for (int64_t c = c0; c < c1; c += A) {
-        float ps[A], pm[A];
-        int32_t pi[A];
+        float ps[A], pm[A], pq[A], pn[A];
+        int32_t pi[A], pj[A];
 #pragma unroll
         for (int a = 0; a < A; ++a) {
             const bool ok = c + a < c1;
             const int64_t o = (c + a) * P.F + f;
             if constexpr (HS) ps[a] = ok ? P.part_sum[o] : 0.f;
             if constexpr (HM) { pm[a] = ok ? P.part_max[o] : 0.f; pi[a] = ok ? P.part_arg[o] : -1; }
+            if constexpr (HX) {
+                pq[a] = ok ? P.part_sq[o] : 0.f;
+                pn[a] = ok ? P.part_min[o] : 0.f;
+                pj[a] = ok ? P.part_amin[o] : -1;
+            }
         }
 #pragma unroll
         for (int a = 0; a < A; ++a) {
             if constexpr (HS) s[a] += ps[a];
             if constexpr (HM) max_merge(m, mi, pm[a], pi[a]);
+            if constexpr (HX) {
+                qs[a] += pq[a];
+                min_merge(mn, ni, pn[a], pj[a]);
+            }
         }
     }
     const int64_t deg = load_rp(P.rowptr, P.rp64, row + 1) - load_rp(P.rowptr, P.rp64, row);
     const int64_t o = row * P.F + f;
+    if constexpr (HX) {
+        const float sum[1] = {(s[0] + s[1]) + (s[2] + s[3])};
+        const float sq[1] = {(qs[0] + qs[1]) + (qs[2] + qs[3])};
+        const float mx[1] = {m}, nn[1] = {mn};
+        const int32_t im[1] = {mi}, in[1] = {ni};
+        store_stats<1>(P, row, f, deg, sum, sq, mx, im, nn, in, false);
+        return;
+    }
     if constexpr (HS) {
         float v = (s[0] + s[1]) + (s[2] + s[3]);
         if (P.reduce & kMean) v = deg > 0 ? v / (float)deg : 0.f;
@@ -787,13 +910,15 @@ hipError_t launch_w(const SpmmParams& p, unsigned grid, hipStream_t s) {
     const bool hs = (p.reduce & (kSum | kMean)) != 0;
     const bool hm = (p.reduce & kMax) != 0;
     if (p.mtab)  // masked sum: the gradient of max
-        hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 1, W, true>), dim3(grid), dim3(kBlock), 0, s, p);
+        hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 1, W, kModeMasked>), dim3(grid), dim3(kBlock), 0, s, p);
+    else if (p.stats)
+        hipLaunchKernelGGL((spmm_main<TX, EPL, true, true, 1, W, kModeStats>), dim3(grid), dim3(kBlock), 0, s, p);
     else if (hs && hm)
-        hipLaunchKernelGGL((spmm_main<TX, EPL, true, true, 1, W, false>), dim3(grid), dim3(kBlock), 0, s, p);
+        hipLaunchKernelGGL((spmm_main<TX, EPL, true, true, 1, W, kModePlain>), dim3(grid), dim3(kBlock), 0, s, p);
     else if (hm)
-        hipLaunchKernelGGL((spmm_main<TX, EPL, false, true, 1, W, false>), dim3(grid), dim3(kBlock), 0, s, p);
+        hipLaunchKernelGGL((spmm_main<TX, EPL, false, true, 1, W, kModePlain>), dim3(grid), dim3(kBlock), 0, s, p);
     else
-        hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 1, W, false>), dim3(grid), dim3(kBlock), 0, s, p);
+        hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 1, W, kModePlain>), dim3(grid), dim3(kBlock), 0, s, p);
     return hipGetLastError();
 }
 
@@ -802,11 +927,11 @@ hipError_t launch_typed(const SpmmParams& p, unsigned grid, hipStream_t s) {
     if (p.n_tables > 1) {
         // typed-node tables: unweighted sum only
         if (p.n_tables <= 2)
-            hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 2, false, false>), dim3(grid), dim3(kBlock), 0, s, p);
+            hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 2, false, kModePlain>), dim3(grid), dim3(kBlock), 0, s, p);
         else if (p.n_tables <= 4)
-            hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 4, false, false>), dim3(grid), dim3(kBlock), 0, s, p);
+            hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 4, false, kModePlain>), dim3(grid), dim3(kBlock), 0, s, p);
         else
-            hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, MP_MAX_TYPES, false, false>), dim3(grid), dim3(kBlock), 0, s, p);
+            hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, MP_MAX_TYPES, false, kModePlain>), dim3(grid), dim3(kBlock), 0, s, p);
         return hipGetLastError();
     }
     return p.w ? launch_w<TX, EPL, true>(p, grid, s) : launch_w<TX, EPL, false>(p, grid, s);
@@ -859,19 +984,22 @@ hipError_t launch_tiny_typed(const SpmmParams& p, unsigned grid, hipStream_t s) 
     const bool hm = (p.reduce & kMax) != 0;
     const bool w = p.w != nullptr;
 #define MP_TINY(HS, HM, WW) \
-    hipLaunchKernelGGL((spmm_tiny<TX, EPL, HS, HM, WW, 1, false>), dim3(grid), dim3(kBlock), 0, s, p)
+    hipLaunchKernelGGL((spmm_tiny<TX, EPL, HS, HM, WW, 1, kModePlain>), dim3(grid), dim3(kBlock), 0, s, p)
     if (p.n_tables > 1) {
         // typed-node tables: unweighted sum only
         if (p.n_tables <= 2)
-            hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, 2, false>), dim3(grid), dim3(kBlock), 0, s, p);
+            hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, 2, kModePlain>), dim3(grid), dim3(kBlock), 0, s, p);
         else if (p.n_tables <= 4)
-            hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, 4, false>), dim3(grid), dim3(kBlock), 0, s, p);
+            hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, 4, kModePlain>), dim3(grid), dim3(kBlock), 0, s, p);
         else
-            hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, MP_MAX_TYPES, false>), dim3(grid), dim3(kBlock), 0, s, p);
+            hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, MP_MAX_TYPES, kModePlain>), dim3(grid), dim3(kBlock), 0, s, p);
     } else if (p.mtab) {
         // masked sum: the gradient of max
-        if (w) hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, true, 1, true>), dim3(grid), dim3(kBlock), 0, s, p);
-        else hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, 1, true>), dim3(grid), dim3(kBlock), 0, s, p);
+        if (w) hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, true, 1, kModeMasked>), dim3(grid), dim3(kBlock), 0, s, p);
+        else hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, 1, kModeMasked>), dim3(grid), dim3(kBlock), 0, s, p);
+    } else if (p.stats) {
+        if (w) hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, true, true, 1, kModeStats>), dim3(grid), dim3(kBlock), 0, s, p);
+        else hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, true, false, 1, kModeStats>), dim3(grid), dim3(kBlock), 0, s, p);
     } else if (hs && hm) { if (w) MP_TINY(true, true, true); else MP_TINY(true, true, false); }
     else if (hm) { if (w) MP_TINY(false, true, true); else MP_TINY(false, true, false); }
     else { if (w) MP_TINY(true, false, true); else MP_TINY(true, false, false); }
@@ -913,9 +1041,10 @@ hipError_t launch_spmm_fixup(const SpmmParams& p, hipStream_t s) {
     const unsigned grid = (unsigned)ceil_div(waves, kWavesPerBlock);
     const bool hs = (p.reduce & (kSum | kMean)) != 0;
     const bool hm = (p.reduce & kMax) != 0;
-    if (hs && hm) hipLaunchKernelGGL((spmm_fixup<true, true>), dim3(grid), dim3(kBlock), 0, s, p);
-    else if (hm) hipLaunchKernelGGL((spmm_fixup<false, true>), dim3(grid), dim3(kBlock), 0, s, p);
-    else hipLaunchKernelGGL((spmm_fixup<true, false>), dim3(grid), dim3(kBlock), 0, s, p);
+    if (p.stats) hipLaunchKernelGGL((spmm_fixup<true, true, true>), dim3(grid), dim3(kBlock), 0, s, p);
+    else if (hs && hm) hipLaunchKernelGGL((spmm_fixup<true, true, false>), dim3(grid), dim3(kBlock), 0, s, p);
+    else if (hm) hipLaunchKernelGGL((spmm_fixup<false, true, false>), dim3(grid), dim3(kBlock), 0, s, p);
+    else hipLaunchKernelGGL((spmm_fixup<true, false, false>), dim3(grid), dim3(kBlock), 0, s, p);
     return hipGetLastError();
 }
 

@@ -200,6 +200,39 @@ def test_backward_errors_and_sizes():
     assert bww(x_dtype=7) == -3
 
 
+def test_multi_errors():
+    L = mp.lib()
+    nb = ctypes.c_size_t(7)
+    assert L.mp_spmm_multi_workspace(None, ctypes.byref(nb)) == 0 and nb.value == 0
+
+    def outs(*specs):
+        arr = (mp.mp_aggr_out * max(len(specs), 1))()
+        for k, (a, o, g) in enumerate(specs):
+            arr[k].aggr, arr[k].out, arr[k].arg = a, o, g
+        return arr
+
+    def multi(specs, n=None, col=FAKE):
+        arr = outs(*specs)
+        return L.mp_spmm_multi(None, FAKE, 0, col, None, FAKE, 0, 10, 10, 8,
+                               len(specs) if n is None else n, arr, None, 0, None)
+
+    assert multi([(mp.MP_SUM, FAKE, None), (mp.MP_SUM, FAKE, None)]) == -4  # duplicate
+    assert multi([(mp.MP_SUM | mp.MP_MAX, FAKE, FAKE)]) == -4  # two aggregators in one
+    assert multi([(64, FAKE, None)]) == -4
+    assert multi([(mp.MP_SUM, FAKE, None)], n=0) == -2
+    assert multi([(mp.MP_SUM, FAKE, None)], n=7) == -2
+    assert multi([(mp.MP_MAX, FAKE, None)]) == -1  # max needs its positions
+    assert multi([(mp.MP_MIN, FAKE, None)]) == -1
+    assert multi([(mp.MP_VAR, None, None)]) == -1
+    assert multi([(mp.MP_STD, FAKE + 2, None)]) == -8
+    assert multi([(mp.MP_SUM, FAKE, None)], col=None) == -1
+    arr = outs((mp.MP_MEAN, FAKE, None))
+    assert L.mp_spmm_multi(None, FAKE, 0, FAKE, None, FAKE, 5, 10, 10, 8, 1, arr, None, 0,
+                           None) == -3
+    assert L.mp_readout_multi(None, FAKE, 0, FAKE, 0, 100, 10, 0, 1, arr, None, 0, None) == -2
+    assert L.mp_readout_multi(None, None, 0, FAKE, 0, 100, 10, 8, 1, arr, None, 0, None) == -1
+
+
 def test_validate_errors():
     L = mp.lib()
     assert L.mp_validate_sorted(FAKE, 10, None, None) == -1
