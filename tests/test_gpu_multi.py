@@ -133,7 +133,6 @@ def test_multi_ties_and_signed_zero():
     rp_o, col_o, _, _ = oracle.coo_to_csr(src, dst, 4)
     res = mp.spmm_multi(dev(rp_o.astype(np.int32)), dev(col_o), dev(x), ALL)
     torch.cuda.synchronize()
-    g = graphgen.Graph("ties", 4, 4, src, dst, 2, x=x)
     compare(res, rp_o, col_o, None, {"x": x}, ALL, torch.float32)
     assert res["argmin"].cpu().tolist()[1] == [3, 3]  # -0.0 ties +0.0: first edge
 
