@@ -38,6 +38,8 @@ METRIC = "SpMM effective HBM GB/s (% of peak) + edge·features/s, sum/mean/max"
 HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 WORKLOAD = "chunglu-124M"
 BACKWARD = "chunglu-124M-backward"
+STACKED = "chunglu-124M-stacked"
+READOUT = "readout-2.4M"
 DOMINANT = "spmm_main<float, 4, true, false, 1, false, false>"  # fp32 sum, the largest launch of a step
 DOMINANT_SRC = ["paper_2507_16991_amd/csrc/spmm.hip", "paper_2507_16991_amd/csrc/mp_internal.hpp"]
 COUNTER_SUMMARY = os.path.join(ROOT, "profiles", "spmm_main_f32_sum_chunglu124M_counters.txt")
@@ -84,6 +86,15 @@ def grad_w_bytes(N_dst, E, F):
     """One x row gathered per edge, the output gradient read once per row,
     one fp32 per edge written."""
     return 4 * (N_dst + 1) + 4 * E + E * F * 4 + N_dst * F * 4 + 4 * E
+
+
+def multi_bytes(N, E, F, xb, names, rowptr_b=4, col=True):
+    """One gather of every edge's row feeds all requested statistics; each
+    output row is written once (max and min with their int32 positions)."""
+    b = (N + 1) * rowptr_b + (4 * E if col else 0) + E * F * xb
+    for n in names:
+        b += N * F * (8 if n in ("max", "min") else 4)
+    return b
 
 
 def plan_bytes(N):
@@ -141,6 +152,8 @@ def build_step(args, mp, torch, np, dev):
     t0 = time.time()
     if args.workload == BACKWARD:
         g = graphgen.workload(WORKLOAD, seed=args.seed, bf16=False)
+    elif args.workload in (STACKED, READOUT):
+        g = graphgen.workload(WORKLOAD, seed=args.seed)
     else:
         g = graphgen.workload(args.workload, seed=args.seed)
     print(f"[bench] generated {args.workload} in {time.time() - t0:.1f}s", file=sys.stderr,
@@ -180,6 +193,10 @@ def build_step(args, mp, torch, np, dev):
 
     if args.workload == BACKWARD:
         return backward_step(g, mp, torch, np, dev, mark)
+    if args.workload == STACKED:
+        return stacked_step(g, mp, torch, np, dev, mark)
+    if args.workload == READOUT:
+        return readout_step(g, mp, torch, np, dev, mark, args.seed)
 
     N, E, F = g.n_dst, g.E, g.F
     src = torch.from_numpy(g.src).to(dev)
@@ -315,7 +332,114 @@ def backward_step(g, mp, torch, np, dev, mark):
     return g, step, ops
 
 
+PNA = ["mean", "min", "max", "std"]
+
+
+def stacked_step(g, mp, torch, np, dev, mark):
+    """The headline graph with a stacked aggregation (mean, min, max and std,
+    the aggregator set of principal neighbourhood aggregation) from one gather,
+    for fp32 and for bf16 features, after COO->CSR and the plan."""
+    N, E, F = g.n_dst, g.E, g.F
+    it = mp.MP_I32
+    src = torch.from_numpy(g.src).to(dev)
+    dst = torch.from_numpy(g.dst).to(dev)
+    xs = {"f32": (torch.from_numpy(g.x).to(dev), mp.MP_F32, 4),
+          "bf16": (torch.from_numpy(g.x_bf16.view(np.int16)).to(dev).view(torch.bfloat16),
+                   mp.MP_BF16, 2)}
+    rowptr = torch.empty(N + 1, dtype=torch.int32, device=dev)
+    col = torch.empty(E, dtype=torch.int32, device=dev)
+    ws_csr = torch.empty(mp.mp_coo_to_csr_workspace(E, N, it, 0), dtype=torch.uint8, device=dev)
+    nplan = mp.mp_spmm_plan_size(N, E)
+    plan_buf = torch.empty(nplan, dtype=torch.uint8, device=dev)
+    outs = [(mp.AGGR[n], torch.empty(N, F, dtype=torch.float32, device=dev),
+             torch.empty(N, F, dtype=torch.int32, device=dev) if n in ("max", "min") else None)
+            for n in PNA]
+    ops = [("csr", csr_bytes(N, E), 0), ("plan", plan_bytes(N), 0)]
+    for k, (_, _, xb) in xs.items():
+        ops.append((f"stacked_{k}", multi_bytes(N, E, F, xb, PNA), E * F))
+    plans, wss = {}, {}
+
+    def step(evs=None):
+        mark(evs, 0)
+        mp.mp_coo_to_csr(src, dst, E, N, rowptr, it, col, None, None, None, ws_csr,
+                         ws_csr.numel())
+        mark(evs, 1)
+        if "h" in plans:
+            mp.mp_spmm_plan_free(plans["h"])
+        plans["h"] = h = mp.mp_spmm_plan_build(rowptr, it, N, E, F, mp.MP_F32, plan_buf, nplan)
+        mark(evs, 2)
+        nb = mp.mp_spmm_multi_workspace(h)
+        if "ws" not in wss or wss["ws"].numel() < nb:
+            wss["ws"] = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
+        i = 2
+        for k, (x, xd, _) in xs.items():
+            mp.mp_spmm_multi(h, rowptr, it, col, None, x, xd, N, N, F, outs, wss["ws"],
+                             wss["ws"].numel())
+            i += 1
+            mark(evs, i)
+
+    return g, step, ops
+
+
+def readout_step(g, mp, torch, np, dev, mark, seed):
+    """A global readout: the headline graph's 2,449,029 node rows (F = 100,
+    fp32 and bf16) split into 1,024 graphs of a seeded mini-batch, given as a
+    sorted batch vector; ptr from the sorted-COO
+    fast path, the plan, then sum, mean, max and std per graph from one pass.
+    Graph sizes are proportional to seeded uniform draws in [1, 2 N / 1024]."""
+    import graphgen
+
+    N, F = g.n_src, g.F
+    B = 1024
+    u = graphgen.uniform_ints(seed, 13, B, 2 * N // B).astype(np.int64) + 1
+    sizes = u * N // int(u.sum())  # proportional to the draws, summing to N
+    sizes[-1] = N - int(sizes[:-1].sum())
+    batch = torch.from_numpy(np.repeat(np.arange(B, dtype=np.int32), sizes)).to(dev)
+    nodes = torch.arange(N, dtype=torch.int32, device=dev)
+    ptr = torch.empty(B + 1, dtype=torch.int32, device=dev)
+    col = torch.empty(N, dtype=torch.int32, device=dev)
+    xs = {"f32": (torch.from_numpy(g.x).to(dev), mp.MP_F32, 4),
+          "bf16": (torch.from_numpy(g.x_bf16.view(np.int16)).to(dev).view(torch.bfloat16),
+                   mp.MP_BF16, 2)}
+    nplan = mp.mp_spmm_plan_size(B, N)
+    plan_buf = torch.empty(nplan, dtype=torch.uint8, device=dev)
+    names = ["sum", "mean", "max", "std"]
+    outs = [(mp.AGGR[n], torch.empty(B, F, dtype=torch.float32, device=dev),
+             torch.empty(B, F, dtype=torch.int32, device=dev) if n == "max" else None)
+            for n in names]
+    ops = [("ptr", 4 * N + 4 * (B + 1), 0), ("plan", plan_bytes(B), 0)]
+    for k, (_, _, xb) in xs.items():
+        ops.append((f"readout_{k}", multi_bytes(B, N, F, xb, names, col=False), N * F))
+    plans, wss = {}, {}
+
+    def step(evs=None):
+        mark(evs, 0)
+        mp.mp_sorted_coo_to_csr(nodes, batch, N, B, ptr, mp.MP_I32, col, None, None, None)
+        mark(evs, 1)
+        if "h" in plans:
+            mp.mp_spmm_plan_free(plans["h"])
+        plans["h"] = h = mp.mp_spmm_plan_build(ptr, mp.MP_I32, B, N, F, mp.MP_F32, plan_buf,
+                                               nplan)
+        mark(evs, 2)
+        nb = mp.mp_spmm_multi_workspace(h)
+        if "ws" not in wss or wss["ws"].numel() < nb:
+            wss["ws"] = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
+        i = 2
+        for k, (x, xd, _) in xs.items():
+            mp.mp_readout_multi(h, ptr, mp.MP_I32, x, xd, N, B, F, outs, wss["ws"],
+                                wss["ws"].numel())
+            i += 1
+            mark(evs, i)
+
+    g.n_dst, g.E = B, N
+    return g, step, ops
+
+
 OP_KERNELS = {
+    "stacked_f32": "spmm_main, stats mode (mean, min, max, std from one gather)",
+    "stacked_bf16": "spmm_main, stats mode (mean, min, max, std from one gather)",
+    "readout_f32": "spmm_main, stats mode over consecutive node rows (readout)",
+    "readout_bf16": "spmm_main, stats mode over consecutive node rows (readout)",
     "grad_x_sum_f32": "spmm_main (sum over the transposed CSR)",
     "grad_x_mean_f32": "spmm_main (sum over the transposed CSR of G/deg)",
     "grad_x_max_f32": "spmm_main, masked (argmax routing over the transposed CSR)",
@@ -390,6 +514,13 @@ def run(args):
                           "COO->CSR (+perm, weights to CSR order) + plan + mean + weighted sum"),
         "uniform-10k": (f"uniform-10k: uniform random graph, N={N}, E={E}, F={F}, fp32 U(-1,1), "
                         f"seed {args.seed}", "COO->CSR + plan + sum"),
+        STACKED: (f"{STACKED}: the Chung-Lu graph of {WORKLOAD} (N={N}, E={E}, F={F}, fp32 and "
+                  f"bf16 N(0,1) features), seed {args.seed}",
+                  "COO->CSR + plan + stacked {mean, min, max, std} x {fp32, bf16 features}"),
+        READOUT: (f"{READOUT}: the {WORKLOAD} node rows (2449029 x {F}, fp32 and bf16) in "
+                  f"1024 graphs of a sorted batch vector, seed {args.seed}",
+                  "ptr from the sorted batch + plan + readout {sum, mean, max, std} x "
+                  "{fp32, bf16}"),
         BACKWARD: (f"{BACKWARD}: the Chung-Lu graph of {WORKLOAD} (N={N}, E={E}, F={F}, fp32 "
                    f"x and output gradient N(0,1)), seed {args.seed}",
                    "CSR transpose + plan + dL/dx {sum, mean, max} + dL/dw sum"),
@@ -570,8 +701,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--workload", default=WORKLOAD,
-                    choices=[WORKLOAD, BACKWARD, "web-1.6B", "powerlaw-1.2M", "uniform-10k",
-                             "hetero-20M"],
+                    choices=[WORKLOAD, BACKWARD, STACKED, READOUT, "web-1.6B", "powerlaw-1.2M",
+                             "uniform-10k", "hetero-20M"],
                     help="benchmark workload (the default is the metric's configuration)")
     ap.add_argument("--cpu-rows", type=int, default=0,
                     help="rows of the CPU-oracle aggregation sample (0: all rows)")
