@@ -431,8 +431,8 @@ def readout_step(g, mp, torch, np, dev, mark, seed):
             i += 1
             mark(evs, i)
 
-    g.n_dst, g.E = B, N
-    return g, step, ops
+    from types import SimpleNamespace
+    return SimpleNamespace(n_dst=B, n_src=N, E=N, F=F), step, ops
 
 
 OP_KERNELS = {
