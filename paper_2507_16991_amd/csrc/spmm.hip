@@ -144,8 +144,10 @@ __device__ inline void min_merge(float& va, int32_t& ia, float vb, int32_t ib) {
 // ---- accumulator state -------------------------------------------------------
 
 // HX (stats mode, which also sets HS and HM): the sum of squares and the
-// (min, position) pair are kept as well.
-template <int EPL, bool HS, bool HM, bool HX = false, int NA = ((HM || HX) ? 2 : 4)>
+// (min, position) pair are kept as well, in a single partial (six running
+// values per element already keep the adds of a step independent; more
+// partials would cost occupancy).
+template <int EPL, bool HS, bool HM, bool HX = false, int NA = (HX ? 1 : (HM ? 2 : 4))>
 struct Acc {
     static constexpr int A = NA;  // independent partial accumulators
     static constexpr int AX = HX ? NA : 1;
