@@ -144,10 +144,8 @@ __device__ inline void min_merge(float& va, int32_t& ia, float vb, int32_t ib) {
 // ---- accumulator state -------------------------------------------------------
 
 // HX (stats mode, which also sets HS and HM): the sum of squares and the
-// (min, position) pair are kept as well, in a single partial (six running
-// values per element already keep the adds of a step independent; more
-// partials would cost occupancy).
-template <int EPL, bool HS, bool HM, bool HX = false, int NA = (HX ? 1 : (HM ? 2 : 4))>
+// (min, position) pair are kept as well.
+template <int EPL, bool HS, bool HM, bool HX = false, int NA = (HM ? 2 : 4)>
 struct Acc {
     static constexpr int A = NA;  // independent partial accumulators
     static constexpr int AX = HX ? NA : 1;
@@ -237,6 +235,14 @@ struct Acc {
         }
     }
 };
+
+// Accumulator of a kernel instance.  Stats mode keeps six running values per
+// element: with fp32 features one partial (the registers of a second would
+// cost occupancy, and the gathers, not the adds, bound it); with bf16
+// features, whose rows arrive twice as fast, two.
+template <typename TX, int EPL, bool HS, bool HM, int MODE>
+using AccFor = Acc<EPL, HS, HM, MODE == kModeStats,
+                   MODE == kModeStats ? (sizeof(TX) == 4 ? 1 : 2) : (HM ? 2 : 4)>;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -360,11 +366,11 @@ __device__ inline int32_t col_at(const SpmmParams& P, int64_t p) {
 // permute, issues all U feature-row loads, and only then accumulates.
 template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, int MODE>
 __device__ inline void wave_range(const SpmmParams& P,
-                                  Acc<EPL, HS, HM, MODE == kModeStats>& acc, int64_t e0,
+                                  AccFor<TX, EPL, HS, HM, MODE>& acc, int64_t e0,
                                   int64_t e1, int lane, int slot, bool feat_ok, int64_t fe, int U) {
     constexpr bool MK = MODE == kModeMasked;
     using R = typename RawVec<TX, EPL>::T;
-    constexpr int A = Acc<EPL, HS, HM, MODE == kModeStats>::A;
+    constexpr int A = AccFor<TX, EPL, HS, HM, MODE>::A;
     const int S = P.S;
     const int SU = S * U;
     const int steps = kWave / SU;
@@ -440,12 +446,12 @@ __device__ inline void wave_range(const SpmmParams& P,
 // COOP: the slot has at least U lanes, which load its next U columns
 // together; otherwise each lane loads the columns itself.
 template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, int MODE, bool COOP>
-__device__ inline void slot_row(const SpmmParams& P, Acc<EPL, HS, HM, MODE == kModeStats>& acc,
+__device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MODE>& acc,
                                 int64_t e0, int32_t my_n, int32_t max_n, int slot, int j,
                                 bool feat_ok, int64_t fe) {
     constexpr bool MK = MODE == kModeMasked;
     using R = typename RawVec<TX, EPL>::T;
-    constexpr int A = Acc<EPL, HS, HM, MODE == kModeStats>::A;
+    constexpr int A = AccFor<TX, EPL, HS, HM, MODE>::A;
     const int L = P.L;
     for (int32_t it = 0; it < max_n; it += kUnroll) {
         const char* addr[kUnroll];
@@ -535,7 +541,7 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
     const int j = lane - slot * L;
     const bool slot_ok = slot < S;
 
-    Acc<EPL, HS, HM, HX> acc;
+    AccFor<TX, EPL, HS, HM, MODE> acc;
     acc.init();
 
     if (wv < P.n_hub_waves + P.n_mid_waves) {
