@@ -59,6 +59,10 @@ def _L():
         lib.oracle_spmm_multi.argtypes = [i64, p, i64, i64, p, p, p, p, i32, i64, p, p, p, p,
                                           p, i32]
         lib.oracle_spmm_multi.restype = i32
+        lib.oracle_segment_matmul.argtypes = [i32, p, p, p, i64, i64, p, p]
+        lib.oracle_segment_matmul.restype = i32
+        lib.oracle_segment_matmul_backward.argtypes = [i32, p, p, p, p, i64, i64, p, p, p, p]
+        lib.oracle_segment_matmul_backward.restype = i32
         lib.oracle_csr_transpose.argtypes = [i64, i64, p, p, p, p, p]
         lib.oracle_csr_transpose.restype = i32
         lib.oracle_spmm_backward_x.argtypes = [i64, p, i64, i64, p, p, p, p, i32, i64, i32, p,
@@ -312,3 +316,38 @@ def spmm_backward_w(rowptr, col, reduce, x=None, x_bf16=None, g=None, g_bf16=Non
     if rc != 0:
         raise ValueError(f"oracle_spmm_backward_w failed ({rc})")
     return gw, sc
+
+
+def segment_matmul(seg, x_bf16, w_bf16):
+    """out[r] = x[r] @ W[t] for rows r of segment t (bf16 bits in, fp64 out).
+    seg: [T+1] row offsets; x_bf16 [N, F]; w_bf16 [T, F, Fo].  Returns (out,
+    scale) fp64 [N, Fo]."""
+    seg = _c(seg, np.int64)
+    x = _c(x_bf16, np.uint16)
+    w = _c(w_bf16, np.uint16)
+    T, F, Fo = w.shape
+    N = x.shape[0]
+    out = np.empty((N, Fo), np.float64)
+    sc = np.empty((N, Fo), np.float64)
+    rc = _L().oracle_segment_matmul(T, _p(seg), _p(x), _p(w), F, Fo, _p(out), _p(sc))
+    if rc != 0:
+        raise ValueError(f"oracle_segment_matmul failed ({rc})")
+    return out, sc
+
+
+def segment_matmul_backward(seg, x_bf16, w_bf16, dout_bf16):
+    """Gradients of segment_matmul given dL/d out (bf16 bits [N, Fo]).
+    Returns (dx, dx_scale [N, F], dw, dw_scale [T, F, Fo]) in fp64."""
+    seg = _c(seg, np.int64)
+    x = _c(x_bf16, np.uint16)
+    w = _c(w_bf16, np.uint16)
+    d = _c(dout_bf16, np.uint16)
+    T, F, Fo = w.shape
+    N = x.shape[0]
+    dx, dxs = np.empty((N, F), np.float64), np.empty((N, F), np.float64)
+    dw, dws = np.empty((T, F, Fo), np.float64), np.empty((T, F, Fo), np.float64)
+    rc = _L().oracle_segment_matmul_backward(T, _p(seg), _p(x), _p(w), _p(d), F, Fo, _p(dx),
+                                             _p(dxs), _p(dw), _p(dws))
+    if rc != 0:
+        raise ValueError(f"oracle_segment_matmul_backward failed ({rc})")
+    return dx, dxs, dw, dws

@@ -38,6 +38,12 @@
  * messages, sum of (m - mean)^2 / deg, and its square root.  A global readout
  * is the same aggregation over contiguous segments of nodes (col = identity).
  *
+ * Segment matmul (Sec. 2.2, heterogeneous GNNs: the projections
+ * {H_T W_T} over node types, with a three-dimensional weight W of shape
+ * [|T|, F, F'], and their gradients with respect to H_T and W): rows of X are
+ * grouped by type in contiguous segments; each segment is multiplied by its
+ * own weight matrix.
+ *
  * Backward (Sec. 2.2: the backward pass of an aggregation runs over the
  * transposed adjacency, which is why CSR and CSC are both cached): the
  * derivatives of the aggregation above with respect to the features x and the
@@ -578,4 +584,82 @@ int oracle_spmm_multi(int64_t n_rows, const int64_t* rows, int64_t N_dst, int64_
         }
     }
     return bad ? -1 : 0;
+}
+
+/* ---- segment matmul -------------------------------------------------------- */
+
+/* value of a bf16 matrix element (bits) as fp64 */
+static inline double bf(const uint16_t* a, int64_t i) { return (double)widen_bf16(a[i]); }
+
+/* out[r, o] = sum_f X[r, f] * W[t, f, o] for every row r of segment t
+ * (seg[t] <= r < seg[t+1]); scale[r, o] = sum_f |X[r, f] * W[t, f, o]|.
+ * X [N, F], W [T, F, Fo] bf16 bits; out, scale [N, Fo] fp64 (scale may be
+ * NULL).  Returns 0, or -1 for bad segment bounds. */
+int oracle_segment_matmul(int T, const int64_t* seg, const uint16_t* X, const uint16_t* W,
+                          int64_t F, int64_t Fo, double* out, double* scale) {
+    if (seg[0] != 0) return -1;
+    for (int t = 0; t < T; ++t)
+        if (seg[t + 1] < seg[t]) return -1;
+    for (int t = 0; t < T; ++t) {
+        const uint16_t* Wt = W + (int64_t)t * F * Fo;
+#pragma omp parallel for schedule(static)
+        for (int64_t r = seg[t]; r < seg[t + 1]; ++r)
+            for (int64_t o = 0; o < Fo; ++o) {
+                double s = 0.0, a = 0.0;
+                for (int64_t f = 0; f < F; ++f) {
+                    double p = bf(X, r * F + f) * bf(Wt, f * Fo + o);
+                    s += p;
+                    a += fabs(p);
+                }
+                out[r * Fo + o] = s;
+                if (scale) scale[r * Fo + o] = a;
+            }
+    }
+    return 0;
+}
+
+/* Gradients of the segment matmul given dOut = dL/d out [N, Fo] (bf16 bits):
+ *   dX[r, f]    = sum_o dOut[r, o] * W[t, f, o]           (r in segment t)
+ *   dW[t, f, o] = sum_{r in segment t} X[r, f] * dOut[r, o]
+ * with the matching sums of absolute values in dx_scale, dw_scale.  Any
+ * output may be NULL.  Returns 0, or -1 for bad segment bounds. */
+int oracle_segment_matmul_backward(int T, const int64_t* seg, const uint16_t* X,
+                                   const uint16_t* W, const uint16_t* dOut, int64_t F,
+                                   int64_t Fo, double* dX, double* dx_scale, double* dW,
+                                   double* dw_scale) {
+    if (seg[0] != 0) return -1;
+    for (int t = 0; t < T; ++t)
+        if (seg[t + 1] < seg[t]) return -1;
+    for (int t = 0; t < T; ++t) {
+        const uint16_t* Wt = W + (int64_t)t * F * Fo;
+        if (dX) {
+#pragma omp parallel for schedule(static)
+            for (int64_t r = seg[t]; r < seg[t + 1]; ++r)
+                for (int64_t f = 0; f < F; ++f) {
+                    double s = 0.0, a = 0.0;
+                    for (int64_t o = 0; o < Fo; ++o) {
+                        double p = bf(dOut, r * Fo + o) * bf(Wt, f * Fo + o);
+                        s += p;
+                        a += fabs(p);
+                    }
+                    dX[r * F + f] = s;
+                    if (dx_scale) dx_scale[r * F + f] = a;
+                }
+        }
+        if (dW) {
+#pragma omp parallel for schedule(static)
+            for (int64_t i = 0; i < F * Fo; ++i) {
+                int64_t f = i / Fo, o = i - f * Fo;
+                double s = 0.0, a = 0.0;
+                for (int64_t r = seg[t]; r < seg[t + 1]; ++r) {
+                    double p = bf(X, r * F + f) * bf(dOut, r * Fo + o);
+                    s += p;
+                    a += fabs(p);
+                }
+                dW[(int64_t)t * F * Fo + i] = s;
+                if (dw_scale) dw_scale[(int64_t)t * F * Fo + i] = a;
+            }
+        }
+    }
+    return 0;
 }
