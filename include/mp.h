@@ -310,6 +310,46 @@ int mp_spmm_backward_w(const void* rowptr, int rowptr_itype, const int32_t* col,
                        float* grad_w, void* ws, size_t ws_bytes, void* stream);
 
 /* ---------------------------------------------------------------------------
+ * Segment matmul (Sec. 2.2, heterogeneous GNNs: the projections {H_T W_T}
+ * over node types with a weight tensor of shape [|T|, F, F'], forward and the
+ * gradients with respect to H_T and W).  Rows of x are grouped by type in
+ * contiguous segments seg[t] <= r < seg[t+1]; segment t uses W[t].  Inputs
+ * are bf16 (row-major), products accumulate in fp32 on the matrix cores
+ * (MFMA), in an order fixed by the tiling: outputs are deterministic.
+ * Shared rules: seg is a HOST array of T+1 row offsets (seg[0] = 0,
+ * non-decreasing, seg[T] = N <= INT32_MAX), 1 <= T <= MP_MAX_TYPES; F and Fo
+ * are multiples of 8 in [8, 65536]; bf16 arrays and workspaces are 16-byte
+ * aligned.
+ * ------------------------------------------------------------------------- */
+
+/* Workspace bytes for mp_segment_matmul (W transposed, T*F*Fo*2 bytes). */
+int mp_segment_matmul_workspace(int T, int64_t F, int64_t Fo, size_t* bytes);
+
+/* out[r, :] = x[r, :] @ W[t] for every row r of segment t.
+ *   x    [N, F] bf16;  W [T, F, Fo] bf16;  out [N, Fo] of out_dtype (fp32, or
+ *        bf16 rounded to nearest even from the fp32 result).
+ * Asynchronous on `stream`. */
+int mp_segment_matmul(const int64_t* seg, int T, const void* x, const void* W, int64_t F,
+                      int64_t Fo, void* out, int out_dtype, void* ws, size_t ws_bytes,
+                      void* stream);
+
+/* Workspace bytes for mp_segment_matmul_backward (fp32 partial products of
+ * the weight gradient: one F x Fo tile per 2048 rows of a segment). */
+int mp_segment_matmul_backward_workspace(const int64_t* seg, int T, int64_t F, int64_t Fo,
+                                         size_t* bytes);
+
+/* Gradients of mp_segment_matmul given dout = dL/d out [N, Fo] bf16:
+ *   dx[r, :]  = dout[r, :] @ W[t]^T        ([N, F] of dx_dtype; needs W)
+ *   dW[t]     = x[seg_t]^T @ dout[seg_t]    ([T, F, Fo] fp32; needs x and ws;
+ *               each segment's rows are reduced in fixed chunks whose
+ *               partials are added in order, so no atomics are used)
+ * Either output may be NULL (not both).  An empty segment gives dW[t] = 0.
+ * Asynchronous on `stream`. */
+int mp_segment_matmul_backward(const int64_t* seg, int T, const void* x, const void* W,
+                               const void* dout, int64_t F, int64_t Fo, void* dx, int dx_dtype,
+                               float* dW, void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
  * Heterogeneous message passing (Sec. 2.2, nested Eq. (1)): per destination
  * node type T, out_T = sum over relations r ending at T (ascending r) of the
  * sum aggregation over r's edges.  Built as one combined destination-major

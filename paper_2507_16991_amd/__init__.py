@@ -27,7 +27,9 @@ __all__ = [
     "mp_spmm_backward_x", "mp_spmm_backward_w_workspace", "mp_spmm_backward_w",
     "csr_transpose", "spmm_backward_x", "spmm_backward_w", "MP_MIN", "MP_VAR", "MP_STD", "AGGR",
     "mp_aggr_out", "mp_spmm_multi_workspace", "mp_spmm_multi", "mp_readout_multi", "spmm_multi",
-    "readout",
+    "readout", "mp_segment_matmul_workspace", "mp_segment_matmul",
+    "mp_segment_matmul_backward_workspace", "mp_segment_matmul_backward", "segment_matmul",
+    "segment_matmul_backward",
     "mp_spmm_plan_size", "mp_spmm_plan_build", "mp_spmm_plan_free", "mp_spmm_workspace",
     "mp_spmm", "mp_hetero_build_workspace", "mp_hetero_build", "mp_hetero_spmm",
     "mp_validate_coo", "mp_validate_csr", "coo_to_csr", "Plan", "spmm", "hetero_build",
@@ -96,6 +98,10 @@ def lib():
         L.mp_validate_coo.argtypes = [p, p, i64, i64, i64, p, p]
         L.mp_validate_csr.argtypes = [p, i32, p, i64, i64, i64, p, p]
         L.mp_validate_sorted.argtypes = [p, i64, p, p]
+        L.mp_segment_matmul_workspace.argtypes = [i32, i64, i64, psz]
+        L.mp_segment_matmul.argtypes = [p, i32, p, p, i64, i64, p, i32, p, sz, p]
+        L.mp_segment_matmul_backward_workspace.argtypes = [p, i32, i64, i64, psz]
+        L.mp_segment_matmul_backward.argtypes = [p, i32, p, p, p, i64, i64, p, i32, p, p, sz, p]
         L.mp_spmm_multi_workspace.argtypes = [p, psz]
         L.mp_spmm_multi.argtypes = [p, p, i32, p, p, p, i32, i64, i64, i64, i32, p, p, sz, p]
         L.mp_readout_multi.argtypes = [p, p, i32, p, i32, i64, i64, i64, i32, p, p, sz, p]
@@ -110,6 +116,8 @@ def lib():
         for name in ("mp_coo_to_csr_workspace", "mp_coo_to_csr", "mp_sorted_coo_to_csr",
                      "mp_validate_sorted", "mp_csr_transpose_workspace", "mp_csr_transpose",
                      "mp_spmm_multi_workspace", "mp_spmm_multi", "mp_readout_multi",
+                     "mp_segment_matmul_workspace", "mp_segment_matmul",
+                     "mp_segment_matmul_backward_workspace", "mp_segment_matmul_backward",
                      "mp_spmm_backward_x_workspace", "mp_spmm_backward_x",
                      "mp_spmm_backward_w_workspace", "mp_spmm_backward_w", "mp_spmm_plan_size",
                      "mp_spmm_plan_build", "mp_spmm_workspace", "mp_spmm",
@@ -336,6 +344,32 @@ def mp_readout_multi(plan_handle, ptr, ptr_itype, x, x_dtype, N_nodes, N_seg, F,
         _ptr(ws), ws_bytes, _stream(stream)))
 
 
+def _seg_array(seg):
+    a = (ctypes.c_int64 * len(seg))(*[int(v) for v in seg])
+    return a
+
+
+def mp_segment_matmul_workspace(T, F, Fo) -> int:
+    return _bytes("mp_segment_matmul_workspace", T, F, Fo)
+
+
+def mp_segment_matmul(seg, T, x, W, F, Fo, out, out_dtype, ws, ws_bytes, stream=None):
+    _check("mp_segment_matmul", lib().mp_segment_matmul(
+        _seg_array(seg), T, _ptr(x), _ptr(W), F, Fo, _ptr(out), out_dtype, _ptr(ws), ws_bytes,
+        _stream(stream)))
+
+
+def mp_segment_matmul_backward_workspace(seg, T, F, Fo) -> int:
+    return _bytes("mp_segment_matmul_backward_workspace", _seg_array(seg), T, F, Fo)
+
+
+def mp_segment_matmul_backward(seg, T, x, W, dout, F, Fo, dx, dx_dtype, dW, ws, ws_bytes,
+                               stream=None):
+    _check("mp_segment_matmul_backward", lib().mp_segment_matmul_backward(
+        _seg_array(seg), T, _ptr(x), _ptr(W), _ptr(dout), F, Fo, _ptr(dx), dx_dtype, _ptr(dW),
+        _ptr(ws), ws_bytes, _stream(stream)))
+
+
 def mp_validate_sorted(dst, E, d_count, stream=None):
     _check("mp_validate_sorted", lib().mp_validate_sorted(_ptr(dst), E, _ptr(d_count),
                                                           _stream(stream)))
@@ -542,6 +576,31 @@ def readout(ptr, x, aggrs, *, plan: Plan | None = None, stream=None):
     mp_readout_multi(h, ptr, _itype_code(ptr.dtype), x, _dtype_code(x.dtype), N_nodes, N_seg, F,
                      outs, ws, 0 if ws is None else ws.numel(), stream)
     return res
+
+
+def segment_matmul(seg, x, W, *, out_dtype=torch.float32, stream=None):
+    """out[r] = x[r] @ W[t] for the rows of segment t (seg: host list of T+1
+    offsets; x [N, F] and W [T, F, Fo] bf16)."""
+    T, F, Fo = (int(v) for v in W.shape)
+    N = int(x.shape[0])
+    out = torch.empty(N, Fo, dtype=out_dtype, device=x.device)
+    ws = _workspace(mp_segment_matmul_workspace(T, F, Fo), x.device)
+    mp_segment_matmul(seg, T, x, W, F, Fo, out, _dtype_code(out_dtype), ws, ws.numel(), stream)
+    return out
+
+
+def segment_matmul_backward(seg, x, W, dout, *, dx_dtype=torch.float32, want_dx=True,
+                            want_dw=True, stream=None):
+    """Gradients of segment_matmul: (dx [N, F] or None, dW [T, F, Fo] fp32 or None)."""
+    T, F, Fo = (int(v) for v in W.shape)
+    N = int(dout.shape[0])
+    dx = torch.empty(N, F, dtype=dx_dtype, device=dout.device) if want_dx else None
+    dW = torch.empty(T, F, Fo, dtype=torch.float32, device=dout.device) if want_dw else None
+    ws = _workspace(mp_segment_matmul_backward_workspace(seg, T, F, Fo), dout.device) \
+        if want_dw else None
+    mp_segment_matmul_backward(seg, T, x, W, dout, F, Fo, dx, _dtype_code(dx_dtype), dW, ws,
+                               0 if ws is None else ws.numel(), stream)
+    return dx, dW
 
 
 def hetero_build(N_per_type, rels, dst_type, *, rowptr_dtype=torch.int32, stream=None):

@@ -299,6 +299,40 @@ int multi_impl(const mp_plan* plan, const void* rowptr, int rowptr_itype, const 
     return run_spmm(plan, P, g, x_dtype, N_dst, ws, ws_bytes, s);
 }
 
+// ---- segment matmul ------------------------------------------------------------
+
+constexpr int64_t kGmmRowsPerChunk = 2048;  // rows per partial of the weight gradient
+
+// Validate the host segment offsets; fill P.seg and return the row count.
+int gmm_segments(const int64_t* seg, int T, GmmParams& P, int64_t* N_rows) {
+    if (!seg) return MP_ERR_NULL;
+    if (T < 1 || T > MP_MAX_TYPES) return MP_ERR_SIZE;
+    if (seg[0] != 0) return MP_ERR_SIZE;
+    for (int t = 0; t < T; ++t)
+        if (seg[t + 1] < seg[t]) return MP_ERR_SIZE;
+    if (seg[T] > INT32_MAX) return MP_ERR_SIZE;
+    P.T = T;
+    for (int t = 0; t <= T; ++t) P.seg[t] = seg[t];
+    *N_rows = seg[T];
+    return MP_OK;
+}
+
+int gmm_dims(int64_t F, int64_t Fo) {
+    // 16-byte row chunks of bf16
+    if (F < 8 || Fo < 8 || F > 65536 || Fo > 65536 || F % 8 || Fo % 8) return MP_ERR_SIZE;
+    return MP_OK;
+}
+
+int64_t gmm_chunks(const int64_t* seg, int T, int64_t* off) {
+    int64_t c = 0;
+    for (int t = 0; t < T; ++t) {
+        off[t] = c;
+        c += ceil_div(seg[t + 1] - seg[t], kGmmRowsPerChunk);
+    }
+    off[T] = c;
+    return c;
+}
+
 }  // namespace
 
 extern "C" {
@@ -731,6 +765,129 @@ int mp_spmm_backward_w(const void* rowptr, int rowptr_itype, const int32_t* col,
     P.reduce = reduce;
     P.grad_w = grad_w;
     return hip_status(launch_spmm_grad_w(P, x_dtype, g_dtype, g.epl, s));
+}
+
+int mp_segment_matmul_workspace(int T, int64_t F, int64_t Fo, size_t* bytes) {
+    if (!bytes) return MP_ERR_NULL;
+    if (T < 1 || T > MP_MAX_TYPES) return MP_ERR_SIZE;
+    int st = gmm_dims(F, Fo);
+    if (st != MP_OK) return st;
+    *bytes = align_up((size_t)T * (size_t)F * (size_t)Fo * 2, 256);  // W transposed
+    return MP_OK;
+}
+
+int mp_segment_matmul(const int64_t* seg, int T, const void* x, const void* W, int64_t F,
+                      int64_t Fo, void* out, int out_dtype, void* ws, size_t ws_bytes,
+                      void* stream) {
+    if (!valid_dtype(out_dtype)) return MP_ERR_DTYPE;
+    GmmParams P{};
+    int64_t N = 0;
+    int st = gmm_segments(seg, T, P, &N);
+    if (st != MP_OK) return st;
+    st = gmm_dims(F, Fo);
+    if (st != MP_OK) return st;
+    if (!W || !ws || (N > 0 && (!x || !out))) return MP_ERR_NULL;
+    if ((uintptr_t)x % 16 || (uintptr_t)W % 16 || (uintptr_t)ws % 16 ||
+        (uintptr_t)out % (out_dtype == MP_BF16 ? 2 : 4))
+        return MP_ERR_ALIGN;
+    size_t need = 0;
+    mp_segment_matmul_workspace(T, F, Fo, &need);
+    if (ws_bytes < need) return MP_ERR_WORKSPACE;
+    hipStream_t s = as_stream(stream);
+    uint16_t* Wt = static_cast<uint16_t*>(ws);
+    if (launch_transpose_w(static_cast<const uint16_t*>(W), T, F, Fo, Wt, s) != hipSuccess)
+        return MP_ERR_HIP;
+    const int64_t ntn = ceil_div(Fo, gmm_tile_cols());
+    int64_t tiles = 0;
+    for (int t = 0; t < T; ++t) {
+        P.tile_off[t] = tiles;
+        tiles += ceil_div(seg[t + 1] - seg[t], gmm_tile_rows()) * ntn;
+    }
+    P.tile_off[T] = tiles;
+    P.A = static_cast<const uint16_t*>(x);
+    P.lda = F;
+    P.K = F;
+    P.B = Wt;
+    P.ldb = F;
+    P.b_stride = Fo * F;
+    P.N = Fo;
+    P.C = out;
+    P.ldc = Fo;
+    P.c_bf16 = out_dtype == MP_BF16;
+    return hip_status(launch_gmm_nt(P, tiles, s));
+}
+
+int mp_segment_matmul_backward_workspace(const int64_t* seg, int T, int64_t F, int64_t Fo,
+                                         size_t* bytes) {
+    if (!bytes) return MP_ERR_NULL;
+    GmmParams P{};
+    int64_t N = 0;
+    int st = gmm_segments(seg, T, P, &N);
+    if (st != MP_OK) return st;
+    st = gmm_dims(F, Fo);
+    if (st != MP_OK) return st;
+    int64_t off[MP_MAX_TYPES + 1];
+    const int64_t chunks = gmm_chunks(seg, T, off);
+    *bytes = align_up((size_t)(chunks > 0 ? chunks : 1) * (size_t)F * (size_t)Fo * 4, 256);
+    return MP_OK;
+}
+
+int mp_segment_matmul_backward(const int64_t* seg, int T, const void* x, const void* W,
+                               const void* dout, int64_t F, int64_t Fo, void* dx, int dx_dtype,
+                               float* dW, void* ws, size_t ws_bytes, void* stream) {
+    if (!valid_dtype(dx_dtype)) return MP_ERR_DTYPE;
+    GmmParams P{};
+    int64_t N = 0;
+    int st = gmm_segments(seg, T, P, &N);
+    if (st != MP_OK) return st;
+    st = gmm_dims(F, Fo);
+    if (st != MP_OK) return st;
+    if (!dx && !dW) return MP_ERR_NULL;
+    if (N > 0 && !dout) return MP_ERR_NULL;
+    if (dx && !W) return MP_ERR_NULL;
+    if (dW && (!ws || (N > 0 && !x))) return MP_ERR_NULL;
+    if ((uintptr_t)x % 16 || (uintptr_t)W % 16 || (uintptr_t)dout % 16 || (uintptr_t)ws % 16 ||
+        (uintptr_t)dx % (dx_dtype == MP_BF16 ? 2 : 4) || (uintptr_t)dW % 4)
+        return MP_ERR_ALIGN;
+    hipStream_t s = as_stream(stream);
+    if (dx && N > 0) {
+        // dX = dOut W^T: W[t] stored [F][Fo] is already the transposed operand
+        GmmParams Q = P;
+        const int64_t ntn = ceil_div(F, gmm_tile_cols());
+        int64_t tiles = 0;
+        for (int t = 0; t < T; ++t) {
+            Q.tile_off[t] = tiles;
+            tiles += ceil_div(seg[t + 1] - seg[t], gmm_tile_rows()) * ntn;
+        }
+        Q.tile_off[T] = tiles;
+        Q.A = static_cast<const uint16_t*>(dout);
+        Q.lda = Fo;
+        Q.K = Fo;
+        Q.B = static_cast<const uint16_t*>(W);
+        Q.ldb = Fo;
+        Q.b_stride = F * Fo;
+        Q.N = F;
+        Q.C = dx;
+        Q.ldc = F;
+        Q.c_bf16 = dx_dtype == MP_BF16;
+        if (launch_gmm_nt(Q, tiles, s) != hipSuccess) return MP_ERR_HIP;
+    }
+    if (dW) {
+        size_t need = 0;
+        mp_segment_matmul_backward_workspace(seg, T, F, Fo, &need);
+        if (ws_bytes < need) return MP_ERR_WORKSPACE;
+        const int64_t chunks = gmm_chunks(seg, T, P.tile_off);
+        P.A = static_cast<const uint16_t*>(x);
+        P.lda = F;
+        P.B = static_cast<const uint16_t*>(dout);
+        P.ldb = Fo;
+        P.M = F;
+        P.N = Fo;
+        P.part = static_cast<float*>(ws);
+        P.rows_per_chunk = kGmmRowsPerChunk;
+        if (launch_gmm_weight_grad(P, chunks, dW, s) != hipSuccess) return MP_ERR_HIP;
+    }
+    return MP_OK;
 }
 
 // ---- heterogeneous ----------------------------------------------------------

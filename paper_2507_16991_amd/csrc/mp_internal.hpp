@@ -195,6 +195,27 @@ hipError_t launch_scale_inv_deg(const void* g, int g_bf16, const void* rowptr, i
 hipError_t launch_spmm_grad_w(const GradWParams& p, int x_dtype, int g_dtype, int epl,
                               hipStream_t s);
 
+// ---- segment matmul (gmm.hip) --------------------------------------------------
+struct GmmParams {
+    const uint16_t* A;  // bf16 rows of the left operand
+    const uint16_t* B;  // bf16: per segment Bt[t] = B + t * b_stride (gmm_nt), or G (weight grad)
+    void* C;            // output (gmm_nt)
+    float* part;        // fp32 partial tiles (weight grad)
+    int64_t lda, ldb, ldc, b_stride;
+    int64_t M, N, K;    // gmm_nt: N columns, K inner; weight grad: M x N = F x Fo
+    int T;
+    int64_t seg[MP_MAX_TYPES + 1];       // row offsets of the segments
+    int64_t tile_off[MP_MAX_TYPES + 1];  // first tile (gmm_nt) or chunk (weight grad) of each
+    int64_t rows_per_chunk;
+    int c_bf16;
+};
+hipError_t launch_gmm_nt(const GmmParams& p, int64_t tiles, hipStream_t s);
+hipError_t launch_gmm_weight_grad(const GmmParams& p, int64_t chunks, float* dW, hipStream_t s);
+hipError_t launch_transpose_w(const uint16_t* W, int64_t T, int64_t F, int64_t Fo, uint16_t* Wt,
+                              hipStream_t s);
+int64_t gmm_tile_rows();
+int64_t gmm_tile_cols();
+
 hipError_t launch_spmm(const SpmmParams& p, int x_dtype, int epl, hipStream_t s);
 hipError_t launch_spmm_tiny(const SpmmParams& p, int x_dtype, int epl, hipStream_t s);
 hipError_t launch_plan_rowrange(const void* rowptr, int rp64, const int32_t* rowlist, int64_t N,

@@ -233,6 +233,39 @@ def test_multi_errors():
     assert L.mp_readout_multi(None, None, 0, FAKE, 0, 100, 10, 8, 1, arr, None, 0, None) == -1
 
 
+def test_segment_matmul_errors_and_sizes():
+    L = mp.lib()
+    nb = ctypes.c_size_t(0)
+    assert L.mp_segment_matmul_workspace(3, 128, 64, ctypes.byref(nb)) == 0
+    assert nb.value == 3 * 128 * 64 * 2
+    seg = (ctypes.c_int64 * 4)(0, 5000, 5000, 7000)
+    assert L.mp_segment_matmul_backward_workspace(seg, 3, 64, 32, ctypes.byref(nb)) == 0
+    assert nb.value == 4 * 64 * 32 * 4  # chunks of 2048 rows: 3 + 0 + 1
+    assert L.mp_segment_matmul_workspace(0, 128, 64, ctypes.byref(nb)) == -2
+    assert L.mp_segment_matmul_workspace(2, 12, 64, ctypes.byref(nb)) == -2
+
+    def fwd(seg_vals, T=None, F=16, Fo=16, x=FAKE, ws_bytes=1 << 20, out_dtype=0):
+        sg = (ctypes.c_int64 * len(seg_vals))(*seg_vals)
+        T = len(seg_vals) - 1 if T is None else T
+        return L.mp_segment_matmul(sg, T, x, FAKE, F, Fo, FAKE, out_dtype, FAKE, ws_bytes, None)
+
+    assert fwd([1, 10]) == -2          # seg[0] != 0
+    assert fwd([0, 10, 5]) == -2       # decreasing
+    assert fwd([0, 10], T=17) == -2
+    assert fwd([0, 10], F=20) == -2    # F not a multiple of 8
+    assert fwd([0, 10], x=FAKE + 8) == -8
+    assert fwd([0, 10], ws_bytes=16) == -5
+    assert fwd([0, 10], out_dtype=4) == -3
+    sg = (ctypes.c_int64 * 2)(0, 10)
+    assert L.mp_segment_matmul(None, 1, FAKE, FAKE, 16, 16, FAKE, 0, FAKE, 1 << 20, None) == -1
+    assert L.mp_segment_matmul_backward(sg, 1, FAKE, FAKE, FAKE, 16, 16, None, 0, None, FAKE,
+                                        1 << 20, None) == -1  # nothing requested
+    assert L.mp_segment_matmul_backward(sg, 1, FAKE, None, FAKE, 16, 16, FAKE, 0, None, FAKE,
+                                        1 << 20, None) == -1  # dx needs W
+    assert L.mp_segment_matmul_backward(sg, 1, FAKE, FAKE, FAKE, 16, 16, None, 0, FAKE, FAKE,
+                                        16, None) == -5
+
+
 def test_validate_errors():
     L = mp.lib()
     assert L.mp_validate_sorted(FAKE, 10, None, None) == -1
