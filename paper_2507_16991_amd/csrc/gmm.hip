@@ -84,8 +84,8 @@ __device__ inline void store_tile(const f32x16 (&acc)[2][2], int64_t r0, int64_t
 
 // C[r, n] = sum_k A[r, k] Bt[t][n, k] for the rows of segment t.
 __global__ __launch_bounds__(kThreads) void gmm_nt(GmmParams P) {
-    __shared__ uint16_t As[kBM][kLds];
-    __shared__ uint16_t Bs[kBN][kLds];
+    __shared__ __attribute__((aligned(16))) uint16_t As[kBM][kLds];  // rows of 80 B: 16-B reads
+    __shared__ __attribute__((aligned(16))) uint16_t Bs[kBN][kLds];
     const int64_t tile = blockIdx.x;
     int t = 0;
     while (t + 1 < P.T && P.tile_off[t + 1] <= tile) ++t;
@@ -138,8 +138,8 @@ __global__ __launch_bounds__(kThreads) void gmm_nt(GmmParams P) {
 // Both operands are read row by row and written to LDS transposed, so that
 // the MFMA fragments (contiguous in the row index k) are 16-byte reads.
 __global__ __launch_bounds__(kThreads) void gmm_tn_partial(GmmParams P) {
-    __shared__ uint16_t As[kBM][kLds];
-    __shared__ uint16_t Bs[kBN][kLds];
+    __shared__ __attribute__((aligned(16))) uint16_t As[kBM][kLds];  // rows of 80 B: 16-B reads
+    __shared__ __attribute__((aligned(16))) uint16_t Bs[kBN][kLds];
     const int64_t tile = blockIdx.x;
     const int64_t ntm = (P.M + kBM - 1) / kBM, ntn = (P.N + kBN - 1) / kBN;
     const int64_t chunk = tile / (ntm * ntn);
