@@ -39,6 +39,7 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 WORKLOAD = "chunglu-124M"
 BACKWARD = "chunglu-124M-backward"
 STACKED = "chunglu-124M-stacked"
+PROJECTION = "hetero-20M-projection"
 READOUT = "readout-2.4M"
 DOMINANT = "spmm_main<float, 4, true, false, 1, false, false>"  # fp32 sum, the largest launch of a step
 DOMINANT_SRC = ["paper_2507_16991_amd/csrc/spmm.hip", "paper_2507_16991_amd/csrc/mp_internal.hpp"]
@@ -150,6 +151,8 @@ def build_step(args, mp, torch, np, dev):
     import graphgen
 
     t0 = time.time()
+    if args.workload == PROJECTION:
+        return projection_step(args, mp, torch, np, dev)
     if args.workload == BACKWARD:
         g = graphgen.workload(WORKLOAD, seed=args.seed, bf16=False)
     elif args.workload in (STACKED, READOUT):
@@ -435,7 +438,63 @@ def readout_step(g, mp, torch, np, dev, mark, seed):
     return SimpleNamespace(n_dst=B, n_src=N, E=N, F=F), step, ops
 
 
+def projection_step(args, mp, torch, np, dev):
+    """Typed projections {H_T W_T} of the typed graph's node tables (1.9M,
+    736k, 8.7k rows; F = F' = 128; bf16 x, W and output gradient, N(0,1),
+    W scaled by 1/sqrt(F)): forward (fp32 out), input gradient (fp32) and
+    weight gradient (fp32), as one training step of the projection."""
+    import graphgen
+    from types import SimpleNamespace
+
+    sizes = [1_900_000, 736_000, 8_700]
+    F = Fo = 128
+    T = len(sizes)
+    seg = [0] + [int(v) for v in np.cumsum(sizes)]
+    N = seg[-1]
+    t0 = time.time()
+    bf = lambda a: torch.from_numpy(graphgen.f32_to_bf16(a).view(np.int16)).to(dev).view(
+        torch.bfloat16)
+    x = bf(graphgen.normal_f32(args.seed, 3, N * F).reshape(N, F))
+    W = bf((graphgen.normal_f32(args.seed, 5, T * F * Fo) / np.sqrt(F)).astype(np.float32)
+           .reshape(T, F, Fo))
+    dout = bf(graphgen.normal_f32(args.seed, 11, N * Fo).reshape(N, Fo))
+    print(f"[bench] generated projection inputs in {time.time() - t0:.1f}s", file=sys.stderr,
+          flush=True)
+    out = torch.empty(N, Fo, dtype=torch.float32, device=dev)
+    dx = torch.empty(N, F, dtype=torch.float32, device=dev)
+    dW = torch.empty(T, F, Fo, dtype=torch.float32, device=dev)
+    ws_f = torch.empty(mp.mp_segment_matmul_workspace(T, F, Fo), dtype=torch.uint8, device=dev)
+    nb = mp.mp_segment_matmul_backward_workspace(seg, T, F, Fo)
+    ws_b = torch.empty(nb, dtype=torch.uint8, device=dev)
+    chunks = nb // (F * Fo * 4)
+    wb = T * F * Fo * 2
+    ops = [("proj_fwd", 2 * N * F + 2 * wb + 4 * N * Fo, 0),
+           ("proj_dx", 2 * N * Fo + wb + 4 * N * F, 0),
+           ("proj_dw", 2 * N * F + 2 * N * Fo + 2 * chunks * F * Fo * 4 + T * F * Fo * 4, 0)]
+    flops = 2 * N * F * Fo
+
+    def step(evs=None):
+        stream = torch.cuda.current_stream()
+        if evs is not None:
+            evs[0].record(stream)
+        mp.mp_segment_matmul(seg, T, x, W, F, Fo, out, mp.MP_F32, ws_f, ws_f.numel())
+        if evs is not None:
+            evs[1].record(stream)
+        mp.mp_segment_matmul_backward(seg, T, x, W, dout, F, Fo, dx, mp.MP_F32, None, None, 0)
+        if evs is not None:
+            evs[2].record(stream)
+        mp.mp_segment_matmul_backward(seg, T, x, W, dout, F, Fo, None, mp.MP_F32, dW, ws_b,
+                                      ws_b.numel())
+        if evs is not None:
+            evs[3].record(stream)
+
+    return SimpleNamespace(n_dst=N, n_src=N, E=0, F=F, flops_per_op=flops), step, ops
+
+
 OP_KERNELS = {
+    "proj_fwd": "gmm_nt (bf16 MFMA 32x32x16, fp32 out)",
+    "proj_dx": "gmm_nt (bf16 MFMA 32x32x16, fp32 out)",
+    "proj_dw": "gmm_tn_partial + reduce_partials (bf16 MFMA 32x32x16)",
     "stacked_f32": "spmm_main, stats mode (mean, min, max, std from one gather)",
     "stacked_bf16": "spmm_main, stats mode (mean, min, max, std from one gather)",
     "readout_f32": "spmm_main, stats mode over consecutive node rows (readout)",
@@ -492,10 +551,14 @@ def run(args):
     breakdown = {n: {"ms": round(op_ms[n], 4),
                      "GB_per_s": round(op_bytes[n] / (op_ms[n] * 1e-3) / 1e9, 1)}
                  for n in names}
+    if getattr(g, "flops_per_op", 0):
+        for n in names:  # every projection op is 2 N F F' flops
+            breakdown[n]["TFLOP_per_s"] = round(g.flops_per_op / (op_ms[n] * 1e-3) / 1e12, 1)
     value = step_bytes / (ms_step * 1e-3) / 1e9
     web = args.workload == "web-1.6B"
     headline = args.workload == WORKLOAD
-    dom = max((o for o in ops if o[2] > 0), key=lambda o: op_ms[o[0]])[0]
+    dom = max((o for o in ops if o[2] > 0 or args.workload == PROJECTION),
+              key=lambda o: op_ms[o[0]])[0]
     dom_kernel = DOMINANT + ", fp32 sum" if headline else OP_KERNELS.get(dom, f"spmm_main ({dom})")
     if headline:
         dom = "sum_f32"
@@ -514,6 +577,9 @@ def run(args):
                           "COO->CSR (+perm, weights to CSR order) + plan + mean + weighted sum"),
         "uniform-10k": (f"uniform-10k: uniform random graph, N={N}, E={E}, F={F}, fp32 U(-1,1), "
                         f"seed {args.seed}", "COO->CSR + plan + sum"),
+        PROJECTION: (f"{PROJECTION}: typed projections of the node tables of hetero-20M "
+                     f"(1.9M, 736k, 8.7k rows), F = F' = {F}, bf16 inputs, seed {args.seed}",
+                     "segment matmul forward + input gradient + weight gradient"),
         STACKED: (f"{STACKED}: the Chung-Lu graph of {WORKLOAD} (N={N}, E={E}, F={F}, fp32 and "
                   f"bf16 N(0,1) features), seed {args.seed}",
                   "COO->CSR + plan + stacked {mean, min, max, std} x {fp32, bf16 features}"),
@@ -701,8 +767,8 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--workload", default=WORKLOAD,
-                    choices=[WORKLOAD, BACKWARD, STACKED, READOUT, "web-1.6B", "powerlaw-1.2M",
-                             "uniform-10k", "hetero-20M"],
+                    choices=[WORKLOAD, BACKWARD, STACKED, READOUT, PROJECTION, "web-1.6B",
+                             "powerlaw-1.2M", "uniform-10k", "hetero-20M"],
                     help="benchmark workload (the default is the metric's configuration)")
     ap.add_argument("--cpu-rows", type=int, default=0,
                     help="rows of the CPU-oracle aggregation sample (0: all rows)")
