@@ -11,7 +11,7 @@
 //     64 x 64 (2 x 2 MFMA tiles each).  A tile never spans two segments.
 //   * gmm_tn_partial + reduce_partials: the weight gradient dW[t] =
 //     X_t^T dOut_t, a reduction over the segment's rows: fixed chunks of rows
-//     give fp32 partial tiles that a second kernel adds in chunk order (no
+//     give fp32 partial tiles that a second kernel adds in a fixed order (no
 //     atomics, deterministic).
 //
 // MFMA operand layout (32x32x16 bf16, wave64): lane l holds A[l % 32][8 (l/32)
@@ -135,11 +135,40 @@ __global__ __launch_bounds__(kThreads) void gmm_nt(GmmParams P) {
 
 // Partial weight gradient of one chunk of rows of segment t:
 // Part[chunk][m, n] = sum over the chunk's rows r of X[r, m] * G[r, n].
-// Both operands are read row by row and written to LDS transposed, so that
-// the MFMA fragments (contiguous in the row index k) are 16-byte reads.
+// The reduction index k is the row r, so the operand tiles are kept in LDS
+// in their natural row-major layout, [k][m] and [k][n], written with 8-byte
+// stores; a fragment (eight consecutive k at one m) is then gathered with
+// eight 2-byte reads.  Rows of kTnLds bf16 (264 B) put rows k and k + 8 on
+// different banks, so the two halves of a wavefront do not collide.
+constexpr int kTnLds = kBM + 4;
+
+__device__ inline void mma_step_tn(const uint16_t (*As)[kTnLds], const uint16_t (*Bs)[kTnLds],
+                                   int wm, int wn, int lane, f32x16 (&acc)[2][2]) {
+#pragma unroll
+    for (int s = 0; s < kBK / 16; ++s) {
+        const int kk = s * 16 + 8 * (lane >> 5);
+        bf16x8 a[2], b[2];
+#pragma unroll
+        for (int i = 0; i < 2; ++i) {
+            const int m = wm * 64 + i * 32 + (lane & 31);
+            const int n = wn * 64 + i * 32 + (lane & 31);
+#pragma unroll
+            for (int j = 0; j < 8; ++j) {
+                a[i][j] = __builtin_bit_cast(__bf16, As[kk + j][m]);
+                b[i][j] = __builtin_bit_cast(__bf16, Bs[kk + j][n]);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < 2; ++i)
+#pragma unroll
+            for (int j = 0; j < 2; ++j)
+                acc[i][j] = __builtin_amdgcn_mfma_f32_32x32x16_bf16(a[i], b[j], acc[i][j], 0, 0, 0);
+    }
+}
+
 __global__ __launch_bounds__(kThreads) void gmm_tn_partial(GmmParams P) {
-    __shared__ __attribute__((aligned(16))) uint16_t As[kBM][kLds];  // rows of 80 B: 16-B reads
-    __shared__ __attribute__((aligned(16))) uint16_t Bs[kBN][kLds];
+    __shared__ __attribute__((aligned(16))) uint16_t As[kBK][kTnLds];
+    __shared__ __attribute__((aligned(16))) uint16_t Bs[kBK][kTnLds];
     const int64_t tile = blockIdx.x;
     const int64_t ntm = (P.M + kBM - 1) / kBM, ntn = (P.N + kBN - 1) / kBN;
     const int64_t chunk = tile / (ntm * ntn);
@@ -179,33 +208,40 @@ __global__ __launch_bounds__(kThreads) void gmm_tn_partial(GmmParams P) {
         for (int q = 0; q < 2; ++q) {
             const int c = tid + kThreads * q;
             const int kr = c >> 4, mc = (c & 15) * 8;
-            const uint32_t av[4] = {ra[q].x, ra[q].y, ra[q].z, ra[q].w};
-            const uint32_t bv[4] = {rb[q].x, rb[q].y, rb[q].z, rb[q].w};
-#pragma unroll
-            for (int e = 0; e < 4; ++e) {
-                As[mc + 2 * e][kr] = (uint16_t)(av[e] & 0xFFFFu);
-                As[mc + 2 * e + 1][kr] = (uint16_t)(av[e] >> 16);
-                Bs[mc + 2 * e][kr] = (uint16_t)(bv[e] & 0xFFFFu);
-                Bs[mc + 2 * e + 1][kr] = (uint16_t)(bv[e] >> 16);
-            }
+            uint2* pa = reinterpret_cast<uint2*>(&As[kr][mc]);
+            uint2* pb = reinterpret_cast<uint2*>(&Bs[kr][mc]);
+            pa[0] = make_uint2(ra[q].x, ra[q].y);
+            pa[1] = make_uint2(ra[q].z, ra[q].w);
+            pb[0] = make_uint2(rb[q].x, rb[q].y);
+            pb[1] = make_uint2(rb[q].z, rb[q].w);
         }
         __syncthreads();
-        mma_step(As, Bs, wm, wn, lane, acc);
+        mma_step_tn(As, Bs, wm, wn, lane, acc);
     }
     float* part = P.part + chunk * P.M * P.N;
     store_tile(acc, m0, P.M, n0, P.N, wm, wn, lane, part, P.N, 0);
 }
 
-// dW[t][i] = sum over the chunks of segment t, in order, of Part[chunk][i].
+// dW[t][i] = sum over the chunks of segment t of Part[chunk][i], in a fixed
+// order: eight running sums over chunks c = 8q + s, then a fixed tree.  Eight
+// independent loads per iteration keep the long sums from waiting on each
+// load in turn.
 __global__ __launch_bounds__(256) void reduce_partials(GmmParams P, float* __restrict__ dW) {
     const int64_t mn = P.M * P.N;
     const int64_t g = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (g >= (int64_t)P.T * mn) return;
     const int t = (int)(g / mn);
     const int64_t i = g - (int64_t)t * mn;
-    float s = 0.f;
-    for (int64_t c = P.tile_off[t]; c < P.tile_off[t + 1]; ++c) s += P.part[c * mn + i];
-    dW[g] = s;
+    const int64_t c0 = P.tile_off[t], c1 = P.tile_off[t + 1];
+    float s[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+    for (int64_t c = c0; c < c1; c += 8) {
+        float v[8];
+#pragma unroll
+        for (int u = 0; u < 8; ++u) v[u] = c + u < c1 ? P.part[(c + u) * mn + i] : 0.f;
+#pragma unroll
+        for (int u = 0; u < 8; ++u) s[u] += v[u];
+    }
+    dW[g] = ((s[0] + s[1]) + (s[2] + s[3])) + ((s[4] + s[5]) + (s[6] + s[7]));
 }
 
 // Wt[t][o][f] = W[t][f][o] (bf16).
