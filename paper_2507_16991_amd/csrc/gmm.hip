@@ -107,8 +107,10 @@ __global__ __launch_bounds__(kThreads) void gmm_nt(GmmParams P) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    for (int64_t k0 = 0; k0 < P.K; k0 += kBK) {
-        uint4 ra[2], rb[2];
+    // the next K step's tiles are loaded into registers while this one's
+    // products run
+    uint4 ra[2], rb[2];
+    auto load = [&](int64_t k0) {
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
             const int c = tid + kThreads * q;  // 512 chunks of 8 bf16 per tile
@@ -119,6 +121,9 @@ __global__ __launch_bounds__(kThreads) void gmm_nt(GmmParams P) {
             if (gr < row_end && gk < P.K) ra[q] = *reinterpret_cast<const uint4*>(A + gr * P.lda + gk);
             if (gn < P.N && gk < P.K) rb[q] = *reinterpret_cast<const uint4*>(Bt + gn * P.ldb + gk);
         }
+    };
+    load(0);
+    for (int64_t k0 = 0; k0 < P.K; k0 += kBK) {
         __syncthreads();  // the previous step's reads of As/Bs are done
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
@@ -128,6 +133,7 @@ __global__ __launch_bounds__(kThreads) void gmm_nt(GmmParams P) {
             *reinterpret_cast<uint4*>(&Bs[row][kc]) = rb[q];
         }
         __syncthreads();
+        if (k0 + kBK < P.K) load(k0 + kBK);
         mma_step(As, Bs, wm, wn, lane, acc);
     }
     store_tile(acc, r0, row_end, n0, P.N, wm, wn, lane, P.C, P.ldc, P.c_bf16);
@@ -191,8 +197,8 @@ __global__ __launch_bounds__(kThreads) void gmm_tn_partial(GmmParams P) {
 #pragma unroll
             for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
 
-    for (int64_t k0 = r_begin; k0 < r_end; k0 += kBK) {
-        uint4 ra[2], rb[2];
+    uint4 ra[2], rb[2];
+    auto load = [&](int64_t k0) {
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
             const int c = tid + kThreads * q;  // 32 rows x 16 chunks of 8 bf16
@@ -203,6 +209,9 @@ __global__ __launch_bounds__(kThreads) void gmm_tn_partial(GmmParams P) {
             if (gr < r_end && m0 + mc < P.M) ra[q] = *reinterpret_cast<const uint4*>(P.A + gr * P.lda + m0 + mc);
             if (gr < r_end && n0 + mc < P.N) rb[q] = *reinterpret_cast<const uint4*>(P.B + gr * P.ldb + n0 + mc);
         }
+    };
+    load(r_begin);
+    for (int64_t k0 = r_begin; k0 < r_end; k0 += kBK) {
         __syncthreads();
 #pragma unroll
         for (int q = 0; q < 2; ++q) {
@@ -216,6 +225,7 @@ __global__ __launch_bounds__(kThreads) void gmm_tn_partial(GmmParams P) {
             pb[1] = make_uint2(rb[q].z, rb[q].w);
         }
         __syncthreads();
+        if (k0 + kBK < r_end) load(k0 + kBK);  // in flight during the products
         mma_step_tn(As, Bs, wm, wn, lane, acc);
     }
     float* part = P.part + chunk * P.M * P.N;
