@@ -41,8 +41,12 @@ BACKWARD = "chunglu-124M-backward"
 STACKED = "chunglu-124M-stacked"
 PROJECTION = "hetero-20M-projection"
 READOUT = "readout-2.4M"
-DOMINANT = "spmm_main<float, 4, true, false, 1, false, false>"  # fp32 sum, the largest launch of a step
-DOMINANT_SRC = ["paper_2507_16991_amd/csrc/spmm.hip", "paper_2507_16991_amd/csrc/mp_internal.hpp"]
+DOMINANT = "spmm_main<float, 4, true, false, 1, false, 0>"  # fp32 sum, the largest launch of a step
+# the dominant kernel's source: spmm.hip and the aggregation section of the
+# internal header (file, first line marker or None, end marker or None)
+DOMINANT_SRC = [("paper_2507_16991_amd/csrc/spmm.hip", None, None),
+                ("paper_2507_16991_amd/csrc/mp_internal.hpp", "// ---- aggregation (spmm.hip)",
+                 "// ---- backward (backward.hip)")]
 COUNTER_SUMMARY = os.path.join(ROOT, "profiles", "spmm_main_f32_sum_chunglu124M_counters.txt")
 CALIB_BYTES = 1 << 30  # plain copy used to scale the HBM counters
 
@@ -103,11 +107,18 @@ def plan_bytes(N):
     return 4 * (N + 1) + 4 * N + 4 * (N + 1)
 
 
-def source_digest(paths):
+def source_digest(parts):
+    """SHA-1 of the listed source text: whole files, or the lines of a file
+    from a start marker up to (not including) an end marker."""
     h = hashlib.sha1()
-    for p in paths:
-        with open(os.path.join(ROOT, p), "rb") as f:
-            h.update(f.read())
+    for path, start, end in parts:
+        with open(os.path.join(ROOT, path), "rb") as f:
+            text = f.read()
+        if start is not None:
+            text = text[text.index(start.encode()):]
+        if end is not None:
+            text = text[:text.index(end.encode())]
+        h.update(text)
     return h.hexdigest()
 
 
@@ -621,6 +632,7 @@ def run(args):
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": None if traffic is None else round(traffic / (dom_ms * 1e-3) / 1e9, 1),
+            "traffic_bytes_per_launch": None if traffic is None else int(traffic),
             "algorithmic_bytes_per_launch": dom_bytes,
             "avg_launch_ms": round(dom_ms, 4),
         },
