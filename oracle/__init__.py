@@ -71,6 +71,16 @@ def _L():
         lib.oracle_spmm_backward_w.argtypes = [i64, p, i64, i64, p, p, p, i32, p, i32, i64, i32,
                                                p, p, p, i32]
         lib.oracle_spmm_backward_w.restype = i32
+        lib.oracle_message_gather.argtypes = [i64, i64, p, p, p, i32, i64, p]
+        lib.oracle_message_gather.restype = i32
+        lib.oracle_message_scale.argtypes = [i64, i64, p, p, p, i64, p]
+        lib.oracle_message_scale.restype = i32
+        lib.oracle_message_backward.argtypes = [i64, p, p, i32, i64, i32, p, p]
+        lib.oracle_message_backward.restype = i32
+        lib.oracle_edge_dot.argtypes = [i64, i64, p, i32, p, i32, p, i64, p, p, p]
+        lib.oracle_edge_dot.restype = i32
+        lib.oracle_message_backward_x.argtypes = [i64, i64, p, p, p, i64, p, p]
+        lib.oracle_message_backward_x.restype = i32
         _lib = lib
     return _lib
 
@@ -351,3 +361,103 @@ def segment_matmul_backward(seg, x_bf16, w_bf16, dout_bf16):
     if rc != 0:
         raise ValueError(f"oracle_segment_matmul_backward failed ({rc})")
     return dx, dxs, dw, dws
+
+
+# ---- edge-materialized messages (explanation mode) ------------------------------------
+
+def message_gather(idx, x=None, x_bf16=None, w=None):
+    """Materialized messages msg[p] = x[idx[p]] (or fl32(w[p] * x[idx[p]])),
+    fp32 [E, F]; with idx = the CSR columns, row p is the message of CSR edge p."""
+    idx = _c(idx, np.int32)
+    xa, isb, n_src, F = _x_args(x, x_bf16)
+    E = idx.shape[0]
+    w = _c(w, np.float32)
+    msg = np.empty((E, F), np.float32)
+    rc = _L().oracle_message_gather(E, n_src, _p(idx), _p(w), _p(xa), isb, F, _p(msg))
+    if rc != 0:
+        raise ValueError(f"oracle_message_gather failed ({rc})")
+    return msg
+
+
+def message_scale(msg, mask, idx=None):
+    """The edge-mask callback: out[p] = fl32(msg[p] * mask[idx[p]]) (idx None:
+    mask[p]).  Returns a new fp32 [E, F] array."""
+    msg = _c(msg, np.float32)
+    mask = _c(mask, np.float32)
+    idx = _c(idx, np.int32)
+    E, F = msg.shape
+    out = np.empty_like(msg)
+    rc = _L().oracle_message_scale(E, F, _p(msg), _p(mask), _p(idx), mask.shape[0], _p(out))
+    if rc != 0:
+        raise ValueError(f"oracle_message_scale failed ({rc})")
+    return out
+
+
+def aggregate_messages(rowptr, msg=None, msg_bf16=None, rows=None, nthreads=None,
+                       want=("sum", "mean", "max", "scale")):
+    """Aggregation of materialized messages: row v reduces the message rows
+    rowptr[v] .. rowptr[v+1] - 1 (the aggregation of ``spmm`` with column p at
+    position p, so argmax is a message row)."""
+    rowptr = _c(rowptr, np.int64)
+    E = int(rowptr[-1])
+    ident = np.arange(E, dtype=np.int32)
+    return spmm(rowptr, ident, x=msg, x_bf16=msg_bf16, rows=rows, nthreads=nthreads, want=want)
+
+
+def spmm_materialized(rowptr, col, x=None, x_bf16=None, w=None, callback=None,
+                      want=("sum", "mean", "max", "scale")):
+    """Explanation-mode aggregation: materialize the messages, apply the
+    callback c (a function of the fp32 [E, F] message table returning one of
+    the same shape; None: identity), aggregate.  Returns (aggregates, msg)."""
+    msg = message_gather(col, x=x, x_bf16=x_bf16, w=w)
+    if callback is not None:
+        msg = np.ascontiguousarray(callback(msg), dtype=np.float32)
+    return aggregate_messages(rowptr, msg, want=want), msg
+
+
+def message_backward(rowptr, reduce, g=None, g_bf16=None, argout=None):
+    """dL/dmsg [E, F] fp32 of the aggregation of materialized messages, given
+    g = dL/d out (fp32, or g_bf16 bits) and, for max, the forward argout."""
+    rowptr = _c(rowptr, np.int64)
+    ga, gisb, F = _g_args(g, g_bf16)
+    n_dst = rowptr.shape[0] - 1
+    E = int(rowptr[-1])
+    am = _c(argout, np.int64)
+    dmsg = np.empty((E, F), np.float32)
+    rc = _L().oracle_message_backward(n_dst, _p(rowptr), _p(ga), gisb, F, REDUCE_CODES[reduce],
+                                      _p(am), _p(dmsg))
+    if rc != 0:
+        raise ValueError(f"oracle_message_backward failed ({rc})")
+    return dmsg
+
+
+def edge_dot(a=None, a_bf16=None, b=None, b_bf16=None, bidx=None, oidx=None):
+    """out[oidx[p]] = sum_f a[p, f] * b[bidx[p], f] (fp64; None indices are
+    the identity).  Returns (out [E], scale [E])."""
+    aa, aisb, E, F = _x_args(a, a_bf16)
+    ba, bisb, n_b, Fb = _x_args(b, b_bf16)
+    if Fb != F:
+        raise ValueError("a and b widths differ")
+    bidx, oidx = _c(bidx, np.int32), _c(oidx, np.int32)
+    out = np.empty(E, np.float64)
+    sc = np.empty(E, np.float64)
+    rc = _L().oracle_edge_dot(E, F, _p(aa), aisb, _p(ba), bisb, _p(bidx), n_b, _p(oidx),
+                              _p(out), _p(sc))
+    if rc != 0:
+        raise ValueError(f"oracle_edge_dot failed ({rc})")
+    return out, sc
+
+
+def message_backward_x(col, n_src, dmsg, w=None):
+    """dL/dx [N_src, F] fp64 of the messages w[p] * x[col[p]] given dL/dmsg,
+    summed per source in CSR order.  Returns (gx, scale)."""
+    col = _c(col, np.int32)
+    dmsg = _c(dmsg, np.float32)
+    w = _c(w, np.float32)
+    E, F = dmsg.shape
+    gx = np.empty((n_src, F), np.float64)
+    sc = np.empty((n_src, F), np.float64)
+    rc = _L().oracle_message_backward_x(E, n_src, _p(col), _p(w), _p(dmsg), F, _p(gx), _p(sc))
+    if rc != 0:
+        raise ValueError(f"oracle_message_backward_x failed ({rc})")
+    return gx, sc

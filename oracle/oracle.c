@@ -51,6 +51,11 @@
  * weighted message is not differentiated (the message is taken as w * x).
  * The max routes each output element's gradient to the one edge the forward
  * pass reported for it (argmax), and nowhere for an empty row.
+ *
+ * Explanation mode (Sec. 2.4, with the PyG 1 materialization recalled in
+ * Sec. 2.2): messages materialized as an E x F table, edited by a callback c,
+ * then aggregated; and the gradients of that pipeline (with respect to each
+ * message, to x, and to a per-edge factor such as an edge mask).
  */
 #include <math.h>
 #include <stdint.h>
@@ -659,6 +664,134 @@ int oracle_segment_matmul_backward(int T, const int64_t* seg, const uint16_t* X,
                 dW[(int64_t)t * F * Fo + i] = s;
                 if (dw_scale) dw_scale[(int64_t)t * F * Fo + i] = a;
             }
+        }
+    }
+    return 0;
+}
+
+/* ---- edge-materialized messages (explanation mode) ---------------------- */
+/*
+ * Sec. 2.2 recalls that the first PyG materialized every message in edge
+ * space and then aggregated it into node space; in explanation mode (Sec. 2.4)
+ * message passing returns to that materialization so that a callback c, a
+ * map from the E x F messages to E x F messages, can edit every message
+ * before the aggregation:  h_v' = f(h_v, AGG{ c(g(h_w, e_wv, h_v)) }).
+ * Messages are kept in destination-major CSR order: row p holds the message
+ * of CSR edge p, so aggregating materialized messages is the aggregation of
+ * oracle_spmm over the rows of the message table with column p at position p.
+ */
+
+/* msg[p, f] = x[idx[p], f], or fl32(w[p] * x[idx[p], f]) when w is given
+ * (the same message as oracle_spmm).  idx is any int32 index array of length
+ * E into the N_src rows of x (the CSR columns give the sources' features).
+ * Returns 0, or -1 for an index out of range. */
+int oracle_message_gather(int64_t E, int64_t N_src, const int32_t* idx, const float* w,
+                          const void* x, int x_is_bf16, int64_t F, float* msg) {
+    for (int64_t p = 0; p < E; ++p)
+        if (idx[p] < 0 || idx[p] >= N_src) return -1;
+    for (int64_t p = 0; p < E; ++p)
+        for (int64_t f = 0; f < F; ++f)
+            msg[p * F + f] = message(x, x_is_bf16, F, idx[p], f, w, p);
+    return 0;
+}
+
+/* The edge-mask callback (a per-edge weight on every incoming message):
+ * out[p, f] = fl32(msg[p, f] * mask[j]) with j = idx[p] (idx NULL: j = p),
+ * one correctly rounded fp32 product.  out may equal msg.  Returns 0, or -1
+ * for an index out of range. */
+int oracle_message_scale(int64_t E, int64_t F, const float* msg, const float* mask,
+                         const int32_t* idx, int64_t n_mask, float* out) {
+    for (int64_t p = 0; p < E; ++p) {
+        int64_t j = idx ? idx[p] : p;
+        if (j < 0 || j >= n_mask) return -1;
+    }
+    for (int64_t p = 0; p < E; ++p) {
+        double s = (double)mask[idx ? idx[p] : p];
+        for (int64_t f = 0; f < F; ++f) out[p * F + f] = (float)((double)msg[p * F + f] * s);
+    }
+    return 0;
+}
+
+/* Gradient of the aggregation of materialized messages with respect to each
+ * message, given g = dL/d out [N_dst, F] (fp32 or bf16 bits), for the CSR
+ * edge p of row v:
+ *   sum   dmsg[p, f] = g[v, f]
+ *   mean  dmsg[p, f] = fl32(g[v, f] / deg(v))   (one correctly rounded division)
+ *   max   dmsg[p, f] = g[v, f] if argout[v, f] == p, else 0
+ * Returns 0, or -1 for a bad reduce. */
+int oracle_message_backward(int64_t N_dst, const int64_t* rowptr, const void* g, int g_is_bf16,
+                            int64_t F, int reduce, const int64_t* argout, float* dmsg) {
+    if (reduce != ORACLE_SUM && reduce != ORACLE_MEAN && reduce != ORACLE_MAX) return -1;
+    if (reduce == ORACLE_MAX && !argout) return -1;
+    for (int64_t v = 0; v < N_dst; ++v) {
+        int64_t deg = rowptr[v + 1] - rowptr[v];
+        for (int64_t p = rowptr[v]; p < rowptr[v + 1]; ++p)
+            for (int64_t f = 0; f < F; ++f) {
+                float gv = feature(g, g_is_bf16, F, v, f);
+                float d;
+                if (reduce == ORACLE_SUM)
+                    d = gv;
+                else if (reduce == ORACLE_MEAN)
+                    d = (float)((double)gv / (double)deg);
+                else
+                    d = argout[v * F + f] == p ? gv : 0.0f;
+                dmsg[p * F + f] = d;
+            }
+    }
+    return 0;
+}
+
+/* Per-edge dot products: for p in [0, E),
+ *   out[o] = sum_f a[p, f] * b[j, f],  scale[o] = sum_f |a[p, f] * b[j, f]|
+ * with j = bidx[p] (bidx NULL: j = p) and o = oidx[p] (oidx NULL: o = p), in
+ * fp64.  a is [E, F], b is [N_b, F], each fp32 or bf16 bits.  This is the
+ * gradient of the materialized messages with respect to a per-edge factor:
+ * the edge weights (a = dL/dmsg, b = x, bidx = col) or an edge mask applied
+ * by the callback (a = dL/d(masked msg), b = the unmasked messages).
+ * Returns 0, or -1 for an index out of range. */
+int oracle_edge_dot(int64_t E, int64_t F, const void* a, int a_is_bf16, const void* b,
+                    int b_is_bf16, const int32_t* bidx, int64_t N_b, const int32_t* oidx,
+                    double* out, double* scale) {
+    for (int64_t p = 0; p < E; ++p) {
+        int64_t j = bidx ? bidx[p] : p;
+        int64_t o = oidx ? oidx[p] : p;
+        if (j < 0 || j >= N_b || o < 0 || o >= E) return -1;
+    }
+    for (int64_t p = 0; p < E; ++p) {
+        int64_t j = bidx ? bidx[p] : p;
+        int64_t o = oidx ? oidx[p] : p;
+        double s = 0.0, sa = 0.0;
+        for (int64_t f = 0; f < F; ++f) {
+            double t = (double)feature(a, a_is_bf16, F, p, f) * (double)feature(b, b_is_bf16, F, j, f);
+            s += t;
+            sa += fabs(t);
+        }
+        out[o] = s;
+        if (scale) scale[o] = sa;
+    }
+    return 0;
+}
+
+/* Gradient of the materialized messages w[p] * x[col[p], :] with respect to
+ * x, given dmsg = dL/dmsg [E, F] fp32:
+ *   gx[u, f] = sum over CSR edges p with col[p] == u, in CSR order, of
+ *              w_p * dmsg[p, f]     (w_p = 1 when w is NULL)
+ *   scale[u, f] = the same sum of absolute values.
+ * Returns 0, or -1 for a column out of range. */
+int oracle_message_backward_x(int64_t E, int64_t N_src, const int32_t* col, const float* w,
+                              const float* dmsg, int64_t F, double* gx, double* scale) {
+    for (int64_t k = 0; k < N_src * F; ++k) {
+        gx[k] = 0.0;
+        if (scale) scale[k] = 0.0;
+    }
+    for (int64_t p = 0; p < E; ++p) {
+        int64_t u = col[p];
+        if (u < 0 || u >= N_src) return -1;
+        double wp = w ? (double)w[p] : 1.0;
+        for (int64_t f = 0; f < F; ++f) {
+            double t = wp * (double)dmsg[p * F + f];
+            gx[u * F + f] += t;
+            if (scale) scale[u * F + f] += fabs(t);
         }
     }
     return 0;
