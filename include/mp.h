@@ -62,7 +62,8 @@ typedef enum mp_status {
     MP_ERR_WORKSPACE = -5, /* workspace or plan buffer too small */
     MP_ERR_PLAN = -6,      /* plan does not match the arguments */
     MP_ERR_HIP = -7,       /* a HIP launch, copy or query failed */
-    MP_ERR_ALIGN = -8      /* a pointer is not aligned to its element size */
+    MP_ERR_ALIGN = -8,     /* a pointer is not aligned to its element size */
+    MP_ERR_CALLBACK = -9   /* a message callback returned nonzero */
 } mp_status;
 
 /* Feature / output element types. */
@@ -348,6 +349,127 @@ int mp_segment_matmul_backward_workspace(const int64_t* seg, int T, int64_t F, i
 int mp_segment_matmul_backward(const int64_t* seg, int T, const void* x, const void* W,
                                const void* dout, int64_t F, int64_t Fo, void* dx, int dx_dtype,
                                float* dW, void* ws, size_t ws_bytes, void* stream);
+
+/* ---------------------------------------------------------------------------
+ * Edge-materialized message passing with a message callback.  In the
+ * explanation mode of Sec. 2.4, message passing falls back to the edge-level
+ * materialization of the first PyG (recalled in Sec. 2.2), so that a callback
+ * c mapping the E x F messages to E x F messages can edit every message
+ * before the aggregation:  h_v' = f(h_v, AGG{ c(g(h_w, e_wv, h_v)) })
+ * (perturbing messages, weighting them with an edge mask, or capturing them).
+ * Messages live in a caller-owned [E, F] table in destination-major CSR
+ * order: row p is the message of CSR edge p, i.e. of COO edge perm[p].  The
+ * aggregation of the table is the segmented reduction of mp_spmm over
+ * consecutive rows (no atomics: the order of every sum is fixed, so results
+ * are deterministic).  Arbitrary messages g can be built by the caller from
+ * gathered tables (mp_message_gather of x by col gives the source rows, by
+ * the rows of mp_csr_rows the destination rows) and aggregated with
+ * mp_message_aggregate.
+ * The gradient with respect to x of messages w[p] * x[col[p], :] given
+ * dL/dmsg is mp_spmm over the transposed CSR (mp_csr_transpose) with the
+ * forward positions posT as column indices, dL/dmsg as the feature table and
+ * the transposed weights: gx[u] = sum over edges p from u of w[p] dL/dmsg[p].
+ * ------------------------------------------------------------------------- */
+
+/* row[p] = the destination row v of CSR position p (rowptr[v] <= p <
+ * rowptr[v+1]), int32 [E]; the destination index of every edge in CSR
+ * order.  Sizes: 1 <= N_dst <= INT32_MAX, 0 <= E <= INT32_MAX.
+ * Asynchronous on `stream`. */
+int mp_csr_rows(const void* rowptr, int rowptr_itype, int64_t N_dst, int64_t E, int32_t* row,
+                void* stream);
+
+/* MESSAGE, materialized: msg[p, :] = w[p] * x[idx[p], :] (one correctly
+ * rounded fp32 product per element, as in mp_spmm) or x[idx[p], :] when w is
+ * NULL, for p in [0, E).
+ *   idx  [E] int32 rows of x, 0 <= idx[p] < N_src (the CSR col for the
+ *        sources' features).
+ *   w    [E] fp32 or NULL.
+ *   x    [N_src, F] of x_dtype.
+ *   msg  [E, F] of msg_dtype: MP_F32, or MP_BF16 only for unweighted bf16 x
+ *        (then an exact copy of the rows); MP_ERR_DTYPE otherwise.
+ * Sizes: 0 <= E <= INT32_MAX, 0 <= N_src <= INT32_MAX, 1 <= F <= 65536.
+ * Asynchronous on `stream`. */
+int mp_message_gather(const int32_t* idx, const float* w, const void* x, int x_dtype,
+                      int64_t N_src, int64_t E, int64_t F, void* msg, int msg_dtype,
+                      void* stream);
+
+/* The edge-mask callback of explanation mode, and its gradient with respect
+ * to its input: out[p, :] = in[p, :] * mask[j] with j = idx[p] (idx NULL:
+ * j = p), one correctly rounded fp32 product per element.
+ *   in, out  [E, F] fp32 (out may equal in: in place).
+ *   mask     [n_mask] fp32 (per COO edge with idx = perm, or per CSR edge).
+ *   idx      [E] int32 in [0, n_mask), or NULL (then n_mask >= E).
+ * Asynchronous on `stream`. */
+int mp_message_scale(const float* in, float* out, int64_t E, int64_t F, const float* mask,
+                     const int32_t* idx, int64_t n_mask, void* stream);
+
+/* AGGREGATION of materialized messages: out[v] = AGG over rows p in
+ * [rowptr[v], rowptr[v+1]) of msg[p, :], exactly as mp_spmm with column p at
+ * position p and no weights (same reductions, output dtypes, empty-row values
+ * and argmax convention: argout holds the message row, i.e. the CSR position).
+ *   msg  [E, F] of msg_dtype (MP_F32, or MP_BF16).
+ * plan (optional): built from the same rowptr with this F.  ws: as
+ * mp_spmm_workspace.  Asynchronous on `stream`. */
+int mp_message_aggregate(const mp_plan* plan, const void* rowptr, int rowptr_itype,
+                         const void* msg, int msg_dtype, int64_t E, int64_t N_dst, int64_t F,
+                         int reduce, void* out, int out_dtype, void* out_max, int max_dtype,
+                         int32_t* argout, void* ws, size_t ws_bytes, void* stream);
+
+/* A message callback c.  Called on the calling host thread, once per
+ * mp_spmm_materialized call, after the message table has been enqueued on
+ * `stream` and before the aggregation is: it must enqueue its own work on
+ * `stream` (or finish it before returning), reading and writing the [E, F]
+ * table msg of msg_dtype in place.  user is passed through unchanged.  A
+ * nonzero return aborts the call with MP_ERR_CALLBACK. */
+typedef int (*mp_message_fn)(void* msg, int msg_dtype, int64_t E, int64_t F, void* user,
+                             void* stream);
+
+/* Explanation-mode aggregation: msg = gather (as mp_message_gather with
+ * idx = col), then c(msg, ...) if c is not NULL, then the aggregation of
+ * msg (as mp_message_aggregate).  With c NULL the outputs equal mp_spmm's up
+ * to the order of floating-point sums (max and argout exactly).
+ *   msg  caller's [E, F] table of msg_dtype (left holding the messages
+ *        after the callback).
+ * Every argument of the three steps is checked before anything is enqueued.
+ * On MP_ERR_CALLBACK the gather (and whatever c enqueued) has run and the
+ * outputs are untouched.  Asynchronous on `stream` apart from the callback. */
+int mp_spmm_materialized(const mp_plan* plan, const void* rowptr, int rowptr_itype,
+                         const int32_t* col, const float* w, const void* x, int x_dtype,
+                         int64_t N_src, int64_t N_dst, int64_t E, int64_t F, void* msg,
+                         int msg_dtype, mp_message_fn c, void* user, int reduce, void* out,
+                         int out_dtype, void* out_max, int max_dtype, int32_t* argout, void* ws,
+                         size_t ws_bytes, void* stream);
+
+/* Workspace bytes for mp_message_backward (the row of every CSR position:
+ * 4 * E, rounded up to 256). */
+int mp_message_backward_workspace(int64_t E, size_t* bytes);
+
+/* Gradient of the aggregation of materialized messages with respect to each
+ * message, given grad_out = dL/dout [N_dst, F] (fp32 or bf16), for the CSR
+ * edge p of row v (reduce is exactly one of MP_SUM, MP_MEAN, MP_MAX):
+ *   sum   dmsg[p, :] = grad_out[v, :]
+ *   mean  dmsg[p, :] = grad_out[v, :] / deg(v)   (correctly rounded)
+ *   max   dmsg[p, f] = grad_out[v, f] if argout[v, f] == p, else 0
+ *   dmsg   [E, F] fp32 out;  argout [N_dst, F] int32 from the forward (max).
+ * Sizes: 1 <= N_dst <= INT32_MAX, 0 <= E <= INT32_MAX, 1 <= F <= 65536.
+ * Asynchronous on `stream`. */
+int mp_message_backward(const void* rowptr, int rowptr_itype, const int32_t* argout,
+                        const void* grad_out, int g_dtype, int64_t N_dst, int64_t E, int64_t F,
+                        int reduce, float* dmsg, void* ws, size_t ws_bytes, void* stream);
+
+/* Per-edge dot products: out[o] = sum_f a[p, f] * b[j, f] with j = bidx[p]
+ * (bidx NULL: j = p) and o = oidx[p] (oidx NULL: o = p), for p in [0, E),
+ * accumulated in fp32 in a fixed order.  The gradient of materialized
+ * messages with respect to a per-edge factor: the edge weights (a = dL/dmsg,
+ * b = x, bidx = col) or an edge mask applied by the callback (a = dL/d(masked
+ * messages), b = the unmasked messages, oidx = perm for COO order).
+ *   a  [E, F] of a_dtype;  b [N_b, F] of b_dtype;  out [E] fp32.
+ *   oidx must be a permutation of [0, E) when given.
+ * Sizes: 0 <= E <= INT32_MAX, 0 <= N_b <= INT32_MAX, 1 <= F <= 65536.
+ * Asynchronous on `stream`. */
+int mp_edge_dot(const void* a, int a_dtype, const void* b, int b_dtype, const int32_t* bidx,
+                int64_t N_b, const int32_t* oidx, int64_t E, int64_t F, float* out,
+                void* stream);
 
 /* ---------------------------------------------------------------------------
  * Heterogeneous message passing (Sec. 2.2, nested Eq. (1)): per destination

@@ -33,7 +33,11 @@ __all__ = [
     "mp_spmm_plan_size", "mp_spmm_plan_build", "mp_spmm_plan_free", "mp_spmm_workspace",
     "mp_spmm", "mp_hetero_build_workspace", "mp_hetero_build", "mp_hetero_spmm",
     "mp_validate_coo", "mp_validate_csr", "coo_to_csr", "Plan", "spmm", "hetero_build",
-    "hetero_spmm", "LIB_PATH",
+    "hetero_spmm", "LIB_PATH", "MESSAGE_FN", "mp_csr_rows", "mp_message_gather",
+    "mp_message_scale", "mp_message_aggregate", "mp_spmm_materialized",
+    "mp_message_backward_workspace", "mp_message_backward", "mp_edge_dot", "csr_rows",
+    "message_gather", "message_scale", "message_aggregate", "spmm_materialized",
+    "message_backward", "edge_dot",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -48,6 +52,11 @@ MP_MIN, MP_VAR, MP_STD = 8, 16, 32
 AGGR = {"sum": MP_SUM, "mean": MP_MEAN, "max": MP_MAX, "min": MP_MIN, "var": MP_VAR,
         "std": MP_STD}
 MP_MAX_TYPES = 16
+MP_ERR_CALLBACK = -9
+
+# int c(void* msg, int msg_dtype, int64_t E, int64_t F, void* user, void* stream)
+MESSAGE_FN = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.c_void_p, ctypes.c_int, ctypes.c_int64,
+                              ctypes.c_int64, ctypes.c_void_p, ctypes.c_void_p)
 
 _lib = None
 
@@ -113,7 +122,20 @@ def lib():
         L.mp_spmm_backward_w_workspace.argtypes = [i64, psz]
         L.mp_spmm_backward_w.argtypes = [p, i32, p, p, i32, p, i32, p, i64, i64, i64, i64, i32, p,
                                          p, sz, p]
-        for name in ("mp_coo_to_csr_workspace", "mp_coo_to_csr", "mp_sorted_coo_to_csr",
+        L.mp_csr_rows.argtypes = [p, i32, i64, i64, p, p]
+        L.mp_message_gather.argtypes = [p, p, p, i32, i64, i64, i64, p, i32, p]
+        L.mp_message_scale.argtypes = [p, p, i64, i64, p, p, i64, p]
+        L.mp_message_aggregate.argtypes = [p, p, i32, p, i32, i64, i64, i64, i32, p, i32, p, i32,
+                                           p, p, sz, p]
+        L.mp_spmm_materialized.argtypes = [p, p, i32, p, p, p, i32, i64, i64, i64, i64, p, i32,
+                                           p, p, i32, p, i32, p, i32, p, p, sz, p]
+        L.mp_message_backward_workspace.argtypes = [i64, psz]
+        L.mp_message_backward.argtypes = [p, i32, p, p, i32, i64, i64, i64, i32, p, p, sz, p]
+        L.mp_edge_dot.argtypes = [p, i32, p, i32, p, i64, p, i64, i64, p, p]
+        for name in ("mp_csr_rows", "mp_message_gather", "mp_message_scale",
+                     "mp_message_aggregate", "mp_spmm_materialized",
+                     "mp_message_backward_workspace", "mp_message_backward", "mp_edge_dot",
+                     "mp_coo_to_csr_workspace", "mp_coo_to_csr", "mp_sorted_coo_to_csr",
                      "mp_validate_sorted", "mp_csr_transpose_workspace", "mp_csr_transpose",
                      "mp_spmm_multi_workspace", "mp_spmm_multi", "mp_readout_multi",
                      "mp_segment_matmul_workspace", "mp_segment_matmul",
@@ -380,6 +402,60 @@ def mp_validate_csr(rowptr, rowptr_itype, col, N_dst, N_src, E, d_count, stream=
                                                     N_src, E, _ptr(d_count), _stream(stream)))
 
 
+def mp_csr_rows(rowptr, rowptr_itype, N_dst, E, row, stream=None):
+    _check("mp_csr_rows", lib().mp_csr_rows(_ptr(rowptr), rowptr_itype, N_dst, E, _ptr(row),
+                                            _stream(stream)))
+
+
+def mp_message_gather(idx, w, x, x_dtype, N_src, E, F, msg, msg_dtype, stream=None):
+    _check("mp_message_gather", lib().mp_message_gather(
+        _ptr(idx), _ptr(w), _ptr(x), x_dtype, N_src, E, F, _ptr(msg), msg_dtype, _stream(stream)))
+
+
+def mp_message_scale(msg_in, msg_out, E, F, mask, idx, n_mask, stream=None):
+    _check("mp_message_scale", lib().mp_message_scale(
+        _ptr(msg_in), _ptr(msg_out), E, F, _ptr(mask), _ptr(idx), n_mask, _stream(stream)))
+
+
+def mp_message_aggregate(plan_handle, rowptr, rowptr_itype, msg, msg_dtype, E, N_dst, F, reduce,
+                         out, out_dtype, out_max, max_dtype, argout, ws, ws_bytes, stream=None):
+    _check("mp_message_aggregate", lib().mp_message_aggregate(
+        plan_handle, _ptr(rowptr), rowptr_itype, _ptr(msg), msg_dtype, E, N_dst, F, reduce,
+        _ptr(out), out_dtype, _ptr(out_max), max_dtype, _ptr(argout), _ptr(ws), ws_bytes,
+        _stream(stream)))
+
+
+def mp_spmm_materialized(plan_handle, rowptr, rowptr_itype, col, w, x, x_dtype, N_src, N_dst, E,
+                         F, msg, msg_dtype, c, user, reduce, out, out_dtype, out_max, max_dtype,
+                         argout, ws, ws_bytes, stream=None):
+    """c: a MESSAGE_FN (keep a reference to it for the call), a function
+    address, or None."""
+    if isinstance(c, int):
+        c = ctypes.cast(c, MESSAGE_FN)
+    _check("mp_spmm_materialized", lib().mp_spmm_materialized(
+        plan_handle, _ptr(rowptr), rowptr_itype, _ptr(col), _ptr(w), _ptr(x), x_dtype, N_src,
+        N_dst, E, F, _ptr(msg), msg_dtype, ctypes.cast(c, ctypes.c_void_p) if c else None, user,
+        reduce, _ptr(out), out_dtype, _ptr(out_max), max_dtype, _ptr(argout), _ptr(ws), ws_bytes,
+        _stream(stream)))
+
+
+def mp_message_backward_workspace(E) -> int:
+    return _bytes("mp_message_backward_workspace", E)
+
+
+def mp_message_backward(rowptr, rowptr_itype, argout, grad_out, g_dtype, N_dst, E, F, reduce,
+                        dmsg, ws, ws_bytes, stream=None):
+    _check("mp_message_backward", lib().mp_message_backward(
+        _ptr(rowptr), rowptr_itype, _ptr(argout), _ptr(grad_out), g_dtype, N_dst, E, F, reduce,
+        _ptr(dmsg), _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def mp_edge_dot(a, a_dtype, b, b_dtype, bidx, N_b, oidx, E, F, out, stream=None):
+    _check("mp_edge_dot", lib().mp_edge_dot(
+        _ptr(a), a_dtype, _ptr(b), b_dtype, _ptr(bidx), N_b, _ptr(oidx), E, F, _ptr(out),
+        _stream(stream)))
+
+
 # ---- convenience wrappers ---------------------------------------------------------
 
 def coo_to_csr(src: torch.Tensor, dst: torch.Tensor, N: int, *, rowptr_dtype=torch.int32,
@@ -631,4 +707,127 @@ def hetero_spmm(N_per_type, x_per_type, dst_type, rowptr, col, *, plan: Plan | N
                    plan.handle if plan is not None else None, rowptr, _itype_code(rowptr.dtype),
                    col, MP_SUM, out, _dtype_code(out.dtype), ws, 0 if ws is None else ws.numel(),
                    stream)
+    return out
+
+
+# ---- edge-materialized messages (explanation mode) ------------------------------------
+
+def csr_rows(rowptr, E, *, stream=None):
+    """The destination row of every CSR position (int32 [E])."""
+    N_dst = int(rowptr.numel()) - 1
+    row = _edge_array(int(E), torch.int32, rowptr.device)
+    mp_csr_rows(rowptr, _itype_code(rowptr.dtype), N_dst, int(E), row, stream)
+    return row
+
+
+def message_gather(idx, x, *, w=None, msg_dtype=torch.float32, out=None, stream=None):
+    """msg[p] = w[p] * x[idx[p]] (or x[idx[p]]): the materialized messages,
+    [E, F] of msg_dtype (bf16 only for unweighted bf16 x)."""
+    E = int(idx.numel())
+    N_src, F = int(x.shape[0]), int(x.shape[1])
+    if out is None:
+        out = torch.empty(max(E, 1), F, dtype=msg_dtype, device=x.device)[:E]
+    mp_message_gather(idx, w, x, _dtype_code(x.dtype), N_src, E, F, out, _dtype_code(out.dtype),
+                      stream)
+    return out
+
+
+def message_scale(msg, mask, *, idx=None, out=None, stream=None):
+    """out[p] = msg[p] * mask[idx[p]] (idx None: mask[p]); out may be msg."""
+    E, F = int(msg.shape[0]), int(msg.shape[1])
+    if out is None:
+        out = torch.empty_like(msg)
+    mp_message_scale(msg, out, E, F, mask, idx, int(mask.numel()), stream)
+    return out
+
+
+def message_aggregate(rowptr, msg, reduce, *, plan: Plan | None = None, out_dtype=torch.float32,
+                      max_dtype=None, stream=None):
+    """Aggregate the message rows of each CSR row: (out, out_max, argout)
+    like spmm, argout = the message row."""
+    N_dst = int(rowptr.numel()) - 1
+    E, F = int(msg.shape[0]), int(msg.shape[1])
+    dev = msg.device
+    hs = bool(reduce & (MP_SUM | MP_MEAN))
+    hm = bool(reduce & MP_MAX)
+    out = torch.empty(N_dst, F, dtype=out_dtype, device=dev) if hs else None
+    out_max = torch.empty(N_dst, F, dtype=max_dtype or torch.float32, device=dev) if hm else None
+    argout = torch.empty(N_dst, F, dtype=torch.int32, device=dev) if hm else None
+    ws = plan.workspace(reduce) if plan is not None else None
+    mp_message_aggregate(plan.handle if plan is not None else None, rowptr,
+                         _itype_code(rowptr.dtype), msg, _dtype_code(msg.dtype), E, N_dst, F,
+                         reduce, out, _dtype_code(out.dtype) if hs else MP_F32, out_max,
+                         _dtype_code(out_max.dtype) if hm else MP_F32, argout, ws,
+                         0 if ws is None else ws.numel(), stream)
+    return out, out_max, argout
+
+
+def spmm_materialized(rowptr, col, x, reduce, *, callback=None, w=None, plan: Plan | None = None,
+                      msg=None, msg_dtype=torch.float32, out_dtype=torch.float32, max_dtype=None,
+                      stream=None):
+    """Explanation-mode aggregation: gather the messages into msg ([E, F],
+    allocated unless given), call callback(msg) (a Python function that edits
+    the tensor in place, enqueuing its work on the current stream), then
+    aggregate.  Returns (out, out_max, argout, msg)."""
+    N_dst = int(rowptr.numel()) - 1
+    N_src, F = int(x.shape[0]), int(x.shape[1])
+    E = int(col.numel())
+    dev = x.device
+    if msg is None:
+        msg = torch.empty(max(E, 1), F, dtype=msg_dtype, device=dev)[:E]
+    hs = bool(reduce & (MP_SUM | MP_MEAN))
+    hm = bool(reduce & MP_MAX)
+    out = torch.empty(N_dst, F, dtype=out_dtype, device=dev) if hs else None
+    out_max = torch.empty(N_dst, F, dtype=max_dtype or torch.float32, device=dev) if hm else None
+    argout = torch.empty(N_dst, F, dtype=torch.int32, device=dev) if hm else None
+    ws = plan.workspace(reduce) if plan is not None else None
+    failure = []
+
+    def trampoline(ptr, dtype, e, f, user, strm):
+        try:
+            callback(msg)
+            return 0
+        except Exception as exc:  # reported after the C call returns
+            failure.append(exc)
+            return 1
+
+    c = MESSAGE_FN(trampoline) if callback is not None else None
+    try:
+        mp_spmm_materialized(plan.handle if plan is not None else None, rowptr,
+                             _itype_code(rowptr.dtype), col, w, x, _dtype_code(x.dtype), N_src,
+                             N_dst, E, F, msg, _dtype_code(msg.dtype), c, None, reduce, out,
+                             _dtype_code(out.dtype) if hs else MP_F32, out_max,
+                             _dtype_code(out_max.dtype) if hm else MP_F32, argout, ws,
+                             0 if ws is None else ws.numel(), stream)
+    except MPError as err:
+        if failure:
+            raise err from failure[0]
+        raise
+    return out, out_max, argout, msg
+
+
+def message_backward(rowptr, grad_out, reduce, *, E=None, argout=None, out=None, stream=None):
+    """dL/dmsg [E, F] fp32 of message_aggregate for one reduction."""
+    N_dst = int(rowptr.numel()) - 1
+    F = int(grad_out.shape[1])
+    if E is None:
+        E = int(rowptr[-1].item())
+    dev = grad_out.device
+    if out is None:
+        out = torch.empty(max(E, 1), F, dtype=torch.float32, device=dev)[:E]
+    nb = mp_message_backward_workspace(E)
+    ws = _workspace(nb, dev) if nb else None
+    mp_message_backward(rowptr, _itype_code(rowptr.dtype), argout, grad_out,
+                        _dtype_code(grad_out.dtype), N_dst, E, F, reduce, out, ws,
+                        0 if ws is None else ws.numel(), stream)
+    return out
+
+
+def edge_dot(a, b, *, bidx=None, oidx=None, out=None, stream=None):
+    """out[oidx[p]] = sum_f a[p, f] * b[bidx[p], f] (fp32 [E])."""
+    E, F = int(a.shape[0]), int(a.shape[1])
+    if out is None:
+        out = _edge_array(E, torch.float32, a.device)
+    mp_edge_dot(a, _dtype_code(a.dtype), b, _dtype_code(b.dtype), bidx, int(b.shape[0]), oidx, E,
+                F, out, stream)
     return out

@@ -299,6 +299,105 @@ int multi_impl(const mp_plan* plan, const void* rowptr, int rowptr_itype, const 
     return run_spmm(plan, P, g, x_dtype, N_dst, ws, ws_bytes, s);
 }
 
+// ---- aggregation call (mp_spmm, mp_message_aggregate) ---------------------------
+
+// The arguments of one aggregation; col == nullptr reads position p as
+// column p (a table of materialized messages).
+struct SpmmCall {
+    const mp_plan* plan;
+    const void* rowptr;
+    int rowptr_itype;
+    const int32_t* col;
+    const float* w;
+    const void* x;
+    int x_dtype;
+    int64_t N_src, N_dst, F;
+    int reduce;
+    void* out;
+    int out_dtype;
+    void* out_max;
+    int max_dtype;
+    int32_t* argout;
+    void* ws;
+    size_t ws_bytes;
+};
+
+// Every argument check of an aggregation, before anything is enqueued.
+int spmm_check(const SpmmCall& c) {
+    if (!valid_reduce(c.reduce)) return MP_ERR_REDUCE;
+    if (!valid_itype(c.rowptr_itype) || !valid_dtype(c.x_dtype)) return MP_ERR_DTYPE;
+    const bool hs = (c.reduce & (MP_SUM | MP_MEAN)) != 0;
+    const bool hm = (c.reduce & MP_MAX) != 0;
+    if (hs && !valid_dtype(c.out_dtype)) return MP_ERR_DTYPE;
+    if (hm && !valid_dtype(c.max_dtype)) return MP_ERR_DTYPE;
+    if (hm && c.max_dtype == MP_BF16 && (c.x_dtype != MP_BF16 || c.w != nullptr))
+        return MP_ERR_DTYPE;
+    if (c.N_src < 0 || c.N_src > INT32_MAX || c.N_dst < 0 || c.N_dst > INT32_MAX || c.F < 1 ||
+        c.F > 65536)
+        return MP_ERR_SIZE;
+    if (!c.rowptr) return MP_ERR_NULL;
+    if (c.N_dst > 0) {
+        if (!c.x) return MP_ERR_NULL;
+        if (hs && !c.out) return MP_ERR_NULL;
+        if (hm && (!c.out_max || !c.argout)) return MP_ERR_NULL;
+    }
+    int st = check_plan(c.plan, c.rowptr, c.rowptr_itype, c.N_dst, c.F);
+    if (st != MP_OK) return st;
+    const int eb = c.x_dtype == MP_BF16 ? 2 : 4;
+    if ((uintptr_t)c.x % eb || (uintptr_t)c.rowptr % (c.rowptr_itype == MP_I64 ? 8 : 4) ||
+        (uintptr_t)c.col % 4 || (uintptr_t)c.w % 4 || (uintptr_t)c.argout % 4 ||
+        (hs && (uintptr_t)c.out % (c.out_dtype == MP_BF16 ? 2 : 4)) ||
+        (hm && (uintptr_t)c.out_max % (c.max_dtype == MP_BF16 ? 2 : 4)))
+        return MP_ERR_ALIGN;
+    size_t need = 0;
+    mp_spmm_workspace(c.plan, c.reduce, &need);
+    if (c.N_dst > 0 && need > 0 && (c.ws_bytes < need || !c.ws)) return MP_ERR_WORKSPACE;
+    return MP_OK;
+}
+
+// Enqueue a checked aggregation.
+int spmm_launch(const SpmmCall& c, hipStream_t s) {
+    if (c.N_dst == 0) return MP_OK;
+    Geometry g = make_geometry(c.F, c.x_dtype, (uintptr_t)c.x);
+    SpmmParams P{};
+    P.rowptr = c.rowptr;
+    P.rp64 = c.rowptr_itype == MP_I64;
+    P.col = c.col;
+    P.w = c.w;
+    P.n_tables = 1;
+    P.table_ptr[0] = static_cast<const char*>(c.x);
+    P.table_off[0] = 0;
+    P.F = c.F;
+    P.reduce = c.reduce;
+    P.out = c.out;
+    P.out_bf16 = c.out_dtype == MP_BF16;
+    P.out_max = c.out_max;
+    P.max_bf16 = c.max_dtype == MP_BF16;
+    P.argout = c.argout;
+    P.vec_store = (((uintptr_t)c.out | (uintptr_t)c.out_max | (uintptr_t)c.argout) % 16) == 0;
+    return run_spmm(c.plan, P, g, c.x_dtype, c.N_dst, c.ws, c.ws_bytes, s);
+}
+
+// ---- edge-materialized messages ---------------------------------------------------
+
+// Check a message gather and describe it.
+int gather_check(const int32_t* idx, const float* w, const void* x, int x_dtype, int64_t N_src,
+                 int64_t E, int64_t F, void* msg, int msg_dtype, MessageGather* a) {
+    if (!valid_dtype(x_dtype) || !valid_dtype(msg_dtype)) return MP_ERR_DTYPE;
+    if (msg_dtype == MP_BF16 && (x_dtype != MP_BF16 || w != nullptr)) return MP_ERR_DTYPE;
+    if (E < 0 || E > INT32_MAX || N_src < 0 || N_src > INT32_MAX || F < 1 || F > 65536)
+        return MP_ERR_SIZE;
+    if (E > 0 && (!idx || !x || !msg)) return MP_ERR_NULL;
+    const int bx = x_dtype == MP_BF16 ? 2 : 4, bm = msg_dtype == MP_BF16 ? 2 : 4;
+    if ((uintptr_t)idx % 4 || (uintptr_t)w % 4 || (uintptr_t)x % bx || (uintptr_t)msg % bm)
+        return MP_ERR_ALIGN;
+    const uintptr_t ptrs[2] = {(uintptr_t)x, (uintptr_t)msg};
+    const int sizes[2] = {bx, bm};
+    *a = MessageGather{idx, w, x, x_dtype == MP_BF16, msg, msg_dtype == MP_BF16, E, F,
+                       message_epl(F, ptrs, sizes, 2, 8)};
+    return MP_OK;
+}
+
 // ---- segment matmul ------------------------------------------------------------
 
 constexpr int64_t kGmmRowsPerChunk = 2048;  // rows per partial of the weight gradient
@@ -350,6 +449,7 @@ const char* mp_status_str(int status) {
         case MP_ERR_PLAN: return "plan does not match the arguments";
         case MP_ERR_HIP: return "HIP launch or copy failed";
         case MP_ERR_ALIGN: return "pointer not aligned to its element size";
+        case MP_ERR_CALLBACK: return "the message callback failed";
         default: return "unknown status";
     }
 }
@@ -538,48 +638,11 @@ int mp_spmm(const mp_plan* plan, const void* rowptr, int rowptr_itype, const int
             const float* w, const void* x, int x_dtype, int64_t N_src, int64_t N_dst, int64_t F,
             int reduce, void* out, int out_dtype, void* out_max, int max_dtype, int32_t* argout,
             void* ws, size_t ws_bytes, void* stream) {
-    if (!valid_reduce(reduce)) return MP_ERR_REDUCE;
-    if (!valid_itype(rowptr_itype) || !valid_dtype(x_dtype)) return MP_ERR_DTYPE;
-    const bool hs = (reduce & (MP_SUM | MP_MEAN)) != 0;
-    const bool hm = (reduce & MP_MAX) != 0;
-    if (hs && !valid_dtype(out_dtype)) return MP_ERR_DTYPE;
-    if (hm && !valid_dtype(max_dtype)) return MP_ERR_DTYPE;
-    if (hm && max_dtype == MP_BF16 && (x_dtype != MP_BF16 || w != nullptr)) return MP_ERR_DTYPE;
-    if (N_src < 0 || N_src > INT32_MAX || N_dst < 0 || N_dst > INT32_MAX || F < 1 || F > 65536)
-        return MP_ERR_SIZE;
-    if (!rowptr) return MP_ERR_NULL;
-    if (N_dst > 0) {
-        if (!col || !x) return MP_ERR_NULL;
-        if (hs && !out) return MP_ERR_NULL;
-        if (hm && (!out_max || !argout)) return MP_ERR_NULL;
-    }
-    int st = check_plan(plan, rowptr, rowptr_itype, N_dst, F);
-    if (st != MP_OK) return st;
-    const int eb = x_dtype == MP_BF16 ? 2 : 4;
-    if ((uintptr_t)x % eb || (uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4) ||
-        (uintptr_t)col % 4 || (uintptr_t)w % 4 || (uintptr_t)argout % 4 ||
-        (hs && (uintptr_t)out % (out_dtype == MP_BF16 ? 2 : 4)) ||
-        (hm && (uintptr_t)out_max % (max_dtype == MP_BF16 ? 2 : 4)))
-        return MP_ERR_ALIGN;
-    if (N_dst == 0) return MP_OK;
-    Geometry g = make_geometry(F, x_dtype, (uintptr_t)x);
-    SpmmParams P{};
-    P.rowptr = rowptr;
-    P.rp64 = rowptr_itype == MP_I64;
-    P.col = col;
-    P.w = w;
-    P.n_tables = 1;
-    P.table_ptr[0] = static_cast<const char*>(x);
-    P.table_off[0] = 0;
-    P.F = F;
-    P.reduce = reduce;
-    P.out = out;
-    P.out_bf16 = out_dtype == MP_BF16;
-    P.out_max = out_max;
-    P.max_bf16 = max_dtype == MP_BF16;
-    P.argout = argout;
-    P.vec_store = (((uintptr_t)out | (uintptr_t)out_max | (uintptr_t)argout) % 16) == 0;
-    return run_spmm(plan, P, g, x_dtype, N_dst, ws, ws_bytes, as_stream(stream));
+    if (N_dst > 0 && !col) return MP_ERR_NULL;
+    SpmmCall c{plan, rowptr, rowptr_itype, col, w, x, x_dtype, N_src, N_dst, F, reduce,
+               out, out_dtype, out_max, max_dtype, argout, ws, ws_bytes};
+    const int st = spmm_check(c);
+    return st != MP_OK ? st : spmm_launch(c, as_stream(stream));
 }
 
 // ---- backward ------------------------------------------------------------------
@@ -765,6 +828,143 @@ int mp_spmm_backward_w(const void* rowptr, int rowptr_itype, const int32_t* col,
     P.reduce = reduce;
     P.grad_w = grad_w;
     return hip_status(launch_spmm_grad_w(P, x_dtype, g_dtype, g.epl, s));
+}
+
+// ---- edge-materialized messages ------------------------------------------------
+
+int mp_csr_rows(const void* rowptr, int rowptr_itype, int64_t N_dst, int64_t E, int32_t* row,
+                void* stream) {
+    if (!valid_itype(rowptr_itype)) return MP_ERR_DTYPE;
+    if (N_dst < 1 || N_dst > INT32_MAX || E < 0 || E > INT32_MAX) return MP_ERR_SIZE;
+    if (!rowptr || (E > 0 && !row)) return MP_ERR_NULL;
+    if ((uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4) || (uintptr_t)row % 4)
+        return MP_ERR_ALIGN;
+    return hip_status(launch_rows_of_edges(rowptr, rowptr_itype == MP_I64, N_dst, E, row,
+                                           as_stream(stream)));
+}
+
+int mp_message_gather(const int32_t* idx, const float* w, const void* x, int x_dtype,
+                      int64_t N_src, int64_t E, int64_t F, void* msg, int msg_dtype,
+                      void* stream) {
+    MessageGather a{};
+    const int st = gather_check(idx, w, x, x_dtype, N_src, E, F, msg, msg_dtype, &a);
+    return st != MP_OK ? st : hip_status(launch_message_gather(a, as_stream(stream)));
+}
+
+int mp_message_scale(const float* in, float* out, int64_t E, int64_t F, const float* mask,
+                     const int32_t* idx, int64_t n_mask, void* stream) {
+    if (E < 0 || E > INT32_MAX || F < 1 || F > 65536 || n_mask < 0) return MP_ERR_SIZE;
+    if (E == 0) return MP_OK;
+    if (!in || !out || !mask) return MP_ERR_NULL;
+    if (!idx && n_mask < E) return MP_ERR_SIZE;
+    if ((uintptr_t)in % 4 || (uintptr_t)out % 4 || (uintptr_t)mask % 4 || (uintptr_t)idx % 4)
+        return MP_ERR_ALIGN;
+    const uintptr_t ptrs[2] = {(uintptr_t)in, (uintptr_t)out};
+    const int sizes[2] = {4, 4};
+    const int epl = message_epl(F, ptrs, sizes, 2, 4);
+    return hip_status(launch_message_scale(in, out, mask, idx, E, F, epl, as_stream(stream)));
+}
+
+int mp_message_aggregate(const mp_plan* plan, const void* rowptr, int rowptr_itype,
+                         const void* msg, int msg_dtype, int64_t E, int64_t N_dst, int64_t F,
+                         int reduce, void* out, int out_dtype, void* out_max, int max_dtype,
+                         int32_t* argout, void* ws, size_t ws_bytes, void* stream) {
+    if (E < 0 || E > INT32_MAX) return MP_ERR_SIZE;
+    SpmmCall c{plan, rowptr, rowptr_itype, nullptr, nullptr, msg, msg_dtype, E, N_dst, F,
+               reduce, out, out_dtype, out_max, max_dtype, argout, ws, ws_bytes};
+    const int st = spmm_check(c);
+    return st != MP_OK ? st : spmm_launch(c, as_stream(stream));
+}
+
+int mp_spmm_materialized(const mp_plan* plan, const void* rowptr, int rowptr_itype,
+                         const int32_t* col, const float* w, const void* x, int x_dtype,
+                         int64_t N_src, int64_t N_dst, int64_t E, int64_t F, void* msg,
+                         int msg_dtype, mp_message_fn c, void* user, int reduce, void* out,
+                         int out_dtype, void* out_max, int max_dtype, int32_t* argout, void* ws,
+                         size_t ws_bytes, void* stream) {
+    if (E < 0 || E > INT32_MAX) return MP_ERR_SIZE;
+    if (plan && plan->E != E) return MP_ERR_PLAN;
+    MessageGather a{};
+    int st = gather_check(col, w, x, x_dtype, N_src, E, F, msg, msg_dtype, &a);
+    if (st != MP_OK) return st;
+    SpmmCall agg{plan, rowptr, rowptr_itype, nullptr, nullptr, msg, msg_dtype, E, N_dst, F,
+                 reduce, out, out_dtype, out_max, max_dtype, argout, ws, ws_bytes};
+    st = spmm_check(agg);
+    if (st != MP_OK) return st;
+    hipStream_t s = as_stream(stream);
+    if (launch_message_gather(a, s) != hipSuccess) return MP_ERR_HIP;
+    if (c && c(msg, msg_dtype, E, F, user, stream) != 0) return MP_ERR_CALLBACK;
+    return spmm_launch(agg, s);
+}
+
+int mp_message_backward_workspace(int64_t E, size_t* bytes) {
+    if (!bytes) return MP_ERR_NULL;
+    if (E < 0 || E > INT32_MAX) return MP_ERR_SIZE;
+    *bytes = E == 0 ? 0 : align_up((size_t)E * 4, 256);
+    return MP_OK;
+}
+
+int mp_message_backward(const void* rowptr, int rowptr_itype, const int32_t* argout,
+                        const void* grad_out, int g_dtype, int64_t N_dst, int64_t E, int64_t F,
+                        int reduce, float* dmsg, void* ws, size_t ws_bytes, void* stream) {
+    if (reduce != MP_SUM && reduce != MP_MEAN && reduce != MP_MAX) return MP_ERR_REDUCE;
+    if (!valid_itype(rowptr_itype) || !valid_dtype(g_dtype)) return MP_ERR_DTYPE;
+    if (N_dst < 1 || N_dst > INT32_MAX || E < 0 || E > INT32_MAX || F < 1 || F > 65536)
+        return MP_ERR_SIZE;
+    if (!rowptr) return MP_ERR_NULL;
+    if (E == 0) return MP_OK;
+    if (!grad_out || !dmsg || !ws) return MP_ERR_NULL;
+    if (reduce == MP_MAX && !argout) return MP_ERR_NULL;
+    if (ws_bytes < align_up((size_t)E * 4, 256)) return MP_ERR_WORKSPACE;
+    const int eg = g_dtype == MP_BF16 ? 2 : 4;
+    if ((uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4) || (uintptr_t)argout % 4 ||
+        (uintptr_t)grad_out % eg || (uintptr_t)dmsg % 4)
+        return MP_ERR_ALIGN;
+    hipStream_t s = as_stream(stream);
+    int32_t* row = static_cast<int32_t*>(ws);
+    if (launch_rows_of_edges(rowptr, rowptr_itype == MP_I64, N_dst, E, row, s) != hipSuccess)
+        return MP_ERR_HIP;
+    const uintptr_t ptrs[3] = {(uintptr_t)grad_out, (uintptr_t)dmsg,
+                               reduce == MP_MAX ? (uintptr_t)argout : 0};
+    const int sizes[3] = {eg, 4, 4};
+    MessageBackward b{rowptr, rowptr_itype == MP_I64, row, argout, grad_out, g_dtype == MP_BF16,
+                      E, F, reduce, message_epl(F, ptrs, sizes, 3, 4), dmsg};
+    return hip_status(launch_message_backward(b, s));
+}
+
+int mp_edge_dot(const void* a, int a_dtype, const void* b, int b_dtype, const int32_t* bidx,
+                int64_t N_b, const int32_t* oidx, int64_t E, int64_t F, float* out,
+                void* stream) {
+    if (!valid_dtype(a_dtype) || !valid_dtype(b_dtype)) return MP_ERR_DTYPE;
+    if (E < 0 || E > INT32_MAX || N_b < 0 || N_b > INT32_MAX || F < 1 || F > 65536)
+        return MP_ERR_SIZE;
+    if (!bidx && N_b < E) return MP_ERR_SIZE;
+    if (E == 0) return MP_OK;
+    if (!a || !b || !out) return MP_ERR_NULL;
+    const int ea = a_dtype == MP_BF16 ? 2 : 4, eb = b_dtype == MP_BF16 ? 2 : 4;
+    if ((uintptr_t)a % ea || (uintptr_t)b % eb || (uintptr_t)bidx % 4 || (uintptr_t)oidx % 4 ||
+        (uintptr_t)out % 4)
+        return MP_ERR_ALIGN;
+    // one lane-chunk of EPL elements per table: b's vector width must keep a's
+    // chunk aligned too (a's address scaled to b's element size)
+    uintptr_t al = (uintptr_t)b;
+    al |= ea == eb ? (uintptr_t)a : (ea > eb ? (uintptr_t)a >> 1 : (uintptr_t)a << 1);
+    Geometry g = make_geometry(F, b_dtype, al);
+    GradWParams P{};
+    P.col = bidx;
+    P.row = nullptr;
+    P.x = b;
+    P.g = a;
+    P.F = F;
+    P.E = E;
+    P.L = g.L;
+    P.S = g.S;
+    P.FT = g.FT;
+    P.ltot = g.ltot;
+    P.reduce = MP_SUM;
+    P.grad_w = out;
+    P.oidx = oidx;
+    return hip_status(launch_spmm_grad_w(P, b_dtype, a_dtype, g.epl, as_stream(stream)));
 }
 
 int mp_segment_matmul_workspace(int T, int64_t F, int64_t Fo, size_t* bytes) {

@@ -10,7 +10,9 @@
 //     product of grad_out[v] and x[col[p]] per CSR edge p of row v (a
 //     sampled dense-dense product).  Edge-parallel: every wavefront takes 64
 //     consecutive CSR positions, so hub rows need no special handling; the
-//     per-edge dot is reduced over the lanes of a slot in a fixed tree.
+//     per-edge dot is reduced over the lanes of a slot in a fixed tree.  With
+//     the row or column array absent (position p reads row p) the same kernel
+//     gives the per-edge dot products of the edge-materialized path.
 //
 // The gradient with respect to x reuses the aggregation kernels of spmm.hip
 // over the transposed CSR (sum, mean after scale_inv_deg, and a masked sum
@@ -145,10 +147,12 @@ __global__ __launch_bounds__(kBlock) void spmm_grad_w(GradWParams P) {
     const bool slot_ok = slot < S;
     const int64_t rem = P.E - p0;
 
+    // absent index arrays are the identity (per-edge dot products of two
+    // edge-space tables, or of one edge-space table and gathered rows)
     int32_t myc = 0, myv = 0;
     if (lane < rem) {
-        myc = __builtin_nontemporal_load(P.col + p0 + lane);
-        myv = __builtin_nontemporal_load(P.row + p0 + lane);
+        myc = P.col ? __builtin_nontemporal_load(P.col + p0 + lane) : (int32_t)(p0 + lane);
+        myv = P.row ? __builtin_nontemporal_load(P.row + p0 + lane) : (int32_t)(p0 + lane);
     }
     // the largest power of two below L: first stride of the slot reduction
     int top = 1;
@@ -212,7 +216,7 @@ __global__ __launch_bounds__(kBlock) void spmm_grad_w(GradWParams P) {
             const int64_t deg = rp_at(P.rowptr, P.rp64, (int64_t)myv + 1) - rp_at(P.rowptr, P.rp64, myv);
             result = result / (float)deg;
         }
-        P.grad_w[p0 + lane] = result;
+        P.grad_w[P.oidx ? (int64_t)P.oidx[p0 + lane] : p0 + lane] = result;
     }
 }
 

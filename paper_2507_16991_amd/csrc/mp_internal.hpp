@@ -177,8 +177,8 @@ struct SpmmParams {
 struct GradWParams {
     const void* rowptr;
     int rp64;
-    const int32_t* col;
-    const int32_t* row;     // destination row of every CSR position
+    const int32_t* col;     // row of x read by position p; nullptr: p itself
+    const int32_t* row;     // destination row of every CSR position; nullptr: p
     const void* x;          // [N_src, F]
     const void* g;          // [N_dst, F] gradient of the aggregation output
     const int32_t* argout;  // [N_dst, F] (max only)
@@ -187,6 +187,7 @@ struct GradWParams {
     int64_t ltot;
     int reduce;             // exactly one of kSum, kMean, kMax
     float* grad_w;          // [E]
+    const int32_t* oidx;    // nullptr, or grad_w[oidx[p]] receives position p's dot
 };
 hipError_t launch_rows_of_edges(const void* rowptr, int rp64, int64_t N, int64_t E, int32_t* row,
                                 hipStream_t s);
@@ -229,5 +230,36 @@ hipError_t launch_plan_chunks(const void* rowptr, int rp64, const int32_t* rowli
 // sort's exclusive digit starts), header[nclass] = N, header[nclass+1] = chunks
 hipError_t launch_plan_header(const uint32_t* class_start, int nclass, const uint32_t* chunk_off,
                               int64_t N, uint32_t* header, hipStream_t s);
+
+// ---- edge-materialized messages (messages.hip) ----------------------------------
+struct MessageGather {
+    const int32_t* idx;  // [E] row of x of every message
+    const float* w;      // [E] or nullptr
+    const void* x;       // [N_src, F]
+    int x_bf16;
+    void* msg;           // [E, F]: fp32, or bf16 (unweighted bf16 x, an exact copy)
+    int msg_bf16;
+    int64_t E, F;
+    int epl;             // elements per lane-chunk (message_epl)
+};
+struct MessageBackward {
+    const void* rowptr;
+    int rp64;
+    const int32_t* row;     // [E] destination row of every CSR position
+    const int32_t* argout;  // [N_dst, F] (max only)
+    const void* g;          // [N_dst, F] dL/dout
+    int g_bf16;
+    int64_t E, F;
+    int reduce;             // exactly one of kSum, kMean, kMax
+    int epl;
+    float* dmsg;            // [E, F]
+};
+// Largest lane-chunk width in {max_epl, ..., 2, 1} that divides F, keeps each
+// listed element size within 16 bytes per access and divides every pointer.
+int message_epl(int64_t F, const uintptr_t* ptrs, const int* elem_bytes, int n, int max_epl);
+hipError_t launch_message_gather(const MessageGather& a, hipStream_t s);
+hipError_t launch_message_scale(const float* in, float* out, const float* mask,
+                                const int32_t* idx, int64_t E, int64_t F, int epl, hipStream_t s);
+hipError_t launch_message_backward(const MessageBackward& a, hipStream_t s);
 
 }  // namespace mp

@@ -31,8 +31,8 @@ def test_exports_every_declared_function():
 
 def test_version_and_status_strings():
     assert mp.mp_version() == 1
-    for st in range(-8, 1):
-        assert mp.mp_status_str(st)
+    for st in range(-9, 1):
+        assert mp.mp_status_str(st) != "unknown status"
     assert mp.mp_status_str(-99) == "unknown status"
 
 
@@ -272,3 +272,90 @@ def test_validate_errors():
     assert L.mp_validate_sorted(FAKE, -1, FAKE, None) == -2
     assert L.mp_validate_coo(FAKE, FAKE, 10, 5, 5, None, None) == -1
     assert L.mp_validate_csr(FAKE, 4, FAKE, 5, 5, 10, FAKE, None) == -3
+
+
+# ---- edge-materialized messages -------------------------------------------------------
+
+def test_message_gather_argument_errors():
+    L = mp.lib()
+    F32, BF16 = mp.MP_F32, mp.MP_BF16
+    assert L.mp_message_gather(FAKE, None, FAKE, 5, 10, 10, 4, FAKE, F32, None) == -3
+    assert L.mp_message_gather(FAKE, None, FAKE, F32, 10, 10, 4, FAKE, BF16, None) == -3
+    assert L.mp_message_gather(FAKE, FAKE, FAKE, BF16, 10, 10, 4, FAKE, BF16, None) == -3
+    assert L.mp_message_gather(FAKE, None, FAKE, F32, 10, -1, 4, FAKE, F32, None) == -2
+    assert L.mp_message_gather(FAKE, None, FAKE, F32, 10, 10, 0, FAKE, F32, None) == -2
+    assert L.mp_message_gather(FAKE, None, FAKE, F32, 10, 2**31, 4, FAKE, F32, None) == -2
+    assert L.mp_message_gather(None, None, FAKE, F32, 10, 10, 4, FAKE, F32, None) == -1
+    assert L.mp_message_gather(FAKE, None, FAKE, F32, 10, 10, 4, None, F32, None) == -1
+    assert L.mp_message_gather(FAKE, None, FAKE, F32, 10, 10, 4, FAKE + 2, F32, None) == -8
+    assert L.mp_message_gather(None, None, None, F32, 0, 0, 4, None, F32, None) == 0
+
+
+def test_message_scale_argument_errors():
+    L = mp.lib()
+    assert L.mp_message_scale(FAKE, FAKE, 10, 4, None, None, 10, None) == -1
+    assert L.mp_message_scale(FAKE, FAKE, 10, 4, FAKE, None, 9, None) == -2
+    assert L.mp_message_scale(FAKE, FAKE, 10, 0, FAKE, None, 10, None) == -2
+    assert L.mp_message_scale(FAKE + 2, FAKE, 10, 4, FAKE, None, 10, None) == -8
+    assert L.mp_message_scale(None, None, 0, 4, None, None, 0, None) == 0
+
+
+def test_message_aggregate_argument_errors():
+    L = mp.lib()
+    F32, BF16 = mp.MP_F32, mp.MP_BF16
+    args = lambda **k: [k.get("plan"), k.get("rowptr", FAKE), mp.MP_I32, FAKE,
+                        k.get("mdt", F32), k.get("E", 100), 10, 4, k.get("reduce", mp.MP_SUM),
+                        FAKE, F32, FAKE, k.get("xdt", F32), FAKE, None, 0, None]
+    assert L.mp_message_aggregate(*args(reduce=3)) == -4
+    assert L.mp_message_aggregate(*args(rowptr=None)) == -1
+    assert L.mp_message_aggregate(*args(E=2**31)) == -2
+    assert L.mp_message_aggregate(*args(reduce=mp.MP_MAX, xdt=BF16)) == -3
+
+
+def test_materialized_checks_everything_before_the_callback():
+    L = mp.lib()
+    calls = []
+    cb = mp.MESSAGE_FN(lambda *a: calls.append(a) or 0)
+    F32 = mp.MP_F32
+
+    def call(reduce=mp.MP_SUM, msg=FAKE, col=FAKE, E=100, msg_dtype=F32):
+        return L.mp_spmm_materialized(None, FAKE, mp.MP_I32, col, None, FAKE, F32, 50, 10, E, 4,
+                                      msg, msg_dtype, ctypes.cast(cb, ctypes.c_void_p), None,
+                                      reduce, FAKE, F32, FAKE, F32, FAKE, None, 0, None)
+
+    assert call(reduce=3) == -4
+    assert call(msg=None) == -1
+    assert call(col=None) == -1
+    assert call(E=-1) == -2
+    assert call(msg_dtype=mp.MP_BF16) == -3
+    assert calls == []
+
+
+def test_message_backward_argument_errors():
+    L = mp.lib()
+    F32 = mp.MP_F32
+    assert mp.mp_message_backward_workspace(0) == 0
+    assert mp.mp_message_backward_workspace(1000) >= 4000
+    assert L.mp_message_backward(FAKE, mp.MP_I32, None, FAKE, F32, 10, 100, 4, 3, FAKE, FAKE,
+                                 1 << 20, None) == -4
+    assert L.mp_message_backward(FAKE, mp.MP_I32, None, FAKE, F32, 10, 100, 4, mp.MP_MAX, FAKE,
+                                 FAKE, 1 << 20, None) == -1
+    assert L.mp_message_backward(FAKE, mp.MP_I32, None, FAKE, F32, 10, 100, 4, mp.MP_SUM, FAKE,
+                                 FAKE, 16, None) == -5
+    assert L.mp_message_backward(FAKE, mp.MP_I32, None, FAKE, F32, 0, 100, 4, mp.MP_SUM, FAKE,
+                                 FAKE, 1 << 20, None) == -2
+    assert L.mp_message_backward(FAKE, mp.MP_I32, None, None, F32, 10, 0, 4, mp.MP_SUM, None,
+                                 None, 0, None) == 0
+
+
+def test_edge_dot_and_csr_rows_argument_errors():
+    L = mp.lib()
+    F32 = mp.MP_F32
+    assert L.mp_edge_dot(FAKE, F32, FAKE, F32, None, 5, None, 10, 4, FAKE, None) == -2
+    assert L.mp_edge_dot(FAKE, 3, FAKE, F32, FAKE, 5, None, 10, 4, FAKE, None) == -3
+    assert L.mp_edge_dot(None, F32, FAKE, F32, FAKE, 5, None, 10, 4, FAKE, None) == -1
+    assert L.mp_edge_dot(FAKE + 2, F32, FAKE, F32, FAKE, 5, None, 10, 4, FAKE, None) == -8
+    assert L.mp_edge_dot(None, F32, None, F32, None, 0, None, 0, 4, None, None) == 0
+    assert L.mp_csr_rows(FAKE, mp.MP_I32, 0, 10, FAKE, None) == -2
+    assert L.mp_csr_rows(FAKE, mp.MP_I32, 5, 10, None, None) == -1
+    assert L.mp_csr_rows(FAKE + 4, mp.MP_I64, 5, 10, FAKE, None) == -8
