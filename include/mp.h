@@ -426,8 +426,10 @@ typedef int (*mp_message_fn)(void* msg, int msg_dtype, int64_t E, int64_t F, voi
 
 /* Explanation-mode aggregation: msg = gather (as mp_message_gather with
  * idx = col), then c(msg, ...) if c is not NULL, then the aggregation of
- * msg (as mp_message_aggregate).  With c NULL the outputs equal mp_spmm's up
- * to the order of floating-point sums (max and argout exactly).
+ * msg (as mp_message_aggregate).  With c NULL the max and argout equal
+ * mp_spmm's exactly, and so do unweighted fp32 sums; a weighted mp_spmm may
+ * fuse each product into its sum (one rounding fewer), so weighted sums agree
+ * within rounding.
  *   msg  caller's [E, F] table of msg_dtype (left holding the messages
  *        after the callback).
  * Every argument of the three steps is checked before anything is enqueued.
