@@ -41,6 +41,7 @@ BACKWARD = "chunglu-124M-backward"
 STACKED = "chunglu-124M-stacked"
 PROJECTION = "hetero-20M-projection"
 READOUT = "readout-2.4M"
+EXPLAIN = "chunglu-124M-explain"
 DOMINANT = "spmm_main<float, 4, true, false, 1, false, 0>"  # fp32 sum, the largest launch of a step
 # the dominant kernel's source: spmm.hip and the aggregation section of the
 # internal header (file, first line marker or None, end marker or None)
@@ -164,7 +165,7 @@ def build_step(args, mp, torch, np, dev):
     t0 = time.time()
     if args.workload == PROJECTION:
         return projection_step(args, mp, torch, np, dev)
-    if args.workload == BACKWARD:
+    if args.workload in (BACKWARD, EXPLAIN):
         g = graphgen.workload(WORKLOAD, seed=args.seed, bf16=False)
     elif args.workload in (STACKED, READOUT):
         g = graphgen.workload(WORKLOAD, seed=args.seed)
@@ -207,6 +208,8 @@ def build_step(args, mp, torch, np, dev):
 
     if args.workload == BACKWARD:
         return backward_step(g, mp, torch, np, dev, mark)
+    if args.workload == EXPLAIN:
+        return explain_step(g, mp, torch, np, dev, mark, args.seed)
     if args.workload == STACKED:
         return stacked_step(g, mp, torch, np, dev, mark)
     if args.workload == READOUT:
@@ -342,6 +345,74 @@ def backward_step(g, mp, torch, np, dev, mark):
         mp.mp_spmm_backward_w(rowptr, it, col, x, mp.MP_F32, G, mp.MP_F32, None, N, N, E, F,
                               mp.MP_SUM, gw, ws_w, ws_w.numel())
         mark(evs, i + 1)
+
+    return g, step, ops
+
+
+def explain_step(g, mp, torch, np, dev, mark, seed):
+    """One explainer iteration on the headline graph in explanation mode:
+    messages materialized in edge space (fp32, 49.5 GB), an edge mask applied
+    by the callback, sum aggregation, then the backward pass: dL/dmsg, the
+    mask gradient (COO order), the callback's input gradient, and dL/dx over
+    the transposed CSR with forward positions as columns.  The CSR, its
+    transpose and their plans are built once before timing (the cached
+    EdgeIndex formats); the mask is U(0.5, 1) per COO edge and the output
+    gradient N(0,1)."""
+    import graphgen
+
+    N, E, F = g.n_dst, g.E, g.F
+    it = mp.MP_I32
+    src = torch.from_numpy(g.src).to(dev)
+    dst = torch.from_numpy(g.dst).to(dev)
+    rowptr, col, perm, _ = mp.coo_to_csr(src, dst, N, want_perm=True)
+    del src, dst
+    rowptrT, _, posT, _ = mp.csr_transpose(rowptr, col, N)
+    x = torch.from_numpy(g.x).to(dev)
+    mask = torch.from_numpy(graphgen.uniform_f32(seed, 9, E) * np.float32(0.25)
+                            + np.float32(0.75)).to(dev)
+    G = torch.from_numpy(graphgen.normal_f32(1, 11, N * F).reshape(N, F)).to(dev)
+    plan = mp.Plan(rowptr, E, F)
+    planT = mp.Plan(rowptrT, E, F)
+    m_pre = torch.empty(E, F, dtype=torch.float32, device=dev)
+    m = torch.empty(E, F, dtype=torch.float32, device=dev)  # masked messages, then dL/dm_pre
+    dm = torch.empty(E, F, dtype=torch.float32, device=dev)
+    out = torch.empty(N, F, dtype=torch.float32, device=dev)
+    gx = torch.empty(N, F, dtype=torch.float32, device=dev)
+    dmask = torch.empty(E, dtype=torch.float32, device=dev)
+    ws_b = torch.empty(mp.mp_message_backward_workspace(E), dtype=torch.uint8, device=dev)
+    ws_f = plan.workspace(mp.MP_SUM)
+    ws_t = planT.workspace(mp.MP_SUM)
+    torch.cuda.synchronize()
+    EF4 = E * F * 4
+    rp = 4 * (N + 1)
+    ops = [("msg_gather_f32", 4 * E + 2 * EF4, 0),
+           ("mask_callback", 8 * E + 2 * EF4, 0),
+           ("msg_sum", rp + EF4 + N * F * 4, E * F),
+           ("msg_backward_sum", rp + 8 * E + N * F * 4 + EF4, 0),
+           ("mask_grad", 2 * EF4 + 8 * E, 0),
+           ("msg_input_grad", 8 * E + 2 * EF4, 0),
+           ("grad_x_sum", rp + 4 * E + EF4 + N * F * 4, E * F)]
+    nb = lambda t: 0 if t is None else t.numel()
+
+    def step(evs=None):
+        mark(evs, 0)
+        mp.mp_message_gather(col, None, x, mp.MP_F32, N, E, F, m_pre, mp.MP_F32)
+        mark(evs, 1)
+        mp.mp_message_scale(m_pre, m, E, F, mask, perm, E)
+        mark(evs, 2)
+        mp.mp_message_aggregate(plan.handle, rowptr, it, m, mp.MP_F32, E, N, F, mp.MP_SUM, out,
+                                mp.MP_F32, None, mp.MP_F32, None, ws_f, nb(ws_f))
+        mark(evs, 3)
+        mp.mp_message_backward(rowptr, it, None, G, mp.MP_F32, N, E, F, mp.MP_SUM, dm, ws_b,
+                               ws_b.numel())
+        mark(evs, 4)
+        mp.mp_edge_dot(dm, mp.MP_F32, m_pre, mp.MP_F32, None, E, perm, E, F, dmask)
+        mark(evs, 5)
+        mp.mp_message_scale(dm, m, E, F, mask, perm, E)
+        mark(evs, 6)
+        mp.mp_spmm(planT.handle, rowptrT, it, posT, None, m, mp.MP_F32, E, N, F, mp.MP_SUM, gx,
+                   mp.MP_F32, None, mp.MP_F32, None, ws_t, nb(ws_t))
+        mark(evs, 7)
 
     return g, step, ops
 
@@ -514,6 +585,13 @@ OP_KERNELS = {
     "grad_x_mean_f32": "spmm_main (sum over the transposed CSR of G/deg)",
     "grad_x_max_f32": "spmm_main, masked (argmax routing over the transposed CSR)",
     "grad_w_sum_f32": "spmm_grad_w (per-edge dot products)",
+    "msg_gather_f32": "message_gather (edge-space gather of x rows)",
+    "mask_callback": "message_scale (edge mask)",
+    "msg_sum": "spmm_main over message rows",
+    "msg_backward_sum": "message_backward (dL/dmsg)",
+    "mask_grad": "spmm_grad_w as per-edge dot products",
+    "msg_input_grad": "message_scale (callback input gradient)",
+    "grad_x_sum": "spmm_main over the transposed CSR, message rows gathered by position",
 }
 
 
@@ -568,7 +646,7 @@ def run(args):
     value = step_bytes / (ms_step * 1e-3) / 1e9
     web = args.workload == "web-1.6B"
     headline = args.workload == WORKLOAD
-    dom = max((o for o in ops if o[2] > 0 or args.workload == PROJECTION),
+    dom = max((o for o in ops if o[2] > 0 or args.workload in (PROJECTION, EXPLAIN)),
               key=lambda o: op_ms[o[0]])[0]
     dom_kernel = DOMINANT + ", fp32 sum" if headline else OP_KERNELS.get(dom, f"spmm_main ({dom})")
     if headline:
@@ -598,6 +676,10 @@ def run(args):
                   f"1024 graphs of a sorted batch vector, seed {args.seed}",
                   "ptr from the sorted batch + plan + readout {sum, mean, max, std} x "
                   "{fp32, bf16}"),
+        EXPLAIN: (f"{EXPLAIN}: the Chung-Lu graph of {WORKLOAD} (N={N}, E={E}, F={F}, fp32 "
+                  f"x and output gradient N(0,1), edge mask U(0.5, 1)), seed {args.seed}",
+                  "materialized messages + edge-mask callback + sum + dL/dmsg + mask gradient "
+                  "+ callback input gradient + dL/dx"),
         BACKWARD: (f"{BACKWARD}: the Chung-Lu graph of {WORKLOAD} (N={N}, E={E}, F={F}, fp32 "
                    f"x and output gradient N(0,1)), seed {args.seed}",
                    "CSR transpose + plan + dL/dx {sum, mean, max} + dL/dw sum"),
@@ -779,7 +861,7 @@ def main():
     ap.add_argument("--warmup", type=int, default=2)
     ap.add_argument("--seed", type=int, default=0)
     ap.add_argument("--workload", default=WORKLOAD,
-                    choices=[WORKLOAD, BACKWARD, STACKED, READOUT, PROJECTION, "web-1.6B",
+                    choices=[WORKLOAD, BACKWARD, STACKED, READOUT, PROJECTION, EXPLAIN, "web-1.6B",
                              "powerlaw-1.2M", "uniform-10k", "hetero-20M"],
                     help="benchmark workload (the default is the metric's configuration)")
     ap.add_argument("--cpu-rows", type=int, default=0,
