@@ -19,7 +19,7 @@
 // lane-chunks of EPL elements (one vector access each): consecutive threads
 // take consecutive chunks, so the table side is read and written fully
 // coalesced, and a gathered feature row is read by consecutive lanes.  Each
-// thread handles kItems chunks spaced one block apart, issuing all index
+// thread handles a few chunks spaced one block apart, issuing all index
 // loads, then all row loads, before any store.
 #include <type_traits>
 
@@ -29,8 +29,10 @@ namespace mp {
 namespace {
 
 constexpr int kBlock = 256;
+// lane-chunks per thread: 4 for the gather and the scale, 8 for the
+// gradient (its loads hit the caches, its stores stream: more in flight)
 constexpr int kItems = 4;
-constexpr int64_t kChunksPerBlock = (int64_t)kBlock * kItems;
+constexpr int kItemsBackward = 8;
 
 __device__ inline float bf16_bits(uint32_t b) { return __uint_as_float(b << 16); }
 
@@ -121,25 +123,27 @@ __device__ inline void load_ints(const int32_t* p, int32_t (&v)[EPL]) {
 }
 
 // The chunks of this thread in virtual block vb: chunk g = vb * kBlock *
-// kItems + i * kBlock + tid lies in table row p = g / cpr at lane-chunk
+// ITEMS + i * kBlock + tid lies in table row p = g / cpr at lane-chunk
 // k = g % cpr.  One 64-bit division per virtual block (uniform), 32-bit
 // divisions per chunk.  Virtual blocks are walked with a grid stride, so the
 // grid stays within the launch limits for any table size.
+template <int ITEMS>
 struct ChunkPos {
-    int64_t g[kItems];
-    int64_t p[kItems];
-    int32_t k[kItems];
-    bool ok[kItems];
+    int64_t g[ITEMS];
+    int64_t p[ITEMS];
+    int32_t k[ITEMS];
+    bool ok[ITEMS];
 };
 
-__device__ inline ChunkPos chunk_positions(int64_t vb, int64_t total, int64_t cpr) {
-    ChunkPos c;
-    const int64_t g0 = vb * kChunksPerBlock;
+template <int ITEMS>
+__device__ inline ChunkPos<ITEMS> chunk_positions(int64_t vb, int64_t total, int64_t cpr) {
+    ChunkPos<ITEMS> c;
+    const int64_t g0 = vb * (int64_t)(kBlock * ITEMS);
     const int64_t p0 = g0 / cpr;
     const uint32_t r0 = (uint32_t)(g0 - p0 * cpr);
     const uint32_t ucpr = (uint32_t)cpr;
 #pragma unroll
-    for (int i = 0; i < kItems; ++i) {
+    for (int i = 0; i < ITEMS; ++i) {
         const uint32_t local = r0 + (uint32_t)(i * kBlock) + threadIdx.x;
         const uint32_t dp = local / ucpr;
         c.g[i] = g0 + i * kBlock + threadIdx.x;
@@ -151,15 +155,16 @@ __device__ inline ChunkPos chunk_positions(int64_t vb, int64_t total, int64_t cp
 }
 
 // Virtual blocks of the table: the grid walks them with a stride.
+template <int ITEMS>
 __device__ inline int64_t vblocks(int64_t total) {
-    return (total + kChunksPerBlock - 1) / kChunksPerBlock;
+    return (total + kBlock * ITEMS - 1) / (kBlock * ITEMS);
 }
 
 // msg[p, k-th chunk] = (w[p] *) x[idx[p], k-th chunk].  TM = float: the
 // fp32 message (one correctly rounded product when weighted); TM = uint16_t:
 // an unweighted bf16 row copied unchanged.
 template <typename TX, typename TM, int EPL, bool W>
-__device__ inline void gather_vblock(const ChunkPos& c, const int32_t* __restrict__ idx,
+__device__ inline void gather_vblock(const ChunkPos<kItems>& c, const int32_t* __restrict__ idx,
                                      const float* __restrict__ w, const TX* __restrict__ x,
                                      int64_t F, TM* __restrict__ msg) {
     int32_t src[kItems];
@@ -200,9 +205,9 @@ __global__ __launch_bounds__(kBlock) void message_gather(const int32_t* __restri
                                                          const TX* __restrict__ x, int64_t F,
                                                          int64_t cpr, int64_t total,
                                                          TM* __restrict__ msg) {
-    const int64_t nvb = vblocks(total);
+    const int64_t nvb = vblocks<kItems>(total);
     for (int64_t vb = blockIdx.x; vb < nvb; vb += gridDim.x)
-        gather_vblock<TX, TM, EPL, W>(chunk_positions(vb, total, cpr), idx, w, x, F, msg);
+        gather_vblock<TX, TM, EPL, W>(chunk_positions<kItems>(vb, total, cpr), idx, w, x, F, msg);
 }
 
 // out[p, :] = in[p, :] * mask[idx ? idx[p] : p], fp32, one rounding.
@@ -212,9 +217,9 @@ __global__ __launch_bounds__(kBlock) void message_scale(const float* __restrict_
                                                         const float* __restrict__ mask,
                                                         const int32_t* __restrict__ idx,
                                                         int64_t cpr, int64_t total) {
-    const int64_t nvb = vblocks(total);
+    const int64_t nvb = vblocks<kItems>(total);
     for (int64_t vb = blockIdx.x; vb < nvb; vb += gridDim.x) {
-        const ChunkPos c = chunk_positions(vb, total, cpr);
+        const ChunkPos<kItems> c = chunk_positions<kItems>(vb, total, cpr);
         float s[kItems], v[kItems][EPL];
 #pragma unroll
         for (int i = 0; i < kItems; ++i) {
@@ -243,19 +248,20 @@ __device__ inline int64_t rp_load(const void* rp, int rp64, int64_t i) {
 // sum g[v, :]; mean g[v, :] / deg(v) (correctly rounded; in fp64 for degrees
 // beyond 2^24, which fp32 cannot hold); max g[v, f] where argout[v, f] == p.
 template <typename TG, int EPL, int MODE>
-__device__ inline void backward_vblock(const ChunkPos& c, const void* __restrict__ rowptr, int rp64,
+__device__ inline void backward_vblock(const ChunkPos<kItemsBackward>& c,
+                                       const void* __restrict__ rowptr, int rp64,
                                        const int32_t* __restrict__ row,
                                        const int32_t* __restrict__ argout,
                                        const TG* __restrict__ g, int64_t F,
                                        float* __restrict__ dmsg) {
-    int32_t v[kItems];
+    int32_t v[kItemsBackward];
 #pragma unroll
-    for (int i = 0; i < kItems; ++i) v[i] = c.ok[i] ? row[c.p[i]] : 0;
-    float gv[kItems][EPL];
-    int32_t am[MODE == kMax ? kItems : 1][EPL];
-    int64_t deg[kItems];
+    for (int i = 0; i < kItemsBackward; ++i) v[i] = c.ok[i] ? row[c.p[i]] : 0;
+    float gv[kItemsBackward][EPL];
+    int32_t am[MODE == kMax ? kItemsBackward : 1][EPL];
+    int64_t deg[kItemsBackward];
 #pragma unroll
-    for (int i = 0; i < kItems; ++i) {
+    for (int i = 0; i < kItemsBackward; ++i) {
         deg[i] = 1;
         if (!c.ok[i]) continue;
         const int64_t o = (int64_t)v[i] * F + (int64_t)c.k[i] * EPL;
@@ -265,7 +271,7 @@ __device__ inline void backward_vblock(const ChunkPos& c, const void* __restrict
             deg[i] = rp_load(rowptr, rp64, (int64_t)v[i] + 1) - rp_load(rowptr, rp64, v[i]);
     }
 #pragma unroll
-    for (int i = 0; i < kItems; ++i) {
+    for (int i = 0; i < kItemsBackward; ++i) {
         if (!c.ok[i]) continue;
         float d[EPL];
 #pragma unroll
@@ -292,17 +298,17 @@ __global__ __launch_bounds__(kBlock) void message_backward(const void* __restric
                                                            const TG* __restrict__ g, int64_t F,
                                                            int64_t cpr, int64_t total,
                                                            float* __restrict__ dmsg) {
-    const int64_t nvb = vblocks(total);
+    const int64_t nvb = vblocks<kItemsBackward>(total);
     for (int64_t vb = blockIdx.x; vb < nvb; vb += gridDim.x)
-        backward_vblock<TG, EPL, MODE>(chunk_positions(vb, total, cpr), rowptr, rp64, row,
-                                       argout, g, F, dmsg);
+        backward_vblock<TG, EPL, MODE>(chunk_positions<kItemsBackward>(vb, total, cpr), rowptr,
+                                       rp64, row, argout, g, F, dmsg);
 }
 
 // Launch at most this many blocks; larger tables are walked by the grid stride.
 constexpr int64_t kMaxGrid = int64_t(1) << 20;
 
-unsigned grid_for(int64_t total) {
-    const int64_t b = ceil_div(total, kChunksPerBlock);
+unsigned grid_for(int64_t total, int items = kItems) {
+    const int64_t b = ceil_div(total, (int64_t)kBlock * items);
     return (unsigned)(b < kMaxGrid ? b : kMaxGrid);
 }
 
@@ -343,7 +349,7 @@ template <typename TG, int EPL>
 hipError_t backward_mode(const MessageBackward& a, hipStream_t s) {
     const int64_t cpr = a.F / EPL, total = a.E * cpr;
     const TG* g = static_cast<const TG*>(a.g);
-    const dim3 grid(grid_for(total)), block(kBlock);
+    const dim3 grid(grid_for(total, kItemsBackward)), block(kBlock);
     if (a.reduce == kMax)
         hipLaunchKernelGGL((message_backward<TG, EPL, kMax>), grid, block, 0, s, a.rowptr, a.rp64,
                            a.row, a.argout, g, a.F, cpr, total, a.dmsg);
