@@ -170,17 +170,33 @@ __global__ __launch_bounds__(kBlock) void spmm_grad_w(GradWParams P) {
             const int64_t fe = chunk * EPL;
             float xv[U][EPL], gv[U][EPL];
             int32_t mv[MODE == kMax ? U : 1][EPL];
-            bool ok[U];
+            bool ok[U], fresh[U];
+            int32_t vprev = -1;
 #pragma unroll
             for (int u = 0; u < U; ++u) {
                 const int t = base + u * S + slot;
                 const int32_t c = __shfl(myc, t & (kWave - 1));
                 const int32_t v = __shfl(myv, t & (kWave - 1));
                 ok[u] = feat_ok && t < kWave && t < rem;
+                // consecutive edges of a slot mostly share their row: its
+                // gradient chunk (and argmax chunk) is loaded once and reused
+                fresh[u] = u == 0 || v != vprev;
+                vprev = v;
                 if (ok[u]) {
                     load_vals<TX, EPL>(reinterpret_cast<const TX*>(P.x) + (int64_t)c * P.F + fe, xv[u]);
-                    load_vals<TG, EPL>(reinterpret_cast<const TG*>(P.g) + (int64_t)v * P.F + fe, gv[u]);
-                    if constexpr (MODE == kMax) load_ints<EPL>(P.argout + (int64_t)v * P.F + fe, mv[u]);
+                    if (fresh[u]) {
+                        load_vals<TG, EPL>(reinterpret_cast<const TG*>(P.g) + (int64_t)v * P.F + fe, gv[u]);
+                        if constexpr (MODE == kMax) load_ints<EPL>(P.argout + (int64_t)v * P.F + fe, mv[u]);
+                    }
+                }
+            }
+#pragma unroll
+            for (int u = 1; u < U; ++u) {
+                if (fresh[u]) continue;  // a valid edge's predecessor in the slot is valid
+#pragma unroll
+                for (int k = 0; k < EPL; ++k) {
+                    gv[u][k] = gv[u - 1][k];
+                    if constexpr (MODE == kMax) mv[u][k] = mv[u - 1][k];
                 }
             }
 #pragma unroll
