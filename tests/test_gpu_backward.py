@@ -136,6 +136,32 @@ def mixed():
     return graphgen.mixed_graph(0, f=64)
 
 
+@pytest.mark.parametrize("F,gdtype", [(24, torch.float32), (24, torch.bfloat16), (7, torch.float32)])
+@pytest.mark.parametrize("with_rowptr", [False, True])
+def test_backward_max_long_rows(F, gdtype, with_rowptr):
+    """Destination rows of up to 70,000 edges (positions beyond 16 bits
+    within a row), empty and single-edge rows; the forward rowptr is optional
+    for the max gradient."""
+    degs = [1, 100, 65535, 65536, 65537, 0, 300, 70000, 3]
+    n_dst = len(degs)
+    n_src = 5000
+    dst = np.repeat(np.arange(n_dst, dtype=np.int32), degs)
+    src = graphgen.uniform_ints(5, 1, dst.size, n_src)
+    shuffle = graphgen.permutation(5, 4, dst.size)
+    src, dst = src[shuffle], dst[shuffle]
+    x = graphgen.normal_f32(5, 3, n_src * F).reshape(n_src, F)
+    rp_o, col_o, _, _ = oracle.coo_to_csr(src, dst, n_dst, n_src=n_src)
+    am_o = oracle.spmm(rp_o, col_o, x=x, want=("max",))["argmax"]
+    G, gkw = grad_input(2, n_dst, F, gdtype)
+    rpt, colt, post, _, _ = check_transpose(rp_o, col_o, n_src)
+    gx = mp.spmm_backward_x(rpt, colt, G, mp.MP_MAX, posT=post,
+                            rowptr=dev(rp_o.astype(np.int32)) if with_rowptr else None,
+                            argout=dev(am_o.astype(np.int32)))
+    torch.cuda.synchronize()
+    ref, scale = oracle.spmm_backward_x(rp_o, col_o, n_src, "max", argout=am_o, **gkw)
+    assert scaled_error(gx.cpu().numpy(), ref, scale) <= TOL[gdtype]
+
+
 @pytest.mark.parametrize("reduce", ["sum", "mean", "max"])
 @pytest.mark.parametrize("gdtype", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("weighted", [False, True])
