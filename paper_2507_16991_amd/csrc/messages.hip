@@ -317,11 +317,15 @@ hipError_t gather_w(const MessageGather& a, hipStream_t s) {
     const int64_t cpr = a.F / EPL, total = a.E * cpr;
     const TX* x = static_cast<const TX*>(a.x);
     if (a.msg_bf16) {
-        if constexpr (std::is_same<TX, uint16_t>::value)
+        // a bf16 table is only the exact copy of unweighted bf16 rows
+        if constexpr (std::is_same<TX, uint16_t>::value) {
             hipLaunchKernelGGL((message_gather<TX, uint16_t, EPL, false>), dim3(grid_for(total)),
                                dim3(kBlock), 0, s, a.idx, a.w, x, a.F, cpr, total,
                                static_cast<uint16_t*>(a.msg));
-        return hipGetLastError();
+            return hipGetLastError();
+        } else {
+            return hipErrorInvalidValue;
+        }
     }
     if (a.w)
         hipLaunchKernelGGL((message_gather<TX, float, EPL, true>), dim3(grid_for(total)),
