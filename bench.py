@@ -252,13 +252,22 @@ def build_step(args, mp, torch, np, dev):
         reds = [("sum", mp.MP_SUM, False)]
     else:
         reds = [("sum", mp.MP_SUM, False), ("mean", mp.MP_MEAN, False), ("max", mp.MP_MAX, False)]
+    # a feature table whose rows are not whole cache lines is first copied
+    # into rows a whole number of lines apart (once per step, shared by the
+    # table's aggregations): each gathered row then touches the fewest lines
     calls = []
     for k, (x, xd, xb) in xs.items():
+        ld = mp.aligned_ld(F, x.dtype)
+        if ld != F:
+            xp = torch.empty(N, ld, dtype=x.dtype, device=dev)[:, :F]
+            ops.append((f"layout_{k}", 2 * N * F * xb, 0))
+            calls.append(("layout", k, x, xp, xd, ld))
+            x = xp
         for rn, red, wt in reds:
             mb = 4 if k == "f32" else 2
             ops.append((f"{rn}_{k}", spmm_bytes(N, E, F, xb, red, max_b=mb, rowptr_b=rp_b, w=wt),
                         E * F))
-            calls.append((k, x, xd, red, wt))
+            calls.append(("spmm", k, x, xd, red, wt, ld))
 
     plans = {}
     wss = {}
@@ -275,7 +284,14 @@ def build_step(args, mp, torch, np, dev):
         plans["h"] = mp.mp_spmm_plan_build(rowptr, it, N, E, F, xs[k0][1], plan_buf, nplan)
         mark(evs, 2)
         i = 2
-        for k, x, xd, red, wt in calls:
+        for c in calls:
+            if c[0] == "layout":
+                _, k, x, xp, xd, ld = c
+                mp.mp_copy_rows(x, F, xp, ld, N, F, xd)
+                i += 1
+                mark(evs, i)
+                continue
+            _, k, x, xd, red, wt, ld = c
             h = plans["h"]
             nb = mp.mp_spmm_workspace(h, red)
             key = (k, red)
@@ -283,7 +299,7 @@ def build_step(args, mp, torch, np, dev):
                 wss[key] = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
             hs = bool(red & (mp.MP_SUM | mp.MP_MEAN))
             hm = bool(red & mp.MP_MAX)
-            mp.mp_spmm(h, rowptr, it, col, w_csr if wt else None, x, xd, N, N, F, red,
+            mp.mp_spmm(h, rowptr, it, col, w_csr if wt else None, x, xd, N, N, F, ld, red,
                        out if hs else None, mp.MP_F32, mx[k] if hm else None, xd,
                        arg if hm else None, wss[key], wss[key].numel())
             i += 1
@@ -412,7 +428,7 @@ def explain_step(g, mp, torch, np, dev, mark, seed):
         mark(evs, 5)
         mp.mp_message_scale(dm, m, E, F, mask, None, E)
         mark(evs, 6)
-        mp.mp_spmm(planT.handle, rowptrT, it, posT, None, m, mp.MP_F32, E, N, F, mp.MP_SUM, gx,
+        mp.mp_spmm(planT.handle, rowptrT, it, posT, None, m, mp.MP_F32, E, N, F, F, mp.MP_SUM, gx,
                    mp.MP_F32, None, mp.MP_F32, None, ws_t, nb(ws_t))
         mark(evs, 7)
 
@@ -442,8 +458,14 @@ def stacked_step(g, mp, torch, np, dev, mark):
              torch.empty(N, F, dtype=torch.int32, device=dev) if n in ("max", "min") else None)
             for n in PNA]
     ops = [("csr", csr_bytes(N, E), 0), ("plan", plan_bytes(N), 0)]
-    for k, (_, _, xb) in xs.items():
+    tables = []  # (key, x, dtype code, row stride, padded copy or None)
+    for k, (x, xd, xb) in xs.items():
+        ld = mp.aligned_ld(F, x.dtype)
+        xp = torch.empty(N, ld, dtype=x.dtype, device=dev)[:, :F] if ld != F else None
+        if xp is not None:
+            ops.append((f"layout_{k}", 2 * N * F * xb, 0))
         ops.append((f"stacked_{k}", multi_bytes(N, E, F, xb, PNA), E * F))
+        tables.append((k, x, xd, ld, xp))
     plans, wss = {}, {}
 
     def step(evs=None):
@@ -459,8 +481,13 @@ def stacked_step(g, mp, torch, np, dev, mark):
         if "ws" not in wss or wss["ws"].numel() < nb:
             wss["ws"] = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
         i = 2
-        for k, (x, xd, _) in xs.items():
-            mp.mp_spmm_multi(h, rowptr, it, col, None, x, xd, N, N, F, outs, wss["ws"],
+        for k, x, xd, ld, xp in tables:
+            if xp is not None:
+                mp.mp_copy_rows(x, F, xp, ld, N, F, xd)
+                i += 1
+                mark(evs, i)
+                x = xp
+            mp.mp_spmm_multi(h, rowptr, it, col, None, x, xd, N, N, F, ld, outs, wss["ws"],
                              wss["ws"].numel())
             i += 1
             mark(evs, i)
@@ -513,7 +540,7 @@ def readout_step(g, mp, torch, np, dev, mark, seed):
             wss["ws"] = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
         i = 2
         for k, (x, xd, _) in xs.items():
-            mp.mp_readout_multi(h, ptr, mp.MP_I32, x, xd, N, B, F, outs, wss["ws"],
+            mp.mp_readout_multi(h, ptr, mp.MP_I32, x, xd, N, B, F, F, outs, wss["ws"],
                                 wss["ws"].numel())
             i += 1
             mark(evs, i)

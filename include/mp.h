@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define MP_VERSION 1
+#define MP_VERSION 2
 
 /* Status codes. */
 typedef enum mp_status {
@@ -169,7 +169,10 @@ int mp_spmm_workspace(const mp_plan* plan, int reduce, size_t* bytes);
  *               no workspace); a mismatch returns MP_ERR_PLAN.
  *   rowptr      [N_dst+1] of rowptr_itype; col [rowptr[N_dst]] int32.
  *   w           [E] fp32 in CSR order, or NULL (unweighted).
- *   x           [N_src, F] row-major, x_dtype (MP_F32 or MP_BF16).
+ *   x           [N_src, F] of x_dtype (MP_F32 or MP_BF16), row r starting
+ *               at element r * ldx (ldx >= F; ldx = F for a contiguous
+ *               table).  A row stride whose row bytes are a multiple of 128
+ *               starts every row on a cache line (see mp_copy_rows).
  *   reduce      MP_SUM, MP_MEAN, MP_MAX, MP_SUM|MP_MAX or MP_MEAN|MP_MAX.
  *   out         [N_dst, F] of out_dtype: the sum or mean (required iff
  *               reduce has SUM or MEAN).  Accumulation is fp32; a bf16 output
@@ -184,12 +187,22 @@ int mp_spmm_workspace(const mp_plan* plan, int reduce, size_t* bytes);
  * compared with '>' so that -0.0 and +0.0 tie and the earlier edge wins.
  * A weighted message for MAX is the fp32 product fl32(w * x); sums may fuse
  * the multiply into the add.  Size limits: 0 <= N_src, N_dst <= INT32_MAX,
- * 1 <= F <= 65536, E <= INT32_MAX (argout and col are int32).
+ * 1 <= F <= 65536, ldx >= F, E <= INT32_MAX (argout and col are int32).
  * Asynchronous on `stream` (no host synchronization when plan != NULL). */
 int mp_spmm(const mp_plan* plan, const void* rowptr, int rowptr_itype, const int32_t* col,
             const float* w, const void* x, int x_dtype, int64_t N_src, int64_t N_dst,
-            int64_t F, int reduce, void* out, int out_dtype, void* out_max, int max_dtype,
-            int32_t* argout, void* ws, size_t ws_bytes, void* stream);
+            int64_t F, int64_t ldx, int reduce, void* out, int out_dtype, void* out_max,
+            int max_dtype, int32_t* argout, void* ws, size_t ws_bytes, void* stream);
+
+/* Feature-table layout: out[r, 0:F] = in[r, 0:F] for 0 <= r < N, rows of in
+ * ld_in and rows of out ld_out elements apart (ld_in, ld_out >= F; padding
+ * elements of out are not written; in and out must not overlap).  Used to
+ * give a table whose rows are not a multiple of the 128-byte cache line a
+ * stride that is (e.g. bf16 rows of F = 100 stored 128 elements apart), so
+ * that each row gathered by the aggregation touches the fewest lines.
+ * dtype: MP_F32 or MP_BF16.  Asynchronous on `stream`. */
+int mp_copy_rows(const void* in, int64_t ld_in, void* out, int64_t ld_out, int64_t N, int64_t F,
+                 int dtype, void* stream);
 
 /* ---------------------------------------------------------------------------
  * Stacked aggregations (Sec. 2.2, "Aggregations as a First-Class Principle":
@@ -220,22 +233,24 @@ typedef struct mp_aggr_out {
 int mp_spmm_multi_workspace(const mp_plan* plan, size_t* bytes);
 
 /* Stacked aggregation over the destination-major CSR: arguments as in
- * mp_spmm (x fp32 or bf16, optional CSR-order weights w, plan optional), plus
- * n_out (1..6) outputs described by the host array outs.  Duplicate or
- * unknown aggregators give MP_ERR_REDUCE.  Asynchronous on `stream`. */
+ * mp_spmm (x fp32 or bf16 with row stride ldx >= F, optional CSR-order
+ * weights w, plan optional), plus n_out (1..6) outputs described by the host
+ * array outs.  Duplicate or unknown aggregators give MP_ERR_REDUCE.
+ * Asynchronous on `stream`. */
 int mp_spmm_multi(const mp_plan* plan, const void* rowptr, int rowptr_itype, const int32_t* col,
                   const float* w, const void* x, int x_dtype, int64_t N_src, int64_t N_dst,
-                  int64_t F, int n_out, const mp_aggr_out* outs, void* ws, size_t ws_bytes,
-                  void* stream);
+                  int64_t F, int64_t ldx, int n_out, const mp_aggr_out* outs, void* ws,
+                  size_t ws_bytes, void* stream);
 
 /* Global readout: the same stacked aggregation over segments of consecutive
  * node rows, given by ptr [N_seg+1] (the CSR of a sorted batch vector, e.g.
  * from mp_sorted_coo_to_csr of (node id, batch)); ptr[N_seg] must equal
- * N_nodes.  x is [N_nodes, F]; arg holds node indices.  plan (optional) is
- * built on ptr with N_seg rows and E = N_nodes. */
+ * N_nodes.  x is [N_nodes, F] with row stride ldx >= F; arg holds node
+ * indices.  plan (optional) is built on ptr with N_seg rows and E = N_nodes. */
 int mp_readout_multi(const mp_plan* plan, const void* ptr, int ptr_itype, const void* x,
-                     int x_dtype, int64_t N_nodes, int64_t N_seg, int64_t F, int n_out,
-                     const mp_aggr_out* outs, void* ws, size_t ws_bytes, void* stream);
+                     int x_dtype, int64_t N_nodes, int64_t N_seg, int64_t F, int64_t ldx,
+                     int n_out, const mp_aggr_out* outs, void* ws, size_t ws_bytes,
+                     void* stream);
 
 /* ---------------------------------------------------------------------------
  * Backward pass (Sec. 2.2: the backward pass of an aggregation over A runs

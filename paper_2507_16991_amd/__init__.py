@@ -37,7 +37,7 @@ __all__ = [
     "mp_message_scale", "mp_message_aggregate", "mp_spmm_materialized",
     "mp_message_backward_workspace", "mp_message_backward", "mp_edge_dot", "csr_rows",
     "message_gather", "message_scale", "message_aggregate", "spmm_materialized",
-    "message_backward", "edge_dot",
+    "message_backward", "edge_dot", "mp_copy_rows", "aligned_ld", "pad_rows",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -98,8 +98,9 @@ def lib():
         L.mp_spmm_plan_free.argtypes = [p]
         L.mp_spmm_plan_free.restype = None
         L.mp_spmm_workspace.argtypes = [p, i32, psz]
-        L.mp_spmm.argtypes = [p, p, i32, p, p, p, i32, i64, i64, i64, i32, p, i32, p, i32, p, p,
-                              sz, p]
+        L.mp_spmm.argtypes = [p, p, i32, p, p, p, i32, i64, i64, i64, i64, i32, p, i32, p, i32, p,
+                              p, sz, p]
+        L.mp_copy_rows.argtypes = [p, i64, p, i64, i64, i64, i32, p]
         L.mp_hetero_build_workspace.argtypes = [i32, p, i32, p, i32, i32, psz]
         L.mp_hetero_build.argtypes = [i32, p, i32, p, i32, p, i32, p, p, sz, p]
         L.mp_hetero_spmm.argtypes = [i32, p, p, i32, i64, i32, p, p, i32, p, i32, p, i32, p, sz,
@@ -112,8 +113,9 @@ def lib():
         L.mp_segment_matmul_backward_workspace.argtypes = [p, i32, i64, i64, psz]
         L.mp_segment_matmul_backward.argtypes = [p, i32, p, p, p, i64, i64, p, i32, p, p, sz, p]
         L.mp_spmm_multi_workspace.argtypes = [p, psz]
-        L.mp_spmm_multi.argtypes = [p, p, i32, p, p, p, i32, i64, i64, i64, i32, p, p, sz, p]
-        L.mp_readout_multi.argtypes = [p, p, i32, p, i32, i64, i64, i64, i32, p, p, sz, p]
+        L.mp_spmm_multi.argtypes = [p, p, i32, p, p, p, i32, i64, i64, i64, i64, i32, p, p, sz,
+                                    p]
+        L.mp_readout_multi.argtypes = [p, p, i32, p, i32, i64, i64, i64, i64, i32, p, p, sz, p]
         L.mp_csr_transpose_workspace.argtypes = [i64, i64, i32, i32, psz]
         L.mp_csr_transpose.argtypes = [p, i32, p, i64, i64, i64, p, i32, p, p, p, p, p, sz, p]
         L.mp_spmm_backward_x_workspace.argtypes = [p, i64, i64, i32, psz]
@@ -132,7 +134,7 @@ def lib():
         L.mp_message_backward_workspace.argtypes = [i64, psz]
         L.mp_message_backward.argtypes = [p, i32, p, p, i32, i64, i64, i64, i32, p, p, sz, p]
         L.mp_edge_dot.argtypes = [p, i32, p, i32, p, i64, p, i64, i64, p, p]
-        for name in ("mp_csr_rows", "mp_message_gather", "mp_message_scale",
+        for name in ("mp_copy_rows", "mp_csr_rows", "mp_message_gather", "mp_message_scale",
                      "mp_message_aggregate", "mp_spmm_materialized",
                      "mp_message_backward_workspace", "mp_message_backward", "mp_edge_dot",
                      "mp_coo_to_csr_workspace", "mp_coo_to_csr", "mp_sorted_coo_to_csr",
@@ -164,6 +166,16 @@ def _ptr(t):
         # only when nothing was ever allocated, see _edge_array)
         return t.untyped_storage().data_ptr() + t.storage_offset() * t.element_size() or None
     return t.data_ptr()
+
+
+def _rows_ptr(t):
+    """Address of a 2-D table whose rows may be strided (stride(1) == 1,
+    stride(0) >= shape[1]), and that stride in elements."""
+    if t.dim() != 2 or (t.shape[0] > 1 and t.stride(1) != 1) or t.stride(0) < t.shape[1]:
+        raise ValueError("feature tables passed to libmp must have unit column stride")
+    if t.numel() == 0:
+        return _ptr(t.contiguous()), int(t.shape[1])
+    return t.data_ptr(), int(t.stride(0)) if t.shape[0] > 1 else int(t.shape[1])
 
 
 def _stream(stream):
@@ -258,12 +270,21 @@ def mp_spmm_workspace(plan_handle, reduce) -> int:
     return _bytes("mp_spmm_workspace", plan_handle, reduce)
 
 
-def mp_spmm(plan_handle, rowptr, rowptr_itype, col, w, x, x_dtype, N_src, N_dst, F, reduce, out,
-            out_dtype, out_max, max_dtype, argout, ws, ws_bytes, stream=None):
+def mp_spmm(plan_handle, rowptr, rowptr_itype, col, w, x, x_dtype, N_src, N_dst, F, ldx, reduce,
+            out, out_dtype, out_max, max_dtype, argout, ws, ws_bytes, stream=None):
+    """x: a tensor (its row stride is used when strided) or a raw address."""
+    xp = _rows_ptr(x)[0] if isinstance(x, torch.Tensor) else x
     _check("mp_spmm", lib().mp_spmm(
-        plan_handle, _ptr(rowptr), rowptr_itype, _ptr(col), _ptr(w), _ptr(x), x_dtype, N_src,
-        N_dst, F, reduce, _ptr(out), out_dtype, _ptr(out_max), max_dtype, _ptr(argout), _ptr(ws),
-        ws_bytes, _stream(stream)))
+        plan_handle, _ptr(rowptr), rowptr_itype, _ptr(col), _ptr(w), xp, x_dtype, N_src,
+        N_dst, F, ldx, reduce, _ptr(out), out_dtype, _ptr(out_max), max_dtype, _ptr(argout),
+        _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def mp_copy_rows(x_in, ld_in, x_out, ld_out, N, F, dtype, stream=None):
+    pi = _rows_ptr(x_in)[0] if isinstance(x_in, torch.Tensor) else x_in
+    po = _rows_ptr(x_out)[0] if isinstance(x_out, torch.Tensor) else x_out
+    _check("mp_copy_rows", lib().mp_copy_rows(pi, ld_in, po, ld_out, N, F, dtype,
+                                              _stream(stream)))
 
 
 def _rel_array(rels):
@@ -350,19 +371,21 @@ def _aggr_array(outs):
     return arr
 
 
-def mp_spmm_multi(plan_handle, rowptr, rowptr_itype, col, w, x, x_dtype, N_src, N_dst, F, outs,
-                  ws, ws_bytes, stream=None):
+def mp_spmm_multi(plan_handle, rowptr, rowptr_itype, col, w, x, x_dtype, N_src, N_dst, F, ldx,
+                  outs, ws, ws_bytes, stream=None):
     arr = _aggr_array(outs)
+    xp = _rows_ptr(x)[0] if isinstance(x, torch.Tensor) else x
     _check("mp_spmm_multi", lib().mp_spmm_multi(
-        plan_handle, _ptr(rowptr), rowptr_itype, _ptr(col), _ptr(w), _ptr(x), x_dtype, N_src,
-        N_dst, F, len(outs), arr, _ptr(ws), ws_bytes, _stream(stream)))
+        plan_handle, _ptr(rowptr), rowptr_itype, _ptr(col), _ptr(w), xp, x_dtype, N_src,
+        N_dst, F, ldx, len(outs), arr, _ptr(ws), ws_bytes, _stream(stream)))
 
 
-def mp_readout_multi(plan_handle, ptr, ptr_itype, x, x_dtype, N_nodes, N_seg, F, outs, ws,
+def mp_readout_multi(plan_handle, ptr, ptr_itype, x, x_dtype, N_nodes, N_seg, F, ldx, outs, ws,
                      ws_bytes, stream=None):
     arr = _aggr_array(outs)
+    xp = _rows_ptr(x)[0] if isinstance(x, torch.Tensor) else x
     _check("mp_readout_multi", lib().mp_readout_multi(
-        plan_handle, _ptr(ptr), ptr_itype, _ptr(x), x_dtype, N_nodes, N_seg, F, len(outs), arr,
+        plan_handle, _ptr(ptr), ptr_itype, xp, x_dtype, N_nodes, N_seg, F, ldx, len(outs), arr,
         _ptr(ws), ws_bytes, _stream(stream)))
 
 
@@ -549,8 +572,9 @@ def spmm(rowptr, col, x, reduce, *, w=None, plan: Plan | None = None, out_dtype=
     if hm and argout is None:
         argout = torch.empty(N_dst, F, dtype=torch.int32, device=dev)
     ws = plan.workspace(reduce) if plan is not None else None
+    ldx = _rows_ptr(x)[1]
     mp_spmm(plan.handle if plan is not None else None, rowptr, _itype_code(rowptr.dtype), col, w,
-            x, _dtype_code(x.dtype), N_src, N_dst, F, reduce, out if hs else None,
+            x, _dtype_code(x.dtype), N_src, N_dst, F, ldx, reduce, out if hs else None,
             _dtype_code(out.dtype) if hs else MP_F32, out_max if hm else None,
             _dtype_code(out_max.dtype) if hm else MP_F32, argout if hm else None, ws,
             0 if ws is None else ws.numel(), stream)
@@ -636,7 +660,7 @@ def spmm_multi(rowptr, col, x, aggrs, *, w=None, plan: Plan | None = None, strea
     nb = mp_spmm_multi_workspace(h)
     ws = _workspace(nb, x.device) if nb else None
     mp_spmm_multi(h, rowptr, _itype_code(rowptr.dtype), col, w, x, _dtype_code(x.dtype), N_src,
-                  N_dst, F, outs, ws, 0 if ws is None else ws.numel(), stream)
+                  N_dst, F, _rows_ptr(x)[1], outs, ws, 0 if ws is None else ws.numel(), stream)
     return res
 
 
@@ -650,7 +674,7 @@ def readout(ptr, x, aggrs, *, plan: Plan | None = None, stream=None):
     nb = mp_spmm_multi_workspace(h)
     ws = _workspace(nb, x.device) if nb else None
     mp_readout_multi(h, ptr, _itype_code(ptr.dtype), x, _dtype_code(x.dtype), N_nodes, N_seg, F,
-                     outs, ws, 0 if ws is None else ws.numel(), stream)
+                     _rows_ptr(x)[1], outs, ws, 0 if ws is None else ws.numel(), stream)
     return res
 
 
@@ -707,6 +731,40 @@ def hetero_spmm(N_per_type, x_per_type, dst_type, rowptr, col, *, plan: Plan | N
                    plan.handle if plan is not None else None, rowptr, _itype_code(rowptr.dtype),
                    col, MP_SUM, out, _dtype_code(out.dtype), ws, 0 if ws is None else ws.numel(),
                    stream)
+    return out
+
+
+# ---- feature-table layout --------------------------------------------------------------
+
+CACHE_LINE = 128
+
+
+def aligned_ld(F: int, dtype) -> int:
+    """Row stride (elements) for a table of F-element rows: F itself, or the
+    next stride whose row bytes are a multiple of the 128-byte cache line when
+    that makes a randomly gathered row touch fewer lines on average (rows of
+    at least one line, padded by at most half their size)."""
+    b = torch.tensor([], dtype=dtype).element_size()
+    rb = F * b
+    if rb % CACHE_LINE == 0 or rb < CACHE_LINE:
+        return F
+    step = __import__("math").gcd(rb, CACHE_LINE)
+    offs = range(0, CACHE_LINE, step)
+    lines = sum(-(-(o + rb) // CACHE_LINE) for o in offs) / len(offs)
+    padded = -(-rb // CACHE_LINE)
+    if padded < lines and 2 * padded * CACHE_LINE <= 3 * rb:
+        return padded * CACHE_LINE // b
+    return F
+
+
+def pad_rows(x, ld=None, *, out=None, stream=None):
+    """x [N, F] copied into rows ld elements apart (default aligned_ld);
+    returns the [N, F] view of the padded [N, ld] buffer."""
+    N, F = int(x.shape[0]), int(x.shape[1])
+    ld = aligned_ld(F, x.dtype) if ld is None else int(ld)
+    if out is None:
+        out = torch.empty(max(N, 1), ld, dtype=x.dtype, device=x.device)[:N, :F]
+    mp_copy_rows(x, _rows_ptr(x)[1], out, _rows_ptr(out)[1], N, F, _dtype_code(x.dtype), stream)
     return out
 
 

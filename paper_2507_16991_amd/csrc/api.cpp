@@ -174,6 +174,7 @@ namespace {
 // generic layout) and launch the main kernel plus the hub fix-up.
 int run_spmm(const mp_plan* plan, SpmmParams& P, const Geometry& g, int x_dtype, int64_t N_dst,
              void* ws, size_t ws_bytes, hipStream_t s) {
+    if (P.ldx == 0) P.ldx = P.F;  // contiguous feature rows
     P.L = g.L;
     P.S = g.S;
     P.FT = g.FT;
@@ -272,9 +273,11 @@ int fill_multi_outputs(int n_out, const mp_aggr_out* outs, int64_t rows, SpmmPar
 
 int multi_impl(const mp_plan* plan, const void* rowptr, int rowptr_itype, const int32_t* col,
                const float* w, const void* x, int x_dtype, int64_t N_src, int64_t N_dst, int64_t F,
-               int n_out, const mp_aggr_out* outs, void* ws, size_t ws_bytes, hipStream_t s) {
+               int64_t ldx, int n_out, const mp_aggr_out* outs, void* ws, size_t ws_bytes,
+               hipStream_t s) {
     if (!valid_itype(rowptr_itype) || !valid_dtype(x_dtype)) return MP_ERR_DTYPE;
-    if (N_src < 0 || N_src > INT32_MAX || N_dst < 0 || N_dst > INT32_MAX || F < 1 || F > 65536)
+    if (N_src < 0 || N_src > INT32_MAX || N_dst < 0 || N_dst > INT32_MAX || F < 1 || F > 65536 ||
+        ldx < F)
         return MP_ERR_SIZE;
     if (!rowptr) return MP_ERR_NULL;
     if (N_dst > 0 && !x) return MP_ERR_NULL;
@@ -288,7 +291,7 @@ int multi_impl(const mp_plan* plan, const void* rowptr, int rowptr_itype, const 
         (uintptr_t)col % 4 || (uintptr_t)w % 4)
         return MP_ERR_ALIGN;
     if (N_dst == 0) return MP_OK;
-    Geometry g = make_geometry(F, x_dtype, (uintptr_t)x);
+    Geometry g = make_geometry(F, x_dtype, (uintptr_t)x | (uintptr_t)(ldx * eb));
     P.rowptr = rowptr;
     P.rp64 = rowptr_itype == MP_I64;
     P.col = col;
@@ -296,6 +299,7 @@ int multi_impl(const mp_plan* plan, const void* rowptr, int rowptr_itype, const 
     P.n_tables = 1;
     P.table_ptr[0] = static_cast<const char*>(x);
     P.F = F;
+    P.ldx = ldx;
     return run_spmm(plan, P, g, x_dtype, N_dst, ws, ws_bytes, s);
 }
 
@@ -312,6 +316,7 @@ struct SpmmCall {
     const void* x;
     int x_dtype;
     int64_t N_src, N_dst, F;
+    int64_t ldx;  // row stride of x in elements (>= F)
     int reduce;
     void* out;
     int out_dtype;
@@ -333,7 +338,7 @@ int spmm_check(const SpmmCall& c) {
     if (hm && c.max_dtype == MP_BF16 && (c.x_dtype != MP_BF16 || c.w != nullptr))
         return MP_ERR_DTYPE;
     if (c.N_src < 0 || c.N_src > INT32_MAX || c.N_dst < 0 || c.N_dst > INT32_MAX || c.F < 1 ||
-        c.F > 65536)
+        c.F > 65536 || c.ldx < c.F)
         return MP_ERR_SIZE;
     if (!c.rowptr) return MP_ERR_NULL;
     if (c.N_dst > 0) {
@@ -358,7 +363,8 @@ int spmm_check(const SpmmCall& c) {
 // Enqueue a checked aggregation.
 int spmm_launch(const SpmmCall& c, hipStream_t s) {
     if (c.N_dst == 0) return MP_OK;
-    Geometry g = make_geometry(c.F, c.x_dtype, (uintptr_t)c.x);
+    const int eb = c.x_dtype == MP_BF16 ? 2 : 4;
+    Geometry g = make_geometry(c.F, c.x_dtype, (uintptr_t)c.x | (uintptr_t)(c.ldx * eb));
     SpmmParams P{};
     P.rowptr = c.rowptr;
     P.rp64 = c.rowptr_itype == MP_I64;
@@ -368,6 +374,7 @@ int spmm_launch(const SpmmCall& c, hipStream_t s) {
     P.table_ptr[0] = static_cast<const char*>(c.x);
     P.table_off[0] = 0;
     P.F = c.F;
+    P.ldx = c.ldx;
     P.reduce = c.reduce;
     P.out = c.out;
     P.out_bf16 = c.out_dtype == MP_BF16;
@@ -618,28 +625,29 @@ int mp_spmm_multi_workspace(const mp_plan* plan, size_t* bytes) {
 
 int mp_spmm_multi(const mp_plan* plan, const void* rowptr, int rowptr_itype, const int32_t* col,
                   const float* w, const void* x, int x_dtype, int64_t N_src, int64_t N_dst,
-                  int64_t F, int n_out, const mp_aggr_out* outs, void* ws, size_t ws_bytes,
-                  void* stream) {
+                  int64_t F, int64_t ldx, int n_out, const mp_aggr_out* outs, void* ws,
+                  size_t ws_bytes, void* stream) {
     if (N_dst > 0 && !col) return MP_ERR_NULL;
-    return multi_impl(plan, rowptr, rowptr_itype, col, w, x, x_dtype, N_src, N_dst, F, n_out, outs,
-                      ws, ws_bytes, as_stream(stream));
+    return multi_impl(plan, rowptr, rowptr_itype, col, w, x, x_dtype, N_src, N_dst, F, ldx, n_out,
+                      outs, ws, ws_bytes, as_stream(stream));
 }
 
 int mp_readout_multi(const mp_plan* plan, const void* ptr, int ptr_itype, const void* x,
-                     int x_dtype, int64_t N_nodes, int64_t N_seg, int64_t F, int n_out,
-                     const mp_aggr_out* outs, void* ws, size_t ws_bytes, void* stream) {
+                     int x_dtype, int64_t N_nodes, int64_t N_seg, int64_t F, int64_t ldx,
+                     int n_out, const mp_aggr_out* outs, void* ws, size_t ws_bytes,
+                     void* stream) {
     // segments of consecutive node rows: the CSR of the sorted batch vector,
     // whose column of position p is p itself
-    return multi_impl(plan, ptr, ptr_itype, nullptr, nullptr, x, x_dtype, N_nodes, N_seg, F, n_out,
-                      outs, ws, ws_bytes, as_stream(stream));
+    return multi_impl(plan, ptr, ptr_itype, nullptr, nullptr, x, x_dtype, N_nodes, N_seg, F, ldx,
+                      n_out, outs, ws, ws_bytes, as_stream(stream));
 }
 
 int mp_spmm(const mp_plan* plan, const void* rowptr, int rowptr_itype, const int32_t* col,
             const float* w, const void* x, int x_dtype, int64_t N_src, int64_t N_dst, int64_t F,
-            int reduce, void* out, int out_dtype, void* out_max, int max_dtype, int32_t* argout,
-            void* ws, size_t ws_bytes, void* stream) {
+            int64_t ldx, int reduce, void* out, int out_dtype, void* out_max, int max_dtype,
+            int32_t* argout, void* ws, size_t ws_bytes, void* stream) {
     if (N_dst > 0 && !col) return MP_ERR_NULL;
-    SpmmCall c{plan, rowptr, rowptr_itype, col, w, x, x_dtype, N_src, N_dst, F, reduce,
+    SpmmCall c{plan, rowptr, rowptr_itype, col, w, x, x_dtype, N_src, N_dst, F, ldx, reduce,
                out, out_dtype, out_max, max_dtype, argout, ws, ws_bytes};
     const int st = spmm_check(c);
     return st != MP_OK ? st : spmm_launch(c, as_stream(stream));
@@ -830,6 +838,19 @@ int mp_spmm_backward_w(const void* rowptr, int rowptr_itype, const int32_t* col,
     return hip_status(launch_spmm_grad_w(P, x_dtype, g_dtype, g.epl, s));
 }
 
+// ---- feature-table layout --------------------------------------------------------
+
+int mp_copy_rows(const void* in, int64_t ld_in, void* out, int64_t ld_out, int64_t N, int64_t F,
+                 int dtype, void* stream) {
+    if (!valid_dtype(dtype)) return MP_ERR_DTYPE;
+    if (N < 0 || F < 1 || ld_in < F || ld_out < F) return MP_ERR_SIZE;
+    if (N == 0) return MP_OK;
+    if (!in || !out) return MP_ERR_NULL;
+    const int eb = dtype == MP_BF16 ? 2 : 4;
+    if ((uintptr_t)in % eb || (uintptr_t)out % eb) return MP_ERR_ALIGN;
+    return hip_status(launch_copy_rows(in, ld_in, out, ld_out, N, F, eb, as_stream(stream)));
+}
+
 // ---- edge-materialized messages ------------------------------------------------
 
 int mp_csr_rows(const void* rowptr, int rowptr_itype, int64_t N_dst, int64_t E, int32_t* row,
@@ -870,7 +891,7 @@ int mp_message_aggregate(const mp_plan* plan, const void* rowptr, int rowptr_ity
                          int reduce, void* out, int out_dtype, void* out_max, int max_dtype,
                          int32_t* argout, void* ws, size_t ws_bytes, void* stream) {
     if (E < 0 || E > INT32_MAX) return MP_ERR_SIZE;
-    SpmmCall c{plan, rowptr, rowptr_itype, nullptr, nullptr, msg, msg_dtype, E, N_dst, F,
+    SpmmCall c{plan, rowptr, rowptr_itype, nullptr, nullptr, msg, msg_dtype, E, N_dst, F, F,
                reduce, out, out_dtype, out_max, max_dtype, argout, ws, ws_bytes};
     const int st = spmm_check(c);
     return st != MP_OK ? st : spmm_launch(c, as_stream(stream));
@@ -887,7 +908,7 @@ int mp_spmm_materialized(const mp_plan* plan, const void* rowptr, int rowptr_ity
     MessageGather a{};
     int st = gather_check(col, w, x, x_dtype, N_src, E, F, msg, msg_dtype, &a);
     if (st != MP_OK) return st;
-    SpmmCall agg{plan, rowptr, rowptr_itype, nullptr, nullptr, msg, msg_dtype, E, N_dst, F,
+    SpmmCall agg{plan, rowptr, rowptr_itype, nullptr, nullptr, msg, msg_dtype, E, N_dst, F, F,
                  reduce, out, out_dtype, out_max, max_dtype, argout, ws, ws_bytes};
     st = spmm_check(agg);
     if (st != MP_OK) return st;

@@ -108,7 +108,8 @@ struct Geometry {
     int64_t ltot;    // lane-chunks per feature row
     int L, S, FT;    // lanes per slot, slots per wave, feature tiles
 };
-// x_align: the feature pointer value(s), OR-ed (only the low bits matter).
+// x_align: the feature pointer value(s) and row strides in bytes, OR-ed
+// (only the low bits matter).
 Geometry make_geometry(int64_t F, int x_dtype, uintptr_t x_align);
 
 // Degree classes of the plan (keys of the row sort).
@@ -129,9 +130,10 @@ struct SpmmParams {
     const char* table_ptr[MP_MAX_TYPES];
     int64_t table_off[MP_MAX_TYPES + 1];
     // byte offset from table_ptr[0] such that global row c of table t starts
-    // at table_ptr[0] + voff[t] + c * F * elem_bytes
+    // at table_ptr[0] + voff[t] + c * ldx * elem_bytes
     int64_t voff[MP_MAX_TYPES];
     int64_t F;
+    int64_t ldx;  // row stride of the feature tables in elements (>= F)
     int L, S, FT;
     int64_t ltot;
     // work list (waves, in launch order): hub chunks, mid rows, small groups
@@ -261,5 +263,10 @@ hipError_t launch_message_gather(const MessageGather& a, hipStream_t s);
 hipError_t launch_message_scale(const float* in, float* out, const float* mask,
                                 const int32_t* idx, int64_t E, int64_t F, int epl, hipStream_t s);
 hipError_t launch_message_backward(const MessageBackward& a, hipStream_t s);
+
+// ---- feature-table layout (layout.hip) -------------------------------------------
+// out[r, 0:F] = in[r, 0:F] for r < N, rows ld_in / ld_out elements apart.
+hipError_t launch_copy_rows(const void* in, int64_t ld_in, void* out, int64_t ld_out, int64_t N,
+                            int64_t F, int elem_bytes, hipStream_t s);
 
 }  // namespace mp

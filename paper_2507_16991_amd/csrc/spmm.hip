@@ -109,21 +109,21 @@ __device__ inline int64_t load_rp(const void* rp, int rp64, int64_t i) {
     return rp64 ? static_cast<const int64_t*>(rp)[i] : (int64_t) static_cast<const int32_t*>(rp)[i];
 }
 
-// Address of feature element `fe` of source row c.  With NT > 1 tables
-// (typed nodes; NT is a compile-time bound on n_tables), c is a global id and
-// its table is the last one whose offset is <= c: one compare and one 64-bit
-// select per table.  Addresses stay offsets from the first table's pointer,
-// so loads remain global-memory loads.
+// Address of feature element `fe` of source row c (rows ldx elements apart).
+// With NT > 1 tables (typed nodes; NT is a compile-time bound on n_tables), c
+// is a global id and its table is the last one whose offset is <= c: one
+// compare and one 64-bit select per table.  Addresses stay offsets from the
+// first table's pointer, so loads remain global-memory loads.
 template <typename TX, int NT>
 __device__ inline const char* feat_addr(const SpmmParams& P, int32_t c, int64_t fe) {
     if constexpr (NT == 1) {
-        return P.table_ptr[0] + ((int64_t)c * P.F + fe) * (int64_t)sizeof(TX);
+        return P.table_ptr[0] + ((int64_t)c * P.ldx + fe) * (int64_t)sizeof(TX);
     } else {
         int64_t vo = 0;
 #pragma unroll
         for (int k = 1; k < NT; ++k)
             vo = (k < P.n_tables && c >= (int32_t)P.table_off[k]) ? P.voff[k] : vo;
-        return P.table_ptr[0] + vo + ((int64_t)c * P.F + fe) * (int64_t)sizeof(TX);
+        return P.table_ptr[0] + vo + ((int64_t)c * P.ldx + fe) * (int64_t)sizeof(TX);
     }
 }
 

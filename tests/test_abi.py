@@ -30,7 +30,7 @@ def test_exports_every_declared_function():
 
 
 def test_version_and_status_strings():
-    assert mp.mp_version() == 1
+    assert mp.mp_version() == 2
     for st in range(-9, 1):
         assert mp.mp_status_str(st) != "unknown status"
     assert mp.mp_status_str(-99) == "unknown status"
@@ -92,7 +92,7 @@ def test_plan_errors():
 
 def _spmm(**kw):
     a = dict(plan=None, rowptr=FAKE, itype=0, col=FAKE, w=None, x=FAKE, x_dtype=0, N_src=10,
-             N_dst=10, F=8, reduce=1, out=FAKE, out_dtype=0, out_max=None, max_dtype=0,
+             N_dst=10, F=8, ldx=8, reduce=1, out=FAKE, out_dtype=0, out_max=None, max_dtype=0,
              argout=None, ws=None, ws_bytes=0, stream=None)
     a.update(kw)
     return mp.lib().mp_spmm(*a.values())
@@ -113,6 +113,28 @@ def test_spmm_argument_errors():
     assert _spmm(reduce=4, out_max=FAKE, argout=None) == -1
     assert _spmm(col=None) == -1
     assert _spmm(x=FAKE + 2) == -8
+    assert _spmm(ldx=7) == -2  # rows may not overlap
+
+
+def test_copy_rows_argument_errors():
+    L = mp.lib()
+    assert L.mp_copy_rows(FAKE, 8, FAKE, 8, 10, 8, 7, None) == -3
+    assert L.mp_copy_rows(FAKE, 7, FAKE, 8, 10, 8, 0, None) == -2
+    assert L.mp_copy_rows(FAKE, 8, FAKE, 7, 10, 8, 0, None) == -2
+    assert L.mp_copy_rows(FAKE, 8, FAKE, 8, -1, 8, 0, None) == -2
+    assert L.mp_copy_rows(None, 8, FAKE, 8, 10, 8, 0, None) == -1
+    assert L.mp_copy_rows(FAKE + 2, 8, FAKE, 8, 10, 8, 0, None) == -8
+    assert L.mp_copy_rows(None, 8, None, 8, 0, 8, 0, None) == 0
+
+
+def test_aligned_row_strides():
+    import torch
+    assert mp.aligned_ld(100, torch.bfloat16) == 128   # 200-byte rows: 2.5 -> 2 lines
+    assert mp.aligned_ld(50, torch.float32) == 64
+    assert mp.aligned_ld(100, torch.float32) == 100    # 400-byte rows touch 4 lines anyway
+    assert mp.aligned_ld(64, torch.bfloat16) == 64     # already whole lines
+    assert mp.aligned_ld(24, torch.bfloat16) == 24     # below one line: never padded
+    assert mp.aligned_ld(300, torch.bfloat16) == 320
 
 
 def test_hetero_errors():
@@ -213,7 +235,7 @@ def test_multi_errors():
 
     def multi(specs, n=None, col=FAKE):
         arr = outs(*specs)
-        return L.mp_spmm_multi(None, FAKE, 0, col, None, FAKE, 0, 10, 10, 8,
+        return L.mp_spmm_multi(None, FAKE, 0, col, None, FAKE, 0, 10, 10, 8, 8,
                                len(specs) if n is None else n, arr, None, 0, None)
 
     assert multi([(mp.MP_SUM, FAKE, None), (mp.MP_SUM, FAKE, None)]) == -4  # duplicate
@@ -227,10 +249,12 @@ def test_multi_errors():
     assert multi([(mp.MP_STD, FAKE + 2, None)]) == -8
     assert multi([(mp.MP_SUM, FAKE, None)], col=None) == -1
     arr = outs((mp.MP_MEAN, FAKE, None))
-    assert L.mp_spmm_multi(None, FAKE, 0, FAKE, None, FAKE, 5, 10, 10, 8, 1, arr, None, 0,
+    assert L.mp_spmm_multi(None, FAKE, 0, FAKE, None, FAKE, 5, 10, 10, 8, 8, 1, arr, None, 0,
                            None) == -3
-    assert L.mp_readout_multi(None, FAKE, 0, FAKE, 0, 100, 10, 0, 1, arr, None, 0, None) == -2
-    assert L.mp_readout_multi(None, None, 0, FAKE, 0, 100, 10, 8, 1, arr, None, 0, None) == -1
+    assert L.mp_spmm_multi(None, FAKE, 0, FAKE, None, FAKE, 0, 10, 10, 8, 4, 1, arr, None, 0,
+                           None) == -2
+    assert L.mp_readout_multi(None, FAKE, 0, FAKE, 0, 100, 10, 0, 0, 1, arr, None, 0, None) == -2
+    assert L.mp_readout_multi(None, None, 0, FAKE, 0, 100, 10, 8, 8, 1, arr, None, 0, None) == -1
 
 
 def test_segment_matmul_errors_and_sizes():

@@ -157,6 +157,30 @@ def test_readout(use_plan, dtype):
     compare(res, rp_o, col_o, None, xkw, ALL, dtype)
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_row_strided_features(mixed, dtype):
+    """Stacked aggregation and readout over a feature table whose rows are
+    F + 28 elements apart (a view of a wider table)."""
+    g, rp_o, col_o, w_o = mixed
+    F = g.F
+    x = dev(g.x) if dtype == torch.float32 else dev(g.x_bf16.view(np.int16)).view(torch.bfloat16)
+    xkw = {"x": g.x} if dtype == torch.float32 else {"x_bf16": g.x_bf16}
+    xs = torch.zeros(g.n_src, F + 28, dtype=dtype, device=DEV)[:, :F]
+    xs.copy_(x)
+    rp = dev(rp_o.astype(np.int32))
+    plan = mp.Plan(rp, g.E, F, dtype)
+    res = mp.spmm_multi(rp, dev(col_o), xs, ALL, plan=plan)
+    torch.cuda.synchronize()
+    compare(res, rp_o, col_o, None, xkw, ALL, dtype)
+    # readout of the same rows in 7 consecutive segments
+    n = g.n_src
+    cuts = np.linspace(0, n, 8).astype(np.int64)
+    ptr = dev(cuts.astype(np.int32))
+    res = mp.readout(ptr, xs, ALL)
+    torch.cuda.synchronize()
+    compare(res, cuts, np.arange(n, dtype=np.int32), None, xkw, ALL, dtype)
+
+
 def test_readout_from_sorted_batch_vector():
     # ptr from the batch vector with the sorted-COO fast path, then the readout
     rng = np.random.default_rng(5)

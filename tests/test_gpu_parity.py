@@ -217,6 +217,47 @@ def test_spmm_feature_widths(F, dtype, monkeypatch):
             run_case(g, rp_o, col_o, w_o, dtype, reduce, True, use_plan)
 
 
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("pad", [0, 1, 4, 28])
+def test_spmm_row_stride(mixed, dtype, pad):
+    """Feature rows F + pad elements apart (a view of a wider table): an odd
+    stride forces narrower vector loads, a stride of whole cache lines is the
+    aligned layout; results equal the contiguous table's, and the oracle's."""
+    g, rp_o, col_o, w_o = mixed
+    F = g.F
+    rp, col, w = dev(rp_o.astype(np.int32)), dev(col_o), dev(w_o)
+    x = x_of(g, dtype)
+    wide = torch.zeros(g.n_src, F + pad, dtype=dtype, device=DEV)
+    xs = wide[:, :F]
+    xs.copy_(x)
+    plan = mp.Plan(rp, g.E, F, dtype)
+    for reduce in (mp.MP_SUM | mp.MP_MAX, mp.MP_MEAN):
+        a = mp.spmm(rp, col, xs, reduce, w=w, plan=plan)
+        b = mp.spmm(rp, col, x, reduce, w=w, plan=plan)
+        torch.cuda.synchronize()
+        compare_spmm(rp_o, col_o, w_o, x_f32_host(g, dtype), *a, reduce, dtype)
+        eb = x.element_size()
+        vec = lambda n: next(v for v in (16, 8, 4, 2, 1) if n % v == 0)
+        if vec((F + pad) * eb) >= vec(F * eb):  # same lane-chunks: same order, same bits
+            for u, v in zip(a, b):
+                if u is not None:
+                    assert torch.equal(u, v)
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("F,ld", [(100, 128), (3, 5), (64, 64), (300, 320)])
+def test_pad_rows(dtype, F, ld):
+    rng = np.random.default_rng(F)
+    x = torch.from_numpy(rng.standard_normal((777, F)).astype(np.float32)).to(DEV).to(dtype)
+    xp = mp.pad_rows(x, ld)
+    torch.cuda.synchronize()
+    assert xp.shape == (777, F) and xp.stride(0) == ld
+    assert torch.equal(xp, x)
+    back = mp.pad_rows(xp, F)  # strided in, contiguous out
+    torch.cuda.synchronize()
+    assert torch.equal(back, x)
+
+
 def test_spmm_signed_weights_and_ties(monkeypatch):
     g = graphgen.mixed_graph(3, f=16, signed_weights=True)
     g.x = (np.round(g.x * 2) / 2).astype(np.float32)  # coarse values: many ties
