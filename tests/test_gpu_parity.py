@@ -244,6 +244,36 @@ def test_spmm_row_stride(mixed, dtype, pad):
                     assert torch.equal(u, v)
 
 
+@pytest.mark.parametrize("F,ld,dtype", [(100, 128, torch.bfloat16), (3, 4, torch.float32),
+                                        (5, 8, torch.bfloat16), (300, 320, torch.bfloat16),
+                                        (522, 528, torch.bfloat16), (50, 64, torch.float32),
+                                        (7, 9, torch.float32)])
+@pytest.mark.parametrize("use_plan", [False, True])
+def test_spmm_padded_rows_partial_chunks(monkeypatch, F, ld, dtype, use_plan):
+    """Rows read in whole vectors that run into the row padding: the last
+    lane-chunk of a row holds fewer than EPL features, which must be neither
+    stored nor allowed to touch a neighbouring output row or hub partial."""
+    g = graphgen.mixed_graph(F, n=700, e=9000, f=F)
+    monkeypatch.setenv("MP_HUB_MIN", "128")
+    monkeypatch.setenv("MP_CHUNK", "32")
+    rp_o, col_o, _, w_o = oracle.coo_to_csr(g.src, g.dst, g.n_dst, val=g.w)
+    rp, col, w = dev(rp_o.astype(np.int32)), dev(col_o), dev(w_o)
+    x = x_of(g, dtype)
+    xs = mp.pad_rows(x, ld)
+    # poison the padding: it is read but must never reach an output
+    wide = xs.as_strided((g.n_src, ld), (ld, 1))
+    wide[:, F:] = float("nan")
+    plan = mp.Plan(rp, g.E, F, dtype) if use_plan else None
+    for reduce, wt in ((mp.MP_SUM | mp.MP_MAX, False), (mp.MP_MEAN, True), (mp.MP_MAX, True)):
+        res = mp.spmm(rp, col, xs, reduce, w=w if wt else None, plan=plan)
+        torch.cuda.synchronize()
+        compare_spmm(rp_o, col_o, w_o if wt else None, x_f32_host(g, dtype), *res, reduce, dtype)
+    stats = mp.spmm_multi(rp, col, xs, ["sum", "min", "std"], plan=plan)
+    torch.cuda.synchronize()
+    for k in ("sum", "min", "std"):
+        assert bool(torch.isfinite(stats[k]).all())
+
+
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 @pytest.mark.parametrize("F,ld", [(100, 128), (3, 5), (64, 64), (300, 320)])
 def test_pad_rows(dtype, F, ld):
