@@ -172,10 +172,7 @@ int mp_spmm_workspace(const mp_plan* plan, int reduce, size_t* bytes);
  *   x           [N_src, F] of x_dtype (MP_F32 or MP_BF16), row r starting
  *               at element r * ldx (ldx >= F; ldx = F for a contiguous
  *               table).  A row stride whose row bytes are a multiple of 128
- *               starts every row on a cache line (see mp_copy_rows).  With
- *               ldx > F, a row may be read past F up to the next multiple of
- *               16 bytes, never past ldx: those padding elements must be
- *               readable (they are never used).
+ *               starts every row on a cache line (see mp_copy_rows).
  *   reduce      MP_SUM, MP_MEAN, MP_MAX, MP_SUM|MP_MAX or MP_MEAN|MP_MAX.
  *   out         [N_dst, F] of out_dtype: the sum or mean (required iff
  *               reduce has SUM or MEAN).  Accumulation is fp32; a bf16 output

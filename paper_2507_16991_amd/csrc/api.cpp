@@ -291,7 +291,7 @@ int multi_impl(const mp_plan* plan, const void* rowptr, int rowptr_itype, const 
         (uintptr_t)col % 4 || (uintptr_t)w % 4)
         return MP_ERR_ALIGN;
     if (N_dst == 0) return MP_OK;
-    Geometry g = make_geometry(F, x_dtype, (uintptr_t)x | (uintptr_t)(ldx * eb), ldx);
+    Geometry g = make_geometry(F, x_dtype, (uintptr_t)x | (uintptr_t)(ldx * eb));
     P.rowptr = rowptr;
     P.rp64 = rowptr_itype == MP_I64;
     P.col = col;
@@ -364,7 +364,7 @@ int spmm_check(const SpmmCall& c) {
 int spmm_launch(const SpmmCall& c, hipStream_t s) {
     if (c.N_dst == 0) return MP_OK;
     const int eb = c.x_dtype == MP_BF16 ? 2 : 4;
-    Geometry g = make_geometry(c.F, c.x_dtype, (uintptr_t)c.x | (uintptr_t)(c.ldx * eb), c.ldx);
+    Geometry g = make_geometry(c.F, c.x_dtype, (uintptr_t)c.x | (uintptr_t)(c.ldx * eb));
     SpmmParams P{};
     P.rowptr = c.rowptr;
     P.rp64 = c.rowptr_itype == MP_I64;

@@ -109,10 +109,8 @@ struct Geometry {
     int L, S, FT;    // lanes per slot, slots per wave, feature tiles
 };
 // x_align: the feature pointer value(s) and row strides in bytes, OR-ed
-// (only the low bits matter).  ld: the row stride in elements (0: F); when
-// ld > F the last lane-chunk of a row may extend into the row's padding, its
-// elements beyond F read but never stored.
-Geometry make_geometry(int64_t F, int x_dtype, uintptr_t x_align, int64_t ld = 0);
+// (only the low bits matter).
+Geometry make_geometry(int64_t F, int x_dtype, uintptr_t x_align);
 
 // Degree classes of the plan (keys of the row sort).
 constexpr int kSmallClasses = 16;       // class c < 16: small row, deg < 2^c ... see plan

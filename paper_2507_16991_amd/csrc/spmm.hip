@@ -247,11 +247,9 @@ using AccFor = Acc<EPL, HS, HM, MODE == kModeStats,
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
 
-// Store the first n of EPL consecutive 4-byte values (n < EPL only in the
-// last lane-chunk of a row read from a padded table); 16-byte stores when
-// allowed (vec: whole chunk, 16-byte aligned).
+// Store EPL consecutive 4-byte values; 16-byte stores when allowed.
 template <int EPL, typename T>
-__device__ inline void store4(T* out, const T (&v)[EPL], bool vec, int n = EPL) {
+__device__ inline void store4(T* out, const T (&v)[EPL], bool vec) {
     static_assert(sizeof(T) == 4, "4-byte elements");
     if constexpr (EPL == 4 || EPL == 8) {
         if (vec) {
@@ -268,14 +266,12 @@ __device__ inline void store4(T* out, const T (&v)[EPL], bool vec, int n = EPL) 
         }
     }
 #pragma unroll
-    for (int k = 0; k < EPL; ++k)
-        if (k < n) out[k] = v[k];
+    for (int k = 0; k < EPL; ++k) out[k] = v[k];
 }
 
-// Store the first n of EPL consecutive bf16 values (as bits); 8-byte stores
-// when allowed (vec: whole chunk, aligned).
+// Store EPL consecutive bf16 values (as bits); 8/16-byte stores when allowed.
 template <int EPL>
-__device__ inline void store2(uint16_t* out, const uint16_t (&b)[EPL], bool vec, int n = EPL) {
+__device__ inline void store2(uint16_t* out, const uint16_t (&b)[EPL], bool vec) {
     if constexpr (EPL == 4 || EPL == 8) {
         if (vec) {
 #pragma unroll
@@ -289,21 +285,7 @@ __device__ inline void store2(uint16_t* out, const uint16_t (&b)[EPL], bool vec,
         }
     }
 #pragma unroll
-    for (int k = 0; k < EPL; ++k)
-        if (k < n) out[k] = b[k];
-}
-
-// Valid features of the lane-chunk at fe (fewer than EPL only in the last
-// chunk of a row read from a padded table), and whether the chunk's outputs
-// can be written with vector stores (a whole chunk at an offset aligned to 4
-// elements, from 16-byte aligned output arrays).
-template <int EPL>
-__device__ inline int chunk_valid(const SpmmParams& P, int64_t fe) {
-    return P.F - fe < EPL ? (int)(P.F - fe) : EPL;
-}
-template <int EPL>
-__device__ inline bool chunk_vec(const SpmmParams& P, int64_t o, int n) {
-    return P.vec_store != 0 && n == EPL && (o & 3) == 0;
+    for (int k = 0; k < EPL; ++k) out[k] = b[k];
 }
 
 template <int EPL>
@@ -311,8 +293,7 @@ __device__ inline void store_row(const SpmmParams& P, int64_t row, int64_t fe, i
                                  const float (&s)[EPL], const float (&m)[EPL],
                                  const int32_t (&idx)[EPL], bool hs, bool hm) {
     const int64_t o = row * P.F + fe;
-    const int n = chunk_valid<EPL>(P, fe);
-    const bool vec = chunk_vec<EPL>(P, o, n);
+    const bool vec = P.vec_store != 0;
     if (hs) {
         float v[EPL];
         const bool mean = (P.reduce & kMean) != 0;
@@ -323,9 +304,9 @@ __device__ inline void store_row(const SpmmParams& P, int64_t row, int64_t fe, i
             uint16_t b[EPL];
 #pragma unroll
             for (int k = 0; k < EPL; ++k) b[k] = to_bf16(v[k]);
-            store2<EPL>(static_cast<uint16_t*>(P.out) + o, b, vec, n);
+            store2<EPL>(static_cast<uint16_t*>(P.out) + o, b, vec);
         } else {
-            store4<EPL>(static_cast<float*>(P.out) + o, v, vec, n);
+            store4<EPL>(static_cast<float*>(P.out) + o, v, vec);
         }
     }
     if (hm) {
@@ -337,11 +318,11 @@ __device__ inline void store_row(const SpmmParams& P, int64_t row, int64_t fe, i
             uint16_t b[EPL];
 #pragma unroll
             for (int k = 0; k < EPL; ++k) b[k] = (uint16_t)(__float_as_uint(mv[k]) >> 16);
-            store2<EPL>(static_cast<uint16_t*>(P.out_max) + o, b, vec, n);
+            store2<EPL>(static_cast<uint16_t*>(P.out_max) + o, b, vec);
         } else {
-            store4<EPL>(static_cast<float*>(P.out_max) + o, mv, vec, n);
+            store4<EPL>(static_cast<float*>(P.out_max) + o, mv, vec);
         }
-        store4<EPL>(P.argout + o, idx, vec, n);
+        store4<EPL>(P.argout + o, idx, vec);
     }
 }
 
@@ -351,10 +332,8 @@ template <int EPL>
 __device__ inline void store_stats(const SpmmParams& P, int64_t row, int64_t fe, int64_t deg,
                                    const float (&s)[EPL], const float (&q)[EPL],
                                    const float (&m)[EPL], const int32_t (&im)[EPL],
-                                   const float (&n)[EPL], const int32_t (&in)[EPL]) {
+                                   const float (&n)[EPL], const int32_t (&in)[EPL], bool vec) {
     const int64_t o = row * P.F + fe;
-    const int nv = chunk_valid<EPL>(P, fe);
-    const bool vec = chunk_vec<EPL>(P, o, nv);
     const float dv = (float)deg;
     float mean[EPL], var[EPL], sd[EPL], mx[EPL], mn[EPL];
 #pragma unroll
@@ -366,12 +345,12 @@ __device__ inline void store_stats(const SpmmParams& P, int64_t row, int64_t fe,
         mx[k] = im[k] < 0 ? 0.f : m[k];
         mn[k] = in[k] < 0 ? 0.f : n[k];
     }
-    if (P.o_sum) store4<EPL>(P.o_sum + o, s, vec, nv);
-    if (P.o_mean) store4<EPL>(P.o_mean + o, mean, vec, nv);
-    if (P.o_max) { store4<EPL>(P.o_max + o, mx, vec, nv); store4<EPL>(P.o_amax + o, im, vec, nv); }
-    if (P.o_min) { store4<EPL>(P.o_min + o, mn, vec, nv); store4<EPL>(P.o_amin + o, in, vec, nv); }
-    if (P.o_var) store4<EPL>(P.o_var + o, var, vec, nv);
-    if (P.o_std) store4<EPL>(P.o_std + o, sd, vec, nv);
+    if (P.o_sum) store4<EPL>(P.o_sum + o, s, vec);
+    if (P.o_mean) store4<EPL>(P.o_mean + o, mean, vec);
+    if (P.o_max) { store4<EPL>(P.o_max + o, mx, vec); store4<EPL>(P.o_amax + o, im, vec); }
+    if (P.o_min) { store4<EPL>(P.o_min + o, mn, vec); store4<EPL>(P.o_amin + o, in, vec); }
+    if (P.o_var) store4<EPL>(P.o_var + o, var, vec);
+    if (P.o_std) store4<EPL>(P.o_std + o, sd, vec);
 }
 
 // Column of CSR position p: col[p], or p itself when col is absent (a
@@ -613,10 +592,8 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
         if (slot == 0 && feat_ok) {
             if (hub) {
                 const int64_t o = cidx * P.F + fe;
-                const int nv = chunk_valid<EPL>(P, fe);
 #pragma unroll
                 for (int k = 0; k < EPL; ++k) {
-                    if (k >= nv) break;
                     if constexpr (HS) P.part_sum[o + k] = acc.s[0][k];
                     if constexpr (HM) { P.part_max[o + k] = acc.m[0][k]; P.part_arg[o + k] = acc.i[0][k]; }
                     if constexpr (HX) {
@@ -627,7 +604,7 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
                 }
             } else if constexpr (HX) {
                 store_stats<EPL>(P, row, fe, e1 - e0, acc.s[0], acc.q[0], acc.m[0], acc.i[0],
-                                 acc.n[0], acc.j[0]);
+                                 acc.n[0], acc.j[0], P.vec_store != 0);
             } else {
                 store_row<EPL>(P, row, fe, e1 - e0, acc.s[0], acc.m[0], acc.i[0], HS, HM);
             }
@@ -666,7 +643,7 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
     if (feat_ok) {
         if constexpr (HX)
             store_stats<EPL>(P, row, fe, e1 - e0, acc.s[0], acc.q[0], acc.m[0], acc.i[0],
-                             acc.n[0], acc.j[0]);
+                             acc.n[0], acc.j[0], P.vec_store != 0);
         else
             store_row<EPL>(P, row, fe, e1 - e0, acc.s[0], acc.m[0], acc.i[0], HS, HM);
     }
@@ -790,7 +767,7 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
         if (feat_ok) {
             if constexpr (HX)
                 store_stats<EPL>(P, row, fe, deg, acc.s[0], acc.q[0], acc.m[0], acc.i[0], acc.n[0],
-                                 acc.j[0]);
+                                 acc.j[0], P.vec_store != 0);
             else
                 store_row<EPL>(P, row, fe, deg, acc.s[0], acc.m[0], acc.i[0], HS, HM);
         }
@@ -858,7 +835,7 @@ __global__ __launch_bounds__(kBlock) void spmm_fixup(SpmmParams P) {
         const float sq[1] = {(qs[0] + qs[1]) + (qs[2] + qs[3])};
         const float mx[1] = {m}, nn[1] = {mn};
         const int32_t im[1] = {mi}, in[1] = {ni};
-        store_stats<1>(P, row, f, deg, sum, sq, mx, im, nn, in);
+        store_stats<1>(P, row, f, deg, sum, sq, mx, im, nn, in, false);
         return;
     }
     if constexpr (HS) {
@@ -970,20 +947,14 @@ hipError_t launch_typed(const SpmmParams& p, unsigned grid, hipStream_t s) {
 
 }  // namespace
 
-Geometry make_geometry(int64_t F, int x_dtype, uintptr_t x_align, int64_t ld) {
+Geometry make_geometry(int64_t F, int x_dtype, uintptr_t x_align) {
     Geometry g;
     g.elem_bytes = x_dtype == MP_BF16 ? 2 : 4;
     const int64_t row_bytes = F * g.elem_bytes;
-    const int64_t ld_bytes = (ld > F ? ld : F) * g.elem_bytes;
-    // a vector width is usable when every row start is aligned to it and the
-    // row, rounded up to it, stays inside the row stride (so a padded table
-    // lets the last chunk of a row read into its own padding)
     int vec = 16;
-    while (vec > g.elem_bytes &&
-           (x_align % vec != 0 || (row_bytes + vec - 1) / vec * vec > ld_bytes))
-        vec >>= 1;
+    while (vec > g.elem_bytes && (row_bytes % vec != 0 || x_align % vec != 0)) vec >>= 1;
     g.epl = vec / g.elem_bytes;
-    g.ltot = (row_bytes + vec - 1) / vec;
+    g.ltot = row_bytes / vec;
     if (g.ltot <= kWave) {
         g.L = (int)g.ltot;
         g.S = kWave / g.L;

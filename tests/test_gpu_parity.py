@@ -249,10 +249,10 @@ def test_spmm_row_stride(mixed, dtype, pad):
                                         (522, 528, torch.bfloat16), (50, 64, torch.float32),
                                         (7, 9, torch.float32)])
 @pytest.mark.parametrize("use_plan", [False, True])
-def test_spmm_padded_rows_partial_chunks(monkeypatch, F, ld, dtype, use_plan):
-    """Rows read in whole vectors that run into the row padding: the last
-    lane-chunk of a row holds fewer than EPL features, which must be neither
-    stored nor allowed to touch a neighbouring output row or hub partial."""
+def test_spmm_padded_rows(monkeypatch, F, ld, dtype, use_plan):
+    """Tables whose row padding holds NaN: whatever vector width the row
+    stride allows, no padding element may reach an output row or a hub
+    partial."""
     g = graphgen.mixed_graph(F, n=700, e=9000, f=F)
     monkeypatch.setenv("MP_HUB_MIN", "128")
     monkeypatch.setenv("MP_CHUNK", "32")
