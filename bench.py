@@ -10,7 +10,10 @@ One step = the whole hot path over that graph, inputs already in HBM:
   COO -> CSR (stable radix sort by destination + rowptr), the degree-binned
   plan, then sum, mean and max+argmax aggregation for fp32 features and again
   for bf16 features (fp32 accumulation; sums and means written fp32, bf16 max
-  written bf16, exact).
+  written bf16, exact).  The bf16 table (200-byte rows) is first copied into
+  rows 256 bytes apart, once per step, so that every gathered row spans two
+  cache lines; the fp32 rows (400 bytes) span four lines at any offset and
+  are used as they are.
 
 value = sum over the step's operations of their algorithmic bytes (each edge
 gathers one full feature row; see algorithmic_bytes()) / step time, in GB/s.
