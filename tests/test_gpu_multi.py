@@ -196,17 +196,26 @@ def test_readout_from_sorted_batch_vector():
     compare(res, rp_o, col_o, None, {"x": xf}, ["mean", "max", "std"], torch.float32)
 
 
-def test_multi_chunglu_full_sampled():
-    """Full-size power-law graph: one stacked call (mean, min, max, std) on
-    fp32 features, checked on all hub rows plus random rows."""
-    g = graphgen.workload("chunglu-124M", seed=0, bf16=False)
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+def test_multi_chunglu_full_sampled(dtype):
+    """Full-size power-law graph in the benchmark's configuration: one
+    stacked call (mean, min, max, std) on fp32 features, and on bf16
+    features laid out in 256-byte rows; checked on all hub rows plus random
+    rows."""
+    g = graphgen.workload("chunglu-124M", seed=0, bf16=dtype == torch.bfloat16)
     rp_o, col_o, _, _ = oracle.coo_to_csr(g.src, g.dst, g.n_dst)
     rp, col = dev(rp_o.astype(np.int32)), dev(col_o)
     names = ["mean", "min", "max", "std"]
-    res = mp.spmm_multi(rp, col, dev(g.x), names, plan=mp.Plan(rp, g.E, g.F))
+    if dtype == torch.float32:
+        x, xkw = dev(g.x), {"x": g.x}
+    else:
+        x = mp.pad_rows(dev(g.x_bf16.view(np.int16)).view(torch.bfloat16))
+        assert x.stride(0) == 128
+        xkw = {"x_bf16": g.x_bf16}
+    res = mp.spmm_multi(rp, col, x, names, plan=mp.Plan(rp, g.E, g.F, dtype))
     torch.cuda.synchronize()
     rng = np.random.default_rng(0)
     rows = np.unique(np.concatenate([np.argsort(np.diff(rp_o))[-64:],
                                      rng.integers(0, g.n_dst, 3000)]))
-    errs = compare(res, rp_o, col_o, None, {"x": g.x}, names, torch.float32, rows=rows)
+    errs = compare(res, rp_o, col_o, None, xkw, names, dtype, rows=rows)
     print(f"[note] chunglu multi errors {errs}", file=sys.stderr, flush=True)

@@ -427,13 +427,17 @@ def test_chunglu_124M_csr_bit_exact(chunglu_full):
 
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_chunglu_124M_spmm_sampled(chunglu_full, dtype):
-    """Full-size run in the benchmark's configuration; rows are independent,
-    so a sample of rows (every hub-sized row plus 20k random rows) is checked
-    exactly against the oracle."""
+    """Full-size run in the benchmark's configuration (bf16 features laid
+    out in 256-byte rows, as the benchmark's step does); rows are
+    independent, so a sample of rows (every hub-sized row plus 20k random
+    rows) is checked exactly against the oracle."""
     g, rp_o, col_o, _ = chunglu_full
     rp = dev(rp_o.astype(np.int32))
     col = dev(col_o)
     x = x_of(g, dtype)
+    if dtype == torch.bfloat16:
+        x = mp.pad_rows(x)
+        assert x.stride(0) == 128
     plan = mp.Plan(rp, g.E, g.F, dtype)
     deg = np.diff(rp_o)
     rng_rows = graphgen.uniform_ints(11, 5, 20_000, g.n_dst).astype(np.int64)
