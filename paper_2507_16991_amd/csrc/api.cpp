@@ -170,6 +170,12 @@ struct mp_plan {
 
 namespace {
 
+// A single feature table of `rows` rows, `ld` elements apart, fits 32-bit
+// byte offsets from its base.
+inline int fits_off32(int64_t rows, int64_t ld, int elem_bytes) {
+    return rows * ld * elem_bytes <= (int64_t)UINT32_MAX ? 1 : 0;
+}
+
 // Fill the work description of SpmmParams from a plan (or the plan-free
 // generic layout) and launch the main kernel plus the hub fix-up.
 int run_spmm(const mp_plan* plan, SpmmParams& P, const Geometry& g, int x_dtype, int64_t N_dst,
@@ -300,6 +306,7 @@ int multi_impl(const mp_plan* plan, const void* rowptr, int rowptr_itype, const 
     P.table_ptr[0] = static_cast<const char*>(x);
     P.F = F;
     P.ldx = ldx;
+    P.off32 = fits_off32(N_src, ldx, eb);
     return run_spmm(plan, P, g, x_dtype, N_dst, ws, ws_bytes, s);
 }
 
@@ -375,6 +382,7 @@ int spmm_launch(const SpmmCall& c, hipStream_t s) {
     P.table_off[0] = 0;
     P.F = c.F;
     P.ldx = c.ldx;
+    P.off32 = fits_off32(c.N_src, c.ldx, eb);
     P.reduce = c.reduce;
     P.out = c.out;
     P.out_bf16 = c.out_dtype == MP_BF16;
@@ -771,6 +779,7 @@ int mp_spmm_backward_x(const mp_plan* planT, const void* rowptrT, int rowptrT_it
     P.n_tables = 1;
     P.table_ptr[0] = static_cast<const char*>(table);
     P.F = F;
+    P.off32 = fits_off32(N_dst, F, t_dtype == MP_BF16 ? 2 : 4);
     P.reduce = MP_SUM;
     P.out = grad_x;
     P.out_bf16 = out_dtype == MP_BF16;

@@ -134,6 +134,7 @@ struct SpmmParams {
     int64_t voff[MP_MAX_TYPES];
     int64_t F;
     int64_t ldx;  // row stride of the feature tables in elements (>= F)
+    int off32;    // one table, all of it within 4 GiB of table_ptr[0]
     int L, S, FT;
     int64_t ltot;
     // work list (waves, in launch order): hub chunks, mid rows, small groups

@@ -50,6 +50,21 @@ template <> struct RawVec<uint16_t, 4> { using T = uint2; };
 template <> struct RawVec<uint16_t, 2> { using T = uint32_t; };
 template <> struct RawVec<uint16_t, 1> { using T = uint16_t; };
 
+// One lane-chunk of a feature row at address a.  O32: every row of the table
+// lies within 4 GiB of the table's base t0, so the address is formed from
+// t0 and a 32-bit byte offset (one register per gathered row instead of two,
+// and 32-bit offset arithmetic), which frees registers for more rows in
+// flight.
+template <typename R, bool O32>
+__device__ inline R load_row_chunk(const char* t0, const char* a) {
+    if constexpr (O32) {
+        const uint32_t off = (uint32_t)(a - t0);
+        return *reinterpret_cast<const R*>(t0 + off);
+    } else {
+        return *reinterpret_cast<const R*>(a);
+    }
+}
+
 __device__ inline float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
 __device__ inline float bf16_hi(uint32_t u) { return __uint_as_float(u & 0xFFFF0000u); }
 
@@ -364,7 +379,7 @@ __device__ inline int32_t col_at(const SpmmParams& P, int64_t p) {
 // once, coalesced, one per lane; each inner step then covers SU = S*U edges:
 // slot s takes edges base + u*S + s (u < U), gets their columns by cross-lane
 // permute, issues all U feature-row loads, and only then accumulates.
-template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, int MODE>
+template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, int MODE, bool O32>
 __device__ inline void wave_range(const SpmmParams& P,
                                   AccFor<TX, EPL, HS, HM, MODE>& acc, int64_t e0,
                                   int64_t e1, int lane, int slot, bool feat_ok, int64_t fe, int U) {
@@ -419,7 +434,7 @@ __device__ inline void wave_range(const SpmmParams& P,
             }
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u)
-                if (ok[u]) raw[u] = *reinterpret_cast<const R*>(addr[u]);
+                if (ok[u]) raw[u] = load_row_chunk<R, O32>(P.table_ptr[0], addr[u]);
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
                 const int t = base + u * S + slot;
@@ -445,7 +460,7 @@ __device__ inline void wave_range(const SpmmParams& P,
 // One slot per row: every slot walks its own row's edges, U at a time.
 // COOP: the slot has at least U lanes, which load its next U columns
 // together; otherwise each lane loads the columns itself.
-template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, int MODE, bool COOP>
+template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, int MODE, bool COOP, bool O32>
 __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MODE>& acc,
                                 int64_t e0, int32_t my_n, int32_t max_n, int slot, int j,
                                 bool feat_ok, int64_t fe) {
@@ -513,7 +528,7 @@ __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MOD
         }
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u)
-            if (ok[u]) raw[u] = *reinterpret_cast<const R*>(addr[u]);
+            if (ok[u]) raw[u] = load_row_chunk<R, O32>(P.table_ptr[0], addr[u]);
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u) {
             if (ok[u]) {
@@ -530,7 +545,7 @@ __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MOD
     }
 }
 
-template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, int MODE>
+template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, int MODE, bool O32 = false>
 __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
     constexpr bool HX = MODE == kModeStats;
     const int lane = threadIdx.x & (kWave - 1);
@@ -586,7 +601,7 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
                 e1 = load_rp(P.rowptr, P.rp64, row + 1);
             }
         }
-        wave_range<TX, EPL, HS, HM, NT, W, MODE>(P, acc, e0, e1, lane, slot, feat_ok, fe, U);
+        wave_range<TX, EPL, HS, HM, NT, W, MODE, O32>(P, acc, e0, e1, lane, slot, feat_ok, fe, U);
         acc.fold();
         acc.reduce_slots(S, L, slot, lane);
         if (slot == 0 && feat_ok) {
@@ -636,9 +651,11 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
         max_n = o > max_n ? o : max_n;
     }
     if (L >= kUnroll)
-        slot_row<TX, EPL, HS, HM, NT, W, MODE, true>(P, acc, e0, my_n, max_n, slot, j, feat_ok, fe);
+        slot_row<TX, EPL, HS, HM, NT, W, MODE, true, O32>(P, acc, e0, my_n, max_n, slot, j, feat_ok,
+                                                         fe);
     else
-        slot_row<TX, EPL, HS, HM, NT, W, MODE, false>(P, acc, e0, my_n, max_n, slot, j, feat_ok, fe);
+        slot_row<TX, EPL, HS, HM, NT, W, MODE, false, O32>(P, acc, e0, my_n, max_n, slot, j, feat_ok,
+                                                          fe);
     acc.fold();
     if (feat_ok) {
         if constexpr (HX)
@@ -913,20 +930,20 @@ __global__ void plan_header(const uint32_t* __restrict__ class_start, int nclass
     }
 }
 
-template <typename TX, int EPL, bool W>
+template <typename TX, int EPL, bool W, bool O32>
 hipError_t launch_w(const SpmmParams& p, unsigned grid, hipStream_t s) {
     const bool hs = (p.reduce & (kSum | kMean)) != 0;
     const bool hm = (p.reduce & kMax) != 0;
     if (p.mtab)  // masked sum: the gradient of max
-        hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 1, W, kModeMasked>), dim3(grid), dim3(kBlock), 0, s, p);
+        hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 1, W, kModeMasked, O32>), dim3(grid), dim3(kBlock), 0, s, p);
     else if (p.stats)
-        hipLaunchKernelGGL((spmm_main<TX, EPL, true, true, 1, W, kModeStats>), dim3(grid), dim3(kBlock), 0, s, p);
+        hipLaunchKernelGGL((spmm_main<TX, EPL, true, true, 1, W, kModeStats, O32>), dim3(grid), dim3(kBlock), 0, s, p);
     else if (hs && hm)
-        hipLaunchKernelGGL((spmm_main<TX, EPL, true, true, 1, W, kModePlain>), dim3(grid), dim3(kBlock), 0, s, p);
+        hipLaunchKernelGGL((spmm_main<TX, EPL, true, true, 1, W, kModePlain, O32>), dim3(grid), dim3(kBlock), 0, s, p);
     else if (hm)
-        hipLaunchKernelGGL((spmm_main<TX, EPL, false, true, 1, W, kModePlain>), dim3(grid), dim3(kBlock), 0, s, p);
+        hipLaunchKernelGGL((spmm_main<TX, EPL, false, true, 1, W, kModePlain, O32>), dim3(grid), dim3(kBlock), 0, s, p);
     else
-        hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 1, W, kModePlain>), dim3(grid), dim3(kBlock), 0, s, p);
+        hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 1, W, kModePlain, O32>), dim3(grid), dim3(kBlock), 0, s, p);
     return hipGetLastError();
 }
 
@@ -942,7 +959,14 @@ hipError_t launch_typed(const SpmmParams& p, unsigned grid, hipStream_t s) {
             hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, MP_MAX_TYPES, false, kModePlain>), dim3(grid), dim3(kBlock), 0, s, p);
         return hipGetLastError();
     }
-    return p.w ? launch_w<TX, EPL, true>(p, grid, s) : launch_w<TX, EPL, false>(p, grid, s);
+    // 32-bit row offsets pay off for bf16 rows (measured: 7% on the
+    // 124M-edge graph; fp32 rows are unaffected), so only those are built
+    if constexpr (std::is_same<TX, uint16_t>::value) {
+        if (p.off32)
+            return p.w ? launch_w<TX, EPL, true, true>(p, grid, s)
+                       : launch_w<TX, EPL, false, true>(p, grid, s);
+    }
+    return p.w ? launch_w<TX, EPL, true, false>(p, grid, s) : launch_w<TX, EPL, false, false>(p, grid, s);
 }
 
 }  // namespace
