@@ -45,7 +45,7 @@ STACKED = "chunglu-124M-stacked"
 PROJECTION = "hetero-20M-projection"
 READOUT = "readout-2.4M"
 EXPLAIN = "chunglu-124M-explain"
-DOMINANT = "spmm_main<float, 4, true, false, 1, false, 0>"  # fp32 sum, the largest launch of a step
+DOMINANT = "spmm_main<float, 4, true, false, 1, false, 0, false>"  # fp32 sum, the largest launch of a step
 # the dominant kernel's source: spmm.hip and the aggregation section of the
 # internal header (file, first line marker or None, end marker or None)
 DOMINANT_SRC = [("paper_2507_16991_amd/csrc/spmm.hip", None, None),
