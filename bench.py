@@ -80,14 +80,16 @@ def transpose_bytes(N_dst, N_src, E):
 
 def grad_x_bytes(N_dst, N_src, E, F, mode):
     """Transposed gather of the output gradient, one output row per source.
-    Mean adds the scaled copy of the gradient.  Max gathers the argmax chunk
-    of every edge and feature (and the edge's forward position), but only the
-    routed gradient elements, one per destination row and feature."""
+    Mean adds the scaled copy of the gradient.  Max reads the argmax table
+    once and writes the win masks (ceil(F/32) words per edge), then gathers
+    each edge's forward position and win-mask words, and only the routed
+    gradient elements, one per destination row and feature."""
     b = 4 * (N_src + 1) + 4 * E + N_src * F * 4
     if mode == "mean":
         b += 4 * (N_dst + 1) + 2 * N_dst * F * 4
     if mode == "max":
-        return b + 4 * E + E * F * 4 + N_dst * F * 4
+        mask = E * ((F + 31) // 32) * 4
+        return b + 4 * (N_dst + 1) + N_dst * F * 4 + 2 * mask + 4 * E + N_dst * F * 4
     return b + E * F * 4
 
 
@@ -353,11 +355,11 @@ def backward_step(g, mp, torch, np, dev, mark):
         mark(evs, 2)
         i = 2
         for red in (mp.MP_SUM, mp.MP_MEAN, mp.MP_MAX):
-            nb = mp.mp_spmm_backward_x_workspace(h, N, F, red)
+            nb = mp.mp_spmm_backward_x_workspace(h, N, E, F, red)
             if red not in wss or wss[red].numel() < nb:
                 wss[red] = torch.empty(max(nb, 1), dtype=torch.uint8, device=dev)
             mp.mp_spmm_backward_x(h, rowptrT, it, colT, posT, None, rowptr, it, argout, G,
-                                  mp.MP_F32, N, N, F, red, gx, mp.MP_F32, wss[red],
+                                  mp.MP_F32, N, N, E, F, red, gx, mp.MP_F32, wss[red],
                                   wss[red].numel())
             i += 1
             mark(evs, i)

@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define MP_VERSION 2
+#define MP_VERSION 3
 
 /* Status codes. */
 typedef enum mp_status {
@@ -286,29 +286,35 @@ int mp_csr_transpose(const void* rowptr, int rowptr_itype, const int32_t* col, i
                      int32_t* posT, const float* val_in, float* val_out, void* ws,
                      size_t ws_bytes, void* stream);
 
-/* Workspace bytes for mp_spmm_backward_x (hub partials of planT; for MP_MEAN
- * also an fp32 copy of G divided by the in-degrees, N_dst * F * 4 bytes). */
-int mp_spmm_backward_x_workspace(const mp_plan* planT, int64_t N_dst, int64_t F, int reduce,
-                                 size_t* bytes);
+/* Workspace bytes for mp_spmm_backward_x: hub partials of planT; for MP_MEAN
+ * also an fp32 copy of G divided by the in-degrees (N_dst * F * 4 bytes); for
+ * MP_MAX also the win masks, ceil(F / 32) 32-bit words per edge (bit f of the
+ * words of forward position p: argout[row(p), f] == p). */
+int mp_spmm_backward_x_workspace(const mp_plan* planT, int64_t N_dst, int64_t E, int64_t F,
+                                 int reduce, size_t* bytes);
 
 /* dL/dx of mp_spmm for one reduction (MP_SUM, MP_MEAN or MP_MAX; for a fused
  * forward call add the gradients of its parts).
  *   planT       plan built on rowptrT (N_src rows, same F), or NULL.
  *   rowptrT, colT, posT, wT   from mp_csr_transpose (wT = the forward weights
  *               in transposed order, NULL if unweighted; posT needed for MAX).
- *   rowptr      the forward rowptr (needed for MP_MEAN: in-degrees).
+ *   rowptr      the forward rowptr (needed for MP_MEAN: in-degrees, and for
+ *               MP_MAX: the rows of the forward positions).
  *   argout      [N_dst, F] int32 from the forward call (needed for MP_MAX).
  *   grad_out    [N_dst, F] of g_dtype: G.
+ *   E           number of edges (rowptr[N_dst]); must equal planT's.
  *   grad_x      [N_src, F] of out_dtype, written in full (fp32 accumulation;
  *               a bf16 output is rounded to nearest even once).
+ * MP_MAX first writes the win masks into the workspace (one pass over argout),
+ * then gathers, per edge, only the feature chunks the edge wins.
  * Deterministic: one gather-reduce per source row, no atomics.  Asynchronous
  * on `stream`. */
 int mp_spmm_backward_x(const mp_plan* planT, const void* rowptrT, int rowptrT_itype,
                        const int32_t* colT, const int32_t* posT, const float* wT,
                        const void* rowptr, int rowptr_itype, const int32_t* argout,
-                       const void* grad_out, int g_dtype, int64_t N_dst, int64_t N_src, int64_t F,
-                       int reduce, void* grad_x, int out_dtype, void* ws, size_t ws_bytes,
-                       void* stream);
+                       const void* grad_out, int g_dtype, int64_t N_dst, int64_t N_src, int64_t E,
+                       int64_t F, int reduce, void* grad_x, int out_dtype, void* ws,
+                       size_t ws_bytes, void* stream);
 
 /* Workspace bytes for mp_spmm_backward_w (the row of every CSR edge, 4E). */
 int mp_spmm_backward_w_workspace(int64_t E, size_t* bytes);

@@ -118,9 +118,9 @@ def lib():
         L.mp_readout_multi.argtypes = [p, p, i32, p, i32, i64, i64, i64, i64, i32, p, p, sz, p]
         L.mp_csr_transpose_workspace.argtypes = [i64, i64, i32, i32, psz]
         L.mp_csr_transpose.argtypes = [p, i32, p, i64, i64, i64, p, i32, p, p, p, p, p, sz, p]
-        L.mp_spmm_backward_x_workspace.argtypes = [p, i64, i64, i32, psz]
+        L.mp_spmm_backward_x_workspace.argtypes = [p, i64, i64, i64, i32, psz]
         L.mp_spmm_backward_x.argtypes = [p, p, i32, p, p, p, p, i32, p, p, i32, i64, i64, i64,
-                                         i32, p, i32, p, sz, p]
+                                         i64, i32, p, i32, p, sz, p]
         L.mp_spmm_backward_w_workspace.argtypes = [i64, psz]
         L.mp_spmm_backward_w.argtypes = [p, i32, p, p, i32, p, i32, p, i64, i64, i64, i64, i32, p,
                                          p, sz, p]
@@ -334,16 +334,16 @@ def mp_csr_transpose(rowptr, rowptr_itype, col, N_dst, N_src, E, rowptrT, rowptr
         _ptr(colT), _ptr(posT), _ptr(val_in), _ptr(val_out), _ptr(ws), ws_bytes, _stream(stream)))
 
 
-def mp_spmm_backward_x_workspace(planT_handle, N_dst, F, reduce) -> int:
-    return _bytes("mp_spmm_backward_x_workspace", planT_handle, N_dst, F, reduce)
+def mp_spmm_backward_x_workspace(planT_handle, N_dst, E, F, reduce) -> int:
+    return _bytes("mp_spmm_backward_x_workspace", planT_handle, N_dst, E, F, reduce)
 
 
 def mp_spmm_backward_x(planT_handle, rowptrT, rowptrT_itype, colT, posT, wT, rowptr,
-                       rowptr_itype, argout, grad_out, g_dtype, N_dst, N_src, F, reduce, grad_x,
-                       out_dtype, ws, ws_bytes, stream=None):
+                       rowptr_itype, argout, grad_out, g_dtype, N_dst, N_src, E, F, reduce,
+                       grad_x, out_dtype, ws, ws_bytes, stream=None):
     _check("mp_spmm_backward_x", lib().mp_spmm_backward_x(
         planT_handle, _ptr(rowptrT), rowptrT_itype, _ptr(colT), _ptr(posT), _ptr(wT),
-        _ptr(rowptr), rowptr_itype, _ptr(argout), _ptr(grad_out), g_dtype, N_dst, N_src, F,
+        _ptr(rowptr), rowptr_itype, _ptr(argout), _ptr(grad_out), g_dtype, N_dst, N_src, E, F,
         reduce, _ptr(grad_x), out_dtype, _ptr(ws), ws_bytes, _stream(stream)))
 
 
@@ -605,18 +605,20 @@ def csr_transpose(rowptr, col, N_src, *, rowptrT_dtype=torch.int32, want_pos=Tru
 def spmm_backward_x(rowptrT, colT, grad_out, reduce, *, posT=None, wT=None, rowptr=None,
                     argout=None, planT: Plan | None = None, out_dtype=torch.float32, out=None,
                     stream=None):
-    """dL/dx of spmm for one reduction, over the transposed CSR."""
+    """dL/dx of spmm for one reduction, over the transposed CSR (rowptr, the
+    forward one, is needed for mean and max)."""
     N_src = int(rowptrT.numel()) - 1
     N_dst, F = int(grad_out.shape[0]), int(grad_out.shape[1])
+    E = int(colT.numel())
     dev = grad_out.device
     if out is None:
         out = torch.empty(N_src, F, dtype=out_dtype, device=dev)
     h = planT.handle if planT is not None else None
-    nb = mp_spmm_backward_x_workspace(h, N_dst, F, reduce)
+    nb = mp_spmm_backward_x_workspace(h, N_dst, E, F, reduce)
     ws = _workspace(nb, dev) if nb else None
     mp_spmm_backward_x(h, rowptrT, _itype_code(rowptrT.dtype), colT, posT, wT, rowptr,
                        _itype_code(rowptr.dtype) if rowptr is not None else MP_I32, argout,
-                       grad_out, _dtype_code(grad_out.dtype), N_dst, N_src, F, reduce, out,
+                       grad_out, _dtype_code(grad_out.dtype), N_dst, N_src, E, F, reduce, out,
                        _dtype_code(out.dtype), ws, 0 if ws is None else ws.numel(), stream)
     return out
 

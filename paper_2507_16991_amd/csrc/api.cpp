@@ -706,15 +706,27 @@ int mp_csr_transpose(const void* rowptr, int rowptr_itype, const int32_t* col, i
                            val_out, static_cast<char*>(ws) + c.off, ws_bytes - c.off, s);
 }
 
-int mp_spmm_backward_x_workspace(const mp_plan* planT, int64_t N_dst, int64_t F, int reduce,
-                                 size_t* bytes) {
+// Extra workspace of mp_spmm_backward_x beyond the aggregation's own: the
+// fp32 grad_out / in-degree table (mean) or the win masks (max).
+size_t backward_x_extra(int64_t N_dst, int64_t E, int64_t F, int reduce) {
+    if (reduce == MP_MEAN) return align_up((size_t)N_dst * (size_t)F * 4, 256);
+    // (at least one position's words: the gather may load word 0 unread)
+    if (reduce == MP_MAX)
+        return align_up((size_t)(E > 0 ? E : 1) * (size_t)win_mask_words(F) * 4, 256);
+    return 0;
+}
+
+int mp_spmm_backward_x_workspace(const mp_plan* planT, int64_t N_dst, int64_t E, int64_t F,
+                                 int reduce, size_t* bytes) {
     if (!bytes) return MP_ERR_NULL;
     if (reduce != MP_SUM && reduce != MP_MEAN && reduce != MP_MAX) return MP_ERR_REDUCE;
-    if (N_dst < 0 || F < 1) return MP_ERR_SIZE;
+    if (N_dst < 0 || N_dst > INT32_MAX || E < 0 || E > INT32_MAX || F < 1 || F > 65536)
+        return MP_ERR_SIZE;
     size_t b = 0;
     int st = mp_spmm_workspace(planT, MP_SUM, &b);
     if (st != MP_OK) return st;
-    if (reduce == MP_MEAN) b = align_up(b, 256) + align_up((size_t)N_dst * (size_t)F * 4, 256);
+    const size_t extra = backward_x_extra(N_dst, E, F, reduce);
+    if (extra) b = align_up(b, 256) + extra;
     *bytes = b;
     return MP_OK;
 }
@@ -722,55 +734,66 @@ int mp_spmm_backward_x_workspace(const mp_plan* planT, int64_t N_dst, int64_t F,
 int mp_spmm_backward_x(const mp_plan* planT, const void* rowptrT, int rowptrT_itype,
                        const int32_t* colT, const int32_t* posT, const float* wT,
                        const void* rowptr, int rowptr_itype, const int32_t* argout,
-                       const void* grad_out, int g_dtype, int64_t N_dst, int64_t N_src, int64_t F,
-                       int reduce, void* grad_x, int out_dtype, void* ws, size_t ws_bytes,
-                       void* stream) {
+                       const void* grad_out, int g_dtype, int64_t N_dst, int64_t N_src, int64_t E,
+                       int64_t F, int reduce, void* grad_x, int out_dtype, void* ws,
+                       size_t ws_bytes, void* stream) {
     if (reduce != MP_SUM && reduce != MP_MEAN && reduce != MP_MAX) return MP_ERR_REDUCE;
+    const bool need_rp = reduce != MP_SUM;
     if (!valid_itype(rowptrT_itype) || !valid_dtype(g_dtype) || !valid_dtype(out_dtype))
         return MP_ERR_DTYPE;
-    if (reduce == MP_MEAN && !valid_itype(rowptr_itype)) return MP_ERR_DTYPE;
-    if (N_src < 0 || N_src > INT32_MAX || N_dst < 0 || N_dst > INT32_MAX || F < 1 || F > 65536)
+    if (need_rp && !valid_itype(rowptr_itype)) return MP_ERR_DTYPE;
+    if (N_src < 0 || N_src > INT32_MAX || N_dst < 0 || N_dst > INT32_MAX || E < 0 ||
+        E > INT32_MAX || F < 1 || F > 65536)
         return MP_ERR_SIZE;
     if (!rowptrT) return MP_ERR_NULL;
     if (N_src > 0) {
         if (!colT || !grad_out || !grad_x) return MP_ERR_NULL;
-        if (reduce == MP_MEAN && !rowptr) return MP_ERR_NULL;
+        if (need_rp && !rowptr) return MP_ERR_NULL;
         if (reduce == MP_MAX && (!argout || !posT)) return MP_ERR_NULL;
     }
     int st = check_plan(planT, rowptrT, rowptrT_itype, N_src, F);
     if (st != MP_OK) return st;
+    if (planT && planT->E != E) return MP_ERR_PLAN;
     const int eb = g_dtype == MP_BF16 ? 2 : 4;
     if ((uintptr_t)grad_out % eb || (uintptr_t)rowptrT % (rowptrT_itype == MP_I64 ? 8 : 4) ||
         (uintptr_t)colT % 4 || (uintptr_t)posT % 4 || (uintptr_t)wT % 4 ||
         (uintptr_t)argout % 4 || (uintptr_t)grad_x % (out_dtype == MP_BF16 ? 2 : 4) ||
-        (reduce == MP_MEAN && (uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4)))
+        (need_rp && (uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4)))
         return MP_ERR_ALIGN;
+    // workspace: the aggregation's hub partials, then the reduction's extra
+    size_t part = 0;
+    mp_spmm_workspace(planT, MP_SUM, &part);
+    const size_t extra = backward_x_extra(N_dst, E, F, reduce);
+    if (extra) {
+        part = align_up(part, 256);
+        if (ws_bytes < part + extra || !ws) return MP_ERR_WORKSPACE;
+    }
     if (N_src == 0) return MP_OK;
     hipStream_t s = as_stream(stream);
     const void* table = grad_out;
     int t_dtype = g_dtype;
     void* spmm_ws = ws;
-    size_t spmm_ws_bytes = ws_bytes;
+    size_t spmm_ws_bytes = extra ? part : ws_bytes;
+    char* extra_buf = extra ? static_cast<char*>(ws) + part : nullptr;
     if (reduce == MP_MEAN) {
         // mean: a sum over the transposed CSR of grad_out / in-degree
-        size_t part = 0;
-        mp_spmm_workspace(planT, MP_SUM, &part);
-        part = align_up(part, 256);
-        const size_t need = part + align_up((size_t)N_dst * (size_t)F * 4, 256);
-        if (ws_bytes < need || (!ws && need > 0)) return MP_ERR_WORKSPACE;
-        float* scaled = reinterpret_cast<float*>(static_cast<char*>(ws) + part);
+        float* scaled = reinterpret_cast<float*>(extra_buf);
         if (launch_scale_inv_deg(grad_out, g_dtype == MP_BF16, rowptr, rowptr_itype == MP_I64,
                                  N_dst, F, scaled, s) != hipSuccess)
             return MP_ERR_HIP;
         table = scaled;
         t_dtype = MP_F32;
-        spmm_ws_bytes = part;
     }
-    // the mask table is read in lane-chunks of EPL int32: keep its alignment
-    // within what the feature geometry assumes
-    const uintptr_t mask_align =
-        reduce == MP_MAX ? (t_dtype == MP_BF16 ? (uintptr_t)argout >> 1 : (uintptr_t)argout) : 0;
-    Geometry g = make_geometry(F, t_dtype, (uintptr_t)table | mask_align);
+    uint32_t* mbits = nullptr;
+    if (reduce == MP_MAX) {
+        // max: the win masks of every forward position, then a sum over the
+        // transposed CSR that keeps the features each edge wins
+        mbits = reinterpret_cast<uint32_t*>(extra_buf);
+        if (E > 0 && launch_win_masks(rowptr, rowptr_itype == MP_I64, argout, N_dst, F, mbits,
+                                      s) != hipSuccess)
+            return MP_ERR_HIP;
+    }
+    Geometry g = make_geometry(F, t_dtype, (uintptr_t)table);
     SpmmParams P{};
     P.rowptr = rowptrT;
     P.rp64 = rowptrT_itype == MP_I64;
@@ -786,7 +809,8 @@ int mp_spmm_backward_x(const mp_plan* planT, const void* rowptrT, int rowptrT_it
     P.vec_store = ((uintptr_t)grad_x % 16) == 0;
     if (reduce == MP_MAX) {
         P.ekey = posT;
-        P.mtab = argout;
+        P.mbits = mbits;
+        P.mw = win_mask_words(F);
     }
     return run_spmm(planT, P, g, t_dtype, N_src, spmm_ws, spmm_ws_bytes, s);
 }

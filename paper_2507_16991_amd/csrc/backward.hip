@@ -13,6 +13,10 @@
 //     per-edge dot is reduced over the lanes of a slot in a fixed tree.  With
 //     the row or column array absent (position p reads row p) the same kernel
 //     gives the per-edge dot products of the edge-materialized path.
+//   * win_masks: for the gradient of max, the features each forward edge
+//     wins (one bit per feature), so that the masked sum over the transposed
+//     CSR reads one mask word per edge and lane instead of the argmax chunk
+//     of the edge's destination row.
 //
 // The gradient with respect to x reuses the aggregation kernels of spmm.hip
 // over the transposed CSR (sum, mean after scale_inv_deg, and a masked sum
@@ -74,6 +78,67 @@ __global__ __launch_bounds__(kBlock) void scale_inv_deg(const void* __restrict__
     const float gv = GB ? bf16_bits_to_f32(static_cast<const uint16_t*>(g)[i])
                         : static_cast<const float*>(g)[i];
     out[i] = deg > 0 ? gv / (float)deg : 0.f;
+}
+
+// bits[p * MW + w], bit b: feature f = 32 w + b of row v = row(p) has its
+// maximum at CSR position p (argout[v, f] == p).  One wavefront per row.  The
+// features go in pairs of 64-feature tiles (two argout loads per lane, up to
+// four words per position); the row's positions in chunks of 64.  For each
+// chunk the wavefront clears 4 LDS words per position, every feature whose
+// winner lies in the chunk ORs its bit into its winner's word (an integer OR,
+// so the order does not matter), and lane i stores the words of position i.
+// Every word of every position of the row is written exactly once.  The LDS
+// region is the wavefront's own; LDS operations of one wavefront execute in
+// program order, so no barrier is needed.
+__global__ __launch_bounds__(kBlock) void win_masks(const void* __restrict__ rowptr, int rp64,
+                                                    const int32_t* __restrict__ argout, int64_t N,
+                                                    int64_t F, int64_t MW,
+                                                    uint32_t* __restrict__ bits) {
+    __shared__ __align__(16) uint32_t lds[kWavesPerBlock][kWave * 4];
+    const int lane = threadIdx.x & (kWave - 1);
+    const int wid = threadIdx.x / kWave;
+    const int64_t v = __builtin_amdgcn_readfirstlane(wid) + (int64_t)blockIdx.x * kWavesPerBlock;
+    if (v >= N) return;
+    const int64_t beg = rp_at(rowptr, rp64, v);
+    const int64_t deg = rp_at(rowptr, rp64, v + 1) - beg;
+    if (deg <= 0) return;
+    uint32_t* my = lds[wid];
+    for (int64_t f0 = 0; f0 < F; f0 += 2 * kWave) {
+        // winners of features f0 + lane and f0 + 64 + lane, relative to the
+        // row start (-1: no such feature)
+        // (both loads issued together from in-range addresses, then masked)
+        const int64_t fa = f0 + lane, fb = f0 + kWave + lane;
+        const int32_t aa = argout[v * F + (fa < F ? fa : F - 1)];
+        const int32_t ab = argout[v * F + (fb < F ? fb : F - 1)];
+        const int64_t ra = fa < F ? (int64_t)aa - beg : -1;
+        const int64_t rb = fb < F ? (int64_t)ab - beg : -1;
+        const int64_t w0 = f0 >> 5;  // a multiple of 4
+        const int nw = (int)(MW - w0 < 4 ? MW - w0 : 4);
+        const uint32_t bit = 1u << (lane & 31);
+        const int half = lane >> 5;
+        for (int64_t c0 = 0; c0 < deg; c0 += kWave) {
+            const int n = (int)(deg - c0 < kWave ? deg - c0 : kWave);
+            const int64_t qa = ra - c0, qb = rb - c0;
+            *reinterpret_cast<uint4*>(my + 4 * lane) = make_uint4(0u, 0u, 0u, 0u);
+            __builtin_amdgcn_wave_barrier();
+            if (qa >= 0 && qa < n) atomicOr(my + 4 * qa + half, bit);
+            if (qb >= 0 && qb < n) atomicOr(my + 4 * qb + 2 + half, bit);
+            __builtin_amdgcn_wave_barrier();
+            if (lane < n) {
+                const uint4 r = *reinterpret_cast<const uint4*>(my + 4 * lane);
+                uint32_t* o = bits + (beg + c0 + lane) * MW + w0;
+                if (nw == 4 && (MW & 3) == 0) {
+                    *reinterpret_cast<uint4*>(o) = r;  // 16-byte aligned
+                } else {
+                    o[0] = r.x;
+                    if (nw > 1) o[1] = r.y;
+                    if (nw > 2) o[2] = r.z;
+                    if (nw > 3) o[3] = r.w;
+                }
+            }
+            __builtin_amdgcn_wave_barrier();
+        }
+    }
 }
 
 // EPL consecutive values of a fp32 or bf16 row, widened to fp32; p is aligned
@@ -265,6 +330,15 @@ hipError_t launch_rows_of_edges(const void* rowptr, int rp64, int64_t N, int64_t
     const int64_t threads = ceil_div(E, kRowItems);
     hipLaunchKernelGGL(rows_of_edges, dim3((unsigned)ceil_div(threads, kBlock)), dim3(kBlock), 0,
                        s, rowptr, rp64, N, E, row);
+    return hipGetLastError();
+}
+
+hipError_t launch_win_masks(const void* rowptr, int rp64, const int32_t* argout, int64_t N,
+                            int64_t F, uint32_t* bits, hipStream_t s) {
+    if (N <= 0) return hipSuccess;
+    const unsigned grid = (unsigned)ceil_div(N, kWavesPerBlock);
+    hipLaunchKernelGGL(win_masks, dim3(grid), dim3(kBlock), 0, s, rowptr, rp64, argout, N, F,
+                       win_mask_words(F), bits);
     return hipGetLastError();
 }
 

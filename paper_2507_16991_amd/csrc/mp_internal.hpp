@@ -154,9 +154,13 @@ struct SpmmParams {
     int32_t* argout;
     int vec_store;  // 1: out, out_max and argout are 16-byte aligned
     // masked sum (gradient of max): edge t contributes feature f only where
-    // mtab[c_t * F + f] == ekey[t]; both nullptr otherwise
+    // bit f of the win mask of forward position ekey[t] is set (word
+    // mbits[ekey[t] * mw + f / 32], bit f % 32); both nullptr otherwise.
+    // mbits holds at least mw words even without edges: the kernels load
+    // word 0 for invalid edges and discard it.
     const int32_t* ekey;
-    const int32_t* mtab;
+    const uint32_t* mbits;
+    int64_t mw;
     // stats mode (stacked statistics from one gather): each non-null output
     // [N_dst, F] fp32 (arguments int32) is written
     int stats;
@@ -198,6 +202,11 @@ hipError_t launch_scale_inv_deg(const void* g, int g_bf16, const void* rowptr, i
                                 int64_t F, float* out, hipStream_t s);
 hipError_t launch_spmm_grad_w(const GradWParams& p, int x_dtype, int g_dtype, int epl,
                               hipStream_t s);
+// Win masks of the max aggregation: for every forward CSR position p, mw =
+// ceil(F / 32) words whose bit f says argout[row(p), f] == p.
+inline int64_t win_mask_words(int64_t F) { return (F + 31) / 32; }
+hipError_t launch_win_masks(const void* rowptr, int rp64, const int32_t* argout, int64_t N,
+                            int64_t F, uint32_t* bits, hipStream_t s);
 
 // ---- segment matmul (gmm.hip) --------------------------------------------------
 struct GmmParams {

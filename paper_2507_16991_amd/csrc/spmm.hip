@@ -88,29 +88,19 @@ __device__ inline void widen(const typename RawVec<TX, EPL>::T& r, float (&v)[EP
     }
 }
 
-// EPL consecutive int32 (a lane-chunk of the mask table), 16-byte loads
-// when EPL >= 4; p is aligned to min(16, 4 * EPL) bytes.
+// The EPL bits of a win-mask word that belong to features [fe, fe + EPL) of
+// a lane-chunk (EPL divides 32 and fe is a multiple of EPL, so they never
+// straddle two words).
 template <int EPL>
-__device__ inline void load_mask(const int32_t* p, int32_t (&v)[EPL]) {
-    if constexpr (EPL >= 4) {
-#pragma unroll
-        for (int q = 0; q < EPL / 4; ++q) {
-            const int4 a = reinterpret_cast<const int4*>(p)[q];
-            v[4 * q + 0] = a.x; v[4 * q + 1] = a.y; v[4 * q + 2] = a.z; v[4 * q + 3] = a.w;
-        }
-    } else if constexpr (EPL == 2) {
-        const int2 a = *reinterpret_cast<const int2*>(p);
-        v[0] = a.x; v[1] = a.y;
-    } else {
-        v[0] = *p;
-    }
+__device__ inline uint32_t lane_bits(uint32_t word, int64_t fe) {
+    return (word >> (fe & 31)) & ((1u << EPL) - 1u);
 }
 
-// Keep only the features whose mask entry names this edge.
+// Keep only the features whose win bit is set (bit k of bits: element k).
 template <int EPL>
-__device__ inline void apply_mask(float (&v)[EPL], const int32_t (&m)[EPL], int32_t key) {
+__device__ inline void apply_mask(float (&v)[EPL], uint32_t bits) {
 #pragma unroll
-    for (int k = 0; k < EPL; ++k) v[k] = m[k] == key ? v[k] : 0.f;
+    for (int k = 0; k < EPL; ++k) v[k] = (bits >> k) & 1u ? v[k] : 0.f;
 }
 
 // fp32 -> bf16 bits, round to nearest even (finite values).
@@ -378,12 +368,12 @@ __device__ inline int32_t col_at(const SpmmParams& P, int64_t p) {
 // interleaved.  The column indices (and weights) of up to 64 edges are loaded
 // once, coalesced, one per lane; each inner step then covers SU = S*U edges:
 // slot s takes edges base + u*S + s (u < U), gets their columns by cross-lane
-// permute, issues all U feature-row loads, and only then accumulates.
+// permute, issues all U feature-row loads, and only then accumulates.  (The
+// masked sum has its own pipelined variant below.)
 template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, int MODE, bool O32>
 __device__ inline void wave_range(const SpmmParams& P,
                                   AccFor<TX, EPL, HS, HM, MODE>& acc, int64_t e0,
                                   int64_t e1, int lane, int slot, bool feat_ok, int64_t fe, int U) {
-    constexpr bool MK = MODE == kModeMasked;
     using R = typename RawVec<TX, EPL>::T;
     constexpr int A = AccFor<TX, EPL, HS, HM, MODE>::A;
     const int S = P.S;
@@ -392,18 +382,16 @@ __device__ inline void wave_range(const SpmmParams& P,
     const int tile = steps * SU;
     for (int64_t p0 = e0; p0 < e1; p0 += tile) {
         const int64_t rem = e1 - p0;
-        int32_t myc = 0, myk = -1;
+        int32_t myc = 0;
         float myw = 1.f;
         if (lane < tile && lane < rem) {
             myc = col_at(P, p0 + lane);
             if constexpr (W) myw = __builtin_nontemporal_load(P.w + p0 + lane);
-            if constexpr (MK) myk = __builtin_nontemporal_load(P.ekey + p0 + lane);
         }
         for (int st = 0; st < steps; ++st) {
             const int base = st * SU;
             if (base >= rem) break;
             const char* addr[kUnroll];
-            const int32_t* maddr[kUnroll];
             bool ok[kUnroll];
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
@@ -411,27 +399,8 @@ __device__ inline void wave_range(const SpmmParams& P,
                 const int32_t c = __shfl(myc, t);
                 ok[u] = feat_ok && (u < U) && (t < rem);
                 addr[u] = feat_addr<TX, NT>(P, c, fe);
-                if constexpr (MK) maddr[u] = P.mtab + (int64_t)c * P.F + fe;
             }
             R raw[kUnroll];
-            int32_t mraw[MK ? kUnroll : 1][EPL];
-            int32_t keys[MK ? kUnroll : 1];
-            if constexpr (MK) {
-                // masked sum: load the argmax chunks first and gather a
-                // feature chunk only if one of its features names this edge
-#pragma unroll
-                for (int u = 0; u < kUnroll; ++u) {
-                    keys[u] = __shfl(myk, base + u * S + slot);
-                    if (ok[u]) load_mask<EPL>(maddr[u], mraw[u]);
-                }
-#pragma unroll
-                for (int u = 0; u < kUnroll; ++u) {
-                    bool hit = false;
-#pragma unroll
-                    for (int k = 0; k < EPL; ++k) hit |= mraw[u][k] == keys[u];
-                    ok[u] = ok[u] && hit;
-                }
-            }
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u)
                 if (ok[u]) raw[u] = load_row_chunk<R, O32>(P.table_ptr[0], addr[u]);
@@ -440,8 +409,6 @@ __device__ inline void wave_range(const SpmmParams& P,
                 const int t = base + u * S + slot;
                 float wt = 1.f;
                 if constexpr (W) wt = __shfl(myw, t);
-                int32_t key = -1;
-                if constexpr (MK) key = keys[u];
                 if (ok[u]) {
                     float v[EPL];
                     widen<TX, EPL>(raw[u], v);
@@ -449,11 +416,115 @@ __device__ inline void wave_range(const SpmmParams& P,
 #pragma unroll
                         for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt, v[k]);
                     }
-                    if constexpr (MK) apply_mask<EPL>(v, mraw[u], key);
                     acc.add(u % A, v, (int32_t)(p0 + t));
                 }
             }
         }
+    }
+}
+
+// The masked sum (gradient of max) over edges [e0, e1): the same edge
+// schedule as wave_range, but a feature chunk is gathered only when its
+// edge wins one of its features, which needs that edge's win-mask word
+// first.  The mask words of a step are loaded cooperatively, one per lane
+// (lane l takes word l % mww of the step's edge l / mww, where mww words
+// starting at w_lo cover this wavefront's feature tile), and each lane picks
+// the words it needs by cross-lane permute; U is capped so that a step's
+// words fit the wavefront.  To keep one memory round trip per step, the
+// loads run one step ahead: while step st gathers its chunks, the mask words
+// of step st + 1 are in flight, and while a tile is gathered, the column
+// indices and forward positions of the next tile are too.
+template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, bool O32>
+__device__ inline void wave_range_masked(const SpmmParams& P,
+                                         AccFor<TX, EPL, HS, HM, kModeMasked>& acc, int64_t e0,
+                                         int64_t e1, int lane, int slot, bool feat_ok, int64_t fe,
+                                         int64_t w_lo, int mww) {
+    using R = typename RawVec<TX, EPL>::T;
+    constexpr int A = AccFor<TX, EPL, HS, HM, kModeMasked>::A;
+    if (e0 >= e1) return;
+    const int S = P.S;
+    int U = kUnroll;
+    if (S * U > kWave) U = kWave / S;
+    if (S * U * mww > kWave) U = kWave / (S * mww);  // S * mww <= 64, so U >= 1
+    const int SU = S * U;
+    const int steps = kWave / SU;
+    const int tile = steps * SU;
+    const int me = lane / mww;          // edge of a step whose word this lane loads
+    const int mq = lane - me * mww;     // and which of its words
+    const int wi = (int)((fe >> 5) - w_lo);  // the word of an edge this lane needs
+    // indices of the tile starting at q (lanes past its end keep 0 / -1)
+    auto indices = [&](int64_t q, int32_t& c, int32_t& k, float& w) {
+        c = 0;
+        k = -1;
+        w = 1.f;
+        if (lane < tile && lane < e1 - q) {
+            c = col_at(P, q + lane);
+            if constexpr (W) w = __builtin_nontemporal_load(P.w + q + lane);
+            k = __builtin_nontemporal_load(P.ekey + q + lane);
+        }
+    };
+    // this lane's share of the mask words of the step at `base` of a tile
+    // with `rem` edges left and forward positions in k: an unconditional load
+    // (word 0 for a lane or edge past the end, never read)
+    auto mword = [&](int32_t k, int base, int64_t rem) -> uint32_t {
+        const int32_t key = __shfl(k, (base + me) & (kWave - 1));
+        const bool v = me < SU && base + me < rem;
+        return P.mbits[v ? (int64_t)key * P.mw + w_lo + mq : 0];
+    };
+    int32_t myc, myk;
+    float myw;
+    indices(e0, myc, myk, myw);
+    uint32_t mcur = mword(myk, 0, e1 - e0);
+    for (int64_t p0 = e0; p0 < e1; p0 += tile) {
+        const int64_t rem = e1 - p0;
+        const int64_t nxt = p0 + tile;
+        int32_t nc, nk;
+        float nw;
+        indices(nxt, nc, nk, nw);
+        for (int st = 0; st < steps; ++st) {
+            const int base = st * SU;
+            if (base >= rem) break;
+            const char* addr[kUnroll];
+            bool ok[kUnroll];
+            uint64_t bits = 0;  // EPL bits per edge of this lane's slot
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                const int t = base + u * S + slot;
+                const uint32_t w = __shfl(mcur, ((u * S + slot) * mww + wi) & (kWave - 1));
+                const uint32_t b = feat_ok && u < U && t < rem ? lane_bits<EPL>(w, fe) : 0u;
+                ok[u] = b != 0u;
+                bits |= (uint64_t)b << (u * EPL);
+                addr[u] = feat_addr<TX, NT>(P, __shfl(myc, t & (kWave - 1)), fe);
+            }
+            // the next step's words: of this tile, or the first step of the
+            // next one
+            const uint32_t mnext = st + 1 < steps && base + SU < rem ? mword(myk, base + SU, rem)
+                                                                     : mword(nk, 0, e1 - nxt);
+            R raw[kUnroll];
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u)
+                if (ok[u]) raw[u] = load_row_chunk<R, O32>(P.table_ptr[0], addr[u]);
+#pragma unroll
+            for (int u = 0; u < kUnroll; ++u) {
+                const int t = base + u * S + slot;
+                float wt = 1.f;
+                if constexpr (W) wt = __shfl(myw, t & (kWave - 1));
+                if (ok[u]) {
+                    float v[EPL];
+                    widen<TX, EPL>(raw[u], v);
+                    if constexpr (W) {
+#pragma unroll
+                        for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt, v[k]);
+                    }
+                    apply_mask<EPL>(v, (uint32_t)(bits >> (u * EPL)));
+                    acc.add(u % A, v, (int32_t)(p0 + t));
+                }
+            }
+            mcur = mnext;
+        }
+        myc = nc;
+        myk = nk;
+        myw = nw;
     }
 }
 
@@ -470,7 +541,6 @@ __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MOD
     const int L = P.L;
     for (int32_t it = 0; it < max_n; it += kUnroll) {
         const char* addr[kUnroll];
-        const int32_t* maddr[kUnroll];
         bool ok[kUnroll];
         float wt[kUnroll];
         int32_t key[kUnroll];
@@ -492,7 +562,6 @@ __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MOD
                 if constexpr (MK) key[u] = __shfl(myk, srcl);
                 ok[u] = feat_ok && (it + u < my_n);
                 addr[u] = feat_addr<TX, NT>(P, c, fe);
-                if constexpr (MK) maddr[u] = P.mtab + (int64_t)c * P.F + fe;
             }
         } else {
             int32_t cc[kUnroll];
@@ -506,24 +575,21 @@ __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MOD
                 if constexpr (MK) key[u] = ok[u] ? P.ekey[e0 + it + u] : -1;
             }
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
-                addr[u] = feat_addr<TX, NT>(P, cc[u], fe);
-                if constexpr (MK) maddr[u] = P.mtab + (int64_t)cc[u] * P.F + fe;
-            }
+            for (int u = 0; u < kUnroll; ++u) addr[u] = feat_addr<TX, NT>(P, cc[u], fe);
         }
         R raw[kUnroll];
-        int32_t mraw[MK ? kUnroll : 1][EPL];
+        uint32_t mb[MK ? kUnroll : 1];
         if constexpr (MK) {
-            // masked sum: argmax chunks first, then only the chunks that hit
+            // masked sum: win-mask words first (unconditional loads, word 0
+            // for an invalid edge, so that all are in flight together), then
+            // only the chunks that hit
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u)
-                if (ok[u]) load_mask<EPL>(maddr[u], mraw[u]);
+                mb[u] = P.mbits[ok[u] ? (int64_t)key[u] * P.mw + (fe >> 5) : 0];
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
-                bool hit = false;
-#pragma unroll
-                for (int k = 0; k < EPL; ++k) hit |= mraw[u][k] == key[u];
-                ok[u] = ok[u] && hit;
+                mb[u] = ok[u] ? lane_bits<EPL>(mb[u], fe) : 0u;
+                ok[u] = ok[u] && mb[u] != 0u;
             }
         }
 #pragma unroll
@@ -538,7 +604,7 @@ __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MOD
 #pragma unroll
                     for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt[u], v[k]);
                 }
-                if constexpr (MK) apply_mask<EPL>(v, mraw[u], key[u]);
+                if constexpr (MK) apply_mask<EPL>(v, mb[u]);
                 acc.add(u % A, v, (int32_t)(e0 + it + u));
             }
         }
@@ -601,7 +667,16 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
                 e1 = load_rp(P.rowptr, P.rp64, row + 1);
             }
         }
-        wave_range<TX, EPL, HS, HM, NT, W, MODE, O32>(P, acc, e0, e1, lane, slot, feat_ok, fe, U);
+        if constexpr (MODE == kModeMasked) {
+            // win-mask words covering this feature tile
+            const int64_t w_lo = (int64_t)ft * 2 * EPL;
+            const int64_t wmax = P.mw - w_lo;
+            const int mww = (int)(wmax < 2 * EPL ? wmax : 2 * EPL);
+            wave_range_masked<TX, EPL, HS, HM, NT, W, O32>(P, acc, e0, e1, lane, slot, feat_ok, fe,
+                                                           w_lo, mww);
+        }
+        else
+            wave_range<TX, EPL, HS, HM, NT, W, MODE, O32>(P, acc, e0, e1, lane, slot, feat_ok, fe, U);
         acc.fold();
         acc.reduce_slots(S, L, slot, lane);
         if (slot == 0 && feat_ok) {
@@ -726,28 +801,25 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
         const bool feat_ok = row >= 0 && chunk_j < P.ltot;
         const int64_t fe = chunk_j * EPL;
         R raw[kTinyDeg];
-        int32_t mraw[MK ? kTinyDeg : 1][EPL];
+        uint32_t mb[MK ? kTinyDeg : 1];
         bool ok[kTinyDeg];
         int32_t cc[kTinyDeg];
-        int32_t key[kTinyDeg];
 #pragma unroll
         for (int u = 0; u < kTinyDeg; ++u) {
             cc[u] = __shfl(cv, slot * L + u);
             ok[u] = feat_ok && (u < deg);
-            key[u] = -1;
             if constexpr (MK) {
-                key[u] = __shfl(kv, slot * L + u);
-                if (ok[u]) load_mask<EPL>(P.mtab + (int64_t)cc[u] * P.F + fe, mraw[u]);
+                // unconditional load (word 0 for an invalid edge)
+                const int32_t key = __shfl(kv, slot * L + u);
+                mb[u] = P.mbits[ok[u] ? (int64_t)key * P.mw + (fe >> 5) : 0];
             }
         }
         if constexpr (MK) {
-            // gather a chunk only if one of its features names this edge
+            // gather a chunk only if one of its features is won by this edge
 #pragma unroll
             for (int u = 0; u < kTinyDeg; ++u) {
-                bool hit = false;
-#pragma unroll
-                for (int k = 0; k < EPL; ++k) hit |= mraw[u][k] == key[u];
-                ok[u] = ok[u] && hit;
+                mb[u] = ok[u] ? lane_bits<EPL>(mb[u], fe) : 0u;
+                ok[u] = ok[u] && mb[u] != 0u;
             }
         }
 #pragma unroll
@@ -777,7 +849,7 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
 #pragma unroll
                     for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt[u], v[k]);
                 }
-                if constexpr (MK) apply_mask<EPL>(v, mraw[u], key[u]);
+                if constexpr (MK) apply_mask<EPL>(v, mb[u]);
                 acc.add(0, v, beg + u);
             }
         }
@@ -930,13 +1002,21 @@ __global__ void plan_header(const uint32_t* __restrict__ class_start, int nclass
     }
 }
 
+// masked sum: the gradient of max
+template <typename TX, int EPL, bool O32>
+hipError_t launch_masked(const SpmmParams& p, unsigned grid, hipStream_t s) {
+    if (p.w)
+        hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 1, true, kModeMasked, O32>), dim3(grid), dim3(kBlock), 0, s, p);
+    else
+        hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 1, false, kModeMasked, O32>), dim3(grid), dim3(kBlock), 0, s, p);
+    return hipGetLastError();
+}
+
 template <typename TX, int EPL, bool W, bool O32>
 hipError_t launch_w(const SpmmParams& p, unsigned grid, hipStream_t s) {
     const bool hs = (p.reduce & (kSum | kMean)) != 0;
     const bool hm = (p.reduce & kMax) != 0;
-    if (p.mtab)  // masked sum: the gradient of max
-        hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, 1, W, kModeMasked, O32>), dim3(grid), dim3(kBlock), 0, s, p);
-    else if (p.stats)
+    if (p.stats)
         hipLaunchKernelGGL((spmm_main<TX, EPL, true, true, 1, W, kModeStats, O32>), dim3(grid), dim3(kBlock), 0, s, p);
     else if (hs && hm)
         hipLaunchKernelGGL((spmm_main<TX, EPL, true, true, 1, W, kModePlain, O32>), dim3(grid), dim3(kBlock), 0, s, p);
@@ -959,6 +1039,10 @@ hipError_t launch_typed(const SpmmParams& p, unsigned grid, hipStream_t s) {
             hipLaunchKernelGGL((spmm_main<TX, EPL, true, false, MP_MAX_TYPES, false, kModePlain>), dim3(grid), dim3(kBlock), 0, s, p);
         return hipGetLastError();
     }
+    // the masked sum is bound by memory latency rather than bandwidth: the
+    // registers that 32-bit row offsets free buy more wavefronts in flight
+    if (p.mbits)
+        return p.off32 ? launch_masked<TX, EPL, true>(p, grid, s) : launch_masked<TX, EPL, false>(p, grid, s);
     // 32-bit row offsets pay off for bf16 rows (measured: 7% on the
     // 124M-edge graph; fp32 rows are unaffected), so only those are built
     if constexpr (std::is_same<TX, uint16_t>::value) {
@@ -1025,7 +1109,7 @@ hipError_t launch_tiny_typed(const SpmmParams& p, unsigned grid, hipStream_t s) 
             hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, 4, kModePlain>), dim3(grid), dim3(kBlock), 0, s, p);
         else
             hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, MP_MAX_TYPES, kModePlain>), dim3(grid), dim3(kBlock), 0, s, p);
-    } else if (p.mtab) {
+    } else if (p.mbits) {
         // masked sum: the gradient of max
         if (w) hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, true, 1, kModeMasked>), dim3(grid), dim3(kBlock), 0, s, p);
         else hipLaunchKernelGGL((spmm_tiny<TX, EPL, true, false, false, 1, kModeMasked>), dim3(grid), dim3(kBlock), 0, s, p);

@@ -30,7 +30,7 @@ def test_exports_every_declared_function():
 
 
 def test_version_and_status_strings():
-    assert mp.mp_version() == 2
+    assert mp.mp_version() == 3
     for st in range(-9, 1):
         assert mp.mp_status_str(st) != "unknown status"
     assert mp.mp_status_str(-99) == "unknown status"
@@ -190,12 +190,23 @@ def test_backward_errors_and_sizes():
     L = mp.lib()
     nb = ctypes.c_size_t(0)
     assert L.mp_spmm_backward_w_workspace(1000, ctypes.byref(nb)) == 0 and nb.value == 4096
-    assert L.mp_spmm_backward_x_workspace(None, 10, 8, mp.MP_MEAN, ctypes.byref(nb)) == 0
+    assert L.mp_spmm_backward_x_workspace(None, 10, 100, 8, mp.MP_MEAN, ctypes.byref(nb)) == 0
     assert nb.value == 512
-    assert L.mp_spmm_backward_x_workspace(None, 10, 8, mp.MP_SUM | mp.MP_MAX,
+    assert L.mp_spmm_backward_x_workspace(None, 10, 100, 8, mp.MP_SUM, ctypes.byref(nb)) == 0
+    assert nb.value == 0
+    # max: one 32-bit win-mask word per edge for F <= 32, ceil(F / 32) beyond
+    assert L.mp_spmm_backward_x_workspace(None, 10, 100, 8, mp.MP_MAX, ctypes.byref(nb)) == 0
+    assert nb.value == 512
+    assert L.mp_spmm_backward_x_workspace(None, 10, 1000, 100, mp.MP_MAX,
+                                          ctypes.byref(nb)) == 0
+    assert nb.value == 16128  # 1000 * 4 words * 4 bytes, rounded up to 256
+    assert L.mp_spmm_backward_x_workspace(None, 10, 100, 8, mp.MP_SUM | mp.MP_MAX,
                                           ctypes.byref(nb)) == -4
+    assert L.mp_spmm_backward_x_workspace(None, 10, -1, 8, mp.MP_MAX, ctypes.byref(nb)) == -2
+    assert L.mp_spmm_backward_x_workspace(None, 10, 1 << 31, 8, mp.MP_MAX,
+                                          ctypes.byref(nb)) == -2
     bx = dict(planT=None, rowptrT=FAKE, itT=0, colT=FAKE, posT=FAKE, wT=None, rowptr=FAKE, it=0,
-              argout=FAKE, g=FAKE, g_dtype=0, N_dst=10, N_src=10, F=8, reduce=mp.MP_SUM,
+              argout=FAKE, g=FAKE, g_dtype=0, N_dst=10, N_src=10, E=100, F=8, reduce=mp.MP_SUM,
               out=FAKE, out_dtype=0, ws=None, ws_bytes=0, stream=None)
     def bwx(**kw):
         a = dict(bx, **kw)
@@ -203,8 +214,14 @@ def test_backward_errors_and_sizes():
     assert bwx(reduce=mp.MP_SUM | mp.MP_MAX) == -4
     assert bwx(reduce=mp.MP_MAX, argout=None) == -1
     assert bwx(reduce=mp.MP_MAX, posT=None) == -1
+    assert bwx(reduce=mp.MP_MAX, rowptr=None) == -1  # rows of the forward positions
     assert bwx(reduce=mp.MP_MEAN, rowptr=None) == -1
     assert bwx(reduce=mp.MP_MEAN) == -5  # needs a workspace for the scaled gradient
+    assert bwx(reduce=mp.MP_MAX) == -5  # needs a workspace for the win masks
+    assert bwx(reduce=mp.MP_MAX, ws=FAKE, ws_bytes=511) == -5
+    assert bwx(reduce=mp.MP_MAX, it=5) == -3
+    assert bwx(reduce=mp.MP_MAX, rowptr=FAKE + 2) == -8
+    assert bwx(E=-1) == -2
     assert bwx(g_dtype=3) == -3
     assert bwx(g=FAKE + 2) == -8
     assert bwx(F=0) == -2

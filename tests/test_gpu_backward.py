@@ -136,12 +136,15 @@ def mixed():
     return graphgen.mixed_graph(0, f=64)
 
 
-@pytest.mark.parametrize("F,gdtype", [(24, torch.float32), (24, torch.bfloat16), (7, torch.float32)])
-@pytest.mark.parametrize("with_rowptr", [False, True])
-def test_backward_max_long_rows(F, gdtype, with_rowptr):
+@pytest.mark.parametrize("F,gdtype", [(24, torch.float32), (24, torch.bfloat16), (7, torch.float32),
+                                      (64, torch.float32), (100, torch.bfloat16),
+                                      (130, torch.float32)])
+@pytest.mark.parametrize("rp_dtype", [np.int32, np.int64])
+def test_backward_max_long_rows(F, gdtype, rp_dtype):
     """Destination rows of up to 70,000 edges (positions beyond 16 bits
-    within a row), empty and single-edge rows; the forward rowptr is optional
-    for the max gradient."""
+    within a row, win masks built over many 64-edge chunks of one row), empty
+    and single-edge rows; feature counts that fill one win-mask word, two,
+    four and five (a last tile with one word)."""
     degs = [1, 100, 65535, 65536, 65537, 0, 300, 70000, 3]
     n_dst = len(degs)
     n_src = 5000
@@ -155,11 +158,59 @@ def test_backward_max_long_rows(F, gdtype, with_rowptr):
     G, gkw = grad_input(2, n_dst, F, gdtype)
     rpt, colt, post, _, _ = check_transpose(rp_o, col_o, n_src)
     gx = mp.spmm_backward_x(rpt, colt, G, mp.MP_MAX, posT=post,
-                            rowptr=dev(rp_o.astype(np.int32)) if with_rowptr else None,
+                            rowptr=dev(rp_o.astype(rp_dtype)),
                             argout=dev(am_o.astype(np.int32)))
     torch.cuda.synchronize()
     ref, scale = oracle.spmm_backward_x(rp_o, col_o, n_src, "max", argout=am_o, **gkw)
     assert scaled_error(gx.cpu().numpy(), ref, scale) <= TOL[gdtype]
+
+
+def test_backward_max_dense_wins():
+    """Rows of 1 to 70 edges over 2 sources with many duplicate edges, so a
+    source row collects several wins of one destination and one feature tile
+    can hold more winners than a 64-edge chunk has positions (both ways of
+    building the win masks).  Every routed element of G is a small integer,
+    so the gradient is exact and compared bit for bit."""
+    F = 100
+    degs = np.arange(1, 71)
+    n_dst = degs.size
+    dst = np.repeat(np.arange(n_dst, dtype=np.int32), degs)
+    src = graphgen.uniform_ints(9, 1, dst.size, 2)
+    x = graphgen.normal_f32(9, 3, 2 * F).reshape(2, F)
+    rp_o, col_o, _, _ = oracle.coo_to_csr(src, dst, n_dst, n_src=2)
+    # distinct message values per edge: x varies by source only, so ties
+    # between duplicates go to the first CSR position
+    am_o = oracle.spmm(rp_o, col_o, x=x, want=("max",))["argmax"]
+    g = (graphgen.uniform_ints(9, 5, n_dst * F, 64) - 32).astype(np.float32).reshape(n_dst, F)
+    rpt, colt, post, _, _ = check_transpose(rp_o, col_o, 2)
+    gx = mp.spmm_backward_x(rpt, colt, dev(g), mp.MP_MAX, posT=post,
+                            rowptr=dev(rp_o.astype(np.int32)),
+                            argout=dev(am_o.astype(np.int32)), planT=mp.Plan(rpt, dst.size, F))
+    torch.cuda.synchronize()
+    ref, _ = oracle.spmm_backward_x(rp_o, col_o, 2, "max", argout=am_o, g=g)
+    assert np.array_equal(gx.cpu().numpy(), ref.astype(np.float32))
+
+
+def test_backward_plan_edge_count_mismatch():
+    rp_o = np.array([0, 2, 3], np.int64)
+    col_o = np.array([0, 1, 1], np.int32)
+    rpt, colt, post, _, _ = check_transpose(rp_o, col_o, 2)
+    planT = mp.Plan(rpt, 3, 4)
+    G = torch.ones(2, 4, device=DEV)
+    argout = dev(np.array([[0] * 4, [2] * 4], np.int32))
+    L = mp.lib()
+    nb = mp.mp_spmm_backward_x_workspace(planT.handle, 2, 3, 4, mp.MP_MAX)
+    ws = torch.empty(max(nb, 1), dtype=torch.uint8, device=DEV)
+    out = torch.empty(2, 4, device=DEV)
+    rp = dev(rp_o.astype(np.int32))
+    args = [planT.handle, rpt.data_ptr(), mp.MP_I32, colt.data_ptr(), post.data_ptr(), None,
+            rp.data_ptr(), mp.MP_I32, argout.data_ptr(), G.data_ptr(), mp.MP_F32, 2, 2, 4, 4,
+            mp.MP_MAX, out.data_ptr(), mp.MP_F32, ws.data_ptr(), nb, None]
+    assert L.mp_spmm_backward_x(*args) == -6  # E = 4, the plan has 3 edges
+    args[13] = 3
+    assert L.mp_spmm_backward_x(*args) == 0
+    torch.cuda.synchronize()
+    assert out.cpu().tolist() == [[1.0] * 4, [1.0] * 4]
 
 
 @pytest.mark.parametrize("reduce", ["sum", "mean", "max"])
