@@ -65,78 +65,128 @@ __global__ __launch_bounds__(kBlock) void rows_of_edges(const void* __restrict__
 
 __device__ inline float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
 
-// out[v, f] = g[v, f] / deg(v) in fp32 (0 for an empty row).
-template <bool GB>
+// out[v, f] = g[v, f] / deg(v) in fp32 (0 for an empty row).  Each thread
+// takes V consecutive elements of one row (V divides F); the row index uses
+// 32-bit division when the table has under 2^32 elements.
+template <bool GB, int V>
 __global__ __launch_bounds__(kBlock) void scale_inv_deg(const void* __restrict__ g,
                                                         const void* __restrict__ rowptr, int rp64,
                                                         int64_t N, int64_t F,
                                                         float* __restrict__ out) {
-    const int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
-    if (i >= N * F) return;
-    const int64_t v = i / F;
+    const int64_t n = N * F;
+    const int64_t i = ((int64_t)blockIdx.x * kBlock + threadIdx.x) * V;
+    if (i >= n) return;
+    const int64_t v = n <= (int64_t)UINT32_MAX ? (int64_t)((uint32_t)i / (uint32_t)F) : i / F;
     const int64_t deg = rp_at(rowptr, rp64, v + 1) - rp_at(rowptr, rp64, v);
-    const float gv = GB ? bf16_bits_to_f32(static_cast<const uint16_t*>(g)[i])
-                        : static_cast<const float*>(g)[i];
-    out[i] = deg > 0 ? gv / (float)deg : 0.f;
+    float gv[V];
+    if constexpr (GB) {
+        const uint16_t* gb = static_cast<const uint16_t*>(g) + i;
+        if constexpr (V == 4) {
+            const uint2 u = *reinterpret_cast<const uint2*>(gb);
+            gv[0] = bf16_bits_to_f32(u.x & 0xFFFFu); gv[1] = __uint_as_float(u.x & 0xFFFF0000u);
+            gv[2] = bf16_bits_to_f32(u.y & 0xFFFFu); gv[3] = __uint_as_float(u.y & 0xFFFF0000u);
+        } else {
+            gv[0] = bf16_bits_to_f32(gb[0]);
+        }
+    } else {
+        const float* gf = static_cast<const float*>(g) + i;
+        if constexpr (V == 4) {
+            const float4 a = *reinterpret_cast<const float4*>(gf);
+            gv[0] = a.x; gv[1] = a.y; gv[2] = a.z; gv[3] = a.w;
+        } else {
+            gv[0] = gf[0];
+        }
+    }
+#pragma unroll
+    for (int k = 0; k < V; ++k) gv[k] = deg > 0 ? gv[k] / (float)deg : 0.f;
+    if constexpr (V == 4)
+        *reinterpret_cast<float4*>(out + i) = make_float4(gv[0], gv[1], gv[2], gv[3]);
+    else
+        out[i] = gv[0];
 }
 
 // bits[p * MW + w], bit b: feature f = 32 w + b of row v = row(p) has its
-// maximum at CSR position p (argout[v, f] == p).  One wavefront per row.  The
-// features go in pairs of 64-feature tiles (two argout loads per lane, up to
-// four words per position); the row's positions in chunks of 64.  For each
-// chunk the wavefront clears 4 LDS words per position, every feature whose
-// winner lies in the chunk ORs its bit into its winner's word (an integer OR,
-// so the order does not matter), and lane i stores the words of position i.
-// Every word of every position of the row is written exactly once.  The LDS
-// region is the wavefront's own; LDS operations of one wavefront execute in
-// program order, so no barrier is needed.
-__global__ __launch_bounds__(kBlock) void win_masks(const void* __restrict__ rowptr, int rp64,
+// maximum at CSR position p (argout[v, f] == p).  A wavefront takes
+// kMaskRows consecutive rows, whose row ranges and first argout loads are
+// issued together (a row's own work is short next to a memory round trip).
+// The features go in pairs of 64-feature tiles (two argout values per lane,
+// up to four words per position); a row's positions in chunks of 64.  For
+// each chunk the wavefront clears 4 LDS words per position, every feature
+// whose winner lies in the chunk ORs its bit into its winner's word (an
+// integer OR, so the order does not matter), and lane i stores the words of
+// position i.  Every word of every position is written exactly once.  The
+// LDS region is the wavefront's own; LDS operations of one wavefront execute
+// in program order, so no barrier is needed.
+constexpr int kMaskRows = 4;
+
+template <typename IT>
+__global__ __launch_bounds__(kBlock) void win_masks(const IT* __restrict__ rowptr,
                                                     const int32_t* __restrict__ argout, int64_t N,
                                                     int64_t F, int64_t MW,
                                                     uint32_t* __restrict__ bits) {
     __shared__ __align__(16) uint32_t lds[kWavesPerBlock][kWave * 4];
     const int lane = threadIdx.x & (kWave - 1);
     const int wid = threadIdx.x / kWave;
-    const int64_t v = __builtin_amdgcn_readfirstlane(wid) + (int64_t)blockIdx.x * kWavesPerBlock;
-    if (v >= N) return;
-    const int64_t beg = rp_at(rowptr, rp64, v);
-    const int64_t deg = rp_at(rowptr, rp64, v + 1) - beg;
-    if (deg <= 0) return;
+    const int64_t v0 =
+        (__builtin_amdgcn_readfirstlane(wid) + (int64_t)blockIdx.x * kWavesPerBlock) * kMaskRows;
+    if (v0 >= N) return;
     uint32_t* my = lds[wid];
-    for (int64_t f0 = 0; f0 < F; f0 += 2 * kWave) {
-        // winners of features f0 + lane and f0 + 64 + lane, relative to the
-        // row start (-1: no such feature)
-        // (both loads issued together from in-range addresses, then masked)
-        const int64_t fa = f0 + lane, fb = f0 + kWave + lane;
-        const int32_t aa = argout[v * F + (fa < F ? fa : F - 1)];
-        const int32_t ab = argout[v * F + (fb < F ? fb : F - 1)];
-        const int64_t ra = fa < F ? (int64_t)aa - beg : -1;
-        const int64_t rb = fb < F ? (int64_t)ab - beg : -1;
-        const int64_t w0 = f0 >> 5;  // a multiple of 4
-        const int nw = (int)(MW - w0 < 4 ? MW - w0 : 4);
-        const uint32_t bit = 1u << (lane & 31);
-        const int half = lane >> 5;
-        for (int64_t c0 = 0; c0 < deg; c0 += kWave) {
-            const int n = (int)(deg - c0 < kWave ? deg - c0 : kWave);
-            const int64_t qa = ra - c0, qb = rb - c0;
-            *reinterpret_cast<uint4*>(my + 4 * lane) = make_uint4(0u, 0u, 0u, 0u);
-            __builtin_amdgcn_wave_barrier();
-            if (qa >= 0 && qa < n) atomicOr(my + 4 * qa + half, bit);
-            if (qb >= 0 && qb < n) atomicOr(my + 4 * qb + 2 + half, bit);
-            __builtin_amdgcn_wave_barrier();
-            if (lane < n) {
-                const uint4 r = *reinterpret_cast<const uint4*>(my + 4 * lane);
-                uint32_t* o = bits + (beg + c0 + lane) * MW + w0;
-                if (nw == 4 && (MW & 3) == 0) {
-                    *reinterpret_cast<uint4*>(o) = r;  // 16-byte aligned
-                } else {
-                    o[0] = r.x;
-                    if (nw > 1) o[1] = r.y;
-                    if (nw > 2) o[2] = r.z;
-                    if (nw > 3) o[3] = r.w;
-                }
+    int64_t rb[kMaskRows + 1];
+#pragma unroll
+    for (int i = 0; i <= kMaskRows; ++i) rb[i] = (int64_t)rowptr[v0 + i < N ? v0 + i : N];
+    // features f0 + lane and f0 + 64 + lane (clamped to the row, masked below)
+    const int64_t la = lane < F ? lane : F - 1;
+    const int64_t lb = kWave + lane < F ? kWave + lane : F - 1;
+    int32_t a0[kMaskRows], b0[kMaskRows];
+#pragma unroll
+    for (int i = 0; i < kMaskRows; ++i) {
+        const int64_t v = v0 + i < N ? v0 + i : N - 1;
+        a0[i] = argout[v * F + la];
+        b0[i] = argout[v * F + lb];
+    }
+    const uint32_t bit = 1u << (lane & 31);
+    const int half = lane >> 5;
+#pragma unroll
+    for (int i = 0; i < kMaskRows; ++i) {
+        const int64_t v = v0 + i;
+        const int64_t beg = rb[i];
+        const int64_t deg = rb[i + 1] - beg;
+        if (v >= N || deg <= 0) continue;
+        for (int64_t f0 = 0; f0 < F; f0 += 2 * kWave) {
+            // winners of features f0 + lane and f0 + 64 + lane, relative to
+            // the row start (-1: no such feature)
+            const int64_t fa = f0 + lane, fb = f0 + kWave + lane;
+            int32_t aa = a0[i], ab = b0[i];
+            if (f0 > 0) {
+                aa = argout[v * F + (fa < F ? fa : F - 1)];
+                ab = argout[v * F + (fb < F ? fb : F - 1)];
             }
-            __builtin_amdgcn_wave_barrier();
+            const int64_t ra = fa < F ? (int64_t)aa - beg : -1;
+            const int64_t rbv = fb < F ? (int64_t)ab - beg : -1;
+            const int64_t w0 = f0 >> 5;  // a multiple of 4
+            const int nw = (int)(MW - w0 < 4 ? MW - w0 : 4);
+            for (int64_t c0 = 0; c0 < deg; c0 += kWave) {
+                const int n = (int)(deg - c0 < kWave ? deg - c0 : kWave);
+                const int64_t qa = ra - c0, qb = rbv - c0;
+                *reinterpret_cast<uint4*>(my + 4 * lane) = make_uint4(0u, 0u, 0u, 0u);
+                __builtin_amdgcn_wave_barrier();
+                if (qa >= 0 && qa < n) atomicOr(my + 4 * qa + half, bit);
+                if (qb >= 0 && qb < n) atomicOr(my + 4 * qb + 2 + half, bit);
+                __builtin_amdgcn_wave_barrier();
+                if (lane < n) {
+                    const uint4 r = *reinterpret_cast<const uint4*>(my + 4 * lane);
+                    uint32_t* o = bits + (beg + c0 + lane) * MW + w0;
+                    if (nw == 4 && (MW & 3) == 0) {
+                        *reinterpret_cast<uint4*>(o) = r;  // 16-byte aligned
+                    } else {
+                        o[0] = r.x;
+                        if (nw > 1) o[1] = r.y;
+                        if (nw > 2) o[2] = r.z;
+                        if (nw > 3) o[3] = r.w;
+                    }
+                }
+                __builtin_amdgcn_wave_barrier();
+            }
         }
     }
 }
@@ -336,9 +386,15 @@ hipError_t launch_rows_of_edges(const void* rowptr, int rp64, int64_t N, int64_t
 hipError_t launch_win_masks(const void* rowptr, int rp64, const int32_t* argout, int64_t N,
                             int64_t F, uint32_t* bits, hipStream_t s) {
     if (N <= 0) return hipSuccess;
-    const unsigned grid = (unsigned)ceil_div(N, kWavesPerBlock);
-    hipLaunchKernelGGL(win_masks, dim3(grid), dim3(kBlock), 0, s, rowptr, rp64, argout, N, F,
-                       win_mask_words(F), bits);
+    const unsigned grid = (unsigned)ceil_div(ceil_div(N, kMaskRows), kWavesPerBlock);
+    if (rp64)
+        hipLaunchKernelGGL(win_masks<int64_t>, dim3(grid), dim3(kBlock), 0, s,
+                           static_cast<const int64_t*>(rowptr), argout, N, F, win_mask_words(F),
+                           bits);
+    else
+        hipLaunchKernelGGL(win_masks<int32_t>, dim3(grid), dim3(kBlock), 0, s,
+                           static_cast<const int32_t*>(rowptr), argout, N, F, win_mask_words(F),
+                           bits);
     return hipGetLastError();
 }
 
@@ -346,11 +402,18 @@ hipError_t launch_scale_inv_deg(const void* g, int g_bf16, const void* rowptr, i
                                 int64_t F, float* out, hipStream_t s) {
     const int64_t n = N * F;
     if (n <= 0) return hipSuccess;
-    const unsigned grid = (unsigned)ceil_div(n, kBlock);
-    if (g_bf16)
-        hipLaunchKernelGGL(scale_inv_deg<true>, dim3(grid), dim3(kBlock), 0, s, g, rowptr, rp64, N, F, out);
+    // four elements per thread when rows hold whole groups of four and the
+    // gradient is aligned for it (out is a 256-byte aligned workspace)
+    const bool v4 = F % 4 == 0 && (uintptr_t)g % (g_bf16 ? 8 : 16) == 0;
+    const unsigned grid = (unsigned)ceil_div(v4 ? n / 4 : n, kBlock);
+    if (g_bf16 && v4)
+        hipLaunchKernelGGL((scale_inv_deg<true, 4>), dim3(grid), dim3(kBlock), 0, s, g, rowptr, rp64, N, F, out);
+    else if (g_bf16)
+        hipLaunchKernelGGL((scale_inv_deg<true, 1>), dim3(grid), dim3(kBlock), 0, s, g, rowptr, rp64, N, F, out);
+    else if (v4)
+        hipLaunchKernelGGL((scale_inv_deg<false, 4>), dim3(grid), dim3(kBlock), 0, s, g, rowptr, rp64, N, F, out);
     else
-        hipLaunchKernelGGL(scale_inv_deg<false>, dim3(grid), dim3(kBlock), 0, s, g, rowptr, rp64, N, F, out);
+        hipLaunchKernelGGL((scale_inv_deg<false, 1>), dim3(grid), dim3(kBlock), 0, s, g, rowptr, rp64, N, F, out);
     return hipGetLastError();
 }
 

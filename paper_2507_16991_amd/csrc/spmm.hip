@@ -484,7 +484,10 @@ __device__ inline void wave_range_masked(const SpmmParams& P,
         for (int st = 0; st < steps; ++st) {
             const int base = st * SU;
             if (base >= rem) break;
-            const char* addr[kUnroll];
+            // row-chunk addresses: 32-bit byte offsets from the table base
+            // when the table spans under 4 GiB (one register each)
+            const char* addr[O32 ? 1 : kUnroll];
+            uint32_t off[O32 ? kUnroll : 1];
             bool ok[kUnroll];
             uint64_t bits = 0;  // EPL bits per edge of this lane's slot
 #pragma unroll
@@ -494,7 +497,11 @@ __device__ inline void wave_range_masked(const SpmmParams& P,
                 const uint32_t b = feat_ok && u < U && t < rem ? lane_bits<EPL>(w, fe) : 0u;
                 ok[u] = b != 0u;
                 bits |= (uint64_t)b << (u * EPL);
-                addr[u] = feat_addr<TX, NT>(P, __shfl(myc, t & (kWave - 1)), fe);
+                const int32_t c = __shfl(myc, t & (kWave - 1));
+                if constexpr (O32)
+                    off[u] = ((uint32_t)c * (uint32_t)P.ldx + (uint32_t)fe) * (uint32_t)sizeof(TX);
+                else
+                    addr[u] = feat_addr<TX, NT>(P, c, fe);
             }
             // the next step's words: of this tile, or the first step of the
             // next one
@@ -502,8 +509,14 @@ __device__ inline void wave_range_masked(const SpmmParams& P,
                                                                      : mword(nk, 0, e1 - nxt);
             R raw[kUnroll];
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u)
-                if (ok[u]) raw[u] = load_row_chunk<R, O32>(P.table_ptr[0], addr[u]);
+            for (int u = 0; u < kUnroll; ++u) {
+                if (ok[u]) {
+                    if constexpr (O32)
+                        raw[u] = *reinterpret_cast<const R*>(P.table_ptr[0] + off[u]);
+                    else
+                        raw[u] = *reinterpret_cast<const R*>(addr[u]);
+                }
+            }
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
                 const int t = base + u * S + slot;
