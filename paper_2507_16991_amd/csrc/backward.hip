@@ -269,9 +269,10 @@ __global__ __launch_bounds__(kBlock) void spmm_grad_w(GradWParams P) {
         myc = P.col ? __builtin_nontemporal_load(P.col + p0 + lane) : (int32_t)(p0 + lane);
         myv = P.row ? __builtin_nontemporal_load(P.row + p0 + lane) : (int32_t)(p0 + lane);
     }
-    // the largest power of two below L: first stride of the slot reduction
-    int top = 1;
-    while (2 * top < L) top *= 2;
+    // values per lane left by the slot reduction (L < U), and the lane
+    // stride between the holders of consecutive edges (L >= U)
+    const int nv = U > L ? U / L : 1;
+    const int hstride = U > L ? 1 : L / U;
 
     float result = 0.f;  // lane t ends with the dot of position p0 + t
     const int SU = S * U;
@@ -326,20 +327,46 @@ __global__ __launch_bounds__(kBlock) void spmm_grad_w(GradWParams P) {
                 }
             }
         }
-        // reduce each dot over the slot's L lanes (fixed tree; lane j = 0 holds it)
+        // reduce the U dots over the slot's L lanes (L a power of two, slots
+        // aligned) by recursive halving: at stride m the lanes with bit m set
+        // keep the upper half of their values, the others the lower half, and
+        // each adds its partner's copy of the half it keeps; once one value
+        // is left, plain butterflies finish the sum.  A fixed pattern, so the
+        // result is deterministic.  Afterwards lane j holds in dot[i] (i < nv)
+        // the total of edge u = (j / hstride) * nv + i.
+        int m = L >> 1;
 #pragma unroll
-        for (int u = 0; u < U; ++u)
-            for (int off = top; off >= 1; off >>= 1) {
-                const float o = __shfl(dot[u], (lane + off) & (kWave - 1));
-                if (j + off < L) dot[u] += o;
+        for (int h = U / 2; h >= 1; h >>= 1) {
+            if (m >= 1) {
+                const bool up = (lane & m) != 0;
+#pragma unroll
+                for (int i = 0; i < h; ++i) {
+                    const float send = up ? dot[i] : dot[i + h];
+                    const float keep = up ? dot[i + h] : dot[i];
+                    dot[i] = keep + __shfl_xor(send, m);
+                }
+                m >>= 1;
             }
-        // lane t picks the dot of position base + u*S + s from lane s*L
+        }
+        for (; m >= 1; m >>= 1) dot[0] += __shfl_xor(dot[0], m);
+        // lane t picks the total of position base + u*S + s from its holder
         const int rel = lane - base;
 #pragma unroll
         for (int u = 0; u < U; ++u) {
             const int s = rel - u * S;
-            const float o = __shfl(dot[u], (s >= 0 && s < S ? s * L : 0) & (kWave - 1));
-            if (s >= 0 && s < S) result = o;
+            const bool mine = s >= 0 && s < S;
+            const int src = ((mine ? s : 0) * L + (u / nv) * hstride) & (kWave - 1);
+            float o = __shfl(dot[0], src);
+            if (nv > 1) {
+#pragma unroll
+                for (int i = 1; i < U; ++i) {
+                    if (i < nv) {
+                        const float q = __shfl(dot[i], src);
+                        if (i == u % nv) o = q;
+                    }
+                }
+            }
+            if (mine) result = o;
         }
     }
     if (lane < rem) {
@@ -417,9 +444,18 @@ hipError_t launch_scale_inv_deg(const void* g, int g_bf16, const void* rowptr, i
     return hipGetLastError();
 }
 
-hipError_t launch_spmm_grad_w(const GradWParams& p, int x_dtype, int g_dtype, int epl,
+hipError_t launch_spmm_grad_w(const GradWParams& p0, int x_dtype, int g_dtype, int epl,
                               hipStream_t s) {
-    if (p.E <= 0) return hipSuccess;
+    if (p0.E <= 0) return hipSuccess;
+    // slots of a power-of-two width at aligned lanes, as the dot reduction
+    // needs (lanes past the feature row hold zeros)
+    GradWParams p = p0;
+    if (p.L < kWave) {
+        int lp = 1;
+        while (lp < p.L) lp *= 2;
+        p.L = lp;
+        p.S = kWave / lp;
+    }
     const int64_t waves = ceil_div(p.E, kWave);
     const unsigned grid = (unsigned)ceil_div(waves, kWavesPerBlock);
     if (x_dtype == MP_F32)
