@@ -411,7 +411,7 @@ def explain_step(g, mp, torch, np, dev, mark, seed):
     ops = [("msg_gather_f32", 4 * E + 2 * EF4, 0),
            ("mask_callback", 4 * E + 2 * EF4, 0),
            ("msg_sum", rp + EF4 + N * F * 4, E * F),
-           ("msg_backward_sum", rp + 8 * E + N * F * 4 + EF4, 0),
+           ("msg_backward_sum", rp + N * F * 4 + EF4, 0),
            ("mask_grad", 2 * EF4 + 4 * E, 0),
            ("msg_input_grad", 4 * E + 2 * EF4, 0),
            ("grad_x_sum", rp + 4 * E + EF4 + N * F * 4, E * F)]

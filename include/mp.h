@@ -463,8 +463,8 @@ int mp_spmm_materialized(const mp_plan* plan, const void* rowptr, int rowptr_ity
                          int out_dtype, void* out_max, int max_dtype, int32_t* argout, void* ws,
                          size_t ws_bytes, void* stream);
 
-/* Workspace bytes for mp_message_backward (the row of every CSR position:
- * 4 * E, rounded up to 256). */
+/* Workspace bytes for mp_message_backward: 0 (the call takes no workspace;
+ * ws may be NULL and ws_bytes 0). */
 int mp_message_backward_workspace(int64_t E, size_t* bytes);
 
 /* Gradient of the aggregation of materialized messages with respect to each

@@ -954,7 +954,7 @@ int mp_spmm_materialized(const mp_plan* plan, const void* rowptr, int rowptr_ity
 int mp_message_backward_workspace(int64_t E, size_t* bytes) {
     if (!bytes) return MP_ERR_NULL;
     if (E < 0 || E > INT32_MAX) return MP_ERR_SIZE;
-    *bytes = E == 0 ? 0 : align_up((size_t)E * 4, 256);
+    *bytes = 0;  // the kernels need none
     return MP_OK;
 }
 
@@ -966,23 +966,21 @@ int mp_message_backward(const void* rowptr, int rowptr_itype, const int32_t* arg
     if (N_dst < 1 || N_dst > INT32_MAX || E < 0 || E > INT32_MAX || F < 1 || F > 65536)
         return MP_ERR_SIZE;
     if (!rowptr) return MP_ERR_NULL;
+    (void)ws;
+    (void)ws_bytes;
     if (E == 0) return MP_OK;
-    if (!grad_out || !dmsg || !ws) return MP_ERR_NULL;
+    if (!grad_out || !dmsg) return MP_ERR_NULL;
     if (reduce == MP_MAX && !argout) return MP_ERR_NULL;
-    if (ws_bytes < align_up((size_t)E * 4, 256)) return MP_ERR_WORKSPACE;
     const int eg = g_dtype == MP_BF16 ? 2 : 4;
     if ((uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4) || (uintptr_t)argout % 4 ||
         (uintptr_t)grad_out % eg || (uintptr_t)dmsg % 4)
         return MP_ERR_ALIGN;
     hipStream_t s = as_stream(stream);
-    int32_t* row = static_cast<int32_t*>(ws);
-    if (launch_rows_of_edges(rowptr, rowptr_itype == MP_I64, N_dst, E, row, s) != hipSuccess)
-        return MP_ERR_HIP;
     const uintptr_t ptrs[3] = {(uintptr_t)grad_out, (uintptr_t)dmsg,
                                reduce == MP_MAX ? (uintptr_t)argout : 0};
     const int sizes[3] = {eg, 4, 4};
-    MessageBackward b{rowptr, rowptr_itype == MP_I64, row, argout, grad_out, g_dtype == MP_BF16,
-                      E, F, reduce, message_epl(F, ptrs, sizes, 3, 4), dmsg};
+    MessageBackward b{rowptr, rowptr_itype == MP_I64, argout, grad_out, g_dtype == MP_BF16,
+                      N_dst, E, F, reduce, message_epl(F, ptrs, sizes, 3, 4), dmsg};
     return hip_status(launch_message_backward(b, s));
 }
 

@@ -15,12 +15,14 @@
 //                       mean: divided by the in-degree; max: routed to the
 //                       argmax edge only)
 //
-// All three are streaming kernels over the flat [E, F] table cut into
-// lane-chunks of EPL elements (one vector access each): consecutive threads
-// take consecutive chunks, so the table side is read and written fully
-// coalesced, and a gathered feature row is read by consecutive lanes.  Each
-// thread handles a few chunks spaced one block apart, issuing all index
-// loads, then all row loads, before any store.
+// The gather and the scale are streaming kernels over the flat [E, F] table
+// cut into lane-chunks of EPL elements (one vector access each): consecutive
+// threads take consecutive chunks, so the table side is read and written
+// fully coalesced, and a gathered feature row is read by consecutive lanes.
+// Each thread handles a few chunks spaced one block apart, issuing all index
+// loads, then all row loads, before any store.  The gradient goes row by
+// row: a destination row's gradient is loaded once and written to the
+// consecutive message rows of its edges.
 #include <type_traits>
 
 #include "mp_internal.hpp"
@@ -29,10 +31,8 @@ namespace mp {
 namespace {
 
 constexpr int kBlock = 256;
-// lane-chunks per thread: 4 for the gather and the scale, 8 for the
-// gradient (its loads hit the caches, its stores stream: more in flight)
+// lane-chunks per thread of the gather and the scale
 constexpr int kItems = 4;
-constexpr int kItemsBackward = 8;
 
 __device__ inline float bf16_bits(uint32_t b) { return __uint_as_float(b << 16); }
 
@@ -244,64 +244,64 @@ __device__ inline int64_t rp_load(const void* rp, int rp64, int64_t i) {
     return rp64 ? static_cast<const int64_t*>(rp)[i] : (int64_t) static_cast<const int32_t*>(rp)[i];
 }
 
-// dmsg[p, :] for CSR edge p of row v = row[p], from g = dL/dout [N, F]:
-// sum g[v, :]; mean g[v, :] / deg(v) (correctly rounded; in fp64 for degrees
-// beyond 2^24, which fp32 cannot hold); max g[v, f] where argout[v, f] == p.
-template <typename TG, int EPL, int MODE>
-__device__ inline void backward_vblock(const ChunkPos<kItemsBackward>& c,
-                                       const void* __restrict__ rowptr, int rp64,
-                                       const int32_t* __restrict__ row,
-                                       const int32_t* __restrict__ argout,
-                                       const TG* __restrict__ g, int64_t F,
-                                       float* __restrict__ dmsg) {
-    int32_t v[kItemsBackward];
-#pragma unroll
-    for (int i = 0; i < kItemsBackward; ++i) v[i] = c.ok[i] ? row[c.p[i]] : 0;
-    float gv[kItemsBackward][EPL];
-    int32_t am[MODE == kMax ? kItemsBackward : 1][EPL];
-    int64_t deg[kItemsBackward];
-#pragma unroll
-    for (int i = 0; i < kItemsBackward; ++i) {
-        deg[i] = 1;
-        if (!c.ok[i]) continue;
-        const int64_t o = (int64_t)v[i] * F + (int64_t)c.k[i] * EPL;
-        load_chunk<TG, EPL>(g + o, gv[i]);
-        if constexpr (MODE == kMax) load_ints<EPL>(argout + o, am[i]);
-        if constexpr (MODE == kMean)
-            deg[i] = rp_load(rowptr, rp64, (int64_t)v[i] + 1) - rp_load(rowptr, rp64, v[i]);
-    }
-#pragma unroll
-    for (int i = 0; i < kItemsBackward; ++i) {
-        if (!c.ok[i]) continue;
-        float d[EPL];
-#pragma unroll
-        for (int e = 0; e < EPL; ++e) {
-            if constexpr (MODE == kSum) {
-                d[e] = gv[i][e];
-            } else if constexpr (MODE == kMean) {
-                d[e] = deg[i] <= (int64_t(1) << 24)
-                           ? gv[i][e] / (float)deg[i]
-                           : (float)((double)gv[i][e] / (double)deg[i]);
-            } else {
-                d[e] = am[i][e] == (int32_t)c.p[i] ? gv[i][e] : 0.f;
-            }
-        }
-        store_f32<EPL>(dmsg + c.g[i] * EPL, d);
-    }
-}
-
+// dmsg[p, :] for the CSR edges p of destination row v, from g = dL/dout
+// [N, F]: sum g[v, :]; mean g[v, :] / deg(v) (correctly rounded; in fp64 for
+// degrees beyond 2^24, which fp32 cannot hold); max g[v, f] where
+// argout[v, f] == p.  One wavefront per row: its lanes load the row's
+// gradient chunks once (and, for max, its argmax chunks), then stream them
+// to the message rows of all of v's edges, which are consecutive: slot s of
+// the S slots of L lanes writes edges s, s + S, ..., so one store
+// instruction covers S whole consecutive rows.  Rows wider than 64
+// lane-chunks take one more pass per 64 chunks.  No loads in the store loop.
 template <typename TG, int EPL, int MODE>
 __global__ __launch_bounds__(kBlock) void message_backward(const void* __restrict__ rowptr,
                                                            int rp64,
-                                                           const int32_t* __restrict__ row,
                                                            const int32_t* __restrict__ argout,
-                                                           const TG* __restrict__ g, int64_t F,
-                                                           int64_t cpr, int64_t total,
+                                                           const TG* __restrict__ g, int64_t N,
+                                                           int64_t F, int64_t cpr, int L, int S,
                                                            float* __restrict__ dmsg) {
-    const int64_t nvb = vblocks<kItemsBackward>(total);
-    for (int64_t vb = blockIdx.x; vb < nvb; vb += gridDim.x)
-        backward_vblock<TG, EPL, MODE>(chunk_positions<kItemsBackward>(vb, total, cpr), rowptr,
-                                       rp64, row, argout, g, F, dmsg);
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t v = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave)) +
+                      (int64_t)blockIdx.x * (kBlock / kWave);
+    if (v >= N) return;
+    const int64_t beg = rp_load(rowptr, rp64, v);
+    const int64_t deg = rp_load(rowptr, rp64, v + 1) - beg;
+    const int slot = lane / L;
+    const int j = lane - slot * L;
+    if (deg <= 0 || slot >= S) return;
+    for (int64_t k = j; k < cpr; k += L) {
+        const int64_t o = v * F + k * EPL;
+        float gv[EPL];
+        load_chunk<TG, EPL>(g + o, gv);
+        int32_t am[MODE == kMax ? EPL : 1];
+        if constexpr (MODE == kMax) load_ints<EPL>(argout + o, am);
+        if constexpr (MODE == kMean) {
+#pragma unroll
+            for (int e = 0; e < EPL; ++e)
+                gv[e] = deg <= (int64_t(1) << 24) ? gv[e] / (float)deg
+                                                 : (float)((double)gv[e] / (double)deg);
+        }
+        float* out = dmsg + (beg + slot) * F + k * EPL;
+        const int64_t step = (int64_t)S * F;
+        for (int64_t e = slot; e < deg; e += S, out += step) {
+            float d[EPL];
+#pragma unroll
+            for (int x = 0; x < EPL; ++x) {
+                if constexpr (MODE == kMax)
+                    d[x] = am[x] == (int32_t)(beg + e) ? gv[x] : 0.f;
+                else
+                    d[x] = gv[x];
+            }
+            // plain stores: measured faster here than non-temporal ones
+            // (which the read-and-write kernels above prefer)
+            if constexpr (EPL == 4)
+                *reinterpret_cast<float4*>(out) = make_float4(d[0], d[1], d[2], d[3]);
+            else if constexpr (EPL == 2)
+                *reinterpret_cast<float2*>(out) = make_float2(d[0], d[1]);
+            else
+                *out = d[0];
+        }
+    }
 }
 
 // Launch at most this many blocks; larger tables are walked by the grid stride.
@@ -351,18 +351,20 @@ hipError_t gather_epl(const MessageGather& a, hipStream_t s) {
 
 template <typename TG, int EPL>
 hipError_t backward_mode(const MessageBackward& a, hipStream_t s) {
-    const int64_t cpr = a.F / EPL, total = a.E * cpr;
+    const int64_t cpr = a.F / EPL;
+    const int L = cpr < kWave ? (int)cpr : kWave;
+    const int S = kWave / L;
     const TG* g = static_cast<const TG*>(a.g);
-    const dim3 grid(grid_for(total, kItemsBackward)), block(kBlock);
+    const dim3 grid((unsigned)ceil_div(a.N, kBlock / kWave)), block(kBlock);
     if (a.reduce == kMax)
         hipLaunchKernelGGL((message_backward<TG, EPL, kMax>), grid, block, 0, s, a.rowptr, a.rp64,
-                           a.row, a.argout, g, a.F, cpr, total, a.dmsg);
+                           a.argout, g, a.N, a.F, cpr, L, S, a.dmsg);
     else if (a.reduce == kMean)
         hipLaunchKernelGGL((message_backward<TG, EPL, kMean>), grid, block, 0, s, a.rowptr, a.rp64,
-                           a.row, a.argout, g, a.F, cpr, total, a.dmsg);
+                           a.argout, g, a.N, a.F, cpr, L, S, a.dmsg);
     else
         hipLaunchKernelGGL((message_backward<TG, EPL, kSum>), grid, block, 0, s, a.rowptr, a.rp64,
-                           a.row, a.argout, g, a.F, cpr, total, a.dmsg);
+                           a.argout, g, a.N, a.F, cpr, L, S, a.dmsg);
     return hipGetLastError();
 }
 
@@ -410,7 +412,7 @@ hipError_t launch_message_scale(const float* in, float* out, const float* mask,
 }
 
 hipError_t launch_message_backward(const MessageBackward& a, hipStream_t s) {
-    if (a.E <= 0) return hipSuccess;
+    if (a.E <= 0 || a.N <= 0) return hipSuccess;
     return a.g_bf16 ? backward_epl<uint16_t>(a, s) : backward_epl<float>(a, s);
 }
 

@@ -257,11 +257,10 @@ struct MessageGather {
 struct MessageBackward {
     const void* rowptr;
     int rp64;
-    const int32_t* row;     // [E] destination row of every CSR position
     const int32_t* argout;  // [N_dst, F] (max only)
     const void* g;          // [N_dst, F] dL/dout
     int g_bf16;
-    int64_t E, F;
+    int64_t N, E, F;
     int reduce;             // exactly one of kSum, kMean, kMax
     int epl;
     float* dmsg;            // [E, F]
