@@ -305,6 +305,29 @@ def test_message_backward(mixed, reduce, gdtype, itype):
     assert np.array_equal(dmsg.cpu().numpy().view(np.uint32), ref.view(np.uint32))
 
 
+@pytest.mark.parametrize("F", [1, 3, 100, 300, 520])
+@pytest.mark.parametrize("reduce", ["sum", "mean", "max"])
+def test_message_backward_shapes(F, reduce):
+    """Rows of 0 to 70,000 edges (a row's gradient streamed to many message
+    rows), feature counts with 1-, 2- and 4-element chunks and rows wider
+    than one pass of 64 chunks; argmax positions drawn within each row."""
+    degs = np.array([0, 1, 5, 70_000, 0, 130, 2, 64, 65])
+    n_dst = degs.size
+    rp_o = np.concatenate([[0], np.cumsum(degs)]).astype(np.int64)
+    E = int(rp_o[-1])
+    rng = np.random.default_rng(F)
+    G = rng.standard_normal((n_dst, F)).astype(np.float32)
+    am = np.full((n_dst, F), -1, np.int64)
+    for v in range(n_dst):
+        if degs[v]:
+            am[v] = rp_o[v] + rng.integers(0, degs[v], F)
+    dmsg = mp.message_backward(dev(rp_o.astype(np.int32)), dev(G), REDUCES[reduce], E=E,
+                               argout=dev(am.astype(np.int32)))
+    torch.cuda.synchronize()
+    ref = oracle.message_backward(rp_o, reduce, argout=am, g=G)
+    assert np.array_equal(dmsg.cpu().numpy().view(np.uint32), ref.view(np.uint32))
+
+
 @pytest.mark.parametrize("adtype,bdtype", [(torch.float32, torch.float32),
                                            (torch.bfloat16, torch.float32),
                                            (torch.float32, torch.bfloat16),
