@@ -541,14 +541,121 @@ __device__ inline void wave_range_masked(const SpmmParams& P,
     }
 }
 
+// The masked sum over small rows (one slot per row, as in slot_row): an
+// iteration covers U edges of every slot's row, U capped so that the
+// iteration's win-mask words fit the wavefront one per lane (lane l takes
+// word l % mww of edge u of slot s, l / mww = u * S + s), shared by
+// cross-lane permute as in wave_range_masked.  Loads run ahead: the indices
+// two iterations ahead and the mask words one iteration ahead are in flight
+// while an iteration gathers its chunks.
+template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, bool O32>
+__device__ inline void slot_row_masked(const SpmmParams& P,
+                                       AccFor<TX, EPL, HS, HM, kModeMasked>& acc, int64_t e0,
+                                       int32_t my_n, int32_t max_n, int lane, int slot, int j,
+                                       bool feat_ok, int64_t fe, int64_t w_lo, int mww) {
+    using R = typename RawVec<TX, EPL>::T;
+    constexpr int A = AccFor<TX, EPL, HS, HM, kModeMasked>::A;
+    if (max_n <= 0) return;
+    const int L = P.L, S = P.S;
+    int U = kUnroll;
+    if (U > L) U = L;  // the first U lanes of a slot load its indices
+    if (S * U * mww > kWave) U = kWave / (S * mww);  // S * mww <= 64, so U >= 1
+    const int me = lane / mww;  // edge of an iteration whose word this lane loads
+    const int mq = lane - me * mww;
+    const int mu = me / S, ms = me - mu * S;
+    const bool mload = me < S * U;
+    const int32_t n_ms = __shfl(my_n, (ms * L) & (kWave - 1));  // row length of slot ms
+    const int wi = (int)((fe >> 5) - w_lo);
+    // lanes j < U of each slot: column, weight and forward position of edge
+    // it + j of the slot's row
+    auto indices = [&](int32_t it, int32_t& c, int32_t& k, float& w) {
+        c = 0;
+        k = -1;
+        w = 1.f;
+        if (slot < S && j < U && it + j < my_n) {
+            c = col_at(P, e0 + it + j);
+            if constexpr (W) w = __builtin_nontemporal_load(P.w + e0 + it + j);
+            k = __builtin_nontemporal_load(P.ekey + e0 + it + j);
+        }
+    };
+    // this lane's share of the mask words of iteration it (unconditional
+    // load: word 0 for a lane or edge past the end, never read)
+    auto mword = [&](int32_t it, int32_t k) -> uint32_t {
+        const int32_t key = __shfl(k, (ms * L + mu) & (kWave - 1));
+        const bool v = mload && it + mu < n_ms;
+        return P.mbits[v ? (int64_t)key * P.mw + w_lo + mq : 0];
+    };
+    int32_t c0, k0, c1, k1;
+    float w0, w1;
+    indices(0, c0, k0, w0);
+    indices(U, c1, k1, w1);
+    uint32_t mcur = mword(0, k0);
+    for (int32_t it = 0; it < max_n; it += U) {
+        const char* addr[O32 ? 1 : kUnroll];
+        uint32_t off[O32 ? kUnroll : 1];
+        bool ok[kUnroll];
+        uint64_t bits = 0;  // EPL bits per edge of this lane's slot
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            const uint32_t w = __shfl(mcur, ((u * S + slot) * mww + wi) & (kWave - 1));
+            const uint32_t b = feat_ok && u < U && it + u < my_n ? lane_bits<EPL>(w, fe) : 0u;
+            ok[u] = b != 0u;
+            bits |= (uint64_t)b << (u * EPL);
+            const int32_t c = __shfl(c0, (slot * L + u) & (kWave - 1));
+            if constexpr (O32)
+                off[u] = ((uint32_t)c * (uint32_t)P.ldx + (uint32_t)fe) * (uint32_t)sizeof(TX);
+            else
+                addr[u] = feat_addr<TX, NT>(P, c, fe);
+        }
+        // the next iteration's words (its indices arrived during this one),
+        // then the indices of the iteration after it
+        const uint32_t mnext = mword(it + U, k1);
+        int32_t c2, k2;
+        float w2;
+        indices(it + 2 * U, c2, k2, w2);
+        R raw[kUnroll];
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            if (ok[u]) {
+                if constexpr (O32)
+                    raw[u] = *reinterpret_cast<const R*>(P.table_ptr[0] + off[u]);
+                else
+                    raw[u] = *reinterpret_cast<const R*>(addr[u]);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < kUnroll; ++u) {
+            float wt = 1.f;
+            if constexpr (W) wt = __shfl(w0, (slot * L + u) & (kWave - 1));
+            if (ok[u]) {
+                float v[EPL];
+                widen<TX, EPL>(raw[u], v);
+                if constexpr (W) {
+#pragma unroll
+                    for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt, v[k]);
+                }
+                apply_mask<EPL>(v, (uint32_t)(bits >> (u * EPL)));
+                acc.add(u % A, v, (int32_t)(e0 + it + u));
+            }
+        }
+        mcur = mnext;
+        c0 = c1;
+        k0 = k1;
+        w0 = w1;
+        c1 = c2;
+        k1 = k2;
+        w1 = w2;
+    }
+}
+
 // One slot per row: every slot walks its own row's edges, U at a time.
 // COOP: the slot has at least U lanes, which load its next U columns
-// together; otherwise each lane loads the columns itself.
+// together; otherwise each lane loads the columns itself.  (The masked sum
+// has its own pipelined variant above.)
 template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, int MODE, bool COOP, bool O32>
 __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MODE>& acc,
                                 int64_t e0, int32_t my_n, int32_t max_n, int slot, int j,
                                 bool feat_ok, int64_t fe) {
-    constexpr bool MK = MODE == kModeMasked;
     using R = typename RawVec<TX, EPL>::T;
     constexpr int A = AccFor<TX, EPL, HS, HM, MODE>::A;
     const int L = P.L;
@@ -556,14 +663,12 @@ __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MOD
         const char* addr[kUnroll];
         bool ok[kUnroll];
         float wt[kUnroll];
-        int32_t key[kUnroll];
         if constexpr (COOP) {
-            int32_t myc = 0, myk = -1;
+            int32_t myc = 0;
             float myw = 1.f;
             if (j < kUnroll && it + j < my_n) {
                 myc = col_at(P, e0 + it + j);
                 if constexpr (W) myw = __builtin_nontemporal_load(P.w + e0 + it + j);
-                if constexpr (MK) myk = __builtin_nontemporal_load(P.ekey + e0 + it + j);
             }
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) {
@@ -571,8 +676,6 @@ __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MOD
                 const int32_t c = __shfl(myc, srcl);
                 wt[u] = 1.f;
                 if constexpr (W) wt[u] = __shfl(myw, srcl);
-                key[u] = -1;
-                if constexpr (MK) key[u] = __shfl(myk, srcl);
                 ok[u] = feat_ok && (it + u < my_n);
                 addr[u] = feat_addr<TX, NT>(P, c, fe);
             }
@@ -584,27 +687,11 @@ __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MOD
                 cc[u] = ok[u] ? (P.col ? P.col[e0 + it + u] : (int32_t)(e0 + it + u)) : 0;
                 wt[u] = 1.f;
                 if constexpr (W) wt[u] = ok[u] ? P.w[e0 + it + u] : 1.f;
-                key[u] = -1;
-                if constexpr (MK) key[u] = ok[u] ? P.ekey[e0 + it + u] : -1;
             }
 #pragma unroll
             for (int u = 0; u < kUnroll; ++u) addr[u] = feat_addr<TX, NT>(P, cc[u], fe);
         }
         R raw[kUnroll];
-        uint32_t mb[MK ? kUnroll : 1];
-        if constexpr (MK) {
-            // masked sum: win-mask words first (unconditional loads, word 0
-            // for an invalid edge, so that all are in flight together), then
-            // only the chunks that hit
-#pragma unroll
-            for (int u = 0; u < kUnroll; ++u)
-                mb[u] = P.mbits[ok[u] ? (int64_t)key[u] * P.mw + (fe >> 5) : 0];
-#pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
-                mb[u] = ok[u] ? lane_bits<EPL>(mb[u], fe) : 0u;
-                ok[u] = ok[u] && mb[u] != 0u;
-            }
-        }
 #pragma unroll
         for (int u = 0; u < kUnroll; ++u)
             if (ok[u]) raw[u] = load_row_chunk<R, O32>(P.table_ptr[0], addr[u]);
@@ -617,7 +704,6 @@ __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MOD
 #pragma unroll
                     for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt[u], v[k]);
                 }
-                if constexpr (MK) apply_mask<EPL>(v, mb[u]);
                 acc.add(u % A, v, (int32_t)(e0 + it + u));
             }
         }
@@ -738,12 +824,19 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
         const int32_t o = __shfl_xor(max_n, off);
         max_n = o > max_n ? o : max_n;
     }
-    if (L >= kUnroll)
+    if constexpr (MODE == kModeMasked) {
+        const int64_t w_lo = (int64_t)ft * 2 * EPL;
+        const int64_t wmax = P.mw - w_lo;
+        const int mww = (int)(wmax < 2 * EPL ? wmax : 2 * EPL);
+        slot_row_masked<TX, EPL, HS, HM, NT, W, O32>(P, acc, e0, my_n, max_n, lane, slot, j,
+                                                     feat_ok, fe, w_lo, mww);
+    } else if (L >= kUnroll) {
         slot_row<TX, EPL, HS, HM, NT, W, MODE, true, O32>(P, acc, e0, my_n, max_n, slot, j, feat_ok,
                                                          fe);
-    else
+    } else {
         slot_row<TX, EPL, HS, HM, NT, W, MODE, false, O32>(P, acc, e0, my_n, max_n, slot, j, feat_ok,
                                                           fe);
+    }
     acc.fold();
     if (feat_ok) {
         if constexpr (HX)
