@@ -31,6 +31,9 @@ namespace {
 constexpr int kBlock = 256;
 constexpr int kWavesPerBlock = kBlock / kWave;
 constexpr int kRowItems = 8;  // CSR positions per thread in rows_of_edges
+#ifndef MP_GW_UNROLL
+#define MP_GW_UNROLL 4  // edges per slot per step of the weight gradient (sum, mean)
+#endif
 
 __device__ inline int64_t rp_at(const void* rp, int rp64, int64_t i) {
     return rp64 ? static_cast<const int64_t*>(rp)[i] : (int64_t) static_cast<const int32_t*>(rp)[i];
@@ -250,7 +253,7 @@ __device__ inline void load_ints(const int32_t* p, int32_t (&v)[EPL]) {
 // (u < U) of each step, its L lanes covering the feature row in FT tiles.
 template <typename TX, typename TG, int EPL, int MODE>
 __global__ __launch_bounds__(kBlock) void spmm_grad_w(GradWParams P) {
-    constexpr int U = MODE == kMax ? 4 : 8;
+    constexpr int U = MODE == kMax ? 4 : MP_GW_UNROLL;
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave)) +
                        (int64_t)blockIdx.x * kWavesPerBlock;
