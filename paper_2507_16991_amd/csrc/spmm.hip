@@ -29,6 +29,12 @@ namespace {
 constexpr int kBlock = 256;
 constexpr int kWavesPerBlock = kBlock / kWave;
 constexpr int kUnroll = 8;  // edges gathered per slot per iteration
+#ifndef MP_STATS_UNROLL
+#define MP_STATS_UNROLL 8   // the same for the stacked statistics
+#endif
+#ifndef MP_MASKED_UNROLL
+#define MP_MASKED_UNROLL 8  // the same for the masked sum
+#endif
 
 // Kernel modes: the plain aggregation (sum/mean and/or max); the masked sum
 // (the gradient of max); and the stacked statistics (sum, sum of squares, max
@@ -37,6 +43,12 @@ constexpr int kUnroll = 8;  // edges gathered per slot per iteration
 constexpr int kModePlain = 0;
 constexpr int kModeMasked = 1;
 constexpr int kModeStats = 2;
+
+// Edges per slot per iteration of a mode (array sizes of the gather loops).
+template <int MODE>
+constexpr int unroll_of() {
+    return MODE == kModeStats ? MP_STATS_UNROLL : MODE == kModeMasked ? MP_MASKED_UNROLL : kUnroll;
+}
 
 // ---- feature loads ----------------------------------------------------------
 
@@ -376,6 +388,7 @@ __device__ inline void wave_range(const SpmmParams& P,
                                   int64_t e1, int lane, int slot, bool feat_ok, int64_t fe, int U) {
     using R = typename RawVec<TX, EPL>::T;
     constexpr int A = AccFor<TX, EPL, HS, HM, MODE>::A;
+    constexpr int UN = unroll_of<MODE>();
     const int S = P.S;
     const int SU = S * U;
     const int steps = kWave / SU;
@@ -391,21 +404,21 @@ __device__ inline void wave_range(const SpmmParams& P,
         for (int st = 0; st < steps; ++st) {
             const int base = st * SU;
             if (base >= rem) break;
-            const char* addr[kUnroll];
-            bool ok[kUnroll];
+            const char* addr[UN];
+            bool ok[UN];
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
+            for (int u = 0; u < UN; ++u) {
                 const int t = base + u * S + slot;
                 const int32_t c = __shfl(myc, t);
                 ok[u] = feat_ok && (u < U) && (t < rem);
                 addr[u] = feat_addr<TX, NT>(P, c, fe);
             }
-            R raw[kUnroll];
+            R raw[UN];
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u)
+            for (int u = 0; u < UN; ++u)
                 if (ok[u]) raw[u] = load_row_chunk<R, O32>(P.table_ptr[0], addr[u]);
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
+            for (int u = 0; u < UN; ++u) {
                 const int t = base + u * S + slot;
                 float wt = 1.f;
                 if constexpr (W) wt = __shfl(myw, t);
@@ -441,9 +454,10 @@ __device__ inline void wave_range_masked(const SpmmParams& P,
                                          int64_t w_lo, int mww) {
     using R = typename RawVec<TX, EPL>::T;
     constexpr int A = AccFor<TX, EPL, HS, HM, kModeMasked>::A;
+    constexpr int UN = unroll_of<kModeMasked>();
     if (e0 >= e1) return;
     const int S = P.S;
-    int U = kUnroll;
+    int U = UN;
     if (S * U > kWave) U = kWave / S;
     if (S * U * mww > kWave) U = kWave / (S * mww);  // S * mww <= 64, so U >= 1
     const int SU = S * U;
@@ -486,12 +500,12 @@ __device__ inline void wave_range_masked(const SpmmParams& P,
             if (base >= rem) break;
             // row-chunk addresses: 32-bit byte offsets from the table base
             // when the table spans under 4 GiB (one register each)
-            const char* addr[O32 ? 1 : kUnroll];
-            uint32_t off[O32 ? kUnroll : 1];
-            bool ok[kUnroll];
+            const char* addr[O32 ? 1 : UN];
+            uint32_t off[O32 ? UN : 1];
+            bool ok[UN];
             uint64_t bits = 0;  // EPL bits per edge of this lane's slot
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
+            for (int u = 0; u < UN; ++u) {
                 const int t = base + u * S + slot;
                 const uint32_t w = __shfl(mcur, ((u * S + slot) * mww + wi) & (kWave - 1));
                 const uint32_t b = feat_ok && u < U && t < rem ? lane_bits<EPL>(w, fe) : 0u;
@@ -507,9 +521,9 @@ __device__ inline void wave_range_masked(const SpmmParams& P,
             // next one
             const uint32_t mnext = st + 1 < steps && base + SU < rem ? mword(myk, base + SU, rem)
                                                                      : mword(nk, 0, e1 - nxt);
-            R raw[kUnroll];
+            R raw[UN];
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
+            for (int u = 0; u < UN; ++u) {
                 if (ok[u]) {
                     if constexpr (O32)
                         raw[u] = *reinterpret_cast<const R*>(P.table_ptr[0] + off[u]);
@@ -518,7 +532,7 @@ __device__ inline void wave_range_masked(const SpmmParams& P,
                 }
             }
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
+            for (int u = 0; u < UN; ++u) {
                 const int t = base + u * S + slot;
                 float wt = 1.f;
                 if constexpr (W) wt = __shfl(myw, t & (kWave - 1));
@@ -555,9 +569,10 @@ __device__ inline void slot_row_masked(const SpmmParams& P,
                                        bool feat_ok, int64_t fe, int64_t w_lo, int mww) {
     using R = typename RawVec<TX, EPL>::T;
     constexpr int A = AccFor<TX, EPL, HS, HM, kModeMasked>::A;
+    constexpr int UN = unroll_of<kModeMasked>();
     if (max_n <= 0) return;
     const int L = P.L, S = P.S;
-    int U = kUnroll;
+    int U = UN;
     if (U > L) U = L;  // the first U lanes of a slot load its indices
     if (S * U * mww > kWave) U = kWave / (S * mww);  // S * mww <= 64, so U >= 1
     const int me = lane / mww;  // edge of an iteration whose word this lane loads
@@ -591,12 +606,12 @@ __device__ inline void slot_row_masked(const SpmmParams& P,
     indices(U, c1, k1, w1);
     uint32_t mcur = mword(0, k0);
     for (int32_t it = 0; it < max_n; it += U) {
-        const char* addr[O32 ? 1 : kUnroll];
-        uint32_t off[O32 ? kUnroll : 1];
-        bool ok[kUnroll];
+        const char* addr[O32 ? 1 : UN];
+        uint32_t off[O32 ? UN : 1];
+        bool ok[UN];
         uint64_t bits = 0;  // EPL bits per edge of this lane's slot
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
+        for (int u = 0; u < UN; ++u) {
             const uint32_t w = __shfl(mcur, ((u * S + slot) * mww + wi) & (kWave - 1));
             const uint32_t b = feat_ok && u < U && it + u < my_n ? lane_bits<EPL>(w, fe) : 0u;
             ok[u] = b != 0u;
@@ -613,9 +628,9 @@ __device__ inline void slot_row_masked(const SpmmParams& P,
         int32_t c2, k2;
         float w2;
         indices(it + 2 * U, c2, k2, w2);
-        R raw[kUnroll];
+        R raw[UN];
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
+        for (int u = 0; u < UN; ++u) {
             if (ok[u]) {
                 if constexpr (O32)
                     raw[u] = *reinterpret_cast<const R*>(P.table_ptr[0] + off[u]);
@@ -624,7 +639,7 @@ __device__ inline void slot_row_masked(const SpmmParams& P,
             }
         }
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
+        for (int u = 0; u < UN; ++u) {
             float wt = 1.f;
             if constexpr (W) wt = __shfl(w0, (slot * L + u) & (kWave - 1));
             if (ok[u]) {
@@ -658,20 +673,21 @@ __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MOD
                                 bool feat_ok, int64_t fe) {
     using R = typename RawVec<TX, EPL>::T;
     constexpr int A = AccFor<TX, EPL, HS, HM, MODE>::A;
+    constexpr int UN = unroll_of<MODE>();
     const int L = P.L;
-    for (int32_t it = 0; it < max_n; it += kUnroll) {
-        const char* addr[kUnroll];
-        bool ok[kUnroll];
-        float wt[kUnroll];
+    for (int32_t it = 0; it < max_n; it += UN) {
+        const char* addr[UN];
+        bool ok[UN];
+        float wt[UN];
         if constexpr (COOP) {
             int32_t myc = 0;
             float myw = 1.f;
-            if (j < kUnroll && it + j < my_n) {
+            if (j < UN && it + j < my_n) {
                 myc = col_at(P, e0 + it + j);
                 if constexpr (W) myw = __builtin_nontemporal_load(P.w + e0 + it + j);
             }
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
+            for (int u = 0; u < UN; ++u) {
                 const int srcl = slot * L + u;
                 const int32_t c = __shfl(myc, srcl);
                 wt[u] = 1.f;
@@ -680,23 +696,23 @@ __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MOD
                 addr[u] = feat_addr<TX, NT>(P, c, fe);
             }
         } else {
-            int32_t cc[kUnroll];
+            int32_t cc[UN];
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) {
+            for (int u = 0; u < UN; ++u) {
                 ok[u] = feat_ok && (it + u < my_n);
                 cc[u] = ok[u] ? (P.col ? P.col[e0 + it + u] : (int32_t)(e0 + it + u)) : 0;
                 wt[u] = 1.f;
                 if constexpr (W) wt[u] = ok[u] ? P.w[e0 + it + u] : 1.f;
             }
 #pragma unroll
-            for (int u = 0; u < kUnroll; ++u) addr[u] = feat_addr<TX, NT>(P, cc[u], fe);
+            for (int u = 0; u < UN; ++u) addr[u] = feat_addr<TX, NT>(P, cc[u], fe);
         }
-        R raw[kUnroll];
+        R raw[UN];
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u)
+        for (int u = 0; u < UN; ++u)
             if (ok[u]) raw[u] = load_row_chunk<R, O32>(P.table_ptr[0], addr[u]);
 #pragma unroll
-        for (int u = 0; u < kUnroll; ++u) {
+        for (int u = 0; u < UN; ++u) {
             if (ok[u]) {
                 float v[EPL];
                 widen<TX, EPL>(raw[u], v);
@@ -733,7 +749,7 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
         const int64_t chunk_j = ft * (int64_t)kWave + j;  // lane-chunk index in the row
         const bool feat_ok = slot_ok && chunk_j < P.ltot;
         const int64_t fe = chunk_j * EPL;
-        int U = kUnroll;
+        int U = unroll_of<MODE>();
         if (S * U > kWave) U = kWave / S;
 
         int64_t row, e0, e1, cidx = 0;
@@ -830,7 +846,7 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
         const int mww = (int)(wmax < 2 * EPL ? wmax : 2 * EPL);
         slot_row_masked<TX, EPL, HS, HM, NT, W, O32>(P, acc, e0, my_n, max_n, lane, slot, j,
                                                      feat_ok, fe, w_lo, mww);
-    } else if (L >= kUnroll) {
+    } else if (L >= unroll_of<MODE>()) {
         slot_row<TX, EPL, HS, HM, NT, W, MODE, true, O32>(P, acc, e0, my_n, max_n, slot, j, feat_ok,
                                                          fe);
     } else {
