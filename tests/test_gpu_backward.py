@@ -241,9 +241,13 @@ def test_backward_plan_regimes(monkeypatch, thresholds, reduce):
     backward_case(g, reduce, torch.float32, torch.float32, True, True)
 
 
-@pytest.mark.parametrize("F", [1, 3, 8, 24, 100, 300, 520])
+@pytest.mark.parametrize("F", [1, 3, 8, 24, 64, 100, 128, 256, 300, 520, 1024])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
 def test_backward_feature_widths(F, dtype):
+    """Every lane-chunk width (1 to 8 elements), one to several 64-chunk
+    feature tiles, and win masks of 1 to 32 words per edge (so that the
+    masked gather caps its edges per step at 4 when a step's mask words
+    would not fit the wavefront)."""
     g = graphgen.mixed_graph(F, n=700, e=9000, f=F, signed_weights=True)
     for reduce in ("mean", "max"):
         backward_case(g, reduce, dtype, dtype, True, True, seed=F)
