@@ -10,7 +10,8 @@
 //     product of grad_out[v] and x[col[p]] per CSR edge p of row v (a
 //     sampled dense-dense product).  Edge-parallel: every wavefront takes 64
 //     consecutive CSR positions, so hub rows need no special handling; the
-//     per-edge dot is reduced over the lanes of a slot in a fixed tree.  With
+//     per-edge dots are reduced over the lanes of a slot by recursive
+//     halving, a fixed pattern.  With
 //     the row or column array absent (position p reads row p) the same kernel
 //     gives the per-edge dot products of the edge-materialized path.
 //   * win_masks: for the gradient of max, the features each forward edge
@@ -250,7 +251,8 @@ __device__ inline void load_ints(const int32_t* p, int32_t (&v)[EPL]) {
 // p of row v = row[p]; route is 1 (sum), 1/deg(v) (mean, applied to the
 // finished dot) or [argout[v, f] == p] (max).  A wavefront takes 64
 // consecutive positions; slot s of its S slots takes positions base + u*S + s
-// (u < U) of each step, its L lanes covering the feature row in FT tiles.
+// (u < U) of each step, its L lanes (a power of two, slots aligned) covering
+// the feature row in FT tiles.
 template <typename TX, typename TG, int EPL, int MODE>
 __global__ __launch_bounds__(kBlock) void spmm_grad_w(GradWParams P) {
     constexpr int U = MODE == kMax ? 4 : MP_GW_UNROLL;
