@@ -285,6 +285,16 @@ def test_backward_deterministic(mixed):
     c = mp.spmm_backward_w(rp, col, x, G, mp.MP_SUM)
     d = mp.spmm_backward_w(rp, col, x, G, mp.MP_SUM)
     assert torch.equal(a, b) and torch.equal(c, d)
+    # the max gradient (win masks, then the masked gather), twice
+    am = dev(oracle.spmm(rp_o, col_o, x=mixed.x, want=("max",))["argmax"].astype(np.int32))
+    e = mp.spmm_backward_x(rpt, colt, G, mp.MP_MAX, posT=post, rowptr=rp, argout=am,
+                           planT=planT)
+    f = mp.spmm_backward_x(rpt, colt, G, mp.MP_MAX, posT=post, rowptr=rp, argout=am,
+                           planT=planT)
+    h = mp.spmm_backward_w(rp, col, x, G, mp.MP_MEAN)
+    k = mp.spmm_backward_w(rp, col, x, G, mp.MP_MEAN)
+    torch.cuda.synchronize()
+    assert torch.equal(e, f) and torch.equal(h, k)
 
 
 @pytest.mark.parametrize("name", ["powerlaw-1.2M", "uniform-10k"])

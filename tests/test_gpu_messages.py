@@ -346,7 +346,9 @@ def test_edge_dot(adtype, bdtype, F):
     bd = dev(b32) if bdtype == torch.float32 else bf16_dev(bk["b_bf16"])
     for bi, oi in ((bidx, oidx), (bidx, None)):
         out = mp.edge_dot(ad, bd, bidx=dev(bi), oidx=None if oi is None else dev(oi))
+        again = mp.edge_dot(ad, bd, bidx=dev(bi), oidx=None if oi is None else dev(oi))
         torch.cuda.synchronize()
+        assert torch.equal(out, again)  # a fixed reduction order
         ref, sc = oracle.edge_dot(bidx=bi, oidx=oi, **ak, **bk)
         e = scaled_error(out.cpu().numpy(), ref, sc)
         assert e <= 1e-5, e
