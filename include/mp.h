@@ -50,7 +50,7 @@
 extern "C" {
 #endif
 
-#define MP_VERSION 3
+#define MP_VERSION 4
 
 /* Status codes. */
 typedef enum mp_status {
@@ -504,6 +504,11 @@ int mp_edge_dot(const void* a, int a_dtype, const void* b, int b_dtype, const in
  * ------------------------------------------------------------------------- */
 
 #define MP_MAX_TYPES 16
+/* dst_type value selecting every destination type at once: one CSR whose
+ * rows are all nodes as global ids (type t's rows are offs[t] .. offs[t+1]-1,
+ * offs the prefix sums of N_per_type), built and aggregated in one pass each;
+ * the rows of each type are exactly those of that type's own CSR. */
+#define MP_ALL_TYPES (-1)
 
 /* One relation: edges src_type -> dst_type with local int32 endpoints. */
 typedef struct mp_relation {
@@ -514,8 +519,8 @@ typedef struct mp_relation {
     int64_t E;
 } mp_relation;
 
-/* Workspace bytes for mp_hetero_build of destination type dst_type.
- * N_per_type and rels are host arrays. */
+/* Workspace bytes for mp_hetero_build of destination type dst_type (or
+ * MP_ALL_TYPES).  N_per_type and rels are host arrays. */
 int mp_hetero_build_workspace(int n_types, const int64_t* N_per_type, int n_rel,
                               const mp_relation* rels, int dst_type, int rowptr_itype,
                               size_t* bytes);
@@ -523,6 +528,8 @@ int mp_hetero_build_workspace(int n_types, const int64_t* N_per_type, int n_rel,
 /* Build the combined CSR of destination type dst_type:
  *   rowptr [N_per_type[dst_type]+1] of rowptr_itype, col [E_T] int32 global
  *   source ids, where E_T = sum of E over relations ending at dst_type.
+ * With dst_type = MP_ALL_TYPES: rowptr [N_total+1] over all nodes (global
+ * ids), col [sum of all E].
  * n_types <= MP_MAX_TYPES; the total node count must fit int32. */
 int mp_hetero_build(int n_types, const int64_t* N_per_type, int n_rel,
                     const mp_relation* rels, int dst_type, void* rowptr, int rowptr_itype,
@@ -533,7 +540,8 @@ int mp_hetero_build(int n_types, const int64_t* N_per_type, int n_rel,
  *   x_per_type  host array of n_types device pointers, each [N_t, F] x_dtype.
  *   plan        from mp_spmm_plan_build on this rowptr (or NULL).
  *   reduce      MP_SUM only (the cross-relation aggregator is a sum).
- *   out         [N_per_type[dst_type], F] of out_dtype. */
+ *   out         [N_per_type[dst_type], F] of out_dtype; with MP_ALL_TYPES
+ *               [N_total, F] (every type's rows, in type order). */
 int mp_hetero_spmm(int n_types, const int64_t* N_per_type, const void* const* x_per_type,
                    int x_dtype, int64_t F, int dst_type, const mp_plan* plan,
                    const void* rowptr, int rowptr_itype, const int32_t* col, int reduce,

@@ -37,7 +37,8 @@ __all__ = [
     "mp_message_scale", "mp_message_aggregate", "mp_spmm_materialized",
     "mp_message_backward_workspace", "mp_message_backward", "mp_edge_dot", "csr_rows",
     "message_gather", "message_scale", "message_aggregate", "spmm_materialized",
-    "message_backward", "edge_dot", "mp_copy_rows", "aligned_ld", "pad_rows",
+    "message_backward", "edge_dot", "mp_copy_rows", "aligned_ld", "pad_rows", "MP_MAX_TYPES",
+    "MP_ALL_TYPES",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -52,6 +53,7 @@ MP_MIN, MP_VAR, MP_STD = 8, 16, 32
 AGGR = {"sum": MP_SUM, "mean": MP_MEAN, "max": MP_MAX, "min": MP_MIN, "var": MP_VAR,
         "std": MP_STD}
 MP_MAX_TYPES = 16
+MP_ALL_TYPES = -1  # dst_type selecting every destination type at once
 MP_ERR_CALLBACK = -9
 
 # int c(void* msg, int msg_dtype, int64_t E, int64_t F, void* user, void* stream)
@@ -706,14 +708,17 @@ def segment_matmul_backward(seg, x, W, dout, *, dx_dtype=torch.float32, want_dx=
 
 
 def hetero_build(N_per_type, rels, dst_type, *, rowptr_dtype=torch.int32, stream=None):
-    """Combined destination-major CSR of one destination type.
+    """Combined destination-major CSR of one destination type, or of all of
+    them (dst_type = MP_ALL_TYPES: rows are all nodes as global ids).
 
     rels: list of (src_type, dst_type, src int32 tensor, dst int32 tensor).
     Returns (rowptr, col with global source ids)."""
     it = _itype_code(rowptr_dtype)
     dev = next(r[2].device for r in rels)
-    E_T = sum(int(r[2].numel()) for r in rels if r[1] == dst_type)
-    rowptr = torch.empty(N_per_type[dst_type] + 1, dtype=rowptr_dtype, device=dev)
+    everything = dst_type == MP_ALL_TYPES
+    E_T = sum(int(r[2].numel()) for r in rels if everything or r[1] == dst_type)
+    n_rows = sum(N_per_type) if everything else N_per_type[dst_type]
+    rowptr = torch.empty(n_rows + 1, dtype=rowptr_dtype, device=dev)
     col = _edge_array(E_T, torch.int32, dev)
     nb = mp_hetero_build_workspace(N_per_type, rels, dst_type, it)
     ws = _workspace(nb, dev)
@@ -723,11 +728,13 @@ def hetero_build(N_per_type, rels, dst_type, *, rowptr_dtype=torch.int32, stream
 
 def hetero_spmm(N_per_type, x_per_type, dst_type, rowptr, col, *, plan: Plan | None = None,
                 out_dtype=torch.float32, out=None, stream=None):
-    """Sum over the combined CSR of dst_type, gathering from per-type tables."""
+    """Sum over the combined CSR of dst_type (or of all types), gathering
+    from per-type tables."""
     F = int(x_per_type[0].shape[1])
     dev = x_per_type[0].device
     if out is None:
-        out = torch.empty(N_per_type[dst_type], F, dtype=out_dtype, device=dev)
+        n_rows = sum(N_per_type) if dst_type == MP_ALL_TYPES else N_per_type[dst_type]
+        out = torch.empty(n_rows, F, dtype=out_dtype, device=dev)
     ws = plan.workspace(MP_SUM) if plan is not None else None
     mp_hetero_spmm(N_per_type, x_per_type, _dtype_code(x_per_type[0].dtype), F, dst_type,
                    plan.handle if plan is not None else None, rowptr, _itype_code(rowptr.dtype),

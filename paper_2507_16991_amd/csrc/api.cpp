@@ -1145,9 +1145,11 @@ int mp_segment_matmul_backward(const int64_t* seg, int T, const void* x, const v
 // ---- heterogeneous ----------------------------------------------------------
 
 static int hetero_check(int n_types, const int64_t* N_per_type, int n_rel, const mp_relation* rels,
-                        int dst_type, int64_t* E_T, int64_t* offs) {
+                        int dst_type, int64_t* E_T, int64_t* offs, int64_t* N_rows) {
     if (!N_per_type || (n_rel > 0 && !rels)) return MP_ERR_NULL;
-    if (n_types < 1 || n_types > MP_MAX_TYPES || n_rel < 0 || dst_type < 0 || dst_type >= n_types)
+    const bool all = dst_type == MP_ALL_TYPES;
+    if (n_types < 1 || n_types > MP_MAX_TYPES || n_rel < 0 ||
+        (!all && (dst_type < 0 || dst_type >= n_types)))
         return MP_ERR_SIZE;
     int64_t tot = 0;
     for (int t = 0; t < n_types; ++t) {
@@ -1163,14 +1165,16 @@ static int hetero_check(int n_types, const int64_t* N_per_type, int n_rel, const
         if (R.src_type < 0 || R.src_type >= n_types || R.dst_type < 0 || R.dst_type >= n_types ||
             R.E < 0)
             return MP_ERR_SIZE;
-        if (R.dst_type == dst_type) {
+        if (all || R.dst_type == dst_type) {
             if (R.E > 0 && (!R.src || !R.dst)) return MP_ERR_NULL;
             e += R.E;
         }
     }
     if (e > INT32_MAX) return MP_ERR_SIZE;
-    if (N_per_type[dst_type] < 1) return MP_ERR_SIZE;
+    const int64_t rows = all ? tot : N_per_type[dst_type];
+    if (rows < 1) return MP_ERR_SIZE;
     *E_T = e;
+    *N_rows = rows;
     return MP_OK;
 }
 
@@ -1179,11 +1183,11 @@ int mp_hetero_build_workspace(int n_types, const int64_t* N_per_type, int n_rel,
                               size_t* bytes) {
     if (!bytes) return MP_ERR_NULL;
     if (!valid_itype(rowptr_itype)) return MP_ERR_DTYPE;
-    int64_t E_T = 0, offs[MP_MAX_TYPES + 1];
-    int st = hetero_check(n_types, N_per_type, n_rel, rels, dst_type, &E_T, offs);
+    int64_t E_T = 0, N_rows = 0, offs[MP_MAX_TYPES + 1];
+    int st = hetero_check(n_types, N_per_type, n_rel, rels, dst_type, &E_T, offs, &N_rows);
     if (st != MP_OK) return st;
     size_t cw = 0;
-    st = mp_coo_to_csr_workspace(E_T, N_per_type[dst_type], rowptr_itype, 0, &cw);
+    st = mp_coo_to_csr_workspace(E_T, N_rows, rowptr_itype, 0, &cw);
     if (st != MP_OK) return st;
     *bytes = 2 * align_up((size_t)(E_T > 0 ? E_T : 1) * 4, 256) + cw;
     return MP_OK;
@@ -1193,8 +1197,8 @@ int mp_hetero_build(int n_types, const int64_t* N_per_type, int n_rel, const mp_
                     int dst_type, void* rowptr, int rowptr_itype, int32_t* col, void* ws,
                     size_t ws_bytes, void* stream) {
     if (!valid_itype(rowptr_itype)) return MP_ERR_DTYPE;
-    int64_t E_T = 0, offs[MP_MAX_TYPES + 1];
-    int st = hetero_check(n_types, N_per_type, n_rel, rels, dst_type, &E_T, offs);
+    int64_t E_T = 0, N_rows = 0, offs[MP_MAX_TYPES + 1];
+    int st = hetero_check(n_types, N_per_type, n_rel, rels, dst_type, &E_T, offs, &N_rows);
     if (st != MP_OK) return st;
     if (!rowptr || (E_T > 0 && (!col || !ws))) return MP_ERR_NULL;
     size_t need = 0;
@@ -1207,16 +1211,19 @@ int mp_hetero_build(int n_types, const int64_t* N_per_type, int n_rel, const mp_
     int32_t* src_g = c.take<int32_t>(e);
     int32_t* dst_c = c.take<int32_t>(e);
     int64_t off = 0;
+    const bool all = dst_type == MP_ALL_TYPES;
     for (int r = 0; r < n_rel; ++r) {
         const mp_relation& R = rels[r];
-        if (R.dst_type != dst_type || R.E == 0) continue;
+        if ((!all && R.dst_type != dst_type) || R.E == 0) continue;
+        // sources (and, over all types, destinations) as global node ids
         hipError_t he = launch_offset_copy(R.src, R.E, (int32_t)offs[R.src_type], src_g + off, s);
-        if (he == hipSuccess) he = launch_offset_copy(R.dst, R.E, 0, dst_c + off, s);
+        if (he == hipSuccess)
+            he = launch_offset_copy(R.dst, R.E, all ? (int32_t)offs[R.dst_type] : 0, dst_c + off, s);
         if (he != hipSuccess) return MP_ERR_HIP;
         off += R.E;
     }
-    return coo_to_csr_impl(src_g, dst_c, E_T, N_per_type[dst_type], rowptr, rowptr_itype, col,
-                           nullptr, nullptr, nullptr, c.base + c.off, ws_bytes - c.off, s);
+    return coo_to_csr_impl(src_g, dst_c, E_T, N_rows, rowptr, rowptr_itype, col, nullptr,
+                           nullptr, nullptr, c.base + c.off, ws_bytes - c.off, s);
 }
 
 int mp_hetero_spmm(int n_types, const int64_t* N_per_type, const void* const* x_per_type,
@@ -1226,12 +1233,11 @@ int mp_hetero_spmm(int n_types, const int64_t* N_per_type, const void* const* x_
     if (reduce != MP_SUM) return MP_ERR_REDUCE;
     if (!valid_itype(rowptr_itype) || !valid_dtype(x_dtype) || !valid_dtype(out_dtype))
         return MP_ERR_DTYPE;
-    int64_t E_T = 0, offs[MP_MAX_TYPES + 1];
-    int st = hetero_check(n_types, N_per_type, 0, nullptr, dst_type, &E_T, offs);
+    int64_t E_T = 0, N_dst = 0, offs[MP_MAX_TYPES + 1];
+    int st = hetero_check(n_types, N_per_type, 0, nullptr, dst_type, &E_T, offs, &N_dst);
     if (st != MP_OK) return st;
     if (F < 1 || F > 65536) return MP_ERR_SIZE;
     if (!x_per_type || !rowptr || !out || !col) return MP_ERR_NULL;
-    const int64_t N_dst = N_per_type[dst_type];
     st = check_plan(plan, rowptr, rowptr_itype, N_dst, F);
     if (st != MP_OK) return st;
     const int eb = x_dtype == MP_BF16 ? 2 : 4;

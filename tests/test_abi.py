@@ -30,7 +30,7 @@ def test_exports_every_declared_function():
 
 
 def test_version_and_status_strings():
-    assert mp.mp_version() == 3
+    assert mp.mp_version() == 4
     for st in range(-9, 1):
         assert mp.mp_status_str(st) != "unknown status"
     assert mp.mp_status_str(-99) == "unknown status"
@@ -144,6 +144,10 @@ def test_hetero_errors():
     rel = (mp.mp_relation * 1)(mp.mp_relation(0, 1, FAKE, FAKE, 20))
     assert L.mp_hetero_build_workspace(2, npt, 1, rel, 1, 0, ctypes.byref(b)) == 0 and b.value > 0
     assert L.mp_hetero_build_workspace(2, npt, 1, rel, 2, 0, ctypes.byref(b)) == -2
+    assert L.mp_hetero_build_workspace(2, npt, 1, rel, -2, 0, ctypes.byref(b)) == -2
+    # every destination type at once: rows are all 15 nodes
+    assert L.mp_hetero_build_workspace(2, npt, 1, rel, mp.MP_ALL_TYPES, 0,
+                                       ctypes.byref(b)) == 0 and b.value > 0
     assert L.mp_hetero_build_workspace(0, npt, 1, rel, 0, 0, ctypes.byref(b)) == -2
     bad = (mp.mp_relation * 1)(mp.mp_relation(0, 3, FAKE, FAKE, 20))
     assert L.mp_hetero_build_workspace(2, npt, 1, bad, 1, 0, ctypes.byref(b)) == -2

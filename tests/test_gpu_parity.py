@@ -467,6 +467,7 @@ def run_hetero(g, plan_on=True, one_buffer=False):
         xs = [dev(x.view(np.int16)).view(torch.bfloat16) for x in g.x_bf16]
     outs_o, scs_o = oracle.hetero_sum(g.n_per_type, g.x_bf16, g.rel_src_type, g.rel_dst_type,
                                       g.rel_src, g.rel_dst)
+    per_type = {}
     for t in range(T):
         if t not in g.rel_dst_type:
             continue
@@ -475,9 +476,28 @@ def run_hetero(g, plan_on=True, one_buffer=False):
         plan = mp.Plan(rp, E_T, g.F, torch.bfloat16) if plan_on else None
         out = mp.hetero_spmm(g.n_per_type, xs, t, rp, col, plan=plan)
         torch.cuda.synchronize()
+        per_type[t] = (rp.cpu().numpy().astype(np.int64), col.cpu().numpy())
         err = scaled_error(out.cpu().numpy(), outs_o[t], scs_o[t])
         assert err <= TOL[torch.bfloat16], f"type {t}: error {err}"
         assert err <= 1e-5, f"type {t}: fp32 accumulation error {err}"
+    # every destination type at once: one CSR over all nodes (global ids)
+    # whose row slices are exactly the per-type CSRs, and one aggregation
+    rp, col = mp.hetero_build(g.n_per_type, rels, mp.MP_ALL_TYPES)
+    plan = mp.Plan(rp, int(col.numel()), g.F, torch.bfloat16) if plan_on else None
+    out = mp.hetero_spmm(g.n_per_type, xs, mp.MP_ALL_TYPES, rp, col, plan=plan)
+    torch.cuda.synchronize()
+    rp_h, col_h, out_h = rp.cpu().numpy().astype(np.int64), col.cpu().numpy(), out.cpu().numpy()
+    offs = np.concatenate([[0], np.cumsum(g.n_per_type)])
+    for t in range(T):
+        a, b = offs[t], offs[t + 1]
+        if t in per_type:
+            rp_t, col_t = per_type[t]
+            assert np.array_equal(rp_h[a:b + 1] - rp_h[a], rp_t), f"type {t}: rowptr slice"
+            assert np.array_equal(col_h[rp_h[a]:rp_h[b]], col_t), f"type {t}: col slice"
+            err = scaled_error(out_h[a:b], outs_o[t], scs_o[t])
+            assert err <= 1e-5, f"all types, type {t}: error {err}"
+        else:
+            assert rp_h[b] == rp_h[a] and not out_h[a:b].any(), f"type {t}: no incoming edges"
 
 
 def test_hetero_small():
