@@ -3,7 +3,8 @@
 // builds once as a source-major CSR, the analogue of the cached CSC).
 //
 //   * rows_of_edges: the destination row of every forward CSR position (the
-//     keys the transposed CSR is sorted by carry it as payload).
+//     keys the transposed CSR is sorted by carry it as payload), one
+//     wavefront per row.
 //   * scale_inv_deg: grad_out / in-degree per destination row, the input of
 //     the gradient of mean.
 //   * spmm_grad_w: the gradient with respect to the edge weights, one dot
@@ -31,7 +32,6 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int kWavesPerBlock = kBlock / kWave;
-constexpr int kRowItems = 8;  // CSR positions per thread in rows_of_edges
 #ifndef MP_GW_UNROLL
 #define MP_GW_UNROLL 4  // edges per slot per step of the weight gradient (sum, mean)
 #endif
@@ -40,31 +40,23 @@ __device__ inline int64_t rp_at(const void* rp, int rp64, int64_t i) {
     return rp64 ? static_cast<const int64_t*>(rp)[i] : (int64_t) static_cast<const int32_t*>(rp)[i];
 }
 
-// row[p] = the v with rowptr[v] <= p < rowptr[v+1].  One binary search per
-// thread for its first position, then a forward walk over its 8 positions.
-__global__ __launch_bounds__(kBlock) void rows_of_edges(const void* __restrict__ rowptr, int rp64,
-                                                        int64_t N, int64_t E,
-                                                        int32_t* __restrict__ row) {
-    const int64_t p0 = ((int64_t)blockIdx.x * kBlock + threadIdx.x) * kRowItems;
-    if (p0 >= E) return;
-    // largest v in [0, N) with rowptr[v] <= p0
-    int64_t lo = 0, hi = N - 1;
-    while (lo < hi) {
-        const int64_t mid = (lo + hi + 1) >> 1;
-        if (rp_at(rowptr, rp64, mid) <= p0) lo = mid; else hi = mid - 1;
-    }
-    int64_t v = lo;
-    int64_t next = rp_at(rowptr, rp64, v + 1);
-#pragma unroll
-    for (int k = 0; k < kRowItems; ++k) {
-        const int64_t p = p0 + k;
-        if (p >= E) break;
-        while (next <= p && v + 1 < N) {  // skip rows ending at or before p (and empty rows)
-            ++v;
-            next = rp_at(rowptr, rp64, v + 1);
-        }
-        row[p] = (int32_t)v;
-    }
+// row[p] = the v with rowptr[v] <= p < rowptr[v+1].  One wavefront per row
+// writes the row id over the row's positions (64 consecutive positions per
+// store instruction, no search).  Positions outside [rowptr[0], rowptr[N])
+// of an inconsistent rowptr go to the first or last row, so every entry is
+// a valid row id whatever the input.
+template <typename IT>
+__global__ __launch_bounds__(kBlock) void rows_of_edges(const IT* __restrict__ rowptr, int64_t N,
+                                                        int64_t E, int32_t* __restrict__ row) {
+    const int lane = threadIdx.x & (kWave - 1);
+    const int64_t v = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave)) +
+                      (int64_t)blockIdx.x * kWavesPerBlock;
+    if (v >= N) return;
+    int64_t beg = v == 0 ? 0 : (int64_t)rowptr[v];
+    int64_t end = v == N - 1 ? E : (int64_t)rowptr[v + 1];
+    if (beg < 0) beg = 0;
+    if (end > E) end = E;
+    for (int64_t p = beg + lane; p < end; p += kWave) row[p] = (int32_t)v;
 }
 
 __device__ inline float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
@@ -408,10 +400,14 @@ hipError_t launch_gw_epl(const GradWParams& p, int epl, unsigned grid, hipStream
 
 hipError_t launch_rows_of_edges(const void* rowptr, int rp64, int64_t N, int64_t E, int32_t* row,
                                 hipStream_t s) {
-    if (E <= 0) return hipSuccess;
-    const int64_t threads = ceil_div(E, kRowItems);
-    hipLaunchKernelGGL(rows_of_edges, dim3((unsigned)ceil_div(threads, kBlock)), dim3(kBlock), 0,
-                       s, rowptr, rp64, N, E, row);
+    if (E <= 0 || N <= 0) return hipSuccess;
+    const unsigned grid = (unsigned)ceil_div(N, kWavesPerBlock);
+    if (rp64)
+        hipLaunchKernelGGL(rows_of_edges<int64_t>, dim3(grid), dim3(kBlock), 0, s,
+                           static_cast<const int64_t*>(rowptr), N, E, row);
+    else
+        hipLaunchKernelGGL(rows_of_edges<int32_t>, dim3(grid), dim3(kBlock), 0, s,
+                           static_cast<const int32_t*>(rowptr), N, E, row);
     return hipGetLastError();
 }
 
