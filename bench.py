@@ -53,6 +53,7 @@ DOMINANT_SRC = [("paper_2507_16991_amd/csrc/spmm.hip", None, None),
                  "// ---- backward (backward.hip)")]
 COUNTER_SUMMARY = os.path.join(ROOT, "profiles", "spmm_main_f32_sum_chunglu124M_counters.txt")
 CALIB_BYTES = 1 << 30  # plain copy used to scale the HBM counters
+SORT_STATUS = []  # device status words of the sorts a step runs
 
 
 # ---- algorithmic bytes ------------------------------------------------------------
@@ -280,10 +281,13 @@ def build_step(args, mp, torch, np, dev):
     plans = {}
     wss = {}
 
+    sort_status = mp.new_status(dev)  # checked once after the timed steps
+    SORT_STATUS.append(sort_status)
+
     def step(evs=None):
         mark(evs, 0)
         mp.mp_coo_to_csr(src, dst, E, N, rowptr, it, col, perm, w_coo, w_csr, ws_csr,
-                         ws_csr.numel())
+                         ws_csr.numel(), sort_status)
         mark(evs, 1)
         # one plan per CSR, shared by both feature dtypes
         k0 = next(iter(xs))
@@ -347,10 +351,13 @@ def backward_step(g, mp, torch, np, dev, mark):
     ops.append(("grad_w_sum_f32", grad_w_bytes(N, E, F), E * F))
     plans, wss = {}, {}
 
+    sort_status = mp.new_status(dev)  # checked once after the timed steps
+    SORT_STATUS.append(sort_status)
+
     def step(evs=None):
         mark(evs, 0)
         mp.mp_csr_transpose(rowptr, it, col, N, N, E, rowptrT, it, colT, posT, None, None, ws_t,
-                            ws_t.numel())
+                            ws_t.numel(), sort_status)
         mark(evs, 1)
         if "h" in plans:
             mp.mp_spmm_plan_free(plans["h"])
@@ -476,10 +483,13 @@ def stacked_step(g, mp, torch, np, dev, mark):
         tables.append((k, x, xd, ld, xp))
     plans, wss = {}, {}
 
+    sort_status = mp.new_status(dev)  # checked once after the timed steps
+    SORT_STATUS.append(sort_status)
+
     def step(evs=None):
         mark(evs, 0)
         mp.mp_coo_to_csr(src, dst, E, N, rowptr, it, col, None, None, None, ws_csr,
-                         ws_csr.numel())
+                         ws_csr.numel(), sort_status)
         mark(evs, 1)
         if "h" in plans:
             mp.mp_spmm_plan_free(plans["h"])
@@ -671,6 +681,8 @@ def run(args):
     torch.cuda.synchronize()
     wall = time.perf_counter() - t_start
     ms_step = wall * 1e3 / args.steps
+    for st in SORT_STATUS:  # every sort of the timed steps completed
+        mp.check_status(st, "device sort of a timed step")
 
     op_ms = {n: float(np.mean([evs[i].elapsed_time(evs[i + 1]) for evs in all_evs]))
              for i, n in enumerate(names)}

@@ -31,6 +31,10 @@
  *  - Errors.  Calls return MP_OK (0) or a negative mp_status.  Argument
  *    errors are detected on the host before anything is enqueued, and leave
  *    every output untouched.  MP_ERR_HIP reports a failed launch or copy.
+ *    Calls that sort on the device (mp_coo_to_csr, mp_csr_transpose,
+ *    mp_hetero_build) report device-side failure asynchronously through an
+ *    optional device status word (see mp_coo_to_csr); mp_spmm_plan_build,
+ *    which synchronizes anyway, returns it.
  *  - Index validity.  Edge indices must satisfy 0 <= src < N_src and
  *    0 <= dst < N_dst, and a rowptr must be non-decreasing with rowptr[0] = 0
  *    and rowptr[N_dst] = E.  Violations are not detected by the compute calls
@@ -50,7 +54,7 @@
 extern "C" {
 #endif
 
-#define MP_VERSION 4
+#define MP_VERSION 5
 
 /* Status codes. */
 typedef enum mp_status {
@@ -63,7 +67,9 @@ typedef enum mp_status {
     MP_ERR_PLAN = -6,      /* plan does not match the arguments */
     MP_ERR_HIP = -7,       /* a HIP launch, copy or query failed */
     MP_ERR_ALIGN = -8,     /* a pointer is not aligned to its element size */
-    MP_ERR_CALLBACK = -9   /* a message callback returned nonzero */
+    MP_ERR_CALLBACK = -9,  /* a message callback returned nonzero */
+    MP_ERR_SORT = -10      /* a device sort gave up waiting for an earlier tile;
+                              the CSR it was building is invalid */
 } mp_status;
 
 /* Feature / output element types. */
@@ -113,11 +119,19 @@ int mp_coo_to_csr_workspace(int64_t E, int64_t N, int rowptr_itype, int with_pay
  * Within a row, edges keep ascending COO id (stable), so the result is
  * unique and bit-exact.  Duplicates and self-loops are ordinary edges.
  * E = 0 is valid (rowptr all zero).  ws/ws_bytes: workspace from
- * mp_coo_to_csr_workspace.  Asynchronous on `stream`. */
+ * mp_coo_to_csr_workspace.
+ *   status      [1] int32 (device) or NULL: written on `stream` after the
+ *               sort, MP_OK if it completed, MP_ERR_SORT if a tile of the
+ *               sort gave up its bounded wait for an earlier tile's counts
+ *               (then rowptr, col, perm and val_out are invalid).  The wait
+ *               only spans tiles that are already running, so this is a
+ *               guard against a hung device, not an expected outcome; read
+ *               the word once the stream's work is done.
+ * Asynchronous on `stream`. */
 int mp_coo_to_csr(const int32_t* src, const int32_t* dst, int64_t E, int64_t N,
                   void* rowptr, int rowptr_itype, int32_t* col, int32_t* perm,
                   const float* val_in, float* val_out, void* ws, size_t ws_bytes,
-                  void* stream);
+                  int32_t* status, void* stream);
 
 /* COO edges already sorted by destination (the sort-order metadata the
  * paper's EdgeIndex carries, Sec. 2.2): the CSR is the COO itself, so rowptr
@@ -130,9 +144,9 @@ int mp_sorted_coo_to_csr(const int32_t* src, const int32_t* dst, int64_t E, int6
                          const float* val_in, float* val_out, void* stream);
 
 /* ---------------------------------------------------------------------------
- * Aggregation plan: rows binned by in-degree (Sec. 2.2: the sorted layout
- * "enables greater parallelism"; the plan is built once per CSR and reused,
- * like the CSR cache).
+ * Aggregation plan: rows binned by in-degree (Sec. 2.2: a destination-sorted
+ * layout lets the aggregation run in parallel over rows; the plan is built
+ * once per CSR and reused, like the CSR cache).
  * ------------------------------------------------------------------------- */
 
 typedef struct mp_plan mp_plan;
@@ -149,11 +163,37 @@ int mp_spmm_plan_size(int64_t N_dst, int64_t E, size_t* bytes);
  *   *out        (host) receives a host-side handle; free with
  *               mp_spmm_plan_free.
  * This call SYNCHRONIZES `stream` once: it copies the per-bin row counts to
- * the host to size later launches.  The plan stays valid while rowptr and
- * plan_buf are unchanged. */
+ * the host to size later launches (and returns MP_ERR_SORT, with *out
+ * untouched, if the device sort of the rows by class gave up its bounded
+ * wait).  The plan stays valid while rowptr and plan_buf are unchanged. */
 int mp_spmm_plan_build(const void* rowptr, int rowptr_itype, int64_t N_dst, int64_t E,
                        int64_t F, int x_dtype, void* plan_buf, size_t plan_bytes,
                        void* stream, mp_plan** out);
+
+/* Explicit degree-class thresholds for mp_spmm_plan_build_opts (0 = the
+ * default of that field).  They decide which kernel and which schedule
+ * aggregate a row, and so the fp32 summation order of its sums (results stay
+ * within rounding of each other; integer outputs, max and argmax do not
+ * change).
+ *   small_max   rows of at most this many edges get one slot of a wavefront
+ *               each (at most 16383);
+ *   hub_min     rows of more than this many edges (raised to small_max if
+ *               lower) are cut into edge chunks aggregated by separate
+ *               wavefronts and combined in chunk order;
+ *   chunk_min   the fewest edges of such a chunk (at most 2048 chunks per
+ *               row). */
+typedef struct mp_plan_opts {
+    int64_t small_max;
+    int64_t hub_min;
+    int64_t chunk_min;
+} mp_plan_opts;
+
+/* mp_spmm_plan_build with explicit thresholds (opts NULL: the defaults, i.e.
+ * exactly mp_spmm_plan_build).  Negative fields or chunk_min > INT32_MAX give
+ * MP_ERR_SIZE. */
+int mp_spmm_plan_build_opts(const void* rowptr, int rowptr_itype, int64_t N_dst, int64_t E,
+                            int64_t F, int x_dtype, void* plan_buf, size_t plan_bytes,
+                            const mp_plan_opts* opts, void* stream, mp_plan** out);
 
 /* Release a host handle (NULL is ignored).  Does not touch plan_buf. */
 void mp_spmm_plan_free(mp_plan* plan);
@@ -184,7 +224,10 @@ int mp_spmm_workspace(const mp_plan* plan, int reduce, size_t* bytes);
  *               position p of the first edge attaining the maximum.
  * Output rows are written in full (nothing is accumulated into them).  An
  * empty row gives 0 for sum, mean and max, and -1 in argout.  Messages are
- * compared with '>' so that -0.0 and +0.0 tie and the earlier edge wins.
+ * compared with '>' so that -0.0 and +0.0 tie and the earlier edge wins;
+ * infinities are ordinary values (a row whose messages are all -inf has max
+ * -inf at its first edge).  Messages must not be NaN: outputs are then
+ * unspecified (but every write stays in bounds).
  * A weighted message for MAX is the fp32 product fl32(w * x); sums may fuse
  * the multiply into the add.  Size limits: 0 <= N_src, N_dst <= INT32_MAX,
  * 1 <= F <= 65536, ldx >= F, E <= INT32_MAX (argout and col are int32).
@@ -278,13 +321,15 @@ int mp_csr_transpose_workspace(int64_t E, int64_t N_src, int rowptrT_itype, int 
  *   posT        [E] int32 or NULL: out, the forward CSR position of each edge.
  *   val_in      [E] fp32 in forward CSR order, or NULL; val_out [E] receives
  *               val_in[posT[t]] (both or neither).
+ *   status      [1] int32 (device) or NULL: MP_OK or MP_ERR_SORT, as in
+ *               mp_coo_to_csr.
  * Within a source, edges keep their forward CSR order (a stable sort by col),
  * so the result is unique and bit-exact.  Sizes: 1 <= N_dst, N_src <=
  * INT32_MAX, 0 <= E <= INT32_MAX.  Asynchronous on `stream`. */
 int mp_csr_transpose(const void* rowptr, int rowptr_itype, const int32_t* col, int64_t N_dst,
                      int64_t N_src, int64_t E, void* rowptrT, int rowptrT_itype, int32_t* colT,
                      int32_t* posT, const float* val_in, float* val_out, void* ws,
-                     size_t ws_bytes, void* stream);
+                     size_t ws_bytes, int32_t* status, void* stream);
 
 /* Workspace bytes for mp_spmm_backward_x: hub partials of planT; for MP_MEAN
  * also an fp32 copy of G divided by the in-degrees (N_dst * F * 4 bytes); for
@@ -530,10 +575,12 @@ int mp_hetero_build_workspace(int n_types, const int64_t* N_per_type, int n_rel,
  *   source ids, where E_T = sum of E over relations ending at dst_type.
  * With dst_type = MP_ALL_TYPES: rowptr [N_total+1] over all nodes (global
  * ids), col [sum of all E].
+ * status: [1] int32 (device) or NULL: MP_OK or MP_ERR_SORT, as in
+ * mp_coo_to_csr.
  * n_types <= MP_MAX_TYPES; the total node count must fit int32. */
 int mp_hetero_build(int n_types, const int64_t* N_per_type, int n_rel,
                     const mp_relation* rels, int dst_type, void* rowptr, int rowptr_itype,
-                    int32_t* col, void* ws, size_t ws_bytes, void* stream);
+                    int32_t* col, void* ws, size_t ws_bytes, int32_t* status, void* stream);
 
 /* Sum aggregation over a combined CSR from mp_hetero_build, gathering each
  * source row from its own type's feature table.

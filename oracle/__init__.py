@@ -85,6 +85,18 @@ def _L():
     return _lib
 
 
+def default_threads() -> int:
+    """Threads of the multithreaded oracle loops: OMP_NUM_THREADS when set,
+    else the CPUs this process may run on."""
+    n = int(os.environ.get("OMP_NUM_THREADS", "0") or 0)
+    if n > 0:
+        return n
+    try:
+        return len(os.sched_getaffinity(0)) or 1
+    except AttributeError:
+        return os.cpu_count() or 1
+
+
 def _p(a):
     return None if a is None else ctypes.c_void_p(a.ctypes.data)
 
@@ -140,7 +152,7 @@ def spmm(rowptr, col, x=None, x_bf16=None, w=None, rows=None, nthreads=None,
     am = np.empty((n, F), np.int64) if "max" in want else None
     sc = np.empty((n, F), np.float64) if "scale" in want else None
     if nthreads is None:
-        nthreads = os.cpu_count() or 1
+        nthreads = default_threads()
     rc = _L().oracle_spmm(n, _p(rows), n_dst, n_src, _p(rowptr), _p(col), _p(w), _p(xa), isb,
                           F, _p(s), _p(m), _p(mx), _p(am), _p(sc), int(nthreads))
     if rc != 0:
@@ -165,7 +177,7 @@ def spmm_multi(rowptr, col, x=None, x_bf16=None, w=None, rows=None, nthreads=Non
            "var": np.empty((n, F), np.float64), "std": np.empty((n, F), np.float64),
            "var_scale": np.empty((n, F), np.float64)}
     if nthreads is None:
-        nthreads = os.cpu_count() or 1
+        nthreads = default_threads()
     rc = _L().oracle_spmm_multi(n, _p(rows), n_dst, n_src, _p(rowptr), _p(col), _p(w), _p(xa),
                                 isb, F, _p(out["min"]), _p(out["argmin"]), _p(out["var"]),
                                 _p(out["std"]), _p(out["var_scale"]), int(nthreads))
@@ -319,7 +331,7 @@ def spmm_backward_w(rowptr, col, reduce, x=None, x_bf16=None, g=None, g_bf16=Non
     gw = np.full(E, np.nan, np.float64)
     sc = np.full(E, np.nan, np.float64)
     if nthreads is None:
-        nthreads = os.cpu_count() or 1
+        nthreads = default_threads()
     rc = _L().oracle_spmm_backward_w(n, _p(rows), n_dst, n_src, _p(rowptr), _p(col), _p(xa), xisb,
                                      _p(ga), gisb, F, REDUCE_CODES[reduce], _p(am), _p(gw),
                                      _p(sc), int(nthreads))

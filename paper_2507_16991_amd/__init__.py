@@ -38,12 +38,12 @@ __all__ = [
     "mp_message_backward_workspace", "mp_message_backward", "mp_edge_dot", "csr_rows",
     "message_gather", "message_scale", "message_aggregate", "spmm_materialized",
     "message_backward", "edge_dot", "mp_copy_rows", "aligned_ld", "pad_rows", "MP_MAX_TYPES",
-    "MP_ALL_TYPES",
+    "MP_ALL_TYPES", "MP_ERR_SORT", "mp_plan_opts", "mp_spmm_plan_build_opts", "new_status",
+    "check_status",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
-# MP_LIBRARY may point at another build of the same sources (tuning runs).
-LIB_PATH = os.environ.get("MP_LIBRARY") or os.path.join(_HERE, "libmp.so")
+LIB_PATH = os.path.join(_HERE, "libmp.so")
 
 MP_OK = 0
 MP_F32, MP_BF16 = 0, 1
@@ -55,6 +55,7 @@ AGGR = {"sum": MP_SUM, "mean": MP_MEAN, "max": MP_MAX, "min": MP_MIN, "var": MP_
 MP_MAX_TYPES = 16
 MP_ALL_TYPES = -1  # dst_type selecting every destination type at once
 MP_ERR_CALLBACK = -9
+MP_ERR_SORT = -10
 
 # int c(void* msg, int msg_dtype, int64_t E, int64_t F, void* user, void* stream)
 MESSAGE_FN = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.c_void_p, ctypes.c_int, ctypes.c_int64,
@@ -72,6 +73,11 @@ class MPError(RuntimeError):
 class mp_relation(ctypes.Structure):
     _fields_ = [("src_type", ctypes.c_int32), ("dst_type", ctypes.c_int32),
                 ("src", ctypes.c_void_p), ("dst", ctypes.c_void_p), ("E", ctypes.c_int64)]
+
+
+class mp_plan_opts(ctypes.Structure):
+    _fields_ = [("small_max", ctypes.c_int64), ("hub_min", ctypes.c_int64),
+                ("chunk_min", ctypes.c_int64)]
 
 
 class mp_aggr_out(ctypes.Structure):
@@ -92,11 +98,13 @@ def lib():
         L.mp_status_str.argtypes = [i32]
         L.mp_status_str.restype = ctypes.c_char_p
         L.mp_coo_to_csr_workspace.argtypes = [i64, i64, i32, i32, psz]
-        L.mp_coo_to_csr.argtypes = [p, p, i64, i64, p, i32, p, p, p, p, p, sz, p]
+        L.mp_coo_to_csr.argtypes = [p, p, i64, i64, p, i32, p, p, p, p, p, sz, p, p]
         L.mp_sorted_coo_to_csr.argtypes = [p, p, i64, i64, p, i32, p, p, p, p, p]
         L.mp_spmm_plan_size.argtypes = [i64, i64, psz]
         L.mp_spmm_plan_build.argtypes = [p, i32, i64, i64, i64, i32, p, sz, p,
                                          ctypes.POINTER(ctypes.c_void_p)]
+        L.mp_spmm_plan_build_opts.argtypes = [p, i32, i64, i64, i64, i32, p, sz, p, p,
+                                              ctypes.POINTER(ctypes.c_void_p)]
         L.mp_spmm_plan_free.argtypes = [p]
         L.mp_spmm_plan_free.restype = None
         L.mp_spmm_workspace.argtypes = [p, i32, psz]
@@ -104,7 +112,7 @@ def lib():
                               p, sz, p]
         L.mp_copy_rows.argtypes = [p, i64, p, i64, i64, i64, i32, p]
         L.mp_hetero_build_workspace.argtypes = [i32, p, i32, p, i32, i32, psz]
-        L.mp_hetero_build.argtypes = [i32, p, i32, p, i32, p, i32, p, p, sz, p]
+        L.mp_hetero_build.argtypes = [i32, p, i32, p, i32, p, i32, p, p, sz, p, p]
         L.mp_hetero_spmm.argtypes = [i32, p, p, i32, i64, i32, p, p, i32, p, i32, p, i32, p, sz,
                                      p]
         L.mp_validate_coo.argtypes = [p, p, i64, i64, i64, p, p]
@@ -119,7 +127,8 @@ def lib():
                                     p]
         L.mp_readout_multi.argtypes = [p, p, i32, p, i32, i64, i64, i64, i64, i32, p, p, sz, p]
         L.mp_csr_transpose_workspace.argtypes = [i64, i64, i32, i32, psz]
-        L.mp_csr_transpose.argtypes = [p, i32, p, i64, i64, i64, p, i32, p, p, p, p, p, sz, p]
+        L.mp_csr_transpose.argtypes = [p, i32, p, i64, i64, i64, p, i32, p, p, p, p, p, sz, p,
+                                       p]
         L.mp_spmm_backward_x_workspace.argtypes = [p, i64, i64, i64, i32, psz]
         L.mp_spmm_backward_x.argtypes = [p, p, i32, p, p, p, p, i32, p, p, i32, i64, i64, i64,
                                          i64, i32, p, i32, p, sz, p]
@@ -146,7 +155,8 @@ def lib():
                      "mp_segment_matmul_backward_workspace", "mp_segment_matmul_backward",
                      "mp_spmm_backward_x_workspace", "mp_spmm_backward_x",
                      "mp_spmm_backward_w_workspace", "mp_spmm_backward_w", "mp_spmm_plan_size",
-                     "mp_spmm_plan_build", "mp_spmm_workspace", "mp_spmm",
+                     "mp_spmm_plan_build", "mp_spmm_plan_build_opts", "mp_spmm_workspace",
+                     "mp_spmm",
                      "mp_hetero_build_workspace", "mp_hetero_build", "mp_hetero_spmm",
                      "mp_validate_coo", "mp_validate_csr"):
             getattr(L, name).restype = i32
@@ -238,10 +248,10 @@ def mp_coo_to_csr_workspace(E, N, rowptr_itype, with_payload) -> int:
 
 
 def mp_coo_to_csr(src, dst, E, N, rowptr, rowptr_itype, col, perm, val_in, val_out, ws,
-                  ws_bytes, stream=None):
+                  ws_bytes, status=None, stream=None):
     _check("mp_coo_to_csr", lib().mp_coo_to_csr(
         _ptr(src), _ptr(dst), E, N, _ptr(rowptr), rowptr_itype, _ptr(col), _ptr(perm),
-        _ptr(val_in), _ptr(val_out), _ptr(ws), ws_bytes, _stream(stream)))
+        _ptr(val_in), _ptr(val_out), _ptr(ws), ws_bytes, _ptr(status), _stream(stream)))
 
 
 def mp_sorted_coo_to_csr(src, dst, E, N, rowptr, rowptr_itype, col, perm, val_in, val_out,
@@ -260,6 +270,17 @@ def mp_spmm_plan_build(rowptr, rowptr_itype, N_dst, E, F, x_dtype, plan_buf, pla
     h = ctypes.c_void_p(0)
     _check("mp_spmm_plan_build", lib().mp_spmm_plan_build(
         _ptr(rowptr), rowptr_itype, N_dst, E, F, x_dtype, _ptr(plan_buf), plan_bytes,
+        _stream(stream), ctypes.byref(h)))
+    return h.value
+
+
+def mp_spmm_plan_build_opts(rowptr, rowptr_itype, N_dst, E, F, x_dtype, plan_buf, plan_bytes,
+                            opts=None, stream=None) -> int:
+    """opts: None, or (small_max, hub_min, chunk_min) with 0 for a default."""
+    h = ctypes.c_void_p(0)
+    o = ctypes.byref(mp_plan_opts(*[int(v) for v in opts])) if opts is not None else None
+    _check("mp_spmm_plan_build_opts", lib().mp_spmm_plan_build_opts(
+        _ptr(rowptr), rowptr_itype, N_dst, E, F, x_dtype, _ptr(plan_buf), plan_bytes, o,
         _stream(stream), ctypes.byref(h)))
     return h.value
 
@@ -303,11 +324,11 @@ def mp_hetero_build_workspace(N_per_type, rels, dst_type, rowptr_itype) -> int:
 
 
 def mp_hetero_build(N_per_type, rels, dst_type, rowptr, rowptr_itype, col, ws, ws_bytes,
-                    stream=None):
+                    status=None, stream=None):
     npt = (ctypes.c_int64 * len(N_per_type))(*N_per_type)
     _check("mp_hetero_build", lib().mp_hetero_build(
         len(N_per_type), npt, len(rels), _rel_array(rels), dst_type, _ptr(rowptr), rowptr_itype,
-        _ptr(col), _ptr(ws), ws_bytes, _stream(stream)))
+        _ptr(col), _ptr(ws), ws_bytes, _ptr(status), _stream(stream)))
 
 
 def mp_hetero_spmm(N_per_type, x_per_type, x_dtype, F, dst_type, plan_handle, rowptr,
@@ -330,10 +351,11 @@ def mp_csr_transpose_workspace(E, N_src, rowptrT_itype, with_payload) -> int:
 
 
 def mp_csr_transpose(rowptr, rowptr_itype, col, N_dst, N_src, E, rowptrT, rowptrT_itype, colT,
-                     posT, val_in, val_out, ws, ws_bytes, stream=None):
+                     posT, val_in, val_out, ws, ws_bytes, status=None, stream=None):
     _check("mp_csr_transpose", lib().mp_csr_transpose(
         _ptr(rowptr), rowptr_itype, _ptr(col), N_dst, N_src, E, _ptr(rowptrT), rowptrT_itype,
-        _ptr(colT), _ptr(posT), _ptr(val_in), _ptr(val_out), _ptr(ws), ws_bytes, _stream(stream)))
+        _ptr(colT), _ptr(posT), _ptr(val_in), _ptr(val_out), _ptr(ws), ws_bytes, _ptr(status),
+        _stream(stream)))
 
 
 def mp_spmm_backward_x_workspace(planT_handle, N_dst, E, F, reduce) -> int:
@@ -483,10 +505,36 @@ def mp_edge_dot(a, a_dtype, b, b_dtype, bidx, N_b, oidx, E, F, out, stream=None)
 
 # ---- convenience wrappers ---------------------------------------------------------
 
+def new_status(device) -> torch.Tensor:
+    """A device status word for the sorting calls (int32 [1])."""
+    return torch.empty(1, dtype=torch.int32, device=device)
+
+
+def check_status(status: torch.Tensor, fn: str = "device sort", stream=None) -> None:
+    """Wait for the stream and raise MPError if a sort reported failure."""
+    if hasattr(stream, "synchronize"):
+        stream.synchronize()
+    elif stream is None:
+        torch.cuda.current_stream(status.device).synchronize()
+    else:  # a raw stream handle
+        torch.cuda.synchronize(status.device)
+    _check(fn, int(status.item()))
+
+
+def _sort_status(status, check, device):
+    """(status tensor to pass, whether to check it after the call)."""
+    if status is not None:
+        return status, False
+    return (new_status(device), True) if check else (None, False)
+
+
 def coo_to_csr(src: torch.Tensor, dst: torch.Tensor, N: int, *, rowptr_dtype=torch.int32,
-               want_perm=False, val=None, stream=None, ws=None):
+               want_perm=False, val=None, stream=None, ws=None, status=None, check=True):
     """Stable destination-major CSR of the COO edges (src, dst int32 on GPU).
 
+    The sort's device status is written into `status` (an int32 [1] tensor)
+    when one is given; otherwise, with check=True, the call waits for the
+    stream and raises MPError(MP_ERR_SORT) if the sort failed.
     Returns (rowptr, col, perm or None, val_csr or None)."""
     E = int(src.numel())
     dev = src.device
@@ -498,7 +546,10 @@ def coo_to_csr(src: torch.Tensor, dst: torch.Tensor, N: int, *, rowptr_dtype=tor
     nb = mp_coo_to_csr_workspace(E, N, it, want_perm or val is not None)
     if ws is None or ws.numel() < nb:
         ws = _workspace(nb, dev)
-    mp_coo_to_csr(src, dst, E, N, rowptr, it, col, perm, val, vout, ws, ws.numel(), stream)
+    st, chk = _sort_status(status, check, dev)
+    mp_coo_to_csr(src, dst, E, N, rowptr, it, col, perm, val, vout, ws, ws.numel(), st, stream)
+    if chk:
+        check_status(st, "mp_coo_to_csr", stream)
     return rowptr, col, perm, vout
 
 
@@ -521,9 +572,12 @@ def sorted_coo_to_csr(src: torch.Tensor, dst: torch.Tensor, N: int, *, rowptr_dt
 class Plan:
     """Degree-binned aggregation plan for one CSR and one (F, dtype).
 
-    Building it synchronizes the stream once (bin sizes go to the host)."""
+    Building it synchronizes the stream once (bin sizes go to the host).
+    opts: None for the default thresholds, or (small_max, hub_min, chunk_min)
+    with 0 for a default (mp_plan_opts)."""
 
-    def __init__(self, rowptr: torch.Tensor, E: int, F: int, x_dtype=torch.float32, stream=None):
+    def __init__(self, rowptr: torch.Tensor, E: int, F: int, x_dtype=torch.float32, stream=None,
+                 opts=None):
         self.rowptr = rowptr
         self.itype = _itype_code(rowptr.dtype)
         self.N_dst = int(rowptr.numel()) - 1
@@ -531,8 +585,13 @@ class Plan:
         self.x_dtype = _dtype_code(x_dtype)
         nb = mp_spmm_plan_size(self.N_dst, self.E)
         self.buf = _workspace(nb, rowptr.device)
-        self.handle = mp_spmm_plan_build(rowptr, self.itype, self.N_dst, self.E, self.F,
-                                         self.x_dtype, self.buf, self.buf.numel(), stream)
+        if opts is None:
+            self.handle = mp_spmm_plan_build(rowptr, self.itype, self.N_dst, self.E, self.F,
+                                             self.x_dtype, self.buf, self.buf.numel(), stream)
+        else:
+            self.handle = mp_spmm_plan_build_opts(rowptr, self.itype, self.N_dst, self.E,
+                                                  self.F, self.x_dtype, self.buf,
+                                                  self.buf.numel(), opts, stream)
         self._ws = {}
 
     def workspace(self, reduce: int) -> torch.Tensor | None:
@@ -584,8 +643,9 @@ def spmm(rowptr, col, x, reduce, *, w=None, plan: Plan | None = None, out_dtype=
 
 
 def csr_transpose(rowptr, col, N_src, *, rowptrT_dtype=torch.int32, want_pos=True, val=None,
-                  stream=None):
-    """Source-major CSR of a destination-major CSR's edges.
+                  stream=None, status=None, check=True):
+    """Source-major CSR of a destination-major CSR's edges (status and check
+    as in coo_to_csr).
 
     Returns (rowptrT, colT = destinations, posT = forward CSR positions or
     None, val in transposed order or None)."""
@@ -599,8 +659,11 @@ def csr_transpose(rowptr, col, N_src, *, rowptrT_dtype=torch.int32, want_pos=Tru
     vout = _edge_array(E, torch.float32, dev) if val is not None else None
     nb = mp_csr_transpose_workspace(E, N_src, itT, want_pos or val is not None)
     ws = _workspace(nb, dev) if nb else None
+    st, chk = _sort_status(status, check, dev)
     mp_csr_transpose(rowptr, _itype_code(rowptr.dtype), col, N_dst, N_src, E, rowptrT, itT, colT,
-                     posT, val, vout, ws, 0 if ws is None else ws.numel(), stream)
+                     posT, val, vout, ws, 0 if ws is None else ws.numel(), st, stream)
+    if chk:
+        check_status(st, "mp_csr_transpose", stream)
     return rowptrT, colT, posT, vout
 
 
@@ -707,9 +770,11 @@ def segment_matmul_backward(seg, x, W, dout, *, dx_dtype=torch.float32, want_dx=
     return dx, dW
 
 
-def hetero_build(N_per_type, rels, dst_type, *, rowptr_dtype=torch.int32, stream=None):
+def hetero_build(N_per_type, rels, dst_type, *, rowptr_dtype=torch.int32, stream=None,
+                 status=None, check=True):
     """Combined destination-major CSR of one destination type, or of all of
-    them (dst_type = MP_ALL_TYPES: rows are all nodes as global ids).
+    them (dst_type = MP_ALL_TYPES: rows are all nodes as global ids); status
+    and check as in coo_to_csr.
 
     rels: list of (src_type, dst_type, src int32 tensor, dst int32 tensor).
     Returns (rowptr, col with global source ids)."""
@@ -722,7 +787,10 @@ def hetero_build(N_per_type, rels, dst_type, *, rowptr_dtype=torch.int32, stream
     col = _edge_array(E_T, torch.int32, dev)
     nb = mp_hetero_build_workspace(N_per_type, rels, dst_type, it)
     ws = _workspace(nb, dev)
-    mp_hetero_build(N_per_type, rels, dst_type, rowptr, it, col, ws, ws.numel(), stream)
+    st, chk = _sort_status(status, check, dev)
+    mp_hetero_build(N_per_type, rels, dst_type, rowptr, it, col, ws, ws.numel(), st, stream)
+    if chk:
+        check_status(st, "mp_hetero_build", stream)
     return rowptr, col
 
 

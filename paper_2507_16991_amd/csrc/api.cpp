@@ -32,14 +32,6 @@ struct Carver {
     }
 };
 
-int64_t env_int(const char* name, int64_t dflt) {
-    const char* v = std::getenv(name);
-    if (!v || !*v) return dflt;
-    char* end = nullptr;
-    long long x = std::strtoll(v, &end, 10);
-    return (end && *end == 0 && x > 0) ? (int64_t)x : dflt;
-}
-
 bool valid_itype(int t) { return t == MP_I32 || t == MP_I64; }
 bool valid_dtype(int t) { return t == MP_F32 || t == MP_BF16; }
 bool valid_reduce(int r) {
@@ -80,9 +72,13 @@ int check_csr_sizes(int64_t E, int64_t N) {
 
 int coo_to_csr_impl(const int32_t* src, const int32_t* dst, int64_t E, int64_t N, void* rowptr,
                     int itype, int32_t* col, int32_t* perm, const float* val_in, float* val_out,
-                    void* ws, size_t ws_bytes, hipStream_t s) {
+                    void* ws, size_t ws_bytes, int32_t* status, hipStream_t s) {
     const int rp64 = itype == MP_I64;
-    if (E == 0) return hip_status(launch_fill_rowptr_zero(N, rowptr, rp64, s));
+    if (E == 0) {
+        hipError_t e = launch_fill_rowptr_zero(N, rowptr, rp64, s);
+        if (e == hipSuccess) e = launch_sort_status(nullptr, status, s);
+        return hip_status(e);
+    }
     const int payload = (perm != nullptr || val_out != nullptr) ? 1 : 0;
     CsrLayout L = csr_layout(ws, E, N, payload);
     if (ws_bytes < L.bytes) return MP_ERR_WORKSPACE;
@@ -117,7 +113,7 @@ int coo_to_csr_impl(const int32_t* src, const int32_t* dst, int64_t E, int64_t N
         e = launch_gather_f32(val_in, eid_final, E, val_out, s);
         if (e != hipSuccess) return MP_ERR_HIP;
     }
-    return MP_OK;
+    return hip_status(launch_sort_status(&L.sc, status, s));
 }
 
 // ---- plan --------------------------------------------------------------------
@@ -465,6 +461,7 @@ const char* mp_status_str(int status) {
         case MP_ERR_HIP: return "HIP launch or copy failed";
         case MP_ERR_ALIGN: return "pointer not aligned to its element size";
         case MP_ERR_CALLBACK: return "the message callback failed";
+        case MP_ERR_SORT: return "a device sort gave up waiting; its output is invalid";
         default: return "unknown status";
     }
 }
@@ -481,16 +478,17 @@ int mp_coo_to_csr_workspace(int64_t E, int64_t N, int rowptr_itype, int with_pay
 
 int mp_coo_to_csr(const int32_t* src, const int32_t* dst, int64_t E, int64_t N, void* rowptr,
                   int rowptr_itype, int32_t* col, int32_t* perm, const float* val_in,
-                  float* val_out, void* ws, size_t ws_bytes, void* stream) {
+                  float* val_out, void* ws, size_t ws_bytes, int32_t* status, void* stream) {
     if (!valid_itype(rowptr_itype)) return MP_ERR_DTYPE;
     int st = check_csr_sizes(E, N);
     if (st != MP_OK) return st;
     if (!rowptr) return MP_ERR_NULL;
     if (E > 0 && (!src || !dst || !col || !ws)) return MP_ERR_NULL;
     if (E > 0 && (val_in == nullptr) != (val_out == nullptr)) return MP_ERR_NULL;
-    if ((uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4)) return MP_ERR_ALIGN;
+    if ((uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4) || (uintptr_t)status % 4)
+        return MP_ERR_ALIGN;
     return coo_to_csr_impl(src, dst, E, N, rowptr, rowptr_itype, col, perm, val_in, val_out, ws,
-                           ws_bytes, as_stream(stream));
+                           ws_bytes, status, as_stream(stream));
 }
 
 int mp_sorted_coo_to_csr(const int32_t* src, const int32_t* dst, int64_t E, int64_t N,
@@ -525,9 +523,19 @@ int mp_spmm_plan_size(int64_t N_dst, int64_t E, size_t* bytes) {
 int mp_spmm_plan_build(const void* rowptr, int rowptr_itype, int64_t N_dst, int64_t E, int64_t F,
                        int x_dtype, void* plan_buf, size_t plan_bytes, void* stream,
                        mp_plan** out) {
+    return mp_spmm_plan_build_opts(rowptr, rowptr_itype, N_dst, E, F, x_dtype, plan_buf,
+                                   plan_bytes, nullptr, stream, out);
+}
+
+int mp_spmm_plan_build_opts(const void* rowptr, int rowptr_itype, int64_t N_dst, int64_t E,
+                            int64_t F, int x_dtype, void* plan_buf, size_t plan_bytes,
+                            const mp_plan_opts* opts, void* stream, mp_plan** out) {
     if (!out || !rowptr || !plan_buf) return MP_ERR_NULL;
     if (!valid_itype(rowptr_itype) || !valid_dtype(x_dtype)) return MP_ERR_DTYPE;
     if (N_dst < 0 || N_dst > INT32_MAX || E < 0 || E > INT32_MAX || F < 1 || F > 65536)
+        return MP_ERR_SIZE;
+    const mp_plan_opts o = opts ? *opts : mp_plan_opts{0, 0, 0};
+    if (o.small_max < 0 || o.hub_min < 0 || o.chunk_min < 0 || o.chunk_min > INT32_MAX)
         return MP_ERR_SIZE;
     PlanLayout L = plan_layout(plan_buf, N_dst);
     if (plan_bytes < L.bytes) return MP_ERR_WORKSPACE;
@@ -544,15 +552,15 @@ int mp_spmm_plan_build(const void* rowptr, int rowptr_itype, int64_t N_dst, int6
     p->x_dtype = x_dtype;
     // rows of up to 16 edges per slot get one slot; longer rows a wavefront
     const Geometry geo = make_geometry(F, x_dtype, 16);
-    p->small_max = env_int("MP_SMALL_MAX", 16 * (int64_t)geo.S);
+    p->small_max = o.small_max > 0 ? o.small_max : 16 * (int64_t)geo.S;
     if (p->small_max > 16383) p->small_max = 16383;
     // a wavefront takes S * U edges per step; rows longer than 32 steps are
     // split into chunks of at least 32 steps, so that no wavefront runs a
     // long chain of dependent steps on its own
     const int64_t step_edges = (int64_t)geo.S * (geo.S * 8 > 64 ? 64 / geo.S : 8);
-    p->hub_min = env_int("MP_HUB_MIN", 32 * step_edges);
+    p->hub_min = o.hub_min > 0 ? o.hub_min : 32 * step_edges;
     if (p->hub_min < p->small_max) p->hub_min = p->small_max;
-    p->chunk_min = (int)env_int("MP_CHUNK", 32 * step_edges);
+    p->chunk_min = (int)(o.chunk_min > 0 ? o.chunk_min : 32 * step_edges);
     p->rowlist = L.rowlist;
     p->rowbeg = L.rowbeg;
     p->rowend = L.rowend;
@@ -582,14 +590,14 @@ int mp_spmm_plan_build(const void* rowptr, int rowptr_itype, int64_t N_dst, int6
     if (e == hipSuccess) e = exclusive_scan_u32(L.chunk_off, N_dst + 1, L.scan_ws, s);
     const int nclass = kClassHub + 1;
     if (e == hipSuccess)
-        e = launch_plan_header(L.sc.gbase, nclass, L.chunk_off, N_dst, L.header, s);
+        e = launch_plan_header(L.sc.gbase, nclass, L.chunk_off, N_dst, L.sc.err, L.header, s);
     uint32_t h[64] = {0};
     if (e == hipSuccess)
-        e = hipMemcpyAsync(h, L.header, sizeof(uint32_t) * (nclass + 2), hipMemcpyDeviceToHost, s);
+        e = hipMemcpyAsync(h, L.header, sizeof(uint32_t) * (nclass + 3), hipMemcpyDeviceToHost, s);
     if (e == hipSuccess) e = hipStreamSynchronize(s);
-    if (e != hipSuccess) {
+    if (e != hipSuccess || h[nclass + 2] != 0) {
         delete p;
-        return MP_ERR_HIP;
+        return e != hipSuccess ? MP_ERR_HIP : MP_ERR_SORT;
     }
     p->mid_base = h[kClassMid];
     p->hub_base = h[kClassHub];
@@ -680,7 +688,7 @@ int mp_csr_transpose_workspace(int64_t E, int64_t N_src, int rowptrT_itype, int 
 int mp_csr_transpose(const void* rowptr, int rowptr_itype, const int32_t* col, int64_t N_dst,
                      int64_t N_src, int64_t E, void* rowptrT, int rowptrT_itype, int32_t* colT,
                      int32_t* posT, const float* val_in, float* val_out, void* ws,
-                     size_t ws_bytes, void* stream) {
+                     size_t ws_bytes, int32_t* status, void* stream) {
     if (!valid_itype(rowptr_itype) || !valid_itype(rowptrT_itype)) return MP_ERR_DTYPE;
     int st = check_csr_sizes(E, N_src);
     if (st != MP_OK) return st;
@@ -689,10 +697,14 @@ int mp_csr_transpose(const void* rowptr, int rowptr_itype, const int32_t* col, i
     if (E > 0 && (!col || !colT || !ws)) return MP_ERR_NULL;
     if (E > 0 && (val_in == nullptr) != (val_out == nullptr)) return MP_ERR_NULL;
     if ((uintptr_t)rowptr % (rowptr_itype == MP_I64 ? 8 : 4) ||
-        (uintptr_t)rowptrT % (rowptrT_itype == MP_I64 ? 8 : 4))
+        (uintptr_t)rowptrT % (rowptrT_itype == MP_I64 ? 8 : 4) || (uintptr_t)status % 4)
         return MP_ERR_ALIGN;
     hipStream_t s = as_stream(stream);
-    if (E == 0) return hip_status(launch_fill_rowptr_zero(N_src, rowptrT, rowptrT_itype == MP_I64, s));
+    if (E == 0) {
+        hipError_t e = launch_fill_rowptr_zero(N_src, rowptrT, rowptrT_itype == MP_I64, s);
+        if (e == hipSuccess) e = launch_sort_status(nullptr, status, s);
+        return hip_status(e);
+    }
     size_t need = 0;
     mp_csr_transpose_workspace(E, N_src, rowptrT_itype, posT || val_out, &need);
     if (ws_bytes < need) return MP_ERR_WORKSPACE;
@@ -703,7 +715,7 @@ int mp_csr_transpose(const void* rowptr, int rowptr_itype, const int32_t* col, i
     if (launch_rows_of_edges(rowptr, rowptr_itype == MP_I64, N_dst, E, row, s) != hipSuccess)
         return MP_ERR_HIP;
     return coo_to_csr_impl(row, col, E, N_src, rowptrT, rowptrT_itype, colT, posT, val_in,
-                           val_out, static_cast<char*>(ws) + c.off, ws_bytes - c.off, s);
+                           val_out, static_cast<char*>(ws) + c.off, ws_bytes - c.off, status, s);
 }
 
 // Extra workspace of mp_spmm_backward_x beyond the aggregation's own: the
@@ -1195,12 +1207,13 @@ int mp_hetero_build_workspace(int n_types, const int64_t* N_per_type, int n_rel,
 
 int mp_hetero_build(int n_types, const int64_t* N_per_type, int n_rel, const mp_relation* rels,
                     int dst_type, void* rowptr, int rowptr_itype, int32_t* col, void* ws,
-                    size_t ws_bytes, void* stream) {
+                    size_t ws_bytes, int32_t* status, void* stream) {
     if (!valid_itype(rowptr_itype)) return MP_ERR_DTYPE;
     int64_t E_T = 0, N_rows = 0, offs[MP_MAX_TYPES + 1];
     int st = hetero_check(n_types, N_per_type, n_rel, rels, dst_type, &E_T, offs, &N_rows);
     if (st != MP_OK) return st;
     if (!rowptr || (E_T > 0 && (!col || !ws))) return MP_ERR_NULL;
+    if ((uintptr_t)status % 4) return MP_ERR_ALIGN;
     size_t need = 0;
     st = mp_hetero_build_workspace(n_types, N_per_type, n_rel, rels, dst_type, rowptr_itype, &need);
     if (st != MP_OK) return st;
@@ -1223,7 +1236,7 @@ int mp_hetero_build(int n_types, const int64_t* N_per_type, int n_rel, const mp_
         off += R.E;
     }
     return coo_to_csr_impl(src_g, dst_c, E_T, N_rows, rowptr, rowptr_itype, col, nullptr,
-                           nullptr, nullptr, c.base + c.off, ws_bytes - c.off, s);
+                           nullptr, nullptr, c.base + c.off, ws_bytes - c.off, status, s);
 }
 
 int mp_hetero_spmm(int n_types, const int64_t* N_per_type, const void* const* x_per_type,

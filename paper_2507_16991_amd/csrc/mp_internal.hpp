@@ -60,7 +60,7 @@ struct RadixScratch {
     uint64_t* desc;     // [tiles * 256] look-back descriptors
     uint32_t* gbase;    // [kMaxPasses * 256] global digit histogram -> exclusive starts
     uint32_t* counter;  // [kMaxPasses] dynamic tile ids
-    uint32_t* err;      // look-back wait limit exceeded (debug)
+    uint32_t* err;      // nonzero: a look-back wait gave up (the result is invalid)
 };
 size_t radix_scratch_bytes(int64_t n);
 RadixScratch radix_scratch(void* base, int64_t n);
@@ -80,6 +80,9 @@ hipError_t radix_sort_begin(const uint32_t* keys, int64_t n, int passes, int bit
                             const RadixScratch& sc, hipStream_t s);
 hipError_t radix_sort_pass(const RadixPass& p, hipStream_t s);
 
+// Write the caller's status word (nullptr: nothing) from the error word of
+// the sort that used sc (sc nullptr: no sort ran, MP_OK).
+hipError_t launch_sort_status(const RadixScratch* sc, int32_t* status, hipStream_t s);
 hipError_t launch_rowptr_from_sorted(const uint32_t* keys, int64_t E, int64_t N, void* rowptr,
                                      int rp64, hipStream_t s);
 hipError_t launch_fill_rowptr_zero(int64_t N, void* rowptr, int rp64, hipStream_t s);
@@ -241,7 +244,7 @@ hipError_t launch_plan_chunks(const void* rowptr, int rp64, const int32_t* rowli
 // header[c] = first rowlist position of class c (c < nclass, from the class
 // sort's exclusive digit starts), header[nclass] = N, header[nclass+1] = chunks
 hipError_t launch_plan_header(const uint32_t* class_start, int nclass, const uint32_t* chunk_off,
-                              int64_t N, uint32_t* header, hipStream_t s);
+                              int64_t N, const uint32_t* sort_err, uint32_t* header, hipStream_t s);
 
 // ---- edge-materialized messages (messages.hip) ----------------------------------
 struct MessageGather {

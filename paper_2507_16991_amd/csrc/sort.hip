@@ -1,15 +1,22 @@
 // Stable LSD radix sort of COO edges by destination, and the small kernels
 // around it (rowptr from the sorted keys, payload gather, validation).
 //
-// One pass over a digit: (1) every 4096-key tile counts its digits in LDS;
-// (2) the digit-major table counts[d * tiles + t] is exclusive-scanned, giving
-// each (digit, tile) its global output start; (3) every tile ranks its keys
-// stably (wave-level multisplit with ballots, per-wave LDS counters), stages
-// them in LDS in digit order and writes each digit's run contiguously.  Ranks
-// follow (wave, round, lane) order, which is element order, so each pass is
-// stable and the whole LSD sort keeps ascending COO id within a destination
-// (the order the CSR of Sec. 2.2 must have to be unique).  Only integer
-// arithmetic: the result is bit-exact.
+// The sort is one-sweep: radix_ghist counts the digits of every pass in one
+// read of the keys; then each pass is ONE kernel, radix_onesweep, in which a
+// tile of kSortTile keys (tile ids taken from an atomic counter in launch
+// order) ranks its keys stably (wave-level multisplit: one ballot per digit
+// bit, per-wavefront LDS counters), publishes its per-digit counts, obtains
+// the running totals of all earlier tiles by decoupled look-back over their
+// published descriptors, stages the tile in LDS in digit order and writes
+// each digit's run contiguously.  Ranks follow (wave, round, lane) order,
+// which is element order, so each pass is stable and the whole LSD sort keeps
+// ascending COO id within a destination (the order the CSR of Sec. 2.2 must
+// have to be unique).  Only integer arithmetic: the result is bit-exact.
+//
+// The look-back only waits on tiles that started earlier (their ids were
+// taken first), so it always ends; its wait is nevertheless bounded, and a
+// tile that gives up records it in an error word that the caller turns into
+// MP_ERR_SORT (radix_status) instead of hanging the device.
 #include "mp_internal.hpp"
 
 namespace mp {
@@ -262,6 +269,12 @@ __global__ __launch_bounds__(kSortBlock) void radix_onesweep(RadixPass p) {
     }
 }
 
+// The caller's status word: MP_ERR_SORT if any look-back of the sort gave up,
+// else MP_OK (err NULL: no sort ran).
+__global__ void radix_status(const uint32_t* __restrict__ err, int32_t* __restrict__ status) {
+    if (threadIdx.x == 0) *status = (err && *err) ? (int32_t)MP_ERR_SORT : (int32_t)MP_OK;
+}
+
 // rowptr[v] = first CSR position whose key is >= v, from the sorted keys:
 // position p writes every v in (keys[p-1], keys[p]] (keys[-1] = -1,
 // keys[E] = N), so each of the N+1 entries is written exactly once.  Each
@@ -417,6 +430,12 @@ hipError_t radix_sort_pass(const RadixPass& p, hipStream_t s) {
         hipLaunchKernelGGL(radix_onesweep<true>, dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p);
     else
         hipLaunchKernelGGL(radix_onesweep<false>, dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p);
+    return hipGetLastError();
+}
+
+hipError_t launch_sort_status(const RadixScratch* sc, int32_t* status, hipStream_t s) {
+    if (!status) return hipSuccess;
+    hipLaunchKernelGGL(radix_status, dim3(1), dim3(64), 0, s, sc ? sc->err : nullptr, status);
     return hipGetLastError();
 }
 

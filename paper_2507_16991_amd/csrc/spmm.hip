@@ -1,8 +1,8 @@
 // Segmented aggregation over the destination-major CSR (the AGGREGATION step
 // of Eq. (1) in PyG 2.0, with message w * x[src]), and its degree-binned plan.
 //
-// Work is split three ways by in-degree (Sec. 2.2: the sorted layout "enables
-// greater parallelism"), all inside ONE launch whose wavefronts take, in
+// Work is split three ways by in-degree (Sec. 2.2: a destination-sorted layout
+// lets the aggregation run in parallel over rows), all inside ONE launch whose wavefronts take, in
 // order: hub-row edge chunks (longest first), mid rows (one wavefront per
 // row, its slots interleaving the row's edges), and groups of small rows (one
 // slot of L lanes per row).  A slot is a group of L lanes that together hold
@@ -17,8 +17,11 @@
 // kernel).  No floating-point atomics anywhere.
 //
 // Max: (value, CSR position) pairs; a later edge replaces the running pair
-// only when strictly greater, and pairs are combined preferring the larger
-// value, then the smaller position -- the first edge attaining the maximum.
+// only when strictly greater (or when the pair is still empty, position -1),
+// and pairs are combined preferring a non-empty pair, then the larger value,
+// then the smaller position -- the first edge attaining the maximum, also
+// for rows of -inf messages.  (NaN messages are outside the contract: the
+// strided partials would not reproduce a sequential scan's answer.)
 #include <type_traits>
 
 #include "mp_internal.hpp"
@@ -179,7 +182,7 @@ struct Acc {
 #pragma unroll
             for (int k = 0; k < EPL; ++k) {
                 if constexpr (HS) s[a][k] = 0.f;
-                // -inf: the first (finite) message always replaces it
+                // empty: position -1 (the first message always replaces it)
                 if constexpr (HM) { m[a][k] = -__builtin_huge_valf(); i[a][k] = -1; }
                 if constexpr (HX) {
                     q[a][k] = 0.f;
@@ -193,14 +196,17 @@ struct Acc {
 #pragma unroll
         for (int k = 0; k < EPL; ++k) {
             if constexpr (HS) s[a][k] += v[k];
+            // the first message always replaces the empty pair (position -1),
+            // so a row whose messages are all -inf (+inf for min) still
+            // reports its first edge
             if constexpr (HM) {
-                const bool take = v[k] > m[a][k];
+                const bool take = v[k] > m[a][k] || i[a][k] < 0;
                 m[a][k] = take ? v[k] : m[a][k];
                 i[a][k] = take ? pos : i[a][k];
             }
             if constexpr (HX) {
                 q[a][k] = __builtin_fmaf(v[k], v[k], q[a][k]);
-                const bool take = v[k] < n[a][k];
+                const bool take = v[k] < n[a][k] || j[a][k] < 0;
                 n[a][k] = take ? v[k] : n[a][k];
                 j[a][k] = take ? pos : j[a][k];
             }
@@ -1113,14 +1119,16 @@ __global__ __launch_bounds__(256) void plan_rowrange(const void* rowptr, int rp6
 
 // header[c] = start of class c in rowlist (c < nclass), header[nclass] = N,
 // header[nclass + 1] = total hub chunks
+// header: class starts, N, the chunk count and the sort's error word
 __global__ void plan_header(const uint32_t* __restrict__ class_start, int nclass,
                             const uint32_t* __restrict__ chunk_off, int64_t N,
-                            uint32_t* __restrict__ header) {
+                            const uint32_t* __restrict__ sort_err, uint32_t* __restrict__ header) {
     const int c = threadIdx.x;
     if (c < nclass) header[c] = class_start[c];
     if (c == 0) {
         header[nclass] = (uint32_t)N;
         header[nclass + 1] = chunk_off[N];
+        header[nclass + 2] = *sort_err;
     }
 }
 
@@ -1302,9 +1310,9 @@ hipError_t launch_plan_chunks(const void* rowptr, int rp64, const int32_t* rowli
 }
 
 hipError_t launch_plan_header(const uint32_t* class_start, int nclass, const uint32_t* chunk_off,
-                              int64_t N, uint32_t* header, hipStream_t s) {
+                              int64_t N, const uint32_t* sort_err, uint32_t* header, hipStream_t s) {
     hipLaunchKernelGGL(plan_header, dim3(1), dim3(64), 0, s, class_start, nclass, chunk_off, N,
-                       header);
+                       sort_err, header);
     return hipGetLastError();
 }
 

@@ -30,8 +30,8 @@ def test_exports_every_declared_function():
 
 
 def test_version_and_status_strings():
-    assert mp.mp_version() == 4
-    for st in range(-9, 1):
+    assert mp.mp_version() == 5
+    for st in range(-10, 1):
         assert mp.mp_status_str(st) != "unknown status"
     assert mp.mp_status_str(-99) == "unknown status"
 
@@ -57,21 +57,23 @@ def test_coo_to_csr_argument_errors():
     L = mp.lib()
     # bad index type
     assert L.mp_coo_to_csr(FAKE, FAKE, 10, 5, FAKE, 7, FAKE, None, None, None, FAKE, 1 << 20,
-                           None) == -3
+                           None, None) == -3
     # NULL rowptr / src
     assert L.mp_coo_to_csr(FAKE, FAKE, 10, 5, None, 0, FAKE, None, None, None, FAKE, 1 << 20,
-                           None) == -1
+                           None, None) == -1
     assert L.mp_coo_to_csr(None, FAKE, 10, 5, FAKE, 0, FAKE, None, None, None, FAKE, 1 << 20,
-                           None) == -1
+                           None, None) == -1
     # val_in without val_out
     assert L.mp_coo_to_csr(FAKE, FAKE, 10, 5, FAKE, 0, FAKE, None, FAKE, None, FAKE, 1 << 20,
-                           None) == -1
-    # misaligned int64 rowptr
+                           None, None) == -1
+    # misaligned int64 rowptr; misaligned status word
     assert L.mp_coo_to_csr(FAKE, FAKE, 10, 5, FAKE + 4, 1, FAKE, None, None, None, FAKE, 1 << 20,
-                           None) == -8
+                           None, None) == -8
+    assert L.mp_coo_to_csr(FAKE, FAKE, 10, 5, FAKE, 0, FAKE, None, None, None, FAKE, 1 << 20,
+                           FAKE + 2, None) == -8
     # workspace too small
     assert L.mp_coo_to_csr(FAKE, FAKE, 10, 5, FAKE, 0, FAKE, None, None, None, FAKE, 16,
-                           None) == -5
+                           None, None) == -5
 
 
 def test_plan_errors():
@@ -88,6 +90,14 @@ def test_plan_errors():
     assert mp.mp_spmm_workspace(None, mp.MP_SUM) == 0
     with pytest.raises(mp.MPError):
         mp.mp_spmm_workspace(None, 3)  # SUM|MEAN is not a valid combination
+    # explicit thresholds: negative fields and chunks over INT32_MAX are rejected
+    for bad in ((-1, 0, 0), (0, -1, 0), (0, 0, -1), (0, 0, 1 << 31)):
+        o = mp.mp_plan_opts(*bad)
+        assert L.mp_spmm_plan_build_opts(FAKE, 0, 100, 1000, 64, 0, FAKE, 1 << 30,
+                                         ctypes.byref(o), None, ctypes.byref(h)) == -2
+    o = mp.mp_plan_opts(8, 64, 16)
+    assert L.mp_spmm_plan_build_opts(FAKE, 0, 100, 1000, 64, 0, FAKE, 16, ctypes.byref(o), None,
+                                     ctypes.byref(h)) == -5
 
 
 def _spmm(**kw):
@@ -151,6 +161,11 @@ def test_hetero_errors():
     assert L.mp_hetero_build_workspace(0, npt, 1, rel, 0, 0, ctypes.byref(b)) == -2
     bad = (mp.mp_relation * 1)(mp.mp_relation(0, 3, FAKE, FAKE, 20))
     assert L.mp_hetero_build_workspace(2, npt, 1, bad, 1, 0, ctypes.byref(b)) == -2
+    # build: NULL col, small workspace, misaligned status word
+    assert L.mp_hetero_build(2, npt, 1, rel, 1, FAKE, 0, None, FAKE, 1 << 20, None, None) == -1
+    assert L.mp_hetero_build(2, npt, 1, rel, 1, FAKE, 0, FAKE, FAKE, 16, None, None) == -5
+    assert L.mp_hetero_build(2, npt, 1, rel, 1, FAKE, 0, FAKE, FAKE, 1 << 20, FAKE + 2,
+                             None) == -8
     xs = (ctypes.c_void_p * 2)(FAKE, FAKE)
     assert L.mp_hetero_spmm(2, npt, xs, 0, 8, 1, None, FAKE, 0, FAKE, mp.MP_MEAN, FAKE, 0, None,
                             0, None) == -4
@@ -173,11 +188,12 @@ def test_transpose_errors_and_sizes():
     assert L.mp_csr_transpose_workspace(1000, 50, 0, 1, ctypes.byref(nb)) == 0
     assert nb.value >= 4 * 1000
     assert L.mp_csr_transpose_workspace(1000, 0, 0, 1, ctypes.byref(nb)) == -2
-    args = [FAKE, 0, FAKE, 10, 20, 100, FAKE, 0, FAKE, FAKE, None, None, FAKE, 1 << 20, None]
+    args = [FAKE, 0, FAKE, 10, 20, 100, FAKE, 0, FAKE, FAKE, None, None, FAKE, 1 << 20, None,
+            None]
     def call(**kw):
         a = list(args)
         names = ["rowptr", "it", "col", "N_dst", "N_src", "E", "rowptrT", "itT", "colT", "posT",
-                 "val_in", "val_out", "ws", "ws_bytes", "stream"]
+                 "val_in", "val_out", "ws", "ws_bytes", "status", "stream"]
         for k, v in kw.items():
             a[names.index(k)] = v
         return L.mp_csr_transpose(*a)
@@ -187,6 +203,7 @@ def test_transpose_errors_and_sizes():
     assert call(rowptrT=None) == -1
     assert call(val_in=FAKE) == -1
     assert call(rowptrT=FAKE + 4, itT=1) == -8
+    assert call(status=FAKE + 1) == -8
     assert call(ws_bytes=16) == -5
 
 

@@ -94,7 +94,8 @@ def test_transpose_without_positions():
 
 # ---- gradients ----------------------------------------------------------------------
 
-def backward_case(g, reduce, gdtype, xdtype, weighted, use_plan, seed=0, out_dtype=torch.float32):
+def backward_case(g, reduce, gdtype, xdtype, weighted, use_plan, seed=0, out_dtype=torch.float32,
+                  opts=None):
     """Run both gradients on device and compare with the oracle; returns the
     worst scaled errors."""
     rp_o, col_o, _, w_o = oracle.coo_to_csr(g.src, g.dst, g.n_dst, n_src=g.n_src, val=g.w)
@@ -111,7 +112,7 @@ def backward_case(g, reduce, gdtype, xdtype, weighted, use_plan, seed=0, out_dty
     w = dev(w_o) if weighted else None
     argout = dev(am_o.astype(np.int32)) if am_o is not None else None
     rpt, colt, post, wt, _ = check_transpose(rp_o, col_o, g.n_src, w_o)
-    planT = mp.Plan(rpt, g.E, F, gdtype) if use_plan else None
+    planT = mp.Plan(rpt, g.E, F, gdtype, opts=opts) if use_plan else None
     gx = mp.spmm_backward_x(rpt, colt, G, RED[reduce], posT=post, wT=wt if weighted else None,
                             rowptr=rp, argout=argout, planT=planT, out_dtype=out_dtype)
     torch.cuda.synchronize()
@@ -228,17 +229,14 @@ def test_backward_w_mixed_dtypes(mixed, reduce, xdtype, gdtype):
     backward_case(mixed, reduce, gdtype, xdtype, True, True)
 
 
-@pytest.mark.parametrize("thresholds", [("8", "64", "16"), ("1", "2", "1")])
+@pytest.mark.parametrize("thresholds", [(8, 64, 16), (1, 2, 1)])
 @pytest.mark.parametrize("reduce", ["sum", "max"])
-def test_backward_plan_regimes(monkeypatch, thresholds, reduce):
+def test_backward_plan_regimes(thresholds, reduce):
     """Power-law sources, so the transposed CSR has hub rows; tiny thresholds
     push them through every code path, including the chunk fix-up."""
     g = graphgen.chung_lu_graph(2, 4000, 60_000, 32, dmax=3000.0)
     g.w = graphgen.uniform_f32(2, 7, g.E)
-    monkeypatch.setenv("MP_SMALL_MAX", thresholds[0])
-    monkeypatch.setenv("MP_HUB_MIN", thresholds[1])
-    monkeypatch.setenv("MP_CHUNK", thresholds[2])
-    backward_case(g, reduce, torch.float32, torch.float32, True, True)
+    backward_case(g, reduce, torch.float32, torch.float32, True, True, opts=thresholds)
 
 
 @pytest.mark.parametrize("F", [1, 3, 8, 24, 64, 100, 128, 256, 300, 520, 1024])

@@ -163,16 +163,13 @@ def test_aggregate(mixed, reduce, dtype, use_plan):
     compare_aggregate(ref, rp_o, out, out_max, argout, r, dtype)
 
 
-@pytest.mark.parametrize("thresholds", [("8", "64", "16"), ("1", "2", "1")])
-def test_aggregate_plan_regimes(mixed, monkeypatch, thresholds):
+@pytest.mark.parametrize("thresholds", [(8, 64, 16), (1, 2, 1)])
+def test_aggregate_plan_regimes(mixed, thresholds):
     """Small hub thresholds send most rows through the hub-chunk path."""
     g, rp_o, col_o, _, _ = mixed
-    monkeypatch.setenv("MP_SMALL_MAX", thresholds[0])
-    monkeypatch.setenv("MP_HUB_MIN", thresholds[1])
-    monkeypatch.setenv("MP_CHUNK", thresholds[2])
     rp = dev(rp_o.astype(np.int32))
     msg = mp.message_gather(dev(col_o), dev(g.x))
-    plan = mp.Plan(rp, g.E, g.F, torch.float32)
+    plan = mp.Plan(rp, g.E, g.F, torch.float32, opts=thresholds)
     out, out_max, argout = mp.message_aggregate(rp, msg, mp.MP_SUM | mp.MP_MAX, plan=plan)
     torch.cuda.synchronize()
     ref = oracle.aggregate_messages(rp_o, oracle.message_gather(col_o, x=g.x))

@@ -84,10 +84,10 @@ def mixed():
     return g, rp_o, col_o, w_o
 
 
-def run_multi(g, rp_o, col_o, w_o, names, dtype, weighted, use_plan):
+def run_multi(g, rp_o, col_o, w_o, names, dtype, weighted, use_plan, opts=None):
     rp, col = dev(rp_o.astype(np.int32)), dev(col_o)
     x, xkw = x_pair(g, dtype)
-    plan = mp.Plan(rp, g.E, g.F, dtype) if use_plan else None
+    plan = mp.Plan(rp, g.E, g.F, dtype, opts=opts) if use_plan else None
     res = mp.spmm_multi(rp, col, x, names, w=dev(w_o) if weighted else None, plan=plan)
     torch.cuda.synchronize()
     return compare(res, rp_o, col_o, w_o if weighted else None, xkw, names, dtype)
@@ -106,23 +106,18 @@ def test_multi_subsets(mixed, names):
     run_multi(*mixed, names, torch.float32, True, True)
 
 
-@pytest.mark.parametrize("thresholds", [("8", "64", "16"), ("1", "2", "1")])
+@pytest.mark.parametrize("thresholds", [(8, 64, 16), (1, 2, 1)])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
-def test_multi_plan_regimes(mixed, monkeypatch, thresholds, dtype):
-    monkeypatch.setenv("MP_SMALL_MAX", thresholds[0])
-    monkeypatch.setenv("MP_HUB_MIN", thresholds[1])
-    monkeypatch.setenv("MP_CHUNK", thresholds[2])
-    run_multi(*mixed, ALL, dtype, True, True)
+def test_multi_plan_regimes(mixed, thresholds, dtype):
+    run_multi(*mixed, ALL, dtype, True, True, opts=thresholds)
 
 
 @pytest.mark.parametrize("F", [1, 3, 8, 24, 100, 300, 520])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
-def test_multi_feature_widths(F, dtype, monkeypatch):
-    monkeypatch.setenv("MP_HUB_MIN", "128")
-    monkeypatch.setenv("MP_CHUNK", "32")
+def test_multi_feature_widths(F, dtype):
     g = graphgen.mixed_graph(F, n=700, e=9000, f=F)
     rp_o, col_o, _, w_o = oracle.coo_to_csr(g.src, g.dst, g.n_dst, val=g.w)
-    run_multi(g, rp_o, col_o, w_o, ALL, dtype, False, True)
+    run_multi(g, rp_o, col_o, w_o, ALL, dtype, False, True, opts=(0, 128, 32))
 
 
 def test_multi_ties_and_signed_zero():

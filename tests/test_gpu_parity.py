@@ -170,12 +170,12 @@ def mixed():
 
 
 def run_case(g, rp_o, col_o, w_o, dtype, reduce, weighted, use_plan, out_dtype=torch.float32,
-             max_dtype=torch.float32, itype=torch.int32):
+             max_dtype=torch.float32, itype=torch.int32, opts=None):
     rp = dev(rp_o.astype(np.int32 if itype == torch.int32 else np.int64))
     col = dev(col_o)
     x = x_of(g, dtype)
     w = dev(w_o) if weighted else None
-    plan = mp.Plan(rp, g.E, g.F, dtype) if use_plan else None
+    plan = mp.Plan(rp, g.E, g.F, dtype, opts=opts) if use_plan else None
     out, out_max, argout = mp.spmm(rp, col, x, reduce, w=w, plan=plan, out_dtype=out_dtype,
                                    max_dtype=max_dtype)
     torch.cuda.synchronize()
@@ -192,29 +192,24 @@ def test_spmm_mixed(mixed, reduce, dtype, weighted, use_plan):
     run_case(g, rp_o, col_o, w_o, dtype, REDUCES[reduce], weighted, use_plan)
 
 
-@pytest.mark.parametrize("thresholds", [("8", "64", "16"), ("1", "2", "1"), ("64", "256", "64")])
+@pytest.mark.parametrize("thresholds", [(8, 64, 16), (1, 2, 1), (64, 256, 64)])
 @pytest.mark.parametrize("reduce", ["sum", "mean+max"])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
-def test_spmm_plan_regimes(mixed, monkeypatch, thresholds, reduce, dtype):
+def test_spmm_plan_regimes(mixed, thresholds, reduce, dtype):
     """Push rows through every code path: small groups, mid rows, hub chunks
     (with tiny chunks, so hubs have many chunks) and the chunk fix-up."""
     g, rp_o, col_o, w_o = mixed
-    monkeypatch.setenv("MP_SMALL_MAX", thresholds[0])
-    monkeypatch.setenv("MP_HUB_MIN", thresholds[1])
-    monkeypatch.setenv("MP_CHUNK", thresholds[2])
-    run_case(g, rp_o, col_o, w_o, dtype, REDUCES[reduce], True, True)
+    run_case(g, rp_o, col_o, w_o, dtype, REDUCES[reduce], True, True, opts=thresholds)
 
 
 @pytest.mark.parametrize("F", [1, 2, 3, 5, 8, 24, 100, 128, 300, 520])
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
-def test_spmm_feature_widths(F, dtype, monkeypatch):
+def test_spmm_feature_widths(F, dtype):
     g = graphgen.mixed_graph(F, n=700, e=9000, f=F)
-    monkeypatch.setenv("MP_HUB_MIN", "128")
-    monkeypatch.setenv("MP_CHUNK", "32")
     rp_o, col_o, _, w_o = oracle.coo_to_csr(g.src, g.dst, g.n_dst, val=g.w)
     for reduce in (mp.MP_SUM, mp.MP_MEAN | mp.MP_MAX):
         for use_plan in (False, True):
-            run_case(g, rp_o, col_o, w_o, dtype, reduce, True, use_plan)
+            run_case(g, rp_o, col_o, w_o, dtype, reduce, True, use_plan, opts=(0, 128, 32))
 
 
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
@@ -249,13 +244,11 @@ def test_spmm_row_stride(mixed, dtype, pad):
                                         (522, 528, torch.bfloat16), (50, 64, torch.float32),
                                         (7, 9, torch.float32)])
 @pytest.mark.parametrize("use_plan", [False, True])
-def test_spmm_padded_rows(monkeypatch, F, ld, dtype, use_plan):
+def test_spmm_padded_rows(F, ld, dtype, use_plan):
     """Tables whose row padding holds NaN: whatever vector width the row
     stride allows, no padding element may reach an output row or a hub
     partial."""
     g = graphgen.mixed_graph(F, n=700, e=9000, f=F)
-    monkeypatch.setenv("MP_HUB_MIN", "128")
-    monkeypatch.setenv("MP_CHUNK", "32")
     rp_o, col_o, _, w_o = oracle.coo_to_csr(g.src, g.dst, g.n_dst, val=g.w)
     rp, col, w = dev(rp_o.astype(np.int32)), dev(col_o), dev(w_o)
     x = x_of(g, dtype)
@@ -263,7 +256,7 @@ def test_spmm_padded_rows(monkeypatch, F, ld, dtype, use_plan):
     # poison the padding: it is read but must never reach an output
     wide = xs.as_strided((g.n_src, ld), (ld, 1))
     wide[:, F:] = float("nan")
-    plan = mp.Plan(rp, g.E, F, dtype) if use_plan else None
+    plan = mp.Plan(rp, g.E, F, dtype, opts=(0, 128, 32)) if use_plan else None
     for reduce, wt in ((mp.MP_SUM | mp.MP_MAX, False), (mp.MP_MEAN, True), (mp.MP_MAX, True)):
         res = mp.spmm(rp, col, xs, reduce, w=w if wt else None, plan=plan)
         torch.cuda.synchronize()
@@ -288,16 +281,52 @@ def test_pad_rows(dtype, F, ld):
     assert torch.equal(back, x)
 
 
-def test_spmm_signed_weights_and_ties(monkeypatch):
+def test_spmm_signed_weights_and_ties():
     g = graphgen.mixed_graph(3, f=16, signed_weights=True)
     g.x = (np.round(g.x * 2) / 2).astype(np.float32)  # coarse values: many ties
     g.x_bf16 = graphgen.f32_to_bf16(g.x)
-    monkeypatch.setenv("MP_HUB_MIN", "256")
-    monkeypatch.setenv("MP_CHUNK", "64")
     rp_o, col_o, _, w_o = oracle.coo_to_csr(g.src, g.dst, g.n_dst, val=g.w)
     for dtype in (torch.float32, torch.bfloat16):
         for weighted in (False, True):
-            run_case(g, rp_o, col_o, w_o, dtype, mp.MP_SUM | mp.MP_MAX, weighted, True)
+            run_case(g, rp_o, col_o, w_o, dtype, mp.MP_SUM | mp.MP_MAX, weighted, True,
+                     opts=(0, 256, 64))
+
+
+@pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
+@pytest.mark.parametrize("use_plan", [False, True])
+def test_spmm_infinite_messages(mixed, dtype, use_plan):
+    """Infinities are ordinary values: a row whose messages of a feature are
+    all -inf has max -inf at its FIRST edge (the empty pair is always
+    replaced by the first message), and +inf wins wherever it occurs.
+    Feature 0 is -inf in every source row, feature 1 +inf in every source
+    row, feature 2 -inf in every other source row; the rest stay finite."""
+    g, rp_o, col_o, w_o = mixed
+    x = g.x.copy()
+    x[:, 0] = -np.inf
+    x[:, 1] = np.inf
+    x[::2, 2] = -np.inf
+    xb = graphgen.f32_to_bf16(x)
+    xh = x if dtype == torch.float32 else graphgen.bf16_to_f32(xb)
+    xd = dev(x) if dtype == torch.float32 else dev(xb.view(np.int16)).view(torch.bfloat16)
+    rp, col = dev(rp_o.astype(np.int32)), dev(col_o)
+    plan = mp.Plan(rp, g.E, g.F, dtype, opts=(8, 64, 16)) if use_plan else None
+    _, out_max, argout = mp.spmm(rp, col, xd, mp.MP_MAX, plan=plan)
+    torch.cuda.synchronize()
+    ref = oracle.spmm(rp_o, col_o, x=xh, want=("max",))
+    assert np.array_equal(argout.cpu().numpy().astype(np.int64), ref["argmax"])
+    assert np.array_equal(out_max.cpu().numpy().view(np.uint32), ref["max"].view(np.uint32))
+    deg = np.diff(rp_o)
+    first = np.where(deg > 0, rp_o[:-1], -1)
+    assert np.array_equal(ref["argmax"][:, 0], first), "oracle: all -inf -> first edge"
+    # the stacked statistics: min of the +inf feature at the first edge too
+    res = mp.spmm_multi(rp, col, xd, ["max", "min"], plan=plan)
+    torch.cuda.synchronize()
+    assert np.array_equal(res["argmax"].cpu().numpy().astype(np.int64), ref["argmax"])
+    mref = oracle.spmm_multi(rp_o, col_o, x=xh)
+    assert np.array_equal(res["argmin"].cpu().numpy().astype(np.int64), mref["argmin"])
+    assert np.array_equal(res["min"].cpu().numpy().view(np.uint32),
+                          mref["min"].view(np.uint32))
+    assert np.array_equal(mref["argmin"][:, 1], first), "oracle: all +inf -> first edge"
 
 
 def test_spmm_output_dtypes(mixed):
@@ -352,12 +381,10 @@ def test_plan_mismatch_rejected_and_dtype_shared(mixed):
     assert e.value.status == -6
 
 
-def test_determinism_across_runs_and_streams(mixed, monkeypatch):
+def test_determinism_across_runs_and_streams(mixed):
     g, rp_o, col_o, w_o = mixed
-    monkeypatch.setenv("MP_HUB_MIN", "256")
-    monkeypatch.setenv("MP_CHUNK", "64")
     rp, col, x, w = dev(rp_o.astype(np.int32)), dev(col_o), x_of(g, torch.float32), dev(w_o)
-    plan = mp.Plan(rp, g.E, g.F)
+    plan = mp.Plan(rp, g.E, g.F, opts=(0, 256, 64))
     outs = []
     for k in range(3):
         s = torch.cuda.Stream() if k == 2 else torch.cuda.current_stream()
@@ -425,12 +452,43 @@ def test_chunglu_124M_csr_bit_exact(chunglu_full):
     assert np.array_equal(perm.cpu().numpy().astype(np.int64), perm_o)
 
 
+def compare_rows_chunked(ref, rp_o, out, out_max, argout, reduce, tol, chunk=1 << 18):
+    """Every row of a full-size call against the oracle's outputs for all
+    rows, in blocks of rows (bounded host memory).  Returns the worst scaled
+    error of the sum or mean."""
+    deg = np.diff(rp_o)
+    y = out.float().cpu().numpy() if out is not None else None
+    m = out_max.float().cpu().numpy() if out_max is not None else None
+    a = argout.cpu().numpy() if argout is not None else None
+    worst = 0.0
+    n = deg.shape[0]
+    for r0 in range(0, n, chunk):
+        r1 = min(n, r0 + chunk)
+        if reduce & mp.MP_SUM:
+            e = scaled_error(y[r0:r1], ref["sum"][r0:r1], ref["scale"][r0:r1])
+            assert e <= tol, f"rows {r0}..{r1}: sum error {e}"
+            worst = max(worst, e)
+        if reduce & mp.MP_MEAN:
+            sc = ref["scale"][r0:r1] / np.maximum(deg[r0:r1], 1)[:, None]
+            e = scaled_error(y[r0:r1], ref["mean"][r0:r1], sc)
+            assert e <= tol, f"rows {r0}..{r1}: mean error {e}"
+            worst = max(worst, e)
+        if reduce & mp.MP_MAX:
+            bad = np.argwhere(a[r0:r1].astype(np.int64) != ref["argmax"][r0:r1])
+            assert bad.size == 0, f"argmax differs at row {r0 + bad[0][0]}, feature {bad[0][1]}"
+            assert np.array_equal(m[r0:r1].view(np.uint32),
+                                  ref["max"][r0:r1].view(np.uint32)), f"max bits, rows {r0}.."
+    return worst
+
+
 @pytest.mark.parametrize("dtype", [torch.float32, torch.bfloat16])
-def test_chunglu_124M_spmm_sampled(chunglu_full, dtype):
+def test_chunglu_124M_spmm_all_rows(chunglu_full, dtype):
     """Full-size run in the benchmark's configuration (bf16 features laid
-    out in 256-byte rows, as the benchmark's step does); rows are
-    independent, so a sample of rows (every hub-sized row plus 20k random
-    rows) is checked exactly against the oracle."""
+    out in 256-byte rows, as the benchmark's step does), compared with the
+    oracle on EVERY one of the 2,449,029 rows: sum, mean, max + argmax and
+    the fused sum|max call.  bf16 features widen to fp32 exactly and are
+    accumulated in fp32, so their sums and means are held to the fp32 bound
+    (1e-5) as well as the stated 1e-2."""
     g, rp_o, col_o, _ = chunglu_full
     rp = dev(rp_o.astype(np.int32))
     col = dev(col_o)
@@ -439,16 +497,13 @@ def test_chunglu_124M_spmm_sampled(chunglu_full, dtype):
         x = mp.pad_rows(x)
         assert x.stride(0) == 128
     plan = mp.Plan(rp, g.E, g.F, dtype)
-    deg = np.diff(rp_o)
-    rng_rows = graphgen.uniform_ints(11, 5, 20_000, g.n_dst).astype(np.int64)
-    rows = np.unique(np.concatenate([np.nonzero(deg >= 2048)[0], rng_rows,
-                                     [0, g.n_dst - 1]])).astype(np.int64)
-    xh = x_f32_host(g, dtype)
-    for reduce in (mp.MP_SUM, mp.MP_MEAN, mp.MP_MAX):
+    ref = (oracle.spmm(rp_o, col_o, x=g.x) if dtype == torch.float32
+           else oracle.spmm(rp_o, col_o, x_bf16=g.x_bf16))
+    for reduce in (mp.MP_SUM, mp.MP_MEAN, mp.MP_MAX, mp.MP_SUM | mp.MP_MAX):
         out, out_max, argout = mp.spmm(rp, col, x, reduce, plan=plan)
         torch.cuda.synchronize()
-        errs = compare_spmm(rp_o, col_o, None, xh, out, out_max, argout, reduce, dtype, rows=rows)
-        print("chunglu", dtype, reduce, errs)
+        worst = compare_rows_chunked(ref, rp_o, out, out_max, argout, reduce, TOL[torch.float32])
+        sys.stderr.write(f"chunglu all rows {dtype} reduce {reduce}: worst error {worst:.3e}\n")
         del out, out_max, argout
 
 
