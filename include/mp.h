@@ -257,8 +257,12 @@ int mp_copy_rows(const void* in, int64_t ld_in, void* out, int64_t ld_out, int64
  *   MP_MAX / MP_MIN  the largest / smallest m_p and, in arg, the CSR position
  *           of the first edge attaining it ('>' / '<' comparisons, so -0.0
  *           and +0.0 tie and the earlier edge wins);
- *   MP_VAR  population variance, sum m_p^2 / deg - mean^2 (fp32, clamped at
- *           0);  MP_STD  its square root.
+ *   MP_VAR  population variance, sum (m_p - mean)^2 / deg, evaluated in one
+ *           pass about a shift K (the mean of up to 8 messages of the row):
+ *           sum (m_p - K)^2 / deg - (sum (m_p - K) / deg)^2 in fp32, clamped
+ *           at 0, so that it keeps its digits when the mean is large against
+ *           the spread (rows of equal messages give exactly 0);
+ *   MP_STD  its square root.
  * An empty row gives 0 everywhere and -1 in arg.  All sums accumulate in
  * fp32 in an order fixed by the plan; outputs are fp32.
  * ------------------------------------------------------------------------- */

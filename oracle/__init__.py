@@ -57,7 +57,7 @@ def _L():
         lib.oracle_csr_rows.argtypes = [i64, i64, p, p, i64, p, p, p]
         lib.oracle_csr_rows.restype = i32
         lib.oracle_spmm_multi.argtypes = [i64, p, i64, i64, p, p, p, p, i32, i64, p, p, p, p,
-                                          p, i32]
+                                          i32]
         lib.oracle_spmm_multi.restype = i32
         lib.oracle_segment_matmul.argtypes = [i32, p, p, p, i64, i64, p, p]
         lib.oracle_segment_matmul.restype = i32
@@ -166,7 +166,7 @@ def spmm(rowptr, col, x=None, x_bf16=None, w=None, rows=None, nthreads=None,
 def spmm_multi(rowptr, col, x=None, x_bf16=None, w=None, rows=None, nthreads=None):
     """Min (+ first argmin), population variance, standard deviation and the
     variance error scale of every row (or the listed rows).  Returns a dict of
-    'min' fp32, 'argmin' int64, 'var', 'std', 'var_scale' fp64, shape [rows, F]."""
+    'min' fp32, 'argmin' int64, 'var', 'std' fp64, shape [rows, F]."""
     rowptr, col = _c(rowptr, np.int64), _c(col, np.int32)
     xa, isb, n_src, F = _x_args(x, x_bf16)
     n_dst = rowptr.shape[0] - 1
@@ -174,13 +174,12 @@ def spmm_multi(rowptr, col, x=None, x_bf16=None, w=None, rows=None, nthreads=Non
     n = n_dst if rows is None else rows.shape[0]
     w = _c(w, np.float32)
     out = {"min": np.empty((n, F), np.float32), "argmin": np.empty((n, F), np.int64),
-           "var": np.empty((n, F), np.float64), "std": np.empty((n, F), np.float64),
-           "var_scale": np.empty((n, F), np.float64)}
+           "var": np.empty((n, F), np.float64), "std": np.empty((n, F), np.float64)}
     if nthreads is None:
         nthreads = default_threads()
     rc = _L().oracle_spmm_multi(n, _p(rows), n_dst, n_src, _p(rowptr), _p(col), _p(w), _p(xa),
                                 isb, F, _p(out["min"]), _p(out["argmin"]), _p(out["var"]),
-                                _p(out["std"]), _p(out["var_scale"]), int(nthreads))
+                                _p(out["std"]), int(nthreads))
     if rc != 0:
         raise ValueError(f"oracle_spmm_multi failed ({rc})")
     return out

@@ -535,14 +535,11 @@ int oracle_spmm_backward_w(int64_t n_rows, const int64_t* rows, int64_t N_dst, i
  *   out_var[k,f]: sum_p (m_p - mean)^2 / deg, mean = sum_p m_p / deg, both
  *                 in fp64 (two passes; 0 for an empty row)
  *   out_std[k,f]: sqrt(out_var[k,f])
- *   var_scale[k,f]: sum_p m_p^2 / deg + (sum_p |m_p| / deg)^2, the size of
- *                 the terms a one-pass fp32 evaluation of the variance
- *                 subtracts (error scale)
  * Any output may be NULL.  Returns 0, or -1 for a bad row or column. */
 int oracle_spmm_multi(int64_t n_rows, const int64_t* rows, int64_t N_dst, int64_t N_src,
                       const int64_t* rowptr, const int32_t* col, const float* w, const void* x,
                       int x_is_bf16, int64_t F, float* out_min, int64_t* argmin,
-                      double* out_var, double* out_std, double* var_scale, int nthreads) {
+                      double* out_var, double* out_std, int nthreads) {
     int bad = 0;
 #pragma omp parallel for schedule(static) num_threads(nthreads > 0 ? nthreads : 1) reduction(| : bad)
     for (int64_t k = 0; k < n_rows; ++k) {
@@ -559,7 +556,7 @@ int oracle_spmm_multi(int64_t n_rows, const int64_t* rows, int64_t N_dst, int64_
         for (int64_t f = 0; f < F; ++f) {
             float least = 0.0f;
             int64_t arg = -1;
-            double s = 0.0, a = 0.0, q = 0.0;
+            double s = 0.0;
             for (int64_t p = p0; p < p1; ++p) {
                 float m = message(x, x_is_bf16, F, col[p], f, w, p);
                 if (arg < 0 || m < least) {
@@ -567,8 +564,6 @@ int oracle_spmm_multi(int64_t n_rows, const int64_t* rows, int64_t N_dst, int64_
                     arg = p;
                 }
                 s += (double)m;
-                a += fabs((double)m);
-                q += (double)m * (double)m;
             }
             double var = 0.0;
             if (deg > 0) {
@@ -583,9 +578,6 @@ int oracle_spmm_multi(int64_t n_rows, const int64_t* rows, int64_t N_dst, int64_
             if (argmin) argmin[k * F + f] = arg;
             if (out_var) out_var[k * F + f] = var;
             if (out_std) out_std[k * F + f] = sqrt(var);
-            if (var_scale)
-                var_scale[k * F + f] =
-                    deg > 0 ? q / (double)deg + (a / (double)deg) * (a / (double)deg) : 0.0;
         }
     }
     return bad ? -1 : 0;

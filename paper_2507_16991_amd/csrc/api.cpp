@@ -207,6 +207,7 @@ int run_spmm(const mp_plan* plan, SpmmParams& P, const Geometry& g, int x_dtype,
             P.part_sum = hs ? c.take<float>(cells) : nullptr;
             P.part_max = hm ? c.take<float>(cells) : nullptr;
             P.part_arg = hm ? c.take<int32_t>(cells) : nullptr;
+            P.part_dsum = hx ? c.take<float>(cells) : nullptr;
             P.part_sq = hx ? c.take<float>(cells) : nullptr;
             P.part_min = hx ? c.take<float>(cells) : nullptr;
             P.part_amin = hx ? c.take<int32_t>(cells) : nullptr;
@@ -634,8 +635,9 @@ int mp_spmm_multi_workspace(const mp_plan* plan, size_t* bytes) {
         *bytes = 0;
         return MP_OK;
     }
-    // hub partials: sum, sum of squares, max and min values, their positions
-    *bytes = 6 * align_up((size_t)plan->n_chunks * (size_t)plan->F * 4, 256);
+    // hub partials: sum, shifted sum and sum of squares, max and min values,
+    // their positions
+    *bytes = 7 * align_up((size_t)plan->n_chunks * (size_t)plan->F * 4, 256);
     return MP_OK;
 }
 

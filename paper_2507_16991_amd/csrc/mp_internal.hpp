@@ -178,7 +178,8 @@ struct SpmmParams {
     float* part_sum;
     float* part_max;
     int32_t* part_arg;
-    float* part_sq;
+    float* part_dsum;  // stats: hub partial sums of (m - K)
+    float* part_sq;    // stats: hub partial sums of (m - K)^2
     float* part_min;
     int32_t* part_amin;
 };

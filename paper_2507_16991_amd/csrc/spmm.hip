@@ -17,10 +17,10 @@
 // kernel).  No floating-point atomics anywhere.
 //
 // Max: (value, CSR position) pairs; a later edge replaces the running pair
-// only when strictly greater (or when the pair is still empty, position -1),
-// and pairs are combined preferring a non-empty pair, then the larger value,
-// then the smaller position -- the first edge attaining the maximum, also
-// for rows of -inf messages.  (NaN messages are outside the contract: the
+// only when strictly greater (the first edge of a partial always replaces the
+// empty pair, position -1), and pairs are combined preferring a non-empty pair, then the
+// larger value, then the smaller position -- the first edge attaining the
+// maximum, also for rows of -inf messages.  (NaN messages are outside the contract: the
 // strided partials would not reproduce a sequential scan's answer.)
 #include <type_traits>
 
@@ -34,6 +34,9 @@ constexpr int kWavesPerBlock = kBlock / kWave;
 constexpr int kUnroll = 8;  // edges gathered per slot per iteration
 #ifndef MP_STATS_UNROLL
 #define MP_STATS_UNROLL 8   // the same for the stacked statistics
+#endif
+#ifndef MP_STATS_WAVES
+#define MP_STATS_WAVES 4    // stats mode: wavefronts per SIMD the registers must allow
 #endif
 #ifndef MP_MASKED_UNROLL
 #define MP_MASKED_UNROLL 8  // the same for the masked sum
@@ -147,6 +150,15 @@ __device__ inline const char* feat_addr(const SpmmParams& P, int32_t c, int64_t 
     }
 }
 
+// a - b, never fused with the product that formed a: a weighted message is
+// the rounded product fl(w * x), and a deviation fused into fma(w, x, -K)
+// would belong to the unrounded one (a one-edge row would get a variance of
+// the product's rounding error squared instead of 0)
+__device__ inline float sub_rounded(float a, float b) {
+#pragma clang fp contract(off)
+    return a - b;
+}
+
 // Keep the pair with the larger value; on equal values the smaller position.
 __device__ inline void max_merge(float& va, int32_t& ia, float vb, int32_t ib) {
     const bool take = (ib >= 0) && (ia < 0 || vb > va || (vb == va && ib < ia));
@@ -163,8 +175,14 @@ __device__ inline void min_merge(float& va, int32_t& ia, float vb, int32_t ib) {
 
 // ---- accumulator state -------------------------------------------------------
 
-// HX (stats mode, which also sets HS and HM): the sum of squares and the
-// (min, position) pair are kept as well.
+// HX (stats mode, which also sets HS and HM): the (min, position) pair and,
+// for the variance, the sum and the sum of squares of the messages minus a
+// shift K, are kept as well.  K is the mean of a few messages of the row (the
+// same K for every partial, slot and hub chunk of the row), so the shifted
+// messages are small whenever the row's spread is small next to its mean,
+// and  var = sum (m-K)^2 / deg - (sum (m-K) / deg)^2  subtracts terms of the
+// size of the variance itself instead of E[m^2] and E[m]^2 (whose difference
+// loses every digit when the mean is large against the spread).
 template <int EPL, bool HS, bool HM, bool HX = false, int NA = (HM ? 2 : 4)>
 struct Acc {
     static constexpr int A = NA;  // independent partial accumulators
@@ -172,9 +190,11 @@ struct Acc {
     float s[A][EPL];
     float m[A][EPL];
     int32_t i[A][EPL];
-    float q[AX][EPL];
+    float d[AX][EPL];  // sum of (m - K)
+    float q[AX][EPL];  // sum of (m - K)^2
     float n[AX][EPL];
     int32_t j[AX][EPL];
+    float K[HX ? EPL : 1];  // the row's shift
 
     __device__ inline void init() {
 #pragma unroll
@@ -185,11 +205,22 @@ struct Acc {
                 // empty: position -1 (the first message always replaces it)
                 if constexpr (HM) { m[a][k] = -__builtin_huge_valf(); i[a][k] = -1; }
                 if constexpr (HX) {
+                    d[a][k] = 0.f;
                     q[a][k] = 0.f;
                     n[a][k] = __builtin_huge_valf();
                     j[a][k] = -1;
                 }
             }
+#pragma unroll
+        for (int k = 0; k < (HX ? EPL : 1); ++k) K[k] = 0.f;
+    }
+    // the shift: the mean of cnt >= 1 messages whose fp32 sum is t
+    __device__ inline void set_shift(const float (&t)[EPL], int cnt) {
+        if constexpr (HX) {
+            const float c = (float)(cnt > 0 ? cnt : 1);
+#pragma unroll
+            for (int k = 0; k < EPL; ++k) K[k] = t[k] / c;
+        }
     }
     // message values v (already weighted) of CSR position pos
     __device__ inline void add(int a, const float (&v)[EPL], int32_t pos) {
@@ -198,14 +229,19 @@ struct Acc {
             if constexpr (HS) s[a][k] += v[k];
             // the first message always replaces the empty pair (position -1),
             // so a row whose messages are all -inf (+inf for min) still
-            // reports its first edge
+            // reports its first edge.  (A wavefront-uniform "first message"
+            // flag instead of the position test was measured: the compiler
+            // then keeps a separate first-step copy of the loop, 16 to 24
+            // registers more.)
             if constexpr (HM) {
                 const bool take = v[k] > m[a][k] || i[a][k] < 0;
                 m[a][k] = take ? v[k] : m[a][k];
                 i[a][k] = take ? pos : i[a][k];
             }
             if constexpr (HX) {
-                q[a][k] = __builtin_fmaf(v[k], v[k], q[a][k]);
+                const float dv = sub_rounded(v[k], K[k]);
+                d[a][k] += dv;
+                q[a][k] = __builtin_fmaf(dv, dv, q[a][k]);
                 const bool take = v[k] < n[a][k] || j[a][k] < 0;
                 n[a][k] = take ? v[k] : n[a][k];
                 j[a][k] = take ? pos : j[a][k];
@@ -223,6 +259,7 @@ struct Acc {
                     if constexpr (HS) s[a][k] += s[a + step][k];
                     if constexpr (HM) max_merge(m[a][k], i[a][k], m[a + step][k], i[a + step][k]);
                     if constexpr (HX) {
+                        d[a][k] += d[a + step][k];
                         q[a][k] += q[a + step][k];
                         min_merge(n[a][k], j[a][k], n[a + step][k], j[a + step][k]);
                     }
@@ -246,10 +283,12 @@ struct Acc {
                     if (use) max_merge(m[0][k], i[0][k], om, oi);
                 }
                 if constexpr (HX) {
+                    const float od = __shfl(d[0][k], src);
                     const float oq = __shfl(q[0][k], src);
                     const float on = __shfl(n[0][k], src);
                     const int32_t oj = __shfl(j[0][k], src);
                     if (use) {
+                        d[0][k] += od;
                         q[0][k] += oq;
                         min_merge(n[0][k], j[0][k], on, oj);
                     }
@@ -350,19 +389,23 @@ __device__ inline void store_row(const SpmmParams& P, int64_t row, int64_t fe, i
 }
 
 // Stats mode: write every requested statistic of a finished row (fp32).
-// Variance is the population variance E[m^2] - E[m]^2, clamped at 0.
+// s is the plain sum; d and q the sums of (m - K) and (m - K)^2 for the
+// row's shift K.  Variance is the population variance
+// q / deg - (d / deg)^2 (shift-invariant), clamped at 0.
 template <int EPL>
 __device__ inline void store_stats(const SpmmParams& P, int64_t row, int64_t fe, int64_t deg,
-                                   const float (&s)[EPL], const float (&q)[EPL],
-                                   const float (&m)[EPL], const int32_t (&im)[EPL],
-                                   const float (&n)[EPL], const int32_t (&in)[EPL], bool vec) {
+                                   const float (&s)[EPL], const float (&d)[EPL],
+                                   const float (&q)[EPL], const float (&m)[EPL],
+                                   const int32_t (&im)[EPL], const float (&n)[EPL],
+                                   const int32_t (&in)[EPL], bool vec) {
     const int64_t o = row * P.F + fe;
     const float dv = (float)deg;
     float mean[EPL], var[EPL], sd[EPL], mx[EPL], mn[EPL];
 #pragma unroll
     for (int k = 0; k < EPL; ++k) {
         mean[k] = deg > 0 ? s[k] / dv : 0.f;
-        const float v = deg > 0 ? q[k] / dv - mean[k] * mean[k] : 0.f;
+        const float c = d[k] / dv;
+        const float v = deg > 0 ? q[k] / dv - c * c : 0.f;
         var[k] = v > 0.f ? v : 0.f;
         sd[k] = __builtin_sqrtf(var[k]);
         mx[k] = im[k] < 0 ? 0.f : m[k];
@@ -391,11 +434,13 @@ __device__ inline int32_t col_at(const SpmmParams& P, int64_t p) {
 template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, int MODE, bool O32>
 __device__ inline void wave_range(const SpmmParams& P,
                                   AccFor<TX, EPL, HS, HM, MODE>& acc, int64_t e0,
-                                  int64_t e1, int lane, int slot, bool feat_ok, int64_t fe, int U) {
+                                  int64_t e1, int lane, int slot, bool feat_ok, int64_t fe, int U,
+                                  bool shift_first) {
     using R = typename RawVec<TX, EPL>::T;
     constexpr int A = AccFor<TX, EPL, HS, HM, MODE>::A;
     constexpr int UN = unroll_of<MODE>();
     const int S = P.S;
+    const int j = lane - slot * P.L;  // lane within the slot
     const int SU = S * U;
     const int steps = kWave / SU;
     const int tile = steps * SU;
@@ -423,6 +468,31 @@ __device__ inline void wave_range(const SpmmParams& P,
 #pragma unroll
             for (int u = 0; u < UN; ++u)
                 if (ok[u]) raw[u] = load_row_chunk<R, O32>(P.table_ptr[0], addr[u]);
+            if constexpr (MODE == kModeStats) {
+                if (shift_first) {
+                    // the row's first step: the mean of slot 0's messages
+                    // (edges u * S of the row) is the row's shift, passed from
+                    // slot 0's lane j to lane j of every slot
+                    shift_first = false;
+                    float t[EPL] = {};
+                    int cnt = 0;
+#pragma unroll
+                    for (int u = 0; u < UN; ++u) {
+                        float wt = 1.f;
+                        if constexpr (W) wt = __shfl(myw, (u * S + slot) & (kWave - 1));
+                        if (u < U && u * S < rem) ++cnt;
+                        if (slot == 0 && ok[u]) {
+                            float v[EPL];
+                            widen<TX, EPL>(raw[u], v);
+#pragma unroll
+                            for (int k = 0; k < EPL; ++k) t[k] += W ? __fmul_rn(wt, v[k]) : v[k];
+                        }
+                    }
+#pragma unroll
+                    for (int k = 0; k < EPL; ++k) t[k] = __shfl(t[k], j);
+                    acc.set_shift(t, cnt);
+                }
+            }
 #pragma unroll
             for (int u = 0; u < UN; ++u) {
                 const int t = base + u * S + slot;
@@ -717,6 +787,21 @@ __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MOD
 #pragma unroll
         for (int u = 0; u < UN; ++u)
             if (ok[u]) raw[u] = load_row_chunk<R, O32>(P.table_ptr[0], addr[u]);
+        if constexpr (MODE == kModeStats) {
+            if (it == 0) {  // the row's shift: the mean of its first UN messages
+                float t[EPL] = {};
+#pragma unroll
+                for (int u = 0; u < UN; ++u) {
+                    if (ok[u]) {
+                        float v[EPL];
+                        widen<TX, EPL>(raw[u], v);
+#pragma unroll
+                        for (int k = 0; k < EPL; ++k) t[k] += W ? __fmul_rn(wt[u], v[k]) : v[k];
+                    }
+                }
+                acc.set_shift(t, my_n < UN ? my_n : UN);
+            }
+        }
 #pragma unroll
         for (int u = 0; u < UN; ++u) {
             if (ok[u]) {
@@ -732,8 +817,59 @@ __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MOD
     }
 }
 
+// The shift of a hub row for the variance: the mean of the row's first
+// min(deg, 8) messages, summed in edge order.  Every wavefront of every chunk
+// of the row loads the same messages and so computes the identical shift
+// (one extra pair of dependent loads per hub chunk, which spans 32 or more
+// steps).
+template <typename TX, int EPL, int NT, bool W, bool O32>
+__device__ inline void hub_shift(const SpmmParams& P, int64_t r0, int64_t deg, bool feat_ok,
+                                 int64_t fe, float (&t)[EPL], int& cnt) {
+    using R = typename RawVec<TX, EPL>::T;
+    constexpr int KS = 8;
+    cnt = deg < KS ? (int)deg : KS;
+    int32_t c[KS];
+    float w[KS];
+#pragma unroll
+    for (int u = 0; u < KS; ++u) {
+        c[u] = u < cnt ? col_at(P, r0 + u) : 0;
+        w[u] = 1.f;
+        if constexpr (W) w[u] = u < cnt ? P.w[r0 + u] : 1.f;
+    }
+    R raw[KS];
+#pragma unroll
+    for (int u = 0; u < KS; ++u)
+        if (feat_ok && u < cnt)
+            raw[u] = load_row_chunk<R, O32>(P.table_ptr[0], feat_addr<TX, NT>(P, c[u], fe));
+#pragma unroll
+    for (int k = 0; k < EPL; ++k) t[k] = 0.f;
+#pragma unroll
+    for (int u = 0; u < KS; ++u) {
+        if (feat_ok && u < cnt) {
+            float v[EPL];
+            widen<TX, EPL>(raw[u], v);
+#pragma unroll
+            for (int k = 0; k < EPL; ++k) t[k] += W ? __fmul_rn(w[u], v[k]) : v[k];
+        }
+    }
+}
+
+// Stats mode keeps seven running values per element.  Where they fit
+// (unweighted, 32-bit row offsets, at most 8 accumulated elements per lane),
+// the register budget is capped so that MP_STATS_WAVES wavefronts fit a SIMD
+// without spilling: the gathers need wavefronts in flight more than the
+// scheduler needs the registers.
+template <typename TX, int EPL, bool HS, bool HM, bool W, int MODE, bool O32>
+constexpr int waves_hint() {
+    return MODE == kModeStats && !W && O32 && AccFor<TX, EPL, HS, HM, MODE>::A * EPL <= 8
+               ? MP_STATS_WAVES
+               : 1;
+}
+
 template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, int MODE, bool O32 = false>
-__global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
+__global__ __launch_bounds__(kBlock)
+__attribute__((amdgpu_waves_per_eu(waves_hint<TX, EPL, HS, HM, W, MODE, O32>())))
+void spmm_main(SpmmParams P) {
     constexpr bool HX = MODE == kModeStats;
     const int lane = threadIdx.x & (kWave - 1);
     const int64_t wv = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave)) +
@@ -777,6 +913,12 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
             e0 = r0 + k * csz;
             e1 = e0 + csz < r1 ? e0 + csz : r1;
             cidx = item;
+            if constexpr (HX) {
+                float t[EPL];
+                int cnt;
+                hub_shift<TX, EPL, NT, W, O32>(P, r0, deg, feat_ok, fe, t, cnt);
+                acc.set_shift(t, cnt);
+            }
         } else {
             if (P.rowbeg) {
                 row = P.rowlist[P.mid_base + item];
@@ -797,7 +939,8 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
                                                            w_lo, mww);
         }
         else
-            wave_range<TX, EPL, HS, HM, NT, W, MODE, O32>(P, acc, e0, e1, lane, slot, feat_ok, fe, U);
+            wave_range<TX, EPL, HS, HM, NT, W, MODE, O32>(P, acc, e0, e1, lane, slot, feat_ok, fe, U,
+                                                          !hub);
         acc.fold();
         acc.reduce_slots(S, L, slot, lane);
         if (slot == 0 && feat_ok) {
@@ -808,14 +951,15 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
                     if constexpr (HS) P.part_sum[o + k] = acc.s[0][k];
                     if constexpr (HM) { P.part_max[o + k] = acc.m[0][k]; P.part_arg[o + k] = acc.i[0][k]; }
                     if constexpr (HX) {
+                        P.part_dsum[o + k] = acc.d[0][k];
                         P.part_sq[o + k] = acc.q[0][k];
                         P.part_min[o + k] = acc.n[0][k];
                         P.part_amin[o + k] = acc.j[0][k];
                     }
                 }
             } else if constexpr (HX) {
-                store_stats<EPL>(P, row, fe, e1 - e0, acc.s[0], acc.q[0], acc.m[0], acc.i[0],
-                                 acc.n[0], acc.j[0], P.vec_store != 0);
+                store_stats<EPL>(P, row, fe, e1 - e0, acc.s[0], acc.d[0], acc.q[0], acc.m[0],
+                                 acc.i[0], acc.n[0], acc.j[0], P.vec_store != 0);
             } else {
                 store_row<EPL>(P, row, fe, e1 - e0, acc.s[0], acc.m[0], acc.i[0], HS, HM);
             }
@@ -862,8 +1006,8 @@ __global__ __launch_bounds__(kBlock) void spmm_main(SpmmParams P) {
     acc.fold();
     if (feat_ok) {
         if constexpr (HX)
-            store_stats<EPL>(P, row, fe, e1 - e0, acc.s[0], acc.q[0], acc.m[0], acc.i[0],
-                             acc.n[0], acc.j[0], P.vec_store != 0);
+            store_stats<EPL>(P, row, fe, e1 - e0, acc.s[0], acc.d[0], acc.q[0], acc.m[0],
+                             acc.i[0], acc.n[0], acc.j[0], P.vec_store != 0);
         else
             store_row<EPL>(P, row, fe, e1 - e0, acc.s[0], acc.m[0], acc.i[0], HS, HM);
     }
@@ -968,6 +1112,19 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
 
         Acc<EPL, HS, HM, HX, 1> acc;
         acc.init();
+        if constexpr (HX) {  // the shift: the mean of all (at most kTinyDeg) messages
+            float t[EPL] = {};
+#pragma unroll
+            for (int u = 0; u < kTinyDeg; ++u) {
+                if (ok[u]) {
+                    float v[EPL];
+                    widen<TX, EPL>(raw[u], v);
+#pragma unroll
+                    for (int k = 0; k < EPL; ++k) t[k] += W ? __fmul_rn(wt[u], v[k]) : v[k];
+                }
+            }
+            acc.set_shift(t, deg);
+        }
 #pragma unroll
         for (int u = 0; u < kTinyDeg; ++u) {
             if (ok[u]) {
@@ -983,8 +1140,8 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
         }
         if (feat_ok) {
             if constexpr (HX)
-                store_stats<EPL>(P, row, fe, deg, acc.s[0], acc.q[0], acc.m[0], acc.i[0], acc.n[0],
-                                 acc.j[0], P.vec_store != 0);
+                store_stats<EPL>(P, row, fe, deg, acc.s[0], acc.d[0], acc.q[0], acc.m[0],
+                                 acc.i[0], acc.n[0], acc.j[0], P.vec_store != 0);
             else
                 store_row<EPL>(P, row, fe, deg, acc.s[0], acc.m[0], acc.i[0], HS, HM);
         }
@@ -1002,7 +1159,8 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
 
 // Combine the chunk partials of every hub row, in chunk order, and write the
 // row.  One wavefront per (hub row, 64-feature tile); lane = one feature.
-// HX: the stats partials too (sum of squares, min and its position).
+// HX: the stats partials too (the shifted sums and sums of squares, all
+// chunks of a row using the same shift, and min with its position).
 template <bool HS, bool HM, bool HX>
 __global__ __launch_bounds__(kBlock) void spmm_fixup(SpmmParams P) {
     const int lane = threadIdx.x & (kWave - 1);
@@ -1017,11 +1175,12 @@ __global__ __launch_bounds__(kBlock) void spmm_fixup(SpmmParams P) {
     const int64_t c0 = P.chunk_off[P.hub_base + h], c1 = P.chunk_off[P.hub_base + h + 1];
     constexpr int A = 4;
     float s[A] = {0.f, 0.f, 0.f, 0.f};
+    float ds[A] = {0.f, 0.f, 0.f, 0.f};
     float qs[A] = {0.f, 0.f, 0.f, 0.f};
     float m = 0.f, mn = 0.f;
     int32_t mi = -1, ni = -1;
     for (int64_t c = c0; c < c1; c += A) {
-        float ps[A], pm[A], pq[A], pn[A];
+        float ps[A], pm[A], pd[A], pq[A], pn[A];
         int32_t pi[A], pj[A];
 #pragma unroll
         for (int a = 0; a < A; ++a) {
@@ -1030,6 +1189,7 @@ __global__ __launch_bounds__(kBlock) void spmm_fixup(SpmmParams P) {
             if constexpr (HS) ps[a] = ok ? P.part_sum[o] : 0.f;
             if constexpr (HM) { pm[a] = ok ? P.part_max[o] : 0.f; pi[a] = ok ? P.part_arg[o] : -1; }
             if constexpr (HX) {
+                pd[a] = ok ? P.part_dsum[o] : 0.f;
                 pq[a] = ok ? P.part_sq[o] : 0.f;
                 pn[a] = ok ? P.part_min[o] : 0.f;
                 pj[a] = ok ? P.part_amin[o] : -1;
@@ -1040,6 +1200,7 @@ __global__ __launch_bounds__(kBlock) void spmm_fixup(SpmmParams P) {
             if constexpr (HS) s[a] += ps[a];
             if constexpr (HM) max_merge(m, mi, pm[a], pi[a]);
             if constexpr (HX) {
+                ds[a] += pd[a];
                 qs[a] += pq[a];
                 min_merge(mn, ni, pn[a], pj[a]);
             }
@@ -1049,10 +1210,11 @@ __global__ __launch_bounds__(kBlock) void spmm_fixup(SpmmParams P) {
     const int64_t o = row * P.F + f;
     if constexpr (HX) {
         const float sum[1] = {(s[0] + s[1]) + (s[2] + s[3])};
+        const float dsum[1] = {(ds[0] + ds[1]) + (ds[2] + ds[3])};
         const float sq[1] = {(qs[0] + qs[1]) + (qs[2] + qs[3])};
         const float mx[1] = {m}, nn[1] = {mn};
         const int32_t im[1] = {mi}, in[1] = {ni};
-        store_stats<1>(P, row, f, deg, sum, sq, mx, im, nn, in, false);
+        store_stats<1>(P, row, f, deg, sum, dsum, sq, mx, im, nn, in, false);
         return;
     }
     if constexpr (HS) {
@@ -1177,6 +1339,13 @@ hipError_t launch_typed(const SpmmParams& p, unsigned grid, hipStream_t s) {
     // 124M-edge graph; fp32 rows are unaffected), so only those are built
     if constexpr (std::is_same<TX, uint16_t>::value) {
         if (p.off32)
+            return p.w ? launch_w<TX, EPL, true, true>(p, grid, s)
+                       : launch_w<TX, EPL, false, true>(p, grid, s);
+    }
+    // ... and for fp32 rows in stats mode, where the registers they free
+    // keep the kernel at four wavefronts per SIMD
+    if constexpr (std::is_same<TX, float>::value) {
+        if (p.off32 && p.stats)
             return p.w ? launch_w<TX, EPL, true, true>(p, grid, s)
                        : launch_w<TX, EPL, false, true>(p, grid, s);
     }
