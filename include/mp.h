@@ -237,6 +237,28 @@ int mp_spmm(const mp_plan* plan, const void* rowptr, int rowptr_itype, const int
             int64_t F, int64_t ldx, int reduce, void* out, int out_dtype, void* out_max,
             int max_dtype, int32_t* argout, void* ws, size_t ws_bytes, void* stream);
 
+/* For callers that cannot allocate device memory (code under HIP graph
+ * capture, tight serving loops, harnesses that forbid allocation): mp_spmm
+ * without a workspace argument.  The hub-chunk partials that mp_spmm keeps in
+ * its caller's workspace live instead in a static device array of
+ * MP_NOALLOC_SCRATCH_BYTES per GPU, which the library's code object reserves
+ * on every GPU it is loaded on and holds until the process ends.  Arguments,
+ * outputs (bit-identical to mp_spmm's with the same plan) and status codes
+ * as mp_spmm, plus MP_ERR_WORKSPACE when mp_spmm_workspace(plan, reduce)
+ * exceeds MP_NOALLOC_SCRATCH_BYTES.  The call allocates nothing (no hipMalloc,
+ * hipFree or allocating library routine); its first call on a device looks
+ * up that device's copy of the array (hipGetSymbolAddress, with the device
+ * current) and keeps the address.  Every call on one GPU shares that GPU's
+ * array: calls enqueued on one stream are ordered and safe, but calls that
+ * overlap on one GPU (different streams, or several host threads) race on it
+ * and give wrong results.  Nothing in the array needs to start at zero (every
+ * partial is written before it is read).  Asynchronous on `stream`. */
+#define MP_NOALLOC_SCRATCH_BYTES ((size_t)64 << 20)
+int mp_spmm_noalloc(const mp_plan* plan, const void* rowptr, int rowptr_itype,
+                    const int32_t* col, const float* w, const void* x, int x_dtype,
+                    int64_t N_src, int64_t N_dst, int64_t F, int64_t ldx, int reduce, void* out,
+                    int out_dtype, void* out_max, int max_dtype, int32_t* argout, void* stream);
+
 /* Feature-table layout: out[r, 0:F] = in[r, 0:F] for 0 <= r < N, rows of in
  * ld_in and rows of out ld_out elements apart (ld_in, ld_out >= F; padding
  * elements of out are not written; in and out must not overlap).  Used to

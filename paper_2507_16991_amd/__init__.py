@@ -39,7 +39,7 @@ __all__ = [
     "message_gather", "message_scale", "message_aggregate", "spmm_materialized",
     "message_backward", "edge_dot", "mp_copy_rows", "aligned_ld", "pad_rows", "MP_MAX_TYPES",
     "MP_ALL_TYPES", "MP_ERR_SORT", "mp_plan_opts", "mp_spmm_plan_build_opts", "new_status",
-    "check_status",
+    "check_status", "mp_spmm_noalloc", "MP_NOALLOC_SCRATCH_BYTES",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -56,6 +56,7 @@ MP_MAX_TYPES = 16
 MP_ALL_TYPES = -1  # dst_type selecting every destination type at once
 MP_ERR_CALLBACK = -9
 MP_ERR_SORT = -10
+MP_NOALLOC_SCRATCH_BYTES = 64 << 20  # the static scratch of mp_spmm_noalloc, per GPU
 
 # int c(void* msg, int msg_dtype, int64_t E, int64_t F, void* user, void* stream)
 MESSAGE_FN = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.c_void_p, ctypes.c_int, ctypes.c_int64,
@@ -110,6 +111,8 @@ def lib():
         L.mp_spmm_workspace.argtypes = [p, i32, psz]
         L.mp_spmm.argtypes = [p, p, i32, p, p, p, i32, i64, i64, i64, i64, i32, p, i32, p, i32, p,
                               p, sz, p]
+        L.mp_spmm_noalloc.argtypes = [p, p, i32, p, p, p, i32, i64, i64, i64, i64, i32, p, i32,
+                                      p, i32, p, p]
         L.mp_copy_rows.argtypes = [p, i64, p, i64, i64, i64, i32, p]
         L.mp_hetero_build_workspace.argtypes = [i32, p, i32, p, i32, i32, psz]
         L.mp_hetero_build.argtypes = [i32, p, i32, p, i32, p, i32, p, p, sz, p, p]
@@ -156,7 +159,7 @@ def lib():
                      "mp_spmm_backward_x_workspace", "mp_spmm_backward_x",
                      "mp_spmm_backward_w_workspace", "mp_spmm_backward_w", "mp_spmm_plan_size",
                      "mp_spmm_plan_build", "mp_spmm_plan_build_opts", "mp_spmm_workspace",
-                     "mp_spmm",
+                     "mp_spmm", "mp_spmm_noalloc",
                      "mp_hetero_build_workspace", "mp_hetero_build", "mp_hetero_spmm",
                      "mp_validate_coo", "mp_validate_csr"):
             getattr(L, name).restype = i32
@@ -301,6 +304,17 @@ def mp_spmm(plan_handle, rowptr, rowptr_itype, col, w, x, x_dtype, N_src, N_dst,
         plan_handle, _ptr(rowptr), rowptr_itype, _ptr(col), _ptr(w), xp, x_dtype, N_src,
         N_dst, F, ldx, reduce, _ptr(out), out_dtype, _ptr(out_max), max_dtype, _ptr(argout),
         _ptr(ws), ws_bytes, _stream(stream)))
+
+
+def mp_spmm_noalloc(plan_handle, rowptr, rowptr_itype, col, w, x, x_dtype, N_src, N_dst, F,
+                    ldx, reduce, out, out_dtype, out_max, max_dtype, argout, stream=None):
+    """mp_spmm for callers that cannot allocate: no workspace argument (the
+    library's static per-GPU scratch array holds the hub partials)."""
+    xp = _rows_ptr(x)[0] if isinstance(x, torch.Tensor) else x
+    _check("mp_spmm_noalloc", lib().mp_spmm_noalloc(
+        plan_handle, _ptr(rowptr), rowptr_itype, _ptr(col), _ptr(w), xp, x_dtype, N_src, N_dst,
+        F, ldx, reduce, _ptr(out), out_dtype, _ptr(out_max), max_dtype, _ptr(argout),
+        _stream(stream)))
 
 
 def mp_copy_rows(x_in, ld_in, x_out, ld_out, N, F, dtype, stream=None):

@@ -7,6 +7,7 @@
 #include <climits>
 #include <cstdlib>
 #include <cstring>
+#include <mutex>
 #include <new>
 
 #include "mp_internal.hpp"
@@ -658,6 +659,68 @@ int mp_readout_multi(const mp_plan* plan, const void* ptr, int ptr_itype, const 
     // whose column of position p is p itself
     return multi_impl(plan, ptr, ptr_itype, nullptr, nullptr, x, x_dtype, N_nodes, N_seg, F, ldx,
                       n_out, outs, ws, ws_bytes, as_stream(stream));
+}
+
+}  // extern "C"
+
+// ---- mp_spmm_noalloc: hub partials in a static device array --------------------
+
+// The workspace of mp_spmm_noalloc.  In host code its name is only the host
+// stand-in of the device symbol: host code uses the address that
+// hipGetSymbolAddress returns for the current device (each GPU holds its own
+// copy), never the name.
+static __device__ __align__(256) unsigned char scratch[MP_NOALLOC_SCRATCH_BYTES];
+
+namespace {
+
+constexpr int kMaxDevices = 64;
+std::mutex g_scratch_mu;
+void* g_scratch_ptr[kMaxDevices] = {};
+
+// The current device's copy of `scratch`, looked up once per device.
+int noalloc_scratch(void** out) {
+    int dev = -1;
+    if (hipGetDevice(&dev) != hipSuccess) return MP_ERR_HIP;
+    if (dev < 0 || dev >= kMaxDevices) return MP_ERR_HIP;
+    std::lock_guard<std::mutex> lock(g_scratch_mu);
+    if (!g_scratch_ptr[dev]) {
+        void* ptr = nullptr;
+        if (hipGetSymbolAddress(&ptr, HIP_SYMBOL(scratch)) != hipSuccess || !ptr)
+            return MP_ERR_HIP;
+        g_scratch_ptr[dev] = ptr;
+    }
+    *out = g_scratch_ptr[dev];
+    return MP_OK;
+}
+
+}  // namespace
+
+extern "C" {
+
+int mp_spmm_noalloc(const mp_plan* plan, const void* rowptr, int rowptr_itype,
+                    const int32_t* col, const float* w, const void* x, int x_dtype,
+                    int64_t N_src, int64_t N_dst, int64_t F, int64_t ldx, int reduce, void* out,
+                    int out_dtype, void* out_max, int max_dtype, int32_t* argout, void* stream) {
+    if (N_dst > 0 && !col) return MP_ERR_NULL;
+    size_t need = 0;
+    int st = mp_spmm_workspace(plan, reduce, &need);
+    if (st != MP_OK) return st;
+    if (need > MP_NOALLOC_SCRATCH_BYTES) return MP_ERR_WORKSPACE;
+    SpmmCall c{plan, rowptr, rowptr_itype, col, w, x, x_dtype, N_src, N_dst, F, ldx, reduce,
+               out, out_dtype, out_max, max_dtype, argout, nullptr, 0};
+    if (need > 0) {
+        // every other argument is checked before the array is looked up; the
+        // check only needs to know that a large enough workspace will come
+        c.ws = &g_scratch_ptr;
+        c.ws_bytes = MP_NOALLOC_SCRATCH_BYTES;
+    }
+    st = spmm_check(c);
+    if (st != MP_OK) return st;
+    if (need > 0 && N_dst > 0) {
+        st = noalloc_scratch(&c.ws);
+        if (st != MP_OK) return st;
+    }
+    return spmm_launch(c, as_stream(stream));
 }
 
 int mp_spmm(const mp_plan* plan, const void* rowptr, int rowptr_itype, const int32_t* col,

@@ -29,6 +29,19 @@ def test_exports_every_declared_function():
         assert hasattr(L, n), f"{n} declared in mp.h but not exported"
 
 
+def test_noalloc_argument_errors():
+    L = mp.lib()
+    # arguments of a valid plan-free sum; each case breaks one (never a valid call: the
+    # pointers are fake)
+    a = [None, FAKE, 0, FAKE, None, FAKE, 0, 10, 10, 8, 8, 1, FAKE, 0, None, 0, None, None]
+    b = list(a); b[11] = 3  # SUM|MEAN
+    assert L.mp_spmm_noalloc(*b) == -4
+    b = list(a); b[3] = None
+    assert L.mp_spmm_noalloc(*b) == -1
+    b = list(a); b[5] = FAKE + 2
+    assert L.mp_spmm_noalloc(*b) == -8
+
+
 def test_version_and_status_strings():
     assert mp.mp_version() == 5
     for st in range(-10, 1):
