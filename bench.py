@@ -163,6 +163,39 @@ def hetero_bytes(g, F):
     return b_csr, b_sum, ef
 
 
+class ColdEvents:
+    """Events of one cold-cache step: before each operation a 1 GiB buffer is
+    written (more than the 256 MB MALL and the 4 MB L2 of each XCD), so every
+    operation starts with its inputs evicted from the caches; start[i] and
+    end[i] bracket operation i alone."""
+
+    def __init__(self, torch, n_ops, flush):
+        self.start = [torch.cuda.Event(enable_timing=True) for _ in range(n_ops)]
+        self.end = [torch.cuda.Event(enable_timing=True) for _ in range(n_ops)]
+        self.flush = flush
+
+    def times(self):
+        return [a.elapsed_time(b) for a, b in zip(self.start, self.end)]
+
+
+def make_mark(stream):
+    """mark(evs, i): the boundary before operation i (i = n_ops: after the
+    last).  evs is None (untimed), a list of n_ops + 1 events (warm: the
+    operations back to back), or a ColdEvents (a cache flush before each)."""
+    def mark(evs, i):
+        if evs is None:
+            return
+        if isinstance(evs, ColdEvents):
+            if i > 0:
+                evs.end[i - 1].record(stream)
+            if i < len(evs.start):
+                evs.flush()
+                evs.start[i].record(stream)
+        else:
+            evs[i].record(stream)
+    return mark
+
+
 def build_step(args, mp, torch, np, dev):
     """Generate the workload, upload it, and return (graph, step(evs), op list).
 
@@ -182,10 +215,7 @@ def build_step(args, mp, torch, np, dev):
     print(f"[bench] generated {args.workload} in {time.time() - t0:.1f}s", file=sys.stderr,
           flush=True)
     stream = torch.cuda.current_stream()
-
-    def mark(evs, i):
-        if evs is not None:
-            evs[i].record(stream)
+    mark = make_mark(stream)
 
     if args.workload == "hetero-20M":
         F = g.F
@@ -278,6 +308,11 @@ def build_step(args, mp, torch, np, dev):
                         E * F))
             calls.append(("spmm", k, x, xd, red, wt, ld))
 
+    # the gather ceilings of this workload: the CSR column stream over each
+    # feature table, as the aggregations read it (table, row stride and
+    # algorithmic row bytes)
+    g.probe = {"col": col, "tables": {c[1]: (c[2], c[6] * xs[c[1]][2], F * xs[c[1]][2])
+                                      for c in calls if c[0] == "spmm"}}
     plans = {}
     wss = {}
 
@@ -602,20 +637,17 @@ def projection_step(args, mp, torch, np, dev):
            ("proj_dw", 2 * N * F + 2 * N * Fo + 2 * chunks * F * Fo * 4 + T * F * Fo * 4, 0)]
     flops = 2 * N * F * Fo
 
+    mark = make_mark(torch.cuda.current_stream())
+
     def step(evs=None):
-        stream = torch.cuda.current_stream()
-        if evs is not None:
-            evs[0].record(stream)
+        mark(evs, 0)
         mp.mp_segment_matmul(seg, T, x, W, F, Fo, out, mp.MP_F32, ws_f, ws_f.numel())
-        if evs is not None:
-            evs[1].record(stream)
+        mark(evs, 1)
         mp.mp_segment_matmul_backward(seg, T, x, W, dout, F, Fo, dx, mp.MP_F32, None, None, 0)
-        if evs is not None:
-            evs[2].record(stream)
+        mark(evs, 2)
         mp.mp_segment_matmul_backward(seg, T, x, W, dout, F, Fo, None, mp.MP_F32, dW, ws_b,
                                       ws_b.numel())
-        if evs is not None:
-            evs[3].record(stream)
+        mark(evs, 3)
 
     return SimpleNamespace(n_dst=N, n_src=N, E=0, F=F, flops_per_op=flops), step, ops
 
@@ -658,6 +690,9 @@ def run(args):
     N, E, F = g.n_dst, g.E, g.F
     names = [o[0] for o in ops]
     op_bytes = {o[0]: o[1] for o in ops}
+    if args.dump_ops:
+        with open(args.dump_ops, "w") as f:
+            json.dump([{"name": o[0], "bytes": o[1]} for o in ops], f)
     step_bytes = sum(o[1] for o in ops)
     step_ef = sum(o[2] for o in ops)
 
@@ -672,6 +707,7 @@ def run(args):
         torch.cuda.synchronize()
         del a, b
 
+    # warm: K steps back to back, one event per operation boundary
     all_evs = [[torch.cuda.Event(enable_timing=True) for _ in range(len(ops) + 1)]
                for _ in range(args.steps)]
     torch.cuda.synchronize()
@@ -683,15 +719,50 @@ def run(args):
     ms_step = wall * 1e3 / args.steps
     for st in SORT_STATUS:  # every sort of the timed steps completed
         mp.check_status(st, "device sort of a timed step")
+    warm = {n: [evs[i].elapsed_time(evs[i + 1]) for evs in all_evs] for i, n in enumerate(names)}
+    op_ms = {n: float(np.mean(v)) for n, v in warm.items()}
 
-    op_ms = {n: float(np.mean([evs[i].elapsed_time(evs[i + 1]) for evs in all_evs]))
-             for i, n in enumerate(names)}
-    breakdown = {n: {"ms": round(op_ms[n], 4),
-                     "GB_per_s": round(op_bytes[n] / (op_ms[n] * 1e-3) / 1e9, 1)}
-                 for n in names}
+    # cold: every operation alone after a 1 GiB write (caches flushed)
+    cold = {}
+    if args.cold_reps > 0:
+        flush_buf = torch.empty(1 << 28, dtype=torch.int32, device=dev)
+        cev = [ColdEvents(torch, len(ops), lambda: flush_buf.fill_(7))
+               for _ in range(args.cold_reps)]
+        for c in cev:
+            step(c)
+        torch.cuda.synchronize()
+        for st in SORT_STATUS:
+            mp.check_status(st, "device sort of a cold step")
+        times = [c.times() for c in cev]
+        cold = {n: [t[i] for t in times] for i, n in enumerate(names)}
+        del flush_buf
+
+    def gbs(nbytes, ms):
+        return round(nbytes / (ms * 1e-3) / 1e9, 1)
+
+    breakdown = {}
+    for n in names:
+        w = warm[n]
+        d = {"ms": round(op_ms[n], 4), "ms_median": round(float(np.median(w)), 4),
+             "ms_min": round(float(np.min(w)), 4), "GB_per_s": gbs(op_bytes[n], op_ms[n])}
+        if n in cold:
+            cm = float(np.median(cold[n]))
+            d.update({"cold_ms_median": round(cm, 4),
+                      "cold_ms_min": round(float(np.min(cold[n])), 4),
+                      "cold_GB_per_s": gbs(op_bytes[n], cm)})
+        breakdown[n] = d
     if getattr(g, "flops_per_op", 0):
         for n in names:  # every projection op is 2 N F F' flops
             breakdown[n]["TFLOP_per_s"] = round(g.flops_per_op / (op_ms[n] * 1e-3) / 1e12, 1)
+    ceil = measure_ceilings(g, mp, torch, np, dev) if args.ceilings and hasattr(g, "probe") \
+        else None
+    if ceil:
+        for n in names:  # aggregations against the gather of their own table
+            k = n.rsplit("_", 1)[-1]
+            if f"gather_{k}" in ceil and n.split("_")[0] in ("sum", "mean", "max", "wsum",
+                                                              "sum+max"):
+                breakdown[n]["frac_of_gather_ceiling"] = round(
+                    breakdown[n]["GB_per_s"] / ceil[f"gather_{k}"]["GB_per_s"], 4)
     value = step_bytes / (ms_step * 1e-3) / 1e9
     web = args.workload == "web-1.6B"
     headline = args.workload == WORKLOAD
@@ -764,14 +835,78 @@ def run(args):
             "unit": "GB/s",
             "frac": round(achieved / HBM_PEAK_GBS, 4),
             "traffic": None if traffic is None else round(traffic / (dom_ms * 1e-3) / 1e9, 1),
+            "traffic_note": "FETCH_SIZE + WRITE_SIZE per launch (copy-calibrated) over the "
+                            "launch time: bytes leaving the L2, MALL hits included, so an "
+                            "upper bound on HBM traffic",
             "traffic_bytes_per_launch": None if traffic is None else int(traffic),
             "algorithmic_bytes_per_launch": dom_bytes,
             "avg_launch_ms": round(dom_ms, 4),
         },
     }
+    if ceil:
+        result["ceilings"] = ceil
+        k = dom.rsplit("_", 1)[-1]
+        if f"gather_{k}" in ceil:
+            mc = ceil[f"gather_{k}"]["GB_per_s"]
+            result["roofline"]["measured_ceiling"] = {
+                "GB_per_s": mc, "probe": ceil[f"gather_{k}"]["what"]}
+            result["roofline"]["frac_of_measured_ceiling"] = round(achieved / mc, 4)
     if args.cpu_baseline and headline:
         result["cpu_baseline"] = cpu_baseline(g, N, E, F, step_bytes, args)
     print(json.dumps(result), flush=True)
+
+
+def measure_ceilings(g, mp, torch, np, dev, reps=5):
+    """What the device delivers for the aggregation's traffic, measured with
+    the library's bandwidth probes on this workload's own buffers: a streaming
+    read and a copy, and, per feature table, the row gather in CSR column
+    order (every edge reads its column index and one row; no reduction, no
+    output).  GB/s of algorithmic bytes (for the gather 4 + F*b per edge),
+    median of `reps` timed runs after one untimed."""
+    col = g.probe["col"]
+    E = int(col.numel())
+    sink = torch.zeros(mp.MP_PROBE_SINK_WORDS, dtype=torch.int32, device=dev)
+    big = torch.empty(1 << 28, dtype=torch.int32, device=dev)  # 1 GiB
+    big2 = torch.empty_like(big)
+
+    def timed(fn):
+        ts = []
+        for r in range(reps + 1):
+            a = torch.cuda.Event(enable_timing=True)
+            b = torch.cuda.Event(enable_timing=True)
+            a.record()
+            fn()
+            b.record()
+            torch.cuda.synchronize()
+            ts.append(a.elapsed_time(b))
+        return float(np.median(ts[1:]))
+
+    res = {}
+    for name, nbytes, fn in [("read", 1 << 30, lambda: mp.mp_probe_read(big, 1 << 30, sink)),
+                             ("copy", 2 << 30, lambda: mp.mp_probe_copy(big, big2, 1 << 30))]:
+        ms = timed(fn)
+        res[name] = {"ms": round(ms, 4), "GB_per_s": round(nbytes / (ms * 1e-3) / 1e9, 1),
+                     "what": "1 GiB streaming read" if name == "read" else
+                     "1 GiB streaming copy (read + write)"}
+    del big, big2
+    for k, (x, stride, row) in g.probe["tables"].items():
+        probe_row = (row + 15) // 16 * 16
+        ms = timed(lambda: mp.mp_probe_gather(col, E, x, stride, probe_row, sink))
+        res[f"gather_{k}"] = {
+            "ms": round(ms, 4), "GB_per_s": round(E * (4 + row) / (ms * 1e-3) / 1e9, 1),
+            "what": f"{E} rows of {row} B ({k} features, rows {stride} B apart) gathered in CSR "
+                    f"column order, 16-byte loads"}
+    return res
+
+
+def cpu_model():
+    try:
+        for line in open("/proc/cpuinfo"):
+            if line.startswith("model name"):
+                return line.split(":", 1)[1].strip()
+    except OSError:
+        pass
+    return "unknown"
 
 
 def cpu_baseline(g, N, E, F, step_bytes, args):
@@ -783,7 +918,7 @@ def cpu_baseline(g, N, E, F, step_bytes, args):
 
     import oracle
 
-    threads = int(os.environ.get("OMP_NUM_THREADS", "0") or 0) or (os.cpu_count() or 1)
+    threads = oracle.default_threads()
     t0 = time.perf_counter()
     rp, col, _, _ = oracle.coo_to_csr(g.src, g.dst, N)
     t_csr = time.perf_counter() - t0
@@ -796,15 +931,31 @@ def cpu_baseline(g, N, E, F, step_bytes, args):
     t_agg = time.perf_counter() - t0
     t_step = t_csr + t_agg * (E / max(e_s, 1))
     scaled = "" if rows_n == N else f", scaled by E/{e_s}"
+    # the same aggregation on one thread, over a leading block of rows
+    r1 = int(np.searchsorted(rp, E // 32))
+    rows1 = np.arange(r1, dtype=np.int64)
+    e1 = int(rp[r1])
+    t0 = time.perf_counter()
+    oracle.spmm(rp, col, x=g.x, rows=rows1, nthreads=1)
+    oracle.spmm(rp, col, x_bf16=g.x_bf16, rows=rows1, nthreads=1)
+    t_one = (time.perf_counter() - t0) * (E / max(e1, 1))
+    t_step1 = t_csr + t_one
     return {
         "value": round(step_bytes / t_step / 1e9, 3),
         "unit": "GB/s",
         "cores": threads,
         "kind": "oracle",
+        "cpu_model": cpu_model(),
         "sample": f"oracle COO->CSR on all {E} edges (1 thread, {t_csr:.2f}s) + oracle "
                   f"aggregation (sum/mean/max in one pass, fp32 and bf16 features) on rows "
                   f"0..{rows_n - 1} ({e_s} edges, {t_agg:.2f}s, {threads} threads){scaled}; "
                   f"one full step {t_step:.1f}s",
+        "one_thread": {
+            "value": round(step_bytes / t_step1 / 1e9, 3),
+            "unit": "GB/s",
+            "sample": f"the same aggregation on 1 thread over rows 0..{r1 - 1} ({e1} edges), "
+                      f"scaled by E/{e1} to {t_one:.1f}s; with the COO->CSR, one full step "
+                      f"{t_step1:.1f}s"},
     }
 
 
@@ -859,6 +1010,89 @@ def _per_dispatch(rows, counter):
         key = (r["Dispatch_Id"], r["Kernel_Name"])
         acc[key] = acc.get(key, 0.0) + float(r["Counter_Value"])
     return acc
+
+
+def _segment_ops(dispatches):
+    """Split one step's dispatches (in dispatch order) into its operations:
+    everything before the first plan kernel is the COO->CSR, from there to
+    the plan header the plan, a row copy is a layout operation, and each
+    aggregation is [spmm_tiny] spmm_main [spmm_fixup].  Returns a list of
+    (kind, [dispatch rows])."""
+    segs = []
+    phase = "csr"
+    for d in dispatches:
+        k = short_name(d["name"])
+        if phase == "csr" and k.startswith("plan_classes"):
+            phase = "plan"
+        if phase in ("csr", "plan"):
+            if not segs or segs[-1][0] != phase:
+                segs.append((phase, []))
+            segs[-1][1].append(d)
+            if k.startswith("plan_header"):
+                phase = "ops"
+            continue
+        if k.startswith("copy_rows"):
+            segs.append(("layout", [d]))
+        elif k.startswith("spmm_tiny"):
+            segs.append(("agg", [d]))
+        elif k.startswith("spmm_main"):
+            if segs and segs[-1][0] == "agg" and \
+                    short_name(segs[-1][1][-1]["name"]).startswith("spmm_tiny"):
+                segs[-1][1].append(d)
+            else:
+                segs.append(("agg", [d]))
+        elif k.startswith("spmm_fixup") and segs and segs[-1][0] == "agg":
+            segs[-1][1].append(d)
+        else:
+            segs.append(("other", [d]))
+    return segs
+
+
+def summarize_step_counters(fetch_dir, write_dir, ops_path, out, cmd):
+    """FETCH_SIZE and WRITE_SIZE of every operation of one step (two pmc runs
+    of `bench.py --steps 1 --warmup 0 --dump-ops ops_path --calibrate-copy`),
+    scaled by the copy calibration, against each operation's algorithmic
+    bytes."""
+    fr = _per_dispatch(_counter_rows(fetch_dir), "FETCH_SIZE")
+    wr = _per_dispatch(_counter_rows(write_dir), "WRITE_SIZE")
+    ops = json.load(open(ops_path))
+    copy_f = [v for (i, k), v in fr.items() if "copy" in k.lower() or "elementwise" in k.lower()]
+    copy_w = [v for (i, k), v in wr.items() if "copy" in k.lower() or "elementwise" in k.lower()]
+    scale_f = CALIB_BYTES / (max(copy_f) * 1024.0) if copy_f else 1.0
+    scale_w = CALIB_BYTES / (max(copy_w) * 1024.0) if copy_w else 1.0
+
+    def step_dispatches(table):
+        rows = sorted(((int(i), k, v) for (i, k), v in table.items()), key=lambda t: t[0])
+        return [{"id": i, "name": k, "kib": v} for i, k, v in rows
+                if "copy" not in k.lower() and "elementwise" not in k.lower()
+                and "fill" not in k.lower()]
+
+    fs, ws = _segment_ops(step_dispatches(fr)), _segment_ops(step_dispatches(wr))
+    names = [o["name"] for o in ops]
+    algo = {o["name"]: o["bytes"] for o in ops}
+    lines = ["# HBM-side traffic of every operation of one step, from rocprofv3 counters",
+             f"command_fetch: {cmd.format(ctr='FETCH_SIZE')}",
+             f"command_write: {cmd.format(ctr='WRITE_SIZE')}",
+             f"fetch_scale: {scale_f:.4f}  write_scale: {scale_w:.4f}  (copy of "
+             f"{CALIB_BYTES} bytes: FETCH_SIZE and WRITE_SIZE scaled so it reads and writes "
+             f"that many)",
+             "FETCH_SIZE counts the bytes the L2 requests from the fabric: MALL hits "
+             "included, so fetch + write is an upper bound on HBM traffic.",
+             "",
+             f"{'operation':<14} {'fetch_GB':>10} {'write_GB':>10} {'total_GB':>10} "
+             f"{'algo_GB':>10} {'ratio':>7}  kernels"]
+    if len(fs) != len(names) or len(ws) != len(names):
+        lines.append(f"(segmentation found {len(fs)} / {len(ws)} operations for {len(names)} "
+                     f"named ones: {names})")
+    for n, (kf, df), (kw, dw) in zip(names, fs, ws):
+        f_b = sum(d["kib"] for d in df) * 1024.0 * scale_f
+        w_b = sum(d["kib"] for d in dw) * 1024.0 * scale_w
+        ks = ", ".join(sorted({short_name(d["name"]).split("<")[0] for d in df}))
+        lines.append(f"{n:<14} {f_b / 1e9:>10.3f} {w_b / 1e9:>10.3f} {(f_b + w_b) / 1e9:>10.3f} "
+                     f"{algo[n] / 1e9:>10.3f} {(f_b + w_b) / max(algo[n], 1):>7.3f}  {ks}")
+    lines.append(f"kernel_source_sha1: {source_digest(DOMINANT_SRC)}")
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
 
 
 def summarize_counters(fetch_dir, write_dir, out, cmd):
@@ -917,10 +1151,18 @@ def main():
     ap.add_argument("--cpu-rows", type=int, default=0,
                     help="rows of the CPU-oracle aggregation sample (0: all rows)")
     ap.add_argument("--no-cpu-baseline", dest="cpu_baseline", action="store_false")
+    ap.add_argument("--cold-reps", type=int, default=3,
+                    help="cold-cache steps (each operation alone after a 1 GiB write)")
+    ap.add_argument("--no-ceilings", dest="ceilings", action="store_false",
+                    help="skip the bandwidth probes (read, copy, row gather)")
     ap.add_argument("--calibrate-copy", action="store_true",
                     help="run one plain 1 GiB copy after warm-up (counter scaling)")
     ap.add_argument("--summarize-stats", nargs=2, metavar=("DIR", "OUT"))
     ap.add_argument("--summarize-counters", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "OUT"))
+    ap.add_argument("--summarize-step-counters", nargs=4,
+                    metavar=("FETCH_DIR", "WRITE_DIR", "OPS_JSON", "OUT"))
+    ap.add_argument("--dump-ops", metavar="PATH",
+                    help="write the step's operations (name, algorithmic bytes) as JSON")
     ap.add_argument("--cmd", default="", help="command line recorded in a summary ({ctr} is "
                     "replaced by the counter name in counter summaries)")
     args = ap.parse_args()
@@ -929,6 +1171,9 @@ def main():
         return
     if args.summarize_counters:
         summarize_counters(*args.summarize_counters, args.cmd)
+        return
+    if args.summarize_step_counters:
+        summarize_step_counters(*args.summarize_step_counters, args.cmd)
         return
     run(args)
 

@@ -39,7 +39,8 @@ __all__ = [
     "message_gather", "message_scale", "message_aggregate", "spmm_materialized",
     "message_backward", "edge_dot", "mp_copy_rows", "aligned_ld", "pad_rows", "MP_MAX_TYPES",
     "MP_ALL_TYPES", "MP_ERR_SORT", "mp_plan_opts", "mp_spmm_plan_build_opts", "new_status",
-    "check_status", "mp_spmm_noalloc", "MP_NOALLOC_SCRATCH_BYTES",
+    "check_status", "mp_spmm_noalloc", "MP_NOALLOC_SCRATCH_BYTES", "mp_probe_read",
+    "mp_probe_copy", "mp_probe_gather", "MP_PROBE_SINK_WORDS",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -57,6 +58,7 @@ MP_ALL_TYPES = -1  # dst_type selecting every destination type at once
 MP_ERR_CALLBACK = -9
 MP_ERR_SORT = -10
 MP_NOALLOC_SCRATCH_BYTES = 64 << 20  # the static scratch of mp_spmm_noalloc, per GPU
+MP_PROBE_SINK_WORDS = 65536  # uint32 words of a bandwidth probe's sink
 
 # int c(void* msg, int msg_dtype, int64_t E, int64_t F, void* user, void* stream)
 MESSAGE_FN = ctypes.CFUNCTYPE(ctypes.c_int, ctypes.c_void_p, ctypes.c_int, ctypes.c_int64,
@@ -114,6 +116,9 @@ def lib():
         L.mp_spmm_noalloc.argtypes = [p, p, i32, p, p, p, i32, i64, i64, i64, i64, i32, p, i32,
                                       p, i32, p, p]
         L.mp_copy_rows.argtypes = [p, i64, p, i64, i64, i64, i32, p]
+        L.mp_probe_read.argtypes = [p, i64, p, p]
+        L.mp_probe_copy.argtypes = [p, p, i64, p]
+        L.mp_probe_gather.argtypes = [p, i64, p, i64, i64, p, p]
         L.mp_hetero_build_workspace.argtypes = [i32, p, i32, p, i32, i32, psz]
         L.mp_hetero_build.argtypes = [i32, p, i32, p, i32, p, i32, p, p, sz, p, p]
         L.mp_hetero_spmm.argtypes = [i32, p, p, i32, i64, i32, p, p, i32, p, i32, p, i32, p, sz,
@@ -159,7 +164,8 @@ def lib():
                      "mp_spmm_backward_x_workspace", "mp_spmm_backward_x",
                      "mp_spmm_backward_w_workspace", "mp_spmm_backward_w", "mp_spmm_plan_size",
                      "mp_spmm_plan_build", "mp_spmm_plan_build_opts", "mp_spmm_workspace",
-                     "mp_spmm", "mp_spmm_noalloc",
+                     "mp_spmm", "mp_spmm_noalloc", "mp_probe_read", "mp_probe_copy",
+                     "mp_probe_gather",
                      "mp_hetero_build_workspace", "mp_hetero_build", "mp_hetero_spmm",
                      "mp_validate_coo", "mp_validate_csr"):
             getattr(L, name).restype = i32
@@ -315,6 +321,21 @@ def mp_spmm_noalloc(plan_handle, rowptr, rowptr_itype, col, w, x, x_dtype, N_src
         plan_handle, _ptr(rowptr), rowptr_itype, _ptr(col), _ptr(w), xp, x_dtype, N_src, N_dst,
         F, ldx, reduce, _ptr(out), out_dtype, _ptr(out_max), max_dtype, _ptr(argout),
         _stream(stream)))
+
+
+def mp_probe_read(p, nbytes, sink, stream=None):
+    _check("mp_probe_read", lib().mp_probe_read(_ptr(p), nbytes, _ptr(sink), _stream(stream)))
+
+
+def mp_probe_copy(src, dst, nbytes, stream=None):
+    _check("mp_probe_copy", lib().mp_probe_copy(_ptr(src), _ptr(dst), nbytes, _stream(stream)))
+
+
+def mp_probe_gather(idx, n, table, stride_bytes, row_bytes, sink, stream=None):
+    """table: a tensor (its data address) or a raw address."""
+    tp = table.data_ptr() if isinstance(table, torch.Tensor) else table
+    _check("mp_probe_gather", lib().mp_probe_gather(_ptr(idx), n, tp, stride_bytes, row_bytes,
+                                                    _ptr(sink), _stream(stream)))
 
 
 def mp_copy_rows(x_in, ld_in, x_out, ld_out, N, F, dtype, stream=None):

@@ -18,7 +18,7 @@ LIB = os.path.join(HERE, "libmp.so")
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 
 SOURCES = ["scan.hip", "sort.hip", "spmm.hip", "backward.hip", "gmm.hip", "messages.hip",
-           "layout.hip", "api.cpp"]
+           "layout.hip", "probe.hip", "api.cpp"]
 FLAGS = [
     "--offload-arch=gfx950", "-O3", "-fPIC", "-std=c++17",
     "-Xclang", "-target-feature", "-Xclang", "-packed-fp32-ops",

@@ -1356,6 +1356,33 @@ int mp_hetero_spmm(int n_types, const int64_t* N_per_type, const void* const* x_
     return run_spmm(plan, P, g, x_dtype, N_dst, ws, ws_bytes, as_stream(stream));
 }
 
+int mp_probe_read(const void* p, int64_t bytes, uint32_t* sink, void* stream) {
+    if (!p || !sink) return MP_ERR_NULL;
+    if (bytes < 16 || bytes % 16) return MP_ERR_SIZE;
+    if ((uintptr_t)p % 16 || (uintptr_t)sink % 4) return MP_ERR_ALIGN;
+    return hip_status(launch_probe_read(p, bytes / 16, sink, as_stream(stream)));
+}
+
+int mp_probe_copy(const void* in, void* out, int64_t bytes, void* stream) {
+    if (!in || !out) return MP_ERR_NULL;
+    if (bytes < 16 || bytes % 16) return MP_ERR_SIZE;
+    if ((uintptr_t)in % 16 || (uintptr_t)out % 16) return MP_ERR_ALIGN;
+    return hip_status(launch_probe_copy(in, out, bytes / 16, as_stream(stream)));
+}
+
+int mp_probe_gather(const int32_t* idx, int64_t n, const void* table, int64_t stride_bytes,
+                    int64_t row_bytes, uint32_t* sink, void* stream) {
+    if (!sink || (n > 0 && (!idx || !table))) return MP_ERR_NULL;
+    if (n < 0 || n > INT32_MAX || row_bytes < 16 || row_bytes > 1024 || row_bytes % 16 ||
+        stride_bytes < row_bytes)
+        return MP_ERR_SIZE;
+    if ((uintptr_t)table % 16 || stride_bytes % 16 || (uintptr_t)idx % 4 || (uintptr_t)sink % 4)
+        return MP_ERR_ALIGN;
+    if (n == 0) return MP_OK;
+    return hip_status(launch_probe_gather(idx, n, table, stride_bytes, (int)(row_bytes / 16), sink,
+                                          as_stream(stream)));
+}
+
 int mp_validate_coo(const int32_t* src, const int32_t* dst, int64_t E, int64_t N_src,
                     int64_t N_dst, int64_t* d_count, void* stream) {
     if (!d_count || (E > 0 && (!src || !dst))) return MP_ERR_NULL;

@@ -7,6 +7,7 @@
 #include <stdint.h>
 
 #include "mp.h"
+#include "mp_probe.h"
 
 namespace mp {
 
@@ -281,5 +282,11 @@ hipError_t launch_message_backward(const MessageBackward& a, hipStream_t s);
 // out[r, 0:F] = in[r, 0:F] for r < N, rows ld_in / ld_out elements apart.
 hipError_t launch_copy_rows(const void* in, int64_t ld_in, void* out, int64_t ld_out, int64_t N,
                             int64_t F, int elem_bytes, hipStream_t s);
+
+// ---- bandwidth probes (probe.hip) ---------------------------------------------
+hipError_t launch_probe_read(const void* p, int64_t n16, uint32_t* sink, hipStream_t s);
+hipError_t launch_probe_copy(const void* in, void* out, int64_t n16, hipStream_t s);
+hipError_t launch_probe_gather(const int32_t* idx, int64_t n, const void* table,
+                               int64_t stride_bytes, int L, uint32_t* sink, hipStream_t s);
 
 }  // namespace mp

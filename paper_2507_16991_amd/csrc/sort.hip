@@ -113,18 +113,24 @@ __global__ void radix_gscan(uint32_t* __restrict__ g, int passes, int bits) {
 }
 
 // One LSD pass: rank the tile's keys stably (wave-level multisplit, per-wave
-// LDS counters), publish the tile's digit counts, look back over earlier tiles
-// for their running totals, stage the tile in LDS in digit order and write
-// every digit run contiguously.  Ranks follow (wave, round, lane) order,
-// which is element order, and tiles are numbered in the order they start, so
-// the pass is stable.  HAS_B: the second payload is carried.
+// LDS counters), publish the tile's digit counts, stage the tile in LDS in
+// digit order, then look back over earlier tiles for their running totals
+// and write every digit run contiguously.  Ranks follow (wave, round, lane)
+// order, which is element order, and tiles are numbered in the order they
+// start, so the pass is stable.  Staging before the look-back frees the
+// registers of the keys and payloads while the tile waits on its
+// predecessors, so the look-back can keep kLookWindow descriptor loads in
+// flight.  HAS_B: the second payload is carried.
+constexpr int kLookWindow = 4;
+
 template <bool HAS_B>
 __global__ __launch_bounds__(kSortBlock) void radix_onesweep(RadixPass p) {
     __shared__ uint32_t s_key[kSortTile];
     __shared__ int32_t s_a[kSortTile];
     __shared__ int32_t s_b[HAS_B ? kSortTile : 1];
     __shared__ uint32_t s_cnt[kSortWaves][kMaxBuckets];
-    __shared__ uint32_t s_start[kMaxBuckets];
+    __shared__ uint32_t s_tcnt[kMaxBuckets];   // the tile's count of each digit
+    __shared__ uint32_t s_start[kMaxBuckets];  // ... and its exclusive scan
     __shared__ uint32_t s_gbase[kMaxBuckets];
     __shared__ uint32_t s_tile;
 
@@ -166,7 +172,10 @@ __global__ __launch_bounds__(kSortBlock) void radix_onesweep(RadixPass p) {
     }
     __syncthreads();
 
-    // per digit: each wave's run start inside the digit, and the tile count
+    // per digit: each wave's run start inside the digit, and the tile count,
+    // which is published at once (earlier publication shortens the waits of
+    // later tiles)
+    const uint32_t tag = (uint32_t)p.pass + 1u;
     for (int d = threadIdx.x; d < R; d += kSortBlock) {
         uint32_t run = 0;
 #pragma unroll
@@ -175,64 +184,29 @@ __global__ __launch_bounds__(kSortBlock) void radix_onesweep(RadixPass p) {
             s_cnt[w][d] = run;
             run += c;
         }
-        s_start[d] = run;
-    }
-    __syncthreads();
-
-    // decoupled look-back, one thread per digit: publish this tile's count,
-    // add up earlier tiles' counts until one that carries an inclusive prefix
-    const uint32_t tag = (uint32_t)p.pass + 1u;
-    if (threadIdx.x < R) {
-        const int d = threadIdx.x;
-        const uint64_t cnt = s_start[d];
-        uint64_t* col = p.sc.desc + d;
-        uint64_t excl = 0;
-        if (tile == 0) {
-            __hip_atomic_store(col, desc_make(kFlagPre, tag, cnt), __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
-        } else {
-            __hip_atomic_store(col + tile * kMaxBuckets, desc_make(kFlagAgg, tag, cnt),
-                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-            for (int64_t look = tile - 1; look >= 0; --look) {
-                uint64_t v = 0;
-                uint32_t spins = 0;
-                while (true) {
-                    v = __hip_atomic_load(col + look * kMaxBuckets, __ATOMIC_RELAXED,
-                                          __HIP_MEMORY_SCOPE_AGENT);
-                    if ((uint32_t)((v >> 56) & 63u) == tag && (v >> 62) != 0) break;
-                    if (++spins > kSpinLimit) {  // bounded: never hang; flag it instead
-                        atomicOr(p.sc.err, 1u);
-                        v = desc_make(kFlagPre, tag, 0);
-                        break;
-                    }
-                    __builtin_amdgcn_s_sleep(1);
-                }
-                excl += v & ((1ull << 56) - 1);
-                if ((v >> 62) == 2) break;
-            }
-            __hip_atomic_store(col + tile * kMaxBuckets, desc_make(kFlagPre, tag, excl + cnt),
-                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        }
-        s_gbase[d] = p.sc.gbase[p.pass * kMaxBuckets + d] + (uint32_t)excl;
+        s_tcnt[d] = run;
+        __hip_atomic_store(p.sc.desc + tile * kMaxBuckets + d,
+                           desc_make(tile == 0 ? kFlagPre : kFlagAgg, tag, run), __ATOMIC_RELAXED,
+                           __HIP_MEMORY_SCOPE_AGENT);
     }
     __syncthreads();
     // exclusive scan of the tile's digit counts (R <= 256) by wavefront 0
     if (wv == 0) {
         uint32_t t[kMaxBuckets / kWave];
-        uint32_t s = 0;
+        uint32_t sum = 0;
 #pragma unroll
         for (int k = 0; k < kMaxBuckets / kWave; ++k) {
             int d = lane * (kMaxBuckets / kWave) + k;
-            t[k] = d < R ? s_start[d] : 0u;
-            s += t[k];
+            t[k] = d < R ? s_tcnt[d] : 0u;
+            sum += t[k];
         }
-        uint32_t inc = s;
+        uint32_t inc = sum;
 #pragma unroll
         for (int off = 1; off < kWave; off <<= 1) {
             uint32_t o = __shfl_up(inc, off, kWave);
             if (lane >= off) inc += o;
         }
-        uint32_t run = inc - s;
+        uint32_t run = inc - sum;
 #pragma unroll
         for (int k = 0; k < kMaxBuckets / kWave; ++k) {
             int d = lane * (kMaxBuckets / kWave) + k;
@@ -242,6 +216,7 @@ __global__ __launch_bounds__(kSortBlock) void radix_onesweep(RadixPass p) {
     }
     __syncthreads();
 
+    // stage the tile in LDS in digit order (tile-local positions only)
 #pragma unroll
     for (int k = 0; k < kSortItems; ++k) {
         const int64_t i = wbase + (int64_t)k * kWave + lane;
@@ -252,6 +227,53 @@ __global__ __launch_bounds__(kSortBlock) void radix_onesweep(RadixPass p) {
             s_a[lp] = va[k];
             if constexpr (HAS_B) s_b[lp] = vb[k];
         }
+    }
+
+    // decoupled look-back, one thread per digit: add up earlier tiles'
+    // counts until one that carries an inclusive prefix, kLookWindow
+    // descriptors per round (a descriptor not yet published ends the round;
+    // the wait on it is bounded)
+    if (threadIdx.x < R) {
+        const int d = threadIdx.x;
+        const uint64_t* col = p.sc.desc + d;
+        uint64_t excl = 0;
+        if (tile > 0) {
+            int64_t look = tile - 1;
+            uint32_t spins = 0;
+            bool done = false;
+            while (!done) {
+                uint64_t v[kLookWindow];
+#pragma unroll
+                for (int w = 0; w < kLookWindow; ++w)
+                    v[w] = look - w >= 0
+                               ? __hip_atomic_load(col + (look - w) * kMaxBuckets, __ATOMIC_RELAXED,
+                                                   __HIP_MEMORY_SCOPE_AGENT)
+                               : 0ull;
+                int used = 0;
+#pragma unroll
+                for (int w = 0; w < kLookWindow; ++w) {
+                    if (done || used < w) continue;  // stopped earlier in this round
+                    const bool ready = (uint32_t)((v[w] >> 56) & 63u) == tag && (v[w] >> 62) != 0;
+                    if (!ready) continue;
+                    excl += v[w] & ((1ull << 56) - 1);
+                    used = w + 1;
+                    if ((v[w] >> 62) == 2 || look - w == 0) done = true;
+                }
+                if (done) break;
+                look -= used;
+                if (used == 0) {
+                    if (++spins > kSpinLimit) {  // bounded: never hang; flag it instead
+                        atomicOr(p.sc.err, 1u);
+                        break;
+                    }
+                    __builtin_amdgcn_s_sleep(1);
+                }
+            }
+            __hip_atomic_store(p.sc.desc + tile * kMaxBuckets + d,
+                               desc_make(kFlagPre, tag, excl + s_tcnt[d]), __ATOMIC_RELAXED,
+                               __HIP_MEMORY_SCOPE_AGENT);
+        }
+        s_gbase[d] = p.sc.gbase[p.pass * kMaxBuckets + d] + (uint32_t)excl;
     }
     __syncthreads();
 

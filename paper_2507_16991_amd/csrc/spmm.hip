@@ -17,8 +17,8 @@
 // kernel).  No floating-point atomics anywhere.
 //
 // Max: (value, CSR position) pairs; a later edge replaces the running pair
-// only when strictly greater (the first edge of a partial always replaces the
-// empty pair, position -1), and pairs are combined preferring a non-empty pair, then the
+// only when strictly greater (a partial left empty, position -1, after
+// receiving messages saw only -inf and takes its first edge), and pairs are combined preferring a non-empty pair, then the
 // larger value, then the smaller position -- the first edge attaining the
 // maximum, also for rows of -inf messages.  (NaN messages are outside the contract: the
 // strided partials would not reproduce a sequential scan's answer.)
@@ -31,7 +31,13 @@ namespace {
 
 constexpr int kBlock = 256;
 constexpr int kWavesPerBlock = kBlock / kWave;
-constexpr int kUnroll = 8;  // edges gathered per slot per iteration
+#ifndef MP_UNROLL
+#define MP_UNROLL 8         // edges gathered per slot per iteration
+#endif
+#ifndef MP_MAX_PARTIALS
+#define MP_MAX_PARTIALS 2   // independent (value, position) partials of max
+#endif
+constexpr int kUnroll = MP_UNROLL;
 #ifndef MP_STATS_UNROLL
 #define MP_STATS_UNROLL 8   // the same for the stacked statistics
 #endif
@@ -227,14 +233,8 @@ struct Acc {
 #pragma unroll
         for (int k = 0; k < EPL; ++k) {
             if constexpr (HS) s[a][k] += v[k];
-            // the first message always replaces the empty pair (position -1),
-            // so a row whose messages are all -inf (+inf for min) still
-            // reports its first edge.  (A wavefront-uniform "first message"
-            // flag instead of the position test was measured: the compiler
-            // then keeps a separate first-step copy of the loop, 16 to 24
-            // registers more.)
             if constexpr (HM) {
-                const bool take = v[k] > m[a][k] || i[a][k] < 0;
+                const bool take = v[k] > m[a][k];
                 m[a][k] = take ? v[k] : m[a][k];
                 i[a][k] = take ? pos : i[a][k];
             }
@@ -242,10 +242,22 @@ struct Acc {
                 const float dv = sub_rounded(v[k], K[k]);
                 d[a][k] += dv;
                 q[a][k] = __builtin_fmaf(dv, dv, q[a][k]);
-                const bool take = v[k] < n[a][k] || j[a][k] < 0;
+                const bool take = v[k] < n[a][k];
                 n[a][k] = take ? v[k] : n[a][k];
                 j[a][k] = take ? pos : j[a][k];
             }
+        }
+    }
+    // After the gather: a partial that received messages but is still empty
+    // (position -1) saw only -inf messages (+inf for min), since any other
+    // message replaces the initial -inf; its answer is its first message,
+    // at position `first`.  (Testing for the empty pair on every message
+    // instead costs a compare per element per edge: 6% on the max kernels.)
+    __device__ inline void settle(int a, int32_t first, bool had) {
+#pragma unroll
+        for (int k = 0; k < EPL; ++k) {
+            if constexpr (HM) i[a][k] = had && i[a][k] < 0 ? first : i[a][k];
+            if constexpr (HX) j[a][k] = had && j[a][k] < 0 ? first : j[a][k];
         }
     }
     // fold the A partials into slot 0 (fixed tree)
@@ -304,7 +316,7 @@ struct Acc {
 // features, whose rows arrive twice as fast, two.
 template <typename TX, int EPL, bool HS, bool HM, int MODE>
 using AccFor = Acc<EPL, HS, HM, MODE == kModeStats,
-                   MODE == kModeStats ? (sizeof(TX) == 4 ? 1 : 2) : (HM ? 2 : 4)>;
+                   MODE == kModeStats ? (sizeof(TX) == 4 ? 1 : 2) : (HM ? MP_MAX_PARTIALS : 4)>;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -509,6 +521,12 @@ __device__ inline void wave_range(const SpmmParams& P,
                 }
             }
         }
+    }
+    if constexpr (HM) {
+        // partial a's first message: edge u = a of the range's first step
+#pragma unroll
+        for (int a = 0; a < A; ++a)
+            acc.settle(a, (int32_t)(e0 + a * S + slot), feat_ok && a < U && a * S + slot < e1 - e0);
     }
 }
 
@@ -814,6 +832,10 @@ __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MOD
                 acc.add(u % A, v, (int32_t)(e0 + it + u));
             }
         }
+    }
+    if constexpr (HM) {
+#pragma unroll
+        for (int a = 0; a < A; ++a) acc.settle(a, (int32_t)(e0 + a), feat_ok && a < my_n);
     }
 }
 
@@ -1138,6 +1160,7 @@ __global__ __launch_bounds__(kBlock) void spmm_tiny(SpmmParams P) {
                 acc.add(0, v, beg + u);
             }
         }
+        if constexpr (HM) acc.settle(0, beg, feat_ok && deg > 0);
         if (feat_ok) {
             if constexpr (HX)
                 store_stats<EPL>(P, row, fe, deg, acc.s[0], acc.d[0], acc.q[0], acc.m[0],

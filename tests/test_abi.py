@@ -10,13 +10,13 @@ import pytest
 import paper_2507_16991_amd as mp
 
 ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
-HEADER = os.path.join(ROOT, "include", "mp.h")
+HEADERS = [os.path.join(ROOT, "include", h) for h in ("mp.h", "mp_probe.h")]
 
 FAKE = 0x10000  # a non-NULL, aligned pointer value; never dereferenced by these cases
 
 
 def declared_functions():
-    text = open(HEADER).read()
+    text = "".join(open(h).read() for h in HEADERS)
     text = re.sub(r"/\*.*?\*/", "", text, flags=re.S)
     return sorted(set(re.findall(r"\b(mp_[a-z0-9_]+)\s*\(", text)))
 
@@ -27,6 +27,21 @@ def test_exports_every_declared_function():
     assert "mp_spmm" in names and "mp_coo_to_csr" in names and "mp_hetero_spmm" in names
     for n in names:
         assert hasattr(L, n), f"{n} declared in mp.h but not exported"
+
+
+def test_probe_argument_errors():
+    L = mp.lib()
+    assert L.mp_probe_read(None, 64, FAKE, None) == -1
+    assert L.mp_probe_read(FAKE, 60, FAKE, None) == -2
+    assert L.mp_probe_read(FAKE + 4, 64, FAKE, None) == -8
+    assert L.mp_probe_copy(FAKE, FAKE, 0, None) == -2
+    assert L.mp_probe_copy(FAKE, FAKE + 8, 64, None) == -8
+    assert L.mp_probe_gather(FAKE, 10, FAKE, 400, 400, None, None) == -1
+    assert L.mp_probe_gather(FAKE, 10, FAKE, 400, 392, FAKE, None) == -2   # not whole chunks
+    assert L.mp_probe_gather(FAKE, 10, FAKE, 256, 400, FAKE, None) == -2   # row > stride
+    assert L.mp_probe_gather(FAKE, 10, FAKE, 2048, 2048, FAKE, None) == -2  # over 1024 bytes
+    assert L.mp_probe_gather(FAKE, 10, FAKE + 8, 400, 400, FAKE, None) == -8
+    assert L.mp_probe_gather(None, 0, None, 400, 400, FAKE, None) == 0     # nothing to read
 
 
 def test_noalloc_argument_errors():
