@@ -23,7 +23,7 @@ constexpr int kWave = 64;
 constexpr int kSortBlock = MP_SORT_BLOCK;          // threads per workgroup
 constexpr int kSortItems = MP_SORT_ITEMS;          // keys per thread
 constexpr int kSortTile = kSortBlock * kSortItems; // keys per workgroup
-constexpr int kSortMaxBits = 8;                    // digit width cap (256 buckets)
+constexpr int kSortMaxBits = 9;                    // digit width cap (512 buckets)
 
 inline int64_t ceil_div(int64_t a, int64_t b) { return (a + b - 1) / b; }
 inline size_t align_up(size_t v, size_t a) { return (v + a - 1) / a * a; }
@@ -55,11 +55,11 @@ hipError_t exclusive_scan_u32(uint32_t* data, int64_t n, void* ws, hipStream_t s
 // read of the keys (and clears the look-back descriptors); then each
 // radix_sort_pass() ranks, offsets and scatters in a single kernel, getting
 // the offsets of earlier tiles by decoupled look-back.
-constexpr int kMaxPasses = 4;  // 32-bit keys, digits of at most 8 bits
+constexpr int kMaxPasses = 4;  // keys of at most 31 bits, digits of at most 9 bits
 
 struct RadixScratch {
-    uint64_t* desc;     // [tiles * 256] look-back descriptors
-    uint32_t* gbase;    // [kMaxPasses * 256] global digit histogram -> exclusive starts
+    uint64_t* desc;     // [tiles * R] look-back descriptors (R = 2^bits <= 512)
+    uint32_t* gbase;    // [kMaxPasses * 512] global digit histogram -> exclusive starts
     uint32_t* counter;  // [kMaxPasses] dynamic tile ids
     uint32_t* err;      // nonzero: a look-back wait gave up (the result is invalid)
 };

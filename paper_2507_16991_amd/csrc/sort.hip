@@ -56,7 +56,7 @@ __global__ __launch_bounds__(256) void radix_clear(uint64_t* __restrict__ desc, 
                                                    uint32_t* __restrict__ err) {
     const int64_t i0 = (int64_t)blockIdx.x * 256 + threadIdx.x;
     for (int64_t i = i0; i < ndesc; i += (int64_t)gridDim.x * 256) desc[i] = 0;
-    if (i0 < kMaxPasses * 256) gbase[i0] = 0;
+    if (i0 < kMaxPasses * kMaxBuckets) gbase[i0] = 0;
     if (i0 < kMaxPasses) counter[i0] = 0;
     if (i0 == 0) *err = 0;
 }
@@ -118,30 +118,39 @@ __global__ void radix_gscan(uint32_t* __restrict__ g, int passes, int bits) {
 // and write every digit run contiguously.  Ranks follow (wave, round, lane)
 // order, which is element order, and tiles are numbered in the order they
 // start, so the pass is stable.  Staging before the look-back frees the
-// registers of the keys and payloads while the tile waits on its
-// predecessors, so the look-back can keep kLookWindow descriptor loads in
-// flight.  HAS_B: the second payload is carried.
+// registers of the keys while the tile waits on its predecessors, so the
+// look-back can keep kLookWindow descriptor loads in flight.  Descriptors of
+// a pass over R = 2^bits digits lie R apart per tile.
+//   HAS_B: the second payload is carried.
+//   WIDE:  digits of up to 9 bits (512 buckets).  Their per-wave counters take
+//          twice the LDS, so the keys and the payloads go through ONE staging
+//          buffer in turn (keys staged before the look-back, each payload
+//          after the previous array is written), which keeps two tiles per CU.
+//          Narrow passes (up to 8 bits) stage all arrays at once.
 constexpr int kLookWindow = 4;
 
-template <bool HAS_B>
-__global__ __launch_bounds__(kSortBlock) void radix_onesweep(RadixPass p) {
-    __shared__ uint32_t s_key[kSortTile];
-    __shared__ int32_t s_a[kSortTile];
-    __shared__ int32_t s_b[HAS_B ? kSortTile : 1];
-    __shared__ uint32_t s_cnt[kSortWaves][kMaxBuckets];
-    __shared__ uint32_t s_tcnt[kMaxBuckets];   // the tile's count of each digit
-    __shared__ uint32_t s_start[kMaxBuckets];  // ... and its exclusive scan
-    __shared__ uint32_t s_gbase[kMaxBuckets];
+template <bool HAS_B, bool WIDE>
+__global__ __launch_bounds__(kSortBlock)
+__attribute__((amdgpu_waves_per_eu(HAS_B ? 1 : 2 * kSortBlock / 256)))  // two tiles per CU
+void radix_onesweep(RadixPass p) {
+    constexpr int NB = WIDE ? kMaxBuckets : kMaxBuckets / 2;  // buckets this variant handles
+    constexpr int NSTAGE = WIDE ? 1 : (HAS_B ? 3 : 2);         // staging arrays
+    __shared__ uint32_t s_stage[NSTAGE][kSortTile];
+    __shared__ uint16_t s_lp[WIDE ? kSortTile : 1];  // WIDE: staged slot of every key
+    __shared__ uint32_t s_cnt[kSortWaves][NB];
+    __shared__ uint32_t s_tcnt[NB];   // the tile's count of each digit
+    __shared__ uint32_t s_start[NB];  // ... and its exclusive scan
+    __shared__ uint32_t s_gbase[NB];
     __shared__ uint32_t s_tile;
 
     const int R = 1 << p.bits;
     const int lane = threadIdx.x & (kWave - 1);
     const int wv = threadIdx.x / kWave;
-    for (int i = threadIdx.x; i < kSortWaves * kMaxBuckets; i += kSortBlock)
-        (&s_cnt[0][0])[i] = 0;
+    for (int i = threadIdx.x; i < kSortWaves * NB; i += kSortBlock) (&s_cnt[0][0])[i] = 0;
     if (threadIdx.x == 0) s_tile = atomicAdd(&p.sc.counter[p.pass], 1u);
     __syncthreads();
     const int64_t tile = s_tile;
+    uint64_t* const desc = p.sc.desc + tile * R;
 
     const int64_t tbase = tile * kSortTile;
     const int64_t wbase = tbase + (int64_t)wv * kWaveKeys;
@@ -185,18 +194,18 @@ __global__ __launch_bounds__(kSortBlock) void radix_onesweep(RadixPass p) {
             run += c;
         }
         s_tcnt[d] = run;
-        __hip_atomic_store(p.sc.desc + tile * kMaxBuckets + d,
-                           desc_make(tile == 0 ? kFlagPre : kFlagAgg, tag, run), __ATOMIC_RELAXED,
-                           __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_store(desc + d, desc_make(tile == 0 ? kFlagPre : kFlagAgg, tag, run),
+                           __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     }
     __syncthreads();
-    // exclusive scan of the tile's digit counts (R <= 256) by wavefront 0
+    // exclusive scan of the tile's digit counts (R <= NB) by wavefront 0
     if (wv == 0) {
-        uint32_t t[kMaxBuckets / kWave];
+        constexpr int PER = NB / kWave;
+        uint32_t t[PER];
         uint32_t sum = 0;
 #pragma unroll
-        for (int k = 0; k < kMaxBuckets / kWave; ++k) {
-            int d = lane * (kMaxBuckets / kWave) + k;
+        for (int k = 0; k < PER; ++k) {
+            int d = lane * PER + k;
             t[k] = d < R ? s_tcnt[d] : 0u;
             sum += t[k];
         }
@@ -208,24 +217,30 @@ __global__ __launch_bounds__(kSortBlock) void radix_onesweep(RadixPass p) {
         }
         uint32_t run = inc - sum;
 #pragma unroll
-        for (int k = 0; k < kMaxBuckets / kWave; ++k) {
-            int d = lane * (kMaxBuckets / kWave) + k;
+        for (int k = 0; k < PER; ++k) {
+            int d = lane * PER + k;
             if (d < R) s_start[d] = run;
             run += t[k];
         }
     }
     __syncthreads();
 
-    // stage the tile in LDS in digit order (tile-local positions only)
+    // stage the tile in LDS in digit order (tile-local positions only): all
+    // arrays, or for WIDE passes the keys alone (each key's slot is kept in
+    // LDS for the payloads)
 #pragma unroll
     for (int k = 0; k < kSortItems; ++k) {
         const int64_t i = wbase + (int64_t)k * kWave + lane;
+        const uint32_t d = (key[k] >> p.shift) & (uint32_t)(R - 1);
+        const uint32_t lp = s_start[d] + s_cnt[wv][d] + rank[k];
         if (i < p.n) {
-            const uint32_t d = (key[k] >> p.shift) & (uint32_t)(R - 1);
-            const uint32_t lp = s_start[d] + s_cnt[wv][d] + rank[k];
-            s_key[lp] = key[k];
-            s_a[lp] = va[k];
-            if constexpr (HAS_B) s_b[lp] = vb[k];
+            s_stage[0][lp] = key[k];
+            if constexpr (WIDE) {
+                s_lp[k * kSortBlock + threadIdx.x] = (uint16_t)lp;
+            } else {
+                s_stage[1][lp] = (uint32_t)va[k];
+                if constexpr (HAS_B) s_stage[2][lp] = (uint32_t)vb[k];
+            }
         }
     }
 
@@ -246,7 +261,7 @@ __global__ __launch_bounds__(kSortBlock) void radix_onesweep(RadixPass p) {
 #pragma unroll
                 for (int w = 0; w < kLookWindow; ++w)
                     v[w] = look - w >= 0
-                               ? __hip_atomic_load(col + (look - w) * kMaxBuckets, __ATOMIC_RELAXED,
+                               ? __hip_atomic_load(col + (look - w) * R, __ATOMIC_RELAXED,
                                                    __HIP_MEMORY_SCOPE_AGENT)
                                : 0ull;
                 int used = 0;
@@ -269,24 +284,53 @@ __global__ __launch_bounds__(kSortBlock) void radix_onesweep(RadixPass p) {
                     __builtin_amdgcn_s_sleep(1);
                 }
             }
-            __hip_atomic_store(p.sc.desc + tile * kMaxBuckets + d,
-                               desc_make(kFlagPre, tag, excl + s_tcnt[d]), __ATOMIC_RELAXED,
-                               __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_store(desc + d, desc_make(kFlagPre, tag, excl + s_tcnt[d]),
+                               __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         }
         s_gbase[d] = p.sc.gbase[p.pass * kMaxBuckets + d] + (uint32_t)excl;
     }
     __syncthreads();
 
+    // write the digit runs: thread t takes staged slots t, t + kSortBlock, ...
     const int64_t nvalid = (p.n - tbase) < kSortTile ? (p.n - tbase) : kSortTile;
-    for (int i = threadIdx.x; i < nvalid; i += kSortBlock) {
-        const uint32_t kk = s_key[i];
-        const uint32_t d = (kk >> p.shift) & (uint32_t)(R - 1);
-        const int64_t pos = (int64_t)s_gbase[d] + (i - (int64_t)s_start[d]);
-        if (pos >= p.n) continue;  // cannot happen for consistent counts; never write past n
-        if (p.keys_out) p.keys_out[pos] = kk;
-        if (p.a_out) p.a_out[pos] = s_a[i];
-        if constexpr (HAS_B) {
-            if (p.b_out) p.b_out[pos] = s_b[i];
+    int32_t pos[WIDE ? kSortItems : 1];
+#pragma unroll
+    for (int k = 0; k < kSortItems; ++k) {
+        const int i = (int)threadIdx.x + k * kSortBlock;
+        if constexpr (WIDE) pos[k] = -1;
+        if (i < nvalid) {
+            const uint32_t kk = s_stage[0][i];
+            const uint32_t d = (kk >> p.shift) & (uint32_t)(R - 1);
+            const int64_t q = (int64_t)s_gbase[d] + (i - (int64_t)s_start[d]);
+            if (q < p.n) {  // cannot fail for consistent counts; never write past n
+                if constexpr (WIDE) pos[k] = (int32_t)q;
+                if (p.keys_out) p.keys_out[q] = kk;
+                if constexpr (!WIDE) {
+                    if (p.a_out) p.a_out[q] = (int32_t)s_stage[1][i];
+                    if constexpr (HAS_B) {
+                        if (p.b_out) p.b_out[q] = (int32_t)s_stage[2][i];
+                    }
+                }
+            }
+        }
+    }
+    if constexpr (WIDE) {
+        // the payloads, one at a time through the same buffer
+        for (int which = 0; which < (HAS_B ? 2 : 1); ++which) {
+            int32_t* out = which == 0 ? p.a_out : p.b_out;
+            __syncthreads();  // every read of the buffer's previous contents is done
+#pragma unroll
+            for (int k = 0; k < kSortItems; ++k) {
+                const int64_t i = wbase + (int64_t)k * kWave + lane;
+                if (i < p.n)
+                    s_stage[0][s_lp[k * kSortBlock + threadIdx.x]] =
+                        (uint32_t)(which == 0 ? va[k] : vb[k]);
+            }
+            __syncthreads();
+            if (!out) continue;
+#pragma unroll
+            for (int k = 0; k < kSortItems; ++k)
+                if (pos[k] >= 0) out[pos[k]] = (int32_t)s_stage[0][threadIdx.x + k * kSortBlock];
         }
     }
 }
@@ -429,7 +473,7 @@ hipError_t radix_sort_begin(const uint32_t* keys, int64_t n, int passes, int bit
                             const RadixScratch& sc, hipStream_t s) {
     if (n <= 0) return hipSuccess;
     const int64_t tiles = ceil_div(n, kSortTile);
-    const int64_t ndesc = tiles * kMaxBuckets;
+    const int64_t ndesc = tiles * ((int64_t)1 << bits);  // R descriptors per tile
     unsigned g = grid_for(ndesc, 256);
     if (g > 8192) g = 8192;
     // every histogram word needs a thread, however few descriptors there are
@@ -448,10 +492,18 @@ hipError_t radix_sort_begin(const uint32_t* keys, int64_t n, int passes, int bit
 hipError_t radix_sort_pass(const RadixPass& p, hipStream_t s) {
     if (p.n <= 0) return hipSuccess;
     const int64_t tiles = ceil_div(p.n, kSortTile);
-    if (p.b_out)
-        hipLaunchKernelGGL(radix_onesweep<true>, dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p);
-    else
-        hipLaunchKernelGGL(radix_onesweep<false>, dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p);
+    const bool wide = p.bits > kSortMaxBits - 1;
+    if (p.b_out) {
+        if (wide)
+            hipLaunchKernelGGL((radix_onesweep<true, true>), dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p);
+        else
+            hipLaunchKernelGGL((radix_onesweep<true, false>), dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p);
+    } else {
+        if (wide)
+            hipLaunchKernelGGL((radix_onesweep<false, true>), dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p);
+        else
+            hipLaunchKernelGGL((radix_onesweep<false, false>), dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p);
+    }
     return hipGetLastError();
 }
 

@@ -347,3 +347,37 @@ def test_backward_chunglu_full_sampled():
         print(f"[note] grad_w {reduce} error {e:.3g}", file=sys.stderr, flush=True)
         assert e <= TOL[torch.float32]
         del gw
+
+
+@pytest.mark.parametrize("reduce", ["sum", "mean"])
+@pytest.mark.parametrize("weighted", [False, True])
+@pytest.mark.parametrize("use_plan", [False, True])
+def test_undirected_forward_csr_as_transpose(reduce, weighted, use_plan):
+    """An undirected graph (every edge in both directions) with symmetric
+    weights: the forward CSR lists, for each node, the same neighbours and
+    weights as its transpose, so dL/dx of sum and mean may be taken over the
+    forward CSR itself (posT NULL), skipping the second CSR, as include/mp.h
+    documents.  Checked against the oracle's gradient (which transposes) and
+    against the gradient over the real transposed CSR."""
+    n, e_half, F = 3000, 25_000, 48
+    a = graphgen.uniform_ints(21, 1, e_half, n)
+    b = graphgen.uniform_ints(21, 2, e_half, n)
+    wh = graphgen.uniform_f32(21, 7, e_half)
+    src = np.concatenate([a, b]).astype(np.int32)
+    dst = np.concatenate([b, a]).astype(np.int32)
+    w = np.concatenate([wh, wh]).astype(np.float32)  # w(u, v) = w(v, u)
+    rp_o, col_o, _, w_o = oracle.coo_to_csr(src, dst, n, n_src=n, val=w)
+    w_use = w_o if weighted else None
+    G, gkw = grad_input(22, n, F, torch.float32)
+    rp, col = dev(rp_o.astype(np.int32)), dev(col_o)
+    wd = dev(w_o) if weighted else None
+    plan = mp.Plan(rp, src.size, F) if use_plan else None
+    gx = mp.spmm_backward_x(rp, col, G, RED[reduce], posT=None, wT=wd, rowptr=rp, planT=plan)
+    rpt, colt, post, wt, _ = check_transpose(rp_o, col_o, n, w_o)
+    gx2 = mp.spmm_backward_x(rpt, colt, G, RED[reduce], posT=post, wT=wt if weighted else None,
+                             rowptr=rp)
+    torch.cuda.synchronize()
+    ref, scale = oracle.spmm_backward_x(rp_o, col_o, n, reduce, w=w_use, **gkw)
+    for y in (gx, gx2):
+        err = scaled_error(y.cpu().numpy(), ref, scale)
+        assert err <= TOL[torch.float32], f"{reduce} undirected grad_x error {err}"
