@@ -1076,8 +1076,9 @@ def summarize_step_counters(fetch_dir, write_dir, ops_path, out, cmd):
              f"fetch_scale: {scale_f:.4f}  write_scale: {scale_w:.4f}  (copy of "
              f"{CALIB_BYTES} bytes: FETCH_SIZE and WRITE_SIZE scaled so it reads and writes "
              f"that many)",
-             "FETCH_SIZE counts the bytes the L2 requests from the fabric: MALL hits "
-             "included, so fetch + write is an upper bound on HBM traffic.",
+             "FETCH_SIZE and WRITE_SIZE count L2 egress: the bytes the L2 requests from "
+             "and writes to the fabric, MALL hits included, so fetch + write is an upper "
+             "bound on HBM traffic, not a measured HBM rate.",
              "",
              f"{'operation':<14} {'fetch_GB':>10} {'write_GB':>10} {'total_GB':>10} "
              f"{'algo_GB':>10} {'ratio':>7}  kernels"]
@@ -1090,6 +1091,15 @@ def summarize_step_counters(fetch_dir, write_dir, ops_path, out, cmd):
         ks = ", ".join(sorted({short_name(d["name"]).split("<")[0] for d in df}))
         lines.append(f"{n:<14} {f_b / 1e9:>10.3f} {w_b / 1e9:>10.3f} {(f_b + w_b) / 1e9:>10.3f} "
                      f"{algo[n] / 1e9:>10.3f} {(f_b + w_b) / max(algo[n], 1):>7.3f}  {ks}")
+        per = {}
+        for d in df:
+            per.setdefault(short_name(d["name"]).split("<")[0], [0.0, 0.0])[0] += d["kib"]
+        for d in dw:
+            per.setdefault(short_name(d["name"]).split("<")[0], [0.0, 0.0])[1] += d["kib"]
+        if len(per) > 1:
+            for k, (kf_, kw_) in sorted(per.items(), key=lambda t: -(t[1][0] + t[1][1])):
+                lines.append(f"  {k:<24} {kf_ * 1024.0 * scale_f / 1e9:>10.3f} "
+                             f"{kw_ * 1024.0 * scale_w / 1e9:>10.3f}")
     lines.append(f"kernel_source_sha1: {source_digest(DOMINANT_SRC)}")
     open(out, "w").write("\n".join(lines) + "\n")
     print("\n".join(lines))
