@@ -21,6 +21,8 @@ gathers one full feature row; see algorithmic_bytes()) / step time, in GB/s.
 Other modes (used to produce the committed summaries under profiles/):
   --summarize-stats DIR OUT        kernel-trace stats of a rocprofv3 run -> OUT
   --summarize-counters F W OUT     FETCH_SIZE (F) and WRITE_SIZE (W) runs -> OUT
+  --summarize-step-counters F W OPS OUT   the same for every operation of a step
+  --summarize-sq DIR OUT           shader counters (occupancy, VALU, waits) per kernel
 """
 from __future__ import annotations
 
@@ -1001,6 +1003,13 @@ def _counter_rows(d):
     return list(csv.DictReader(open(path)))
 
 
+def _is_calib(kernel_name):
+    """torch's copy kernel (the --calibrate-copy run), not the library's own
+    row copy."""
+    k = kernel_name.lower()
+    return ("copy" in k or "elementwise" in k) and not short_name(kernel_name).startswith("copy_rows")
+
+
 def _per_dispatch(rows, counter):
     """{(dispatch id, kernel name): value} summed over the counter's instances."""
     acc = {}
@@ -1056,15 +1065,15 @@ def summarize_step_counters(fetch_dir, write_dir, ops_path, out, cmd):
     fr = _per_dispatch(_counter_rows(fetch_dir), "FETCH_SIZE")
     wr = _per_dispatch(_counter_rows(write_dir), "WRITE_SIZE")
     ops = json.load(open(ops_path))
-    copy_f = [v for (i, k), v in fr.items() if "copy" in k.lower() or "elementwise" in k.lower()]
-    copy_w = [v for (i, k), v in wr.items() if "copy" in k.lower() or "elementwise" in k.lower()]
+    copy_f = [v for (i, k), v in fr.items() if _is_calib(k)]
+    copy_w = [v for (i, k), v in wr.items() if _is_calib(k)]
     scale_f = CALIB_BYTES / (max(copy_f) * 1024.0) if copy_f else 1.0
     scale_w = CALIB_BYTES / (max(copy_w) * 1024.0) if copy_w else 1.0
 
     def step_dispatches(table):
         rows = sorted(((int(i), k, v) for (i, k), v in table.items()), key=lambda t: t[0])
         return [{"id": i, "name": k, "kib": v} for i, k, v in rows
-                if "copy" not in k.lower() and "elementwise" not in k.lower()
+                if not _is_calib(k)
                 and "fill" not in k.lower()]
 
     fs, ws = _segment_ops(step_dispatches(fr)), _segment_ops(step_dispatches(wr))
@@ -1105,6 +1114,79 @@ def summarize_step_counters(fetch_dir, write_dir, ops_path, out, cmd):
     print("\n".join(lines))
 
 
+SQ_COUNTERS = ["SQ_WAVES", "SQ_WAVE_CYCLES", "SQ_WAIT_ANY", "SQ_ACTIVE_INST_VALU",
+               "SQ_INSTS_VALU", "SQ_INSTS_VMEM_RD", "SQ_INSTS_LDS", "SQ_BUSY_CYCLES",
+               "GRBM_GUI_ACTIVE"]
+CU_NUM = 256
+XCD_NUM = 8
+CLOCK_HZ = 2.4e9
+
+
+def summarize_sq(d, out, cmd, kernels=None):
+    """Per-kernel shader counters of one `rocprofv3 --pmc <SQ_COUNTERS>` run,
+    averaged over the kernel's dispatches, with the ratios rocprofv3 itself
+    defines for gfx950: occupancy = 400 * SQ_WAVE_CYCLES / GRBM_GUI_ACTIVE /
+    CUs / 32 (percent of 32 wavefronts per CU), VALU busy = 100 *
+    SQ_ACTIVE_INST_VALU / CUs / GRBM_GUI_ACTIVE; wait = SQ_WAIT_ANY /
+    SQ_WAVE_CYCLES (the share of wavefront time spent waiting on memory,
+    LDS or a barrier); and the VALU floor, SQ_INSTS_VALU / (CUs * clock),
+    the time the kernel's vector instructions take at one wave64 instruction
+    per CU per cycle.  rocprofv3's CSV holds GRBM_GUI_ACTIVE summed over the
+    8 XCDs, while its formulas take one XCD's count (a maximum over them), so
+    the count is divided by 8 here; clk = that count / the kernel's duration
+    is the shader clock the kernel ran at."""
+    rows = _counter_rows(d)
+    per = {}  # short kernel name -> counter -> [values per dispatch]
+    for r in rows:
+        name = short_name(r["Kernel_Name"])
+        c = r.get("Counter_Name")
+        if c not in SQ_COUNTERS:
+            continue
+        key = (r["Dispatch_Id"], name)
+        red = max if c == "GRBM_GUI_ACTIVE" else (lambda a, b: a + b)
+        disp = per.setdefault(name, {}).setdefault(c, {})
+        v = float(r["Counter_Value"])
+        disp[key] = red(disp[key], v) if key in disp else v
+    dur = {}
+    try:
+        for r in csv.DictReader(open(_find(d, "*kernel_stats.csv"))):
+            dur[short_name(r["Name"])] = float(r["AverageNs"]) / 1e6
+    except SystemExit:
+        pass
+    lines = ["# Shader counters per kernel (rocprofv3 --pmc, averaged over dispatches)",
+             f"command: {cmd}",
+             "G = GRBM_GUI_ACTIVE / 8 (the CSV sums it over the 8 XCDs); "
+             "occ% = 400*SQ_WAVE_CYCLES/G/256/32 (share of 32 wavefronts per CU); "
+             "valu% = 100*SQ_ACTIVE_INST_VALU/256/G; wait% = SQ_WAIT_ANY/SQ_WAVE_CYCLES; "
+             "clk = G / ms; valu_floor_ms = SQ_INSTS_VALU/(256 CUs * 2.4 GHz); "
+             "ms = kernel-trace average (counter collection serializes dispatches)",
+             "",
+             f"{'kernel':<64} {'calls':>5} {'ms':>8} {'clk_GHz':>7} {'occ%':>6} {'valu%':>6} "
+             f"{'wait%':>6} {'valu/wave':>9} {'vmem/wave':>9} {'lds/wave':>8} {'valu_floor_ms':>13}"]
+    order = sorted(per, key=lambda n: -dur.get(n, 0.0))
+    for name in order:
+        if kernels and not any(k in name for k in kernels):
+            continue
+        c = {k: sum(v.values()) / max(len(v), 1) for k, v in per[name].items()}
+        calls = max(len(v) for v in per[name].values())
+        g = c.get("GRBM_GUI_ACTIVE", 0.0) / XCD_NUM
+        wc = c.get("SQ_WAVE_CYCLES", 0.0)
+        waves = max(c.get("SQ_WAVES", 0.0), 1.0)
+        occ = 400.0 * wc / g / CU_NUM / 32 if g else float("nan")
+        valu = 100.0 * c.get("SQ_ACTIVE_INST_VALU", 0.0) / CU_NUM / g if g else float("nan")
+        wait = 100.0 * c.get("SQ_WAIT_ANY", 0.0) / wc if wc else float("nan")
+        floor_ms = c.get("SQ_INSTS_VALU", 0.0) / (CU_NUM * CLOCK_HZ) * 1e3
+        ms = dur.get(name)
+        clk = g / (ms * 1e-3) / 1e9 if ms else float("nan")
+        lines.append(f"{name[:64]:<64} {calls:>5} {'' if ms is None else f'{ms:.3f}':>8} "
+                     f"{clk:>7.2f} {occ:>6.1f} {valu:>6.1f} {wait:>6.1f} "
+                     f"{c.get('SQ_INSTS_VALU', 0.0) / waves:>9.0f} "
+                     f"{c.get('SQ_INSTS_VMEM_RD', 0.0) / waves:>9.0f} "
+                     f"{c.get('SQ_INSTS_LDS', 0.0) / waves:>8.0f} {floor_ms:>13.3f}")
+    open(out, "w").write("\n".join(lines) + "\n")
+    print("\n".join(lines))
+
+
 def summarize_counters(fetch_dir, write_dir, out, cmd):
     fr = _per_dispatch(_counter_rows(fetch_dir), "FETCH_SIZE")
     wr = _per_dispatch(_counter_rows(write_dir), "WRITE_SIZE")
@@ -1114,8 +1196,8 @@ def summarize_counters(fetch_dir, write_dir, out, cmd):
         return vals
 
     # calibration: the plain copy of CALIB_BYTES (reads and writes that many)
-    copy_f = [v for (i, k), v in fr.items() if "copy" in k.lower() or "elementwise" in k.lower()]
-    copy_w = [v for (i, k), v in wr.items() if "copy" in k.lower() or "elementwise" in k.lower()]
+    copy_f = [v for (i, k), v in fr.items() if _is_calib(k)]
+    copy_w = [v for (i, k), v in wr.items() if _is_calib(k)]
     cf = max(copy_f) if copy_f else None
     cw = max(copy_w) if copy_w else None
     scale_f = CALIB_BYTES / (cf * 1024.0) if cf else 1.0
@@ -1169,6 +1251,8 @@ def main():
                     help="run one plain 1 GiB copy after warm-up (counter scaling)")
     ap.add_argument("--summarize-stats", nargs=2, metavar=("DIR", "OUT"))
     ap.add_argument("--summarize-counters", nargs=3, metavar=("FETCH_DIR", "WRITE_DIR", "OUT"))
+    ap.add_argument("--summarize-sq", nargs=2, metavar=("DIR", "OUT"),
+                    help="per-kernel shader counters of a `rocprofv3 --pmc` run of SQ_COUNTERS")
     ap.add_argument("--summarize-step-counters", nargs=4,
                     metavar=("FETCH_DIR", "WRITE_DIR", "OPS_JSON", "OUT"))
     ap.add_argument("--dump-ops", metavar="PATH",
@@ -1176,6 +1260,9 @@ def main():
     ap.add_argument("--cmd", default="", help="command line recorded in a summary ({ctr} is "
                     "replaced by the counter name in counter summaries)")
     args = ap.parse_args()
+    if args.summarize_sq:
+        summarize_sq(*args.summarize_sq, args.cmd)
+        return
     if args.summarize_stats:
         summarize_stats(*args.summarize_stats, args.cmd)
         return

@@ -167,10 +167,15 @@ struct mp_plan {
 
 namespace {
 
-// A single feature table of `rows` rows, `ld` elements apart, fits 32-bit
-// byte offsets from its base.
+// A single feature table of `rows` rows, `ld` elements apart, is addressed
+// with 32-bit byte offsets from its base: it spans under 4 GiB, and row
+// indices and the row stride in bytes fit 24 bits, so that the kernels form
+// an offset with one 24-bit multiply-add.
 inline int fits_off32(int64_t rows, int64_t ld, int elem_bytes) {
-    return rows * ld * elem_bytes <= (int64_t)UINT32_MAX ? 1 : 0;
+    return rows * ld * elem_bytes <= (int64_t)UINT32_MAX && rows <= ((int64_t)1 << 24) &&
+                   ld * elem_bytes < ((int64_t)1 << 24)
+               ? 1
+               : 0;
 }
 
 // Fill the work description of SpmmParams from a plan (or the plan-free

@@ -84,19 +84,15 @@ template <> struct RawVec<uint16_t, 4> { using T = uint2; };
 template <> struct RawVec<uint16_t, 2> { using T = uint32_t; };
 template <> struct RawVec<uint16_t, 1> { using T = uint16_t; };
 
-// One lane-chunk of a feature row at address a.  O32: every row of the table
-// lies within 4 GiB of the table's base t0, so the address is formed from
-// t0 and a 32-bit byte offset (one register per gathered row instead of two,
-// and 32-bit offset arithmetic), which frees registers for more rows in
-// flight.
-template <typename R, bool O32>
-__device__ inline R load_row_chunk(const char* t0, const char* a) {
-    if constexpr (O32) {
-        const uint32_t off = (uint32_t)(a - t0);
-        return *reinterpret_cast<const R*>(t0 + off);
-    } else {
-        return *reinterpret_cast<const R*>(a);
-    }
+// Byte offset of element fe of row c from the table's base when the table is
+// addressed with 32-bit offsets (O32): the table spans under 4 GiB, has at
+// most 2^24 rows and a row stride under 2^24 bytes, so one full-rate 24-bit
+// multiply-add forms the offset (a 32-bit multiply is a quarter-rate
+// instruction, and the gathers issue one per row).
+template <typename TX>
+__device__ inline uint32_t off32(const SpmmParams& P, int32_t c, int64_t fe) {
+    return __umul24((uint32_t)c, (uint32_t)P.ldx * (uint32_t)sizeof(TX)) +
+           (uint32_t)fe * (uint32_t)sizeof(TX);
 }
 
 __device__ inline float bf16_lo(uint32_t u) { return __uint_as_float(u << 16); }
@@ -164,6 +160,28 @@ __device__ inline const char* feat_addr(const SpmmParams& P, int32_t c, int64_t 
             vo = (k < P.n_tables && c >= (int32_t)P.table_off[k]) ? P.voff[k] : vo;
         return P.table_ptr[0] + vo + ((int64_t)c * P.ldx + fe) * (int64_t)sizeof(TX);
     }
+}
+
+// One lane-chunk (EPL elements from fe) of source row c.  O32: the address is
+// the table's base plus a 32-bit byte offset (one register per gathered row
+// instead of two), which frees registers for more rows in flight.
+template <typename TX, int EPL, int NT, bool O32>
+__device__ inline typename RawVec<TX, EPL>::T load_chunk(const SpmmParams& P, int32_t c,
+                                                          int64_t fe) {
+    using R = typename RawVec<TX, EPL>::T;
+    if constexpr (O32) {
+        static_assert(NT == 1, "32-bit offsets address one table");
+        return *reinterpret_cast<const R*>(P.table_ptr[0] + off32<TX>(P, c, fe));
+    } else {
+        return *reinterpret_cast<const R*>(feat_addr<TX, NT>(P, c, fe));
+    }
+}
+
+// A wave-uniform 64-bit value held in scalar registers.
+__device__ inline int64_t uniform64(int64_t x) {
+    const uint32_t lo = __builtin_amdgcn_readfirstlane((uint32_t)x);
+    const uint32_t hi = __builtin_amdgcn_readfirstlane((uint32_t)((uint64_t)x >> 32));
+    return (int64_t)(((uint64_t)hi << 32) | lo);
 }
 
 // a - b, never fused with the product that formed a: a weighted message is
@@ -452,7 +470,12 @@ __device__ inline int32_t col_at(const SpmmParams& P, int64_t p) {
 // interleaved.  The column indices (and weights) of up to 64 edges are loaded
 // once, coalesced, one per lane; each inner step then covers SU = S*U edges:
 // slot s takes edges base + u*S + s (u < U), gets their columns by cross-lane
-// permute, issues all U feature-row loads, and only then accumulates.  (The
+// permute, issues all U feature-row loads, and only then accumulates.  A step
+// whose SU edges all exist (every step of a range but its last, and the
+// first one of a row that sets the variance shift) runs without per-edge
+// conditions: lanes that hold no feature chunk load the row's first chunk
+// instead (a line the slot's first lane fetches anyway) and accumulate values
+// that are never stored, so the step needs no exec-mask branches.  (The
 // masked sum has its own pipelined variant below.)
 template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, int MODE, bool O32>
 __device__ inline void wave_range(const SpmmParams& P,
@@ -467,71 +490,116 @@ __device__ inline void wave_range(const SpmmParams& P,
     const int SU = S * U;
     const int steps = kWave / SU;
     const int tile = steps * SU;
+    e0 = uniform64(e0);
+    e1 = uniform64(e1);
+    const int64_t fe_ld = feat_ok ? fe : 0;
+    const bool full_u = U == UN;
+    // column indices (and weights) of the tile at q, one per lane
+    auto load_tile = [&](int64_t q, int32_t& c, float& w) {
+        c = 0;
+        w = 1.f;
+        if (lane < tile && lane < e1 - q) {
+            c = col_at(P, q + lane);
+            if constexpr (W) w = __builtin_nontemporal_load(P.w + q + lane);
+        }
+    };
+    // a step whose edges may run past the range (t >= rem) or with U < UN;
+    // set_shift: the row's first step, whose slot-0 messages (edges u * S of
+    // the row) give the row's shift, passed from slot 0's lane j to lane j of
+    // every slot
+    auto general_step = [&](int64_t p0, int32_t myc, float myw, int base, bool set_shift) {
+        const int64_t rem = e1 - p0;
+        int32_t cu[UN];
+        bool ok[UN];
+#pragma unroll
+        for (int u = 0; u < UN; ++u) {
+            const int t = base + u * S + slot;
+            cu[u] = __shfl(myc, t);
+            ok[u] = feat_ok && (u < U) && (t < rem);
+        }
+        R raw[UN];
+#pragma unroll
+        for (int u = 0; u < UN; ++u)
+            if (ok[u]) raw[u] = load_chunk<TX, EPL, NT, O32>(P, cu[u], fe);
+        if constexpr (MODE == kModeStats) {
+            if (set_shift) {
+                float t[EPL] = {};
+                int cnt = 0;
+#pragma unroll
+                for (int u = 0; u < UN; ++u) {
+                    float wt = 1.f;
+                    if constexpr (W) wt = __shfl(myw, (u * S + slot) & (kWave - 1));
+                    if (u < U && u * S < rem) ++cnt;
+                    if (slot == 0 && ok[u]) {
+                        float v[EPL];
+                        widen<TX, EPL>(raw[u], v);
+#pragma unroll
+                        for (int k = 0; k < EPL; ++k) t[k] += W ? __fmul_rn(wt, v[k]) : v[k];
+                    }
+                }
+#pragma unroll
+                for (int k = 0; k < EPL; ++k) t[k] = __shfl(t[k], j);
+                acc.set_shift(t, cnt);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < UN; ++u) {
+            const int t = base + u * S + slot;
+            float wt = 1.f;
+            if constexpr (W) wt = __shfl(myw, t);
+            if (ok[u]) {
+                float v[EPL];
+                widen<TX, EPL>(raw[u], v);
+                if constexpr (W) {
+#pragma unroll
+                    for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt, v[k]);
+                }
+                acc.add(u % A, v, (int32_t)(p0 + t));
+            }
+        }
+    };
+    int32_t myc;
+    float myw;
+    load_tile(e0, myc, myw);
+    int st0 = 0;
+    if constexpr (MODE == kModeStats) {
+        if (shift_first && e0 < e1) {
+            general_step(e0, myc, myw, 0, true);
+            st0 = 1;
+        }
+    }
     for (int64_t p0 = e0; p0 < e1; p0 += tile) {
         const int64_t rem = e1 - p0;
-        int32_t myc = 0;
-        float myw = 1.f;
-        if (lane < tile && lane < rem) {
-            myc = col_at(P, p0 + lane);
-            if constexpr (W) myw = __builtin_nontemporal_load(P.w + p0 + lane);
-        }
-        for (int st = 0; st < steps; ++st) {
+        const int64_t nf = full_u ? rem / SU : 0;
+        const int nfull = nf < steps ? (int)nf : steps;
+        int st = st0;
+        // full steps: every edge exists, no per-edge conditions
+        for (; st < nfull; ++st) {
             const int base = st * SU;
-            if (base >= rem) break;
-            const char* addr[UN];
-            bool ok[UN];
-#pragma unroll
-            for (int u = 0; u < UN; ++u) {
-                const int t = base + u * S + slot;
-                const int32_t c = __shfl(myc, t);
-                ok[u] = feat_ok && (u < U) && (t < rem);
-                addr[u] = feat_addr<TX, NT>(P, c, fe);
-            }
             R raw[UN];
 #pragma unroll
             for (int u = 0; u < UN; ++u)
-                if (ok[u]) raw[u] = load_row_chunk<R, O32>(P.table_ptr[0], addr[u]);
-            if constexpr (MODE == kModeStats) {
-                if (shift_first) {
-                    // the row's first step: the mean of slot 0's messages
-                    // (edges u * S of the row) is the row's shift, passed from
-                    // slot 0's lane j to lane j of every slot
-                    shift_first = false;
-                    float t[EPL] = {};
-                    int cnt = 0;
-#pragma unroll
-                    for (int u = 0; u < UN; ++u) {
-                        float wt = 1.f;
-                        if constexpr (W) wt = __shfl(myw, (u * S + slot) & (kWave - 1));
-                        if (u < U && u * S < rem) ++cnt;
-                        if (slot == 0 && ok[u]) {
-                            float v[EPL];
-                            widen<TX, EPL>(raw[u], v);
-#pragma unroll
-                            for (int k = 0; k < EPL; ++k) t[k] += W ? __fmul_rn(wt, v[k]) : v[k];
-                        }
-                    }
-#pragma unroll
-                    for (int k = 0; k < EPL; ++k) t[k] = __shfl(t[k], j);
-                    acc.set_shift(t, cnt);
-                }
-            }
+                raw[u] = load_chunk<TX, EPL, NT, O32>(P, __shfl(myc, base + u * S + slot), fe_ld);
+            const int32_t pos = (int32_t)(p0 + base) + slot;
 #pragma unroll
             for (int u = 0; u < UN; ++u) {
-                const int t = base + u * S + slot;
-                float wt = 1.f;
-                if constexpr (W) wt = __shfl(myw, t);
-                if (ok[u]) {
-                    float v[EPL];
-                    widen<TX, EPL>(raw[u], v);
-                    if constexpr (W) {
+                float v[EPL];
+                widen<TX, EPL>(raw[u], v);
+                if constexpr (W) {
+                    const float wt = __shfl(myw, base + u * S + slot);
 #pragma unroll
-                        for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt, v[k]);
-                    }
-                    acc.add(u % A, v, (int32_t)(p0 + t));
+                    for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt, v[k]);
                 }
+                acc.add(u % A, v, pos + u * S);
             }
         }
+        for (; st < steps; ++st) {
+            const int base = st * SU;
+            if (base >= rem) break;
+            general_step(p0, myc, myw, base, false);
+        }
+        st0 = 0;
+        load_tile(p0 + tile, myc, myw);
     }
     if constexpr (HM) {
         // partial a's first message: edge u = a of the range's first step
@@ -618,7 +686,7 @@ __device__ inline void wave_range_masked(const SpmmParams& P,
                 bits |= (uint64_t)b << (u * EPL);
                 const int32_t c = __shfl(myc, t & (kWave - 1));
                 if constexpr (O32)
-                    off[u] = ((uint32_t)c * (uint32_t)P.ldx + (uint32_t)fe) * (uint32_t)sizeof(TX);
+                    off[u] = off32<TX>(P, c, fe);
                 else
                     addr[u] = feat_addr<TX, NT>(P, c, fe);
             }
@@ -723,7 +791,7 @@ __device__ inline void slot_row_masked(const SpmmParams& P,
             bits |= (uint64_t)b << (u * EPL);
             const int32_t c = __shfl(c0, (slot * L + u) & (kWave - 1));
             if constexpr (O32)
-                off[u] = ((uint32_t)c * (uint32_t)P.ldx + (uint32_t)fe) * (uint32_t)sizeof(TX);
+                off[u] = off32<TX>(P, c, fe);
             else
                 addr[u] = feat_addr<TX, NT>(P, c, fe);
         }
@@ -770,18 +838,24 @@ __device__ inline void slot_row_masked(const SpmmParams& P,
 
 // One slot per row: every slot walks its own row's edges, U at a time.
 // COOP: the slot has at least U lanes, which load its next U columns
-// together; otherwise each lane loads the columns itself.  (The masked sum
-// has its own pipelined variant above.)
+// together; otherwise each lane loads the columns itself.  With COOP, the
+// iterations in which every slot's row still has U edges (min_n: the
+// shortest row of the wavefront) run without per-edge conditions, as the full
+// steps of wave_range do.  (The masked sum has its own pipelined variant
+// above.)
 template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, int MODE, bool COOP, bool O32>
 __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MODE>& acc,
-                                int64_t e0, int32_t my_n, int32_t max_n, int slot, int j,
-                                bool feat_ok, int64_t fe) {
+                                int64_t e0, int32_t my_n, int32_t max_n, int32_t min_n,
+                                int slot, int j, bool feat_ok, int64_t fe) {
     using R = typename RawVec<TX, EPL>::T;
     constexpr int A = AccFor<TX, EPL, HS, HM, MODE>::A;
     constexpr int UN = unroll_of<MODE, HS, HM>();
     const int L = P.L;
-    for (int32_t it = 0; it < max_n; it += UN) {
-        const char* addr[UN];
+    const int64_t fe_ld = feat_ok ? fe : 0;
+    // an iteration in which a slot's row may end (it + u >= my_n); set_shift:
+    // the first one, whose messages give the row's shift
+    auto general_iter = [&](int32_t it, bool set_shift) {
+        int32_t cc[UN];
         bool ok[UN];
         float wt[UN];
         if constexpr (COOP) {
@@ -794,14 +868,12 @@ __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MOD
 #pragma unroll
             for (int u = 0; u < UN; ++u) {
                 const int srcl = slot * L + u;
-                const int32_t c = __shfl(myc, srcl);
+                cc[u] = __shfl(myc, srcl);
                 wt[u] = 1.f;
                 if constexpr (W) wt[u] = __shfl(myw, srcl);
                 ok[u] = feat_ok && (it + u < my_n);
-                addr[u] = feat_addr<TX, NT>(P, c, fe);
             }
         } else {
-            int32_t cc[UN];
 #pragma unroll
             for (int u = 0; u < UN; ++u) {
                 ok[u] = feat_ok && (it + u < my_n);
@@ -809,15 +881,13 @@ __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MOD
                 wt[u] = 1.f;
                 if constexpr (W) wt[u] = ok[u] ? P.w[e0 + it + u] : 1.f;
             }
-#pragma unroll
-            for (int u = 0; u < UN; ++u) addr[u] = feat_addr<TX, NT>(P, cc[u], fe);
         }
         R raw[UN];
 #pragma unroll
         for (int u = 0; u < UN; ++u)
-            if (ok[u]) raw[u] = load_row_chunk<R, O32>(P.table_ptr[0], addr[u]);
+            if (ok[u]) raw[u] = load_chunk<TX, EPL, NT, O32>(P, cc[u], fe);
         if constexpr (MODE == kModeStats) {
-            if (it == 0) {  // the row's shift: the mean of its first UN messages
+            if (set_shift) {  // the mean of the row's first UN messages
                 float t[EPL] = {};
 #pragma unroll
                 for (int u = 0; u < UN; ++u) {
@@ -843,7 +913,40 @@ __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MOD
                 acc.add(u % A, v, (int32_t)(e0 + it + u));
             }
         }
+    };
+    int32_t it = 0;
+    if constexpr (MODE == kModeStats) {
+        general_iter(0, true);
+        it = UN;
     }
+    if constexpr (COOP) {
+        // every slot's row has UN more edges: no per-edge conditions
+        for (; it + UN <= min_n; it += UN) {
+            int32_t myc = 0;
+            float myw = 1.f;
+            if (j < UN && it + j < my_n) {
+                myc = col_at(P, e0 + it + j);
+                if constexpr (W) myw = __builtin_nontemporal_load(P.w + e0 + it + j);
+            }
+            R raw[UN];
+#pragma unroll
+            for (int u = 0; u < UN; ++u)
+                raw[u] = load_chunk<TX, EPL, NT, O32>(P, __shfl(myc, slot * L + u), fe_ld);
+            const int32_t pos = (int32_t)(e0 + it);
+#pragma unroll
+            for (int u = 0; u < UN; ++u) {
+                float v[EPL];
+                widen<TX, EPL>(raw[u], v);
+                if constexpr (W) {
+                    const float wt = __shfl(myw, slot * L + u);
+#pragma unroll
+                    for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt, v[k]);
+                }
+                acc.add(u % A, v, pos + u);
+            }
+        }
+    }
+    for (; it < max_n; it += UN) general_iter(it, false);
     if constexpr (HM) {
 #pragma unroll
         for (int a = 0; a < A; ++a) acc.settle(a, (int32_t)(e0 + a), feat_ok && a < my_n);
@@ -873,7 +976,7 @@ __device__ inline void hub_shift(const SpmmParams& P, int64_t r0, int64_t deg, b
 #pragma unroll
     for (int u = 0; u < KS; ++u)
         if (feat_ok && u < cnt)
-            raw[u] = load_row_chunk<R, O32>(P.table_ptr[0], feat_addr<TX, NT>(P, c[u], fe));
+            raw[u] = load_chunk<TX, EPL, NT, O32>(P, c[u], fe);
 #pragma unroll
     for (int k = 0; k < EPL; ++k) t[k] = 0.f;
 #pragma unroll
@@ -894,9 +997,9 @@ __device__ inline void hub_shift(const SpmmParams& P, int64_t r0, int64_t deg, b
 // scheduler needs the registers.
 template <typename TX, int EPL, bool HS, bool HM, bool W, int MODE, bool O32>
 constexpr int waves_hint() {
-    return MODE == kModeStats && !W && O32 && AccFor<TX, EPL, HS, HM, MODE>::A * EPL <= 8
-               ? MP_STATS_WAVES
-               : 1;
+    if (MODE == kModeStats && !W && O32 && AccFor<TX, EPL, HS, HM, MODE>::A * EPL <= 8)
+        return MP_STATS_WAVES;
+    return 1;
 }
 
 template <typename TX, int EPL, bool HS, bool HM, int NT, bool W, int MODE, bool O32 = false>
@@ -1018,11 +1121,16 @@ void spmm_main(SpmmParams P) {
     }
     const int32_t my_n = (int32_t)(e1 - e0);
     int32_t max_n = my_n;
+    int32_t min_n = row_ok ? my_n : INT32_MAX;  // the shortest row of the wavefront
 #pragma unroll
     for (int off = 1; off < kWave; off <<= 1) {
         const int32_t o = __shfl_xor(max_n, off);
         max_n = o > max_n ? o : max_n;
+        const int32_t on = __shfl_xor(min_n, off);
+        min_n = on < min_n ? on : min_n;
     }
+    max_n = __builtin_amdgcn_readfirstlane(max_n);
+    min_n = __builtin_amdgcn_readfirstlane(min_n);
     if constexpr (MODE == kModeMasked) {
         const int64_t w_lo = (int64_t)ft * 2 * EPL;
         const int64_t wmax = P.mw - w_lo;
@@ -1030,11 +1138,11 @@ void spmm_main(SpmmParams P) {
         slot_row_masked<TX, EPL, HS, HM, NT, W, O32>(P, acc, e0, my_n, max_n, lane, slot, j,
                                                      feat_ok, fe, w_lo, mww);
     } else if (L >= unroll_of<MODE, HS, HM>()) {
-        slot_row<TX, EPL, HS, HM, NT, W, MODE, true, O32>(P, acc, e0, my_n, max_n, slot, j, feat_ok,
-                                                         fe);
+        slot_row<TX, EPL, HS, HM, NT, W, MODE, true, O32>(P, acc, e0, my_n, max_n, min_n, slot, j,
+                                                         feat_ok, fe);
     } else {
-        slot_row<TX, EPL, HS, HM, NT, W, MODE, false, O32>(P, acc, e0, my_n, max_n, slot, j, feat_ok,
-                                                          fe);
+        slot_row<TX, EPL, HS, HM, NT, W, MODE, false, O32>(P, acc, e0, my_n, max_n, min_n, slot, j,
+                                                          feat_ok, fe);
     }
     acc.fold();
     if (feat_ok) {
