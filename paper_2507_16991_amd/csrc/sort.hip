@@ -39,15 +39,28 @@ __device__ inline uint64_t desc_make(uint64_t flag, uint32_t tag, uint64_t v) {
 }
 
 // Lanes of the wavefront that hold a valid key with the same digit as this
-// lane (one ballot per digit bit).
+// lane: one ballot per digit bit; a lane differs from this one where the
+// ballot's bit differs from this lane's own bit (sign-extended to a full
+// word, so that one XOR per half-mask finds those lanes).  The bits are
+// unrolled up to kSortMaxBits under a wave-uniform test.
 __device__ inline uint64_t digit_peers(bool ok, uint32_t d, int bits) {
-    uint64_t peers = __ballot(ok);
-    for (int b = 0; b < bits; ++b) {
-        const bool bit = (d >> b) & 1u;
-        const uint64_t bal = __ballot(bit);
-        peers &= bit ? bal : ~bal;
+    uint32_t dlo = 0, dhi = 0;  // lanes whose digit differs in some bit
+#pragma unroll
+    for (int b = 0; b < kSortMaxBits; ++b) {
+        if (b < bits) {
+            const int32_t sb = (int32_t)(d << (31 - b)) >> 31;  // 0 or -1
+            const uint64_t bal = __ballot(sb != 0);
+            dlo |= (uint32_t)bal ^ (uint32_t)sb;
+            dhi |= (uint32_t)(bal >> 32) ^ (uint32_t)sb;
+        }
     }
-    return peers;
+    return __ballot(ok) & ~(((uint64_t)dhi << 32) | dlo);
+}
+
+// Set bits of m below this lane.
+__device__ inline uint32_t count_below(uint64_t m) {
+    return __builtin_amdgcn_mbcnt_hi((uint32_t)(m >> 32),
+                                     __builtin_amdgcn_mbcnt_lo((uint32_t)m, 0u));
 }
 
 __global__ __launch_bounds__(256) void radix_clear(uint64_t* __restrict__ desc, int64_t ndesc,
@@ -154,7 +167,6 @@ void radix_onesweep(RadixPass p) {
 
     const int64_t tbase = tile * kSortTile;
     const int64_t wbase = tbase + (int64_t)wv * kWaveKeys;
-    const uint64_t lt_mask = (lane == 0) ? 0ull : (~0ull >> (kWave - lane));
 
     uint32_t key[kSortItems];
     int32_t va[kSortItems], vb[kSortItems];
@@ -172,7 +184,7 @@ void radix_onesweep(RadixPass p) {
         const bool ok = wbase + (int64_t)k * kWave + lane < p.n;
         const uint32_t d = (key[k] >> p.shift) & (uint32_t)(R - 1);
         const uint64_t peers = digit_peers(ok, d, p.bits);
-        const uint32_t below = (uint32_t)__popcll(peers & lt_mask);
+        const uint32_t below = count_below(peers);
         const uint32_t base = s_cnt[wv][d];
         rank[k] = base + below;
         // the lowest peer advances the counter for all of them; every lane has

@@ -44,8 +44,14 @@ constexpr int kUnroll = MP_UNROLL;
 #ifndef MP_STATS_WAVES
 #define MP_STATS_WAVES 4    // stats mode: wavefronts per SIMD the registers must allow
 #endif
+#ifndef MP_SUM_WAVES
+#define MP_SUM_WAVES 6      // unweighted bf16 sums with 32-bit row offsets: the same
+#endif
 #ifndef MP_MASKED_UNROLL
 #define MP_MASKED_UNROLL 8  // the same for the masked sum
+#endif
+#ifndef MP_MASKED_PARTIALS
+#define MP_MASKED_PARTIALS 4  // partial sums per element of the masked sum
 #endif
 
 // Kernel modes: the plain aggregation (sum/mean and/or max); the masked sum
@@ -344,8 +350,9 @@ struct Acc {
 // features, whose rows arrive twice as fast, two.
 template <typename TX, int EPL, bool HS, bool HM, int MODE>
 using AccFor = Acc<EPL, HS, HM, MODE == kModeStats,
-                   MODE == kModeStats ? (sizeof(TX) == 4 ? 1 : 2)
-                                      : (HM ? (HS ? 2 : MP_MAX_PARTIALS) : 4)>;
+                   MODE == kModeStats    ? (sizeof(TX) == 4 ? 1 : 2)
+                   : MODE == kModeMasked ? MP_MASKED_PARTIALS
+                                         : (HM ? (HS ? 2 : MP_MAX_PARTIALS) : 4)>;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -994,11 +1001,14 @@ __device__ inline void hub_shift(const SpmmParams& P, int64_t r0, int64_t deg, b
 // (unweighted, 32-bit row offsets, at most 8 accumulated elements per lane),
 // the register budget is capped so that MP_STATS_WAVES wavefronts fit a SIMD
 // without spilling: the gathers need wavefronts in flight more than the
-// scheduler needs the registers.
+// scheduler needs the registers.  Unweighted bf16 sums of up to 4 elements
+// per lane with 32-bit row offsets are capped likewise (MP_SUM_WAVES).
 template <typename TX, int EPL, bool HS, bool HM, bool W, int MODE, bool O32>
 constexpr int waves_hint() {
     if (MODE == kModeStats && !W && O32 && AccFor<TX, EPL, HS, HM, MODE>::A * EPL <= 8)
         return MP_STATS_WAVES;
+    if (MODE == kModePlain && HS && !HM && !W && O32 && sizeof(TX) == 2 && EPL <= 4)
+        return MP_SUM_WAVES;
     return 1;
 }
 
