@@ -1137,8 +1137,10 @@ def summarize_sq(d, out, cmd, kernels=None):
     is the shader clock the kernel ran at."""
     rows = _counter_rows(d)
     per = {}  # short kernel name -> counter -> [values per dispatch]
+    lds = {}  # short kernel name -> LDS bytes per workgroup
     for r in rows:
         name = short_name(r["Kernel_Name"])
+        lds[name] = r.get("LDS_Block_Size", "?")
         c = r.get("Counter_Name")
         if c not in SQ_COUNTERS:
             continue
@@ -1161,8 +1163,9 @@ def summarize_sq(d, out, cmd, kernels=None):
              "clk = G / ms; valu_floor_ms = SQ_INSTS_VALU/(256 CUs * 2.4 GHz); "
              "ms = kernel-trace average (counter collection serializes dispatches)",
              "",
-             f"{'kernel':<64} {'calls':>5} {'ms':>8} {'clk_GHz':>7} {'occ%':>6} {'valu%':>6} "
-             f"{'wait%':>6} {'valu/wave':>9} {'vmem/wave':>9} {'lds/wave':>8} {'valu_floor_ms':>13}"]
+             f"{'kernel':<64} {'calls':>5} {'ms':>8} {'lds_B':>6} {'clk_GHz':>7} "
+             f"{'occ%':>6} {'valu%':>6} {'wait%':>6} {'valu/wave':>9} {'vmem/wave':>9} "
+             f"{'lds/wave':>8} {'valu_floor_ms':>13}"]
     order = sorted(per, key=lambda n: -dur.get(n, 0.0))
     for name in order:
         if kernels and not any(k in name for k in kernels):
@@ -1179,7 +1182,7 @@ def summarize_sq(d, out, cmd, kernels=None):
         ms = dur.get(name)
         clk = g / (ms * 1e-3) / 1e9 if ms else float("nan")
         lines.append(f"{name[:64]:<64} {calls:>5} {'' if ms is None else f'{ms:.3f}':>8} "
-                     f"{clk:>7.2f} {occ:>6.1f} {valu:>6.1f} {wait:>6.1f} "
+                     f"{lds.get(name, '?'):>6} {clk:>7.2f} {occ:>6.1f} {valu:>6.1f} {wait:>6.1f} "
                      f"{c.get('SQ_INSTS_VALU', 0.0) / waves:>9.0f} "
                      f"{c.get('SQ_INSTS_VMEM_RD', 0.0) / waves:>9.0f} "
                      f"{c.get('SQ_INSTS_LDS', 0.0) / waves:>8.0f} {floor_ms:>13.3f}")

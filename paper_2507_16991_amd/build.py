@@ -56,5 +56,49 @@ def build(lib: str = LIB, defines=()) -> str:
     return lib
 
 
+def resource_usage(out: str, pattern: str = "") -> str:
+    """Registers, spills, LDS and occupancy of every kernel, as the compiler
+    reports them (-Rpass-analysis=kernel-resource-usage), one line per kernel
+    whose demangled name matches `pattern`; written to `out`."""
+    import re
+    rows = []
+    for src in SOURCES:
+        if not src.endswith(".hip"):
+            continue
+        cmd = [HIPCC, *FLAGS, "--offload-device-only", "-c", os.path.join(CSRC, src),
+               "-o", os.devnull, "-Rpass-analysis=kernel-resource-usage"]
+        err = subprocess.run(cmd, capture_output=True, text=True).stderr
+        cur = None
+        for line in err.splitlines():
+            m = re.search(r"remark: (.*?) \[-Rpass", line)
+            if not m:
+                continue
+            key, _, val = m.group(1).strip().partition(":")
+            if key == "Function Name":
+                cur = {"src": src, "name": val.strip()}
+                rows.append(cur)
+            elif cur is not None:
+                cur[key.strip()] = val.strip()
+    names = subprocess.run(["c++filt"], input="\n".join(r["name"] for r in rows),
+                           capture_output=True, text=True).stdout.splitlines()
+    lines = ["# kernel resource usage (hipcc -Rpass-analysis=kernel-resource-usage, gfx950)",
+             f"command: python paper_2507_16991_amd/build.py --resource-usage {out}"
+             + (f" '{pattern}'" if pattern else ""), "",
+             f"{'vgpr':>4} {'agpr':>4} {'sgpr':>4} {'spill':>5} {'lds_B':>6} {'waves/SIMD':>10}  kernel"]
+    for r, n in zip(rows, names):
+        n = n.replace("mp::(anonymous namespace)::", "").replace("void ", "")
+        n = n.replace("(mp::SpmmParams)", "").replace("(mp::RadixPass)", "")
+        if pattern and not re.search(pattern, n):
+            continue
+        lines.append(f"{r.get('VGPRs', '?'):>4} {r.get('AGPRs', '?'):>4} {r.get('TotalSGPRs', '?'):>4} "
+                     f"{r.get('VGPRs Spill', '?'):>5} {r.get('LDS Size [bytes/block]', '?'):>6} "
+                     f"{r.get('Occupancy [waves/SIMD]', '?'):>10}  {r['src']}: {n}")
+    open(out, "w").write("\n".join(lines) + "\n")
+    return out
+
+
 if __name__ == "__main__":
-    print(build())
+    if len(sys.argv) > 2 and sys.argv[1] == "--resource-usage":
+        print(resource_usage(sys.argv[2], sys.argv[3] if len(sys.argv) > 3 else ""))
+    else:
+        print(build())
