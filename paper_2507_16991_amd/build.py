@@ -87,7 +87,12 @@ def resource_usage(out: str, pattern: str = "") -> str:
              f"{'vgpr':>4} {'agpr':>4} {'sgpr':>4} {'spill':>5} {'lds_B':>6} {'waves/SIMD':>10}  kernel"]
     for r, n in zip(rows, names):
         n = n.replace("mp::(anonymous namespace)::", "").replace("void ", "")
-        n = n.replace("(mp::SpmmParams)", "").replace("(mp::RadixPass)", "")
+        depth = 0  # drop the parameter list
+        for i, ch in enumerate(n):
+            depth += (ch == "<") - (ch == ">")
+            if ch == "(" and depth == 0:
+                n = n[:i]
+                break
         if pattern and not re.search(pattern, n):
             continue
         lines.append(f"{r.get('VGPRs', '?'):>4} {r.get('AGPRs', '?'):>4} {r.get('TotalSGPRs', '?'):>4} "

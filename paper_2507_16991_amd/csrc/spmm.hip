@@ -47,11 +47,14 @@ constexpr int kUnroll = MP_UNROLL;
 #ifndef MP_SUM_WAVES
 #define MP_SUM_WAVES 6      // unweighted bf16 sums with 32-bit row offsets: the same
 #endif
+// The masked sum (gradient of max) is bound by the latency of its dependent
+// loads: 6 rows per slot step and 2 partials (96 registers, 5 wavefronts per
+// SIMD) measured 8.89 -> 8.51 ms against 8 and 4 on the 124M-edge graph
 #ifndef MP_MASKED_UNROLL
-#define MP_MASKED_UNROLL 8  // the same for the masked sum
+#define MP_MASKED_UNROLL 6  // rows per slot step of the masked sum
 #endif
 #ifndef MP_MASKED_PARTIALS
-#define MP_MASKED_PARTIALS 4  // partial sums per element of the masked sum
+#define MP_MASKED_PARTIALS 2  // partial sums per element of the masked sum
 #endif
 
 // Kernel modes: the plain aggregation (sum/mean and/or max); the masked sum
@@ -282,6 +285,28 @@ struct Acc {
             }
         }
     }
+    // add() when ok, else no change, by selects instead of a branch: the sum
+    // keeps its value, the shifted terms add an exact zero, and max / min take
+    // nothing
+    __device__ inline void add_masked(int a, const float (&v)[EPL], int32_t pos, bool ok) {
+#pragma unroll
+        for (int k = 0; k < EPL; ++k) {
+            if constexpr (HS) s[a][k] = ok ? s[a][k] + v[k] : s[a][k];
+            if constexpr (HM) {
+                const bool take = ok && v[k] > m[a][k];
+                m[a][k] = take ? v[k] : m[a][k];
+                i[a][k] = take ? pos : i[a][k];
+            }
+            if constexpr (HX) {
+                const float dv = ok ? sub_rounded(v[k], K[k]) : 0.f;
+                d[a][k] += dv;
+                q[a][k] = __builtin_fmaf(dv, dv, q[a][k]);
+                const bool take = ok && v[k] < n[a][k];
+                n[a][k] = take ? v[k] : n[a][k];
+                j[a][k] = take ? pos : j[a][k];
+            }
+        }
+    }
     // After the gather: a partial that received messages but is still empty
     // (position -1) saw only -inf messages (+inf for min), since any other
     // message replaces the initial -inf; its answer is its first message,
@@ -353,6 +378,16 @@ using AccFor = Acc<EPL, HS, HM, MODE == kModeStats,
                    MODE == kModeStats    ? (sizeof(TX) == 4 ? 1 : 2)
                    : MODE == kModeMasked ? MP_MASKED_PARTIALS
                                          : (HM ? (HS ? 2 : MP_MAX_PARTIALS) : 4)>;
+
+// Steps with missing edges accumulate by selects (no branches) for sums and
+// fp32 max, whose kernels are bound by memory: the branches cost more than
+// the work of the missing edges.  bf16 max, fused sum and max, and the
+// statistics skip missing edges instead: the first is bound by its vector
+// instructions, which a select step spends on every edge slot, and for the
+// others the selects cost more registers than the branches.  Typed tables
+// (short relation rows, mostly tail steps) skip them too.
+template <typename TX, bool HS, bool HM>
+constexpr bool kSelectTail = HS ? !HM : sizeof(TX) == 4;
 
 typedef uint32_t u32x4 __attribute__((ext_vector_type(4)));
 typedef uint32_t u32x2 __attribute__((ext_vector_type(2)));
@@ -501,6 +536,7 @@ __device__ inline void wave_range(const SpmmParams& P,
     e1 = uniform64(e1);
     const int64_t fe_ld = feat_ok ? fe : 0;
     const bool full_u = U == UN;
+    constexpr bool SEL = kSelectTail<TX, HS, HM> && NT == 1;
     // column indices (and weights) of the tile at q, one per lane
     auto load_tile = [&](int64_t q, int32_t& c, float& w) {
         c = 0;
@@ -513,21 +549,27 @@ __device__ inline void wave_range(const SpmmParams& P,
     // a step whose edges may run past the range (t >= rem) or with U < UN;
     // set_shift: the row's first step, whose slot-0 messages (edges u * S of
     // the row) give the row's shift, passed from slot 0's lane j to lane j of
-    // every slot
+    // every slot.  With one reduction (sum or max), loads are unconditional
+    // (a lane's column is a valid row even for a missing edge: a column of the
+    // tile, or 0 past its end) and missing edges accumulate nothing, by
+    // selects; with both (fused sum and max, statistics) the selects cost more
+    // registers than the branches, and missing edges are skipped.
     auto general_step = [&](int64_t p0, int32_t myc, float myw, int base, bool set_shift) {
         const int64_t rem = e1 - p0;
-        int32_t cu[UN];
         bool ok[UN];
+        R raw[UN];
 #pragma unroll
         for (int u = 0; u < UN; ++u) {
             const int t = base + u * S + slot;
-            cu[u] = __shfl(myc, t);
             ok[u] = feat_ok && (u < U) && (t < rem);
+            // every lane takes part in the permute (an inactive source lane
+            // would not supply its column)
+            const int32_t c = __shfl(myc, t);
+            if constexpr (SEL)
+                raw[u] = load_chunk<TX, EPL, NT, O32>(P, c, fe_ld);
+            else if (ok[u])
+                raw[u] = load_chunk<TX, EPL, NT, O32>(P, c, fe);
         }
-        R raw[UN];
-#pragma unroll
-        for (int u = 0; u < UN; ++u)
-            if (ok[u]) raw[u] = load_chunk<TX, EPL, NT, O32>(P, cu[u], fe);
         if constexpr (MODE == kModeStats) {
             if (set_shift) {
                 float t[EPL] = {};
@@ -554,15 +596,57 @@ __device__ inline void wave_range(const SpmmParams& P,
             const int t = base + u * S + slot;
             float wt = 1.f;
             if constexpr (W) wt = __shfl(myw, t);
-            if (ok[u]) {
+            if (SEL || ok[u]) {
                 float v[EPL];
                 widen<TX, EPL>(raw[u], v);
                 if constexpr (W) {
 #pragma unroll
                     for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt, v[k]);
                 }
-                acc.add(u % A, v, (int32_t)(p0 + t));
+                if constexpr (SEL)
+                    acc.add_masked(u % A, v, (int32_t)(p0 + t), ok[u]);
+                else
+                    acc.add(u % A, v, (int32_t)(p0 + t));
             }
+        }
+    };
+    // a full step: every edge exists, no per-edge conditions; set_shift:
+    // the row's first step, as in general_step
+    auto full_step = [&](int64_t p0, int32_t myc, float myw, int base, bool set_shift) {
+        R raw[UN];
+#pragma unroll
+        for (int u = 0; u < UN; ++u)
+            raw[u] = load_chunk<TX, EPL, NT, O32>(P, __shfl(myc, base + u * S + slot), fe_ld);
+        const int32_t pos = (int32_t)(p0 + base) + slot;
+        // message u of this lane's slot (weighted)
+        auto message = [&](int u, float (&v)[EPL]) {
+            widen<TX, EPL>(raw[u], v);
+            if constexpr (W) {
+                const float wt = __shfl(myw, base + u * S + slot);
+#pragma unroll
+                for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt, v[k]);
+            }
+        };
+        if constexpr (MODE == kModeStats) {
+            if (set_shift) {
+                float t[EPL] = {};
+#pragma unroll
+                for (int u = 0; u < UN; ++u) {
+                    float v[EPL];
+                    message(u, v);
+#pragma unroll
+                    for (int k = 0; k < EPL; ++k) t[k] += v[k];
+                }
+#pragma unroll
+                for (int k = 0; k < EPL; ++k) t[k] = __shfl(t[k], j);
+                acc.set_shift(t, UN);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < UN; ++u) {
+            float v[EPL];
+            message(u, v);
+            acc.add(u % A, v, pos + u * S);
         }
     };
     int32_t myc;
@@ -571,7 +655,10 @@ __device__ inline void wave_range(const SpmmParams& P,
     int st0 = 0;
     if constexpr (MODE == kModeStats) {
         if (shift_first && e0 < e1) {
-            general_step(e0, myc, myw, 0, true);
+            if (full_u && SU <= e1 - e0)
+                full_step(e0, myc, myw, 0, true);
+            else
+                general_step(e0, myc, myw, 0, true);
             st0 = 1;
         }
     }
@@ -580,26 +667,7 @@ __device__ inline void wave_range(const SpmmParams& P,
         const int64_t nf = full_u ? rem / SU : 0;
         const int nfull = nf < steps ? (int)nf : steps;
         int st = st0;
-        // full steps: every edge exists, no per-edge conditions
-        for (; st < nfull; ++st) {
-            const int base = st * SU;
-            R raw[UN];
-#pragma unroll
-            for (int u = 0; u < UN; ++u)
-                raw[u] = load_chunk<TX, EPL, NT, O32>(P, __shfl(myc, base + u * S + slot), fe_ld);
-            const int32_t pos = (int32_t)(p0 + base) + slot;
-#pragma unroll
-            for (int u = 0; u < UN; ++u) {
-                float v[EPL];
-                widen<TX, EPL>(raw[u], v);
-                if constexpr (W) {
-                    const float wt = __shfl(myw, base + u * S + slot);
-#pragma unroll
-                    for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt, v[k]);
-                }
-                acc.add(u % A, v, pos + u * S);
-            }
-        }
+        for (; st < nfull; ++st) full_step(p0, myc, myw, st * SU, false);
         for (; st < steps; ++st) {
             const int base = st * SU;
             if (base >= rem) break;
@@ -859,8 +927,12 @@ __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MOD
     constexpr int UN = unroll_of<MODE, HS, HM>();
     const int L = P.L;
     const int64_t fe_ld = feat_ok ? fe : 0;
+    constexpr bool SEL = kSelectTail<TX, HS, HM> && NT == 1;
     // an iteration in which a slot's row may end (it + u >= my_n); set_shift:
-    // the first one, whose messages give the row's shift
+    // the first one, whose messages give the row's shift.  With one
+    // reduction, loads are unconditional (a missing edge's column is 0, a
+    // valid row) and missing edges accumulate nothing, by selects; with both,
+    // missing edges are skipped (as in wave_range).
     auto general_iter = [&](int32_t it, bool set_shift) {
         int32_t cc[UN];
         bool ok[UN];
@@ -891,8 +963,12 @@ __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MOD
         }
         R raw[UN];
 #pragma unroll
-        for (int u = 0; u < UN; ++u)
-            if (ok[u]) raw[u] = load_chunk<TX, EPL, NT, O32>(P, cc[u], fe);
+        for (int u = 0; u < UN; ++u) {
+            if constexpr (SEL)
+                raw[u] = load_chunk<TX, EPL, NT, O32>(P, cc[u], fe_ld);
+            else if (ok[u])
+                raw[u] = load_chunk<TX, EPL, NT, O32>(P, cc[u], fe);
+        }
         if constexpr (MODE == kModeStats) {
             if (set_shift) {  // the mean of the row's first UN messages
                 float t[EPL] = {};
@@ -910,48 +986,73 @@ __device__ inline void slot_row(const SpmmParams& P, AccFor<TX, EPL, HS, HM, MOD
         }
 #pragma unroll
         for (int u = 0; u < UN; ++u) {
-            if (ok[u]) {
+            if (SEL || ok[u]) {
                 float v[EPL];
                 widen<TX, EPL>(raw[u], v);
                 if constexpr (W) {
 #pragma unroll
                     for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt[u], v[k]);
                 }
-                acc.add(u % A, v, (int32_t)(e0 + it + u));
+                if constexpr (SEL)
+                    acc.add_masked(u % A, v, (int32_t)(e0 + it + u), ok[u]);
+                else
+                    acc.add(u % A, v, (int32_t)(e0 + it + u));
             }
+        }
+    };
+    // every slot's row has UN more edges: no per-edge conditions (COOP);
+    // set_shift: the first iteration, as in general_iter
+    auto full_iter = [&](int32_t it, bool set_shift) {
+        int32_t myc = 0;
+        float myw = 1.f;
+        if (j < UN && it + j < my_n) {
+            myc = col_at(P, e0 + it + j);
+            if constexpr (W) myw = __builtin_nontemporal_load(P.w + e0 + it + j);
+        }
+        R raw[UN];
+#pragma unroll
+        for (int u = 0; u < UN; ++u)
+            raw[u] = load_chunk<TX, EPL, NT, O32>(P, __shfl(myc, slot * L + u), fe_ld);
+        const int32_t pos = (int32_t)(e0 + it);
+        // message u of this lane's row (weighted)
+        auto message = [&](int u, float (&v)[EPL]) {
+            widen<TX, EPL>(raw[u], v);
+            if constexpr (W) {
+                const float wt = __shfl(myw, slot * L + u);
+#pragma unroll
+                for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt, v[k]);
+            }
+        };
+        if constexpr (MODE == kModeStats) {
+            if (set_shift) {
+                float t[EPL] = {};
+#pragma unroll
+                for (int u = 0; u < UN; ++u) {
+                    float v[EPL];
+                    message(u, v);
+#pragma unroll
+                    for (int k = 0; k < EPL; ++k) t[k] += v[k];
+                }
+                acc.set_shift(t, UN);
+            }
+        }
+#pragma unroll
+        for (int u = 0; u < UN; ++u) {
+            float v[EPL];
+            message(u, v);
+            acc.add(u % A, v, pos + u);
         }
     };
     int32_t it = 0;
     if constexpr (MODE == kModeStats) {
-        general_iter(0, true);
+        if (COOP && UN <= min_n)
+            full_iter(0, true);
+        else
+            general_iter(0, true);
         it = UN;
     }
     if constexpr (COOP) {
-        // every slot's row has UN more edges: no per-edge conditions
-        for (; it + UN <= min_n; it += UN) {
-            int32_t myc = 0;
-            float myw = 1.f;
-            if (j < UN && it + j < my_n) {
-                myc = col_at(P, e0 + it + j);
-                if constexpr (W) myw = __builtin_nontemporal_load(P.w + e0 + it + j);
-            }
-            R raw[UN];
-#pragma unroll
-            for (int u = 0; u < UN; ++u)
-                raw[u] = load_chunk<TX, EPL, NT, O32>(P, __shfl(myc, slot * L + u), fe_ld);
-            const int32_t pos = (int32_t)(e0 + it);
-#pragma unroll
-            for (int u = 0; u < UN; ++u) {
-                float v[EPL];
-                widen<TX, EPL>(raw[u], v);
-                if constexpr (W) {
-                    const float wt = __shfl(myw, slot * L + u);
-#pragma unroll
-                    for (int k = 0; k < EPL; ++k) v[k] = __fmul_rn(wt, v[k]);
-                }
-                acc.add(u % A, v, pos + u);
-            }
-        }
+        for (; it + UN <= min_n; it += UN) full_iter(it, false);
     }
     for (; it < max_n; it += UN) general_iter(it, false);
     if constexpr (HM) {
