@@ -414,6 +414,11 @@ def backward_step(g, mp, torch, np, dev, mark):
                               mp.MP_SUM, gw, ws_w, ws_w.numel())
         mark(evs, i + 1)
 
+    # the gather ceilings: G's rows in the transposed CSR's column order, as
+    # the sum and mean gradients read them, and one 16-byte chunk of each (a
+    # scattered read per edge: the access pattern of the max gradient's won
+    # chunks and mask words)
+    g.probe = {"col": colT, "tables": {"G": (G, F * 4, F * 4)}, "chunk16": (G, F * 4)}
     return g, step, ops
 
 
@@ -759,6 +764,10 @@ def run(args):
     ceil = measure_ceilings(g, mp, torch, np, dev) if args.ceilings and hasattr(g, "probe") \
         else None
     if ceil:
+        for n in names:  # gradients over the transposed CSR against G's gather
+            if "gather_G" in ceil and n in ("grad_x_sum_f32", "grad_x_mean_f32"):
+                breakdown[n]["frac_of_gather_ceiling"] = round(
+                    breakdown[n]["GB_per_s"] / ceil["gather_G"]["GB_per_s"], 4)
         for n in names:  # aggregations against the gather of their own table
             k = n.rsplit("_", 1)[-1]
             if f"gather_{k}" in ceil and n.split("_")[0] in ("sum", "mean", "max", "wsum",
@@ -898,6 +907,13 @@ def measure_ceilings(g, mp, torch, np, dev, reps=5):
             "ms": round(ms, 4), "GB_per_s": round(E * (4 + row) / (ms * 1e-3) / 1e9, 1),
             "what": f"{E} rows of {row} B ({k} features, rows {stride} B apart) gathered in CSR "
                     f"column order, 16-byte loads"}
+    if "chunk16" in g.probe:
+        x, stride = g.probe["chunk16"]
+        ms = timed(lambda: mp.mp_probe_gather(col, E, x, stride, 16, sink))
+        res["chunk16"] = {
+            "ms": round(ms, 4), "G_reads_per_s": round(E / (ms * 1e-3) / 1e9, 2),
+            "what": f"{E} scattered 16-byte reads: the first chunk of each row (rows {stride} B "
+                    f"apart) in CSR column order"}
     return res
 
 

@@ -442,9 +442,10 @@ __device__ inline void store_row(const SpmmParams& P, int64_t row, int64_t fe, i
     if (hs) {
         float v[EPL];
         const bool mean = (P.reduce & kMean) != 0;
-        const float dv = (float)deg;
+        // one division per lane, then products (within 2 ulp of the quotient)
+        const float inv = deg > 0 ? 1.f / (float)deg : 0.f;
 #pragma unroll
-        for (int k = 0; k < EPL; ++k) v[k] = mean ? (deg > 0 ? s[k] / dv : 0.f) : s[k];
+        for (int k = 0; k < EPL; ++k) v[k] = mean ? s[k] * inv : s[k];
         if (P.out_bf16) {
             uint16_t b[EPL];
 #pragma unroll
@@ -474,7 +475,10 @@ __device__ inline void store_row(const SpmmParams& P, int64_t row, int64_t fe, i
 // Stats mode: write every requested statistic of a finished row (fp32).
 // s is the plain sum; d and q the sums of (m - K) and (m - K)^2 for the
 // row's shift K.  Variance is the population variance
-// q / deg - (d / deg)^2 (shift-invariant), clamped at 0.
+// q / deg - (d / deg)^2 (shift-invariant), clamped at 0, with exact
+// quotients (they cancel exactly on a row of equal messages, whose variance
+// is then exactly 0); the mean is a product with one reciprocal of the
+// degree per lane (within 2 ulp of the quotient).
 template <int EPL>
 __device__ inline void store_stats(const SpmmParams& P, int64_t row, int64_t fe, int64_t deg,
                                    const float (&s)[EPL], const float (&d)[EPL],
@@ -483,10 +487,11 @@ __device__ inline void store_stats(const SpmmParams& P, int64_t row, int64_t fe,
                                    const int32_t (&in)[EPL], bool vec) {
     const int64_t o = row * P.F + fe;
     const float dv = (float)deg;
+    const float inv = deg > 0 ? 1.f / dv : 0.f;
     float mean[EPL], var[EPL], sd[EPL], mx[EPL], mn[EPL];
 #pragma unroll
     for (int k = 0; k < EPL; ++k) {
-        mean[k] = deg > 0 ? s[k] / dv : 0.f;
+        mean[k] = s[k] * inv;
         const float c = d[k] / dv;
         const float v = deg > 0 ? q[k] / dv - c * c : 0.f;
         var[k] = v > 0.f ? v : 0.f;
