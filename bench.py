@@ -758,6 +758,9 @@ def run(args):
                       "cold_ms_min": round(float(np.min(cold[n])), 4),
                       "cold_GB_per_s": gbs(op_bytes[n], cm)})
         breakdown[n] = d
+    for n in names:  # the sorts: edges (keys) per second
+        if n in ("csr", "transpose", "hetero_build"):
+            breakdown[n]["keys_per_s"] = round(E / (op_ms[n] * 1e-3), -6)
     if getattr(g, "flops_per_op", 0):
         for n in names:  # every projection op is 2 N F F' flops
             breakdown[n]["TFLOP_per_s"] = round(g.flops_per_op / (op_ms[n] * 1e-3) / 1e12, 1)
