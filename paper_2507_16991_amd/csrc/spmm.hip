@@ -369,23 +369,25 @@ struct Acc {
     }
 };
 
-// Accumulator of a kernel instance.  Stats mode keeps six running values per
-// element: with fp32 features one partial (the registers of a second would
-// cost occupancy, and the gathers, not the adds, bound it); with bf16
-// features, whose rows arrive twice as fast, two.
+// Accumulator of a kernel instance.  Stats mode keeps seven running values
+// per element in one partial for either feature dtype: the kernel is bound by
+// its vector instructions, and a second partial costs registers and
+// instructions (bf16 statistics: 8.79 -> 8.57 ms with one partial on the
+// 124M-edge graph) without shortening anything that limits it.
 template <typename TX, int EPL, bool HS, bool HM, int MODE>
 using AccFor = Acc<EPL, HS, HM, MODE == kModeStats,
-                   MODE == kModeStats    ? (sizeof(TX) == 4 ? 1 : 2)
+                   MODE == kModeStats    ? 1
                    : MODE == kModeMasked ? MP_MASKED_PARTIALS
                                          : (HM ? (HS ? 2 : MP_MAX_PARTIALS) : 4)>;
 
 // Steps with missing edges accumulate by selects (no branches) for sums and
 // fp32 max, whose kernels are bound by memory: the branches cost more than
 // the work of the missing edges.  bf16 max, fused sum and max, and the
-// statistics skip missing edges instead: the first is bound by its vector
-// instructions, which a select step spends on every edge slot, and for the
-// others the selects cost more registers than the branches.  Typed tables
-// (short relation rows, mostly tail steps) skip them too.
+// statistics skip missing edges instead: the first and the last are bound by
+// their vector instructions, which a select step spends on every edge slot
+// (fp32 statistics measured 10.32 -> 10.72 ms with selects), and for fused
+// sum and max the selects cost more registers than the branches.  Typed
+// tables (short relation rows, mostly tail steps) skip them too.
 template <typename TX, bool HS, bool HM>
 constexpr bool kSelectTail = HS ? !HM : sizeof(TX) == 4;
 
