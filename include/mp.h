@@ -123,7 +123,8 @@ int mp_coo_to_csr_workspace(int64_t E, int64_t N, int rowptr_itype, int with_pay
  *   status      [1] int32 (device) or NULL: written on `stream` after the
  *               sort, MP_OK if it completed, MP_ERR_SORT if a tile of the
  *               sort gave up its bounded wait for an earlier tile's counts
- *               (then rowptr, col, perm and val_out are invalid).  The wait
+ *               (then col, perm and val_out are invalid and rowptr is not
+ *               written).  The wait
  *               only spans tiles that are already running, so this is a
  *               guard against a hung device, not an expected outcome; read
  *               the word once the stream's work is done.
@@ -138,7 +139,8 @@ int mp_coo_to_csr(const int32_t* src, const int32_t* dst, int64_t E, int64_t N,
  * is derived from dst directly, col = src, perm = 0..E-1 and val_out =
  * val_in (each optional output as in mp_coo_to_csr).  The caller asserts the
  * order; mp_validate_sorted counts violations.  No workspace.  If dst is not
- * non-decreasing the outputs are unspecified (but stay in bounds). */
+ * non-decreasing the outputs are unspecified (but stay in bounds, and the
+ * work stays bounded: rowptr is found by one binary search per row). */
 int mp_sorted_coo_to_csr(const int32_t* src, const int32_t* dst, int64_t E, int64_t N,
                          void* rowptr, int rowptr_itype, int32_t* col, int32_t* perm,
                          const float* val_in, float* val_out, void* stream);

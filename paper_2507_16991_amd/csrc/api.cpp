@@ -108,7 +108,7 @@ int coo_to_csr_impl(const int32_t* src, const int32_t* dst, int64_t E, int64_t N
         a_in = rp.a_out;
         b_in = rp.b_out;
     }
-    hipError_t e = launch_rowptr_from_sorted(L.kA, E, N, rowptr, rp64, s);
+    hipError_t e = launch_rowptr_from_sorted(L.kA, E, N, rowptr, rp64, L.sc.err, s);
     if (e != hipSuccess) return MP_ERR_HIP;
     if (val_in && val_out) {
         e = launch_gather_f32(val_in, eid_final, E, val_out, s);
@@ -511,9 +511,10 @@ int mp_sorted_coo_to_csr(const int32_t* src, const int32_t* dst, int64_t E, int6
     hipStream_t s = as_stream(stream);
     const int rp64 = rowptr_itype == MP_I64;
     if (E == 0) return hip_status(launch_fill_rowptr_zero(N, rowptr, rp64, s));
-    // the sorted keys are dst itself (non-negative int32 read as uint32)
-    hipError_t e = launch_rowptr_from_sorted(reinterpret_cast<const uint32_t*>(dst), E, N,
-                                             rowptr, rp64, s);
+    // the sorted keys are dst itself (non-negative int32 read as uint32);
+    // a binary search per row keeps the work bounded if dst is not sorted
+    hipError_t e = launch_rowptr_by_search(reinterpret_cast<const uint32_t*>(dst), E, N,
+                                           rowptr, rp64, s);
     if (e == hipSuccess) e = launch_offset_copy(src, E, 0, col, s);
     if (e == hipSuccess && perm) e = launch_iota(E, perm, s);
     if (e == hipSuccess && val_in) e = launch_copy_f32(val_in, E, val_out, s);

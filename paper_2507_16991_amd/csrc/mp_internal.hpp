@@ -15,7 +15,7 @@ constexpr int kWave = 64;
 
 // ---- radix sort geometry (COO -> CSR) ---------------------------------------
 #ifndef MP_SORT_BLOCK
-#define MP_SORT_BLOCK 512
+#define MP_SORT_BLOCK 1024
 #endif
 #ifndef MP_SORT_ITEMS
 #define MP_SORT_ITEMS 16
@@ -84,8 +84,14 @@ hipError_t radix_sort_pass(const RadixPass& p, hipStream_t s);
 // Write the caller's status word (nullptr: nothing) from the error word of
 // the sort that used sc (sc nullptr: no sort ran, MP_OK).
 hipError_t launch_sort_status(const RadixScratch* sc, int32_t* status, hipStream_t s);
+// rowptr of keys sorted by a radix sort whose error word is sort_err (the
+// kernel does nothing when the sort failed); nullptr: no such word
 hipError_t launch_rowptr_from_sorted(const uint32_t* keys, int64_t E, int64_t N, void* rowptr,
-                                     int rp64, hipStream_t s);
+                                     int rp64, const uint32_t* sort_err, hipStream_t s);
+// rowptr of keys sorted by the caller, by binary search (bounded work for
+// any order of keys)
+hipError_t launch_rowptr_by_search(const uint32_t* keys, int64_t E, int64_t N, void* rowptr,
+                                   int rp64, hipStream_t s);
 hipError_t launch_fill_rowptr_zero(int64_t N, void* rowptr, int rp64, hipStream_t s);
 hipError_t launch_gather_f32(const float* in, const int32_t* idx, int64_t n, float* out,
                              hipStream_t s);

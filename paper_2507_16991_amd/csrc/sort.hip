@@ -135,21 +135,25 @@ __global__ void radix_gscan(uint32_t* __restrict__ g, int passes, int bits) {
 // look-back can keep kLookWindow descriptor loads in flight.  Descriptors of
 // a pass over R = 2^bits digits lie R apart per tile.
 //   HAS_B: the second payload is carried.
-//   WIDE:  digits of up to 9 bits (512 buckets).  Their per-wave counters take
-//          twice the LDS, so the keys and the payloads go through ONE staging
-//          buffer in turn (keys staged before the look-back, each payload
-//          after the previous array is written), which keeps two tiles per CU.
-//          Narrow passes (up to 8 bits) stage all arrays at once.
+//   WIDE:  digits of up to 9 bits (512 buckets: twice the per-wave counters).
+// A tile's arrays are staged in LDS all at once where they fit beside the
+// counters (narrow digits, one payload); otherwise (ONEBUF) the keys and
+// then each payload go through one staging buffer in turn: keys before the
+// look-back, each payload after the previous array is written.
 constexpr int kLookWindow = 4;
+// tiles resident per CU, as the LDS allows: two of 512 threads or one of 1024
+constexpr int kSortTilesPerCU = kSortBlock >= 1024 ? 1 : 2;
 
 template <bool HAS_B, bool WIDE>
 __global__ __launch_bounds__(kSortBlock)
-__attribute__((amdgpu_waves_per_eu(HAS_B ? 1 : 2 * kSortBlock / 256)))  // two tiles per CU
+__attribute__((amdgpu_waves_per_eu(HAS_B ? 1 : kSortTilesPerCU * kSortBlock / 256)))
 void radix_onesweep(RadixPass p) {
     constexpr int NB = WIDE ? kMaxBuckets : kMaxBuckets / 2;  // buckets this variant handles
-    constexpr int NSTAGE = WIDE ? 1 : (HAS_B ? 3 : 2);         // staging arrays
+    // all arrays staged at once where they fit in LDS, else one at a time
+    constexpr bool ONEBUF = WIDE || (HAS_B ? 3 : 2) * kSortTile * 4 > 128 * 1024;
+    constexpr int NSTAGE = ONEBUF ? 1 : (HAS_B ? 3 : 2);  // staging arrays
     __shared__ uint32_t s_stage[NSTAGE][kSortTile];
-    __shared__ uint16_t s_lp[WIDE ? kSortTile : 1];  // WIDE: staged slot of every key
+    __shared__ uint16_t s_lp[ONEBUF ? kSortTile : 1];  // ONEBUF: staged slot of every key
     __shared__ uint32_t s_cnt[kSortWaves][NB];
     __shared__ uint32_t s_tcnt[NB];   // the tile's count of each digit
     __shared__ uint32_t s_start[NB];  // ... and its exclusive scan
@@ -238,8 +242,8 @@ void radix_onesweep(RadixPass p) {
     __syncthreads();
 
     // stage the tile in LDS in digit order (tile-local positions only): all
-    // arrays, or for WIDE passes the keys alone (each key's slot is kept in
-    // LDS for the payloads)
+    // arrays, or with ONEBUF the keys alone (each key's slot is kept in LDS
+    // for the payloads)
 #pragma unroll
     for (int k = 0; k < kSortItems; ++k) {
         const int64_t i = wbase + (int64_t)k * kWave + lane;
@@ -247,7 +251,7 @@ void radix_onesweep(RadixPass p) {
         const uint32_t lp = s_start[d] + s_cnt[wv][d] + rank[k];
         if (i < p.n) {
             s_stage[0][lp] = key[k];
-            if constexpr (WIDE) {
+            if constexpr (ONEBUF) {
                 s_lp[k * kSortBlock + threadIdx.x] = (uint16_t)lp;
             } else {
                 s_stage[1][lp] = (uint32_t)va[k];
@@ -305,19 +309,19 @@ void radix_onesweep(RadixPass p) {
 
     // write the digit runs: thread t takes staged slots t, t + kSortBlock, ...
     const int64_t nvalid = (p.n - tbase) < kSortTile ? (p.n - tbase) : kSortTile;
-    int32_t pos[WIDE ? kSortItems : 1];
+    int32_t pos[ONEBUF ? kSortItems : 1];
 #pragma unroll
     for (int k = 0; k < kSortItems; ++k) {
         const int i = (int)threadIdx.x + k * kSortBlock;
-        if constexpr (WIDE) pos[k] = -1;
+        if constexpr (ONEBUF) pos[k] = -1;
         if (i < nvalid) {
             const uint32_t kk = s_stage[0][i];
             const uint32_t d = (kk >> p.shift) & (uint32_t)(R - 1);
             const int64_t q = (int64_t)s_gbase[d] + (i - (int64_t)s_start[d]);
             if (q < p.n) {  // cannot fail for consistent counts; never write past n
-                if constexpr (WIDE) pos[k] = (int32_t)q;
+                if constexpr (ONEBUF) pos[k] = (int32_t)q;
                 if (p.keys_out) p.keys_out[q] = kk;
-                if constexpr (!WIDE) {
+                if constexpr (!ONEBUF) {
                     if (p.a_out) p.a_out[q] = (int32_t)s_stage[1][i];
                     if constexpr (HAS_B) {
                         if (p.b_out) p.b_out[q] = (int32_t)s_stage[2][i];
@@ -326,7 +330,7 @@ void radix_onesweep(RadixPass p) {
             }
         }
     }
-    if constexpr (WIDE) {
+    if constexpr (ONEBUF) {
         // the payloads, one at a time through the same buffer
         for (int which = 0; which < (HAS_B ? 2 : 1); ++which) {
             int32_t* out = which == 0 ? p.a_out : p.b_out;
@@ -361,10 +365,14 @@ constexpr int kRowptrItems = 8;
 
 template <typename RP, bool VEC>
 __global__ __launch_bounds__(256) void rowptr_from_sorted(const uint32_t* __restrict__ keys,
-                                                          int64_t E, int64_t N, RP* __restrict__ rowptr) {
+                                                          int64_t E, int64_t N, RP* __restrict__ rowptr,
+                                                          const uint32_t* __restrict__ sort_err) {
     static_assert(kRowptrItems == 8, "two 16-byte loads per thread");
     const int64_t p0 = ((int64_t)blockIdx.x * 256 + threadIdx.x) * kRowptrItems;
     if (p0 > E) return;
+    // keys left unsorted by a failed sort would make the fills below run
+    // over up to N rows per thread; the caller gets MP_ERR_SORT instead
+    if (sort_err && *sort_err) return;
     uint32_t k8[kRowptrItems];
     if (VEC && p0 + kRowptrItems <= E) {
         // VEC: keys is 16-byte aligned and p0 a multiple of 8, so the loads are aligned
@@ -385,6 +393,23 @@ __global__ __launch_bounds__(256) void rowptr_from_sorted(const uint32_t* __rest
         if (cur > N) cur = N;  // keys are < N for valid input; stay inside rowptr regardless
         for (int64_t v = prev + 1; v <= cur; ++v) rowptr[v] = (RP)p;
         if (cur > prev) prev = cur;
+    }
+}
+
+// rowptr[v] = the first position p with keys[p] >= v (E if none), by binary
+// search: the CSR of keys sorted by the caller, with work bounded by
+// (N + 1) * log2(E) reads whatever the order of keys.
+template <typename RP>
+__global__ __launch_bounds__(256) void rowptr_by_search(const uint32_t* __restrict__ keys,
+                                                        int64_t E, int64_t N, RP* __restrict__ rowptr) {
+    for (int64_t v = (int64_t)blockIdx.x * 256 + threadIdx.x; v <= N;
+         v += (int64_t)gridDim.x * 256) {
+        int64_t lo = 0, hi = E;
+        while (lo < hi) {
+            const int64_t mid = (lo + hi) >> 1;
+            if ((int64_t)keys[mid] < v) lo = mid + 1; else hi = mid;
+        }
+        rowptr[v] = (RP)(v == N ? E : lo);
     }
 }
 
@@ -526,22 +551,34 @@ hipError_t launch_sort_status(const RadixScratch* sc, int32_t* status, hipStream
 }
 
 hipError_t launch_rowptr_from_sorted(const uint32_t* keys, int64_t E, int64_t N, void* rowptr,
-                                     int rp64, hipStream_t s) {
+                                     int rp64, const uint32_t* sort_err, hipStream_t s) {
     const unsigned g = grid_for(ceil_div(E + 1, kRowptrItems), 256);
     const bool vec = reinterpret_cast<uintptr_t>(keys) % 16 == 0;
     if (rp64) {
         auto* rp = static_cast<int64_t*>(rowptr);
         if (vec)
-            hipLaunchKernelGGL((rowptr_from_sorted<int64_t, true>), dim3(g), dim3(256), 0, s, keys, E, N, rp);
+            hipLaunchKernelGGL((rowptr_from_sorted<int64_t, true>), dim3(g), dim3(256), 0, s, keys, E, N, rp, sort_err);
         else
-            hipLaunchKernelGGL((rowptr_from_sorted<int64_t, false>), dim3(g), dim3(256), 0, s, keys, E, N, rp);
+            hipLaunchKernelGGL((rowptr_from_sorted<int64_t, false>), dim3(g), dim3(256), 0, s, keys, E, N, rp, sort_err);
     } else {
         auto* rp = static_cast<int32_t*>(rowptr);
         if (vec)
-            hipLaunchKernelGGL((rowptr_from_sorted<int32_t, true>), dim3(g), dim3(256), 0, s, keys, E, N, rp);
+            hipLaunchKernelGGL((rowptr_from_sorted<int32_t, true>), dim3(g), dim3(256), 0, s, keys, E, N, rp, sort_err);
         else
-            hipLaunchKernelGGL((rowptr_from_sorted<int32_t, false>), dim3(g), dim3(256), 0, s, keys, E, N, rp);
+            hipLaunchKernelGGL((rowptr_from_sorted<int32_t, false>), dim3(g), dim3(256), 0, s, keys, E, N, rp, sort_err);
     }
+    return hipGetLastError();
+}
+
+hipError_t launch_rowptr_by_search(const uint32_t* keys, int64_t E, int64_t N, void* rowptr,
+                                   int rp64, hipStream_t s) {
+    const unsigned g = grid_for(N + 1, 256);
+    if (rp64)
+        hipLaunchKernelGGL((rowptr_by_search<int64_t>), dim3(g), dim3(256), 0, s, keys, E, N,
+                           static_cast<int64_t*>(rowptr));
+    else
+        hipLaunchKernelGGL((rowptr_by_search<int32_t>), dim3(g), dim3(256), 0, s, keys, E, N,
+                           static_cast<int32_t*>(rowptr));
     return hipGetLastError();
 }
 

@@ -118,6 +118,20 @@ def test_sorted_coo_to_csr(n, e, itype, offset):
     assert int(cnt.item()) == 0
 
 
+def test_sorted_coo_to_csr_unsorted_input_is_bounded():
+    """dst that is not sorted (a caller's broken promise): the outputs are
+    unspecified but in bounds, and the call finishes (rowptr by one binary
+    search per row, not by fills between consecutive keys)."""
+    n, e = 100_000, 1_000_000
+    dst = graphgen.uniform_ints(7, 2, e, n)  # random order
+    src = graphgen.uniform_ints(7, 1, e, n)
+    rp, col, _, _ = mp.sorted_coo_to_csr(dev(src), dev(dst), n)
+    torch.cuda.synchronize()
+    r = rp.cpu().numpy().astype(np.int64)
+    assert r[0] == 0 and r[-1] == e and r.min() >= 0 and r.max() <= e
+    assert np.array_equal(col.cpu().numpy(), src)
+
+
 def test_validate_sorted_counts_descents():
     dst = np.sort(graphgen.uniform_ints(4, 2, 5000, 100))
     bad = dst.copy()
