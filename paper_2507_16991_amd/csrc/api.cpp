@@ -42,10 +42,20 @@ bool valid_reduce(int r) {
 
 // ---- COO -> CSR workspace layout ---------------------------------------------
 
+// Without the COO-id payload and with more than one pass, the passes before
+// the last write (key, src) packed in 8-byte words, ping-ponging between kv[0]
+// and kv[1]; the last pass writes the keys into the buffer it does not read
+// and src into col.  Otherwise keys and payloads ping-pong as 4-byte arrays.
+#ifndef MP_SORT_PACK
+#define MP_SORT_PACK 1
+#endif
+
 struct CsrLayout {
     int passes, digit;
+    bool packed;
     uint32_t *kA, *kB;
     int32_t *src_tmp, *eid_tmp, *eid_final;
+    uint64_t* kv[2];
     RadixScratch sc;
     size_t bytes;
 };
@@ -55,9 +65,17 @@ CsrLayout csr_layout(void* ws, int64_t E, int64_t N, int with_payload) {
     digit_plan(key_bits(N), &L.passes, &L.digit);
     Carver c(ws);
     const size_t e = (size_t)(E > 0 ? E : 1);
-    L.kA = c.take<uint32_t>(e);
-    L.kB = L.passes > 1 ? c.take<uint32_t>(e) : nullptr;
-    L.src_tmp = L.passes > 1 ? c.take<int32_t>(e) : nullptr;
+    L.packed = MP_SORT_PACK && !with_payload && L.passes > 1;
+    if (L.packed) {
+        L.kv[0] = c.take<uint64_t>(e);
+        L.kv[1] = c.take<uint64_t>(e);
+        // pass passes-1 reads kv[(passes-2) % 2]
+        L.kA = reinterpret_cast<uint32_t*>(L.kv[(L.passes - 1) % 2]);
+    } else {
+        L.kA = c.take<uint32_t>(e);
+        L.kB = L.passes > 1 ? c.take<uint32_t>(e) : nullptr;
+        L.src_tmp = L.passes > 1 ? c.take<int32_t>(e) : nullptr;
+    }
     L.eid_tmp = (with_payload && L.passes > 1) ? c.take<int32_t>(e) : nullptr;
     L.eid_final = with_payload ? c.take<int32_t>(e) : nullptr;
     char* scratch = c.take<char>(radix_scratch_bytes(E));
@@ -89,7 +107,28 @@ int coo_to_csr_impl(const int32_t* src, const int32_t* dst, int64_t E, int64_t N
     if (radix_sort_begin(keys_in, E, L.passes, L.digit, L.sc, s) != hipSuccess) return MP_ERR_HIP;
     const int32_t* a_in = src;
     const int32_t* b_in = nullptr;  // COO id = element index in the first pass
-    for (int p = 0; p < L.passes; ++p) {
+    for (int p = 0; p < L.passes && L.packed; ++p) {
+        RadixPass rp{};
+        if (p == 0) {
+            rp.keys_in = keys_in;
+            rp.a_in = a_in;
+        } else {
+            rp.kv_in = L.kv[(p - 1) % 2];
+        }
+        if (p < L.passes - 1) {
+            rp.kv_out = L.kv[p % 2];
+        } else {
+            rp.keys_out = L.kA;
+            rp.a_out = col;
+        }
+        rp.n = E;
+        rp.pass = p;
+        rp.shift = p * L.digit;
+        rp.bits = L.digit;
+        rp.sc = L.sc;
+        if (radix_sort_pass(rp, s) != hipSuccess) return MP_ERR_HIP;
+    }
+    for (int p = 0; p < L.passes && !L.packed; ++p) {
         const bool last_parity = ((L.passes - 1 - p) % 2) == 0;  // lands where the final pass writes
         RadixPass rp{};
         rp.keys_in = keys_in;

@@ -73,6 +73,10 @@ struct RadixPass {
     uint32_t* keys_out;       // [n] or nullptr
     int32_t* a_out;           // [n] or nullptr
     int32_t* b_out;           // [n] or nullptr
+    // packed (key << 32 | payload a) words in place of keys_in and a_in
+    // (kv_in) or keys_out and a_out (kv_out); not with payload b
+    const uint64_t* kv_in;    // [n] or nullptr
+    uint64_t* kv_out;         // [n] or nullptr
     int64_t n;
     int pass, shift, bits;
     RadixScratch sc;

@@ -136,25 +136,37 @@ __global__ void radix_gscan(uint32_t* __restrict__ g, int passes, int bits) {
 // a pass over R = 2^bits digits lie R apart per tile.
 //   HAS_B: the second payload is carried.
 //   WIDE:  digits of up to 9 bits (512 buckets: twice the per-wave counters).
+//   PIN, POUT: the keys and the payload are read (written) as one array of
+//          (key << 32 | payload) words instead of two arrays; between passes
+//          this makes each digit run one contiguous stretch of memory of
+//          twice the length rather than two, which the scattered writes of a
+//          pass favour.  One payload only.
 // A tile's arrays are staged in LDS all at once where they fit beside the
-// counters (narrow digits, one payload); otherwise (ONEBUF) the keys and
-// then each payload go through one staging buffer in turn: keys before the
-// look-back, each payload after the previous array is written.
+// counters (one payload); otherwise (ONEBUF) the keys and then each payload
+// go through one staging buffer in turn: keys before the look-back, each
+// payload after the previous array is written.
 constexpr int kLookWindow = 4;
 // tiles resident per CU, as the LDS allows: two of 512 threads or one of 1024
 constexpr int kSortTilesPerCU = kSortBlock >= 1024 ? 1 : 2;
+constexpr int kMaxLdsBytes = 160 * 1024;  // LDS of one workgroup on gfx950
 
-template <bool HAS_B, bool WIDE>
+template <bool HAS_B, bool WIDE, bool PIN, bool POUT>
 __global__ __launch_bounds__(kSortBlock)
 __attribute__((amdgpu_waves_per_eu(HAS_B ? 1 : kSortTilesPerCU * kSortBlock / 256)))
 void radix_onesweep(RadixPass p) {
+    static_assert(!(HAS_B && (PIN || POUT)), "packed passes carry one payload");
+    static_assert(kSortTile <= 65536, "16-bit counters and staged slots");
     constexpr int NB = WIDE ? kMaxBuckets : kMaxBuckets / 2;  // buckets this variant handles
+    // per-wave digit counts, then each wave's run start inside its digit
+    using cnt_t = uint16_t;
     // all arrays staged at once where they fit in LDS, else one at a time
-    constexpr bool ONEBUF = WIDE || (HAS_B ? 3 : 2) * kSortTile * 4 > 128 * 1024;
+    constexpr int kFixedLds = kSortWaves * NB * (int)sizeof(cnt_t) + 3 * NB * 4 + 16;
+    constexpr bool ONEBUF = (HAS_B ? 3 : 2) * kSortTile * 4 + kFixedLds > kMaxLdsBytes;
+    static_assert(!(ONEBUF && POUT), "a packed write needs the key and the payload at once");
     constexpr int NSTAGE = ONEBUF ? 1 : (HAS_B ? 3 : 2);  // staging arrays
     __shared__ uint32_t s_stage[NSTAGE][kSortTile];
     __shared__ uint16_t s_lp[ONEBUF ? kSortTile : 1];  // ONEBUF: staged slot of every key
-    __shared__ uint32_t s_cnt[kSortWaves][NB];
+    __shared__ cnt_t s_cnt[kSortWaves][NB];
     __shared__ uint32_t s_tcnt[NB];   // the tile's count of each digit
     __shared__ uint32_t s_start[NB];  // ... and its exclusive scan
     __shared__ uint32_t s_gbase[NB];
@@ -179,8 +191,14 @@ void radix_onesweep(RadixPass p) {
     for (int k = 0; k < kSortItems; ++k) {
         const int64_t i = wbase + (int64_t)k * kWave + lane;
         const bool ok = i < p.n;
-        key[k] = ok ? __builtin_nontemporal_load(p.keys_in + i) : 0u;
-        va[k] = p.a_in ? (ok ? __builtin_nontemporal_load(p.a_in + i) : 0) : (int32_t)i;
+        if constexpr (PIN) {
+            const uint64_t kv = ok ? __builtin_nontemporal_load(p.kv_in + i) : 0ull;
+            key[k] = (uint32_t)(kv >> 32);
+            va[k] = (int32_t)(uint32_t)kv;
+        } else {
+            key[k] = ok ? __builtin_nontemporal_load(p.keys_in + i) : 0u;
+            va[k] = p.a_in ? (ok ? __builtin_nontemporal_load(p.a_in + i) : 0) : (int32_t)i;
+        }
         if constexpr (HAS_B) vb[k] = p.b_in ? (ok ? __builtin_nontemporal_load(p.b_in + i) : 0) : (int32_t)i;
     }
 #pragma unroll
@@ -193,7 +211,7 @@ void radix_onesweep(RadixPass p) {
         rank[k] = base + below;
         // the lowest peer advances the counter for all of them; every lane has
         // read the old value above (LDS ops of one wavefront run in order)
-        if (ok && below == 0) s_cnt[wv][d] = base + (uint32_t)__popcll(peers);
+        if (ok && below == 0) s_cnt[wv][d] = (cnt_t)(base + (uint32_t)__popcll(peers));
     }
     __syncthreads();
 
@@ -206,7 +224,7 @@ void radix_onesweep(RadixPass p) {
 #pragma unroll
         for (int w = 0; w < kSortWaves; ++w) {
             uint32_t c = s_cnt[w][d];
-            s_cnt[w][d] = run;
+            s_cnt[w][d] = (cnt_t)run;
             run += c;
         }
         s_tcnt[d] = run;
@@ -320,8 +338,12 @@ void radix_onesweep(RadixPass p) {
             const int64_t q = (int64_t)s_gbase[d] + (i - (int64_t)s_start[d]);
             if (q < p.n) {  // cannot fail for consistent counts; never write past n
                 if constexpr (ONEBUF) pos[k] = (int32_t)q;
-                if (p.keys_out) p.keys_out[q] = kk;
-                if constexpr (!ONEBUF) {
+                if constexpr (POUT) {
+                    p.kv_out[q] = ((uint64_t)kk << 32) | s_stage[1][i];
+                } else if (p.keys_out) {
+                    p.keys_out[q] = kk;
+                }
+                if constexpr (!ONEBUF && !POUT) {
                     if (p.a_out) p.a_out[q] = (int32_t)s_stage[1][i];
                     if constexpr (HAS_B) {
                         if (p.b_out) p.b_out[q] = (int32_t)s_stage[2][i];
@@ -526,20 +548,33 @@ hipError_t radix_sort_begin(const uint32_t* keys, int64_t n, int passes, int bit
     return hipGetLastError();
 }
 
+template <bool WIDE>
+void launch_onesweep_one_payload(const RadixPass& p, unsigned tiles, hipStream_t s) {
+    const dim3 g(tiles), b(kSortBlock);
+    if (p.kv_in && p.kv_out)
+        hipLaunchKernelGGL((radix_onesweep<false, WIDE, true, true>), g, b, 0, s, p);
+    else if (p.kv_in)
+        hipLaunchKernelGGL((radix_onesweep<false, WIDE, true, false>), g, b, 0, s, p);
+    else if (p.kv_out)
+        hipLaunchKernelGGL((radix_onesweep<false, WIDE, false, true>), g, b, 0, s, p);
+    else
+        hipLaunchKernelGGL((radix_onesweep<false, WIDE, false, false>), g, b, 0, s, p);
+}
+
 hipError_t radix_sort_pass(const RadixPass& p, hipStream_t s) {
     if (p.n <= 0) return hipSuccess;
     const int64_t tiles = ceil_div(p.n, kSortTile);
     const bool wide = p.bits > kSortMaxBits - 1;
     if (p.b_out) {
+        if (p.kv_in || p.kv_out) return hipErrorInvalidValue;  // packed passes: one payload
         if (wide)
-            hipLaunchKernelGGL((radix_onesweep<true, true>), dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p);
+            hipLaunchKernelGGL((radix_onesweep<true, true, false, false>), dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p);
         else
-            hipLaunchKernelGGL((radix_onesweep<true, false>), dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p);
+            hipLaunchKernelGGL((radix_onesweep<true, false, false, false>), dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p);
+    } else if (wide) {
+        launch_onesweep_one_payload<true>(p, (unsigned)tiles, s);
     } else {
-        if (wide)
-            hipLaunchKernelGGL((radix_onesweep<false, true>), dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p);
-        else
-            hipLaunchKernelGGL((radix_onesweep<false, false>), dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p);
+        launch_onesweep_one_payload<false>(p, (unsigned)tiles, s);
     }
     return hipGetLastError();
 }
