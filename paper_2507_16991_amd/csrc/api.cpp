@@ -630,10 +630,8 @@ int mp_spmm_plan_build_opts(const void* rowptr, int rowptr_itype, int64_t N_dst,
         e = radix_sort_pass(rp, s);
     }
     if (e == hipSuccess)
-        e = launch_plan_rowrange(rowptr, rp64, L.rowlist, N_dst, L.rowbeg, L.rowend, s);
-    if (e == hipSuccess)
-        e = launch_plan_chunks(rowptr, rp64, L.rowlist, N_dst, p->hub_min, p->chunk_min,
-                               L.chunk_off, s);
+        e = launch_plan_rows(rowptr, rp64, L.rowlist, N_dst, p->hub_min, p->chunk_min, L.rowbeg,
+                             L.rowend, L.chunk_off, s);
     if (e == hipSuccess) e = exclusive_scan_u32(L.chunk_off, N_dst + 1, L.scan_ws, s);
     const int nclass = kClassHub + 1;
     if (e == hipSuccess)

@@ -246,13 +246,13 @@ int64_t gmm_tile_cols();
 
 hipError_t launch_spmm(const SpmmParams& p, int x_dtype, int epl, hipStream_t s);
 hipError_t launch_spmm_tiny(const SpmmParams& p, int x_dtype, int epl, hipStream_t s);
-hipError_t launch_plan_rowrange(const void* rowptr, int rp64, const int32_t* rowlist, int64_t N,
-                                int32_t* rowbeg, int32_t* rowend, hipStream_t s);
 hipError_t launch_spmm_fixup(const SpmmParams& p, hipStream_t s);
 hipError_t launch_plan_classes(const void* rowptr, int rp64, int64_t N, int64_t small_max,
                                int64_t hub_min, uint32_t* keys, hipStream_t s);
-hipError_t launch_plan_chunks(const void* rowptr, int rp64, const int32_t* rowlist, int64_t N,
-                              int64_t hub_min, int chunk_min, uint32_t* nch, hipStream_t s);
+// per rowlist entry: row range and hub chunk count (nch[N] = 0)
+hipError_t launch_plan_rows(const void* rowptr, int rp64, const int32_t* rowlist, int64_t N,
+                            int64_t hub_min, int chunk_min, int32_t* rowbeg, int32_t* rowend,
+                            uint32_t* nch, hipStream_t s);
 // header[c] = first rowlist position of class c (c < nclass, from the class
 // sort's exclusive digit starts), header[nclass] = N, header[nclass+1] = chunks
 hipError_t launch_plan_header(const uint32_t* class_start, int nclass, const uint32_t* chunk_off,

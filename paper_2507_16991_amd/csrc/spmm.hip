@@ -1508,16 +1508,24 @@ __global__ __launch_bounds__(256) void plan_classes(const void* rowptr, int rp64
     keys[i] = c;
 }
 
-// chunks per rowlist entry (0 unless the row is a hub)
-__global__ __launch_bounds__(256) void plan_chunks(const void* rowptr, int rp64,
-                                                   const int32_t* __restrict__ rowlist, int64_t N,
-                                                   int64_t hub_min, int chunk_min,
-                                                   uint32_t* __restrict__ nch) {
+// Per rowlist entry k: the row's range (rowbeg, rowend) and its chunk count
+// (0 unless the row is a hub); entry N gets 0 chunks, so that the scan of
+// the counts ends in the total.  One read of the row's two rowptr entries.
+__global__ __launch_bounds__(256) void plan_rows(const void* rowptr, int rp64,
+                                                 const int32_t* __restrict__ rowlist, int64_t N,
+                                                 int64_t hub_min, int chunk_min,
+                                                 int32_t* __restrict__ rowbeg,
+                                                 int32_t* __restrict__ rowend,
+                                                 uint32_t* __restrict__ nch) {
     const int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x;
     if (k > N) return;
     if (k == N) { nch[k] = 0; return; }
     const int64_t row = rowlist[k];
-    const int64_t d = load_rp(rowptr, rp64, row + 1) - load_rp(rowptr, rp64, row);
+    const int64_t b = load_rp(rowptr, rp64, row);
+    const int64_t e = load_rp(rowptr, rp64, row + 1);
+    rowbeg[k] = (int32_t)b;
+    rowend[k] = (int32_t)e;
+    const int64_t d = e - b;
     uint32_t c = 0;
     if (d > hub_min) {
         int64_t csz = (d + kMaxChunksPerHub - 1) / kMaxChunksPerHub;
@@ -1525,18 +1533,6 @@ __global__ __launch_bounds__(256) void plan_chunks(const void* rowptr, int rp64,
         c = (uint32_t)((d + csz - 1) / csz);
     }
     nch[k] = c;
-}
-
-// row range of every rowlist entry
-__global__ __launch_bounds__(256) void plan_rowrange(const void* rowptr, int rp64,
-                                                     const int32_t* __restrict__ rowlist, int64_t N,
-                                                     int32_t* __restrict__ rowbeg,
-                                                     int32_t* __restrict__ rowend) {
-    const int64_t k = (int64_t)blockIdx.x * 256 + threadIdx.x;
-    if (k >= N) return;
-    const int64_t row = rowlist[k];
-    rowbeg[k] = (int32_t)load_rp(rowptr, rp64, row);
-    rowend[k] = (int32_t)load_rp(rowptr, rp64, row + 1);
 }
 
 // header[c] = start of class c in rowlist (c < nclass), header[nclass] = N,
@@ -1702,14 +1698,6 @@ hipError_t launch_spmm_tiny(const SpmmParams& p, int x_dtype, int epl, hipStream
     }
 }
 
-hipError_t launch_plan_rowrange(const void* rowptr, int rp64, const int32_t* rowlist, int64_t N,
-                                int32_t* rowbeg, int32_t* rowend, hipStream_t s) {
-    if (N <= 0) return hipSuccess;
-    hipLaunchKernelGGL(plan_rowrange, dim3((unsigned)ceil_div(N, 256)), dim3(256), 0, s, rowptr,
-                       rp64, rowlist, N, rowbeg, rowend);
-    return hipGetLastError();
-}
-
 hipError_t launch_spmm_fixup(const SpmmParams& p, hipStream_t s) {
     if (p.n_hub <= 0) return hipSuccess;
     const int64_t waves = p.n_hub * ceil_div(p.F, kWave);
@@ -1731,10 +1719,11 @@ hipError_t launch_plan_classes(const void* rowptr, int rp64, int64_t N, int64_t 
     return hipGetLastError();
 }
 
-hipError_t launch_plan_chunks(const void* rowptr, int rp64, const int32_t* rowlist, int64_t N,
-                              int64_t hub_min, int chunk_min, uint32_t* nch, hipStream_t s) {
-    hipLaunchKernelGGL(plan_chunks, dim3((unsigned)ceil_div(N + 1, 256)), dim3(256), 0, s, rowptr,
-                       rp64, rowlist, N, hub_min, chunk_min, nch);
+hipError_t launch_plan_rows(const void* rowptr, int rp64, const int32_t* rowlist, int64_t N,
+                            int64_t hub_min, int chunk_min, int32_t* rowbeg, int32_t* rowend,
+                            uint32_t* nch, hipStream_t s) {
+    hipLaunchKernelGGL(plan_rows, dim3((unsigned)ceil_div(N + 1, 256)), dim3(256), 0, s, rowptr,
+                       rp64, rowlist, N, hub_min, chunk_min, rowbeg, rowend, nch);
     return hipGetLastError();
 }
 
