@@ -632,7 +632,10 @@ int mp_spmm_plan_build_opts(const void* rowptr, int rowptr_itype, int64_t N_dst,
     if (e == hipSuccess)
         e = launch_plan_rows(rowptr, rp64, L.rowlist, N_dst, p->hub_min, p->chunk_min, L.rowbeg,
                              L.rowend, L.chunk_off, s);
-    if (e == hipSuccess) e = exclusive_scan_u32(L.chunk_off, N_dst + 1, L.scan_ws, s);
+    // only hub rows have chunks, and they end the class-sorted list: the
+    // entries before the hub class's start are zero
+    if (e == hipSuccess)
+        e = exclusive_scan_u32(L.chunk_off, N_dst + 1, L.scan_ws, s, L.sc.gbase + kClassHub);
     const int nclass = kClassHub + 1;
     if (e == hipSuccess)
         e = launch_plan_header(L.sc.gbase, nclass, L.chunk_off, N_dst, L.sc.err, L.header, s);

@@ -47,7 +47,10 @@ constexpr int kScanItems = 16;
 constexpr int kScanTile = kScanBlock * kScanItems;
 size_t scan_workspace_bytes(int64_t n);
 // In-place exclusive scan of data[0..n); returns the hipError of the launches.
-hipError_t exclusive_scan_u32(uint32_t* data, int64_t n, void* ws, hipStream_t s);
+// zero_below (device word, or nullptr): the caller guarantees data[i] = 0 for
+// i < *zero_below, and the tiles wholly below it are skipped.
+hipError_t exclusive_scan_u32(uint32_t* data, int64_t n, void* ws, hipStream_t s,
+                              const uint32_t* zero_below = nullptr);
 
 // ---- stable LSD radix sort, one sweep per digit (sort.hip) ----------------
 //

@@ -37,9 +37,20 @@ __device__ inline uint32_t block_exclusive_scan(uint32_t v, uint32_t* total) {
     return before + inc - v;
 }
 
+// zero_below (device, or nullptr): data[i] = 0 for every i below *zero_below,
+// so tiles that end there have sum 0 and keep their (all-zero) prefixes.
+__device__ inline bool tile_all_zero(const uint32_t* zero_below, int64_t base) {
+    return zero_below && base + kScanTile <= (int64_t)*zero_below;
+}
+
 __global__ __launch_bounds__(kScanBlock) void scan_tile_sums(const uint32_t* __restrict__ in,
-                                                             int64_t n, uint32_t* __restrict__ part) {
+                                                             int64_t n, uint32_t* __restrict__ part,
+                                                             const uint32_t* zero_below) {
     const int64_t base = (int64_t)blockIdx.x * kScanTile;
+    if (tile_all_zero(zero_below, base)) {
+        if (threadIdx.x == 0) part[blockIdx.x] = 0;
+        return;
+    }
     uint32_t s = 0;
 #pragma unroll
     for (int k = 0; k < kScanItems; ++k) {
@@ -67,7 +78,9 @@ __global__ __launch_bounds__(kScanBlock) void scan_partials(uint32_t* __restrict
 
 // Each thread owns kScanItems consecutive elements of the tile.
 __global__ __launch_bounds__(kScanBlock) void scan_apply(uint32_t* __restrict__ data, int64_t n,
-                                                         const uint32_t* __restrict__ part) {
+                                                         const uint32_t* __restrict__ part,
+                                                         const uint32_t* zero_below) {
+    if (tile_all_zero(zero_below, (int64_t)blockIdx.x * kScanTile)) return;
     const int64_t base = (int64_t)blockIdx.x * kScanTile + (int64_t)threadIdx.x * kScanItems;
     uint32_t v[kScanItems];
     uint32_t s = 0;
@@ -94,13 +107,16 @@ size_t scan_workspace_bytes(int64_t n) {
     return align_up((size_t)tiles * sizeof(uint32_t), 256);
 }
 
-hipError_t exclusive_scan_u32(uint32_t* data, int64_t n, void* ws, hipStream_t s) {
+hipError_t exclusive_scan_u32(uint32_t* data, int64_t n, void* ws, hipStream_t s,
+                              const uint32_t* zero_below) {
     if (n <= 0) return hipSuccess;
     const int64_t tiles = ceil_div(n, kScanTile);
     uint32_t* part = static_cast<uint32_t*>(ws);
-    hipLaunchKernelGGL(scan_tile_sums, dim3((unsigned)tiles), dim3(kScanBlock), 0, s, data, n, part);
+    hipLaunchKernelGGL(scan_tile_sums, dim3((unsigned)tiles), dim3(kScanBlock), 0, s, data, n, part,
+                       zero_below);
     hipLaunchKernelGGL(scan_partials, dim3(1), dim3(kScanBlock), 0, s, part, tiles);
-    hipLaunchKernelGGL(scan_apply, dim3((unsigned)tiles), dim3(kScanBlock), 0, s, data, n, part);
+    hipLaunchKernelGGL(scan_apply, dim3((unsigned)tiles), dim3(kScanBlock), 0, s, data, n, part,
+                       zero_below);
     return hipGetLastError();
 }
 
