@@ -1106,14 +1106,15 @@ __device__ inline void hub_shift(const SpmmParams& P, int64_t r0, int64_t deg, b
 }
 
 // Stats mode keeps seven running values per element.  Where they fit
-// (unweighted, 32-bit row offsets, at most 8 accumulated elements per lane),
-// the register budget is capped so that MP_STATS_WAVES wavefronts fit a SIMD
-// without spilling: the gathers need wavefronts in flight more than the
-// scheduler needs the registers.  Unweighted bf16 sums of up to 4 elements
-// per lane with 32-bit row offsets are capped likewise (MP_SUM_WAVES).
+// (unweighted, 32-bit row offsets, at most 4 elements per lane in one
+// partial), the register budget is capped so that MP_STATS_WAVES wavefronts
+// fit a SIMD without spilling: the gathers need wavefronts in flight more
+// than the scheduler needs the registers.  (Eight bf16 elements per lane
+// would spill under that cap.)  Unweighted bf16 sums of up to 4 elements per
+// lane with 32-bit row offsets are capped likewise (MP_SUM_WAVES).
 template <typename TX, int EPL, bool HS, bool HM, bool W, int MODE, bool O32>
 constexpr int waves_hint() {
-    if (MODE == kModeStats && !W && O32 && AccFor<TX, EPL, HS, HM, MODE>::A * EPL <= 8)
+    if (MODE == kModeStats && !W && O32 && AccFor<TX, EPL, HS, HM, MODE>::A * EPL <= 4)
         return MP_STATS_WAVES;
     if (MODE == kModePlain && HS && !HM && !W && O32 && sizeof(TX) == 2 && EPL <= 4)
         return MP_SUM_WAVES;
