@@ -44,6 +44,7 @@ HBM_PEAK_GBS = 8000.0  # MI355X HBM3E, published
 WORKLOAD = "chunglu-124M"
 BACKWARD = "chunglu-124M-backward"
 STACKED = "chunglu-124M-stacked"
+SORT_TILE = 16384  # keys per tile of the library's radix passes (1024 threads x 16)
 PROJECTION = "hetero-20M-projection"
 READOUT = "readout-2.4M"
 EXPLAIN = "chunglu-124M-explain"
@@ -315,6 +316,11 @@ def build_step(args, mp, torch, np, dev):
     # algorithmic row bytes)
     g.probe = {"col": col, "tables": {c[1]: (c[2], c[6] * xs[c[1]][2], F * xs[c[1]][2])
                                       for c in calls if c[0] == "spmm"}}
+    if args.workload == WORKLOAD:
+        # the radix passes' data movement: the first pass's order over dst
+        kb = max(1, (N - 1).bit_length())
+        passes = -(-kb // 9)
+        g.probe["scatter"] = (dst, -(-kb // passes))
     plans = {}
     wss = {}
 
@@ -875,8 +881,10 @@ def measure_ceilings(g, mp, torch, np, dev, reps=5):
     the library's bandwidth probes on this workload's own buffers: a streaming
     read and a copy, and, per feature table, the row gather in CSR column
     order (every edge reads its column index and one row; no reduction, no
-    output).  GB/s of algorithmic bytes (for the gather 4 + F*b per edge),
-    median of `reps` timed runs after one untimed."""
+    output); on the headline graph also a radix pass's data movement (8-byte
+    words scattered into the stable order of dst's first digit).  GB/s of
+    algorithmic bytes (for the gather 4 + F*b per edge, for the scatter 16 per
+    word), median of `reps` timed runs after one untimed."""
     col = g.probe["col"]
     E = int(col.numel())
     sink = torch.zeros(mp.MP_PROBE_SINK_WORDS, dtype=torch.int32, device=dev)
@@ -910,6 +918,36 @@ def measure_ceilings(g, mp, torch, np, dev, reps=5):
             "ms": round(ms, 4), "GB_per_s": round(E * (4 + row) / (ms * 1e-3) / 1e9, 1),
             "what": f"{E} rows of {row} B ({k} features, rows {stride} B apart) gathered in CSR "
                     f"column order, 16-byte loads"}
+    if "scatter" in g.probe:
+        # one radix pass's data movement over the packed (key, payload) words:
+        # every word read in order and written to its place in the stable
+        # order of dst's first digit, first in source order (a scatter that
+        # does not stage), then with the words of each tile of SORT_TILE keys
+        # taken in digit order (the order in which the staged pass writes, so
+        # a wavefront writes consecutive places of one digit run)
+        keys, bits = g.probe["scatter"]
+        n = int(keys.numel())
+        dig = (keys & ((1 << bits) - 1)).to(torch.int64)
+        order = torch.argsort(dig, stable=True)
+        dest = torch.empty(n, dtype=torch.int32, device=dev)
+        dest[order] = torch.arange(n, dtype=torch.int32, device=dev)
+        tile = torch.arange(n, dtype=torch.int64, device=dev) // SORT_TILE
+        staged = torch.argsort(tile * (1 << bits) + dig, stable=True)
+        dest_staged = dest[staged]
+        del order, dig, tile, staged
+        w_in = torch.zeros(n, dtype=torch.int64, device=dev)
+        w_out = torch.empty_like(w_in)
+        for name, d, how in (("scatter8", dest, "in source order"),
+                             ("scatter8_staged", dest_staged,
+                              f"each tile of {SORT_TILE} taken in digit order")):
+            ms = timed(lambda: mp.mp_probe_scatter(w_in, d, n, 8, w_out))
+            res[name] = {
+                "ms": round(ms, 4), "GB_per_s": round(16 * n / (ms * 1e-3) / 1e9, 1),
+                "what": f"{n} 8-byte words read in order ({how}) and written to their places "
+                        f"in the stable order by the low {bits}-bit digit of dst: one packed "
+                        f"radix pass's reads and writes, 16 B per key (the 4-byte "
+                        f"destinations read besides)"}
+        del dest, dest_staged, w_in, w_out
     if "chunk16" in g.probe:
         x, stride = g.probe["chunk16"]
         ms = timed(lambda: mp.mp_probe_gather(col, E, x, stride, 16, sink))

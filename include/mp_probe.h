@@ -42,6 +42,15 @@ int mp_probe_copy(const void* in, void* out, int64_t bytes, void* stream);
 int mp_probe_gather(const int32_t* idx, int64_t n, const void* table, int64_t stride_bytes,
                     int64_t row_bytes, uint32_t* sink, void* stream);
 
+/* Scatter in the order of a destination stream: out[dest[i]] = in[i] for i
+ * in [0, n), with elements of elem_bytes (4 or 8) bytes -- a radix pass's
+ * data movement (reads in order, writes in the digit runs its stable order
+ * makes) with no ranking (traffic: elem_bytes + 4 read and elem_bytes written
+ * per element).  dest must be a permutation of [0, n) (not checked).  in and
+ * out aligned to elem_bytes, dest to 4, no overlap; 0 <= n <= INT32_MAX. */
+int mp_probe_scatter(const void* in, const int32_t* dest, int64_t n, int64_t elem_bytes,
+                     void* out, void* stream);
+
 #ifdef __cplusplus
 }
 #endif

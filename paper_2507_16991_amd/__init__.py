@@ -40,7 +40,7 @@ __all__ = [
     "message_backward", "edge_dot", "mp_copy_rows", "aligned_ld", "pad_rows", "MP_MAX_TYPES",
     "MP_ALL_TYPES", "MP_ERR_SORT", "mp_plan_opts", "mp_spmm_plan_build_opts", "new_status",
     "check_status", "mp_spmm_noalloc", "MP_NOALLOC_SCRATCH_BYTES", "mp_probe_read",
-    "mp_probe_copy", "mp_probe_gather", "MP_PROBE_SINK_WORDS",
+    "mp_probe_copy", "mp_probe_gather", "mp_probe_scatter", "MP_PROBE_SINK_WORDS",
 ]
 
 _HERE = os.path.dirname(os.path.abspath(__file__))
@@ -119,6 +119,7 @@ def lib():
         L.mp_probe_read.argtypes = [p, i64, p, p]
         L.mp_probe_copy.argtypes = [p, p, i64, p]
         L.mp_probe_gather.argtypes = [p, i64, p, i64, i64, p, p]
+        L.mp_probe_scatter.argtypes = [p, p, i64, i64, p, p]
         L.mp_hetero_build_workspace.argtypes = [i32, p, i32, p, i32, i32, psz]
         L.mp_hetero_build.argtypes = [i32, p, i32, p, i32, p, i32, p, p, sz, p, p]
         L.mp_hetero_spmm.argtypes = [i32, p, p, i32, i64, i32, p, p, i32, p, i32, p, i32, p, sz,
@@ -165,7 +166,7 @@ def lib():
                      "mp_spmm_backward_w_workspace", "mp_spmm_backward_w", "mp_spmm_plan_size",
                      "mp_spmm_plan_build", "mp_spmm_plan_build_opts", "mp_spmm_workspace",
                      "mp_spmm", "mp_spmm_noalloc", "mp_probe_read", "mp_probe_copy",
-                     "mp_probe_gather",
+                     "mp_probe_gather", "mp_probe_scatter",
                      "mp_hetero_build_workspace", "mp_hetero_build", "mp_hetero_spmm",
                      "mp_validate_coo", "mp_validate_csr"):
             getattr(L, name).restype = i32
@@ -336,6 +337,11 @@ def mp_probe_gather(idx, n, table, stride_bytes, row_bytes, sink, stream=None):
     tp = table.data_ptr() if isinstance(table, torch.Tensor) else table
     _check("mp_probe_gather", lib().mp_probe_gather(_ptr(idx), n, tp, stride_bytes, row_bytes,
                                                     _ptr(sink), _stream(stream)))
+
+
+def mp_probe_scatter(src, dest, n, elem_bytes, out, stream=None):
+    _check("mp_probe_scatter", lib().mp_probe_scatter(_ptr(src), _ptr(dest), n, elem_bytes,
+                                                      _ptr(out), _stream(stream)))
 
 
 def mp_copy_rows(x_in, ld_in, x_out, ld_out, N, F, dtype, stream=None):

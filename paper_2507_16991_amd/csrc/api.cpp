@@ -1429,6 +1429,16 @@ int mp_probe_gather(const int32_t* idx, int64_t n, const void* table, int64_t st
                                           as_stream(stream)));
 }
 
+int mp_probe_scatter(const void* in, const int32_t* dest, int64_t n, int64_t elem_bytes, void* out,
+                     void* stream) {
+    if (n > 0 && (!in || !dest || !out)) return MP_ERR_NULL;
+    if (n < 0 || n > INT32_MAX || (elem_bytes != 4 && elem_bytes != 8)) return MP_ERR_SIZE;
+    if ((uintptr_t)in % elem_bytes || (uintptr_t)out % elem_bytes || (uintptr_t)dest % 4)
+        return MP_ERR_ALIGN;
+    if (n == 0) return MP_OK;
+    return hip_status(launch_probe_scatter(in, dest, n, (int)elem_bytes, out, as_stream(stream)));
+}
+
 int mp_validate_coo(const int32_t* src, const int32_t* dst, int64_t E, int64_t N_src,
                     int64_t N_dst, int64_t* d_count, void* stream) {
     if (!d_count || (E > 0 && (!src || !dst))) return MP_ERR_NULL;

@@ -299,6 +299,8 @@ hipError_t launch_copy_rows(const void* in, int64_t ld_in, void* out, int64_t ld
 // ---- bandwidth probes (probe.hip) ---------------------------------------------
 hipError_t launch_probe_read(const void* p, int64_t n16, uint32_t* sink, hipStream_t s);
 hipError_t launch_probe_copy(const void* in, void* out, int64_t n16, hipStream_t s);
+hipError_t launch_probe_scatter(const void* in, const int32_t* dest, int64_t n, int elem_bytes,
+                                void* out, hipStream_t s);
 hipError_t launch_probe_gather(const int32_t* idx, int64_t n, const void* table,
                                int64_t stride_bytes, int L, uint32_t* sink, hipStream_t s);
 

@@ -6,6 +6,9 @@
 // that order -- the aggregation's own gather (its CSR column stream) with no
 // reduction, no output rows and no degree structure.  Every loaded word is
 // folded into an XOR that each wavefront stores once, so no load is dead.
+// And a scatter that writes every element of a buffer to the position a
+// destination stream gives it -- a radix pass's data movement (its digit
+// runs) with no ranking, no staging and no look-back.
 #include "mp_internal.hpp"
 
 namespace mp {
@@ -109,6 +112,29 @@ __global__ __launch_bounds__(kBlock) void probe_gather(const int32_t* __restrict
     sink_wave(x, sink, wv);
 }
 
+// out[dest[i]] = in[i] for i in [0, n): in and dest read in order, out
+// written where dest says (dest is a permutation of [0, n), which the caller
+// guarantees).
+template <typename T>
+__global__ __launch_bounds__(kBlock) void probe_scatter(const T* __restrict__ in,
+                                                        const int32_t* __restrict__ dest,
+                                                        int64_t n, T* __restrict__ out) {
+    const int64_t stride = (int64_t)gridDim.x * kBlock;
+    int64_t i = (int64_t)blockIdx.x * kBlock + threadIdx.x;
+    for (; i + (kReadUnroll - 1) * stride < n; i += kReadUnroll * stride) {
+        T v[kReadUnroll];
+        int32_t d[kReadUnroll];
+#pragma unroll
+        for (int u = 0; u < kReadUnroll; ++u) {
+            v[u] = __builtin_nontemporal_load(in + i + u * stride);
+            d[u] = __builtin_nontemporal_load(dest + i + u * stride);
+        }
+#pragma unroll
+        for (int u = 0; u < kReadUnroll; ++u) out[d[u]] = v[u];
+    }
+    for (; i < n; i += stride) out[dest[i]] = in[i];
+}
+
 constexpr int64_t kMaxGrid = MP_PROBE_SINK_WORDS / kWaves;  // one sink word per wavefront
 
 unsigned grid_for(int64_t n16) {
@@ -129,6 +155,17 @@ hipError_t launch_probe_read(const void* p, int64_t n16, uint32_t* sink, hipStre
 hipError_t launch_probe_copy(const void* in, void* out, int64_t n16, hipStream_t s) {
     hipLaunchKernelGGL(probe_copy, dim3(grid_for(n16)), dim3(kBlock), 0, s,
                        static_cast<const u32x4*>(in), static_cast<u32x4*>(out), n16);
+    return hipGetLastError();
+}
+
+hipError_t launch_probe_scatter(const void* in, const int32_t* dest, int64_t n, int elem_bytes,
+                                void* out, hipStream_t s) {
+    if (elem_bytes == 8)
+        hipLaunchKernelGGL(probe_scatter<uint64_t>, dim3(grid_for(n)), dim3(kBlock), 0, s,
+                           static_cast<const uint64_t*>(in), dest, n, static_cast<uint64_t*>(out));
+    else
+        hipLaunchKernelGGL(probe_scatter<uint32_t>, dim3(grid_for(n)), dim3(kBlock), 0, s,
+                           static_cast<const uint32_t*>(in), dest, n, static_cast<uint32_t*>(out));
     return hipGetLastError();
 }
 

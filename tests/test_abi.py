@@ -42,6 +42,12 @@ def test_probe_argument_errors():
     assert L.mp_probe_gather(FAKE, 10, FAKE, 2048, 2048, FAKE, None) == -2  # over 1024 bytes
     assert L.mp_probe_gather(FAKE, 10, FAKE + 8, 400, 400, FAKE, None) == -8
     assert L.mp_probe_gather(None, 0, None, 400, 400, FAKE, None) == 0     # nothing to read
+    assert L.mp_probe_scatter(FAKE, None, 10, 8, FAKE, None) == -1
+    assert L.mp_probe_scatter(FAKE, FAKE, 10, 2, FAKE, None) == -2          # 4 or 8 bytes
+    assert L.mp_probe_scatter(FAKE, FAKE, -1, 8, FAKE, None) == -2
+    assert L.mp_probe_scatter(FAKE + 4, FAKE, 10, 8, FAKE, None) == -8
+    assert L.mp_probe_scatter(FAKE, FAKE + 2, 10, 4, FAKE, None) == -8
+    assert L.mp_probe_scatter(None, None, 0, 8, None, None) == 0            # nothing to move
 
 
 def test_noalloc_argument_errors():

@@ -2,7 +2,7 @@
 probe loads is folded into an XOR, so the XOR of all sink words equals the
 XOR of every word the probe was asked to read: an exact check that each probe
 reads exactly its input (the read: the whole buffer; the gather: row idx[p]
-for every p, once per index)."""
+for every p, once per index).  The scatter's output is compared whole."""
 import numpy as np
 import pytest
 import torch
@@ -53,3 +53,20 @@ def test_probe_gather(row_bytes, stride, n):
     t2 = tab.reshape(rows, stride // 4)[:, :row_bytes // 4]
     expect = xor_all(t2[idx]) if n else 0
     assert xor_all(s.cpu().numpy()) == expect
+
+
+@pytest.mark.parametrize("elem_bytes", [4, 8])
+@pytest.mark.parametrize("n", [1, 63, 1000, 70_001, 1 << 20])
+def test_probe_scatter(elem_bytes, n):
+    """out[dest[i]] = in[i] for a random permutation dest (exact)."""
+    rng = np.random.default_rng(n + elem_bytes)
+    dt = np.int64 if elem_bytes == 8 else np.int32
+    h = rng.integers(-2**31, 2**31, n).astype(dt)
+    dest = rng.permutation(n).astype(np.int32)
+    d_in = torch.from_numpy(h).to(DEV)
+    out = torch.zeros_like(d_in)
+    mp.mp_probe_scatter(d_in, torch.from_numpy(dest).to(DEV), n, elem_bytes, out)
+    torch.cuda.synchronize()
+    expect = np.empty_like(h)
+    expect[dest] = h
+    assert np.array_equal(out.cpu().numpy(), expect)
