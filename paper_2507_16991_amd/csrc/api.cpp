@@ -51,7 +51,8 @@ bool valid_reduce(int r) {
 #endif
 
 struct CsrLayout {
-    int passes, digit;
+    DigitPlan dp;
+    int passes;
     bool packed;
     uint32_t *kA, *kB;
     int32_t *src_tmp, *eid_tmp, *eid_final;
@@ -62,7 +63,8 @@ struct CsrLayout {
 
 CsrLayout csr_layout(void* ws, int64_t E, int64_t N, int with_payload) {
     CsrLayout L{};
-    digit_plan(key_bits(N), &L.passes, &L.digit);
+    L.dp = digit_plan(key_bits(N));
+    L.passes = L.dp.passes;
     Carver c(ws);
     const size_t e = (size_t)(E > 0 ? E : 1);
     L.packed = MP_SORT_PACK && !with_payload && L.passes > 1;
@@ -104,7 +106,7 @@ int coo_to_csr_impl(const int32_t* src, const int32_t* dst, int64_t E, int64_t N
     int32_t* eid_final = perm ? perm : L.eid_final;
 
     const uint32_t* keys_in = reinterpret_cast<const uint32_t*>(dst);
-    if (radix_sort_begin(keys_in, E, L.passes, L.digit, L.sc, s) != hipSuccess) return MP_ERR_HIP;
+    if (radix_sort_begin(keys_in, E, L.dp, L.sc, s) != hipSuccess) return MP_ERR_HIP;
     const int32_t* a_in = src;
     const int32_t* b_in = nullptr;  // COO id = element index in the first pass
     for (int p = 0; p < L.passes && L.packed; ++p) {
@@ -123,8 +125,8 @@ int coo_to_csr_impl(const int32_t* src, const int32_t* dst, int64_t E, int64_t N
         }
         rp.n = E;
         rp.pass = p;
-        rp.shift = p * L.digit;
-        rp.bits = L.digit;
+        rp.shift = L.dp.shift[p];
+        rp.bits = L.dp.width[p];
         rp.sc = L.sc;
         if (radix_sort_pass(rp, s) != hipSuccess) return MP_ERR_HIP;
     }
@@ -139,8 +141,8 @@ int coo_to_csr_impl(const int32_t* src, const int32_t* dst, int64_t E, int64_t N
         rp.b_out = payload ? (last_parity ? eid_final : L.eid_tmp) : nullptr;
         rp.n = E;
         rp.pass = p;
-        rp.shift = p * L.digit;
-        rp.bits = L.digit;
+        rp.shift = L.dp.shift[p];
+        rp.bits = L.dp.width[p];
         rp.sc = L.sc;
         if (radix_sort_pass(rp, s) != hipSuccess) return MP_ERR_HIP;
         keys_in = rp.keys_out;
@@ -617,7 +619,12 @@ int mp_spmm_plan_build_opts(const void* rowptr, int rowptr_itype, int64_t N_dst,
         return MP_OK;
     }
     hipError_t e = launch_plan_classes(rowptr, rp64, N_dst, p->small_max, p->hub_min, L.keys, s);
-    if (e == hipSuccess) e = radix_sort_begin(L.keys, N_dst, 1, kPlanClassBits, L.sc, s);
+    if (e == hipSuccess) {
+        DigitPlan dp{};
+        dp.passes = 1;
+        dp.width[0] = dp.max_width = kPlanClassBits;
+        e = radix_sort_begin(L.keys, N_dst, dp, L.sc, s);
+    }
     if (e == hipSuccess) {
         RadixPass rp{};
         rp.keys_in = L.keys;

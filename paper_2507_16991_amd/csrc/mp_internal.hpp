@@ -35,10 +35,28 @@ inline int key_bits(int64_t n) {
     return b;
 }
 
-// Split `bits` into passes of at most kSortMaxBits, as evenly as possible.
-inline void digit_plan(int bits, int* passes, int* digit) {
-    *passes = (bits + kSortMaxBits - 1) / kSortMaxBits;
-    *digit = (bits + *passes - 1) / *passes;
+// The digits of an LSD sort of `bits`-bit keys: as few passes of at most
+// kSortMaxBits as cover the key, the bits split as evenly as possible, with
+// the one-bit-wider digits on the last passes.  (The low digits of
+// destination ids take all their values evenly, so a narrower digit there
+// lengthens every digit run of a tile; the top bits of ids below N often
+// take fewer values than their width allows.)
+struct DigitPlan {
+    int passes;
+    int shift[4], width[4];
+    int max_width;
+};
+inline DigitPlan digit_plan(int bits) {
+    DigitPlan d{};
+    d.passes = (bits + kSortMaxBits - 1) / kSortMaxBits;
+    const int base = bits / d.passes, extra = bits % d.passes;
+    for (int p = 0, s = 0; p < d.passes; ++p) {
+        d.width[p] = base + (p >= d.passes - extra ? 1 : 0);
+        d.shift[p] = s;
+        s += d.width[p];
+        if (d.width[p] > d.max_width) d.max_width = d.width[p];
+    }
+    return d;
 }
 
 // ---- exclusive scan of uint32 (scan.hip) -----------------------------------
@@ -84,7 +102,7 @@ struct RadixPass {
     int pass, shift, bits;
     RadixScratch sc;
 };
-hipError_t radix_sort_begin(const uint32_t* keys, int64_t n, int passes, int bits,
+hipError_t radix_sort_begin(const uint32_t* keys, int64_t n, const DigitPlan& dp,
                             const RadixScratch& sc, hipStream_t s);
 hipError_t radix_sort_pass(const RadixPass& p, hipStream_t s);
 

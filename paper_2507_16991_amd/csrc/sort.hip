@@ -77,8 +77,10 @@ __global__ __launch_bounds__(256) void radix_clear(uint64_t* __restrict__ desc, 
 // Global histogram of every pass's digit.  Counts do not depend on order, so
 // each wavefront adds into its own LDS copy with integer atomics (no ranking
 // needed), then one integer atomic per (pass, digit) per workgroup.
+// shifts and widths: one byte per pass (pass p in bits 8p..8p+7).
 __global__ __launch_bounds__(kGhistBlock) void radix_ghist(const uint32_t* __restrict__ keys,
-                                                           int64_t n, int passes, int bits,
+                                                           int64_t n, int passes, uint32_t shifts,
+                                                           uint32_t widths,
                                                            uint32_t* __restrict__ ghist) {
     constexpr int W = kGhistBlock / kWave;
     __shared__ uint32_t h[W][kMaxPasses][kMaxBuckets];
@@ -87,7 +89,6 @@ __global__ __launch_bounds__(kGhistBlock) void radix_ghist(const uint32_t* __res
     __syncthreads();
     const int lane = threadIdx.x & (kWave - 1);
     const int wv = threadIdx.x / kWave;
-    const uint32_t mask = (1u << bits) - 1u;
     const int64_t stride = (int64_t)gridDim.x * W * kWave * kGhistItems;
     for (int64_t base = ((int64_t)blockIdx.x * W + wv) * kWave * kGhistItems; base < n;
          base += stride) {
@@ -100,8 +101,11 @@ __global__ __launch_bounds__(kGhistBlock) void radix_ghist(const uint32_t* __res
 #pragma unroll
         for (int k = 0; k < kGhistItems; ++k) {
             if (base + (int64_t)k * kWave + lane >= n) continue;
-            for (int p = 0; p < passes; ++p)
-                atomicAdd(&h[wv][p][(key[k] >> (p * bits)) & mask], 1u);
+            for (int p = 0; p < passes; ++p) {
+                const uint32_t sh = (shifts >> (8 * p)) & 255u;
+                const uint32_t mask = (1u << ((widths >> (8 * p)) & 255u)) - 1u;
+                atomicAdd(&h[wv][p][(key[k] >> sh) & mask], 1u);
+            }
         }
     }
     __syncthreads();
@@ -113,12 +117,13 @@ __global__ __launch_bounds__(kGhistBlock) void radix_ghist(const uint32_t* __res
     }
 }
 
-// In place: per pass, exclusive scan over the 2^bits digit counts.
-__global__ void radix_gscan(uint32_t* __restrict__ g, int passes, int bits) {
+// In place: per pass, exclusive scan over its digit counts (the counts of
+// digits beyond a pass's width are zero).
+__global__ void radix_gscan(uint32_t* __restrict__ g, int passes) {
     const int p = threadIdx.x;
     if (p >= passes) return;
     uint32_t run = 0;
-    for (int d = 0; d < (1 << bits); ++d) {
+    for (int d = 0; d < kMaxBuckets; ++d) {
         const uint32_t c = g[p * kMaxBuckets + d];
         g[p * kMaxBuckets + d] = run;
         run += c;
@@ -528,11 +533,21 @@ RadixScratch radix_scratch(void* base, int64_t n) {
     return sc;
 }
 
-hipError_t radix_sort_begin(const uint32_t* keys, int64_t n, int passes, int bits,
+hipError_t radix_sort_begin(const uint32_t* keys, int64_t n, const DigitPlan& dp,
                             const RadixScratch& sc, hipStream_t s) {
     if (n <= 0) return hipSuccess;
+    if (dp.passes < 1 || dp.passes > kMaxPasses) return hipErrorInvalidValue;
+    uint32_t shifts = 0, widths = 0;
+    for (int p = 0; p < dp.passes; ++p) {
+        if (dp.width[p] < 1 || dp.width[p] > kSortMaxBits || dp.shift[p] < 0 ||
+            dp.shift[p] + dp.width[p] > 32)
+            return hipErrorInvalidValue;
+        shifts |= (uint32_t)dp.shift[p] << (8 * p);
+        widths |= (uint32_t)dp.width[p] << (8 * p);
+    }
     const int64_t tiles = ceil_div(n, kSortTile);
-    const int64_t ndesc = tiles * ((int64_t)1 << bits);  // R descriptors per tile
+    // a pass over R = 2^width digits uses R descriptors per tile
+    const int64_t ndesc = tiles * ((int64_t)1 << dp.max_width);
     unsigned g = grid_for(ndesc, 256);
     if (g > 8192) g = 8192;
     // every histogram word needs a thread, however few descriptors there are
@@ -542,9 +557,9 @@ hipError_t radix_sort_begin(const uint32_t* keys, int64_t n, int passes, int bit
     const int64_t per_block = (int64_t)kGhistBlock * kGhistItems;
     unsigned gh = grid_for(n, (int)per_block);
     if (gh > 2048) gh = 2048;
-    hipLaunchKernelGGL(radix_ghist, dim3(gh), dim3(kGhistBlock), 0, s, keys, n, passes, bits,
-                       sc.gbase);
-    hipLaunchKernelGGL(radix_gscan, dim3(1), dim3(kWave), 0, s, sc.gbase, passes, bits);
+    hipLaunchKernelGGL(radix_ghist, dim3(gh), dim3(kGhistBlock), 0, s, keys, n, dp.passes, shifts,
+                       widths, sc.gbase);
+    hipLaunchKernelGGL(radix_gscan, dim3(1), dim3(kWave), 0, s, sc.gbase, dp.passes);
     return hipGetLastError();
 }
 
