@@ -318,9 +318,11 @@ def build_step(args, mp, torch, np, dev):
                                       for c in calls if c[0] == "spmm"}}
     if args.workload == WORKLOAD:
         # the radix passes' data movement: the first pass's order over dst
+        # (its digit: the key's bits split evenly over the passes, the first
+        # pass taking the narrower share)
         kb = max(1, (N - 1).bit_length())
         passes = -(-kb // 9)
-        g.probe["scatter"] = (dst, -(-kb // passes))
+        g.probe["scatter"] = (dst, kb // passes)
     plans = {}
     wss = {}
 
