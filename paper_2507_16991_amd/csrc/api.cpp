@@ -42,10 +42,11 @@ bool valid_reduce(int r) {
 
 // ---- COO -> CSR workspace layout ---------------------------------------------
 
-// Without the COO-id payload and with more than one pass, the passes before
-// the last write (key, src) packed in 8-byte words, ping-ponging between kv[0]
-// and kv[1]; the last pass writes the keys into the buffer it does not read
-// and src into col.  Otherwise keys and payloads ping-pong as 4-byte arrays.
+// With more than one pass, the passes before the last write (key, src)
+// packed in 8-byte words, ping-ponging between kv[0] and kv[1]; the last pass
+// writes the keys into the buffer it does not read and src into col.  The
+// COO-id payload, when asked for, ping-pongs as a 4-byte array that ends in
+// perm.  (With one pass, keys and payloads go straight to their outputs.)
 #ifndef MP_SORT_PACK
 #define MP_SORT_PACK 1
 #endif
@@ -67,7 +68,7 @@ CsrLayout csr_layout(void* ws, int64_t E, int64_t N, int with_payload) {
     L.passes = L.dp.passes;
     Carver c(ws);
     const size_t e = (size_t)(E > 0 ? E : 1);
-    L.packed = MP_SORT_PACK && !with_payload && L.passes > 1;
+    L.packed = MP_SORT_PACK && L.passes > 1;
     if (L.packed) {
         L.kv[0] = c.take<uint64_t>(e);
         L.kv[1] = c.take<uint64_t>(e);
@@ -110,6 +111,7 @@ int coo_to_csr_impl(const int32_t* src, const int32_t* dst, int64_t E, int64_t N
     const int32_t* a_in = src;
     const int32_t* b_in = nullptr;  // COO id = element index in the first pass
     for (int p = 0; p < L.passes && L.packed; ++p) {
+        const bool last_parity = ((L.passes - 1 - p) % 2) == 0;  // lands where the final pass writes
         RadixPass rp{};
         if (p == 0) {
             rp.keys_in = keys_in;
@@ -123,6 +125,9 @@ int coo_to_csr_impl(const int32_t* src, const int32_t* dst, int64_t E, int64_t N
             rp.keys_out = L.kA;
             rp.a_out = col;
         }
+        rp.b_in = b_in;
+        rp.b_out = payload ? (last_parity ? eid_final : L.eid_tmp) : nullptr;
+        b_in = rp.b_out;
         rp.n = E;
         rp.pass = p;
         rp.shift = L.dp.shift[p];

@@ -95,7 +95,7 @@ struct RadixPass {
     int32_t* a_out;           // [n] or nullptr
     int32_t* b_out;           // [n] or nullptr
     // packed (key << 32 | payload a) words in place of keys_in and a_in
-    // (kv_in) or keys_out and a_out (kv_out); not with payload b
+    // (kv_in) or keys_out and a_out (kv_out)
     const uint64_t* kv_in;    // [n] or nullptr
     uint64_t* kv_out;         // [n] or nullptr
     int64_t n;

@@ -141,11 +141,13 @@ __global__ void radix_gscan(uint32_t* __restrict__ g, int passes) {
 // a pass over R = 2^bits digits lie R apart per tile.
 //   HAS_B: the second payload is carried.
 //   WIDE:  digits of up to 9 bits (512 buckets: twice the per-wave counters).
-//   PIN, POUT: the keys and the payload are read (written) as one array of
-//          (key << 32 | payload) words instead of two arrays; between passes
-//          this makes each digit run one contiguous stretch of memory of
-//          twice the length rather than two, which the scattered writes of a
-//          pass favour.  One payload only.
+//   PIN, POUT: the keys and payload a are read (written) as one array of
+//          (key << 32 | a) words instead of two arrays; between passes this
+//          makes each digit run one contiguous stretch of memory of twice the
+//          length rather than two, which the scattered writes of a pass
+//          favour.  A pass that stages one array at a time (ONEBUF) writes a
+//          word's two halves in turn, the key with the keys and a with the
+//          payload, to the same lines shortly apart.
 // A tile's arrays are staged in LDS all at once where they fit beside the
 // counters (one payload); otherwise (ONEBUF) the keys and then each payload
 // go through one staging buffer in turn: keys before the look-back, each
@@ -159,7 +161,6 @@ template <bool HAS_B, bool WIDE, bool PIN, bool POUT>
 __global__ __launch_bounds__(kSortBlock)
 __attribute__((amdgpu_waves_per_eu(HAS_B ? 1 : kSortTilesPerCU * kSortBlock / 256)))
 void radix_onesweep(RadixPass p) {
-    static_assert(!(HAS_B && (PIN || POUT)), "packed passes carry one payload");
     static_assert(kSortTile <= 65536, "16-bit counters and staged slots");
     constexpr int NB = WIDE ? kMaxBuckets : kMaxBuckets / 2;  // buckets this variant handles
     // per-wave digit counts, then each wave's run start inside its digit
@@ -167,7 +168,6 @@ void radix_onesweep(RadixPass p) {
     // all arrays staged at once where they fit in LDS, else one at a time
     constexpr int kFixedLds = kSortWaves * NB * (int)sizeof(cnt_t) + 3 * NB * 4 + 16;
     constexpr bool ONEBUF = (HAS_B ? 3 : 2) * kSortTile * 4 + kFixedLds > kMaxLdsBytes;
-    static_assert(!(ONEBUF && POUT), "a packed write needs the key and the payload at once");
     constexpr int NSTAGE = ONEBUF ? 1 : (HAS_B ? 3 : 2);  // staging arrays
     __shared__ uint32_t s_stage[NSTAGE][kSortTile];
     __shared__ uint16_t s_lp[ONEBUF ? kSortTile : 1];  // ONEBUF: staged slot of every key
@@ -343,7 +343,10 @@ void radix_onesweep(RadixPass p) {
             const int64_t q = (int64_t)s_gbase[d] + (i - (int64_t)s_start[d]);
             if (q < p.n) {  // cannot fail for consistent counts; never write past n
                 if constexpr (ONEBUF) pos[k] = (int32_t)q;
-                if constexpr (POUT) {
+                if constexpr (POUT && ONEBUF) {
+                    // the word's key half now, its payload half with the payload
+                    reinterpret_cast<uint32_t*>(p.kv_out)[2 * q + 1] = kk;
+                } else if constexpr (POUT) {
                     p.kv_out[q] = ((uint64_t)kk << 32) | s_stage[1][i];
                 } else if (p.keys_out) {
                     p.keys_out[q] = kk;
@@ -360,7 +363,10 @@ void radix_onesweep(RadixPass p) {
     if constexpr (ONEBUF) {
         // the payloads, one at a time through the same buffer
         for (int which = 0; which < (HAS_B ? 2 : 1); ++which) {
-            int32_t* out = which == 0 ? p.a_out : p.b_out;
+            // payload a of a packed write: the low halves of the words
+            const bool half = POUT && which == 0;
+            int32_t* out = half ? reinterpret_cast<int32_t*>(p.kv_out)
+                                : (which == 0 ? p.a_out : p.b_out);
             __syncthreads();  // every read of the buffer's previous contents is done
 #pragma unroll
             for (int k = 0; k < kSortItems; ++k) {
@@ -373,7 +379,9 @@ void radix_onesweep(RadixPass p) {
             if (!out) continue;
 #pragma unroll
             for (int k = 0; k < kSortItems; ++k)
-                if (pos[k] >= 0) out[pos[k]] = (int32_t)s_stage[0][threadIdx.x + k * kSortBlock];
+                if (pos[k] >= 0)
+                    out[half ? 2 * (int64_t)pos[k] : (int64_t)pos[k]] =
+                        (int32_t)s_stage[0][threadIdx.x + k * kSortBlock];
         }
     }
 }
@@ -563,17 +571,17 @@ hipError_t radix_sort_begin(const uint32_t* keys, int64_t n, const DigitPlan& dp
     return hipGetLastError();
 }
 
-template <bool WIDE>
-void launch_onesweep_one_payload(const RadixPass& p, unsigned tiles, hipStream_t s) {
-    const dim3 g(tiles), b(kSortBlock);
+template <bool HAS_B, bool WIDE>
+void launch_onesweep(const RadixPass& p, int64_t tiles, hipStream_t s) {
+    const dim3 g((unsigned)tiles), b(kSortBlock);
     if (p.kv_in && p.kv_out)
-        hipLaunchKernelGGL((radix_onesweep<false, WIDE, true, true>), g, b, 0, s, p);
+        hipLaunchKernelGGL((radix_onesweep<HAS_B, WIDE, true, true>), g, b, 0, s, p);
     else if (p.kv_in)
-        hipLaunchKernelGGL((radix_onesweep<false, WIDE, true, false>), g, b, 0, s, p);
+        hipLaunchKernelGGL((radix_onesweep<HAS_B, WIDE, true, false>), g, b, 0, s, p);
     else if (p.kv_out)
-        hipLaunchKernelGGL((radix_onesweep<false, WIDE, false, true>), g, b, 0, s, p);
+        hipLaunchKernelGGL((radix_onesweep<HAS_B, WIDE, false, true>), g, b, 0, s, p);
     else
-        hipLaunchKernelGGL((radix_onesweep<false, WIDE, false, false>), g, b, 0, s, p);
+        hipLaunchKernelGGL((radix_onesweep<HAS_B, WIDE, false, false>), g, b, 0, s, p);
 }
 
 hipError_t radix_sort_pass(const RadixPass& p, hipStream_t s) {
@@ -581,15 +589,11 @@ hipError_t radix_sort_pass(const RadixPass& p, hipStream_t s) {
     const int64_t tiles = ceil_div(p.n, kSortTile);
     const bool wide = p.bits > kSortMaxBits - 1;
     if (p.b_out) {
-        if (p.kv_in || p.kv_out) return hipErrorInvalidValue;  // packed passes: one payload
-        if (wide)
-            hipLaunchKernelGGL((radix_onesweep<true, true, false, false>), dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p);
-        else
-            hipLaunchKernelGGL((radix_onesweep<true, false, false, false>), dim3((unsigned)tiles), dim3(kSortBlock), 0, s, p);
-    } else if (wide) {
-        launch_onesweep_one_payload<true>(p, (unsigned)tiles, s);
+        if (wide) launch_onesweep<true, true>(p, tiles, s);
+        else launch_onesweep<true, false>(p, tiles, s);
     } else {
-        launch_onesweep_one_payload<false>(p, (unsigned)tiles, s);
+        if (wide) launch_onesweep<false, true>(p, tiles, s);
+        else launch_onesweep<false, false>(p, tiles, s);
     }
     return hipGetLastError();
 }
