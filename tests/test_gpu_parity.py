@@ -79,6 +79,23 @@ def test_csr_shapes(n, e, itype):
     check_csr(src, dst, n, itype, val)
 
 
+@pytest.mark.parametrize("want_perm", [False, True])
+def test_csr_four_passes(want_perm):
+    """Keys of 29 bits (N = 2^28 + 5): four radix passes (7/7/7/8 bits), with
+    and without the COO-id payload, int64 rowptr."""
+    n, e = (1 << 28) + 5, 300_000
+    src = graphgen.uniform_ints(11, 1, e, n)
+    dst = graphgen.uniform_ints(11, 2, e, n)
+    dst[:1000] = n - 1 - np.arange(1000, dtype=np.int32)  # the top digits are used too
+    if want_perm:
+        check_csr(src, dst, n, torch.int64)
+        return
+    rp, col, _, _ = mp.coo_to_csr(dev(src), dev(dst), n, rowptr_dtype=torch.int64)
+    rp_o, col_o, _, _ = oracle.coo_to_csr(src, dst, n)
+    assert np.array_equal(rp.cpu().numpy(), rp_o), "rowptr"
+    assert np.array_equal(col.cpu().numpy(), col_o), "col"
+
+
 @pytest.mark.parametrize("name,scale", [("uniform-10k", 1.0), ("powerlaw-1.2M", 1.0),
                                         ("chunglu-124M", 0.05)])
 def test_csr_workloads(name, scale):
