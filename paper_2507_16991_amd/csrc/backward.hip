@@ -4,7 +4,7 @@
 //
 //   * rows_of_edges: the destination row of every forward CSR position (the
 //     keys the transposed CSR is sorted by carry it as payload), one
-//     wavefront per row.
+//     wavefront per 64 rows.
 //   * scale_inv_deg: grad_out / in-degree per destination row, the input of
 //     the gradient of mean.
 //   * spmm_grad_w: the gradient with respect to the edge weights, one dot
@@ -40,23 +40,43 @@ __device__ inline int64_t rp_at(const void* rp, int rp64, int64_t i) {
     return rp64 ? static_cast<const int64_t*>(rp)[i] : (int64_t) static_cast<const int32_t*>(rp)[i];
 }
 
-// row[p] = the v with rowptr[v] <= p < rowptr[v+1].  One wavefront per row
-// writes the row id over the row's positions (64 consecutive positions per
-// store instruction, no search).  Positions outside [rowptr[0], rowptr[N])
-// of an inconsistent rowptr go to the first or last row, so every entry is
-// a valid row id whatever the input.
+// row[p] = the v with rowptr[v] <= p < rowptr[v+1].  Each wavefront takes 64
+// consecutive rows: it stages their 65 bounds in LDS, then writes the
+// positions from its first row's start to its last row's end 64 at a time
+// (one store instruction each, however long or short the rows), each lane
+// finding the row of its position by a binary search over the staged
+// bounds.  Bounds are read as 0 for row 0 and E for row N and clamped to
+// [0, E], so every position is written, with a row id below N, whatever the
+// input (an inconsistent rowptr only makes ids wrong).
 template <typename IT>
 __global__ __launch_bounds__(kBlock) void rows_of_edges(const IT* __restrict__ rowptr, int64_t N,
                                                         int64_t E, int32_t* __restrict__ row) {
+    __shared__ int64_t s_b[kWavesPerBlock][kWave + 1];
     const int lane = threadIdx.x & (kWave - 1);
-    const int64_t v = __builtin_amdgcn_readfirstlane((int)(threadIdx.x / kWave)) +
-                      (int64_t)blockIdx.x * kWavesPerBlock;
-    if (v >= N) return;
-    int64_t beg = v == 0 ? 0 : (int64_t)rowptr[v];
-    int64_t end = v == N - 1 ? E : (int64_t)rowptr[v + 1];
-    if (beg < 0) beg = 0;
-    if (end > E) end = E;
-    for (int64_t p = beg + lane; p < end; p += kWave) row[p] = (int32_t)v;
+    const int wl = threadIdx.x / kWave;
+    const int64_t v0 = ((int64_t)blockIdx.x * kWavesPerBlock + wl) * kWave;
+    if (v0 >= N) return;  // uniform per wavefront
+    auto bound = [&](int64_t v) -> int64_t {
+        if (v <= 0) return 0;
+        if (v >= N) return E;
+        const int64_t b = (int64_t)rowptr[v];
+        return b < 0 ? 0 : (b > E ? E : b);
+    };
+    s_b[wl][lane] = bound(v0 + lane);
+    if (lane == 0) s_b[wl][kWave] = bound(v0 + kWave);
+    // the wavefront reads what its own lanes wrote: LDS operations of one
+    // wavefront complete in order
+    __builtin_amdgcn_wave_barrier();
+    const int nr = (int)(N - v0 < kWave ? N - v0 : kWave);  // rows of this wavefront
+    const int64_t p1 = s_b[wl][nr];
+    for (int64_t p = s_b[wl][0] + lane; p < p1; p += kWave) {
+        int lo = 0, hi = nr - 1;  // the last row whose start is <= p
+        while (lo < hi) {
+            const int mid = (lo + hi + 1) >> 1;
+            if (s_b[wl][mid] <= p) lo = mid; else hi = mid - 1;
+        }
+        row[p] = (int32_t)(v0 + lo);
+    }
 }
 
 __device__ inline float bf16_bits_to_f32(uint32_t b) { return __uint_as_float(b << 16); }
@@ -401,7 +421,7 @@ hipError_t launch_gw_epl(const GradWParams& p, int epl, unsigned grid, hipStream
 hipError_t launch_rows_of_edges(const void* rowptr, int rp64, int64_t N, int64_t E, int32_t* row,
                                 hipStream_t s) {
     if (E <= 0 || N <= 0) return hipSuccess;
-    const unsigned grid = (unsigned)ceil_div(N, kWavesPerBlock);
+    const unsigned grid = (unsigned)ceil_div(ceil_div(N, kWave), kWavesPerBlock);
     if (rp64)
         hipLaunchKernelGGL(rows_of_edges<int64_t>, dim3(grid), dim3(kBlock), 0, s,
                            static_cast<const int64_t*>(rowptr), N, E, row);
