@@ -476,6 +476,9 @@ def explain_step(g, mp, torch, np, dev, mark, seed):
            ("msg_input_grad", 4 * E + 2 * EF4, 0),
            ("grad_x_sum", rp + 4 * E + EF4 + N * F * 4, E * F)]
     nb = lambda t: 0 if t is None else t.numel()
+    # the input gradient's own gather: rows of the E-row message-gradient
+    # table in transposed order (each row once, in a scattered order)
+    g.probe = {"col": posT, "tables": {"msg": (m, F * 4, F * 4)}}
 
     def step(evs=None):
         mark(evs, 0)
@@ -779,6 +782,9 @@ def run(args):
             if "gather_G" in ceil and n in ("grad_x_sum_f32", "grad_x_mean_f32"):
                 breakdown[n]["frac_of_gather_ceiling"] = round(
                     breakdown[n]["GB_per_s"] / ceil["gather_G"]["GB_per_s"], 4)
+            if "gather_msg" in ceil and n == "grad_x_sum":
+                breakdown[n]["frac_of_gather_ceiling"] = round(
+                    breakdown[n]["GB_per_s"] / ceil["gather_msg"]["GB_per_s"], 4)
         for n in names:  # aggregations against the gather of their own table
             k = n.rsplit("_", 1)[-1]
             if f"gather_{k}" in ceil and n.split("_")[0] in ("sum", "mean", "max", "wsum",
